@@ -1,0 +1,190 @@
+/*
+ * enova_detect.h -- C ABI of the MI355X (gfx950) batched sliding-window anomaly scorer.
+ *
+ * What it computes is the performance-detection module of ENOVA (arXiv 2407.09486,
+ * Section IV-B, Fig. 3): monitoring metrics of many LLM-service instances (Table II:
+ * arrivals, running/pending requests, execution time, GPU memory and GPU utilisation,
+ * each observed over a window of consecutive steps) are normalised, encoded by a VAE
+ * whose posterior q(z|m) is a diagonal Gaussian, scored by the KL-divergence of that
+ * posterior from the standard-normal prior, thresholded by peaks-over-threshold, and
+ * given a scale-up/scale-down direction by the Mean Difference between the input
+ * window and its reconstruction.
+ *
+ * Conventions for every entry point:
+ *   - every function returns an enova_status; none aborts, throws or exits;
+ *   - arguments are validated on the host before any launch; a failing call writes no output;
+ *   - "device" pointers are HIP device (or managed) memory of the device the detector was
+ *     created on; "host" pointers are ordinary host memory;
+ *   - the caller owns every buffer it passes; the library owns the detector handle, the
+ *     device copies of the weights and its internal workspace;
+ *   - calls on one detector must not overlap (the workspace is reused); distinct detectors
+ *     are independent;
+ *   - enova_last_error() returns a description of the last failure on the calling thread.
+ *
+ * Data layout:
+ *   x: row-major [total_steps][M]: step-major, the M metrics of a step contiguous; the
+ *      streams are concatenated, stream s occupying rows [stream_offsets[s], stream_offsets[s+1]).
+ *   Window k of stream s covers rows [k*S, k*S + W) of that stream (k = 0, 1, ... while
+ *   k*S + W <= T_s; a partial tail is dropped); its flattened input index is j = t*M + m.
+ *   Window outputs are CSR too: window k of stream s is element window_offsets[s] + k.
+ */
+#ifndef ENOVA_DETECT_H
+#define ENOVA_DETECT_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct enova_detector_s *enova_detector;   /* opaque; owned by the library */
+
+typedef enum {
+    ENOVA_OK = 0,
+    ENOVA_EINVAL = 1,        /* a null required pointer, a size out of range, a bad enum */
+    ENOVA_ESHAPE = 2,        /* shapes are valid but the request has no data to act on */
+    ENOVA_ENOMEM = 3,        /* device or host allocation failed */
+    ENOVA_EHIP = 4,          /* a HIP runtime call or a kernel launch failed */
+    ENOVA_EUNSUPPORTED = 5,  /* a valid request this build does not implement */
+    ENOVA_ENUMERIC = 6       /* non-finite values where finite ones are required */
+} enova_status;
+
+typedef enum { ENOVA_F32 = 0, ENOVA_BF16 = 1 } enova_dtype;     /* storage / MFMA type of x and W1 */
+typedef enum { ENOVA_RELU = 0, ENOVA_TANH = 1 } enova_act;       /* hidden activation of encoder and decoder */
+typedef enum {
+    ENOVA_KERNEL_AUTO = 0,   /* the matrix-core kernel when the shape allows it, else the vector kernel */
+    ENOVA_KERNEL_VALU = 1,   /* always the general vector-ALU kernel */
+    ENOVA_KERNEL_MFMA = 2    /* always the matrix-core kernel; EUNSUPPORTED if the shape does not fit */
+} enova_kernel;
+
+/*
+ * Detector shape (Section IV-B: one hidden layer of width H, a diagonal-Gaussian latent
+ * of width L with mean and log-variance heads, prior N(0, I); the decoder's mean head
+ * reconstructs the window).
+ *   metrics M >= 1, window W >= 1, stride S >= 1, hidden H >= 1, latent 1 <= L <= 64,
+ *   W*M <= 65536, ref_frac in (0, 1]: the reference prefix of a stream of T steps is its
+ *   first floor((double)ref_frac * T) steps.
+ */
+typedef struct {
+    int32_t metrics, window, stride, hidden, latent;
+    int32_t dtype;           /* enova_dtype */
+    int32_t act;             /* enova_act */
+    int32_t kernel;          /* enova_kernel */
+    float ref_frac;          /* default 0.5 */
+} enova_detect_config;
+
+/*
+ * Detector weights: HOST pointers, row-major [out][in] (as torch.nn.Linear stores them).
+ * They are copied (and repacked for the kernels) by enova_detect_init; the caller may free
+ * them afterwards. D = W*M; the flattened input index is j = t*M + m.
+ */
+typedef struct {
+    const void *w1;   const float *b1;    /* [H][D] (float, or bf16 bit patterns for ENOVA_BF16), [H] */
+    const float *wmu; const float *bmu;   /* [L][H], [L]   posterior mean head        */
+    const float *wlv; const float *blv;   /* [L][H], [L]   posterior log-variance head */
+    const float *wd1; const float *bd1;   /* [H][L], [H]   decoder hidden layer        */
+    const float *wd2; const float *bd2;   /* [D][H], [D]   decoder mean head (only its column sums are kept) */
+} enova_detect_weights;
+
+/* Create a detector on the current HIP device. Errors: EINVAL (config or weights), ENOMEM, EHIP. */
+enova_status enova_detect_init(const enova_detect_config *config, const enova_detect_weights *weights,
+                               enova_detector *out);
+
+/* Free a detector and all its device memory (synchronises the device). NULL is a no-op. */
+enova_status enova_detect_destroy(enova_detector det);
+
+/*
+ * Host helper (window enumeration of Table II's observation windows).
+ *   stream_offsets_host [n_streams+1]: [0] = 0, non-decreasing (EINVAL otherwise).
+ *   window_offsets_host [n_streams+1] receives the exclusive scan of the per-stream window
+ *   counts n_s = T_s >= W ? (T_s - W) / S + 1 : 0; its last entry is the total window count N.
+ */
+enova_status enova_detect_window_offsets(enova_detector det, const int64_t *stream_offsets_host,
+                                         int32_t n_streams, int64_t *window_offsets_host);
+
+/*
+ * Reference statistics (Section IV-B: metrics are normalised before entering the VAE).
+ * Per stream and metric, mean and population standard deviation over the reference
+ * prefix (accumulated in fp64, stored as fp32). A prefix of zero steps gives mean 0 and
+ * std 1; a std <= 1e-6 * max(1, |mean|) (a metric constant over the reference) becomes 1.
+ *   x              device, [stream_offsets[n]][M], the detector's dtype
+ *   stream_offsets device [n+1]
+ *   out_mean, out_std device [n][M] float
+ * Asynchronous on `stream`.
+ */
+enova_status enova_detect_ref_stats(enova_detector det, const void *x, const int64_t *stream_offsets,
+                                    int32_t n_streams, float *out_mean, float *out_std,
+                                    hipStream_t stream);
+
+/*
+ * Score every window (Section IV-B: KL-divergence of q(z|m) from p(z); Mean Difference
+ * between m and its reconstruction m' for the direction; anomaly iff the KL exceeds the
+ * threshold).
+ *   x              device [stream_offsets[n]][M], the detector's dtype (float or bf16 bits)
+ *   stream_offsets device [n+1]: [0] = 0, non-decreasing (precondition, not checked on device)
+ *   window_offsets device [n+1]: as produced by enova_detect_window_offsets (precondition)
+ *   n_streams      >= 0;   n_windows = window_offsets[n_streams] (precondition)
+ *   ref_mean, ref_std  device [n][M] float, or both NULL: then computed as by
+ *                  enova_detect_ref_stats into the detector's workspace
+ *   threshold      flags are written as score > threshold; NaN: out_flags is not written
+ *   out_scores     device [n_windows] float: 1/2 sum_l (mu_l^2 + e^lv_l - 1 - lv_l)
+ *   out_md         device [n_windows] float or NULL: mean(v) - mean(m'), in normalised units;
+ *                  positive means the window sits above its reconstruction (scale up)
+ *   out_flags      device [n_windows] uint8 or NULL
+ * Inputs are expected finite; a NaN input propagates to that window's score and md, and its
+ * flag is 0. Nothing outside [0, n_windows) is written. Asynchronous on `stream`.
+ * Errors: EINVAL, EUNSUPPORTED (ENOVA_KERNEL_MFMA with an unsupported shape), ENOMEM, EHIP.
+ */
+enova_status enova_detect_score(enova_detector det, const void *x, const int64_t *stream_offsets,
+                                const int64_t *window_offsets, int32_t n_streams, int64_t n_windows,
+                                const float *ref_mean, const float *ref_std, float threshold,
+                                float *out_scores, float *out_md, uint8_t *out_flags,
+                                hipStream_t stream);
+
+/*
+ * Peaks-over-threshold threshold (Section IV-B, citing Siffer et al. 2017), static and global:
+ * the calibration set is the scores of the windows lying wholly inside each stream's reference
+ * prefix (k*S + W <= floor(ref_frac*T_s)); t is its order statistic at ceil(level*n) - 1
+ * (ascending, 0-based); the excesses Y = {c - t : c > t} are fitted by a generalised Pareto
+ * distribution (N_t >= 10: maximum likelihood by Grimshaw's reduction, in fp64 on the host;
+ * 2 <= N_t < 10: method of moments; N_t <= 1: the threshold is t) and
+ *   z_q = t + sigma/gamma * ((q n / N_t)^(-gamma) - 1)   (z_q = t - sigma ln(q n / N_t) if gamma = 0).
+ *   scores         device [n_windows] float (as written by enova_detect_score)
+ *   level in (0,1), q in (0,1)  (defaults 0.98 and 1e-3)
+ *   out_threshold  HOST float
+ *   out_info       HOST double[6] or NULL: t, n, N_t, gamma, sigma, method (0 t, 1 moments, 2 MLE)
+ *   out_flags      device [n_windows] uint8 or NULL: score > z_q for every window
+ * Synchronises `stream` (it returns a host value). ESHAPE if no window is a calibration window.
+ */
+enova_status enova_detect_threshold(enova_detector det, const float *scores,
+                                    const int64_t *stream_offsets, const int64_t *window_offsets,
+                                    int32_t n_streams, int64_t n_windows, double level, double q,
+                                    float *out_threshold, double *out_info, uint8_t *out_flags,
+                                    hipStream_t stream);
+
+/* flags[i] = scores[i] > threshold for i < n_windows (device pointers). Asynchronous. */
+enova_status enova_detect_flag(enova_detector det, const float *scores, int64_t n_windows,
+                               float threshold, uint8_t *out_flags, hipStream_t stream);
+
+/*
+ * Kernel timing: when enabled, enova_detect_score brackets its scoring kernel (and, when it
+ * computes them, the reference-statistics kernel) with HIP events on `stream`;
+ * enova_detect_kernel_times waits for the last call's events and reports milliseconds
+ * (a kernel that did not run reports 0).
+ */
+enova_status enova_detect_set_timing(enova_detector det, int32_t enable);
+enova_status enova_detect_kernel_times(enova_detector det, double *score_kernel_ms,
+                                       double *stats_kernel_ms);
+
+/* Which scoring kernel the detector uses: 1 vector-ALU, 2 matrix-core (MFMA). */
+enova_status enova_detect_kernel_kind(enova_detector det, int32_t *kind);
+
+const char *enova_status_str(enova_status status);
+const char *enova_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ENOVA_DETECT_H */

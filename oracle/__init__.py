@@ -62,8 +62,11 @@ def _load():
     lib.oracle_window_debug.argtypes = [P, I, I, I, I64, I, I, I] + [P] * 10 + [P, P, I, P, P, P]
     lib.oracle_window_debug.restype = None
     lib.oracle_score_batch.argtypes = ([P, P, I, I, I, I, I, I, I, P] + [P] * 10 +
-                                       [I, P, P, P, P, P, P, P, P, I])
+                                       [I, P, P, P, P, P, P, P, P, P, I])
     lib.oracle_score_batch.restype = I
+    lib.oracle_score_pairs.argtypes = ([P, P, I, I, I, I, I, I, I, P] + [P] * 10 +
+                                       [I, P, P, P, P, I64, P, P, P, I])
+    lib.oracle_score_pairs.restype = I
     _lib = lib
     return lib
 
@@ -151,6 +154,7 @@ def score(x, stream_offsets, *, window, stride, weights, act="relu", ref_frac=0.
     N = int(woff[-1])
     sc = np.full(N, np.nan)
     md = np.full(N, np.nan)
+    mds = np.full(N, np.nan)
     mean_o = np.empty((max(n, 1), M))
     std_o = np.empty((max(n, 1), M))
     em = es = None
@@ -166,11 +170,44 @@ def score(x, stream_offsets, *, window, stride, weights, act="relu", ref_frac=0.
             _ptr(w["w1"]), _ptr(w["b1"]), _ptr(w["wmu"]), _ptr(w["bmu"]), _ptr(w["wlv"]),
             _ptr(w["blv"]), _ptr(w["wd1"]), _ptr(w["bd1"]), _ptr(w["wd2"]), _ptr(w["bd2"]),
             1 if bf16 else 0, _ptr(em), _ptr(es), _ptr(woff), _ptr(cnt),
-            _ptr(sc), _ptr(md), _ptr(mean_o), _ptr(std_o), int(threads))
+            _ptr(sc), _ptr(md), _ptr(mds), _ptr(mean_o), _ptr(std_o), int(threads))
     if return_stats:
         return sc, md, {"window_offsets": woff, "mean": mean_o[:n], "std": std_o[:n],
-                        "threads": used, "ref_len": R}
+                        "threads": used, "ref_len": R, "md_scale": mds}
     return sc, md
+
+
+def score_pairs(x, stream_offsets, streams, ks, *, window, stride, weights, act="relu",
+                ref_frac=0.5, bf16=False, ref_mean=None, ref_std=None, threads=0):
+    """Scores, MD and MD scale (mean|v| + mean|m'|) of window ks[i] of stream streams[i]."""
+    lib = _load()
+    x = _f64(x)
+    offs = np.ascontiguousarray(stream_offsets, np.int64)
+    n = len(offs) - 1
+    M = x.shape[1]
+    w = {k: _f64(v) for k, v in weights.items()}
+    H, D = w["w1"].shape
+    L = w["wmu"].shape[0]
+    assert D == window * M
+    ps = np.ascontiguousarray(streams, np.int32)
+    pk = np.ascontiguousarray(ks, np.int64)
+    nwin = window_count(np.diff(offs), window, stride)
+    assert np.all(pk >= 0) and np.all(pk < nwin[ps]), "window index out of range"
+    R = ref_len(np.diff(offs), ref_frac)
+    em = es = None
+    if ref_mean is not None:
+        em = _f64(np.asarray(ref_mean).reshape(n, M))
+        es = _f64(np.asarray(ref_std).reshape(n, M))
+    npairs = len(ps)
+    sc, md, mds = np.empty(npairs), np.empty(npairs), np.empty(npairs)
+    if npairs:
+        lib.oracle_score_pairs(
+            _ptr(x), _ptr(offs), n, M, int(window), int(stride), H, L, ACT[act], _ptr(R),
+            _ptr(w["w1"]), _ptr(w["b1"]), _ptr(w["wmu"]), _ptr(w["bmu"]), _ptr(w["wlv"]),
+            _ptr(w["blv"]), _ptr(w["wd1"]), _ptr(w["bd1"]), _ptr(w["wd2"]), _ptr(w["bd2"]),
+            1 if bf16 else 0, _ptr(em), _ptr(es), _ptr(ps), _ptr(pk), npairs,
+            _ptr(sc), _ptr(md), _ptr(mds), int(threads))
+    return sc, md, mds
 
 
 def window_debug(x_stream, k, *, window, stride, weights, mean, std, act="relu", bf16=False):

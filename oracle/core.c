@@ -91,7 +91,7 @@ typedef struct {
  */
 static void score_window(const double *xs, int M, int W, int S, int64_t k, int H, int L, int act,
                          const oracle_weights *wt, const double *mean, const double *std, int bf16,
-                         double *buf, double *score, double *md, double *dbg)
+                         double *buf, double *score, double *md, double *md_scale, double *dbg)
 {
     const int D = W * M;
     double *v = buf, *h = v + D, *mu = h + H, *lv = mu + L, *hd = lv + L, *mrec = hd + H;
@@ -142,15 +142,18 @@ static void score_window(const double *xs, int M, int W, int S, int64_t k, int H
             a += wt->wd1[i * L + l] * mu[l];
         hd[i] = act_fn(a, act);
     }
-    double diff = 0.0;
+    double diff = 0.0, mag = 0.0;
     for (int j = 0; j < D; ++j) {
         double r = wt->bd2[j];
         for (int i = 0; i < H; ++i)
             r += wt->wd2[(int64_t)j * H + i] * hd[i];
         mrec[j] = r;
         diff += v[j] - r;
+        mag += fabs(v[j]) + fabs(r);
     }
     *md = diff / (double)D;
+    if (md_scale)
+        *md_scale = mag / (double)D;     /* mean|v| + mean|m'|: the scale md is compared at */
     if (dbg) {
         memcpy(dbg, v, sizeof(double) * D);
         memcpy(dbg + D, h, sizeof(double) * H);
@@ -171,7 +174,7 @@ void oracle_window_debug(const double *xs, int M, int W, int S, int64_t k, int H
     oracle_weights wt = {w1, b1, wmu, bmu, wlv, blv, wd1, bd1, wd2, bd2};
     const int D = W * M;
     double *buf = (double *)malloc(sizeof(double) * (2 * (size_t)D + 2 * (size_t)H + 2 * (size_t)L));
-    score_window(xs, M, W, S, k, H, L, act, &wt, mean, std, bf16, buf, score, md, dbg);
+    score_window(xs, M, W, S, k, H, L, act, &wt, mean, std, bf16, buf, score, md, NULL, dbg);
     free(buf);
 }
 
@@ -192,7 +195,8 @@ int oracle_score_batch(const double *x, const int64_t *stream_off, int n, int M,
                        const double *wd2, const double *bd2, int bf16,
                        const double *ext_mean, const double *ext_std,
                        const int64_t *win_off, const int64_t *win_count,
-                       double *score, double *md, double *out_mean, double *out_std, int nthreads)
+                       double *score, double *md, double *md_scale, double *out_mean, double *out_std,
+                       int nthreads)
 {
     oracle_weights wt = {w1, b1, wmu, bmu, wlv, blv, wd1, bd1, wd2, bd2};
     const int D = W * M;
@@ -245,11 +249,13 @@ int oracle_score_batch(const double *x, const int64_t *stream_off, int n, int M,
             }
             int s = lo;
             int64_t k = g - first[s];
-            double sc, dm;
+            double sc, dm, ms;
             score_window(x + stream_off[s] * M, M, W, S, k, H, L, act, &wt, mean + (size_t)s * M,
-                         std + (size_t)s * M, bf16, buf, &sc, &dm, NULL);
+                         std + (size_t)s * M, bf16, buf, &sc, &dm, &ms, NULL);
             score[win_off[s] + k] = sc;
             md[win_off[s] + k] = dm;
+            if (md_scale)
+                md_scale[win_off[s] + k] = ms;
         }
         free(buf);
     }
@@ -258,6 +264,69 @@ int oracle_score_batch(const double *x, const int64_t *stream_off, int n, int M,
     if (out_std)
         memcpy(out_std, std, sizeof(double) * (size_t)n * M);
     free(first);
+    free(mean);
+    free(std);
+    return used;
+}
+
+/*
+ * Sampled windows: pair i is window pk[i] of stream ps[i]. Reference statistics are computed
+ * for every stream that appears (or taken from ext_mean/ext_std [n][M]).
+ */
+int oracle_score_pairs(const double *x, const int64_t *stream_off, int n, int M, int W, int S,
+                       int H, int L, int act, const int64_t *ref_len,
+                       const double *w1, const double *b1, const double *wmu, const double *bmu,
+                       const double *wlv, const double *blv, const double *wd1, const double *bd1,
+                       const double *wd2, const double *bd2, int bf16,
+                       const double *ext_mean, const double *ext_std,
+                       const int32_t *ps, const int64_t *pk, int64_t npairs,
+                       double *score, double *md, double *md_scale, int nthreads)
+{
+    oracle_weights wt = {w1, b1, wmu, bmu, wlv, blv, wd1, bd1, wd2, bd2};
+    const int D = W * M;
+    int used = 1;
+#ifdef _OPENMP
+    if (nthreads > 0)
+        omp_set_num_threads(nthreads);
+#endif
+    double *mean = (double *)malloc(sizeof(double) * ((size_t)n * M + 1));
+    double *std = (double *)malloc(sizeof(double) * ((size_t)n * M + 1));
+    char *need = (char *)calloc((size_t)n + 1, 1);
+    for (int64_t i = 0; i < npairs; ++i)
+        need[ps[i]] = 1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int s = 0; s < n; ++s) {
+        if (!need[s])
+            continue;
+        if (ext_mean) {
+            for (int m = 0; m < M; ++m) {
+                mean[(size_t)s * M + m] = ext_mean[(size_t)s * M + m];
+                std[(size_t)s * M + m] = ext_std[(size_t)s * M + m];
+            }
+        } else {
+            oracle_ref_stats(x + stream_off[s] * M, ref_len[s], M, mean + (size_t)s * M,
+                             std + (size_t)s * M);
+        }
+    }
+#pragma omp parallel
+    {
+#ifdef _OPENMP
+#pragma omp single
+        used = omp_get_num_threads();
+#endif
+        double *buf = (double *)malloc(sizeof(double) * (2 * (size_t)D + 2 * (size_t)H + 2 * (size_t)L));
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t i = 0; i < npairs; ++i) {
+            const int s = ps[i];
+            double ms;
+            score_window(x + stream_off[s] * M, M, W, S, pk[i], H, L, act, &wt, mean + (size_t)s * M,
+                         std + (size_t)s * M, bf16, buf, &score[i], &md[i], &ms, NULL);
+            if (md_scale)
+                md_scale[i] = ms;
+        }
+        free(buf);
+    }
+    free(need);
     free(mean);
     free(std);
     return used;

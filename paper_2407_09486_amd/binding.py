@@ -1,0 +1,256 @@
+"""Thin ctypes binding of libenova_detect (include/enova_detect.h).
+
+Every function keeps the C name and only marshals arguments: torch tensors become device
+pointers, numpy arrays become host pointers, ``torch.cuda.current_stream()`` becomes the
+``hipStream_t``. All computation happens in the library's HIP kernels; if the library is
+missing this module raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libenova_detect.so")
+
+ENOVA_OK, ENOVA_EINVAL, ENOVA_ESHAPE, ENOVA_ENOMEM, ENOVA_EHIP, ENOVA_EUNSUPPORTED, ENOVA_ENUMERIC = range(7)
+ENOVA_F32, ENOVA_BF16 = 0, 1
+ENOVA_RELU, ENOVA_TANH = 0, 1
+ENOVA_KERNEL_AUTO, ENOVA_KERNEL_VALU, ENOVA_KERNEL_MFMA = 0, 1, 2
+
+EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_offsets",
+           "enova_detect_ref_stats", "enova_detect_score", "enova_detect_threshold",
+           "enova_detect_flag", "enova_detect_set_timing", "enova_detect_kernel_times",
+           "enova_detect_kernel_kind", "enova_status_str", "enova_last_error"]
+
+
+class EnovaError(RuntimeError):
+    def __init__(self, status, func, msg):
+        super().__init__(f"{func} -> status {status}: {msg}")
+        self.status = status
+
+
+class enova_detect_config(ctypes.Structure):
+    _fields_ = [("metrics", ctypes.c_int32), ("window", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("latent", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("act", ctypes.c_int32), ("kernel", ctypes.c_int32), ("ref_frac", ctypes.c_float)]
+
+
+class enova_detect_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")]
+
+
+_lib = None
+
+
+def lib():
+    """Load the library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2407_09486_amd.build` "
+                           "(or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, F, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+    st = ctypes.c_int
+    L.enova_detect_init.argtypes = [ctypes.POINTER(enova_detect_config),
+                                    ctypes.POINTER(enova_detect_weights), ctypes.POINTER(P)]
+    L.enova_detect_destroy.argtypes = [P]
+    L.enova_detect_window_offsets.argtypes = [P, P, I32, P]
+    L.enova_detect_ref_stats.argtypes = [P, P, P, I32, P, P, P]
+    L.enova_detect_score.argtypes = [P, P, P, P, I32, I64, P, P, F, P, P, P, P]
+    L.enova_detect_threshold.argtypes = [P, P, P, P, I32, I64, D, D, P, P, P, P]
+    L.enova_detect_flag.argtypes = [P, P, I64, F, P, P]
+    L.enova_detect_set_timing.argtypes = [P, I32]
+    L.enova_detect_kernel_times.argtypes = [P, P, P]
+    L.enova_detect_kernel_kind.argtypes = [P, P]
+    for name in EXPORTS[:-2]:
+        getattr(L, name).restype = st
+    L.enova_status_str.argtypes = [st]
+    L.enova_status_str.restype = ctypes.c_char_p
+    L.enova_last_error.argtypes = []
+    L.enova_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status, func):
+    if status != ENOVA_OK:
+        raise EnovaError(status, func, lib().enova_last_error().decode())
+
+
+def _dptr(t):
+    """Device pointer of a torch tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _hptr(a):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ----------------------------------------------------------------------------- C entry points
+def enova_detect_init(config: enova_detect_config, weights: dict):
+    """weights: host numpy arrays w1 (float32, or uint16 bf16 bits), b1, wmu, bmu, wlv, blv,
+    wd1, bd1, wd2, bd2 (float32), row-major as in the header. Returns the handle (int)."""
+    keep = {}
+    for k, v in weights.items():
+        keep[k] = np.ascontiguousarray(v)
+    names = [f[0] for f in enova_detect_weights._fields_]
+    w = enova_detect_weights(**{k: _hptr(keep[k]) for k in names})
+    h = ctypes.c_void_p()
+    _check(lib().enova_detect_init(ctypes.byref(config), ctypes.byref(w), ctypes.byref(h)),
+           "enova_detect_init")
+    return h.value
+
+
+def enova_detect_destroy(handle):
+    _check(lib().enova_detect_destroy(ctypes.c_void_p(handle)), "enova_detect_destroy")
+
+
+def enova_detect_window_offsets(handle, stream_offsets_host):
+    so = np.ascontiguousarray(stream_offsets_host, dtype=np.int64)
+    out = np.zeros(len(so), np.int64)
+    _check(lib().enova_detect_window_offsets(ctypes.c_void_p(handle), _hptr(so), len(so) - 1, _hptr(out)),
+           "enova_detect_window_offsets")
+    return out
+
+
+def enova_detect_ref_stats(handle, x, stream_offsets, n_streams, out_mean, out_std, stream=None):
+    _check(lib().enova_detect_ref_stats(ctypes.c_void_p(handle), _dptr(x), _dptr(stream_offsets),
+                                        int(n_streams), _dptr(out_mean), _dptr(out_std), _stream(stream)),
+           "enova_detect_ref_stats")
+
+
+def enova_detect_score(handle, x, stream_offsets, window_offsets, n_streams, n_windows,
+                       ref_mean, ref_std, threshold, out_scores, out_md, out_flags, stream=None):
+    _check(lib().enova_detect_score(ctypes.c_void_p(handle), _dptr(x), _dptr(stream_offsets),
+                                    _dptr(window_offsets), int(n_streams), int(n_windows),
+                                    _dptr(ref_mean), _dptr(ref_std), float(threshold),
+                                    _dptr(out_scores), _dptr(out_md), _dptr(out_flags), _stream(stream)),
+           "enova_detect_score")
+
+
+def enova_detect_threshold(handle, scores, stream_offsets, window_offsets, n_streams, n_windows,
+                           level=0.98, q=1e-3, out_flags=None, stream=None):
+    """Returns (threshold, info dict)."""
+    thr = ctypes.c_float()
+    info = (ctypes.c_double * 6)()
+    _check(lib().enova_detect_threshold(ctypes.c_void_p(handle), _dptr(scores), _dptr(stream_offsets),
+                                        _dptr(window_offsets), int(n_streams), int(n_windows),
+                                        float(level), float(q), ctypes.byref(thr), info,
+                                        _dptr(out_flags), _stream(stream)),
+           "enova_detect_threshold")
+    return thr.value, {"t": info[0], "n": int(info[1]), "n_peaks": int(info[2]), "gamma": info[3],
+                       "sigma": info[4], "method": ("t", "moments", "mle")[int(info[5])]}
+
+
+def enova_detect_flag(handle, scores, n_windows, threshold, out_flags, stream=None):
+    _check(lib().enova_detect_flag(ctypes.c_void_p(handle), _dptr(scores), int(n_windows),
+                                   float(threshold), _dptr(out_flags), _stream(stream)),
+           "enova_detect_flag")
+
+
+def enova_detect_set_timing(handle, enable):
+    _check(lib().enova_detect_set_timing(ctypes.c_void_p(handle), 1 if enable else 0),
+           "enova_detect_set_timing")
+
+
+def enova_detect_kernel_times(handle):
+    a, b = ctypes.c_double(), ctypes.c_double()
+    _check(lib().enova_detect_kernel_times(ctypes.c_void_p(handle), ctypes.byref(a), ctypes.byref(b)),
+           "enova_detect_kernel_times")
+    return a.value, b.value
+
+
+def enova_detect_kernel_kind(handle):
+    k = ctypes.c_int32()
+    _check(lib().enova_detect_kernel_kind(ctypes.c_void_p(handle), ctypes.byref(k)),
+           "enova_detect_kernel_kind")
+    return k.value
+
+
+# ----------------------------------------------------------------------------- convenience
+def make_config(metrics, window, stride, hidden, latent=16, dtype="f32", act="relu",
+                kernel="auto", ref_frac=0.5) -> enova_detect_config:
+    return enova_detect_config(
+        metrics=metrics, window=window, stride=stride, hidden=hidden, latent=latent,
+        dtype={"f32": ENOVA_F32, "bf16": ENOVA_BF16}[dtype],
+        act={"relu": ENOVA_RELU, "tanh": ENOVA_TANH}[act],
+        kernel={"auto": ENOVA_KERNEL_AUTO, "valu": ENOVA_KERNEL_VALU, "mfma": ENOVA_KERNEL_MFMA}[kernel],
+        ref_frac=ref_frac)
+
+
+class Detector:
+    """Owns one library handle; methods call the C entry points on torch's current stream."""
+
+    def __init__(self, metrics, window, stride, hidden, weights: dict, latent=16, dtype="f32",
+                 act="relu", kernel="auto", ref_frac=0.5):
+        self.cfg = make_config(metrics, window, stride, hidden, latent, dtype, act, kernel, ref_frac)
+        self.dtype = dtype
+        self.handle = enova_detect_init(self.cfg, weights)
+
+    def close(self):
+        if self.handle:
+            enova_detect_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def kernel_kind(self):
+        return {1: "valu", 2: "mfma"}[enova_detect_kernel_kind(self.handle)]
+
+    def window_offsets(self, stream_offsets_host):
+        return enova_detect_window_offsets(self.handle, stream_offsets_host)
+
+    def score(self, x, stream_offsets, window_offsets, n_windows, ref_mean=None, ref_std=None,
+              threshold=math.nan, md=True, flags=False, stream=None):
+        import torch
+        dev = x.device
+        n = stream_offsets.numel() - 1
+        scores = torch.empty(max(n_windows, 1), dtype=torch.float32, device=dev)[:n_windows]
+        mdv = torch.empty(max(n_windows, 1), dtype=torch.float32, device=dev)[:n_windows] if md else None
+        fl = torch.empty(max(n_windows, 1), dtype=torch.uint8, device=dev)[:n_windows] if flags else None
+        enova_detect_score(self.handle, x, stream_offsets, window_offsets, n, n_windows, ref_mean, ref_std,
+                           threshold, scores, mdv, fl, stream)
+        return scores, mdv, fl
+
+    def threshold(self, scores, stream_offsets, window_offsets, level=0.98, q=1e-3, flags=False,
+                  stream=None):
+        import torch
+        n = stream_offsets.numel() - 1
+        nw = scores.numel()
+        fl = torch.empty(max(nw, 1), dtype=torch.uint8, device=scores.device)[:nw] if flags else None
+        thr, info = enova_detect_threshold(self.handle, scores, stream_offsets, window_offsets, n, nw,
+                                           level, q, fl, stream)
+        return thr, info, fl
+
+
+def weights_for_library(wt, dtype="f32") -> dict:
+    """Host arrays in the library's layout from a ``workloads.Weights``."""
+    d = {k: np.ascontiguousarray(getattr(wt, k), dtype=np.float32)
+         for k in ("b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")}
+    d["w1"] = (np.ascontiguousarray(wt.w1_bits) if dtype == "bf16"
+               else np.ascontiguousarray(wt.w1, dtype=np.float32))
+    return d

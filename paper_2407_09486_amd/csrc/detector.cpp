@@ -1,0 +1,769 @@
+// Host side of libenova_detect: argument validation, weight repacking, workspace management
+// and kernel launches behind the C ABI of include/enova_detect.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "enova_detect.h"
+#include "internal.h"
+
+namespace enova {
+int mfma_nbw_for(int hb);
+hipError_t prepare_score_mfma(const Geometry &g);
+}  // namespace enova
+
+using namespace enova;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+enova_status fail(enova_status st, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+enova_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(ENOVA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Keeps the caller's current device and switches to the detector's for the call's duration.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess)
+            return;
+        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard()
+    {
+        if (ok && prev >= 0)
+            (void)hipSetDevice(prev);
+    }
+};
+
+float bf16_bits_to_float(uint16_t b)
+{
+    uint32_t u = static_cast<uint32_t>(b) << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+}  // namespace
+
+struct enova_detector_s {
+    Geometry g{};
+    int device = 0;
+    int kind = 1;                 // 1 vector-ALU, 2 matrix-core
+    // weights
+    void *w1p = nullptr;          // matrix-core A fragments
+    void *w1t = nullptr;          // [D][H] transposed W1
+    float *small = nullptr;       // every small weight array, one allocation
+    float *b1 = nullptr, *bh = nullptr, *bmu = nullptr, *blv = nullptr, *wmu = nullptr,
+          *wlv = nullptr, *wd1 = nullptr, *bd1 = nullptr, *u = nullptr, *whp = nullptr,
+          *wd1p = nullptr;
+    float sum_bd2 = 0.0f;
+    // workspace
+    float *stats = nullptr;
+    size_t stats_cap = 0;         // floats
+    int64_t *tiles = nullptr;
+    size_t tiles_cap = 0;         // entries
+    int64_t *cal = nullptr;
+    size_t cal_cap = 0;
+    unsigned int *hist = nullptr; // 256 bins + 1 counter
+    float *peaks = nullptr;
+    size_t peaks_cap = 0;
+    // timing
+    bool timing = false;
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    bool ran_stats = false, ran_score = false;
+};
+
+namespace enova {
+
+bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
+{
+    g->M = cfg.metrics;
+    g->W = cfg.window;
+    g->S = cfg.stride;
+    g->H = cfg.hidden;
+    g->L = cfg.latent;
+    g->D = cfg.window * cfg.metrics;
+    g->dtype = cfg.dtype;
+    g->act = cfg.act;
+    g->ref_frac = cfg.ref_frac;
+    g->epc = cfg.dtype == ENOVA_F32 ? 4 : 8;
+    int mp = g->M;
+    while ((static_cast<int64_t>(g->S) * mp) % g->epc)
+        ++mp;
+    g->Mp = mp;
+    g->Q = (g->W + g->S - 1) / g->S;
+    const int64_t cpr = static_cast<int64_t>(g->S) * g->Mp / g->epc;
+    g->CPR = static_cast<int>(cpr);
+    g->CPRP = (g->CPR % 2 == 0) ? g->CPR + 1 : g->CPR;
+    int64_t kc = static_cast<int64_t>(g->Q) * g->CPR;
+    if (kc % 2)
+        ++kc;
+    g->KC = static_cast<int>(kc);
+    int hb = 1;
+    while (hb < 8 && 32 * hb < g->H)
+        hb *= 2;
+    g->HB = hb;
+    g->Hp = 32 * hb;
+    g->NBW = mfma_nbw_for(hb);
+    g->Nb = kWaves * g->NBW * 32;
+    g->lds_bytes = static_cast<size_t>(g->Nb + g->Q) * g->CPRP * 16 +
+                   static_cast<size_t>(g->Nb + g->Q) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
+    g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
+                 g->lds_bytes <= kLdsLimit;
+    if (!g->mfma_ok) {
+        g->Hp = ((g->H + 31) / 32) * 32;
+    }
+    return g->mfma_ok;
+}
+
+}  // namespace enova
+
+namespace {
+
+template <typename T>
+enova_status dev_upload(T **dst, const void *src, size_t bytes)
+{
+    if (bytes == 0)
+        bytes = 16;
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(dst), bytes);
+    if (e != hipSuccess)
+        return fail(ENOVA_ENOMEM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+    if (src) {
+        e = hipMemcpy(*dst, src, bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipMemcpy weights");
+    }
+    return ENOVA_OK;
+}
+
+template <typename T>
+enova_status ensure(T **buf, size_t *cap, size_t need)
+{
+    if (need <= *cap && *buf)
+        return ENOVA_OK;
+    if (*buf) {
+        (void)hipFree(*buf);
+        *buf = nullptr;
+        *cap = 0;
+    }
+    size_t n = std::max<size_t>(need, 64);
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(buf), n * sizeof(T));
+    if (e != hipSuccess)
+        return fail(ENOVA_ENOMEM, "workspace hipMalloc(%zu): %s", n * sizeof(T), hipGetErrorString(e));
+    *cap = n;
+    return ENOVA_OK;
+}
+
+void free_detector(enova_detector d)
+{
+    if (!d)
+        return;
+    void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->cal, d->hist, d->peaks};
+    for (void *p : ptrs)
+        if (p)
+            (void)hipFree(p);
+    for (hipEvent_t e : d->ev)
+        if (e)
+            (void)hipEventDestroy(e);
+    delete d;
+}
+
+int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+enova_status check_config(const enova_detect_config *c)
+{
+    if (!c)
+        return fail(ENOVA_EINVAL, "config is NULL");
+    if (c->metrics < 1 || c->window < 1 || c->stride < 1 || c->hidden < 1 || c->latent < 1)
+        return fail(ENOVA_EINVAL, "metrics, window, stride, hidden and latent must be >= 1");
+    if (c->latent > 64)
+        return fail(ENOVA_EINVAL, "latent %d > 64", c->latent);
+    if (static_cast<int64_t>(c->window) * c->metrics > 65536)
+        return fail(ENOVA_EINVAL, "window*metrics = %lld > 65536",
+                    static_cast<long long>(c->window) * c->metrics);
+    if (c->dtype != ENOVA_F32 && c->dtype != ENOVA_BF16)
+        return fail(ENOVA_EINVAL, "unknown dtype %d", c->dtype);
+    if (c->act != ENOVA_RELU && c->act != ENOVA_TANH)
+        return fail(ENOVA_EINVAL, "unknown activation %d", c->act);
+    if (c->kernel < ENOVA_KERNEL_AUTO || c->kernel > ENOVA_KERNEL_MFMA)
+        return fail(ENOVA_EINVAL, "unknown kernel choice %d", c->kernel);
+    if (!(c->ref_frac > 0.0f && c->ref_frac <= 1.0f))
+        return fail(ENOVA_EINVAL, "ref_frac must be in (0, 1]");
+    return ENOVA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *enova_status_str(enova_status s)
+{
+    switch (s) {
+    case ENOVA_OK: return "ok";
+    case ENOVA_EINVAL: return "invalid argument";
+    case ENOVA_ESHAPE: return "nothing to act on for this shape";
+    case ENOVA_ENOMEM: return "out of memory";
+    case ENOVA_EHIP: return "HIP runtime error";
+    case ENOVA_EUNSUPPORTED: return "unsupported request";
+    case ENOVA_ENUMERIC: return "non-finite values";
+    }
+    return "unknown status";
+}
+
+const char *enova_last_error(void) { return g_last_error.c_str(); }
+
+enova_status enova_detect_init(const enova_detect_config *config, const enova_detect_weights *w,
+                               enova_detector *out)
+{
+    if (!out)
+        return fail(ENOVA_EINVAL, "out is NULL");
+    *out = nullptr;
+    enova_status st = check_config(config);
+    if (st != ENOVA_OK)
+        return st;
+    if (!w || !w->w1 || !w->b1 || !w->wmu || !w->bmu || !w->wlv || !w->blv || !w->wd1 || !w->bd1 ||
+        !w->wd2 || !w->bd2)
+        return fail(ENOVA_EINVAL, "a weight pointer is NULL");
+
+    enova_detector d = new (std::nothrow) enova_detector_s();
+    if (!d)
+        return fail(ENOVA_ENOMEM, "host allocation");
+    Geometry &g = d->g;
+    plan_geometry(*config, &g);
+    if (config->kernel == ENOVA_KERNEL_MFMA && !g.mfma_ok) {
+        free_detector(d);
+        return fail(ENOVA_EUNSUPPORTED,
+                    "matrix-core kernel needs hidden <= 256, latent <= 16 and a tile that fits LDS "
+                    "(H=%d L=%d LDS=%zu)", g.H, g.L, g.lds_bytes);
+    }
+    if (config->kernel == ENOVA_KERNEL_VALU || !g.mfma_ok) {
+        if (g.H > 1024) {
+            free_detector(d);
+            return fail(ENOVA_EUNSUPPORTED, "hidden width %d > 1024 is not supported", g.H);
+        }
+        d->kind = 1;
+    } else {
+        d->kind = 2;
+    }
+    if (hipGetDevice(&d->device) != hipSuccess) {
+        free_detector(d);
+        return fail(ENOVA_EHIP, "no current HIP device");
+    }
+
+    const int H = g.H, L = g.L, D = g.D, Hp = g.Hp;
+    const bool bf = g.dtype == ENOVA_BF16;
+    auto w1v = [&](int h, int j) -> float {
+        if (bf)
+            return bf16_bits_to_float(static_cast<const uint16_t *>(w->w1)[static_cast<int64_t>(h) * D + j]);
+        return static_cast<const float *>(w->w1)[static_cast<int64_t>(h) * D + j];
+    };
+
+    // small arrays: b1[Hp] bd1[Hp] u[Hp] bh[32] bmu[L] blv[L] wmu[L*H] wlv[L*H] wd1[H*L]
+    //               whp[HB*16*64] wd1p[HB*8*64]
+    const size_t n_whp = d->kind == 2 ? static_cast<size_t>(g.HB) * 16 * 64 : 0;
+    const size_t n_wd1p = d->kind == 2 ? static_cast<size_t>(g.HB) * 8 * 64 : 0;
+    const size_t n_small = 3 * static_cast<size_t>(Hp) + 32 + 2 * L + 3 * static_cast<size_t>(L) * H +
+                           n_whp + n_wd1p;
+    std::vector<float> small(n_small, 0.0f);
+    size_t o = 0;
+    const size_t o_b1 = o; o += Hp;
+    const size_t o_bd1 = o; o += Hp;
+    const size_t o_u = o; o += Hp;
+    const size_t o_bh = o; o += 32;
+    const size_t o_bmu = o; o += L;
+    const size_t o_blv = o; o += L;
+    const size_t o_wmu = o; o += static_cast<size_t>(L) * H;
+    const size_t o_wlv = o; o += static_cast<size_t>(L) * H;
+    const size_t o_wd1 = o; o += static_cast<size_t>(H) * L;
+    const size_t o_whp = o; o += n_whp;
+    const size_t o_wd1p = o; o += n_wd1p;
+
+    for (int h = 0; h < H; ++h) {
+        small[o_b1 + h] = w->b1[h];
+        small[o_bd1 + h] = w->bd1[h];
+        double cs = 0.0;
+        for (int j = 0; j < D; ++j)
+            cs += static_cast<double>(w->wd2[static_cast<int64_t>(j) * H + h]);
+        small[o_u + h] = static_cast<float>(cs);
+    }
+    double sb = 0.0;
+    for (int j = 0; j < D; ++j)
+        sb += static_cast<double>(w->bd2[j]);
+    d->sum_bd2 = static_cast<float>(sb);
+    for (int l = 0; l < L; ++l) {
+        small[o_bmu + l] = w->bmu[l];
+        small[o_blv + l] = w->blv[l];
+        if (l < 16) {
+            small[o_bh + l] = w->bmu[l];
+            small[o_bh + 16 + l] = w->blv[l];
+        }
+    }
+    std::memcpy(&small[o_wmu], w->wmu, sizeof(float) * L * H);
+    std::memcpy(&small[o_wlv], w->wlv, sizeof(float) * L * H);
+    std::memcpy(&small[o_wd1], w->wd1, sizeof(float) * H * L);
+    if (d->kind == 2) {
+        for (int hb = 0; hb < g.HB; ++hb)
+            for (int r = 0; r < 16; ++r)
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int row = lane & 31;              // 0..15 mean head, 16..31 log-variance head
+                    const int h = hb * 32 + crow(r, lane >> 5);
+                    float v = 0.0f;
+                    if (h < H) {
+                        if (row < 16 && row < L)
+                            v = w->wmu[row * H + h];
+                        else if (row >= 16 && row - 16 < L)
+                            v = w->wlv[(row - 16) * H + h];
+                    }
+                    small[o_whp + (static_cast<size_t>(hb) * 16 + r) * 64 + lane] = v;
+                }
+        for (int hb = 0; hb < g.HB; ++hb)
+            for (int r = 0; r < 8; ++r)
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int h = hb * 32 + (lane & 31);
+                    const int l = crow(r, lane >> 5);
+                    float v = 0.0f;
+                    if (h < H && l < L)
+                        v = w->wd1[h * L + l];
+                    small[o_wd1p + (static_cast<size_t>(hb) * 8 + r) * 64 + lane] = v;
+                }
+    }
+    st = dev_upload(&d->small, small.data(), small.size() * sizeof(float));
+    if (st != ENOVA_OK) {
+        free_detector(d);
+        return st;
+    }
+    d->b1 = d->small + o_b1;
+    d->bd1 = d->small + o_bd1;
+    d->u = d->small + o_u;
+    d->bh = d->small + o_bh;
+    d->bmu = d->small + o_bmu;
+    d->blv = d->small + o_blv;
+    d->wmu = d->small + o_wmu;
+    d->wlv = d->small + o_wlv;
+    d->wd1 = d->small + o_wd1;
+    d->whp = d->small + o_whp;
+    d->wd1p = d->small + o_wd1p;
+
+    if (d->kind == 1) {
+        // transposed W1 [D][H] in the storage type
+        const size_t esz = bf ? 2 : 4;
+        std::vector<unsigned char> wt(static_cast<size_t>(D) * H * esz);
+        for (int h = 0; h < H; ++h)
+            for (int j = 0; j < D; ++j) {
+                const size_t dst = (static_cast<size_t>(j) * H + h) * esz;
+                const size_t src = (static_cast<size_t>(h) * D + j) * esz;
+                std::memcpy(&wt[dst], static_cast<const unsigned char *>(w->w1) + src, esz);
+            }
+        st = dev_upload(&d->w1t, wt.data(), wt.size());
+    } else {
+        // A fragments: step i, hidden block hb, lane -> 16 bytes of W1[h][chunk 2i + lane/32]
+        const int steps = g.KC / 2;
+        const size_t frag = static_cast<size_t>(steps) * g.HB * 64;
+        std::vector<uint32_t> pk(frag * 4, 0u);
+        for (int i = 0; i < steps; ++i)
+            for (int hb = 0; hb < g.HB; ++hb)
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int h = hb * 32 + (lane & 31);
+                    const int kappa = 2 * i + (lane >> 5);
+                    const int q = kappa / g.CPR;
+                    const int c = kappa - q * g.CPR;
+                    float vals[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    uint16_t bits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    for (int e = 0; e < g.epc; ++e) {
+                        const int jj = c * g.epc + e;
+                        const int tt = jj / g.Mp;
+                        const int m = jj - tt * g.Mp;
+                        const int t = q * g.S + tt;
+                        if (h < H && t < g.W && m < g.M && q < g.Q) {
+                            const int64_t j = static_cast<int64_t>(t) * g.M + m;
+                            if (bf)
+                                bits[e] = static_cast<const uint16_t *>(w->w1)[static_cast<int64_t>(h) * D + j];
+                            else
+                                vals[e] = w1v(h, static_cast<int>(j));
+                        }
+                    }
+                    uint32_t *dst = &pk[((static_cast<size_t>(i) * g.HB + hb) * 64 + lane) * 4];
+                    if (bf) {
+                        for (int e = 0; e < 4; ++e)
+                            dst[e] = static_cast<uint32_t>(bits[2 * e]) |
+                                     (static_cast<uint32_t>(bits[2 * e + 1]) << 16);
+                    } else {
+                        std::memcpy(dst, vals, 16);
+                    }
+                }
+        st = dev_upload(&d->w1p, pk.data(), pk.size() * sizeof(uint32_t));
+        if (st == ENOVA_OK) {
+            hipError_t e = prepare_score_mfma(g);
+            if (e != hipSuccess)
+                st = hip_fail(e, "configure matrix-core kernel");
+        }
+    }
+    if (st == ENOVA_OK) {
+        hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 260 * sizeof(unsigned int));
+        if (e != hipSuccess)
+            st = fail(ENOVA_ENOMEM, "hipMalloc(hist)");
+    }
+    if (st != ENOVA_OK) {
+        free_detector(d);
+        return st;
+    }
+    *out = d;
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_destroy(enova_detector det)
+{
+    if (!det)
+        return ENOVA_OK;
+    DeviceGuard dg(det->device);
+    (void)hipDeviceSynchronize();
+    free_detector(det);
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_window_offsets(enova_detector det, const int64_t *soff, int32_t n,
+                                         int64_t *woff)
+{
+    if (!det || !soff || !woff)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    if (n < 0)
+        return fail(ENOVA_EINVAL, "n_streams < 0");
+    if (soff[0] != 0)
+        return fail(ENOVA_EINVAL, "stream_offsets[0] must be 0");
+    const int64_t W = det->g.W, S = det->g.S;
+    woff[0] = 0;
+    for (int32_t s = 0; s < n; ++s) {
+        const int64_t T = soff[s + 1] - soff[s];
+        if (T < 0)
+            return fail(ENOVA_EINVAL, "stream_offsets decrease at stream %d", s);
+        woff[s + 1] = woff[s] + (T >= W ? (T - W) / S + 1 : 0);
+    }
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_ref_stats(enova_detector det, const void *x, const int64_t *soff,
+                                    int32_t n, float *out_mean, float *out_std, hipStream_t stream)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    if (n < 0)
+        return fail(ENOVA_EINVAL, "n_streams < 0");
+    if (n == 0)
+        return ENOVA_OK;
+    if (!x || !soff || !out_mean || !out_std)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(det->device);
+    hipError_t e = launch_ref_stats(det->g, x, soff, n, out_mean, out_std, stream);
+    if (e != hipSuccess)
+        return hip_fail(e, "reference statistics kernel");
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_score(enova_detector det, const void *x, const int64_t *soff,
+                                const int64_t *woff, int32_t n, int64_t n_windows,
+                                const float *ref_mean, const float *ref_std, float threshold,
+                                float *out_scores, float *out_md, uint8_t *out_flags,
+                                hipStream_t stream)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    if (n < 0 || n_windows < 0)
+        return fail(ENOVA_EINVAL, "n_streams and n_windows must be >= 0");
+    if ((ref_mean == nullptr) != (ref_std == nullptr))
+        return fail(ENOVA_EINVAL, "ref_mean and ref_std must both be given or both be NULL");
+    det->ran_stats = det->ran_score = false;
+    if (n == 0 || n_windows == 0)
+        return ENOVA_OK;
+    if (!x || !soff || !woff || !out_scores)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    const bool want_flags = out_flags != nullptr && !std::isnan(threshold);
+    DeviceGuard dg(det->device);
+    if (!dg.ok)
+        return fail(ENOVA_EHIP, "cannot select the detector's device");
+    const Geometry &g = det->g;
+    hipError_t e;
+    if (det->timing && !det->ev[0]) {
+        for (auto &ev : det->ev)
+            if ((e = hipEventCreate(&ev)) != hipSuccess)
+                return hip_fail(e, "hipEventCreate");
+    }
+    if (!ref_mean) {
+        enova_status st = ensure(&det->stats, &det->stats_cap, 2 * static_cast<size_t>(n) * g.M);
+        if (st != ENOVA_OK)
+            return st;
+        ref_mean = det->stats;
+        ref_std = det->stats + static_cast<size_t>(n) * g.M;
+        if (det->timing)
+            (void)hipEventRecord(det->ev[0], stream);
+        e = launch_ref_stats(g, x, soff, n, det->stats, det->stats + static_cast<size_t>(n) * g.M, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "reference statistics kernel");
+        if (det->timing)
+            (void)hipEventRecord(det->ev[1], stream);
+        det->ran_stats = true;
+    }
+    ScoreParams p{};
+    p.x = x;
+    p.soff = soff;
+    p.woff = woff;
+    p.n_streams = n;
+    p.n_windows = n_windows;
+    p.mean = ref_mean;
+    p.std = ref_std;
+    p.w1p = static_cast<const uint4 *>(det->w1p);
+    p.whp = det->whp;
+    p.wd1p = det->wd1p;
+    p.w1t = det->w1t;
+    p.wmu = det->wmu;
+    p.wlv = det->wlv;
+    p.wd1 = det->wd1;
+    p.b1 = det->b1;
+    p.bh = det->bh;
+    p.bmu = det->bmu;
+    p.blv = det->blv;
+    p.bd1 = det->bd1;
+    p.u = det->u;
+    p.sum_bd2 = det->sum_bd2;
+    p.threshold = threshold;
+    p.write_flags = want_flags ? 1 : 0;
+    p.scores = out_scores;
+    p.md = out_md;
+    p.flags = out_flags;
+    if (det->kind == 2) {
+        enova_status st = ensure(&det->tiles, &det->tiles_cap, static_cast<size_t>(n) + 1);
+        if (st != ENOVA_OK)
+            return st;
+        e = launch_stream_scan(g, soff, woff, n, 0, g.Nb, det->tiles, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "tile scan kernel");
+        p.tile_off = det->tiles;
+        const int64_t grid = (n_windows + g.Nb - 1) / g.Nb + n;
+        if (grid > 0x7fffffffLL)
+            return fail(ENOVA_EUNSUPPORTED, "too many tiles (%lld)", static_cast<long long>(grid));
+        if (det->timing)
+            (void)hipEventRecord(det->ev[2], stream);
+        e = launch_score_mfma(g, p, grid, stream);
+    } else {
+        if ((n_windows + 15) / 16 > 0x7fffffffLL)
+            return fail(ENOVA_EUNSUPPORTED, "too many windows");
+        if (det->timing)
+            (void)hipEventRecord(det->ev[2], stream);
+        e = launch_score_valu(g, p, stream);
+    }
+    if (e != hipSuccess)
+        return hip_fail(e, "scoring kernel");
+    if (det->timing)
+        (void)hipEventRecord(det->ev[3], stream);
+    det->ran_score = true;
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_flag(enova_detector det, const float *scores, int64_t n_windows,
+                               float threshold, uint8_t *out_flags, hipStream_t stream)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    if (n_windows < 0)
+        return fail(ENOVA_EINVAL, "n_windows < 0");
+    if (n_windows == 0)
+        return ENOVA_OK;
+    if (!scores || !out_flags)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(det->device);
+    hipError_t e = launch_flag(scores, n_windows, threshold, out_flags, stream);
+    if (e != hipSuccess)
+        return hip_fail(e, "flag kernel");
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_threshold(enova_detector det, const float *scores, const int64_t *soff,
+                                    const int64_t *woff, int32_t n, int64_t n_windows, double level,
+                                    double q, float *out_threshold, double *out_info,
+                                    uint8_t *out_flags, hipStream_t stream)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    if (!out_threshold)
+        return fail(ENOVA_EINVAL, "out_threshold is NULL");
+    if (!(level > 0.0 && level < 1.0) || !(q > 0.0 && q < 1.0))
+        return fail(ENOVA_EINVAL, "level and q must lie in (0, 1)");
+    if (n < 0 || n_windows < 0)
+        return fail(ENOVA_EINVAL, "n_streams and n_windows must be >= 0");
+    if (n == 0 || n_windows == 0)
+        return fail(ENOVA_ESHAPE, "no windows to calibrate on");
+    if (!scores || !soff || !woff)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(det->device);
+    const Geometry &g = det->g;
+    enova_status st = ensure(&det->cal, &det->cal_cap, static_cast<size_t>(n) + 1);
+    if (st != ENOVA_OK)
+        return st;
+    hipError_t e = launch_stream_scan(g, soff, woff, n, 1, 1, det->cal, stream);
+    if (e != hipSuccess)
+        return hip_fail(e, "calibration scan kernel");
+    int64_t n_cal = 0;
+    if ((e = hipMemcpyAsync(&n_cal, det->cal + n, sizeof(int64_t), hipMemcpyDeviceToHost, stream)) !=
+            hipSuccess ||
+        (e = hipStreamSynchronize(stream)) != hipSuccess)
+        return hip_fail(e, "calibration count");
+    if (n_cal <= 0)
+        return fail(ENOVA_ESHAPE, "no window lies inside a reference prefix");
+
+    // exact order statistic at ceil(level*n) - 1 by a 4-pass radix select over float keys
+    int64_t rank = static_cast<int64_t>(std::ceil(level * static_cast<double>(n_cal))) - 1;
+    if (rank < 0)
+        rank = 0;
+    if (rank > n_cal - 1)
+        rank = n_cal - 1;
+    uint32_t prefix = 0;
+    int64_t n_greater = 0;
+    unsigned int hist[256];
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        if ((e = hipMemsetAsync(det->hist, 0, 256 * sizeof(unsigned int), stream)) != hipSuccess)
+            return hip_fail(e, "hipMemsetAsync");
+        e = launch_calib_hist(scores, woff, det->cal, n, n_cal, shift, prefix, det->hist, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "calibration histogram kernel");
+        if ((e = hipMemcpyAsync(hist, det->hist, sizeof(hist), hipMemcpyDeviceToHost, stream)) !=
+                hipSuccess ||
+            (e = hipStreamSynchronize(stream)) != hipSuccess)
+            return hip_fail(e, "calibration histogram copy");
+        int64_t cum = 0;
+        int digit = -1;
+        for (int dgt = 0; dgt < 256; ++dgt) {
+            if (digit < 0 && rank < cum + hist[dgt]) {
+                digit = dgt;
+                rank -= cum;
+            } else if (digit >= 0) {
+                n_greater += hist[dgt];
+            }
+            cum += hist[dgt];
+        }
+        if (digit < 0)
+            return fail(ENOVA_EHIP, "radix select lost the order statistic");
+        prefix = (prefix << 8) | static_cast<uint32_t>(digit);
+    }
+    const uint32_t key_t = prefix;
+    const uint32_t bits = (key_t & 0x80000000u) ? (key_t & 0x7fffffffu) : ~key_t;
+    float t_f;
+    std::memcpy(&t_f, &bits, 4);
+    if (!std::isfinite(t_f))
+        return fail(ENOVA_ENUMERIC, "non-finite calibration score at the level quantile");
+    std::vector<double> ex;
+    if (n_greater > 0) {
+        if (n_greater > 0x7fffffffLL)
+            return fail(ENOVA_EUNSUPPORTED, "too many peaks");
+        st = ensure(&det->peaks, &det->peaks_cap, static_cast<size_t>(n_greater));
+        if (st != ENOVA_OK)
+            return st;
+        if ((e = hipMemsetAsync(det->hist + 256, 0, sizeof(unsigned int), stream)) != hipSuccess)
+            return hip_fail(e, "hipMemsetAsync");
+        e = launch_calib_collect(scores, woff, det->cal, n, n_cal, key_t, det->peaks,
+                                 static_cast<unsigned int>(n_greater), det->hist + 256, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "peak collection kernel");
+        std::vector<float> pk(static_cast<size_t>(n_greater));
+        unsigned int cnt = 0;
+        if ((e = hipMemcpyAsync(pk.data(), det->peaks, pk.size() * sizeof(float),
+                                hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+            (e = hipMemcpyAsync(&cnt, det->hist + 256, sizeof(cnt), hipMemcpyDeviceToHost, stream)) !=
+                hipSuccess ||
+            (e = hipStreamSynchronize(stream)) != hipSuccess)
+            return hip_fail(e, "peak copy");
+        if (static_cast<int64_t>(cnt) != n_greater)
+            return fail(ENOVA_EHIP, "peak count mismatch (%u vs %lld)", cnt,
+                        static_cast<long long>(n_greater));
+        ex.resize(pk.size());
+        for (size_t i = 0; i < pk.size(); ++i) {
+            if (!std::isfinite(pk[i]))
+                return fail(ENOVA_ENUMERIC, "non-finite calibration score");
+            ex[i] = static_cast<double>(pk[i]) - static_cast<double>(t_f);
+        }
+        std::sort(ex.begin(), ex.end());
+    }
+    PotResult r = pot_from_peaks(static_cast<double>(t_f), n_cal, ex.data(),
+                                 static_cast<int64_t>(ex.size()), q);
+    const float thr = static_cast<float>(r.z);
+    *out_threshold = thr;
+    if (out_info) {
+        out_info[0] = r.t;
+        out_info[1] = static_cast<double>(r.n);
+        out_info[2] = static_cast<double>(r.n_peaks);
+        out_info[3] = r.gamma;
+        out_info[4] = r.sigma;
+        out_info[5] = r.method;
+    }
+    if (out_flags) {
+        e = launch_flag(scores, n_windows, thr, out_flags, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "flag kernel");
+        if ((e = hipStreamSynchronize(stream)) != hipSuccess)
+            return hip_fail(e, "flag kernel");
+    }
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_set_timing(enova_detector det, int32_t enable)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    det->timing = enable != 0;
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_kernel_times(enova_detector det, double *score_ms, double *stats_ms)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    DeviceGuard dg(det->device);
+    float a = 0.0f, b = 0.0f;
+    hipError_t e;
+    if (det->timing && det->ran_score && det->ev[2]) {
+        if ((e = hipEventSynchronize(det->ev[3])) != hipSuccess ||
+            (e = hipEventElapsedTime(&a, det->ev[2], det->ev[3])) != hipSuccess)
+            return hip_fail(e, "score kernel timing");
+    }
+    if (det->timing && det->ran_stats && det->ev[0]) {
+        if ((e = hipEventSynchronize(det->ev[1])) != hipSuccess ||
+            (e = hipEventElapsedTime(&b, det->ev[0], det->ev[1])) != hipSuccess)
+            return hip_fail(e, "stats kernel timing");
+    }
+    if (score_ms)
+        *score_ms = a;
+    if (stats_ms)
+        *stats_ms = b;
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_kernel_kind(enova_detector det, int32_t *kind)
+{
+    if (!det || !kind)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    *kind = det->kind;
+    return ENOVA_OK;
+}
+
+}  // extern "C"

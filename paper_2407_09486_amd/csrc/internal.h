@@ -1,0 +1,106 @@
+// Internal declarations of libenova_detect: kernel parameter blocks and launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+#include "enova_detect.h"
+
+namespace enova {
+
+// ---------------------------------------------------------------------------------------------
+// Geometry of the matrix-core path.
+//
+// The window of W steps x M metrics is cut into Q = ceil(W/S) "super-rows" of S consecutive
+// steps (S*Mp elements, Mp = M padded so a super-row is a whole number of 16-byte chunks).
+// Window k of a stream consists of super-rows k .. k+Q-1 of that stream, so a tile of Nb
+// consecutive windows needs only Nb+Q-1 super-rows staged in LDS: every staged element is
+// normalised once and then read by up to Q windows (implicit im2col of a strided 1-D
+// convolution). The reduction index is walked chunk by chunk: chunk kappa = q*CPR + c is
+// 16-byte chunk c of the window's super-row q.
+// ---------------------------------------------------------------------------------------------
+struct Geometry {
+    int M, W, S, H, L, D;   // true sizes
+    int dtype, act;
+    float ref_frac;
+    int epc;                // elements per 16-byte chunk: 4 (f32) or 8 (bf16)
+    int Mp;                 // metrics padded so that S*Mp % epc == 0
+    int Q;                  // super-rows per window
+    int CPR;                // chunks per super-row
+    int CPRP;               // LDS row pitch in chunks (odd, so 16 consecutive rows hit distinct banks)
+    int KC;                 // chunks per window, rounded up to even
+    int Hp;                 // hidden width padded to 32*HB
+    int HB;                 // 32-row hidden blocks per wave
+    int NBW;                // 32-window blocks per wave
+    int Nb;                 // windows per tile (4 waves)
+    size_t lds_bytes;       // dynamic LDS of the matrix-core kernel
+    bool mfma_ok;
+};
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr size_t kLdsLimit = 160 * 1024;
+
+bool plan_geometry(const enova_detect_config &cfg, Geometry *g);
+
+// Parameter block of the scoring kernels (passed by value).
+struct ScoreParams {
+    const void *x;
+    const int64_t *soff;
+    const int64_t *woff;
+    const int64_t *tile_off;     // matrix-core kernel only
+    int n_streams;
+    int64_t n_windows;
+    const float *mean;
+    const float *std;
+    // matrix-core packed weights
+    const uint4 *w1p;            // [KC/2][HB][64 lanes] 16-byte A fragments
+    const float *whp;            // [HB][16][64] heads (mu rows 0..15, log-var rows 16..31)
+    const float *wd1p;           // [HB][8][64]  decoder hidden layer
+    // vector-kernel weights
+    const void *w1t;             // [D][H] transposed W1 (float or bf16 bits)
+    const float *wmu, *wlv, *wd1;
+    // shared small vectors (padded to Hp / 32)
+    const float *b1;             // [Hp]
+    const float *bh;             // [32]: bmu (padded to 16), blv (padded to 16)
+    const float *bmu, *blv;      // [L]
+    const float *bd1;            // [Hp]
+    const float *u;              // [Hp] column sums of Wd2
+    float sum_bd2;
+    float threshold;
+    int write_flags;
+    float *scores;
+    float *md;
+    uint8_t *flags;
+};
+
+// Launchers (return the launch error).
+hipError_t launch_ref_stats(const Geometry &g, const void *x, const int64_t *soff, int n,
+                            float *mean, float *std, hipStream_t st);
+// out[s] = sum_{r<s} ceil(count(s)/div) for count(s) = (mode 0) windows of stream s,
+// (mode 1) calibration windows of stream s. out has n+1 entries.
+hipError_t launch_stream_scan(const Geometry &g, const int64_t *soff, const int64_t *woff, int n,
+                              int mode, int div, int64_t *out, hipStream_t st);
+hipError_t launch_score_valu(const Geometry &g, const ScoreParams &p, hipStream_t st);
+hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st);
+hipError_t launch_flag(const float *scores, int64_t n, float thr, uint8_t *flags, hipStream_t st);
+// Radix-select pass over the calibration scores: histogram of the 8-bit digit at `shift`
+// among keys whose bits above shift+8 equal `prefix`.
+hipError_t launch_calib_hist(const float *scores, const int64_t *woff, const int64_t *cal_off,
+                             int n, int64_t n_cal, int shift, uint32_t prefix,
+                             unsigned int *hist, hipStream_t st);
+// Copy every calibration score whose key exceeds `key` into out (order unspecified).
+hipError_t launch_calib_collect(const float *scores, const int64_t *woff, const int64_t *cal_off,
+                                int n, int64_t n_cal, uint32_t key, float *out, unsigned int cap,
+                                unsigned int *counter, hipStream_t st);
+
+// Host GPD fit of the excesses (fp64). method: 0 threshold is t, 1 moments, 2 maximum likelihood.
+struct PotResult {
+    double z, t, gamma, sigma;
+    int64_t n, n_peaks;
+    int method;
+};
+PotResult pot_from_peaks(double t, int64_t n, const double *excess, int64_t n_peaks, double q);
+
+}  // namespace enova

@@ -1,0 +1,305 @@
+// Bandwidth-bound helper kernels: reference statistics, per-stream scans, flags and the
+// radix-select passes of the peaks-over-threshold calibration.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace enova {
+
+namespace {
+
+template <int DT>
+__device__ __forceinline__ float load_x(const void *x, int64_t idx)
+{
+    if constexpr (DT == ENOVA_F32) {
+        return static_cast<const float *>(x)[idx];
+    } else {
+        uint32_t b = static_cast<const uint16_t *>(x)[idx];
+        return __uint_as_float(b << 16);
+    }
+}
+
+__device__ __forceinline__ int64_t ref_len_dev(float ref_frac, int64_t T)
+{
+    return static_cast<int64_t>(floor(static_cast<double>(ref_frac) * static_cast<double>(T)));
+}
+
+__device__ __forceinline__ void finish_stats(double x0, double s1, double s2, int64_t R, float *mean,
+                                             float *std)
+{
+    if (R <= 0) {
+        *mean = 0.0f;
+        *std = 1.0f;
+        return;
+    }
+    const double inv = 1.0 / static_cast<double>(R);
+    const double m1 = s1 * inv;
+    const double mu = x0 + m1;
+    double var = s2 * inv - m1 * m1;
+    var = var > 0.0 ? var : 0.0;
+    double sd = sqrt(var);
+    if (sd <= 1e-6 * fmax(1.0, fabs(mu)))
+        sd = 1.0;   // the metric is constant over the reference prefix
+    *mean = static_cast<float>(mu);
+    *std = static_cast<float>(sd);
+}
+
+// Reference statistics of one stream per block. Values are shifted by the first reference
+// value of their metric and accumulated in fp64 (sum and sum of squares), then reduced in a
+// fixed order, so the result does not depend on the launch.
+template <int DT>
+__global__ __launch_bounds__(256) void k_ref_stats(const void *__restrict__ x,
+                                                   const int64_t *__restrict__ soff, int M,
+                                                   float ref_frac, float *__restrict__ mean,
+                                                   float *__restrict__ std)
+{
+    __shared__ double red1[256];
+    __shared__ double red2[256];
+    const int s = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int64_t base = soff[s];
+    const int64_t T = soff[s + 1] - base;
+    const int64_t R = ref_len_dev(ref_frac, T);
+
+    if (M <= 256 && (256 % M) == 0) {
+        const int per = 256 / M;
+        const int m = tid % M;
+        const int r0 = tid / M;
+        const double x0 = R > 0 ? static_cast<double>(load_x<DT>(x, base * M + m)) : 0.0;
+        double s1 = 0.0, s2 = 0.0;
+        int64_t t = r0;
+        for (; t + 3 * per < R; t += 4 * per) {
+            const double d0 = static_cast<double>(load_x<DT>(x, (base + t) * M + m)) - x0;
+            const double d1 = static_cast<double>(load_x<DT>(x, (base + t + per) * M + m)) - x0;
+            const double d2 = static_cast<double>(load_x<DT>(x, (base + t + 2 * per) * M + m)) - x0;
+            const double d3 = static_cast<double>(load_x<DT>(x, (base + t + 3 * per) * M + m)) - x0;
+            s1 += (d0 + d1) + (d2 + d3);
+            s2 += (d0 * d0 + d1 * d1) + (d2 * d2 + d3 * d3);
+        }
+        for (; t < R; t += per) {
+            const double d = static_cast<double>(load_x<DT>(x, (base + t) * M + m)) - x0;
+            s1 += d;
+            s2 += d * d;
+        }
+        red1[tid] = s1;
+        red2[tid] = s2;
+        __syncthreads();
+        if (tid < M) {
+            double a = 0.0, b = 0.0;
+            for (int j = 0; j < per; ++j) {
+                a += red1[tid + j * M];
+                b += red2[tid + j * M];
+            }
+            finish_stats(x0, a, b, R, mean + static_cast<int64_t>(s) * M + tid,
+                         std + static_cast<int64_t>(s) * M + tid);
+        }
+    } else {
+        for (int m = tid; m < M; m += 256) {
+            const double x0 = R > 0 ? static_cast<double>(load_x<DT>(x, base * M + m)) : 0.0;
+            double s1 = 0.0, s2 = 0.0;
+            for (int64_t t = 0; t < R; ++t) {
+                const double d = static_cast<double>(load_x<DT>(x, (base + t) * M + m)) - x0;
+                s1 += d;
+                s2 += d * d;
+            }
+            finish_stats(x0, s1, s2, R, mean + static_cast<int64_t>(s) * M + m,
+                         std + static_cast<int64_t>(s) * M + m);
+        }
+    }
+}
+
+// Single-block exclusive scan of a per-stream count.
+__global__ __launch_bounds__(1024) void k_stream_scan(const int64_t *__restrict__ soff,
+                                                      const int64_t *__restrict__ woff, int n,
+                                                      int mode, int div, int W, int S,
+                                                      float ref_frac, int64_t *__restrict__ out)
+{
+    __shared__ int64_t part[1024];
+    const int tid = threadIdx.x;
+    const int64_t chunk = (static_cast<int64_t>(n) + 1023) / 1024;
+    const int64_t a = tid * chunk;
+    const int64_t b = a + chunk < n ? a + chunk : n;
+    auto count = [&](int64_t s) -> int64_t {
+        int64_t c = woff[s + 1] - woff[s];
+        if (mode == 1) {
+            const int64_t R = ref_len_dev(ref_frac, soff[s + 1] - soff[s]);
+            const int64_t cal = R >= W ? (R - W) / S + 1 : 0;
+            c = cal < c ? cal : c;
+        }
+        return div > 1 ? (c + div - 1) / div : c;
+    };
+    int64_t local = 0;
+    for (int64_t s = a; s < b; ++s)
+        local += count(s);
+    part[tid] = local;
+    __syncthreads();
+    if (tid == 0) {
+        int64_t run = 0;
+        for (int i = 0; i < 1024; ++i) {
+            const int64_t v = part[i];
+            part[i] = run;
+            run += v;
+        }
+        out[n] = run;
+    }
+    __syncthreads();
+    int64_t run = part[tid];
+    for (int64_t s = a; s < b; ++s) {
+        out[s] = run;
+        run += count(s);
+    }
+}
+
+__global__ void k_flag(const float *__restrict__ scores, int64_t n, float thr,
+                       uint8_t *__restrict__ flags)
+{
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
+        flags[i] = scores[i] > thr ? 1 : 0;
+}
+
+// Order-preserving map of a float to an unsigned key.
+__device__ __forceinline__ uint32_t fkey(float f)
+{
+    const uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int kCalItems = 16;   // calibration scores per thread per block
+
+// Upper-bound search: the stream s with cal_off[s] <= ci < cal_off[s+1].
+__device__ __forceinline__ int find_stream(const int64_t *off, int n, int64_t ci)
+{
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= ci)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(256) void k_calib_hist(const float *__restrict__ scores,
+                                                    const int64_t *__restrict__ woff,
+                                                    const int64_t *__restrict__ cal_off, int n,
+                                                    int64_t n_cal, int shift, uint32_t prefix,
+                                                    unsigned int *__restrict__ hist)
+{
+    __shared__ unsigned int h[256];
+    const int tid = threadIdx.x;
+    h[tid] = 0;
+    __syncthreads();
+    const int64_t start = static_cast<int64_t>(blockIdx.x) * 256 * kCalItems;
+    if (start < n_cal) {
+        int s = find_stream(cal_off, n, start);
+        for (int j = 0; j < kCalItems; ++j) {
+            const int64_t ci = start + static_cast<int64_t>(j) * 256 + tid;
+            if (ci >= n_cal)
+                break;
+            while (cal_off[s + 1] <= ci)
+                ++s;
+            const uint32_t key = fkey(scores[woff[s] + (ci - cal_off[s])]);
+            const bool match = shift >= 24 ? true : ((key >> (shift + 8)) == prefix);
+            if (match)
+                atomicAdd(&h[(key >> shift) & 255u], 1u);
+        }
+    }
+    __syncthreads();
+    if (h[tid])
+        atomicAdd(&hist[tid], h[tid]);
+}
+
+__global__ __launch_bounds__(256) void k_calib_collect(const float *__restrict__ scores,
+                                                       const int64_t *__restrict__ woff,
+                                                       const int64_t *__restrict__ cal_off, int n,
+                                                       int64_t n_cal, uint32_t key_t,
+                                                       float *__restrict__ out,
+                                                       unsigned int *__restrict__ counter,
+                                                       unsigned int cap)
+{
+    const int tid = threadIdx.x;
+    const int64_t start = static_cast<int64_t>(blockIdx.x) * 256 * kCalItems;
+    if (start >= n_cal)
+        return;
+    int s = find_stream(cal_off, n, start);
+    for (int j = 0; j < kCalItems; ++j) {
+        const int64_t ci = start + static_cast<int64_t>(j) * 256 + tid;
+        if (ci >= n_cal)
+            break;
+        while (cal_off[s + 1] <= ci)
+            ++s;
+        const float v = scores[woff[s] + (ci - cal_off[s])];
+        if (fkey(v) > key_t) {
+            const unsigned int slot = atomicAdd(counter, 1u);
+            if (slot < cap)
+                out[slot] = v;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_ref_stats(const Geometry &g, const void *x, const int64_t *soff, int n,
+                            float *mean, float *std, hipStream_t st)
+{
+    if (n <= 0)
+        return hipSuccess;
+    if (g.dtype == ENOVA_F32)
+        hipLaunchKernelGGL(k_ref_stats<ENOVA_F32>, dim3(n), dim3(256), 0, st, x, soff, g.M,
+                           g.ref_frac, mean, std);
+    else
+        hipLaunchKernelGGL(k_ref_stats<ENOVA_BF16>, dim3(n), dim3(256), 0, st, x, soff, g.M,
+                           g.ref_frac, mean, std);
+    return hipGetLastError();
+}
+
+hipError_t launch_stream_scan(const Geometry &g, const int64_t *soff, const int64_t *woff, int n,
+                              int mode, int div, int64_t *out, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_stream_scan, dim3(1), dim3(1024), 0, st, soff, woff, n, mode, div, g.W,
+                       g.S, g.ref_frac, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_flag(const float *scores, int64_t n, float thr, uint8_t *flags, hipStream_t st)
+{
+    if (n <= 0)
+        return hipSuccess;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 65536)
+        blocks = 65536;
+    hipLaunchKernelGGL(k_flag, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, scores, n,
+                       thr, flags);
+    return hipGetLastError();
+}
+
+static unsigned cal_blocks(int64_t n_cal)
+{
+    return static_cast<unsigned>((n_cal + 256 * kCalItems - 1) / (256 * kCalItems));
+}
+
+hipError_t launch_calib_hist(const float *scores, const int64_t *woff, const int64_t *cal_off,
+                             int n, int64_t n_cal, int shift, uint32_t prefix, unsigned int *hist,
+                             hipStream_t st)
+{
+    if (n_cal <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_calib_hist, dim3(cal_blocks(n_cal)), dim3(256), 0, st, scores, woff,
+                       cal_off, n, n_cal, shift, prefix, hist);
+    return hipGetLastError();
+}
+
+hipError_t launch_calib_collect(const float *scores, const int64_t *woff, const int64_t *cal_off,
+                                int n, int64_t n_cal, uint32_t key, float *out, unsigned int cap,
+                                unsigned int *counter, hipStream_t st)
+{
+    if (n_cal <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_calib_collect, dim3(cal_blocks(n_cal)), dim3(256), 0, st, scores, woff,
+                       cal_off, n, n_cal, key, out, counter, cap);
+    return hipGetLastError();
+}
+
+}  // namespace enova

@@ -1,0 +1,475 @@
+// Matrix-core (MFMA) scoring kernel for gfx950.
+//
+// A tile is Nb consecutive windows of one stream. Its Nb+Q-1 super-rows are read from HBM
+// once (coalesced 16-byte loads), normalised with the stream's reference statistics and
+// written to LDS (rounded to bf16 for the bf16 workload); then the encoder's first layer --
+// the dense contraction of Section IV-B's VAE, 2*H*D flops per window -- runs as
+//
+//     C[h][n] = sum_k W1[h][k] * V[n][k]      (A = W1 from L2, B = windows from LDS)
+//
+// on v_mfma_f32_32x32x2_f32 (fp32) or v_mfma_f32_32x32x16_bf16 (bf16 operands, fp32
+// accumulation). Window n's row of V is never materialised: its chunk kappa = q*CPR + c is
+// chunk c of LDS super-row (n + q), so one staged element feeds up to Q windows.
+//
+// The accumulator layout of a 32x32 MFMA block (lane l, register r holds row
+// 8*(r/4) + 4*(l/32) + r%4 and column l%32) is exactly the B-operand layout a following
+// 32x32x2 fp32 MFMA needs when its reduction index is permuted the same way, so the rest of
+// the detector chains on the matrix cores without leaving registers:
+//   hidden  h  = act(C + b1)
+//   heads   [mu; logvar] = Wh h + bh          (32 x Hp, Wh pre-permuted on the host)
+//   score   1/2 sum_l (mu_l^2 + e^lv_l - 1 - lv_l)       (lane-pair reduction)
+//   decoder hd = act(Wd1 mu + bd1),  mean(m') = (u . hd + sum bd2) / D
+//   md      mean(v) - mean(m'),  mean(v) from per-super-row sums kept in LDS.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace enova {
+
+namespace {
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+struct MfmaShape {
+    int M, S, W, Mp, Q, CPR, CPRP, KC, act;
+    int tail_rows;   // steps of the window's last super-row that belong to the window
+    float inv_d;
+};
+
+template <int DT>
+__device__ __forceinline__ float load_x(const void *x, int64_t idx)
+{
+    if constexpr (DT == ENOVA_F32) {
+        return static_cast<const float *>(x)[idx];
+    } else {
+        uint32_t b = static_cast<const uint16_t *>(x)[idx];
+        return __uint_as_float(b << 16);
+    }
+}
+
+__device__ __forceinline__ float act_fn(float a, int act)
+{
+    if (act == ENOVA_TANH)
+        return tanhf(a);
+    return a < 0.0f ? 0.0f : a;   // ReLU; a NaN passes through
+}
+
+// e^u - 1 - u without cancellation near 0: Taylor series through u^8 for |u| < 0.5.
+__device__ __forceinline__ float kl_g(float u)
+{
+    if (fabsf(u) < 0.5f) {
+        float p = 1.0f / 40320.0f;
+        p = p * u + 1.0f / 5040.0f;
+        p = p * u + 1.0f / 720.0f;
+        p = p * u + 1.0f / 120.0f;
+        p = p * u + 1.0f / 24.0f;
+        p = p * u + 1.0f / 6.0f;
+        p = p * u + 0.5f;
+        return (u * u) * p;
+    }
+    return expm1f(u) - u;
+}
+
+__device__ __forceinline__ int find_stream(const int64_t *off, int n, int64_t w)
+{
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= w)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
+{
+    const __bf16 ha = static_cast<__bf16>(a);
+    const __bf16 hb = static_cast<__bf16>(b);
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ha)) |
+           (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, hb)) << 16);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// Row of the accumulator register r for lane half g inside a 32x32 block.
+__device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+template <int DT, int HB, int NBW>
+__global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShape g)
+{
+    constexpr int NB = kWaves * NBW * 32;         // windows per tile
+    constexpr int EPC = DT == ENOVA_F32 ? 4 : 8;  // elements per 16-byte chunk
+    extern __shared__ uint4 lds[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int half = lane >> 5;
+
+    // ---- tile -> (stream, first window)
+    const int64_t b = blockIdx.x;
+    const int64_t n_tiles = p.tile_off[p.n_streams];
+    if (b >= n_tiles)
+        return;
+    const int s = find_stream(p.tile_off, p.n_streams, b);
+    const int64_t k0 = (b - p.tile_off[s]) * NB;
+    const int64_t ns = p.woff[s + 1] - p.woff[s];
+    const int nv = static_cast<int>(ns - k0 < NB ? ns - k0 : NB);
+    const int64_t srow = p.soff[s];
+    const int64_t T = p.soff[s + 1] - srow;
+
+    const int Q = g.Q, CPR = g.CPR, CPRP = g.CPRP, M = g.M, Mp = g.Mp, S = g.S;
+    const int nrows = nv + Q;                      // staged super-rows (one spare)
+    uint4 *seg = lds;
+    float *rs = reinterpret_cast<float *>(seg + static_cast<size_t>(NB + Q) * CPRP);
+    float *ps = rs + (NB + Q);
+    float *smean = ps + (NB + Q);
+    float *srinv = smean + Mp;
+
+    for (int m = tid; m < Mp; m += kThreads) {
+        if (m < M) {
+            smean[m] = p.mean[static_cast<int64_t>(s) * M + m];
+            srinv[m] = 1.0f / p.std[static_cast<int64_t>(s) * M + m];
+        } else {
+            smean[m] = 0.0f;
+            srinv[m] = 0.0f;
+        }
+    }
+    __syncthreads();
+
+    // ---- stage: super-row r of the tile covers stream steps (k0 + r)*S .. +S-1
+    const int64_t step0 = k0 * S;
+    const int64_t avail = T - step0;               // stream steps available from step0
+    const bool linear = (Mp == M) && (((srow + step0) * M) % EPC == 0);
+    const int64_t ebase = (srow + step0) * M;      // element index of super-row 0
+    const int64_t eend = (srow + T) * M;           // one past the stream's last element
+    for (int idx = tid; idx < nrows * CPR; idx += kThreads) {
+        const int r = idx / CPR;
+        const int c = idx - r * CPR;
+        float v[EPC];
+        if (linear && ebase + static_cast<int64_t>(idx + 1) * EPC <= eend) {
+            const int64_t e0 = ebase + static_cast<int64_t>(idx) * EPC;
+            if constexpr (DT == ENOVA_F32) {
+                const float4 raw = *reinterpret_cast<const float4 *>(static_cast<const float *>(p.x) + e0);
+                v[0] = raw.x;
+                v[1] = raw.y;
+                v[2] = raw.z;
+                v[3] = raw.w;
+            } else {
+                const uint4 raw = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.x) + e0);
+                v[0] = bf16_lo(raw.x);
+                v[1] = bf16_hi(raw.x);
+                v[2] = bf16_lo(raw.y);
+                v[3] = bf16_hi(raw.y);
+                v[4] = bf16_lo(raw.z);
+                v[5] = bf16_hi(raw.z);
+                v[6] = bf16_lo(raw.w);
+                v[7] = bf16_hi(raw.w);
+            }
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const int m = (c * EPC + e) % M;
+                v[e] = (v[e] - smean[m]) * srinv[m];
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const int jj = c * EPC + e;
+                const int tt = jj / Mp;
+                const int m = jj - tt * Mp;
+                const int64_t step = static_cast<int64_t>(r) * S + tt;
+                float val = 0.0f;
+                if (m < M && step < avail)
+                    val = (load_x<DT>(p.x, (srow + step0 + step) * M + m) - smean[m]) * srinv[m];
+                v[e] = val;
+            }
+        }
+        uint4 out;
+        if constexpr (DT == ENOVA_F32) {
+            out.x = __float_as_uint(v[0]);
+            out.y = __float_as_uint(v[1]);
+            out.z = __float_as_uint(v[2]);
+            out.w = __float_as_uint(v[3]);
+        } else {
+            out.x = pack_bf16x2(v[0], v[1]);
+            out.y = pack_bf16x2(v[2], v[3]);
+            out.z = pack_bf16x2(v[4], v[5]);
+            out.w = pack_bf16x2(v[6], v[7]);
+        }
+        seg[r * CPRP + c] = out;
+    }
+    __syncthreads();
+
+    // ---- per-super-row sums of the staged values (full row, and the window's tail part)
+    const int tail_elems = g.tail_rows * Mp;
+    for (int r = tid; r < nrows; r += kThreads) {
+        float full = 0.0f, part = 0.0f;
+        for (int c = 0; c < CPR; ++c) {
+            const uint4 q4 = seg[r * CPRP + c];
+            float e[EPC];
+            if constexpr (DT == ENOVA_F32) {
+                e[0] = __uint_as_float(q4.x);
+                e[1] = __uint_as_float(q4.y);
+                e[2] = __uint_as_float(q4.z);
+                e[3] = __uint_as_float(q4.w);
+            } else {
+                e[0] = bf16_lo(q4.x);
+                e[1] = bf16_hi(q4.x);
+                e[2] = bf16_lo(q4.y);
+                e[3] = bf16_hi(q4.y);
+                e[4] = bf16_lo(q4.z);
+                e[5] = bf16_hi(q4.z);
+                e[6] = bf16_lo(q4.w);
+                e[7] = bf16_hi(q4.w);
+            }
+#pragma unroll
+            for (int k = 0; k < EPC; ++k) {
+                full += e[k];
+                if (c * EPC + k < tail_elems)
+                    part += e[k];
+            }
+        }
+        rs[r] = full;
+        ps[r] = part;
+    }
+
+    // ---- main contraction
+    int rb[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
+        rb[nb] = n < nv ? n : nv - 1;        // idle columns re-read a valid window
+    }
+    v16f acc[HB][NBW];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[hb][nb][r] = 0.0f;
+
+    const bool wave_active = wave * NBW * 32 < nv;
+    const int nsteps = g.KC / 2;
+    const uint4 *ap = p.w1p + lane;
+    uint4 a_cur[HB];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb)
+        a_cur[hb] = ap[hb * 64];
+    int q = 0, c = half;                       // chunk kappa = 2*i + half
+    while (c >= CPR) {
+        c -= CPR;
+        ++q;
+    }
+    __syncthreads();
+    if (wave_active) {
+        for (int i = 0; i < nsteps; ++i) {
+            uint4 a_nxt[HB];
+            if (i + 1 < nsteps) {
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb)
+                    a_nxt[hb] = ap[((i + 1) * HB + hb) * 64];
+            }
+            uint4 bf[NBW];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                bf[nb] = seg[(rb[nb] + q) * CPRP + c];
+            if constexpr (DT == ENOVA_F32) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+#pragma unroll
+                    for (int hb = 0; hb < HB; ++hb) {
+                        const float av = __uint_as_float(e == 0 ? a_cur[hb].x : e == 1 ? a_cur[hb].y
+                                                        : e == 2 ? a_cur[hb].z : a_cur[hb].w);
+#pragma unroll
+                        for (int nb = 0; nb < NBW; ++nb) {
+                            const float bv = __uint_as_float(e == 0 ? bf[nb].x : e == 1 ? bf[nb].y
+                                                            : e == 2 ? bf[nb].z : bf[nb].w);
+                            acc[hb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[hb][nb], 0, 0, 0);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb) {
+                    const v8bf av = __builtin_bit_cast(v8bf, a_cur[hb]);
+#pragma unroll
+                    for (int nb = 0; nb < NBW; ++nb)
+                        acc[hb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            av, __builtin_bit_cast(v8bf, bf[nb]), acc[hb][nb], 0, 0, 0);
+                }
+            }
+            if (i + 1 < nsteps) {
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb)
+                    a_cur[hb] = a_nxt[hb];
+            }
+            c += 2;
+            while (c >= CPR) {
+                c -= CPR;
+                ++q;
+            }
+        }
+    }
+    if (!wave_active)
+        return;
+
+    // ---- epilogue: hidden activations in place
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const float bias = p.b1[hb * 32 + crow(r, half)];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                acc[hb][nb][r] = act_fn(acc[hb][nb][r] + bias, g.act);
+        }
+    }
+
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        // posterior heads: rows 0..15 mean, 16..31 log-variance
+        v16f z;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            z[r] = 0.0f;
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                z = __builtin_amdgcn_mfma_f32_32x32x2f32(p.whp[(hb * 16 + r) * 64 + lane],
+                                                         acc[hb][nb][r], z, 0, 0, 0);
+        }
+        float kl = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            z[r] += p.bh[crow(r, half)];
+            if (r < 8)
+                kl += z[r] * z[r];
+            else
+                kl += kl_g(z[r]);
+        }
+        kl += __shfl_xor(kl, 32);
+
+        // decoder hidden layer at z = mu, dotted with the column sums of Wd2
+        float dot = 0.0f;
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb) {
+            v16f d;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                d[r] = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 8; ++r)
+                d = __builtin_amdgcn_mfma_f32_32x32x2f32(p.wd1p[(hb * 8 + r) * 64 + lane], z[r], d, 0, 0, 0);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int h = hb * 32 + crow(r, half);
+                dot += p.u[h] * act_fn(d[r] + p.bd1[h], g.act);
+            }
+        }
+        dot += __shfl_xor(dot, 32);
+
+        // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
+        const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
+        float vsum = 0.0f;
+        for (int qq = half; qq < Q - 1; qq += 2)
+            vsum += rs[rb[nb] + qq];
+        if (((Q - 1) & 1) == half)
+            vsum += ps[rb[nb] + Q - 1];
+        vsum += __shfl_xor(vsum, 32);
+
+        if (half == 0 && n < nv) {
+            const int64_t w = p.woff[s] + k0 + n;
+            const float sc = 0.5f * kl;
+            p.scores[w] = sc;
+            if (p.md)
+                p.md[w] = vsum * g.inv_d - (dot + p.sum_bd2) * g.inv_d;
+            if (p.write_flags)
+                p.flags[w] = sc > p.threshold ? 1 : 0;
+        }
+    }
+}
+
+template <int DT, int HB, int NBW>
+hipError_t launch_t(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st)
+{
+    MfmaShape sh;
+    sh.M = g.M;
+    sh.S = g.S;
+    sh.W = g.W;
+    sh.Mp = g.Mp;
+    sh.Q = g.Q;
+    sh.CPR = g.CPR;
+    sh.CPRP = g.CPRP;
+    sh.KC = g.KC;
+    sh.act = g.act;
+    sh.tail_rows = g.W - (g.Q - 1) * g.S;
+    sh.inv_d = 1.0f / static_cast<float>(g.D);
+    auto kern = k_score_mfma<DT, HB, NBW>;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(grid)), dim3(kThreads), g.lds_bytes, st, p, sh);
+    return hipGetLastError();
+}
+
+template <int DT, int HB, int NBW>
+hipError_t prepare_t()
+{
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(k_score_mfma<DT, HB, NBW>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               static_cast<int>(kLdsLimit));
+}
+
+}  // namespace
+
+// Allow the chosen instantiation the full 160 KiB of LDS.
+hipError_t prepare_score_mfma(const Geometry &g)
+{
+    const bool f = g.dtype == ENOVA_F32;
+    switch (g.HB) {
+    case 1: return f ? prepare_t<ENOVA_F32, 1, 4>() : prepare_t<ENOVA_BF16, 1, 4>();
+    case 2: return f ? prepare_t<ENOVA_F32, 2, 4>() : prepare_t<ENOVA_BF16, 2, 4>();
+    case 4: return f ? prepare_t<ENOVA_F32, 4, 2>() : prepare_t<ENOVA_BF16, 4, 2>();
+    case 8: return f ? prepare_t<ENOVA_F32, 8, 1>() : prepare_t<ENOVA_BF16, 8, 1>();
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st)
+{
+    if (grid <= 0)
+        return hipSuccess;
+    if (g.dtype == ENOVA_F32) {
+        switch (g.HB) {
+        case 1: return launch_t<ENOVA_F32, 1, 4>(g, p, grid, st);
+        case 2: return launch_t<ENOVA_F32, 2, 4>(g, p, grid, st);
+        case 4: return launch_t<ENOVA_F32, 4, 2>(g, p, grid, st);
+        case 8: return launch_t<ENOVA_F32, 8, 1>(g, p, grid, st);
+        default: return hipErrorInvalidValue;
+        }
+    }
+    switch (g.HB) {
+    case 1: return launch_t<ENOVA_BF16, 1, 4>(g, p, grid, st);
+    case 2: return launch_t<ENOVA_BF16, 2, 4>(g, p, grid, st);
+    case 4: return launch_t<ENOVA_BF16, 4, 2>(g, p, grid, st);
+    case 8: return launch_t<ENOVA_BF16, 8, 1>(g, p, grid, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+// NBW (32-window blocks per wave) that goes with each hidden-block count HB.
+int mfma_nbw_for(int hb)
+{
+    switch (hb) {
+    case 1: return 4;
+    case 2: return 4;
+    case 4: return 2;
+    case 8: return 1;
+    default: return 0;
+    }
+}
+
+}  // namespace enova

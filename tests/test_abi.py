@@ -1,0 +1,98 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every declared entry
+point, and rejects invalid arguments on the host before touching a device."""
+import ctypes
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2407_09486_amd import binding
+from paper_2407_09486_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _ensure_built():
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2407_09486_amd import build
+        build.build_library()
+
+
+def declared_functions():
+    names = []
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b(enova_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    _ensure_built()
+    L = ctypes.CDLL(binding.LIB_PATH)
+    names = declared_functions()
+    assert len(names) >= 12, names
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in include/ but not exported"
+    assert set(names) == set(binding.EXPORTS)
+
+
+def test_status_strings():
+    _ensure_built()
+    L = binding.lib()
+    for s in range(7):
+        assert L.enova_status_str(s)
+    assert L.enova_status_str(99) == b"unknown status"
+
+
+def _init_status(**over):
+    cfg = dict(metrics=8, window=32, stride=1, hidden=32, latent=16)
+    cfg.update(over)
+    c = binding.make_config(**{k: v for k, v in cfg.items() if k in ("metrics", "window", "stride", "hidden", "latent")})
+    for k in ("dtype", "act", "kernel", "ref_frac"):
+        if k in over:
+            setattr(c, k, over[k])
+    W = wl.make_weights(wl.CONFIGS["c1"])
+    w = binding.weights_for_library(W)
+    keep = [np.ascontiguousarray(v) for v in w.values()]
+    ws = binding.enova_detect_weights(**{k: ctypes.c_void_p(v.ctypes.data) for k, v in zip(w.keys(), keep)})
+    h = ctypes.c_void_p()
+    st = binding.lib().enova_detect_init(ctypes.byref(c), ctypes.byref(ws), ctypes.byref(h))
+    return st, h.value
+
+
+@pytest.mark.parametrize("over", [dict(metrics=0), dict(window=0), dict(stride=-1), dict(hidden=0),
+                                  dict(latent=0), dict(latent=65), dict(dtype=7), dict(act=3),
+                                  dict(kernel=9), dict(ref_frac=0.0), dict(ref_frac=1.5),
+                                  dict(window=4096, metrics=32)])
+def test_init_rejects_bad_config(over):
+    _ensure_built()
+    st, h = _init_status(**over)
+    assert st == binding.ENOVA_EINVAL and not h
+    assert binding.lib().enova_last_error()
+
+
+def test_null_arguments_are_rejected():
+    _ensure_built()
+    L = binding.lib()
+    assert L.enova_detect_init(None, None, None) == binding.ENOVA_EINVAL
+    h = ctypes.c_void_p()
+    c = binding.make_config(8, 32, 1, 32)
+    assert L.enova_detect_init(ctypes.byref(c), None, ctypes.byref(h)) == binding.ENOVA_EINVAL
+    so = np.array([0, 10], np.int64)
+    out = np.zeros(2, np.int64)
+    assert L.enova_detect_window_offsets(None, so.ctypes.data, 1, out.ctypes.data) == binding.ENOVA_EINVAL
+    assert L.enova_detect_score(None, None, None, None, 0, 0, None, None, 0.0, None, None, None,
+                                None) == binding.ENOVA_EINVAL
+    assert L.enova_detect_destroy(None) == binding.ENOVA_OK
+    thr = ctypes.c_float()
+    assert L.enova_detect_threshold(None, None, None, None, 1, 1, 0.98, 1e-3, ctypes.byref(thr), None,
+                                    None, None) == binding.ENOVA_EINVAL
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    with pytest.raises(ValueError):
+        binding._dptr(torch.zeros(3))
