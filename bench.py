@@ -1,0 +1,215 @@
+"""Throughput of the batched sliding-window anomaly scorer on one MI355X.
+
+One step is one pass of the whole detection path over one batch of synthetic streams
+already resident in HBM: window enumeration (host helper + offsets upload), reference
+statistics, scoring of every window (normalise -> encoder -> KL score -> decoder MD),
+the peaks-over-threshold threshold over the calibration windows, and the flags of every
+window. Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--config c5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "metric-windows scored/sec at 1 MI355X; % of HBM/MFMA roofline"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}     # dense MFMA peaks of the MI355X datasheet
+HBM_PEAK_GBS = 8000.0
+# CPU-baseline sample per config: (number of leading streams, windows per stream)
+CPU_SAMPLE = {"c1": (1, None), "c2": (2, 8192), "c3": (8, 1024), "c4": (16, 128), "c5": (24, 16384)}
+KERNEL_SRC = os.path.join(ROOT, "paper_2407_09486_amd", "csrc", "k_score_mfma.hip")
+
+
+def flops_per_window(cfg) -> int:
+    """Algorithmic flops of one window: encoder layer 2HD, posterior heads 4LH, decoder 2LH + 2H."""
+    H, L, D = cfg.hidden, cfg.latent, cfg.d
+    return 2 * H * D + 4 * L * H + 2 * L * H + 2 * H
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("k_score_mfma.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2407_09486_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(config_name: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it still
+    describes the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"score_mfma_{config_name}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.strip().split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, weights):
+    import numpy as np
+
+    import oracle
+    from paper_2407_09486_amd import workloads as wl
+    n_streams, max_w = CPU_SAMPLE.get(cfg.name, (4, 4096))
+    n_streams = min(n_streams, cfg.n_streams)
+    w = wl.generate(cfg, streams=np.arange(n_streams))
+    x = w.values_f64()
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    sc, md, info = oracle.score(x, w.stream_offsets, window=cfg.window, stride=cfg.stride,
+                                weights=weights.as_f64(), act=cfg.act, ref_frac=cfg.ref_frac,
+                                bf16=cfg.dtype == "bf16", max_windows=max_w, threads=cores,
+                                return_stats=True)
+    dt = time.perf_counter() - t0
+    n = int(np.isfinite(sc).sum())
+    sample = (f"{cfg.name}: streams 0..{n_streams - 1}, "
+              + (f"first {max_w} windows each" if max_w else "all windows")
+              + f" ({n} windows, {dt:.1f} s, fp64 oracle incl. reference statistics)")
+    return {"value": n / dt, "unit": "windows/s", "cores": int(info["threads"]), "kind": "oracle",
+            "sample": sample}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c5")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-gib", type=float, default=0.0,
+                    help="also run a plain device copy of this size (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the detector shards by stream with no collectives, "
+              "and this build measures the single-GPU kernel (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2407_09486_amd import binding
+    from paper_2407_09486_amd import workloads as wl
+
+    cfg = wl.CONFIGS[args.config]
+    t_gen = time.perf_counter()
+    w = wl.generate(cfg)
+    weights = wl.make_weights(cfg)
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] {cfg.name}: generated {w.n_streams} streams, {int(w.stream_offsets[-1])} steps "
+          f"in {t_gen:.1f} s", file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    x = torch.from_numpy(w.x_bits.view(np.int16) if cfg.dtype == "bf16" else w.x).to(dev)
+    so = torch.from_numpy(w.stream_offsets).to(dev)
+    so_h = w.stream_offsets
+    del w
+    det = binding.Detector(cfg.metrics, cfg.window, cfg.stride, cfg.hidden,
+                           binding.weights_for_library(weights, cfg.dtype), latent=cfg.latent,
+                           dtype=cfg.dtype, act=cfg.act, ref_frac=cfg.ref_frac)
+    binding.enova_detect_set_timing(det.handle, True)
+    woff_h = det.window_offsets(so_h)
+    N = int(woff_h[-1])
+    woff_pin = torch.from_numpy(woff_h).pin_memory()
+    wo = torch.empty_like(woff_pin, device=dev)
+    scores = torch.empty(N, dtype=torch.float32, device=dev)
+    md = torch.empty(N, dtype=torch.float32, device=dev)
+    flags = torch.empty(N, dtype=torch.uint8, device=dev)
+    n_streams = len(so_h) - 1
+    stream = torch.cuda.current_stream()
+    kernel_ms = []
+    stats_ms = []
+    thr_hist = []
+
+    def step(record):
+        wh = det.window_offsets(so_h)                                   # window enumeration
+        woff_pin.numpy()[:] = wh
+        wo.copy_(woff_pin, non_blocking=True)
+        binding.enova_detect_score(det.handle, x, so, wo, n_streams, N, None, None, math.nan,
+                                   scores, md, None, stream)            # stats + score + md
+        if record:
+            a, b = binding.enova_detect_kernel_times(det.handle)
+            kernel_ms.append(a)
+            stats_ms.append(b)
+        thr, _ = binding.enova_detect_threshold(det.handle, scores, so, wo, n_streams, N, 0.98, 1e-3,
+                                                flags, stream)          # POT threshold + flags
+        thr_hist.append(thr)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(True)
+        print(f"[bench] step {i + 1}/{args.steps} kernel {kernel_ms[-1]:.2f} ms", file=sys.stderr,
+              flush=True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    value = N * args.steps / (wall if wall > 0 else float("nan"))
+    value_ev = N / (ms_step / 1e3)
+
+    if args.copy_probe_gib > 0:
+        nbytes = int(args.copy_probe_gib * (1 << 30))
+        a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    k_ms = float(np.mean(kernel_ms))
+    fpw = flops_per_window(cfg)
+    achieved = fpw * N / (k_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    traffic = load_traffic(cfg.name)
+    roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": traffic,
+            "kernel": "k_score_mfma", "kernel_ms": round(k_ms, 4),
+            "flops_per_window": fpw, "windows_per_launch": N,
+            "stats_kernel_ms": round(float(np.mean(stats_ms)), 4)}
+    out = {
+        "metric": METRIC, "value": round(value_ev, 1), "unit": "windows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic (seeded generators standing in for the paper's industrial series)",
+        "config": {"workload": f"{cfg.name}: {cfg.description}", "streams": n_streams, "windows": N,
+                   "metrics": cfg.metrics, "window": cfg.window, "stride": cfg.stride,
+                   "hidden": cfg.hidden, "latent": cfg.latent, "act": cfg.act,
+                   "data_seed": cfg.data_seed, "weight_seed": cfg.weight_seed,
+                   "wall_windows_per_s": round(value, 1), "threshold": thr_hist[-1]},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, weights)
+    det.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

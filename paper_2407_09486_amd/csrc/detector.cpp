@@ -87,9 +87,13 @@ struct enova_detector_s {
     size_t tiles_cap = 0;         // entries
     int64_t *cal = nullptr;
     size_t cal_cap = 0;
-    unsigned int *hist = nullptr; // 256 bins + 1 counter
-    float *peaks = nullptr;
+    unsigned int *hist = nullptr; // 256 radix bins
+    double *peaks = nullptr;      // excesses over the level quantile, calibration order
     size_t peaks_cap = 0;
+    int64_t *blk = nullptr;       // per-block peak counts, then their exclusive scan
+    size_t blk_cap = 0;
+    double *gx = nullptr;         // evaluation points of the GPD likelihood sums, then the sums
+    size_t gx_cap = 0;
     // timing
     bool timing = false;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
@@ -181,7 +185,8 @@ void free_detector(enova_detector d)
 {
     if (!d)
         return;
-    void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->cal, d->hist, d->peaks};
+    void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->cal, d->hist, d->peaks, d->blk,
+                    d->gx};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
@@ -214,6 +219,36 @@ enova_status check_config(const enova_detect_config *c)
         return fail(ENOVA_EINVAL, "ref_frac must be in (0, 1]");
     return ENOVA_OK;
 }
+
+// Likelihood sums of the GPD fit, evaluated on the device over the compacted excesses.
+struct DeviceGpdSums : GpdSums {
+    enova_detector d;
+    const double *y;
+    int64_t n;
+    hipStream_t st;
+    enova_status status = ENOVA_OK;
+    DeviceGpdSums(enova_detector d_, const double *y_, int64_t n_, hipStream_t s_)
+        : d(d_), y(y_), n(n_), st(s_) {}
+    bool eval(const double *xs, int nx, double *su, double *sv) override
+    {
+        if (nx <= 0)
+            return true;
+        status = ensure(&d->gx, &d->gx_cap, 3 * static_cast<size_t>(nx));
+        if (status != ENOVA_OK)
+            return false;
+        double *dx = d->gx, *dsu = d->gx + nx, *dsv = d->gx + 2 * static_cast<size_t>(nx);
+        hipError_t e;
+        if ((e = hipMemcpyAsync(dx, xs, sizeof(double) * nx, hipMemcpyHostToDevice, st)) != hipSuccess ||
+            (e = launch_gpd_sums(y, n, dx, nx, dsu, dsv, st)) != hipSuccess ||
+            (e = hipMemcpyAsync(su, dsu, sizeof(double) * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = hipMemcpyAsync(sv, dsv, sizeof(double) * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = hipStreamSynchronize(st)) != hipSuccess) {
+            status = hip_fail(e, "GPD likelihood sums");
+            return false;
+        }
+        return true;
+    }
+};
 
 }  // namespace
 
@@ -422,7 +457,7 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
         }
     }
     if (st == ENOVA_OK) {
-        hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 260 * sizeof(unsigned int));
+        hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 256 * sizeof(unsigned int));
         if (e != hipSuccess)
             st = fail(ENOVA_ENOMEM, "hipMalloc(hist)");
     }
@@ -672,40 +707,58 @@ enova_status enova_detect_threshold(enova_detector det, const float *scores, con
     std::memcpy(&t_f, &bits, 4);
     if (!std::isfinite(t_f))
         return fail(ENOVA_ENUMERIC, "non-finite calibration score at the level quantile");
-    std::vector<double> ex;
+    // stable compaction of the excesses y = score - t of every calibration score above t
+    PotResult r{};
+    const double t_d = static_cast<double>(t_f);
     if (n_greater > 0) {
-        if (n_greater > 0x7fffffffLL)
-            return fail(ENOVA_EUNSUPPORTED, "too many peaks");
-        st = ensure(&det->peaks, &det->peaks_cap, static_cast<size_t>(n_greater));
-        if (st != ENOVA_OK)
+        const int64_t nblk = calib_blocks(n_cal);
+        if ((st = ensure(&det->peaks, &det->peaks_cap, static_cast<size_t>(n_greater))) != ENOVA_OK ||
+            (st = ensure(&det->blk, &det->blk_cap, 2 * static_cast<size_t>(nblk) + 2)) != ENOVA_OK)
             return st;
-        if ((e = hipMemsetAsync(det->hist + 256, 0, sizeof(unsigned int), stream)) != hipSuccess)
-            return hip_fail(e, "hipMemsetAsync");
-        e = launch_calib_collect(scores, woff, det->cal, n, n_cal, key_t, det->peaks,
-                                 static_cast<unsigned int>(n_greater), det->hist + 256, stream);
-        if (e != hipSuccess)
-            return hip_fail(e, "peak collection kernel");
-        std::vector<float> pk(static_cast<size_t>(n_greater));
-        unsigned int cnt = 0;
-        if ((e = hipMemcpyAsync(pk.data(), det->peaks, pk.size() * sizeof(float),
-                                hipMemcpyDeviceToHost, stream)) != hipSuccess ||
-            (e = hipMemcpyAsync(&cnt, det->hist + 256, sizeof(cnt), hipMemcpyDeviceToHost, stream)) !=
+        int64_t *cnt = det->blk, *off = det->blk + nblk + 1;
+        if ((e = launch_calib_count(scores, woff, det->cal, n, n_cal, key_t, cnt, stream)) != hipSuccess ||
+            (e = launch_scan_i64(cnt, nblk, off, stream)) != hipSuccess ||
+            (e = launch_calib_compact(scores, woff, det->cal, n, n_cal, key_t, t_d, off, det->peaks,
+                                      n_greater, stream)) != hipSuccess)
+            return hip_fail(e, "peak compaction");
+        int64_t total = 0;
+        if ((e = hipMemcpyAsync(&total, off + nblk, sizeof(int64_t), hipMemcpyDeviceToHost, stream)) !=
                 hipSuccess ||
             (e = hipStreamSynchronize(stream)) != hipSuccess)
-            return hip_fail(e, "peak copy");
-        if (static_cast<int64_t>(cnt) != n_greater)
-            return fail(ENOVA_EHIP, "peak count mismatch (%u vs %lld)", cnt,
+            return hip_fail(e, "peak count");
+        if (total != n_greater)
+            return fail(ENOVA_EHIP, "peak count mismatch (%lld vs %lld)", static_cast<long long>(total),
                         static_cast<long long>(n_greater));
-        ex.resize(pk.size());
-        for (size_t i = 0; i < pk.size(); ++i) {
-            if (!std::isfinite(pk[i]))
-                return fail(ENOVA_ENUMERIC, "non-finite calibration score");
-            ex[i] = static_cast<double>(pk[i]) - static_cast<double>(t_f);
-        }
-        std::sort(ex.begin(), ex.end());
     }
-    PotResult r = pot_from_peaks(static_cast<double>(t_f), n_cal, ex.data(),
-                                 static_cast<int64_t>(ex.size()), q);
+    if (n_greater >= 10) {
+        double ps[3];
+        if ((st = ensure(&det->gx, &det->gx_cap, 96)) != ENOVA_OK)
+            return st;
+        if ((e = launch_peak_stats(det->peaks, n_greater, det->gx, stream)) != hipSuccess ||
+            (e = hipMemcpyAsync(ps, det->gx, sizeof(ps), hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+            (e = hipStreamSynchronize(stream)) != hipSuccess)
+            return hip_fail(e, "peak statistics");
+        if (!std::isfinite(ps[0]) || !std::isfinite(ps[2]))
+            return fail(ENOVA_ENUMERIC, "non-finite calibration score");
+        DeviceGpdSums ev(det, det->peaks, n_greater, stream);
+        bool ok = false;
+        r = pot_mle(t_d, n_cal, n_greater, ps[0], ps[1], ps[2], q, ev, &ok);
+        if (!ok)
+            return ev.status != ENOVA_OK ? ev.status : fail(ENOVA_ENUMERIC, "GPD fit failed");
+    } else {
+        double ex[16];
+        if (n_greater > 0) {
+            if ((e = hipMemcpyAsync(ex, det->peaks, sizeof(double) * n_greater, hipMemcpyDeviceToHost,
+                                    stream)) != hipSuccess ||
+                (e = hipStreamSynchronize(stream)) != hipSuccess)
+                return hip_fail(e, "peak copy");
+            for (int64_t i = 0; i < n_greater; ++i)
+                if (!std::isfinite(ex[i]))
+                    return fail(ENOVA_ENUMERIC, "non-finite calibration score");
+            std::sort(ex, ex + n_greater);
+        }
+        r = pot_small(t_d, n_cal, ex, n_greater, q);
+    }
     const float thr = static_cast<float>(r.z);
     *out_threshold = thr;
     if (out_info) {

@@ -90,17 +90,38 @@ hipError_t launch_flag(const float *scores, int64_t n, float thr, uint8_t *flags
 hipError_t launch_calib_hist(const float *scores, const int64_t *woff, const int64_t *cal_off,
                              int n, int64_t n_cal, int shift, uint32_t prefix,
                              unsigned int *hist, hipStream_t st);
-// Copy every calibration score whose key exceeds `key` into out (order unspecified).
-hipError_t launch_calib_collect(const float *scores, const int64_t *woff, const int64_t *cal_off,
-                                int n, int64_t n_cal, uint32_t key, float *out, unsigned int cap,
-                                unsigned int *counter, hipStream_t st);
+// Stable compaction of the calibration scores whose key exceeds `key`:
+// calib_blocks() blocks; pass 1 counts per block, an exclusive scan gives each block's output
+// offset, pass 2 writes the excesses score - t in calibration order.
+int64_t calib_blocks(int64_t n_cal);
+hipError_t launch_calib_count(const float *scores, const int64_t *woff, const int64_t *cal_off, int n,
+                              int64_t n_cal, uint32_t key, int64_t *block_counts, hipStream_t st);
+hipError_t launch_calib_compact(const float *scores, const int64_t *woff, const int64_t *cal_off,
+                                int n, int64_t n_cal, uint32_t key, double t,
+                                const int64_t *block_off, double *y, int64_t cap, hipStream_t st);
+hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream_t st);
+// su[i] = sum_j 1/(1 + xs[i] y_j), sv[i] = sum_j log(1 + xs[i] y_j)   (fixed-order fp64 sums)
+hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, double *su,
+                           double *sv, hipStream_t st);
+// out = {sum y, min y, max y}
+hipError_t launch_peak_stats(const double *y, int64_t n, double *out, hipStream_t st);
 
-// Host GPD fit of the excesses (fp64). method: 0 threshold is t, 1 moments, 2 maximum likelihood.
+// Peaks-over-threshold fit (fp64). The likelihood sums over the excesses are supplied by an
+// evaluator, so they can run where the excesses live.
 struct PotResult {
     double z, t, gamma, sigma;
     int64_t n, n_peaks;
-    int method;
+    int method;   // 0: the threshold is t, 1: method of moments, 2: maximum likelihood
 };
-PotResult pot_from_peaks(double t, int64_t n, const double *excess, int64_t n_peaks, double q);
+struct GpdSums {
+    virtual ~GpdSums() = default;
+    // su[i] = sum 1/(1 + xs[i] y), sv[i] = sum log(1 + xs[i] y); false on failure
+    virtual bool eval(const double *xs, int nx, double *su, double *sv) = 0;
+};
+// Maximum likelihood (n_peaks >= 10) given the excesses' sum, minimum and maximum.
+PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin, double ymax,
+                  double q, GpdSums &sums, bool *ok);
+// Method of moments / degenerate cases (n_peaks < 10) from the excesses on the host.
+PotResult pot_small(double t, int64_t n, const double *excess, int64_t n_peaks, double q);
 
 }  // namespace enova

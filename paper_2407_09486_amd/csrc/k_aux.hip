@@ -211,18 +211,17 @@ __global__ __launch_bounds__(256) void k_calib_hist(const float *__restrict__ sc
         atomicAdd(&hist[tid], h[tid]);
 }
 
-__global__ __launch_bounds__(256) void k_calib_collect(const float *__restrict__ scores,
-                                                       const int64_t *__restrict__ woff,
-                                                       const int64_t *__restrict__ cal_off, int n,
-                                                       int64_t n_cal, uint32_t key_t,
-                                                       float *__restrict__ out,
-                                                       unsigned int *__restrict__ counter,
-                                                       unsigned int cap)
+// Peaks of the calibration set, pass 1: how many keys above key_t each block holds.
+__global__ __launch_bounds__(256) void k_calib_count(const float *__restrict__ scores,
+                                                     const int64_t *__restrict__ woff,
+                                                     const int64_t *__restrict__ cal_off, int n,
+                                                     int64_t n_cal, uint32_t key_t,
+                                                     int64_t *__restrict__ block_counts)
 {
+    __shared__ int wsum[4];
     const int tid = threadIdx.x;
     const int64_t start = static_cast<int64_t>(blockIdx.x) * 256 * kCalItems;
-    if (start >= n_cal)
-        return;
+    int cnt = 0;
     int s = find_stream(cal_off, n, start);
     for (int j = 0; j < kCalItems; ++j) {
         const int64_t ci = start + static_cast<int64_t>(j) * 256 + tid;
@@ -230,12 +229,162 @@ __global__ __launch_bounds__(256) void k_calib_collect(const float *__restrict__
             break;
         while (cal_off[s + 1] <= ci)
             ++s;
-        const float v = scores[woff[s] + (ci - cal_off[s])];
-        if (fkey(v) > key_t) {
-            const unsigned int slot = atomicAdd(counter, 1u);
-            if (slot < cap)
-                out[slot] = v;
+        cnt += fkey(scores[woff[s] + (ci - cal_off[s])]) > key_t ? 1 : 0;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        cnt += __shfl_xor(cnt, off);
+    if ((tid & 63) == 0)
+        wsum[tid >> 6] = cnt;
+    __syncthreads();
+    if (tid == 0)
+        block_counts[blockIdx.x] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+}
+
+// Pass 2: write the excesses y = score - t of the peaks in calibration order (stable).
+__global__ __launch_bounds__(256) void k_calib_compact(const float *__restrict__ scores,
+                                                       const int64_t *__restrict__ woff,
+                                                       const int64_t *__restrict__ cal_off, int n,
+                                                       int64_t n_cal, uint32_t key_t, double t,
+                                                       const int64_t *__restrict__ block_off,
+                                                       double *__restrict__ y, int64_t cap)
+{
+    __shared__ int wcnt[4];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int64_t start = static_cast<int64_t>(blockIdx.x) * 256 * kCalItems;
+    int64_t run = block_off[blockIdx.x];
+    int s = find_stream(cal_off, n, start);
+    for (int j = 0; j < kCalItems; ++j) {
+        const int64_t ci = start + static_cast<int64_t>(j) * 256 + tid;
+        float v = 0.0f;
+        bool hit = false;
+        if (ci < n_cal) {
+            while (cal_off[s + 1] <= ci)
+                ++s;
+            v = scores[woff[s] + (ci - cal_off[s])];
+            hit = fkey(v) > key_t;
         }
+        const uint64_t mask = __ballot(hit);
+        const int below = __popcll(mask & ((1ull << lane) - 1ull));
+        if (lane == 0)
+            wcnt[wave] = __popcll(mask);
+        __syncthreads();
+        int before = 0;
+        for (int k = 0; k < wave; ++k)
+            before += wcnt[k];
+        const int total = wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
+        const int64_t pos = run + before + below;
+        if (hit && pos < cap)
+            y[pos] = static_cast<double>(v) - t;
+        run += total;
+        __syncthreads();
+    }
+}
+
+// Exclusive scan of n int64 values by one block; out[n] receives the total.
+__global__ __launch_bounds__(1024) void k_scan_i64(const int64_t *__restrict__ in, int64_t n,
+                                                   int64_t *__restrict__ out)
+{
+    __shared__ int64_t part[1024];
+    const int tid = threadIdx.x;
+    const int64_t chunk = (n + 1023) / 1024;
+    const int64_t a = tid * chunk;
+    const int64_t b = a + chunk < n ? a + chunk : n;
+    int64_t local = 0;
+    for (int64_t i = a; i < b; ++i)
+        local += in[i];
+    part[tid] = local;
+    __syncthreads();
+    if (tid == 0) {
+        int64_t r = 0;
+        for (int i = 0; i < 1024; ++i) {
+            const int64_t v = part[i];
+            part[i] = r;
+            r += v;
+        }
+        out[n] = r;
+    }
+    __syncthreads();
+    int64_t r = part[tid];
+    for (int64_t i = a; i < b; ++i) {
+        out[i] = r;
+        r += in[i];
+    }
+}
+
+// Fixed-order block reduction of two fp64 partial sums.
+__device__ __forceinline__ void block_sum2(double &a, double &b, double *sa, double *sb)
+{
+    const int tid = threadIdx.x;
+    sa[tid] = a;
+    sb[tid] = b;
+    __syncthreads();
+    for (int w = 128; w >= 1; w >>= 1) {
+        if (tid < w) {
+            sa[tid] += sa[tid + w];
+            sb[tid] += sb[tid + w];
+        }
+        __syncthreads();
+    }
+    a = sa[0];
+    b = sb[0];
+}
+
+// Likelihood sums of the excesses at the points xs: block i returns
+// su[i] = sum 1/(1 + xs[i] y) and sv[i] = sum log(1 + xs[i] y).
+__global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, int64_t n,
+                                                  const double *__restrict__ xs,
+                                                  double *__restrict__ su, double *__restrict__ sv)
+{
+    __shared__ double sa[256];
+    __shared__ double sb[256];
+    const double x = xs[blockIdx.x];
+    double a = 0.0, b = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += 256) {
+        const double z = 1.0 + x * y[i];
+        a += 1.0 / z;
+        b += log(z);
+    }
+    block_sum2(a, b, sa, sb);
+    if (threadIdx.x == 0) {
+        su[blockIdx.x] = a;
+        sv[blockIdx.x] = b;
+    }
+}
+
+// Sum, minimum and maximum of the excesses (one block, fixed order).
+__global__ __launch_bounds__(256) void k_peak_stats(const double *__restrict__ y, int64_t n,
+                                                    double *__restrict__ out)
+{
+    __shared__ double sa[256];
+    __shared__ double sb[256];
+    __shared__ double sc[256];
+    const int tid = threadIdx.x;
+    double sum = 0.0, lo = INFINITY, hi = -INFINITY;
+    for (int64_t i = tid; i < n; i += 256) {
+        const double v = y[i];
+        sum += v;
+        lo = fmin(lo, v);
+        hi = fmax(hi, v);
+    }
+    sa[tid] = sum;
+    sb[tid] = lo;
+    sc[tid] = hi;
+    __syncthreads();
+    for (int w = 128; w >= 1; w >>= 1) {
+        if (tid < w) {
+            sa[tid] += sa[tid + w];
+            sb[tid] = fmin(sb[tid], sb[tid + w]);
+            sc[tid] = fmax(sc[tid], sc[tid + w]);
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        out[0] = sa[0];
+        out[1] = sb[0];
+        out[2] = sc[0];
     }
 }
 
@@ -291,14 +440,47 @@ hipError_t launch_calib_hist(const float *scores, const int64_t *woff, const int
     return hipGetLastError();
 }
 
-hipError_t launch_calib_collect(const float *scores, const int64_t *woff, const int64_t *cal_off,
-                                int n, int64_t n_cal, uint32_t key, float *out, unsigned int cap,
-                                unsigned int *counter, hipStream_t st)
+int64_t calib_blocks(int64_t n_cal) { return (n_cal + 256 * kCalItems - 1) / (256 * kCalItems); }
+
+hipError_t launch_calib_count(const float *scores, const int64_t *woff, const int64_t *cal_off, int n,
+                              int64_t n_cal, uint32_t key, int64_t *block_counts, hipStream_t st)
 {
     if (n_cal <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_calib_collect, dim3(cal_blocks(n_cal)), dim3(256), 0, st, scores, woff,
-                       cal_off, n, n_cal, key, out, counter, cap);
+    hipLaunchKernelGGL(k_calib_count, dim3(cal_blocks(n_cal)), dim3(256), 0, st, scores, woff,
+                       cal_off, n, n_cal, key, block_counts);
+    return hipGetLastError();
+}
+
+hipError_t launch_calib_compact(const float *scores, const int64_t *woff, const int64_t *cal_off,
+                                int n, int64_t n_cal, uint32_t key, double t,
+                                const int64_t *block_off, double *y, int64_t cap, hipStream_t st)
+{
+    if (n_cal <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_calib_compact, dim3(cal_blocks(n_cal)), dim3(256), 0, st, scores, woff,
+                       cal_off, n, n_cal, key, t, block_off, y, cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_scan_i64, dim3(1), dim3(1024), 0, st, in, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, double *su,
+                           double *sv, hipStream_t st)
+{
+    if (nx <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_gpd_sums, dim3(nx), dim3(256), 0, st, y, n, xs, su, sv);
+    return hipGetLastError();
+}
+
+hipError_t launch_peak_stats(const double *y, int64_t n, double *out, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_peak_stats, dim3(1), dim3(256), 0, st, y, n, out);
     return hipGetLastError();
 }
 

@@ -1,12 +1,17 @@
-// Host fp64 fit of the peaks-over-threshold tail (Section IV-B cites Siffer et al. 2017).
+// Peaks-over-threshold tail fit (Section IV-B cites Siffer et al. 2017), in fp64.
 //
 // The excesses Y over the level-quantile t follow a generalised Pareto distribution
 // GPD(gamma, sigma). Maximum likelihood uses Grimshaw's reduction: with x = gamma/sigma the
 // score equations collapse to one equation in x,
 //     w(x) = u(x) v(x) - 1 = 0,   u = mean 1/(1+xY),   v = 1 + mean log(1+xY),
 // whose roots give gamma = v(x) - 1 and sigma = gamma/x. Roots are bracketed on a fixed grid of
-// each admissible interval and refined by bisection; the exponential tail (gamma = 0,
-// sigma = mean Y) is always a candidate, and the candidate of largest log-likelihood wins.
+// each admissible interval, (-1/Y_max, 0) and (0, 2 (mean - min) / min^2), and refined by
+// k-section (63 interior points per round, all brackets evaluated in one batch) until the
+// bracket cannot shrink in fp64. The exponential tail (gamma = 0, sigma = mean Y) is always a
+// candidate, and the candidate of largest log-likelihood wins (ties: smaller |gamma|).
+//
+// The sums over the (possibly millions of) excesses come from a GpdSums evaluator; the
+// library's evaluator runs them on the device where the excesses were compacted.
 #include <cmath>
 #include <cstdint>
 #include <limits>
@@ -18,127 +23,29 @@ namespace enova {
 
 namespace {
 
-constexpr int kGrid = 512;
-constexpr int kBisect = 200;
+constexpr int kGrid = 512;       // grid points per admissible interval
+constexpr int kInterior = 63;    // k-section points per bracket and round
+constexpr int kRounds = 40;
 
-struct Excess {
-    const double *y;
-    int64_t n;
-
-    double w(double x) const
-    {
-        double su = 0.0, sv = 0.0;
-        for (int64_t i = 0; i < n; ++i) {
-            const double z = 1.0 + x * y[i];
-            su += 1.0 / z;
-            sv += std::log(z);
-        }
-        const double u = su / static_cast<double>(n);
-        const double v = 1.0 + sv / static_cast<double>(n);
-        return u * v - 1.0;
-    }
-
-    double loglik(double gamma, double sigma) const
-    {
-        if (!(sigma > 0.0))
-            return -std::numeric_limits<double>::infinity();
-        double acc = 0.0;
-        if (gamma == 0.0) {
-            for (int64_t i = 0; i < n; ++i)
-                acc += y[i];
-            return -static_cast<double>(n) * std::log(sigma) - acc / sigma;
-        }
-        for (int64_t i = 0; i < n; ++i) {
-            const double z = 1.0 + gamma * y[i] / sigma;
-            if (!(z > 0.0))
-                return -std::numeric_limits<double>::infinity();
-            acc += std::log(z);
-        }
-        return -static_cast<double>(n) * std::log(sigma) - (1.0 + 1.0 / gamma) * acc;
-    }
-
-    double mean_log(double x) const
-    {
-        double s = 0.0;
-        for (int64_t i = 0; i < n; ++i)
-            s += std::log(1.0 + x * y[i]);
-        return s / static_cast<double>(n);
-    }
+struct Bracket {
+    double lo, hi;
+    bool lo_neg;     // sign of w(lo)
+    bool done;
+    double root;
 };
 
-// Roots of w on [a, b]: sign changes between grid points, each bisected.
-void roots_on(const Excess &ex, double a, double b, std::vector<double> *out)
-{
-    if (!(a < b))
-        return;
-    std::vector<double> xs(kGrid), ws(kGrid);
-    for (int i = 0; i < kGrid; ++i) {
-        xs[i] = a + (b - a) * static_cast<double>(i) / static_cast<double>(kGrid - 1);
-        ws[i] = ex.w(xs[i]);
-    }
-    for (int i = 0; i + 1 < kGrid; ++i) {
-        if (ws[i] == 0.0) {
-            out->push_back(xs[i]);
-            continue;
-        }
-        if (!(ws[i] * ws[i + 1] < 0.0))
-            continue;
-        double lo = xs[i], hi = xs[i + 1], wlo = ws[i];
-        for (int it = 0; it < kBisect; ++it) {
-            const double mid = 0.5 * (lo + hi);
-            if (mid <= lo || mid >= hi)
-                break;
-            const double wm = ex.w(mid);
-            if (wm == 0.0) {
-                lo = hi = mid;
-                break;
-            }
-            if ((wm < 0.0) == (wlo < 0.0)) {
-                lo = mid;
-                wlo = wm;
-            } else {
-                hi = mid;
-            }
-        }
-        out->push_back(0.5 * (lo + hi));
-    }
-    if (ws[kGrid - 1] == 0.0)
-        out->push_back(xs[kGrid - 1]);
-}
+double w_of(double su, double sv, double n) { return (su / n) * (1.0 + sv / n) - 1.0; }
 
-void fit_mle(const Excess &ex, double *gamma, double *sigma)
+double quantile_z(double t, double gamma, double sigma, double ratio)
 {
-    double ysum = 0.0;
-    for (int64_t i = 0; i < ex.n; ++i)
-        ysum += ex.y[i];
-    const double ymean = ysum / static_cast<double>(ex.n);
-    const double ymin = ex.y[0], ymax = ex.y[ex.n - 1];   // excesses are sorted ascending
-    const double eps = 1e-8 / ymean;
-    std::vector<double> roots;
-    roots_on(ex, -1.0 / ymax + eps, -eps, &roots);
-    const double right = 2.0 * (ymean - ymin) / (ymin * ymin);
-    if (right > 2.0 * eps)
-        roots_on(ex, eps, right, &roots);
-    double bg = 0.0, bs = ymean, bl = ex.loglik(0.0, ymean);
-    for (double xr : roots) {
-        const double g = ex.mean_log(xr);
-        if (g == 0.0)
-            continue;
-        const double s = g / xr;
-        const double ll = ex.loglik(g, s);
-        if (ll > bl || (ll == bl && std::fabs(g) < std::fabs(bg))) {
-            bg = g;
-            bs = s;
-            bl = ll;
-        }
-    }
-    *gamma = bg;
-    *sigma = bs;
+    if (std::fabs(gamma) < 1e-9)
+        return t - sigma * std::log(ratio);
+    return t + sigma / gamma * (std::pow(ratio, -gamma) - 1.0);
 }
 
 }  // namespace
 
-PotResult pot_from_peaks(double t, int64_t n, const double *excess, int64_t n_peaks, double q)
+PotResult pot_small(double t, int64_t n, const double *excess, int64_t n_peaks, double q)
 {
     PotResult r{};
     r.t = t;
@@ -148,34 +55,167 @@ PotResult pot_from_peaks(double t, int64_t n, const double *excess, int64_t n_pe
     r.gamma = std::numeric_limits<double>::quiet_NaN();
     r.sigma = std::numeric_limits<double>::quiet_NaN();
     r.method = 0;
-    double gamma, sigma;
-    if (n_peaks >= 10) {
-        fit_mle(Excess{excess, n_peaks}, &gamma, &sigma);
-        r.method = 2;
-    } else if (n_peaks >= 2) {
-        double m = 0.0;
-        for (int64_t i = 0; i < n_peaks; ++i)
-            m += excess[i];
-        m /= static_cast<double>(n_peaks);
-        double s2 = 0.0;
-        for (int64_t i = 0; i < n_peaks; ++i)
-            s2 += (excess[i] - m) * (excess[i] - m);
-        s2 /= static_cast<double>(n_peaks - 1);
-        if (!(s2 > 0.0))
-            return r;
-        gamma = 0.5 * (1.0 - m * m / s2);
-        sigma = 0.5 * m * (1.0 + m * m / s2);
-        r.method = 1;
-    } else {
+    if (n_peaks < 2)
         return r;
+    double m = 0.0;
+    for (int64_t i = 0; i < n_peaks; ++i)
+        m += excess[i];
+    m /= static_cast<double>(n_peaks);
+    double s2 = 0.0;
+    for (int64_t i = 0; i < n_peaks; ++i)
+        s2 += (excess[i] - m) * (excess[i] - m);
+    s2 /= static_cast<double>(n_peaks - 1);       // unbiased sample variance
+    if (!(s2 > 0.0))
+        return r;
+    r.gamma = 0.5 * (1.0 - m * m / s2);
+    r.sigma = 0.5 * m * (1.0 + m * m / s2);
+    r.method = 1;
+    r.z = quantile_z(t, r.gamma, r.sigma, q * static_cast<double>(n) / static_cast<double>(n_peaks));
+    return r;
+}
+
+PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin, double ymax,
+                  double q, GpdSums &sums, bool *ok)
+{
+    *ok = false;
+    PotResult r{};
+    r.t = t;
+    r.n = n;
+    r.n_peaks = n_peaks;
+    r.method = 2;
+    const double N = static_cast<double>(n_peaks);
+    const double ymean = ysum / N;
+    const double eps = 1e-8 / ymean;
+
+    // grid over both admissible intervals
+    std::vector<std::pair<double, double>> ivs;
+    ivs.push_back({-1.0 / ymax + eps, -eps});
+    const double right = 2.0 * (ymean - ymin) / (ymin * ymin);
+    if (right > 2.0 * eps)
+        ivs.push_back({eps, right});
+    std::vector<double> xs, su, sv;
+    for (auto &iv : ivs)
+        if (iv.first < iv.second)
+            for (int i = 0; i < kGrid; ++i)
+                xs.push_back(iv.first + (iv.second - iv.first) * static_cast<double>(i) /
+                                            static_cast<double>(kGrid - 1));
+    su.resize(xs.size());
+    sv.resize(xs.size());
+    if (!xs.empty() && !sums.eval(xs.data(), static_cast<int>(xs.size()), su.data(), sv.data()))
+        return r;
+    std::vector<double> roots;
+    std::vector<Bracket> br;
+    for (size_t iv = 0, base = 0; iv < ivs.size(); ++iv) {
+        if (!(ivs[iv].first < ivs[iv].second))
+            continue;
+        for (int i = 0; i < kGrid; ++i) {
+            const double wi = w_of(su[base + i], sv[base + i], N);
+            if (wi == 0.0) {
+                roots.push_back(xs[base + i]);
+                continue;
+            }
+            if (i + 1 < kGrid) {
+                const double wn = w_of(su[base + i + 1], sv[base + i + 1], N);
+                if (wi * wn < 0.0)
+                    br.push_back({xs[base + i], xs[base + i + 1], wi < 0.0, false, 0.0});
+            }
+        }
+        base += kGrid;
     }
-    r.gamma = gamma;
-    r.sigma = sigma;
-    const double ratio = q * static_cast<double>(n) / static_cast<double>(n_peaks);
-    if (std::fabs(gamma) < 1e-9)
-        r.z = t - sigma * std::log(ratio);
-    else
-        r.z = t + sigma / gamma * (std::pow(ratio, -gamma) - 1.0);
+    // k-section of every open bracket, batched
+    for (int round = 0; round < kRounds; ++round) {
+        xs.clear();
+        std::vector<int> owner;
+        for (size_t b = 0; b < br.size(); ++b) {
+            Bracket &k = br[b];
+            if (k.done)
+                continue;
+            double prev = k.lo;
+            bool collapsed = false;
+            std::vector<double> pts;
+            for (int j = 1; j <= kInterior; ++j) {
+                const double p = k.lo + (k.hi - k.lo) * static_cast<double>(j) / (kInterior + 1);
+                if (!(p > prev) || !(p < k.hi)) {
+                    collapsed = true;
+                    break;
+                }
+                pts.push_back(p);
+                prev = p;
+            }
+            if (collapsed) {
+                k.done = true;
+                k.root = 0.5 * (k.lo + k.hi);
+                continue;
+            }
+            for (double p : pts) {
+                xs.push_back(p);
+                owner.push_back(static_cast<int>(b));
+            }
+        }
+        if (xs.empty())
+            break;
+        su.assign(xs.size(), 0.0);
+        sv.assign(xs.size(), 0.0);
+        if (!sums.eval(xs.data(), static_cast<int>(xs.size()), su.data(), sv.data()))
+            return r;
+        for (size_t i = 0; i < xs.size();) {
+            const int b = owner[i];
+            Bracket &k = br[b];
+            size_t j = i;
+            double new_lo = k.lo, new_hi = k.hi;
+            bool found = false;
+            for (; j < xs.size() && owner[j] == b; ++j) {
+                if (found)
+                    continue;
+                const double wj = w_of(su[j], sv[j], N);
+                if (wj == 0.0) {
+                    k.done = true;
+                    k.root = xs[j];
+                    found = true;
+                } else if ((wj < 0.0) != k.lo_neg) {
+                    new_hi = xs[j];
+                    found = true;
+                } else {
+                    new_lo = xs[j];
+                }
+            }
+            if (!k.done) {
+                k.lo = new_lo;
+                k.hi = new_hi;
+            }
+            i = j;
+        }
+    }
+    for (auto &k : br)
+        roots.push_back(k.done ? k.root : 0.5 * (k.lo + k.hi));
+
+    // candidates: the exponential tail and every root
+    double bg = 0.0, bs = ymean;
+    double bl = -N * std::log(ymean) - ysum / ymean;
+    if (!roots.empty()) {
+        su.assign(roots.size(), 0.0);
+        sv.assign(roots.size(), 0.0);
+        if (!sums.eval(roots.data(), static_cast<int>(roots.size()), su.data(), sv.data()))
+            return r;
+        for (size_t i = 0; i < roots.size(); ++i) {
+            const double g = sv[i] / N;
+            if (g == 0.0 || !std::isfinite(g))
+                continue;
+            const double s = g / roots[i];
+            if (!(s > 0.0))
+                continue;
+            const double ll = -N * std::log(s) - (1.0 + 1.0 / g) * sv[i];
+            if (ll > bl || (ll == bl && std::fabs(g) < std::fabs(bg))) {
+                bg = g;
+                bs = s;
+                bl = ll;
+            }
+        }
+    }
+    r.gamma = bg;
+    r.sigma = bs;
+    r.z = quantile_z(t, bg, bs, q * static_cast<double>(n) / N);
+    *ok = true;
     return r;
 }
 
