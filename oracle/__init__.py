@@ -237,7 +237,7 @@ def window_debug(x_stream, k, *, window, stride, weights, mean, std, act="relu",
 
 
 # ----------------------------------------------------------------------------- POT
-GRID = 512          # grid points per search interval for the roots of u(x) v(x) = 1
+GRID = 512          # grid points per admissible interval for the roots of u(x) v(x) = 1
 BISECT_ITERS = 200  # bisection steps (stops earlier once the bracket cannot shrink)
 
 
@@ -248,10 +248,36 @@ def _gpd_loglik(Y, gamma, sigma):
         return -math.inf
     if gamma == 0.0:
         return -N * math.log(sigma) - float(np.sum(Y)) / sigma
-    z = 1.0 + gamma * Y / sigma
-    if np.any(z <= 0):
+    r = gamma * Y / sigma
+    if np.any(r <= -1.0):
         return -math.inf
-    return -N * math.log(sigma) - (1.0 + 1.0 / gamma) * float(np.sum(np.log(z)))
+    return -N * math.log(sigma) - (1.0 + 1.0 / gamma) * float(np.sum(np.log1p(r)))
+
+
+def gpd_grid(ymean, ymin, ymax):
+    """Evaluation grid of Grimshaw's equation over both admissible intervals of x = gamma/sigma.
+
+    Right interval (0, B], B = 2 (mean - min) / min^2: GRID points geometric from
+    eps = 1e-8/mean to B. Left interval (-1/Y_max, 0): x = -f/Y_max with f the logistic of
+    GRID points linear in z from logit(eps*Y_max) to 30, i.e. geometric towards both 0 and the
+    endpoint -1/Y_max. Returns a list of increasing-index arrays, one per interval.
+    """
+    eps = 1e-8 / ymean
+    out = []
+    f0 = eps * ymax
+    if f0 < 0.5:
+        zlo = math.log(f0 / (1.0 - f0))
+        zhi = 30.0
+        xs = []
+        for i in range(GRID):
+            z = zlo + (zhi - zlo) * i / (GRID - 1)
+            xs.append(-(1.0 / (1.0 + math.exp(-z))) / ymax)
+        out.append(xs)
+    right = 2.0 * (ymean - ymin) / (ymin * ymin)
+    if right > 2.0 * eps:
+        ratio = right / eps
+        out.append([eps * ratio ** (i / (GRID - 1)) for i in range(GRID)])
+    return out
 
 
 def grimshaw(Y):
@@ -259,33 +285,25 @@ def grimshaw(Y):
 
     With x = gamma / sigma the likelihood equations reduce to u(x) v(x) = 1 with
     u(x) = mean 1/(1 + x Y) and v(x) = 1 + mean log(1 + x Y); a root gives
-    gamma = v(x) - 1 and sigma = gamma / x. Roots are bracketed on a fixed grid of
-    each admissible interval (-1/Y_max, 0) and (0, 2 (mean - min) / min^2) and
-    bisected; the exponential (gamma = 0, sigma = mean) is always a candidate; the
-    candidate of largest log-likelihood wins (ties: smaller |gamma|).
-    Returns (gamma, sigma, loglik).
+    gamma = v(x) - 1 and sigma = gamma / x. The equation is evaluated without cancellation
+    as w = b - a - a b, a = mean(xY/(1+xY)) = 1 - u, b = mean log1p(xY) = v - 1. Roots are
+    bracketed on the geometric grids of ``gpd_grid`` and bisected; the exponential
+    (gamma = 0, sigma = mean) is always a candidate; the candidate of largest
+    log-likelihood wins (ties: smaller |gamma|). Returns (gamma, sigma, loglik).
     """
     Y = np.asarray(Y, np.float64)
     ymax, ymin, ymean = float(Y.max()), float(Y.min()), float(Y.mean())
 
     def w(xv):
-        z = 1.0 + xv * Y
-        u = float(np.mean(1.0 / z))
-        v = 1.0 + float(np.mean(np.log(z)))
-        return u * v - 1.0
+        xy = xv * Y
+        a = float(np.mean(xy / (1.0 + xy)))
+        b = float(np.mean(np.log1p(xy)))
+        return b - a - a * b
 
-    eps = 1e-8 / ymean
-    intervals = [(-1.0 / ymax + eps, -eps)]
-    right = 2.0 * (ymean - ymin) / (ymin * ymin)
-    if right > 2.0 * eps:
-        intervals.append((eps, right))
     roots = []
-    for a, b in intervals:
-        if not a < b:
-            continue
-        xs = [a + (b - a) * i / (GRID - 1) for i in range(GRID)]
+    for xs in gpd_grid(ymean, ymin, ymax):
         ws = [w(xv) for xv in xs]
-        for i in range(GRID - 1):
+        for i in range(len(xs) - 1):
             if ws[i] == 0.0:
                 roots.append(xs[i])
                 continue
@@ -293,7 +311,7 @@ def grimshaw(Y):
                 lo, hi, wlo = xs[i], xs[i + 1], ws[i]
                 for _ in range(BISECT_ITERS):
                     mid = 0.5 * (lo + hi)
-                    if mid <= lo or mid >= hi:
+                    if mid == lo or mid == hi:
                         break
                     wm = w(mid)
                     if wm == 0.0:
@@ -308,7 +326,7 @@ def grimshaw(Y):
             roots.append(xs[-1])
     best = (0.0, ymean, _gpd_loglik(Y, 0.0, ymean))
     for xr in roots:
-        gamma = float(np.mean(np.log(1.0 + xr * Y)))
+        gamma = float(np.mean(np.log1p(xr * Y)))
         if gamma == 0.0:
             continue
         sigma = gamma / xr

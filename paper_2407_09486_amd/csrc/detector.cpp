@@ -229,22 +229,36 @@ struct DeviceGpdSums : GpdSums {
     enova_status status = ENOVA_OK;
     DeviceGpdSums(enova_detector d_, const double *y_, int64_t n_, hipStream_t s_)
         : d(d_), y(y_), n(n_), st(s_) {}
-    bool eval(const double *xs, int nx, double *su, double *sv) override
+    bool eval(const double *xs, int nx, double *sa, double *sb) override
     {
         if (nx <= 0)
             return true;
-        status = ensure(&d->gx, &d->gx_cap, 3 * static_cast<size_t>(nx));
+        const int ns = gpd_split(n);
+        const size_t np = static_cast<size_t>(nx) * ns;
+        status = ensure(&d->gx, &d->gx_cap, static_cast<size_t>(nx) + 2 * np);
         if (status != ENOVA_OK)
             return false;
-        double *dx = d->gx, *dsu = d->gx + nx, *dsv = d->gx + 2 * static_cast<size_t>(nx);
+        double *dx = d->gx, *dpa = d->gx + nx, *dpb = dpa + np;
+        std::vector<double> pa(np), pb(np);
         hipError_t e;
         if ((e = hipMemcpyAsync(dx, xs, sizeof(double) * nx, hipMemcpyHostToDevice, st)) != hipSuccess ||
-            (e = launch_gpd_sums(y, n, dx, nx, dsu, dsv, st)) != hipSuccess ||
-            (e = hipMemcpyAsync(su, dsu, sizeof(double) * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
-            (e = hipMemcpyAsync(sv, dsv, sizeof(double) * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = launch_gpd_sums(y, n, dx, nx, ns, dpa, dpb, st)) != hipSuccess ||
+            (e = hipMemcpyAsync(pa.data(), dpa, sizeof(double) * np, hipMemcpyDeviceToHost, st)) !=
+                hipSuccess ||
+            (e = hipMemcpyAsync(pb.data(), dpb, sizeof(double) * np, hipMemcpyDeviceToHost, st)) !=
+                hipSuccess ||
             (e = hipStreamSynchronize(st)) != hipSuccess) {
             status = hip_fail(e, "GPD likelihood sums");
             return false;
+        }
+        for (int i = 0; i < nx; ++i) {
+            double a = 0.0, b = 0.0;
+            for (int j = 0; j < ns; ++j) {
+                a += pa[static_cast<size_t>(i) * ns + j];
+                b += pb[static_cast<size_t>(i) * ns + j];
+            }
+            sa[i] = a;
+            sb[i] = b;
         }
         return true;
     }

@@ -100,9 +100,12 @@ hipError_t launch_calib_compact(const float *scores, const int64_t *woff, const 
                                 int n, int64_t n_cal, uint32_t key, double t,
                                 const int64_t *block_off, double *y, int64_t cap, hipStream_t st);
 hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream_t st);
-// su[i] = sum_j 1/(1 + xs[i] y_j), sv[i] = sum_j log(1 + xs[i] y_j)   (fixed-order fp64 sums)
-hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, double *su,
-                           double *sv, hipStream_t st);
+// Partial likelihood sums at the points xs: block (i, j) of nx*nsplit blocks writes
+// pa[i*nsplit + j] = sum xs[i] y/(1 + xs[i] y) and pb[i*nsplit + j] = sum log1p(xs[i] y) over the
+// j-th of nsplit contiguous chunks of y (fixed-order fp64 sums; the caller adds the chunks in order).
+int gpd_split(int64_t n);
+hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
+                           double *pa, double *pb, hipStream_t st);
 // out = {sum y, min y, max y}
 hipError_t launch_peak_stats(const double *y, int64_t n, double *out, hipStream_t st);
 
@@ -115,7 +118,7 @@ struct PotResult {
 };
 struct GpdSums {
     virtual ~GpdSums() = default;
-    // su[i] = sum 1/(1 + xs[i] y), sv[i] = sum log(1 + xs[i] y); false on failure
+    // sa[i] = sum xs[i] y / (1 + xs[i] y), sb[i] = sum log1p(xs[i] y); false on failure
     virtual bool eval(const double *xs, int nx, double *su, double *sv) = 0;
 };
 // Maximum likelihood (n_peaks >= 10) given the excesses' sum, minimum and maximum.

@@ -332,25 +332,30 @@ __device__ __forceinline__ void block_sum2(double &a, double &b, double *sa, dou
     b = sb[0];
 }
 
-// Likelihood sums of the excesses at the points xs: block i returns
-// su[i] = sum 1/(1 + xs[i] y) and sv[i] = sum log(1 + xs[i] y).
+// Likelihood sums of the excesses: block (i, j) covers chunk j of nsplit contiguous chunks of y
+// at the point xs[i] and writes pa = sum xy/(1+xy), pb = sum log1p(xy) in a fixed order.
 __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, int64_t n,
-                                                  const double *__restrict__ xs,
-                                                  double *__restrict__ su, double *__restrict__ sv)
+                                                  const double *__restrict__ xs, int nsplit,
+                                                  double *__restrict__ pa, double *__restrict__ pb)
 {
     __shared__ double sa[256];
     __shared__ double sb[256];
-    const double x = xs[blockIdx.x];
+    const int p = blockIdx.x / nsplit;
+    const int j = blockIdx.x - p * nsplit;
+    const double x = xs[p];
+    const int64_t chunk = (n + nsplit - 1) / nsplit;
+    const int64_t lo = j * chunk;
+    const int64_t hi = lo + chunk < n ? lo + chunk : n;
     double a = 0.0, b = 0.0;
-    for (int64_t i = threadIdx.x; i < n; i += 256) {
-        const double z = 1.0 + x * y[i];
-        a += 1.0 / z;
-        b += log(z);
+    for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
+        const double xy = x * y[i];
+        a += xy / (1.0 + xy);
+        b += log1p(xy);
     }
     block_sum2(a, b, sa, sb);
     if (threadIdx.x == 0) {
-        su[blockIdx.x] = a;
-        sv[blockIdx.x] = b;
+        pa[blockIdx.x] = a;
+        pb[blockIdx.x] = b;
     }
 }
 
@@ -469,12 +474,19 @@ hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream
     return hipGetLastError();
 }
 
-hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, double *su,
-                           double *sv, hipStream_t st)
+int gpd_split(int64_t n)
+{
+    const int64_t s = (n + 32767) / 32768;
+    return static_cast<int>(s < 1 ? 1 : (s > 64 ? 64 : s));
+}
+
+hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
+                           double *pa, double *pb, hipStream_t st)
 {
     if (nx <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_gpd_sums, dim3(nx), dim3(256), 0, st, y, n, xs, su, sv);
+    hipLaunchKernelGGL(k_gpd_sums, dim3(static_cast<unsigned>(nx) * nsplit), dim3(256), 0, st, y, n,
+                       xs, nsplit, pa, pb);
     return hipGetLastError();
 }
 

@@ -3,12 +3,15 @@
 // The excesses Y over the level-quantile t follow a generalised Pareto distribution
 // GPD(gamma, sigma). Maximum likelihood uses Grimshaw's reduction: with x = gamma/sigma the
 // score equations collapse to one equation in x,
-//     w(x) = u(x) v(x) - 1 = 0,   u = mean 1/(1+xY),   v = 1 + mean log(1+xY),
-// whose roots give gamma = v(x) - 1 and sigma = gamma/x. Roots are bracketed on a fixed grid of
-// each admissible interval, (-1/Y_max, 0) and (0, 2 (mean - min) / min^2), and refined by
-// k-section (63 interior points per round, all brackets evaluated in one batch) until the
-// bracket cannot shrink in fp64. The exponential tail (gamma = 0, sigma = mean Y) is always a
-// candidate, and the candidate of largest log-likelihood wins (ties: smaller |gamma|).
+//     u(x) v(x) = 1,   u = mean 1/(1+xY),   v = 1 + mean log(1+xY),
+// whose roots give gamma = v(x) - 1 and sigma = gamma/x. It is evaluated without cancellation as
+//     w(x) = b - a - a b = 0,   a = mean xY/(1+xY) = 1 - u,   b = mean log1p(xY) = v - 1.
+// Roots are bracketed on geometric grids of both admissible intervals: (0, B], B =
+// 2 (mean - min) / min^2, which spans many decades once there are many peaks, and
+// (-1/Y_max, 0), resolved geometrically towards both ends; brackets are refined by k-section
+// (63 interior points per round, all brackets evaluated in one batch) until they cannot shrink.
+// The exponential tail (gamma = 0, sigma = mean Y) is always a candidate, and the candidate of
+// largest log-likelihood wins (ties: smaller |gamma|).
 //
 // The sums over the (possibly millions of) excesses come from a GpdSums evaluator; the
 // library's evaluator runs them on the device where the excesses were compacted.
@@ -34,7 +37,11 @@ struct Bracket {
     double root;
 };
 
-double w_of(double su, double sv, double n) { return (su / n) * (1.0 + sv / n) - 1.0; }
+double w_of(double sa, double sb, double n)
+{
+    const double a = sa / n, b = sb / n;
+    return b - a - a * b;
+}
 
 double quantile_z(double t, double gamma, double sigma, double ratio)
 {
@@ -87,27 +94,36 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
     const double ymean = ysum / N;
     const double eps = 1e-8 / ymean;
 
-    // grid over both admissible intervals
-    std::vector<std::pair<double, double>> ivs;
-    ivs.push_back({-1.0 / ymax + eps, -eps});
+    // geometric grids over both admissible intervals of x
+    std::vector<std::vector<double>> grids;
+    const double f0 = eps * ymax;
+    if (f0 < 0.5) {
+        const double zlo = std::log(f0 / (1.0 - f0)), zhi = 30.0;
+        std::vector<double> g(kGrid);
+        for (int i = 0; i < kGrid; ++i) {
+            const double z = zlo + (zhi - zlo) * static_cast<double>(i) / static_cast<double>(kGrid - 1);
+            g[i] = -(1.0 / (1.0 + std::exp(-z))) / ymax;
+        }
+        grids.push_back(g);
+    }
     const double right = 2.0 * (ymean - ymin) / (ymin * ymin);
-    if (right > 2.0 * eps)
-        ivs.push_back({eps, right});
+    if (right > 2.0 * eps) {
+        const double ratio = right / eps;
+        std::vector<double> g(kGrid);
+        for (int i = 0; i < kGrid; ++i)
+            g[i] = eps * std::pow(ratio, static_cast<double>(i) / static_cast<double>(kGrid - 1));
+        grids.push_back(g);
+    }
     std::vector<double> xs, su, sv;
-    for (auto &iv : ivs)
-        if (iv.first < iv.second)
-            for (int i = 0; i < kGrid; ++i)
-                xs.push_back(iv.first + (iv.second - iv.first) * static_cast<double>(i) /
-                                            static_cast<double>(kGrid - 1));
+    for (auto &g : grids)
+        xs.insert(xs.end(), g.begin(), g.end());
     su.resize(xs.size());
     sv.resize(xs.size());
     if (!xs.empty() && !sums.eval(xs.data(), static_cast<int>(xs.size()), su.data(), sv.data()))
         return r;
     std::vector<double> roots;
     std::vector<Bracket> br;
-    for (size_t iv = 0, base = 0; iv < ivs.size(); ++iv) {
-        if (!(ivs[iv].first < ivs[iv].second))
-            continue;
+    for (size_t gi = 0, base = 0; gi < grids.size(); ++gi) {
         for (int i = 0; i < kGrid; ++i) {
             const double wi = w_of(su[base + i], sv[base + i], N);
             if (wi == 0.0) {
@@ -116,8 +132,14 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
             }
             if (i + 1 < kGrid) {
                 const double wn = w_of(su[base + i + 1], sv[base + i + 1], N);
-                if (wi * wn < 0.0)
-                    br.push_back({xs[base + i], xs[base + i + 1], wi < 0.0, false, 0.0});
+                if (wi * wn < 0.0) {
+                    const double x0 = xs[base + i], x1 = xs[base + i + 1];
+                    // keep lo < hi; lo_neg is the sign of w at lo
+                    if (x0 < x1)
+                        br.push_back({x0, x1, wi < 0.0, false, 0.0});
+                    else
+                        br.push_back({x1, x0, wn < 0.0, false, 0.0});
+                }
             }
         }
         base += kGrid;
@@ -204,7 +226,7 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
             const double s = g / roots[i];
             if (!(s > 0.0))
                 continue;
-            const double ll = -N * std::log(s) - (1.0 + 1.0 / g) * sv[i];
+            const double ll = -N * std::log(s) - (1.0 + 1.0 / g) * sv[i];   // sum log1p(g y / s) = sv
             if (ll > bl || (ll == bl && std::fabs(g) < std::fabs(bg))) {
                 bg = g;
                 bs = s;

@@ -34,6 +34,21 @@ def test_grimshaw_recovers_parameters_within_3se():
     assert abs(s - sigma) < 3 * se_s
 
 
+def test_grimshaw_many_peaks_heavy_tail():
+    """With many excesses Y_min is tiny, so the right admissible interval (0, 2(mean-min)/min^2]
+    spans many decades; the root near gamma/sigma must still be bracketed (a linear grid puts it
+    inside its first cell, where the sign of the equation at the left end is rounding noise)."""
+    gamma, sigma, n = 0.1, 20.0, 100_000
+    Y = st.genpareto.rvs(gamma, scale=sigma, size=n, random_state=np.random.default_rng(21))
+    g, s, ll = oracle.grimshaw(Y)
+    assert abs(g - gamma) < 3 * (1 + gamma) / math.sqrt(n)
+    assert abs(s - sigma) < 3 * sigma * math.sqrt(2 * (1 + gamma) / n)
+    assert ll > oracle._gpd_loglik(Y, 0.0, float(Y.mean()))
+    # the same excesses in another order give the same fit
+    g2, s2, _ = oracle.grimshaw(Y[::-1].copy())
+    assert g2 == pytest.approx(g, rel=1e-9) and s2 == pytest.approx(s, rel=1e-9)
+
+
 def test_exponential_tail_threshold_closed_form():
     """Exp(lam) scores: P(X > z) = e^(-lam z), so the q-quantile of the tail is -ln(q)/lam."""
     lam, q = 0.5, 1e-3
