@@ -123,8 +123,7 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     g->CPR = static_cast<int>(cpr);
     g->CPRP = (g->CPR % 2 == 0) ? g->CPR + 1 : g->CPR;
     int64_t kc = static_cast<int64_t>(g->Q) * g->CPR;
-    if (kc % 2)
-        ++kc;
+    kc = (kc + 3) / 4 * 4;        // an even number of two-chunk steps
     g->KC = static_cast<int>(kc);
     int hb = 1;
     while (hb < 8 && 32 * hb < g->H)
@@ -133,8 +132,8 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     g->Hp = 32 * hb;
     g->NBW = mfma_nbw_for(hb);
     g->Nb = kWaves * g->NBW * 32;
-    g->lds_bytes = static_cast<size_t>(g->Nb + g->Q) * g->CPRP * 16 +
-                   static_cast<size_t>(g->Nb + g->Q) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
+    g->lds_bytes = static_cast<size_t>(g->Nb + g->Q + 2) * g->CPRP * 16 +
+                   static_cast<size_t>(g->Nb + g->Q + 2) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;
     if (!g->mfma_ok) {

@@ -29,7 +29,7 @@ struct Geometry {
     int Q;                  // super-rows per window
     int CPR;                // chunks per super-row
     int CPRP;               // LDS row pitch in chunks (odd, so 16 consecutive rows hit distinct banks)
-    int KC;                 // chunks per window, rounded up to even
+    int KC;                 // chunks per window, rounded up to a multiple of 4
     int Hp;                 // hidden width padded to 32*HB
     int HB;                 // 32-row hidden blocks per wave
     int NBW;                // 32-window blocks per wave

@@ -123,11 +123,12 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
     const int64_t T = p.soff[s + 1] - srow;
 
     const int Q = g.Q, CPR = g.CPR, CPRP = g.CPRP, M = g.M, Mp = g.Mp, S = g.S;
-    const int nrows = nv + Q;                      // staged super-rows (one spare)
+    // staged super-rows: the tile's nv + Q - 1 plus 3 spare rows read only by zero-weight chunks
+    const int nrows = nv + Q + 2;
     uint4 *seg = lds;
-    float *rs = reinterpret_cast<float *>(seg + static_cast<size_t>(NB + Q) * CPRP);
-    float *ps = rs + (NB + Q);
-    float *smean = ps + (NB + Q);
+    float *rs = reinterpret_cast<float *>(seg + static_cast<size_t>(NB + Q + 2) * CPRP);
+    float *ps = rs + (NB + Q + 2);
+    float *smean = ps + (NB + Q + 2);
     float *srinv = smean + Mp;
 
     for (int m = tid; m < Mp; m += kThreads) {
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
-        rb[nb] = n < nv ? n : nv - 1;        // idle columns re-read a valid window
+        rb[nb] = (n < nv ? n : nv - 1) * CPRP;   // idle columns re-read a valid window
     }
     v16f acc[HB][NBW];
 #pragma unroll
@@ -254,85 +255,91 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
                 acc[hb][nb][r] = 0.0f;
 
     const bool wave_active = wave * NBW * 32 < nv;
-    const int nsteps = g.KC / 2;
+    const int nsteps = g.KC / 2;                 // even: KC is a multiple of 4
     const uint4 *ap = p.w1p + lane;
-    uint4 a_cur[HB];
+    // LDS chunk offset of this lane's chunk kappa = 2*i + half inside a window:
+    // (kappa / CPR) * CPRP + kappa % CPR, advanced without branches
+    const int dpitch = CPRP - CPR;
+    int cc = half % CPR;
+    int koff = (half / CPR) * CPRP + cc;
+    const int klast = 2 * (nsteps - 1) + half;
+    const int koff_max = (klast / CPR) * CPRP + klast % CPR;
+    auto advance = [&]() {
+        const bool wrap = cc + 2 >= CPR;
+        cc = cc + 2 - (wrap ? CPR : 0);
+        koff += 2 + (wrap ? dpitch : 0);
+    };
+    auto mma = [&](const uint4 (&a)[HB], const uint4 (&bq)[NBW]) {
+        if constexpr (DT == ENOVA_F32) {
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb)
-        a_cur[hb] = ap[hb * 64];
-    int q = 0, c = half;                       // chunk kappa = 2*i + half
-    while (c >= CPR) {
-        c -= CPR;
-        ++q;
-    }
-    __syncthreads();
-    if (wave_active) {
-        for (int i = 0; i < nsteps; ++i) {
-            uint4 a_nxt[HB];
-            if (i + 1 < nsteps) {
-#pragma unroll
-                for (int hb = 0; hb < HB; ++hb)
-                    a_nxt[hb] = ap[((i + 1) * HB + hb) * 64];
-            }
-            uint4 bf[NBW];
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                bf[nb] = seg[(rb[nb] + q) * CPRP + c];
-            if constexpr (DT == ENOVA_F32) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-#pragma unroll
-                    for (int hb = 0; hb < HB; ++hb) {
-                        const float av = __uint_as_float(e == 0 ? a_cur[hb].x : e == 1 ? a_cur[hb].y
-                                                        : e == 2 ? a_cur[hb].z : a_cur[hb].w);
-#pragma unroll
-                        for (int nb = 0; nb < NBW; ++nb) {
-                            const float bv = __uint_as_float(e == 0 ? bf[nb].x : e == 1 ? bf[nb].y
-                                                            : e == 2 ? bf[nb].z : bf[nb].w);
-                            acc[hb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[hb][nb], 0, 0, 0);
-                        }
-                    }
-                }
-            } else {
+            for (int e = 0; e < 4; ++e) {
 #pragma unroll
                 for (int hb = 0; hb < HB; ++hb) {
-                    const v8bf av = __builtin_bit_cast(v8bf, a_cur[hb]);
+                    const float av = __uint_as_float(e == 0 ? a[hb].x : e == 1 ? a[hb].y
+                                                    : e == 2 ? a[hb].z : a[hb].w);
 #pragma unroll
-                    for (int nb = 0; nb < NBW; ++nb)
-                        acc[hb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            av, __builtin_bit_cast(v8bf, bf[nb]), acc[hb][nb], 0, 0, 0);
+                    for (int nb = 0; nb < NBW; ++nb) {
+                        const float bv = __uint_as_float(e == 0 ? bq[nb].x : e == 1 ? bq[nb].y
+                                                        : e == 2 ? bq[nb].z : bq[nb].w);
+                        acc[hb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[hb][nb], 0, 0, 0);
+                    }
                 }
             }
-            if (i + 1 < nsteps) {
+        } else {
 #pragma unroll
-                for (int hb = 0; hb < HB; ++hb)
-                    a_cur[hb] = a_nxt[hb];
+            for (int hb = 0; hb < HB; ++hb) {
+                const v8bf av = __builtin_bit_cast(v8bf, a[hb]);
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+                    acc[hb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        av, __builtin_bit_cast(v8bf, bq[nb]), acc[hb][nb], 0, 0, 0);
             }
-            c += 2;
-            while (c >= CPR) {
-                c -= CPR;
-                ++q;
-            }
+        }
+    };
+    __syncthreads();
+    if (wave_active) {
+        // ping-pong operand buffers, each step's operands fetched one step ahead
+        uint4 a0[HB], a1[HB], b0[NBW], b1[NBW];
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb)
+            a0[hb] = ap[hb * 64];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+            b0[nb] = seg[rb[nb] + koff];
+        for (int i = 0; i < nsteps; i += 2) {
+            advance();
+#pragma unroll
+            for (int hb = 0; hb < HB; ++hb)
+                a1[hb] = ap[((i + 1) * HB + hb) * 64];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                b1[nb] = seg[rb[nb] + koff];
+            // keep the prefetch ahead of this step's matrix ops (the scheduler would sink it)
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            advance();
+            const int inext = i + 2 < nsteps ? i + 2 : nsteps - 1;
+            const int kn = koff < koff_max ? koff : koff_max;
+#pragma unroll
+            for (int hb = 0; hb < HB; ++hb)
+                a0[hb] = ap[(inext * HB + hb) * 64];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                b0[nb] = seg[rb[nb] + kn];
+            __builtin_amdgcn_sched_barrier(0);
+            mma(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
     if (!wave_active)
         return;
 
-    // ---- epilogue: hidden activations in place
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const float bias = p.b1[hb * 32 + crow(r, half)];
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                acc[hb][nb][r] = act_fn(acc[hb][nb][r] + bias, g.act);
-        }
-    }
-
+    // ---- epilogue
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
-        // posterior heads: rows 0..15 mean, 16..31 log-variance
+        // hidden activations (bias + act, one 32-row block at a time) feed the posterior
+        // heads: rows 0..15 mean, 16..31 log-variance
         v16f z;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -340,9 +347,10 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
 #pragma unroll
         for (int hb = 0; hb < HB; ++hb) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                z = __builtin_amdgcn_mfma_f32_32x32x2f32(p.whp[(hb * 16 + r) * 64 + lane],
-                                                         acc[hb][nb][r], z, 0, 0, 0);
+            for (int r = 0; r < 16; ++r) {
+                const float h = act_fn(acc[hb][nb][r] + p.b1[hb * 32 + crow(r, half)], g.act);
+                z = __builtin_amdgcn_mfma_f32_32x32x2f32(p.whp[(hb * 16 + r) * 64 + lane], h, z, 0, 0, 0);
+            }
         }
         float kl = 0.0f;
 #pragma unroll
@@ -377,10 +385,11 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
         // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
         const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
         float vsum = 0.0f;
+        const int row0 = rb[nb] / CPRP;
         for (int qq = half; qq < Q - 1; qq += 2)
-            vsum += rs[rb[nb] + qq];
+            vsum += rs[row0 + qq];
         if (((Q - 1) & 1) == half)
-            vsum += ps[rb[nb] + Q - 1];
+            vsum += ps[row0 + Q - 1];
         vsum += __shfl_xor(vsum, 32);
 
         if (half == 0 && n < nv) {
