@@ -132,7 +132,10 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     g->Hp = 32 * hb;
     g->NBW = mfma_nbw_for(hb);
     g->Nb = kWaves * g->NBW * 32;
-    g->lds_bytes = static_cast<size_t>(g->Nb + g->Q + 2) * g->CPRP * 16 +
+    // epilogue weights (heads, decoder hidden layer, b1, bd1, u, head biases), the segment, its
+    // row sums and the stream statistics
+    const size_t n_const = static_cast<size_t>(hb) * (16 * 64 + 8 * 64) + 3 * static_cast<size_t>(g->Hp) + 32;
+    g->lds_bytes = n_const * sizeof(float) + static_cast<size_t>(g->Nb + g->Q + 2) * g->CPRP * 16 +
                    static_cast<size_t>(g->Nb + g->Q + 2) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;
@@ -333,21 +336,25 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
     //               whp[HB*16*64] wd1p[HB*8*64]
     const size_t n_whp = d->kind == 2 ? static_cast<size_t>(g.HB) * 16 * 64 : 0;
     const size_t n_wd1p = d->kind == 2 ? static_cast<size_t>(g.HB) * 8 * 64 : 0;
-    const size_t n_small = 3 * static_cast<size_t>(Hp) + 32 + 2 * L + 3 * static_cast<size_t>(L) * H +
-                           n_whp + n_wd1p;
-    std::vector<float> small(n_small, 0.0f);
+    // every sub-array starts on a 16-byte boundary (the kernels copy them with 16-byte loads)
     size_t o = 0;
-    const size_t o_b1 = o; o += Hp;
-    const size_t o_bd1 = o; o += Hp;
-    const size_t o_u = o; o += Hp;
-    const size_t o_bh = o; o += 32;
-    const size_t o_bmu = o; o += L;
-    const size_t o_blv = o; o += L;
-    const size_t o_wmu = o; o += static_cast<size_t>(L) * H;
-    const size_t o_wlv = o; o += static_cast<size_t>(L) * H;
-    const size_t o_wd1 = o; o += static_cast<size_t>(H) * L;
-    const size_t o_whp = o; o += n_whp;
-    const size_t o_wd1p = o; o += n_wd1p;
+    auto take = [&o](size_t n) {
+        const size_t at = o;
+        o += (n + 3) / 4 * 4;
+        return at;
+    };
+    const size_t o_b1 = take(Hp);
+    const size_t o_bd1 = take(Hp);
+    const size_t o_u = take(Hp);
+    const size_t o_bh = take(32);
+    const size_t o_bmu = take(L);
+    const size_t o_blv = take(L);
+    const size_t o_wmu = take(static_cast<size_t>(L) * H);
+    const size_t o_wlv = take(static_cast<size_t>(L) * H);
+    const size_t o_wd1 = take(static_cast<size_t>(H) * L);
+    const size_t o_whp = take(n_whp);
+    const size_t o_wd1p = take(n_wd1p);
+    std::vector<float> small(o, 0.0f);
 
     for (int h = 0; h < H; ++h) {
         small[o_b1 + h] = w->b1[h];

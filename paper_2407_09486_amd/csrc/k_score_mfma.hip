@@ -32,7 +32,7 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 struct MfmaShape {
-    int M, S, W, Mp, Q, CPR, CPRP, KC, act;
+    int M, S, W, Mp, Q, CPR, CPRP, KC;
     int tail_rows;   // steps of the window's last super-row that belong to the window
     float inv_d;
 };
@@ -48,11 +48,13 @@ __device__ __forceinline__ float load_x(const void *x, int64_t idx)
     }
 }
 
-__device__ __forceinline__ float act_fn(float a, int act)
+template <int ACT>
+__device__ __forceinline__ float act_fn(float a)
 {
-    if (act == ENOVA_TANH)
+    if constexpr (ACT == ENOVA_TANH)
         return tanhf(a);
-    return a < 0.0f ? 0.0f : a;   // ReLU; a NaN passes through
+    else
+        return a < 0.0f ? 0.0f : a;   // ReLU; a NaN passes through
 }
 
 // e^u - 1 - u without cancellation near 0: Taylor series through u^8 for |u| < 0.5.
@@ -98,7 +100,7 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u 
 // Row of the accumulator register r for lane half g inside a 32x32 block.
 __device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
-template <int DT, int HB, int NBW>
+template <int DT, int HB, int NBW, int ACT>
 __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShape g)
 {
     constexpr int NB = kWaves * NBW * 32;         // windows per tile
@@ -125,12 +127,35 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
     const int Q = g.Q, CPR = g.CPR, CPRP = g.CPRP, M = g.M, Mp = g.Mp, S = g.S;
     // staged super-rows: the tile's nv + Q - 1 plus 3 spare rows read only by zero-weight chunks
     const int nrows = nv + Q + 2;
-    uint4 *seg = lds;
+    // LDS: the epilogue's weights (heads, decoder hidden layer, b1, bd1, u, head biases), then
+    // the segment, its row sums and the stream's statistics
+    constexpr int HP = 32 * HB;
+    constexpr int N_WHP = HB * 16 * 64, N_WD1P = HB * 8 * 64;
+    constexpr int N_CONST = N_WHP + N_WD1P + 3 * HP + 32;
+    float *s_whp = reinterpret_cast<float *>(lds);
+    float *s_wd1p = s_whp + N_WHP;
+    float *s_b1 = s_wd1p + N_WD1P;
+    float *s_bd1 = s_b1 + HP;
+    float *s_u = s_bd1 + HP;
+    float *s_bh = s_u + HP;
+    uint4 *seg = lds + N_CONST / 4;
     float *rs = reinterpret_cast<float *>(seg + static_cast<size_t>(NB + Q + 2) * CPRP);
     float *ps = rs + (NB + Q + 2);
     float *smean = ps + (NB + Q + 2);
     float *srinv = smean + Mp;
 
+    {
+        auto copy4 = [&](float *dst, const float *src, int n) {
+            for (int i = tid; i < n / 4; i += kThreads)
+                reinterpret_cast<float4 *>(dst)[i] = reinterpret_cast<const float4 *>(src)[i];
+        };
+        copy4(s_whp, p.whp, N_WHP);
+        copy4(s_wd1p, p.wd1p, N_WD1P);
+        copy4(s_b1, p.b1, HP);
+        copy4(s_bd1, p.bd1, HP);
+        copy4(s_u, p.u, HP);
+        copy4(s_bh, p.bh, 32);
+    }
     for (int m = tid; m < Mp; m += kThreads) {
         if (m < M) {
             smean[m] = p.mean[static_cast<int64_t>(s) * M + m];
@@ -335,52 +360,73 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
     if (!wave_active)
         return;
 
-    // ---- epilogue
+    // ---- epilogue (weights from LDS; the NBW window blocks run as independent MFMA chains)
+    // hidden activations, bias + act one 32-row block at a time, feed the posterior heads:
+    // rows 0..15 mean, 16..31 log-variance
+    v16f z[NBW];
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-        // hidden activations (bias + act, one 32-row block at a time) feed the posterior
-        // heads: rows 0..15 mean, 16..31 log-variance
-        v16f z;
+    for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-            z[r] = 0.0f;
+            z[nb][r] = 0.0f;
 #pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float h = act_fn(acc[hb][nb][r] + p.b1[hb * 32 + crow(r, half)], g.act);
-                z = __builtin_amdgcn_mfma_f32_32x32x2f32(p.whp[(hb * 16 + r) * 64 + lane], h, z, 0, 0, 0);
-            }
-        }
-        float kl = 0.0f;
+    for (int hb = 0; hb < HB; ++hb) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            z[r] += p.bh[crow(r, half)];
-            if (r < 8)
-                kl += z[r] * z[r];
-            else
-                kl += kl_g(z[r]);
-        }
-        kl += __shfl_xor(kl, 32);
-
-        // decoder hidden layer at z = mu, dotted with the column sums of Wd2
-        float dot = 0.0f;
+            const float wv = s_whp[(hb * 16 + r) * 64 + lane];
+            const float bias = s_b1[hb * 32 + crow(r, half)];
 #pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-            v16f d;
+            for (int nb = 0; nb < NBW; ++nb)
+                z[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, act_fn<ACT>(acc[hb][nb][r] + bias),
+                                                             z[nb], 0, 0, 0);
+        }
+    }
+    float kl[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        kl[nb] = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            z[nb][r] += s_bh[crow(r, half)];
+            if (r < 8)
+                kl[nb] += z[nb][r] * z[nb][r];
+            else
+                kl[nb] += kl_g(z[nb][r]);
+        }
+        kl[nb] += __shfl_xor(kl[nb], 32);
+    }
+    // decoder hidden layer at z = mu, dotted with the column sums of Wd2
+    float dot[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+        dot[nb] = 0.0f;
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+        v16f d[NBW];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                d[r] = 0.0f;
+                d[nb][r] = 0.0f;
 #pragma unroll
-            for (int r = 0; r < 8; ++r)
-                d = __builtin_amdgcn_mfma_f32_32x32x2f32(p.wd1p[(hb * 8 + r) * 64 + lane], z[r], d, 0, 0, 0);
+        for (int r = 0; r < 8; ++r) {
+            const float wv = s_wd1p[(hb * 8 + r) * 64 + lane];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int h = hb * 32 + crow(r, half);
-                dot += p.u[h] * act_fn(d[r] + p.bd1[h], g.act);
-            }
+            for (int nb = 0; nb < NBW; ++nb)
+                d[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[nb][r], d[nb], 0, 0, 0);
         }
-        dot += __shfl_xor(dot, 32);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int h = hb * 32 + crow(r, half);
+            const float uh = s_u[h], bh = s_bd1[h];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                dot[nb] += uh * act_fn<ACT>(d[nb][r] + bh);
+        }
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        dot[nb] += __shfl_xor(dot[nb], 32);
 
         // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
         const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
@@ -394,19 +440,58 @@ __global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShap
 
         if (half == 0 && n < nv) {
             const int64_t w = p.woff[s] + k0 + n;
-            const float sc = 0.5f * kl;
+            const float sc = 0.5f * kl[nb];
             p.scores[w] = sc;
             if (p.md)
-                p.md[w] = vsum * g.inv_d - (dot + p.sum_bd2) * g.inv_d;
+                p.md[w] = vsum * g.inv_d - (dot[nb] + p.sum_bd2) * g.inv_d;
             if (p.write_flags)
                 p.flags[w] = sc > p.threshold ? 1 : 0;
         }
     }
 }
 
-template <int DT, int HB, int NBW>
-hipError_t launch_t(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st)
+using ScoreKernel = void (*)(ScoreParams, MfmaShape);
+
+template <int DT, int ACT>
+ScoreKernel pick_hb(int hb)
 {
+    switch (hb) {
+    case 1: return k_score_mfma<DT, 1, 4, ACT>;
+    case 2: return k_score_mfma<DT, 2, 4, ACT>;
+    case 4: return k_score_mfma<DT, 4, 2, ACT>;
+    case 8: return k_score_mfma<DT, 8, 1, ACT>;
+    default: return nullptr;
+    }
+}
+
+// The instantiation for a geometry: storage type, hidden blocks per wave and activation.
+ScoreKernel pick(const Geometry &g)
+{
+    const bool relu = g.act == ENOVA_RELU;
+    if (g.dtype == ENOVA_F32)
+        return relu ? pick_hb<ENOVA_F32, ENOVA_RELU>(g.HB) : pick_hb<ENOVA_F32, ENOVA_TANH>(g.HB);
+    return relu ? pick_hb<ENOVA_BF16, ENOVA_RELU>(g.HB) : pick_hb<ENOVA_BF16, ENOVA_TANH>(g.HB);
+}
+
+}  // namespace
+
+// Allow the chosen instantiation the full 160 KiB of LDS.
+hipError_t prepare_score_mfma(const Geometry &g)
+{
+    ScoreKernel k = pick(g);
+    if (!k)
+        return hipErrorInvalidValue;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               static_cast<int>(kLdsLimit));
+}
+
+hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st)
+{
+    if (grid <= 0)
+        return hipSuccess;
+    ScoreKernel k = pick(g);
+    if (!k)
+        return hipErrorInvalidValue;
     MfmaShape sh;
     sh.M = g.M;
     sh.S = g.S;
@@ -416,57 +501,10 @@ hipError_t launch_t(const Geometry &g, const ScoreParams &p, int64_t grid, hipSt
     sh.CPR = g.CPR;
     sh.CPRP = g.CPRP;
     sh.KC = g.KC;
-    sh.act = g.act;
     sh.tail_rows = g.W - (g.Q - 1) * g.S;
     sh.inv_d = 1.0f / static_cast<float>(g.D);
-    auto kern = k_score_mfma<DT, HB, NBW>;
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(grid)), dim3(kThreads), g.lds_bytes, st, p, sh);
+    hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(grid)), dim3(kThreads), g.lds_bytes, st, p, sh);
     return hipGetLastError();
-}
-
-template <int DT, int HB, int NBW>
-hipError_t prepare_t()
-{
-    return hipFuncSetAttribute(reinterpret_cast<const void *>(k_score_mfma<DT, HB, NBW>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                               static_cast<int>(kLdsLimit));
-}
-
-}  // namespace
-
-// Allow the chosen instantiation the full 160 KiB of LDS.
-hipError_t prepare_score_mfma(const Geometry &g)
-{
-    const bool f = g.dtype == ENOVA_F32;
-    switch (g.HB) {
-    case 1: return f ? prepare_t<ENOVA_F32, 1, 4>() : prepare_t<ENOVA_BF16, 1, 4>();
-    case 2: return f ? prepare_t<ENOVA_F32, 2, 4>() : prepare_t<ENOVA_BF16, 2, 4>();
-    case 4: return f ? prepare_t<ENOVA_F32, 4, 2>() : prepare_t<ENOVA_BF16, 4, 2>();
-    case 8: return f ? prepare_t<ENOVA_F32, 8, 1>() : prepare_t<ENOVA_BF16, 8, 1>();
-    default: return hipErrorInvalidValue;
-    }
-}
-
-hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st)
-{
-    if (grid <= 0)
-        return hipSuccess;
-    if (g.dtype == ENOVA_F32) {
-        switch (g.HB) {
-        case 1: return launch_t<ENOVA_F32, 1, 4>(g, p, grid, st);
-        case 2: return launch_t<ENOVA_F32, 2, 4>(g, p, grid, st);
-        case 4: return launch_t<ENOVA_F32, 4, 2>(g, p, grid, st);
-        case 8: return launch_t<ENOVA_F32, 8, 1>(g, p, grid, st);
-        default: return hipErrorInvalidValue;
-        }
-    }
-    switch (g.HB) {
-    case 1: return launch_t<ENOVA_BF16, 1, 4>(g, p, grid, st);
-    case 2: return launch_t<ENOVA_BF16, 2, 4>(g, p, grid, st);
-    case 4: return launch_t<ENOVA_BF16, 4, 2>(g, p, grid, st);
-    case 8: return launch_t<ENOVA_BF16, 8, 1>(g, p, grid, st);
-    default: return hipErrorInvalidValue;
-    }
 }
 
 // NBW (32-window blocks per wave) that goes with each hidden-block count HB.
