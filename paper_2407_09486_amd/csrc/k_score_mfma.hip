@@ -101,7 +101,7 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u 
 __device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
 template <int DT, int HB, int NBW, int ACT>
-__global__ __launch_bounds__(kThreads) void k_score_mfma(ScoreParams p, MfmaShape g)
+__global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_mfma(ScoreParams p, MfmaShape g)
 {
     constexpr int NB = kWaves * NBW * 32;         // windows per tile
     constexpr int EPC = DT == ENOVA_F32 ? 4 : 8;  // elements per 16-byte chunk
