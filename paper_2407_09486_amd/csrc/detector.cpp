@@ -15,7 +15,7 @@
 #include "internal.h"
 
 namespace enova {
-int mfma_nbw_for(int hb);
+void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh);
 hipError_t prepare_score_mfma(const Geometry &g);
 }  // namespace enova
 
@@ -123,20 +123,24 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     g->CPR = static_cast<int>(cpr);
     g->CPRP = (g->CPR % 2 == 0) ? g->CPR + 1 : g->CPR;
     int64_t kc = static_cast<int64_t>(g->Q) * g->CPR;
-    kc = (kc + 3) / 4 * 4;        // an even number of two-chunk steps
+    kc = (kc + 7) / 8 * 8;        // a multiple of 4 two-chunk steps (the prefetch ring depth)
     g->KC = static_cast<int>(kc);
     int hb = 1;
     while (hb < 8 && 32 * hb < g->H)
         hb *= 2;
     g->HB = hb;
     g->Hp = 32 * hb;
-    g->NBW = mfma_nbw_for(hb);
-    g->Nb = kWaves * g->NBW * 32;
+    mfma_layout(g->dtype, hb, &g->HBW, &g->NBW, &g->WH);
+    g->Nb = (kWaves / g->WH) * g->NBW * 32;
     // epilogue weights (heads, decoder hidden layer, b1, bd1, u, head biases), the segment, its
     // row sums and the stream statistics
     const size_t n_const = static_cast<size_t>(hb) * (16 * 64 + 8 * 64) + 3 * static_cast<size_t>(g->Hp) + 32;
-    g->lds_bytes = n_const * sizeof(float) + static_cast<size_t>(g->Nb + g->Q + 2) * g->CPRP * 16 +
-                   static_cast<size_t>(g->Nb + g->Q + 2) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
+    // with several waves along the hidden rows, the segment's space later holds the exchange of
+    // head and decoder partial sums
+    const size_t seg_bytes = static_cast<size_t>(g->Nb + g->Q + kSpareRows - 1) * g->CPRP * 16;
+    const size_t xchg_bytes = g->WH > 1 ? static_cast<size_t>(kWaves) * g->NBW * 17 * 64 * sizeof(float) : 0;
+    g->lds_bytes = n_const * sizeof(float) + std::max(seg_bytes, xchg_bytes) +
+                   static_cast<size_t>(g->Nb + g->Q + kSpareRows - 1) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;
     if (!g->mfma_ok) {
@@ -435,8 +439,9 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
         st = dev_upload(&d->w1t, wt.data(), wt.size());
     } else {
         // A fragments: step i, hidden block hb, lane -> 16 bytes of W1[h][chunk 2i + lane/32]
+        // kPrefetchSteps zero steps follow the last one: the kernel's W1 prefetch runs past it
         const int steps = g.KC / 2;
-        const size_t frag = static_cast<size_t>(steps) * g.HB * 64;
+        const size_t frag = static_cast<size_t>(steps + kPrefetchSteps) * g.HB * 64;
         std::vector<uint32_t> pk(frag * 4, 0u);
         for (int i = 0; i < steps; ++i)
             for (int hb = 0; hb < g.HB; ++hb)

@@ -31,9 +31,11 @@ struct Geometry {
     int CPRP;               // LDS row pitch in chunks (odd, so 16 consecutive rows hit distinct banks)
     int KC;                 // chunks per window, rounded up to a multiple of 4
     int Hp;                 // hidden width padded to 32*HB
-    int HB;                 // 32-row hidden blocks per wave
+    int HB;                 // 32-row hidden blocks of the tile (Hp = 32*HB)
+    int HBW;                // hidden blocks per wave
     int NBW;                // 32-window blocks per wave
-    int Nb;                 // windows per tile (4 waves)
+    int WH;                 // waves along the hidden rows (4/WH along the windows)
+    int Nb;                 // windows per tile
     size_t lds_bytes;       // dynamic LDS of the matrix-core kernel
     bool mfma_ok;
 };
@@ -41,6 +43,12 @@ struct Geometry {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr size_t kLdsLimit = 160 * 1024;
+// The reduction index is padded to a multiple of 8 chunks (4 two-chunk steps, the deepest
+// W1 prefetch ring of the matrix-core kernel); the packed W1 carries kPrefetchSteps zero steps
+// after the last one, and kSpareRows staged super-rows follow a tile's windows, so that the
+// padded chunks and the prefetch of the step after the last read valid memory.
+constexpr int kPrefetchSteps = 4;
+constexpr int kSpareRows = 9;
 
 bool plan_geometry(const enova_detect_config &cfg, Geometry *g);
 

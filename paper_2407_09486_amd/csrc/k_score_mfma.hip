@@ -100,10 +100,17 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u 
 // Row of the accumulator register r for lane half g inside a 32x32 block.
 __device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
-template <int DT, int HB, int NBW, int ACT>
-__global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_mfma(ScoreParams p, MfmaShape g)
+// Wave layout: the 4 waves form WH groups along the hidden rows and kWaves/WH groups along the
+// windows. A wave owns HB 32-row hidden blocks and NBW 32-window blocks; with WH > 1 the waves
+// of a window group share its B fragments and their posterior-head partial sums are reduced
+// through LDS.
+template <int DT, int HB, int NBW, int WH, int ACT>
+__global__ __launch_bounds__(kThreads, (ACT == ENOVA_RELU && WH == 1) ? 2 : 1)
+void k_score_mfma(ScoreParams p, MfmaShape g)
 {
-    constexpr int NB = kWaves * NBW * 32;         // windows per tile
+    constexpr int WN = kWaves / WH;               // window groups
+    constexpr int HBT = HB * WH;                  // hidden blocks of the tile
+    constexpr int NB = WN * NBW * 32;             // windows per tile
     constexpr int EPC = DT == ENOVA_F32 ? 4 : 8;  // elements per 16-byte chunk
     extern __shared__ uint4 lds[];
 
@@ -111,6 +118,8 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int half = lane >> 5;
+    const int wh = wave % WH;                     // hidden-row group of this wave
+    const int wn = wave / WH;                     // window group of this wave
 
     // ---- tile -> (stream, first window)
     const int64_t b = blockIdx.x;
@@ -125,13 +134,15 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
     const int64_t T = p.soff[s + 1] - srow;
 
     const int Q = g.Q, CPR = g.CPR, CPRP = g.CPRP, M = g.M, Mp = g.Mp, S = g.S;
-    // staged super-rows: the tile's nv + Q - 1 plus 3 spare rows read only by zero-weight chunks
-    const int nrows = nv + Q + 2;
+    // staged super-rows: the tile's nv + Q - 1 plus spare rows read only by zero-weight chunks
+    const int nrows = nv + Q + kSpareRows - 1;
     // LDS: the epilogue's weights (heads, decoder hidden layer, b1, bd1, u, head biases), then
     // the segment, its row sums and the stream's statistics
-    constexpr int HP = 32 * HB;
-    constexpr int N_WHP = HB * 16 * 64, N_WD1P = HB * 8 * 64;
+    // (with WH > 1 the segment's space is reused after the main loop to exchange partial sums)
+    constexpr int HP = 32 * HBT;
+    constexpr int N_WHP = HBT * 16 * 64, N_WD1P = HBT * 8 * 64;
     constexpr int N_CONST = N_WHP + N_WD1P + 3 * HP + 32;
+    constexpr int N_XCHG = WH > 1 ? kWaves * NBW * (16 + 1) * 64 : 0;   // floats
     float *s_whp = reinterpret_cast<float *>(lds);
     float *s_wd1p = s_whp + N_WHP;
     float *s_b1 = s_wd1p + N_WD1P;
@@ -139,9 +150,11 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
     float *s_u = s_bd1 + HP;
     float *s_bh = s_u + HP;
     uint4 *seg = lds + N_CONST / 4;
-    float *rs = reinterpret_cast<float *>(seg + static_cast<size_t>(NB + Q + 2) * CPRP);
-    float *ps = rs + (NB + Q + 2);
-    float *smean = ps + (NB + Q + 2);
+    const size_t seg_chunks = static_cast<size_t>(NB + Q + kSpareRows - 1) * CPRP;
+    const size_t seg_span = seg_chunks > N_XCHG / 4 ? seg_chunks : N_XCHG / 4;
+    float *rs = reinterpret_cast<float *>(seg + seg_span);
+    float *ps = rs + (NB + Q + kSpareRows - 1);
+    float *smean = ps + (NB + Q + kSpareRows - 1);
     float *srinv = smean + Mp;
 
     {
@@ -267,7 +280,7 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
     int rb[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
-        const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
+        const int n = wn * NBW * 32 + nb * 32 + (lane & 31);
         rb[nb] = (n < nv ? n : nv - 1) * CPRP;   // idle columns re-read a valid window
     }
     v16f acc[HB][NBW];
@@ -279,16 +292,15 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
             for (int r = 0; r < 16; ++r)
                 acc[hb][nb][r] = 0.0f;
 
-    const bool wave_active = wave * NBW * 32 < nv;
+    const bool wave_active = wn * NBW * 32 < nv;
     const int nsteps = g.KC / 2;                 // even: KC is a multiple of 4
-    const uint4 *ap = p.w1p + lane;
+    // A fragments of step i: w1p[(i * HBT + hb) * 64 + lane]; this wave's blocks start at wh * HB
+    const uint4 *ap = p.w1p + wh * HB * 64 + lane;
     // LDS chunk offset of this lane's chunk kappa = 2*i + half inside a window:
     // (kappa / CPR) * CPRP + kappa % CPR, advanced without branches
     const int dpitch = CPRP - CPR;
     int cc = half % CPR;
     int koff = (half / CPR) * CPRP + cc;
-    const int klast = 2 * (nsteps - 1) + half;
-    const int koff_max = (klast / CPR) * CPRP + klast % CPR;
     auto advance = [&]() {
         const bool wrap = cc + 2 >= CPR;
         cc = cc + 2 - (wrap ? CPR : 0);
@@ -323,46 +335,49 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
     };
     __syncthreads();
     if (wave_active) {
-        // ping-pong operand buffers, each step's operands fetched one step ahead
-        uint4 a0[HB], a1[HB], b0[NBW], b1[NBW];
+        // W1 fragments run PD steps ahead in a register ring (an fp32 step is 4*HB*NBW matrix
+        // ops, a bf16 step only HB*NBW, so bf16 needs the deeper ring to cover an L2 round
+        // trip); window fragments run one step ahead from LDS. The loop is unrolled by PD so
+        // every ring slot is a compile-time register set.
+        constexpr int PD = DT == ENOVA_F32 ? 2 : 4;
+        uint4 a[PD][HB], b[2][NBW];
 #pragma unroll
-        for (int hb = 0; hb < HB; ++hb)
-            a0[hb] = ap[hb * 64];
+        for (int j = 0; j < PD; ++j)
+#pragma unroll
+            for (int hb = 0; hb < HB; ++hb)
+                a[j][hb] = ap[(j * HBT + hb) * 64];
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
-            b0[nb] = seg[rb[nb] + koff];
-        for (int i = 0; i < nsteps; i += 2) {
-            advance();
+            b[0][nb] = seg[rb[nb] + koff];
+        // Prefetches past the last step read the zero steps the host appends to the packed W1
+        // and the spare LDS rows, so no index needs clamping.
+        const uint4 *api = ap + PD * HBT * 64;
+        for (int i = 0; i < nsteps; i += PD) {
 #pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
-                a1[hb] = ap[((i + 1) * HB + hb) * 64];
+            for (int j = 0; j < PD; ++j) {
+                advance();
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                b1[nb] = seg[rb[nb] + koff];
-            // keep the prefetch ahead of this step's matrix ops (the scheduler would sink it)
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            advance();
-            const int inext = i + 2 < nsteps ? i + 2 : nsteps - 1;
-            const int kn = koff < koff_max ? koff : koff_max;
+                for (int nb = 0; nb < NBW; ++nb)
+                    b[(j + 1) & 1][nb] = seg[rb[nb] + koff];
+                // keep the prefetches ahead of this step's matrix ops (the scheduler would sink them)
+                __builtin_amdgcn_sched_barrier(0);
+                mma(a[j], b[j & 1]);
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
-                a0[hb] = ap[(inext * HB + hb) * 64];
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                b0[nb] = seg[rb[nb] + kn];
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
+                for (int hb = 0; hb < HB; ++hb)
+                    a[j][hb] = api[(j * HBT + hb) * 64];
+            }
+            api += PD * HBT * 64;
         }
     }
-    if (!wave_active)
-        return;
+    if constexpr (WH == 1) {
+        if (!wave_active)
+            return;
+    }
 
     // ---- epilogue (weights from LDS; the NBW window blocks run as independent MFMA chains)
     // hidden activations, bias + act one 32-row block at a time, feed the posterior heads:
-    // rows 0..15 mean, 16..31 log-variance
+    // rows 0..15 mean, 16..31 log-variance (this wave's share of the hidden rows)
     v16f z[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb)
@@ -371,15 +386,38 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
             z[nb][r] = 0.0f;
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) {
+        const int hbg = wh * HB + hb;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const float wv = s_whp[(hb * 16 + r) * 64 + lane];
-            const float bias = s_b1[hb * 32 + crow(r, half)];
+            const float wv = s_whp[(hbg * 16 + r) * 64 + lane];
+            const float bias = s_b1[hbg * 32 + crow(r, half)];
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
                 z[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, act_fn<ACT>(acc[hb][nb][r] + bias),
                                                              z[nb], 0, 0, 0);
         }
+    }
+    float *xz = reinterpret_cast<float *>(seg);            // [kWaves][NBW][16][64] head partials
+    float *xd = xz + kWaves * NBW * 16 * 64;               // [kWaves][NBW][64] decoder partials
+    if constexpr (WH > 1) {
+        // every wave of the window group adds the WH partials in the same fixed order
+        __syncthreads();                                   // the segment is no longer read
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                xz[((wave * NBW + nb) * 16 + r) * 64 + lane] = z[nb][r];
+        __syncthreads();
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float t = 0.0f;
+#pragma unroll
+                for (int w2 = 0; w2 < WH; ++w2)
+                    t += xz[(((wn * WH + w2) * NBW + nb) * 16 + r) * 64 + lane];
+                z[nb][r] = t;
+            }
     }
     float kl[NBW];
 #pragma unroll
@@ -402,6 +440,7 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
         dot[nb] = 0.0f;
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) {
+        const int hbg = wh * HB + hb;
         v16f d[NBW];
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
@@ -410,18 +449,34 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
                 d[nb][r] = 0.0f;
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-            const float wv = s_wd1p[(hb * 8 + r) * 64 + lane];
+            const float wv = s_wd1p[(hbg * 8 + r) * 64 + lane];
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
                 d[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[nb][r], d[nb], 0, 0, 0);
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int h = hb * 32 + crow(r, half);
+            const int h = hbg * 32 + crow(r, half);
             const float uh = s_u[h], bh = s_bd1[h];
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb)
                 dot[nb] += uh * act_fn<ACT>(d[nb][r] + bh);
+        }
+    }
+    if constexpr (WH > 1) {
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+            xd[(wave * NBW + nb) * 64 + lane] = dot[nb];
+        __syncthreads();
+        if (wh != 0 || !wave_active)
+            return;
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+            float t = 0.0f;
+#pragma unroll
+            for (int w2 = 0; w2 < WH; ++w2)
+                t += xd[((wn * WH + w2) * NBW + nb) * 64 + lane];
+            dot[nb] = t;
         }
     }
 #pragma unroll
@@ -429,7 +484,7 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
         dot[nb] += __shfl_xor(dot[nb], 32);
 
         // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
-        const int n = wave * NBW * 32 + nb * 32 + (lane & 31);
+        const int n = wn * NBW * 32 + nb * 32 + (lane & 31);
         float vsum = 0.0f;
         const int row0 = rb[nb] / CPRP;
         for (int qq = half; qq < Q - 1; qq += 2)
@@ -453,24 +508,37 @@ __global__ __launch_bounds__(kThreads, ACT == ENOVA_RELU ? 2 : 1) void k_score_m
 using ScoreKernel = void (*)(ScoreParams, MfmaShape);
 
 template <int DT, int ACT>
-ScoreKernel pick_hb(int hb)
+ScoreKernel pick_layout(int hbw, int nbw, int wh)
 {
-    switch (hb) {
-    case 1: return k_score_mfma<DT, 1, 4, ACT>;
-    case 2: return k_score_mfma<DT, 2, 4, ACT>;
-    case 4: return k_score_mfma<DT, 4, 2, ACT>;
-    case 8: return k_score_mfma<DT, 8, 1, ACT>;
-    default: return nullptr;
+    if (wh == 1) {
+        switch (hbw) {
+        case 1: return nbw == 4 ? k_score_mfma<DT, 1, 4, 1, ACT> : nullptr;
+        case 2: return nbw == 4 ? k_score_mfma<DT, 2, 4, 1, ACT> : nullptr;
+        case 4: return nbw == 2 ? k_score_mfma<DT, 4, 2, 1, ACT> : nullptr;
+        case 8:   // bf16 with eight hidden blocks uses the four-wave split below
+            if constexpr (DT == ENOVA_F32)
+                return nbw == 1 ? k_score_mfma<DT, 8, 1, 1, ACT> : nullptr;
+            else
+                return nullptr;
+        default: return nullptr;
+        }
     }
+    if (wh == 2 && hbw == 4 && nbw == 2)
+        return k_score_mfma<DT, 4, 2, 2, ACT>;
+    if (wh == 4 && hbw == 2 && nbw == 4)
+        return k_score_mfma<DT, 2, 4, 4, ACT>;
+    return nullptr;
 }
 
-// The instantiation for a geometry: storage type, hidden blocks per wave and activation.
+// The instantiation for a geometry: storage type, wave layout and activation.
 ScoreKernel pick(const Geometry &g)
 {
     const bool relu = g.act == ENOVA_RELU;
     if (g.dtype == ENOVA_F32)
-        return relu ? pick_hb<ENOVA_F32, ENOVA_RELU>(g.HB) : pick_hb<ENOVA_F32, ENOVA_TANH>(g.HB);
-    return relu ? pick_hb<ENOVA_BF16, ENOVA_RELU>(g.HB) : pick_hb<ENOVA_BF16, ENOVA_TANH>(g.HB);
+        return relu ? pick_layout<ENOVA_F32, ENOVA_RELU>(g.HBW, g.NBW, g.WH)
+                    : pick_layout<ENOVA_F32, ENOVA_TANH>(g.HBW, g.NBW, g.WH);
+    return relu ? pick_layout<ENOVA_BF16, ENOVA_RELU>(g.HBW, g.NBW, g.WH)
+                : pick_layout<ENOVA_BF16, ENOVA_TANH>(g.HBW, g.NBW, g.WH);
 }
 
 }  // namespace
@@ -508,15 +576,19 @@ hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t gr
 }
 
 // NBW (32-window blocks per wave) that goes with each hidden-block count HB.
-int mfma_nbw_for(int hb)
+void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh)
 {
-    switch (hb) {
-    case 1: return 4;
-    case 2: return 4;
-    case 4: return 2;
-    case 8: return 1;
-    default: return 0;
+    if (dtype == ENOVA_BF16 && hb == 8) {
+        // bf16 matrix ops are 4x faster than fp32 ones: a (HB=8, NBW=1) wave tile would need
+        // 8 KiB of W1 per 8 MFMAs. Four waves split the hidden rows and share the windows.
+        *hbw = 2;
+        *nbw = 4;
+        *wh = 4;
+        return;
     }
+    *wh = 1;
+    *hbw = hb;
+    *nbw = hb <= 2 ? 4 : (hb == 4 ? 2 : 1);
 }
 
 }  // namespace enova
