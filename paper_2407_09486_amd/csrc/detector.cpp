@@ -123,8 +123,11 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     g->CPR = static_cast<int>(cpr);
     g->CPRP = (g->CPR % 2 == 0) ? g->CPR + 1 : g->CPR;
     int64_t kc = static_cast<int64_t>(g->Q) * g->CPR;
-    kc = (kc + 7) / 8 * 8;        // a multiple of 4 two-chunk steps (the prefetch ring depth)
+    kc = (kc + 2 * kPrefetchSteps - 1) / (2 * kPrefetchSteps) * (2 * kPrefetchSteps);
     g->KC = static_cast<int>(kc);
+    // the furthest chunk a window fragment prefetch reads: kPrefetchRows steps past the last
+    const int64_t kmax = kc + 2 * kPrefetchRows - 1;
+    g->spare = static_cast<int>(kmax / g->CPR - g->Q + 2);
     int hb = 1;
     while (hb < 8 && 32 * hb < g->H)
         hb *= 2;
@@ -137,10 +140,13 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     const size_t n_const = static_cast<size_t>(hb) * (16 * 64 + 8 * 64) + 3 * static_cast<size_t>(g->Hp) + 32;
     // with several waves along the hidden rows, the segment's space later holds the exchange of
     // head and decoder partial sums
-    const size_t seg_bytes = static_cast<size_t>(g->Nb + g->Q + kSpareRows - 1) * g->CPRP * 16;
-    const size_t xchg_bytes = g->WH > 1 ? static_cast<size_t>(kWaves) * g->NBW * 17 * 64 * sizeof(float) : 0;
-    g->lds_bytes = n_const * sizeof(float) + std::max(seg_bytes, xchg_bytes) +
-                   static_cast<size_t>(g->Nb + g->Q + kSpareRows - 1) * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
+    const size_t rows = static_cast<size_t>(g->Nb + g->Q - 1 + g->spare);
+    const size_t seg_bytes = rows * g->CPRP * 16;
+    const size_t xchg_bytes = g->WH > 1 ? static_cast<size_t>(kWaves) * std::min(g->NBW, 2) * 17 * 64 * sizeof(float) : 0;
+    // the split bf16 layout keeps its epilogue weights in L2 to leave LDS to a 256-window tile
+    g->cl = g->WH == 1;
+    g->lds_bytes = (g->cl ? n_const * sizeof(float) : 0) + std::max(seg_bytes, xchg_bytes) +
+                   rows * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;
     if (!g->mfma_ok) {
@@ -347,6 +353,9 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
         o += (n + 3) / 4 * 4;
         return at;
     };
+    // the matrix-core kernel copies whp, wd1p, b1, bd1, u, bh as one contiguous block into LDS
+    const size_t o_whp = take(n_whp);
+    const size_t o_wd1p = take(n_wd1p);
     const size_t o_b1 = take(Hp);
     const size_t o_bd1 = take(Hp);
     const size_t o_u = take(Hp);
@@ -356,8 +365,6 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
     const size_t o_wmu = take(static_cast<size_t>(L) * H);
     const size_t o_wlv = take(static_cast<size_t>(L) * H);
     const size_t o_wd1 = take(static_cast<size_t>(H) * L);
-    const size_t o_whp = take(n_whp);
-    const size_t o_wd1p = take(n_wd1p);
     std::vector<float> small(o, 0.0f);
 
     for (int h = 0; h < H; ++h) {

@@ -29,12 +29,14 @@ struct Geometry {
     int Q;                  // super-rows per window
     int CPR;                // chunks per super-row
     int CPRP;               // LDS row pitch in chunks (odd, so 16 consecutive rows hit distinct banks)
-    int KC;                 // chunks per window, rounded up to a multiple of 4
+    int KC;                 // chunks per window, rounded up to a multiple of 2*kPrefetchSteps
+    int spare;              // staged super-rows after a tile's last window's Q - 1
     int Hp;                 // hidden width padded to 32*HB
     int HB;                 // 32-row hidden blocks of the tile (Hp = 32*HB)
     int HBW;                // hidden blocks per wave
     int NBW;                // 32-window blocks per wave
     int WH;                 // waves along the hidden rows (4/WH along the windows)
+    bool cl;                // epilogue weights staged in LDS (else read from L2)
     int Nb;                 // windows per tile
     size_t lds_bytes;       // dynamic LDS of the matrix-core kernel
     bool mfma_ok;
@@ -43,12 +45,13 @@ struct Geometry {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr size_t kLdsLimit = 160 * 1024;
-// The reduction index is padded to a multiple of 8 chunks (4 two-chunk steps, the deepest
-// W1 prefetch ring of the matrix-core kernel); the packed W1 carries kPrefetchSteps zero steps
-// after the last one, and kSpareRows staged super-rows follow a tile's windows, so that the
-// padded chunks and the prefetch of the step after the last read valid memory.
-constexpr int kPrefetchSteps = 4;
-constexpr int kSpareRows = 9;
+// The reduction index is padded to a multiple of 2*kPrefetchSteps chunks (the matrix-core
+// kernel's deepest W1 prefetch ring, in two-chunk steps); the packed W1 carries kPrefetchSteps
+// zero steps after the last one, and Geometry::spare staged super-rows follow a tile's windows
+// (enough for the padded chunks and kPrefetchRows steps of window-fragment prefetch), so every
+// prefetch past the last step reads valid memory.
+constexpr int kPrefetchSteps = 8;
+constexpr int kPrefetchRows = 2;
 
 bool plan_geometry(const enova_detect_config &cfg, Geometry *g);
 

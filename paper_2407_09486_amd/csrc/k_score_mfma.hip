@@ -33,6 +33,7 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 struct MfmaShape {
     int M, S, W, Mp, Q, CPR, CPRP, KC;
+    int spare;       // staged super-rows after a tile's last window's Q - 1
     int tail_rows;   // steps of the window's last super-row that belong to the window
     float inv_d;
 };
@@ -104,7 +105,9 @@ __device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g 
 // windows. A wave owns HB 32-row hidden blocks and NBW 32-window blocks; with WH > 1 the waves
 // of a window group share its B fragments and their posterior-head partial sums are reduced
 // through LDS.
-template <int DT, int HB, int NBW, int WH, int ACT>
+// CL: the epilogue weights are copied into LDS with each tile (else read from L2, leaving the
+// LDS to a larger segment).
+template <int DT, int HB, int NBW, int WH, int ACT, bool CL>
 __global__ __launch_bounds__(kThreads, (ACT == ENOVA_RELU && WH == 1) ? 2 : 1)
 void k_score_mfma(ScoreParams p, MfmaShape g)
 {
@@ -135,14 +138,14 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 
     const int Q = g.Q, CPR = g.CPR, CPRP = g.CPRP, M = g.M, Mp = g.Mp, S = g.S;
     // staged super-rows: the tile's nv + Q - 1 plus spare rows read only by zero-weight chunks
-    const int nrows = nv + Q + kSpareRows - 1;
+    const int nrows = nv + Q - 1 + g.spare;
     // LDS: the epilogue's weights (heads, decoder hidden layer, b1, bd1, u, head biases), then
     // the segment, its row sums and the stream's statistics
     // (with WH > 1 the segment's space is reused after the main loop to exchange partial sums)
     constexpr int HP = 32 * HBT;
     constexpr int N_WHP = HBT * 16 * 64, N_WD1P = HBT * 8 * 64;
-    constexpr int N_CONST = N_WHP + N_WD1P + 3 * HP + 32;
-    constexpr int N_XCHG = WH > 1 ? kWaves * NBW * (16 + 1) * 64 : 0;   // floats
+    constexpr int N_CONST = CL ? N_WHP + N_WD1P + 3 * HP + 32 : 0;
+    constexpr int N_XCHG = WH > 1 ? kWaves * (NBW > 2 ? 2 : NBW) * (16 + 1) * 64 : 0;   // floats
     float *s_whp = reinterpret_cast<float *>(lds);
     float *s_wd1p = s_whp + N_WHP;
     float *s_b1 = s_wd1p + N_WD1P;
@@ -150,24 +153,33 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     float *s_u = s_bd1 + HP;
     float *s_bh = s_u + HP;
     uint4 *seg = lds + N_CONST / 4;
-    const size_t seg_chunks = static_cast<size_t>(NB + Q + kSpareRows - 1) * CPRP;
+    const int rows_alloc = NB + Q - 1 + g.spare;
+    const size_t seg_chunks = static_cast<size_t>(rows_alloc) * CPRP;
     const size_t seg_span = seg_chunks > N_XCHG / 4 ? seg_chunks : N_XCHG / 4;
     float *rs = reinterpret_cast<float *>(seg + seg_span);
-    float *ps = rs + (NB + Q + kSpareRows - 1);
-    float *smean = ps + (NB + Q + kSpareRows - 1);
+    float *ps = rs + rows_alloc;
+    float *smean = ps + rows_alloc;
     float *srinv = smean + Mp;
 
-    {
-        auto copy4 = [&](float *dst, const float *src, int n) {
-            for (int i = tid; i < n / 4; i += kThreads)
-                reinterpret_cast<float4 *>(dst)[i] = reinterpret_cast<const float4 *>(src)[i];
-        };
-        copy4(s_whp, p.whp, N_WHP);
-        copy4(s_wd1p, p.wd1p, N_WD1P);
-        copy4(s_b1, p.b1, HP);
-        copy4(s_bd1, p.bd1, HP);
-        copy4(s_u, p.u, HP);
-        copy4(s_bh, p.bh, 32);
+    if constexpr (CL) {
+        // the host lays the epilogue weights out contiguously in this LDS order; copy them with
+        // several 16-byte loads in flight per thread
+        constexpr int N4 = N_CONST / 4;
+        constexpr int CU = 4;
+        const float4 *src = reinterpret_cast<const float4 *>(p.whp);
+        float4 *dst = reinterpret_cast<float4 *>(s_whp);
+        constexpr int FULL = N4 / (kThreads * CU) * (kThreads * CU);
+        for (int base = tid; base < FULL; base += kThreads * CU) {
+            float4 t[CU];
+#pragma unroll
+            for (int u = 0; u < CU; ++u)
+                t[u] = src[base + u * kThreads];
+#pragma unroll
+            for (int u = 0; u < CU; ++u)
+                dst[base + u * kThreads] = t[u];
+        }
+        for (int i = FULL + tid; i < N4; i += kThreads)
+            dst[i] = src[i];
     }
     for (int m = tid; m < Mp; m += kThreads) {
         if (m < M) {
@@ -186,28 +198,48 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     const bool linear = (Mp == M) && (((srow + step0) * M) % EPC == 0);
     const int64_t ebase = (srow + step0) * M;      // element index of super-row 0
     const int64_t eend = (srow + T) * M;           // one past the stream's last element
-    for (int idx = tid; idx < nrows * CPR; idx += kThreads) {
+    // Each thread keeps SU chunk loads in flight before normalising them (one load per loop
+    // trip would serialise a full HBM round trip per chunk).
+    constexpr int SU = 8;
+    const int n_chunks = nrows * CPR;
+    for (int base = tid; base < n_chunks; base += kThreads * SU) {
+      uint4 raw[SU];
+      bool vec[SU];
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        const int idx = base + u * kThreads;
+        vec[u] = idx < n_chunks && linear && ebase + static_cast<int64_t>(idx + 1) * EPC <= eend;
+        if (vec[u]) {
+            const int64_t e0 = ebase + static_cast<int64_t>(idx) * EPC;
+            if constexpr (DT == ENOVA_F32)
+                raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(p.x) + e0);
+            else
+                raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.x) + e0);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        const int idx = base + u * kThreads;
+        if (idx >= n_chunks)
+            continue;
         const int r = idx / CPR;
         const int c = idx - r * CPR;
         float v[EPC];
-        if (linear && ebase + static_cast<int64_t>(idx + 1) * EPC <= eend) {
-            const int64_t e0 = ebase + static_cast<int64_t>(idx) * EPC;
+        if (vec[u]) {
             if constexpr (DT == ENOVA_F32) {
-                const float4 raw = *reinterpret_cast<const float4 *>(static_cast<const float *>(p.x) + e0);
-                v[0] = raw.x;
-                v[1] = raw.y;
-                v[2] = raw.z;
-                v[3] = raw.w;
+                v[0] = __uint_as_float(raw[u].x);
+                v[1] = __uint_as_float(raw[u].y);
+                v[2] = __uint_as_float(raw[u].z);
+                v[3] = __uint_as_float(raw[u].w);
             } else {
-                const uint4 raw = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.x) + e0);
-                v[0] = bf16_lo(raw.x);
-                v[1] = bf16_hi(raw.x);
-                v[2] = bf16_lo(raw.y);
-                v[3] = bf16_hi(raw.y);
-                v[4] = bf16_lo(raw.z);
-                v[5] = bf16_hi(raw.z);
-                v[6] = bf16_lo(raw.w);
-                v[7] = bf16_hi(raw.w);
+                v[0] = bf16_lo(raw[u].x);
+                v[1] = bf16_hi(raw[u].x);
+                v[2] = bf16_lo(raw[u].y);
+                v[3] = bf16_hi(raw[u].y);
+                v[4] = bf16_lo(raw[u].z);
+                v[5] = bf16_hi(raw[u].z);
+                v[6] = bf16_lo(raw[u].w);
+                v[7] = bf16_hi(raw[u].w);
             }
 #pragma unroll
             for (int e = 0; e < EPC; ++e) {
@@ -240,6 +272,7 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
             out.w = pack_bf16x2(v[6], v[7]);
         }
         seg[r * CPRP + c] = out;
+      }
     }
     __syncthreads();
 
@@ -335,33 +368,42 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     };
     __syncthreads();
     if (wave_active) {
-        // W1 fragments run PD steps ahead in a register ring (an fp32 step is 4*HB*NBW matrix
-        // ops, a bf16 step only HB*NBW, so bf16 needs the deeper ring to cover an L2 round
-        // trip); window fragments run one step ahead from LDS. The loop is unrolled by PD so
-        // every ring slot is a compile-time register set.
-        constexpr int PD = DT == ENOVA_F32 ? 2 : 4;
-        uint4 a[PD][HB], b[2][NBW];
+        // W1 fragments run PD steps ahead in a register ring, window fragments PB steps ahead
+        // (ring of 2*PB) from LDS: an fp32 step is 4*HB*NBW matrix ops, a bf16 step only
+        // HB*NBW, so bf16 needs the deeper rings to cover an L2 round trip. The loop is unrolled
+        // by PD so every ring slot is a compile-time register set.
+        // (bf16 with one wave per hidden group runs two waves per SIMD, and four hidden blocks
+        // per wave hold 16 registers per step: a shallower ring for both)
+        constexpr int PD = DT == ENOVA_F32 ? 2 : ((WH == 1 || HB >= 4) ? 4 : 8);
+        constexpr int PB = DT == ENOVA_F32 ? 1 : 2;
+        constexpr int RB = 2 * PB;
+        static_assert(PD % RB == 0 && PD <= kPrefetchSteps && PB <= kPrefetchRows, "prefetch rings");
+        uint4 a[PD][HB], b[RB][NBW];
 #pragma unroll
         for (int j = 0; j < PD; ++j)
 #pragma unroll
             for (int hb = 0; hb < HB; ++hb)
                 a[j][hb] = ap[(j * HBT + hb) * 64];
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-            b[0][nb] = seg[rb[nb] + koff];
-        // Prefetches past the last step read the zero steps the host appends to the packed W1
-        // and the spare LDS rows, so no index needs clamping.
+        for (int j = 0; j < PB; ++j) {
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                b[j][nb] = seg[rb[nb] + koff];
+            advance();
+        }
+        // koff now points PB steps ahead. Prefetches past the last step read the zero steps the
+        // host appends to the packed W1 and the spare LDS rows, so no index needs clamping.
         const uint4 *api = ap + PD * HBT * 64;
         for (int i = 0; i < nsteps; i += PD) {
 #pragma unroll
             for (int j = 0; j < PD; ++j) {
-                advance();
 #pragma unroll
                 for (int nb = 0; nb < NBW; ++nb)
-                    b[(j + 1) & 1][nb] = seg[rb[nb] + koff];
+                    b[(j + PB) % RB][nb] = seg[rb[nb] + koff];
+                advance();
                 // keep the prefetches ahead of this step's matrix ops (the scheduler would sink them)
                 __builtin_amdgcn_sched_barrier(0);
-                mma(a[j], b[j & 1]);
+                mma(a[j], b[j % RB]);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int hb = 0; hb < HB; ++hb)
@@ -375,132 +417,138 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
             return;
     }
 
-    // ---- epilogue (weights from LDS; the NBW window blocks run as independent MFMA chains)
-    // hidden activations, bias + act one 32-row block at a time, feed the posterior heads:
-    // rows 0..15 mean, 16..31 log-variance (this wave's share of the hidden rows)
-    v16f z[NBW];
+    // ---- epilogue, NG window blocks per pass (weights from LDS, or L2 when the segment needs
+    // the LDS); the NG blocks of a pass run as independent MFMA chains
+    constexpr int NG = NBW > 2 ? 2 : NBW;
+    float *xz = reinterpret_cast<float *>(seg);            // [kWaves][NG][16][64] head partials
+    float *xd = xz + kWaves * NG * 16 * 64;                // [kWaves][NG][64] decoder partials
+    const bool storer = WH == 1 || (wh == 0 && wave_active);
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb)
+    for (int g0 = 0; g0 < NBW; g0 += NG) {
+        // hidden activations (bias + act, one 32-row block at a time) feed the posterior heads:
+        // rows 0..15 mean, 16..31 log-variance (this wave's share of the hidden rows)
+        v16f z[NG];
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            z[nb][r] = 0.0f;
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        const int hbg = wh * HB + hb;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const float wv = s_whp[(hbg * 16 + r) * 64 + lane];
-            const float bias = s_b1[hbg * 32 + crow(r, half)];
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                z[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, act_fn<ACT>(acc[hb][nb][r] + bias),
-                                                             z[nb], 0, 0, 0);
-        }
-    }
-    float *xz = reinterpret_cast<float *>(seg);            // [kWaves][NBW][16][64] head partials
-    float *xd = xz + kWaves * NBW * 16 * 64;               // [kWaves][NBW][64] decoder partials
-    if constexpr (WH > 1) {
-        // every wave of the window group adds the WH partials in the same fixed order
-        __syncthreads();                                   // the segment is no longer read
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
+        for (int i = 0; i < NG; ++i)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                xz[((wave * NBW + nb) * 16 + r) * 64 + lane] = z[nb][r];
-        __syncthreads();
+                z[i][r] = 0.0f;
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
+        for (int hb = 0; hb < HB; ++hb) {
+            const int hbg = wh * HB + hb;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
+                const float wv = CL ? s_whp[(hbg * 16 + r) * 64 + lane] : p.whp[(hbg * 16 + r) * 64 + lane];
+                const float bias = CL ? s_b1[hbg * 32 + crow(r, half)] : p.b1[hbg * 32 + crow(r, half)];
+#pragma unroll
+                for (int i = 0; i < NG; ++i)
+                    z[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                        wv, act_fn<ACT>(acc[hb][g0 + i][r] + bias), z[i], 0, 0, 0);
+            }
+        }
+        if constexpr (WH > 1) {
+            // every wave of the window group adds the WH partials in the same fixed order
+            __syncthreads();          // the segment, or the previous pass's exchange, is no longer read
+#pragma unroll
+            for (int i = 0; i < NG; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    xz[((wave * NG + i) * 16 + r) * 64 + lane] = z[i][r];
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < NG; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    float t = 0.0f;
+#pragma unroll
+                    for (int w2 = 0; w2 < WH; ++w2)
+                        t += xz[(((wn * WH + w2) * NG + i) * 16 + r) * 64 + lane];
+                    z[i][r] = t;
+                }
+        }
+        float kl[NG];
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+            kl[i] = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                z[i][r] += CL ? s_bh[crow(r, half)] : p.bh[crow(r, half)];
+                if (r < 8)
+                    kl[i] += z[i][r] * z[i][r];
+                else
+                    kl[i] += kl_g(z[i][r]);
+            }
+            kl[i] += __shfl_xor(kl[i], 32);
+        }
+        // decoder hidden layer at z = mu, dotted with the column sums of Wd2
+        float dot[NG];
+#pragma unroll
+        for (int i = 0; i < NG; ++i)
+            dot[i] = 0.0f;
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb) {
+            const int hbg = wh * HB + hb;
+            v16f d[NG];
+#pragma unroll
+            for (int i = 0; i < NG; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    d[i][r] = 0.0f;
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                const float wv = CL ? s_wd1p[(hbg * 8 + r) * 64 + lane] : p.wd1p[(hbg * 8 + r) * 64 + lane];
+#pragma unroll
+                for (int i = 0; i < NG; ++i)
+                    d[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[i][r], d[i], 0, 0, 0);
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int h = hbg * 32 + crow(r, half);
+                const float uh = CL ? s_u[h] : p.u[h];
+                const float bh = CL ? s_bd1[h] : p.bd1[h];
+#pragma unroll
+                for (int i = 0; i < NG; ++i)
+                    dot[i] += uh * act_fn<ACT>(d[i][r] + bh);
+            }
+        }
+        if constexpr (WH > 1) {
+#pragma unroll
+            for (int i = 0; i < NG; ++i)
+                xd[(wave * NG + i) * 64 + lane] = dot[i];
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < NG; ++i) {
                 float t = 0.0f;
 #pragma unroll
                 for (int w2 = 0; w2 < WH; ++w2)
-                    t += xz[(((wn * WH + w2) * NBW + nb) * 16 + r) * 64 + lane];
-                z[nb][r] = t;
+                    t += xd[((wn * WH + w2) * NG + i) * 64 + lane];
+                dot[i] = t;
             }
-    }
-    float kl[NBW];
-#pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-        kl[nb] = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            z[nb][r] += s_bh[crow(r, half)];
-            if (r < 8)
-                kl[nb] += z[nb][r] * z[nb][r];
-            else
-                kl[nb] += kl_g(z[nb][r]);
-        }
-        kl[nb] += __shfl_xor(kl[nb], 32);
-    }
-    // decoder hidden layer at z = mu, dotted with the column sums of Wd2
-    float dot[NBW];
-#pragma unroll
-    for (int nb = 0; nb < NBW; ++nb)
-        dot[nb] = 0.0f;
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        const int hbg = wh * HB + hb;
-        v16f d[NBW];
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                d[nb][r] = 0.0f;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-            const float wv = s_wd1p[(hbg * 8 + r) * 64 + lane];
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                d[nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[nb][r], d[nb], 0, 0, 0);
         }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int h = hbg * 32 + crow(r, half);
-            const float uh = s_u[h], bh = s_bd1[h];
-#pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
-                dot[nb] += uh * act_fn<ACT>(d[nb][r] + bh);
-        }
-    }
-    if constexpr (WH > 1) {
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-            xd[(wave * NBW + nb) * 64 + lane] = dot[nb];
-        __syncthreads();
-        if (wh != 0 || !wave_active)
-            return;
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb) {
-            float t = 0.0f;
-#pragma unroll
-            for (int w2 = 0; w2 < WH; ++w2)
-                t += xd[((wn * WH + w2) * NBW + nb) * 64 + lane];
-            dot[nb] = t;
-        }
-    }
-#pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-        dot[nb] += __shfl_xor(dot[nb], 32);
+        for (int i = 0; i < NG; ++i) {
+            const int nb = g0 + i;
+            dot[i] += __shfl_xor(dot[i], 32);
 
-        // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
-        const int n = wn * NBW * 32 + nb * 32 + (lane & 31);
-        float vsum = 0.0f;
-        const int row0 = rb[nb] / CPRP;
-        for (int qq = half; qq < Q - 1; qq += 2)
-            vsum += rs[row0 + qq];
-        if (((Q - 1) & 1) == half)
-            vsum += ps[row0 + Q - 1];
-        vsum += __shfl_xor(vsum, 32);
+            // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
+            const int n = wn * NBW * 32 + nb * 32 + (lane & 31);
+            float vsum = 0.0f;
+            const int row0 = rb[nb] / CPRP;
+            for (int qq = half; qq < Q - 1; qq += 2)
+                vsum += rs[row0 + qq];
+            if (((Q - 1) & 1) == half)
+                vsum += ps[row0 + Q - 1];
+            vsum += __shfl_xor(vsum, 32);
 
-        if (half == 0 && n < nv) {
-            const int64_t w = p.woff[s] + k0 + n;
-            const float sc = 0.5f * kl[nb];
-            p.scores[w] = sc;
-            if (p.md)
-                p.md[w] = vsum * g.inv_d - (dot[nb] + p.sum_bd2) * g.inv_d;
-            if (p.write_flags)
-                p.flags[w] = sc > p.threshold ? 1 : 0;
+            if (storer && half == 0 && n < nv) {
+                const int64_t w = p.woff[s] + k0 + n;
+                const float sc = 0.5f * kl[i];
+                p.scores[w] = sc;
+                if (p.md)
+                    p.md[w] = vsum * g.inv_d - (dot[i] + p.sum_bd2) * g.inv_d;
+                if (p.write_flags)
+                    p.flags[w] = sc > p.threshold ? 1 : 0;
+            }
         }
     }
 }
@@ -508,25 +556,25 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 using ScoreKernel = void (*)(ScoreParams, MfmaShape);
 
 template <int DT, int ACT>
-ScoreKernel pick_layout(int hbw, int nbw, int wh)
+ScoreKernel pick_layout(int hbw, int nbw, int wh, bool cl)
 {
-    if (wh == 1) {
+    if (wh == 1 && cl) {
         switch (hbw) {
-        case 1: return nbw == 4 ? k_score_mfma<DT, 1, 4, 1, ACT> : nullptr;
-        case 2: return nbw == 4 ? k_score_mfma<DT, 2, 4, 1, ACT> : nullptr;
-        case 4: return nbw == 2 ? k_score_mfma<DT, 4, 2, 1, ACT> : nullptr;
-        case 8:   // bf16 with eight hidden blocks uses the four-wave split below
+        case 1: return nbw == 4 ? k_score_mfma<DT, 1, 4, 1, ACT, true> : nullptr;
+        case 2: return nbw == 4 ? k_score_mfma<DT, 2, 4, 1, ACT, true> : nullptr;
+        case 4: return nbw == 2 ? k_score_mfma<DT, 4, 2, 1, ACT, true> : nullptr;
+        case 8:   // bf16 with eight hidden blocks uses a split layout below
             if constexpr (DT == ENOVA_F32)
-                return nbw == 1 ? k_score_mfma<DT, 8, 1, 1, ACT> : nullptr;
+                return nbw == 1 ? k_score_mfma<DT, 8, 1, 1, ACT, true> : nullptr;
             else
                 return nullptr;
         default: return nullptr;
         }
     }
-    if (wh == 2 && hbw == 4 && nbw == 2)
-        return k_score_mfma<DT, 4, 2, 2, ACT>;
-    if (wh == 4 && hbw == 2 && nbw == 4)
-        return k_score_mfma<DT, 2, 4, 4, ACT>;
+    if constexpr (DT == ENOVA_BF16) {
+        if (wh == 2 && hbw == 4 && nbw == 4 && !cl)
+            return k_score_mfma<DT, 4, 4, 2, ACT, false>;
+    }
     return nullptr;
 }
 
@@ -535,10 +583,10 @@ ScoreKernel pick(const Geometry &g)
 {
     const bool relu = g.act == ENOVA_RELU;
     if (g.dtype == ENOVA_F32)
-        return relu ? pick_layout<ENOVA_F32, ENOVA_RELU>(g.HBW, g.NBW, g.WH)
-                    : pick_layout<ENOVA_F32, ENOVA_TANH>(g.HBW, g.NBW, g.WH);
-    return relu ? pick_layout<ENOVA_BF16, ENOVA_RELU>(g.HBW, g.NBW, g.WH)
-                : pick_layout<ENOVA_BF16, ENOVA_TANH>(g.HBW, g.NBW, g.WH);
+        return relu ? pick_layout<ENOVA_F32, ENOVA_RELU>(g.HBW, g.NBW, g.WH, g.cl)
+                    : pick_layout<ENOVA_F32, ENOVA_TANH>(g.HBW, g.NBW, g.WH, g.cl);
+    return relu ? pick_layout<ENOVA_BF16, ENOVA_RELU>(g.HBW, g.NBW, g.WH, g.cl)
+                : pick_layout<ENOVA_BF16, ENOVA_TANH>(g.HBW, g.NBW, g.WH, g.cl);
 }
 
 }  // namespace
@@ -569,6 +617,7 @@ hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t gr
     sh.CPR = g.CPR;
     sh.CPRP = g.CPRP;
     sh.KC = g.KC;
+    sh.spare = g.spare;
     sh.tail_rows = g.W - (g.Q - 1) * g.S;
     sh.inv_d = 1.0f / static_cast<float>(g.D);
     hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(grid)), dim3(kThreads), g.lds_bytes, st, p, sh);
@@ -579,11 +628,12 @@ hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t gr
 void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh)
 {
     if (dtype == ENOVA_BF16 && hb == 8) {
-        // bf16 matrix ops are 4x faster than fp32 ones: a (HB=8, NBW=1) wave tile would need
-        // 8 KiB of W1 per 8 MFMAs. Four waves split the hidden rows and share the windows.
-        *hbw = 2;
+        // bf16 matrix ops are 4x faster than fp32 ones, and every tile streams all of W1 from
+        // L2: the tile must hold as many windows as LDS allows. 2 x 2 waves of 128 hidden rows x
+        // 128 windows (256 windows per tile; the epilogue weights then stay in L2).
+        *hbw = 4;
         *nbw = 4;
-        *wh = 4;
+        *wh = 2;
         return;
     }
     *wh = 1;
