@@ -15,7 +15,7 @@
 #include "internal.h"
 
 namespace enova {
-void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh);
+void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh, int *nw);
 hipError_t prepare_score_mfma(const Geometry &g);
 }  // namespace enova
 
@@ -133,8 +133,8 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
         hb *= 2;
     g->HB = hb;
     g->Hp = 32 * hb;
-    mfma_layout(g->dtype, hb, &g->HBW, &g->NBW, &g->WH);
-    g->Nb = (kWaves / g->WH) * g->NBW * 32;
+    mfma_layout(g->dtype, hb, &g->HBW, &g->NBW, &g->WH, &g->NW);
+    g->Nb = (g->NW / g->WH) * g->NBW * 32;
     // epilogue weights (heads, decoder hidden layer, b1, bd1, u, head biases), the segment, its
     // row sums and the stream statistics
     const size_t n_const = static_cast<size_t>(hb) * (16 * 64 + 8 * 64) + 3 * static_cast<size_t>(g->Hp) + 32;
@@ -142,11 +142,11 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     // head and decoder partial sums
     const size_t rows = static_cast<size_t>(g->Nb + g->Q - 1 + g->spare);
     const size_t seg_bytes = rows * g->CPRP * 16;
-    const size_t xchg_bytes = g->WH > 1 ? static_cast<size_t>(kWaves) * std::min(g->NBW, 2) * 17 * 64 * sizeof(float) : 0;
+    const size_t xchg_bytes = g->WH > 1 ? static_cast<size_t>(g->NW) * std::min(g->NBW, 2) * 17 * 64 * sizeof(float) : 0;
     // the split bf16 layout keeps its epilogue weights in L2 to leave LDS to a 256-window tile
     g->cl = g->WH == 1;
     g->lds_bytes = (g->cl ? n_const * sizeof(float) : 0) + std::max(seg_bytes, xchg_bytes) +
-                   rows * 2 * sizeof(float) + 2 * sizeof(float) * g->Mp;
+                   rows * 2 * sizeof(float) + 3 * sizeof(float) * static_cast<size_t>(g->S) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;
     if (!g->mfma_ok) {

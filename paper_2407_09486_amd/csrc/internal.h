@@ -35,14 +35,15 @@ struct Geometry {
     int HB;                 // 32-row hidden blocks of the tile (Hp = 32*HB)
     int HBW;                // hidden blocks per wave
     int NBW;                // 32-window blocks per wave
-    int WH;                 // waves along the hidden rows (4/WH along the windows)
+    int WH;                 // waves along the hidden rows (NW/WH along the windows)
+    int NW;                 // waves per block of the matrix-core kernel (4 or 8)
     bool cl;                // epilogue weights staged in LDS (else read from L2)
     int Nb;                 // windows per tile
     size_t lds_bytes;       // dynamic LDS of the matrix-core kernel
     bool mfma_ok;
 };
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 4;                 // waves per block of the other kernels
 constexpr int kThreads = 64 * kWaves;
 constexpr size_t kLdsLimit = 160 * 1024;
 // The reduction index is padded to a multiple of 2*kPrefetchSteps chunks (the matrix-core

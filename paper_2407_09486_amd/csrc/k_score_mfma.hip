@@ -101,17 +101,18 @@ __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u 
 // Row of the accumulator register r for lane half g inside a 32x32 block.
 __device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
-// Wave layout: the 4 waves form WH groups along the hidden rows and kWaves/WH groups along the
+// Wave layout: the NW waves form WH groups along the hidden rows and NW/WH groups along the
 // windows. A wave owns HB 32-row hidden blocks and NBW 32-window blocks; with WH > 1 the waves
 // of a window group share its B fragments and their posterior-head partial sums are reduced
 // through LDS.
 // CL: the epilogue weights are copied into LDS with each tile (else read from L2, leaving the
 // LDS to a larger segment).
-template <int DT, int HB, int NBW, int WH, int ACT, bool CL>
-__global__ __launch_bounds__(kThreads, (ACT == ENOVA_RELU && WH == 1) ? 2 : 1)
+template <int DT, int HB, int NBW, int WH, int NW, int ACT, bool CL>
+__global__ __launch_bounds__(NW * 64, (NW == 4 && ACT == ENOVA_RELU && WH == 1) ? 2 : 1)
 void k_score_mfma(ScoreParams p, MfmaShape g)
 {
-    constexpr int WN = kWaves / WH;               // window groups
+    constexpr int NT = NW * 64;                   // threads of the block
+    constexpr int WN = NW / WH;                   // window groups
     constexpr int HBT = HB * WH;                  // hidden blocks of the tile
     constexpr int NB = WN * NBW * 32;             // windows per tile
     constexpr int EPC = DT == ENOVA_F32 ? 4 : 8;  // elements per 16-byte chunk
@@ -145,7 +146,7 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     constexpr int HP = 32 * HBT;
     constexpr int N_WHP = HBT * 16 * 64, N_WD1P = HBT * 8 * 64;
     constexpr int N_CONST = CL ? N_WHP + N_WD1P + 3 * HP + 32 : 0;
-    constexpr int N_XCHG = WH > 1 ? kWaves * (NBW > 2 ? 2 : NBW) * (16 + 1) * 64 : 0;   // floats
+    constexpr int N_XCHG = WH > 1 ? NW * (NBW > 2 ? 2 : NBW) * (16 + 1) * 64 : 0;   // floats
     float *s_whp = reinterpret_cast<float *>(lds);
     float *s_wd1p = s_whp + N_WHP;
     float *s_b1 = s_wd1p + N_WD1P;
@@ -156,10 +157,14 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     const int rows_alloc = NB + Q - 1 + g.spare;
     const size_t seg_chunks = static_cast<size_t>(rows_alloc) * CPRP;
     const size_t seg_span = seg_chunks > N_XCHG / 4 ? seg_chunks : N_XCHG / 4;
-    float *rs = reinterpret_cast<float *>(seg + seg_span);
+    // per element j of a super-row (j = c*EPC + e < S*Mp): its metric's mean and 1/std (0 for
+    // padding) and its offset from the row's first element in the stream (-1 for padding)
+    const int SMp = CPR * EPC;
+    float *cmean = reinterpret_cast<float *>(seg + seg_span);
+    float *crinv = cmean + SMp;
+    int *coff = reinterpret_cast<int *>(crinv + SMp);
+    float *rs = reinterpret_cast<float *>(coff + SMp);
     float *ps = rs + rows_alloc;
-    float *smean = ps + rows_alloc;
-    float *srinv = smean + Mp;
 
     if constexpr (CL) {
         // the host lays the epilogue weights out contiguously in this LDS order; copy them with
@@ -168,47 +173,53 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
         constexpr int CU = 4;
         const float4 *src = reinterpret_cast<const float4 *>(p.whp);
         float4 *dst = reinterpret_cast<float4 *>(s_whp);
-        constexpr int FULL = N4 / (kThreads * CU) * (kThreads * CU);
-        for (int base = tid; base < FULL; base += kThreads * CU) {
+        constexpr int FULL = N4 / (NT * CU) * (NT * CU);
+        for (int base = tid; base < FULL; base += NT * CU) {
             float4 t[CU];
 #pragma unroll
             for (int u = 0; u < CU; ++u)
-                t[u] = src[base + u * kThreads];
+                t[u] = src[base + u * NT];
 #pragma unroll
             for (int u = 0; u < CU; ++u)
-                dst[base + u * kThreads] = t[u];
+                dst[base + u * NT] = t[u];
         }
-        for (int i = FULL + tid; i < N4; i += kThreads)
+        for (int i = FULL + tid; i < N4; i += NT)
             dst[i] = src[i];
     }
-    for (int m = tid; m < Mp; m += kThreads) {
+    for (int j = tid; j < SMp; j += NT) {
+        const int tt = j / Mp;
+        const int m = j - tt * Mp;
         if (m < M) {
-            smean[m] = p.mean[static_cast<int64_t>(s) * M + m];
-            srinv[m] = 1.0f / p.std[static_cast<int64_t>(s) * M + m];
+            cmean[j] = p.mean[static_cast<int64_t>(s) * M + m];
+            crinv[j] = 1.0f / p.std[static_cast<int64_t>(s) * M + m];
+            coff[j] = tt * M + m;
         } else {
-            smean[m] = 0.0f;
-            srinv[m] = 0.0f;
+            cmean[j] = 0.0f;
+            crinv[j] = 0.0f;
+            coff[j] = -1;
         }
     }
     __syncthreads();
 
     // ---- stage: super-row r of the tile covers stream steps (k0 + r)*S .. +S-1
     const int64_t step0 = k0 * S;
-    const int64_t avail = T - step0;               // stream steps available from step0
+    const int64_t eavail = (T - step0) * M;        // stream elements from super-row 0 on
     const bool linear = (Mp == M) && (((srow + step0) * M) % EPC == 0);
     const int64_t ebase = (srow + step0) * M;      // element index of super-row 0
-    const int64_t eend = (srow + T) * M;           // one past the stream's last element
     // Each thread keeps SU chunk loads in flight before normalising them (one load per loop
-    // trip would serialise a full HBM round trip per chunk).
+    // trip would serialise a full HBM round trip per chunk). Its chunks are tid + i*NT; their
+    // (row, column) advance by (NT / CPR, NT % CPR) with a carry instead of a division each.
     constexpr int SU = 8;
     const int n_chunks = nrows * CPR;
-    for (int base = tid; base < n_chunks; base += kThreads * SU) {
+    const int dr = NT / CPR, dc = NT - (NT / CPR) * CPR;
+    int cr = tid / CPR, ccol = tid - (tid / CPR) * CPR;
+    for (int base = tid; base < n_chunks; base += NT * SU) {
       uint4 raw[SU];
       bool vec[SU];
 #pragma unroll
       for (int u = 0; u < SU; ++u) {
-        const int idx = base + u * kThreads;
-        vec[u] = idx < n_chunks && linear && ebase + static_cast<int64_t>(idx + 1) * EPC <= eend;
+        const int idx = base + u * NT;
+        vec[u] = idx < n_chunks && linear && static_cast<int64_t>(idx + 1) * EPC <= eavail;
         if (vec[u]) {
             const int64_t e0 = ebase + static_cast<int64_t>(idx) * EPC;
             if constexpr (DT == ENOVA_F32)
@@ -219,11 +230,18 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
       }
 #pragma unroll
       for (int u = 0; u < SU; ++u) {
-        const int idx = base + u * kThreads;
+        const int idx = base + u * NT;
+        const int r = cr, c = ccol;
+        ccol += dc;
+        cr += dr;
+        if (ccol >= CPR) {
+            ccol -= CPR;
+            ++cr;
+        }
         if (idx >= n_chunks)
             continue;
-        const int r = idx / CPR;
-        const int c = idx - r * CPR;
+        const float *mu = cmean + c * EPC;
+        const float *ri = crinv + c * EPC;
         float v[EPC];
         if (vec[u]) {
             if constexpr (DT == ENOVA_F32) {
@@ -242,20 +260,17 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
                 v[7] = bf16_hi(raw[u].w);
             }
 #pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                const int m = (c * EPC + e) % M;
-                v[e] = (v[e] - smean[m]) * srinv[m];
-            }
+            for (int e = 0; e < EPC; ++e)
+                v[e] = (v[e] - mu[e]) * ri[e];
         } else {
+            // padding, the stream's end, or a row start that is not 16-byte aligned
+            const int64_t rel = static_cast<int64_t>(r) * S * M;
 #pragma unroll
             for (int e = 0; e < EPC; ++e) {
-                const int jj = c * EPC + e;
-                const int tt = jj / Mp;
-                const int m = jj - tt * Mp;
-                const int64_t step = static_cast<int64_t>(r) * S + tt;
+                const int off = coff[c * EPC + e];
                 float val = 0.0f;
-                if (m < M && step < avail)
-                    val = (load_x<DT>(p.x, (srow + step0 + step) * M + m) - smean[m]) * srinv[m];
+                if (off >= 0 && rel + off < eavail)
+                    val = (load_x<DT>(p.x, ebase + rel + off) - mu[e]) * ri[e];
                 v[e] = val;
             }
         }
@@ -278,7 +293,7 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 
     // ---- per-super-row sums of the staged values (full row, and the window's tail part)
     const int tail_elems = g.tail_rows * Mp;
-    for (int r = tid; r < nrows; r += kThreads) {
+    for (int r = tid; r < nrows; r += NT) {
         float full = 0.0f, part = 0.0f;
         for (int c = 0; c < CPR; ++c) {
             const uint4 q4 = seg[r * CPRP + c];
@@ -373,17 +388,22 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
         // HB*NBW, so bf16 needs the deeper rings to cover an L2 round trip. The loop is unrolled
         // by PD so every ring slot is a compile-time register set.
         // (bf16 with one wave per hidden group runs two waves per SIMD, and four hidden blocks
-        // per wave hold 16 registers per step: a shallower ring for both)
+        // per wave hold 16 registers per step: a shallower W1 ring for both; the eight-wave
+        // layout has 256 registers per wave and a short LDS latency to cover: one window step)
         constexpr int PD = DT == ENOVA_F32 ? 2 : ((WH == 1 || HB >= 4) ? 4 : 8);
-        constexpr int PB = DT == ENOVA_F32 ? 1 : 2;
+        constexpr int PB = (DT == ENOVA_F32 || NW == 8) ? 1 : 2;
         constexpr int RB = 2 * PB;
         static_assert(PD % RB == 0 && PD <= kPrefetchSteps && PB <= kPrefetchRows, "prefetch rings");
         uint4 a[PD][HB], b[RB][NBW];
 #pragma unroll
-        for (int j = 0; j < PD; ++j)
+        for (int j = 0; j < PD; ++j) {
 #pragma unroll
             for (int hb = 0; hb < HB; ++hb)
                 a[j][hb] = ap[(j * HBT + hb) * 64];
+            // issue the ring in step order: the wait counts inserted at the loop head must hold
+            // for the first trip too, and a reordered prologue makes them wait for the newest loads
+            __builtin_amdgcn_sched_barrier(0);
+        }
 #pragma unroll
         for (int j = 0; j < PB; ++j) {
 #pragma unroll
@@ -401,13 +421,35 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
                 for (int nb = 0; nb < NBW; ++nb)
                     b[(j + PB) % RB][nb] = seg[rb[nb] + koff];
                 advance();
-                // keep the prefetches ahead of this step's matrix ops (the scheduler would sink them)
-                __builtin_amdgcn_sched_barrier(0);
-                mma(a[j], b[j % RB]);
-                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (DT == ENOVA_F32) {
+                    // keep the prefetches ahead of this step's matrix ops (the scheduler would
+                    // sink them)
+                    __builtin_amdgcn_sched_barrier(0);
+                    mma(a[j], b[j % RB]);
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int hb = 0; hb < HB; ++hb)
-                    a[j][hb] = api[(j * HBT + hb) * 64];
+                    for (int hb = 0; hb < HB; ++hb)
+                        a[j][hb] = api[(j * HBT + hb) * 64];
+                } else {
+                    mma(a[j], b[j % RB]);
+#pragma unroll
+                    for (int hb = 0; hb < HB; ++hb)
+                        a[j][hb] = api[(j * HBT + hb) * 64];
+                    // A bf16 matrix op is short, and a wave issues in order: slot the step's
+                    // other instructions between the matrix ops instead of in one run (the
+                    // window-fragment reads first, each W1 reload right after the last op that
+                    // reads its register)
+#pragma unroll
+                    for (int t = 0; t < HB * NBW; ++t) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // matrix op
+                        if (t < NBW)
+                            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+                        if ((t + 1) % NBW == 0)
+                            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global read
+                        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);   // vector ALU
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
             api += PD * HBT * 64;
         }
@@ -420,8 +462,8 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     // ---- epilogue, NG window blocks per pass (weights from LDS, or L2 when the segment needs
     // the LDS); the NG blocks of a pass run as independent MFMA chains
     constexpr int NG = NBW > 2 ? 2 : NBW;
-    float *xz = reinterpret_cast<float *>(seg);            // [kWaves][NG][16][64] head partials
-    float *xd = xz + kWaves * NG * 16 * 64;                // [kWaves][NG][64] decoder partials
+    float *xz = reinterpret_cast<float *>(seg);            // [NW][NG][16][64] head partials
+    float *xd = xz + NW * NG * 16 * 64;                    // [NW][NG][64] decoder partials
     const bool storer = WH == 1 || (wh == 0 && wave_active);
 #pragma unroll
     for (int g0 = 0; g0 < NBW; g0 += NG) {
@@ -556,24 +598,24 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 using ScoreKernel = void (*)(ScoreParams, MfmaShape);
 
 template <int DT, int ACT>
-ScoreKernel pick_layout(int hbw, int nbw, int wh, bool cl)
+ScoreKernel pick_layout(int hbw, int nbw, int wh, int nw, bool cl)
 {
-    if (wh == 1 && cl) {
+    if (wh == 1 && nw == 4 && cl) {
         switch (hbw) {
-        case 1: return nbw == 4 ? k_score_mfma<DT, 1, 4, 1, ACT, true> : nullptr;
-        case 2: return nbw == 4 ? k_score_mfma<DT, 2, 4, 1, ACT, true> : nullptr;
-        case 4: return nbw == 2 ? k_score_mfma<DT, 4, 2, 1, ACT, true> : nullptr;
+        case 1: return nbw == 4 ? k_score_mfma<DT, 1, 4, 1, 4, ACT, true> : nullptr;
+        case 2: return nbw == 4 ? k_score_mfma<DT, 2, 4, 1, 4, ACT, true> : nullptr;
+        case 4: return nbw == 2 ? k_score_mfma<DT, 4, 2, 1, 4, ACT, true> : nullptr;
         case 8:   // bf16 with eight hidden blocks uses a split layout below
             if constexpr (DT == ENOVA_F32)
-                return nbw == 1 ? k_score_mfma<DT, 8, 1, 1, ACT, true> : nullptr;
+                return nbw == 1 ? k_score_mfma<DT, 8, 1, 1, 4, ACT, true> : nullptr;
             else
                 return nullptr;
         default: return nullptr;
         }
     }
     if constexpr (DT == ENOVA_BF16) {
-        if (wh == 2 && hbw == 4 && nbw == 4 && !cl)
-            return k_score_mfma<DT, 4, 4, 2, ACT, false>;
+        if (wh == 4 && nw == 8 && hbw == 2 && nbw == 4 && !cl)
+            return k_score_mfma<DT, 2, 4, 4, 8, ACT, false>;
     }
     return nullptr;
 }
@@ -583,10 +625,10 @@ ScoreKernel pick(const Geometry &g)
 {
     const bool relu = g.act == ENOVA_RELU;
     if (g.dtype == ENOVA_F32)
-        return relu ? pick_layout<ENOVA_F32, ENOVA_RELU>(g.HBW, g.NBW, g.WH, g.cl)
-                    : pick_layout<ENOVA_F32, ENOVA_TANH>(g.HBW, g.NBW, g.WH, g.cl);
-    return relu ? pick_layout<ENOVA_BF16, ENOVA_RELU>(g.HBW, g.NBW, g.WH, g.cl)
-                : pick_layout<ENOVA_BF16, ENOVA_TANH>(g.HBW, g.NBW, g.WH, g.cl);
+        return relu ? pick_layout<ENOVA_F32, ENOVA_RELU>(g.HBW, g.NBW, g.WH, g.NW, g.cl)
+                    : pick_layout<ENOVA_F32, ENOVA_TANH>(g.HBW, g.NBW, g.WH, g.NW, g.cl);
+    return relu ? pick_layout<ENOVA_BF16, ENOVA_RELU>(g.HBW, g.NBW, g.WH, g.NW, g.cl)
+                : pick_layout<ENOVA_BF16, ENOVA_TANH>(g.HBW, g.NBW, g.WH, g.NW, g.cl);
 }
 
 }  // namespace
@@ -620,23 +662,27 @@ hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t gr
     sh.spare = g.spare;
     sh.tail_rows = g.W - (g.Q - 1) * g.S;
     sh.inv_d = 1.0f / static_cast<float>(g.D);
-    hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(grid)), dim3(kThreads), g.lds_bytes, st, p, sh);
+    hipLaunchKernelGGL(k, dim3(static_cast<unsigned>(grid)), dim3(64 * g.NW), g.lds_bytes, st, p, sh);
     return hipGetLastError();
 }
 
-// NBW (32-window blocks per wave) that goes with each hidden-block count HB.
-void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh)
+// Wave layout for a hidden-block count HB: hidden blocks and 32-window blocks per wave, waves
+// along the hidden rows, waves per block.
+void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh, int *nw)
 {
     if (dtype == ENOVA_BF16 && hb == 8) {
         // bf16 matrix ops are 4x faster than fp32 ones, and every tile streams all of W1 from
-        // L2: the tile must hold as many windows as LDS allows. 2 x 2 waves of 128 hidden rows x
-        // 128 windows (256 windows per tile; the epilogue weights then stay in L2).
-        *hbw = 4;
+        // L2: the tile must hold as many windows as LDS allows (256; the epilogue weights then
+        // stay in L2). Eight waves, two per SIMD, keep the matrix cores busy while the other
+        // wave of the SIMD waits: 4 x 2 waves of 64 hidden rows x 128 windows.
+        *hbw = 2;
         *nbw = 4;
-        *wh = 2;
+        *wh = 4;
+        *nw = 8;
         return;
     }
     *wh = 1;
+    *nw = 4;
     *hbw = hb;
     *nbw = hb <= 2 ? 4 : (hb == 4 ? 2 : 1);
 }
