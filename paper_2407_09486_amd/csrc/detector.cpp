@@ -66,6 +66,17 @@ float bf16_bits_to_float(uint16_t b)
     return f;
 }
 
+// Round to nearest even; a NaN stays a (quiet) NaN.
+uint16_t float_to_bf16_bits(float f)
+{
+    uint32_t u;
+    std::memcpy(&u, &f, sizeof(u));
+    if ((u & 0x7fffffffu) > 0x7f800000u)
+        return static_cast<uint16_t>((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
 }  // namespace
 
 struct enova_detector_s {
@@ -245,7 +256,7 @@ struct DeviceGpdSums : GpdSums {
     {
         if (nx <= 0)
             return true;
-        const int ns = gpd_split(n);
+        const int ns = gpd_split(n, nx);
         const size_t np = static_cast<size_t>(nx) * ns;
         status = ensure(&d->gx, &d->gx_cap, static_cast<size_t>(nx) + 2 * np);
         if (status != ENOVA_OK)
@@ -390,7 +401,44 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
     std::memcpy(&small[o_wmu], w->wmu, sizeof(float) * L * H);
     std::memcpy(&small[o_wlv], w->wlv, sizeof(float) * L * H);
     std::memcpy(&small[o_wd1], w->wd1, sizeof(float) * H * L);
-    if (d->kind == 2) {
+    if (d->kind == 2 && bf) {
+        // bf16 workload: the heads and decoder weights as bf16 hi + lo fragments of the
+        // 32x32x16 matrix op; reduction slot (g, t) of heads op m is hidden row crow(8m + t, g),
+        // of the decoder op latent crow(t, g)
+        uint16_t *whb = reinterpret_cast<uint16_t *>(&small[o_whp]);
+        uint16_t *wdb = reinterpret_cast<uint16_t *>(&small[o_wd1p]);
+        for (int hb = 0; hb < g.HB; ++hb)
+            for (int m = 0; m < 2; ++m)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int t = 0; t < 8; ++t) {
+                        const int row = lane & 31;          // 0..15 mean head, 16..31 log-variance
+                        const int h = hb * 32 + crow(8 * m + t, lane >> 5);
+                        float v = 0.0f;
+                        if (h < H) {
+                            if (row < 16 && row < L)
+                                v = w->wmu[row * H + h];
+                            else if (row >= 16 && row - 16 < L)
+                                v = w->wlv[(row - 16) * H + h];
+                        }
+                        const uint16_t hi = float_to_bf16_bits(v);
+                        const uint16_t lo = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+                        whb[((((static_cast<size_t>(hb) * 2 + m) * 2 + 0) * 64 + lane) * 8) + t] = hi;
+                        whb[((((static_cast<size_t>(hb) * 2 + m) * 2 + 1) * 64 + lane) * 8) + t] = lo;
+                    }
+        for (int hb = 0; hb < g.HB; ++hb)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int t = 0; t < 8; ++t) {
+                    const int h = hb * 32 + (lane & 31);
+                    const int l = crow(t, lane >> 5);
+                    float v = 0.0f;
+                    if (h < H && l < L)
+                        v = w->wd1[h * L + l];
+                    const uint16_t hi = float_to_bf16_bits(v);
+                    const uint16_t lo = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+                    wdb[(((static_cast<size_t>(hb) * 2 + 0) * 64 + lane) * 8) + t] = hi;
+                    wdb[(((static_cast<size_t>(hb) * 2 + 1) * 64 + lane) * 8) + t] = lo;
+                }
+    } else if (d->kind == 2) {
         for (int hb = 0; hb < g.HB; ++hb)
             for (int r = 0; r < 16; ++r)
                 for (int lane = 0; lane < 64; ++lane) {
@@ -764,9 +812,9 @@ enova_status enova_detect_threshold(enova_detector det, const float *scores, con
     }
     if (n_greater >= 10) {
         double ps[3];
-        if ((st = ensure(&det->gx, &det->gx_cap, 96)) != ENOVA_OK)
+        if ((st = ensure(&det->gx, &det->gx_cap, 4 + 3 * kPeakBlocks)) != ENOVA_OK)
             return st;
-        if ((e = launch_peak_stats(det->peaks, n_greater, det->gx, stream)) != hipSuccess ||
+        if ((e = launch_peak_stats(det->peaks, n_greater, det->gx, det->gx + 4, stream)) != hipSuccess ||
             (e = hipMemcpyAsync(ps, det->gx, sizeof(ps), hipMemcpyDeviceToHost, stream)) != hipSuccess ||
             (e = hipStreamSynchronize(stream)) != hipSuccess)
             return hip_fail(e, "peak statistics");

@@ -112,14 +112,16 @@ hipError_t launch_calib_compact(const float *scores, const int64_t *woff, const 
                                 int n, int64_t n_cal, uint32_t key, double t,
                                 const int64_t *block_off, double *y, int64_t cap, hipStream_t st);
 hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream_t st);
-// Partial likelihood sums at the points xs: block (i, j) of nx*nsplit blocks writes
-// pa[i*nsplit + j] = sum xs[i] y/(1 + xs[i] y) and pb[i*nsplit + j] = sum log1p(xs[i] y) over the
-// j-th of nsplit contiguous chunks of y (fixed-order fp64 sums; the caller adds the chunks in order).
-int gpd_split(int64_t n);
+// Partial likelihood sums at the points xs: pa[i*nsplit + j] = sum xs[i] y/(1 + xs[i] y) and
+// pb[i*nsplit + j] = sum log1p(xs[i] y) over the j-th of nsplit contiguous chunks of y (fixed-order
+// fp64 sums; the caller adds the chunks in order). gpd_split gives nsplit for n excesses and nx
+// points.
+int gpd_split(int64_t n, int nx);
 hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
                            double *pa, double *pb, hipStream_t st);
-// out = {sum y, min y, max y}
-hipError_t launch_peak_stats(const double *y, int64_t n, double *out, hipStream_t st);
+// out = {sum y, min y, max y}; work holds 3 * kPeakBlocks doubles of block partials
+constexpr int kPeakBlocks = 256;
+hipError_t launch_peak_stats(const double *y, int64_t n, double *out, double *work, hipStream_t st);
 
 // Peaks-over-threshold fit (fp64). The likelihood sums over the excesses are supplied by an
 // evaluator, so they can run where the excesses live.

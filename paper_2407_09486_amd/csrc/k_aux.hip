@@ -332,51 +332,97 @@ __device__ __forceinline__ void block_sum2(double &a, double &b, double *sa, dou
     b = sb[0];
 }
 
-// Likelihood sums of the excesses: block (i, j) covers chunk j of nsplit contiguous chunks of y
-// at the point xs[i] and writes pa = sum xy/(1+xy), pb = sum log1p(xy) in a fixed order.
+// Wave-wide sum in a fixed butterfly order (every lane ends with the same value).
+__device__ __forceinline__ double wave_sum(double v)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+        v += __shfl_xor(v, m);
+    return v;
+}
+
+// Likelihood sums of the excesses: block (g, j) covers chunk j of nsplit contiguous chunks of y
+// at the kGpdX points xs[g*kGpdX ...] (each excess is loaded once for all of them) and writes
+// pa = sum xy/(1+xy), pb = sum log1p(xy) per point in a fixed order.
+constexpr int kGpdX = 8;
 __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, int64_t n,
-                                                  const double *__restrict__ xs, int nsplit,
+                                                  const double *__restrict__ xs, int nx, int nsplit,
                                                   double *__restrict__ pa, double *__restrict__ pb)
 {
-    __shared__ double sa[256];
-    __shared__ double sb[256];
-    const int p = blockIdx.x / nsplit;
-    const int j = blockIdx.x - p * nsplit;
-    const double x = xs[p];
+    __shared__ double red[4][2 * kGpdX];
+    const int grp = blockIdx.x / nsplit;
+    const int j = blockIdx.x - grp * nsplit;
+    double x[kGpdX];
+#pragma unroll
+    for (int k = 0; k < kGpdX; ++k) {
+        const int i = grp * kGpdX + k;
+        x[k] = i < nx ? xs[i] : 0.0;
+    }
     const int64_t chunk = (n + nsplit - 1) / nsplit;
     const int64_t lo = j * chunk;
     const int64_t hi = lo + chunk < n ? lo + chunk : n;
-    double a = 0.0, b = 0.0;
-    for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
-        const double xy = x * y[i];
-        a += xy / (1.0 + xy);
-        b += log1p(xy);
+    double a[kGpdX], b[kGpdX];
+#pragma unroll
+    for (int k = 0; k < kGpdX; ++k) {
+        a[k] = 0.0;
+        b[k] = 0.0;
     }
-    block_sum2(a, b, sa, sb);
-    if (threadIdx.x == 0) {
-        pa[blockIdx.x] = a;
-        pb[blockIdx.x] = b;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
+        const double yi = y[i];
+#pragma unroll
+        for (int k = 0; k < kGpdX; ++k) {
+            const double xy = x[k] * yi;
+            a[k] += xy / (1.0 + xy);
+            b[k] += log1p(xy);
+        }
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int k = 0; k < kGpdX; ++k) {
+        a[k] = wave_sum(a[k]);
+        b[k] = wave_sum(b[k]);
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < kGpdX; ++k) {
+            red[wave][k] = a[k];
+            red[wave][kGpdX + k] = b[k];
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < kGpdX) {
+        const int k = threadIdx.x;
+        const int i = grp * kGpdX + k;
+        if (i < nx) {
+            pa[static_cast<int64_t>(i) * nsplit + j] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
+            pb[static_cast<int64_t>(i) * nsplit + j] =
+                ((red[0][kGpdX + k] + red[1][kGpdX + k]) + red[2][kGpdX + k]) + red[3][kGpdX + k];
+        }
     }
 }
 
-// Sum, minimum and maximum of the excesses (one block, fixed order).
-__global__ __launch_bounds__(256) void k_peak_stats(const double *__restrict__ y, int64_t n,
-                                                    double *__restrict__ out)
+// Sum, minimum and maximum of the excesses: block j of nblk reduces chunk j (fixed order) into
+// part[3j..3j+2]; one block then combines the nblk partials in order.
+__global__ __launch_bounds__(256) void k_peak_partial(const double *__restrict__ y, int64_t n,
+                                                      double *__restrict__ part)
 {
     __shared__ double sa[256];
     __shared__ double sb[256];
     __shared__ double sc[256];
     const int tid = threadIdx.x;
-    double sum = 0.0, lo = INFINITY, hi = -INFINITY;
-    for (int64_t i = tid; i < n; i += 256) {
+    const int64_t chunk = (n + gridDim.x - 1) / gridDim.x;
+    const int64_t lo = blockIdx.x * chunk;
+    const int64_t hi = lo + chunk < n ? lo + chunk : n;
+    double sum = 0.0, mn = INFINITY, mx = -INFINITY;
+    for (int64_t i = lo + tid; i < hi; i += 256) {
         const double v = y[i];
         sum += v;
-        lo = fmin(lo, v);
-        hi = fmax(hi, v);
+        mn = fmin(mn, v);
+        mx = fmax(mx, v);
     }
     sa[tid] = sum;
-    sb[tid] = lo;
-    sc[tid] = hi;
+    sb[tid] = mn;
+    sc[tid] = mx;
     __syncthreads();
     for (int w = 128; w >= 1; w >>= 1) {
         if (tid < w) {
@@ -387,10 +433,26 @@ __global__ __launch_bounds__(256) void k_peak_stats(const double *__restrict__ y
         __syncthreads();
     }
     if (tid == 0) {
-        out[0] = sa[0];
-        out[1] = sb[0];
-        out[2] = sc[0];
+        part[3 * blockIdx.x + 0] = sa[0];
+        part[3 * blockIdx.x + 1] = sb[0];
+        part[3 * blockIdx.x + 2] = sc[0];
     }
+}
+
+__global__ __launch_bounds__(64) void k_peak_final(const double *__restrict__ part, int nblk,
+                                                   double *__restrict__ out)
+{
+    if (threadIdx.x != 0)
+        return;
+    double sum = 0.0, mn = INFINITY, mx = -INFINITY;
+    for (int j = 0; j < nblk; ++j) {
+        sum += part[3 * j];
+        mn = fmin(mn, part[3 * j + 1]);
+        mx = fmax(mx, part[3 * j + 2]);
+    }
+    out[0] = sum;
+    out[1] = mn;
+    out[2] = mx;
 }
 
 }  // namespace
@@ -474,10 +536,16 @@ hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream
     return hipGetLastError();
 }
 
-int gpd_split(int64_t n)
+int gpd_split(int64_t n, int nx)
 {
-    const int64_t s = (n + 32767) / 32768;
-    return static_cast<int>(s < 1 ? 1 : (s > 64 ? 64 : s));
+    // about 2048 blocks in all (eight per compute unit: the fp64 division and log1p chains need
+    // several waves per SIMD to hide their latency), and at least 1024 excesses per chunk
+    const int64_t groups = (nx + kGpdX - 1) / kGpdX;
+    int64_t s = (2048 + groups - 1) / (groups < 1 ? 1 : groups);
+    const int64_t cap = n / 1024;
+    if (s > cap)
+        s = cap;
+    return static_cast<int>(s < 1 ? 1 : s);
 }
 
 hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
@@ -485,14 +553,25 @@ hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx,
 {
     if (nx <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_gpd_sums, dim3(static_cast<unsigned>(nx) * nsplit), dim3(256), 0, st, y, n,
-                       xs, nsplit, pa, pb);
+    const unsigned groups = static_cast<unsigned>((nx + kGpdX - 1) / kGpdX);
+    hipLaunchKernelGGL(k_gpd_sums, dim3(groups * nsplit), dim3(256), 0, st, y, n, xs, nx, nsplit, pa, pb);
     return hipGetLastError();
 }
 
-hipError_t launch_peak_stats(const double *y, int64_t n, double *out, hipStream_t st)
+int peak_blocks(int64_t n)
 {
-    hipLaunchKernelGGL(k_peak_stats, dim3(1), dim3(256), 0, st, y, n, out);
+    const int64_t b = (n + 8191) / 8192;
+    return static_cast<int>(b < 1 ? 1 : (b > kPeakBlocks ? kPeakBlocks : b));
+}
+
+hipError_t launch_peak_stats(const double *y, int64_t n, double *out, double *work, hipStream_t st)
+{
+    const int nblk = peak_blocks(n);
+    hipLaunchKernelGGL(k_peak_partial, dim3(nblk), dim3(256), 0, st, y, n, work);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_peak_final, dim3(1), dim3(64), 0, st, work, nblk, out);
     return hipGetLastError();
 }
 

@@ -98,6 +98,28 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
+// x = hi + lo as two bf16 vectors, lo the rounded remainder. With a bf16 weight split the same
+// way, hi*hi + hi*lo + lo*hi (fp32 accumulation) carries about 16 significant bits: the bf16
+// workload's posterior heads and decoder layer run on three bf16 matrix ops instead of the
+// eight times slower fp32 ones.
+__device__ __forceinline__ void split_bf16x8(const float (&x)[8], v8bf &hi, v8bf &lo)
+{
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const __bf16 h = static_cast<__bf16>(x[t]);
+        hi[t] = h;
+        lo[t] = static_cast<__bf16>(x[t] - static_cast<float>(h));
+    }
+}
+
+__device__ __forceinline__ v16f mfma3_bf16(uint4 a_hi, uint4 a_lo, v8bf b_hi, v8bf b_lo, v16f c)
+{
+    const v8bf ah = __builtin_bit_cast(v8bf, a_hi), al = __builtin_bit_cast(v8bf, a_lo);
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b_hi, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b_lo, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b_hi, c, 0, 0, 0);
+}
+
 // Row of the accumulator register r for lane half g inside a 32x32 block.
 __device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
@@ -478,14 +500,39 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 #pragma unroll
         for (int hb = 0; hb < HB; ++hb) {
             const int hbg = wh * HB + hb;
+            if constexpr (DT == ENOVA_F32) {
+                // reduction index of matrix op r: hidden rows crow(r, 0), crow(r, 1)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float wv = CL ? s_whp[(hbg * 16 + r) * 64 + lane] : p.whp[(hbg * 16 + r) * 64 + lane];
-                const float bias = CL ? s_b1[hbg * 32 + crow(r, half)] : p.b1[hbg * 32 + crow(r, half)];
+                for (int r = 0; r < 16; ++r) {
+                    const float wv = CL ? s_whp[(hbg * 16 + r) * 64 + lane] : p.whp[(hbg * 16 + r) * 64 + lane];
+                    const float bias = CL ? s_b1[hbg * 32 + crow(r, half)] : p.b1[hbg * 32 + crow(r, half)];
 #pragma unroll
-                for (int i = 0; i < NG; ++i)
-                    z[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                        wv, act_fn<ACT>(acc[hb][g0 + i][r] + bias), z[i], 0, 0, 0);
+                    for (int i = 0; i < NG; ++i)
+                        z[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            wv, act_fn<ACT>(acc[hb][g0 + i][r] + bias), z[i], 0, 0, 0);
+                }
+            } else {
+                // reduction slot (g, t) of op m: hidden row crow(8m + t, g); weights packed as
+                // [hidden block][m][hi, lo][lane] 16-byte fragments
+                const uint4 *wsrc = reinterpret_cast<const uint4 *>(CL ? s_whp : p.whp);
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    const uint4 wa_hi = wsrc[((hbg * 2 + m) * 2 + 0) * 64 + lane];
+                    const uint4 wa_lo = wsrc[((hbg * 2 + m) * 2 + 1) * 64 + lane];
+#pragma unroll
+                    for (int i = 0; i < NG; ++i) {
+                        float hv[8];
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) {
+                            const int r = 8 * m + t;
+                            const float bias = CL ? s_b1[hbg * 32 + crow(r, half)] : p.b1[hbg * 32 + crow(r, half)];
+                            hv[t] = act_fn<ACT>(acc[hb][g0 + i][r] + bias);
+                        }
+                        v8bf h_hi, h_lo;
+                        split_bf16x8(hv, h_hi, h_lo);
+                        z[i] = mfma3_bf16(wa_hi, wa_lo, h_hi, h_lo, z[i]);
+                    }
+                }
             }
         }
         if constexpr (WH > 1) {
@@ -522,11 +569,23 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
             }
             kl[i] += __shfl_xor(kl[i], 32);
         }
-        // decoder hidden layer at z = mu, dotted with the column sums of Wd2
+        // decoder hidden layer at z = mu, dotted with the column sums of Wd2 (mu is held in
+        // registers 0..7: latent crow(r, half))
         float dot[NG];
 #pragma unroll
         for (int i = 0; i < NG; ++i)
             dot[i] = 0.0f;
+        v8bf mu_hi[NG], mu_lo[NG];
+        if constexpr (DT == ENOVA_BF16) {
+#pragma unroll
+            for (int i = 0; i < NG; ++i) {
+                float mv[8];
+#pragma unroll
+                for (int t = 0; t < 8; ++t)
+                    mv[t] = z[i][t];
+                split_bf16x8(mv, mu_hi[i], mu_lo[i]);
+            }
+        }
 #pragma unroll
         for (int hb = 0; hb < HB; ++hb) {
             const int hbg = wh * HB + hb;
@@ -536,12 +595,22 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     d[i][r] = 0.0f;
+            if constexpr (DT == ENOVA_F32) {
 #pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                const float wv = CL ? s_wd1p[(hbg * 8 + r) * 64 + lane] : p.wd1p[(hbg * 8 + r) * 64 + lane];
+                for (int r = 0; r < 8; ++r) {
+                    const float wv = CL ? s_wd1p[(hbg * 8 + r) * 64 + lane] : p.wd1p[(hbg * 8 + r) * 64 + lane];
+#pragma unroll
+                    for (int i = 0; i < NG; ++i)
+                        d[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[i][r], d[i], 0, 0, 0);
+                }
+            } else {
+                // weights packed as [hidden block][hi, lo][lane] 16-byte fragments
+                const uint4 *wsrc = reinterpret_cast<const uint4 *>(CL ? s_wd1p : p.wd1p);
+                const uint4 wd_hi = wsrc[(hbg * 2 + 0) * 64 + lane];
+                const uint4 wd_lo = wsrc[(hbg * 2 + 1) * 64 + lane];
 #pragma unroll
                 for (int i = 0; i < NG; ++i)
-                    d[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[i][r], d[i], 0, 0, 0);
+                    d[i] = mfma3_bf16(wd_hi, wd_lo, mu_hi[i], mu_lo[i], d[i]);
             }
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
