@@ -2,6 +2,7 @@
 // radix-select passes of the peaks-over-threshold calibration.
 #include <hip/hip_runtime.h>
 
+#include "gpd_math.h"
 #include "internal.h"
 
 namespace enova {
@@ -371,9 +372,10 @@ __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, 
         const double yi = y[i];
 #pragma unroll
         for (int k = 0; k < kGpdX; ++k) {
-            const double xy = x[k] * yi;
-            a[k] += xy / (1.0 + xy);
-            b[k] += log1p(xy);
+            double ta, tb;
+            gpd_terms(x[k] * yi, ta, tb);
+            a[k] += ta;
+            b[k] += tb;
         }
     }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

@@ -146,6 +146,27 @@ def test_edge_shapes(case, kernel):
     det.close()
 
 
+@pytest.mark.parametrize("hidden", [32, 64, 128, 256])
+@pytest.mark.parametrize("act", ["relu", "tanh"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_every_matrix_core_layout(dtype, act, hidden):
+    """Each wave layout / activation / storage type instantiation of the matrix-core kernel,
+    on ragged streams with several tiles, a partial tile and a stream shorter than a window."""
+    cfg = wl.CONFIGS["c5"].replace(metrics=8, window=32, stride=2, hidden=hidden, latent=16,
+                                   dtype=dtype, act=act, n_streams=4, kind="ragged_mix")
+    lengths = [1200, 45, 31, 700]
+    w = wl.generate(cfg, lengths=lengths)
+    weights = wl.make_weights(cfg, bias_scale=0.1)
+    log(f"[layout] {dtype} {act} H={hidden}")
+    det = detector(cfg, weights, "mfma")
+    sc, md, _, woff = gpu_score(det, w, pad=32)
+    o_sc, o_md, info = oracle_score(cfg, w, weights)
+    assert np.array_equal(woff, info["window_offsets"])
+    check_scores(sc, o_sc, dtype, f"layout-{dtype}-{act}-{hidden}")
+    check_md(md, o_md, info["md_scale"], dtype, f"layout-{dtype}-{act}-{hidden}")
+    det.close()
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("kernel", ["auto", "valu"])
 def test_constant_streams_score_exactly_zero(dtype, kernel):
