@@ -14,11 +14,6 @@
 #include "enova_detect.h"
 #include "internal.h"
 
-namespace enova {
-void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh, int *nw);
-hipError_t prepare_score_mfma(const Geometry &g);
-}  // namespace enova
-
 using namespace enova;
 
 namespace {

@@ -55,6 +55,11 @@ constexpr int kPrefetchSteps = 8;
 constexpr int kPrefetchRows = 2;
 
 bool plan_geometry(const enova_detect_config &cfg, Geometry *g);
+// Wave layout of the matrix-core kernel for dtype and hb 32-row hidden blocks: hidden blocks and
+// 32-window blocks per wave, waves along the hidden rows, waves per block.
+void mfma_layout(int dtype, int hb, int *hbw, int *nbw, int *wh, int *nw);
+// Lets the instantiation chosen for g use the full LDS of a compute unit.
+hipError_t prepare_score_mfma(const Geometry &g);
 
 // Parameter block of the scoring kernels (passed by value).
 struct ScoreParams {

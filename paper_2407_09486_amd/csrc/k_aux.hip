@@ -315,24 +315,6 @@ __global__ __launch_bounds__(1024) void k_scan_i64(const int64_t *__restrict__ i
     }
 }
 
-// Fixed-order block reduction of two fp64 partial sums.
-__device__ __forceinline__ void block_sum2(double &a, double &b, double *sa, double *sb)
-{
-    const int tid = threadIdx.x;
-    sa[tid] = a;
-    sb[tid] = b;
-    __syncthreads();
-    for (int w = 128; w >= 1; w >>= 1) {
-        if (tid < w) {
-            sa[tid] += sa[tid + w];
-            sb[tid] += sb[tid + w];
-        }
-        __syncthreads();
-    }
-    a = sa[0];
-    b = sb[0];
-}
-
 // Wave-wide sum in a fixed butterfly order (every lane ends with the same value).
 __device__ __forceinline__ double wave_sum(double v)
 {

@@ -13,8 +13,9 @@
 //
 // The accumulator layout of a 32x32 MFMA block (lane l, register r holds row
 // 8*(r/4) + 4*(l/32) + r%4 and column l%32) is exactly the B-operand layout a following
-// 32x32x2 fp32 MFMA needs when its reduction index is permuted the same way, so the rest of
-// the detector chains on the matrix cores without leaving registers:
+// 32x32x2 fp32 MFMA needs when its reduction index is permuted the same way (and, eight
+// registers at a time, the B operand of a 32x32x16 bf16 MFMA), so the rest of the detector
+// chains on the matrix cores without leaving registers:
 //   hidden  h  = act(C + b1)
 //   heads   [mu; logvar] = Wh h + bh          (32 x Hp, Wh pre-permuted on the host)
 //   score   1/2 sum_l (mu_l^2 + e^lv_l - 1 - lv_l)       (lane-pair reduction)
@@ -162,9 +163,10 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     const int Q = g.Q, CPR = g.CPR, CPRP = g.CPRP, M = g.M, Mp = g.Mp, S = g.S;
     // staged super-rows: the tile's nv + Q - 1 plus spare rows read only by zero-weight chunks
     const int nrows = nv + Q - 1 + g.spare;
-    // LDS: the epilogue's weights (heads, decoder hidden layer, b1, bd1, u, head biases), then
-    // the segment, its row sums and the stream's statistics
-    // (with WH > 1 the segment's space is reused after the main loop to exchange partial sums)
+    // LDS: the epilogue's weights (heads, decoder hidden layer, b1, bd1, u, head biases) when
+    // CL, then the segment, the per-column statistics and offsets of a super-row, and the row
+    // sums (with WH > 1 the segment's space is reused after the main loop to exchange partial
+    // sums)
     constexpr int HP = 32 * HBT;
     constexpr int N_WHP = HBT * 16 * 64, N_WD1P = HBT * 8 * 64;
     constexpr int N_CONST = CL ? N_WHP + N_WD1P + 3 * HP + 32 : 0;
