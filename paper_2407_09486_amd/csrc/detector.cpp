@@ -151,7 +151,9 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
     const size_t xchg_bytes = g->WH > 1 ? static_cast<size_t>(g->NW) * std::min(g->NBW, 2) * 17 * 64 * sizeof(float) : 0;
     // the split bf16 layout keeps its epilogue weights in L2 to leave LDS to a 256-window tile
     g->cl = g->WH == 1;
-    g->lds_bytes = (g->cl ? n_const * sizeof(float) : 0) + std::max(seg_bytes, xchg_bytes) +
+    // (without the copied block, b1, bd1, u and the head biases still get LDS of their own)
+    const size_t n_small = 3 * static_cast<size_t>(g->Hp) + 32;
+    g->lds_bytes = (g->cl ? n_const : n_small) * sizeof(float) + std::max(seg_bytes, xchg_bytes) +
                    rows * 2 * sizeof(float) + 3 * sizeof(float) * static_cast<size_t>(g->S) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;

@@ -173,10 +173,6 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     constexpr int N_XCHG = WH > 1 ? NW * (NBW > 2 ? 2 : NBW) * (16 + 1) * 64 : 0;   // floats
     float *s_whp = reinterpret_cast<float *>(lds);
     float *s_wd1p = s_whp + N_WHP;
-    float *s_b1 = s_wd1p + N_WD1P;
-    float *s_bd1 = s_b1 + HP;
-    float *s_u = s_bd1 + HP;
-    float *s_bh = s_u + HP;
     uint4 *seg = lds + N_CONST / 4;
     const int rows_alloc = NB + Q - 1 + g.spare;
     const size_t seg_chunks = static_cast<size_t>(rows_alloc) * CPRP;
@@ -189,6 +185,11 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     int *coff = reinterpret_cast<int *>(crinv + SMp);
     float *rs = reinterpret_cast<float *>(coff + SMp);
     float *ps = rs + rows_alloc;
+    // b1, bd1, u and the head biases: inside the copied block when CL, else after the row sums
+    float *s_b1 = CL ? s_wd1p + N_WD1P : ps + rows_alloc;
+    float *s_bd1 = s_b1 + HP;
+    float *s_u = s_bd1 + HP;
+    float *s_bh = s_u + HP;
 
     if constexpr (CL) {
         // the host lays the epilogue weights out contiguously in this LDS order; copy them with
@@ -209,6 +210,14 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
         }
         for (int i = FULL + tid; i < N4; i += NT)
             dst[i] = src[i];
+    } else {
+        for (int i = tid; i < HP; i += NT) {
+            s_b1[i] = p.b1[i];
+            s_bd1[i] = p.bd1[i];
+            s_u[i] = p.u[i];
+        }
+        if (tid < 32)
+            s_bh[tid] = p.bh[tid];
     }
     for (int j = tid; j < SMp; j += NT) {
         const int tt = j / Mp;
@@ -507,7 +516,7 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const float wv = CL ? s_whp[(hbg * 16 + r) * 64 + lane] : p.whp[(hbg * 16 + r) * 64 + lane];
-                    const float bias = CL ? s_b1[hbg * 32 + crow(r, half)] : p.b1[hbg * 32 + crow(r, half)];
+                    const float bias = s_b1[hbg * 32 + crow(r, half)];
 #pragma unroll
                     for (int i = 0; i < NG; ++i)
                         z[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(
@@ -527,7 +536,7 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 #pragma unroll
                         for (int t = 0; t < 8; ++t) {
                             const int r = 8 * m + t;
-                            const float bias = CL ? s_b1[hbg * 32 + crow(r, half)] : p.b1[hbg * 32 + crow(r, half)];
+                            const float bias = s_b1[hbg * 32 + crow(r, half)];
                             hv[t] = act_fn<ACT>(acc[hb][g0 + i][r] + bias);
                         }
                         v8bf h_hi, h_lo;
@@ -563,7 +572,7 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
             kl[i] = 0.0f;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                z[i][r] += CL ? s_bh[crow(r, half)] : p.bh[crow(r, half)];
+                z[i][r] += s_bh[crow(r, half)];
                 if (r < 8)
                     kl[i] += z[i][r] * z[i][r];
                 else
@@ -617,8 +626,8 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int h = hbg * 32 + crow(r, half);
-                const float uh = CL ? s_u[h] : p.u[h];
-                const float bh = CL ? s_bd1[h] : p.bd1[h];
+                const float uh = s_u[h];
+                const float bh = s_bd1[h];
 #pragma unroll
                 for (int i = 0; i < NG; ++i)
                     dot[i] += uh * act_fn<ACT>(d[i][r] + bh);
