@@ -91,6 +91,8 @@ struct enova_detector_s {
     size_t stats_cap = 0;         // floats
     int64_t *tiles = nullptr;
     size_t tiles_cap = 0;         // entries
+    int *tile_map = nullptr;      // stream of each matrix-core block
+    size_t tile_map_cap = 0;      // entries
     int64_t *cal = nullptr;
     size_t cal_cap = 0;
     unsigned int *hist = nullptr; // 256 radix bins
@@ -205,8 +207,8 @@ void free_detector(enova_detector d)
 {
     if (!d)
         return;
-    void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->cal, d->hist, d->peaks, d->blk,
-                    d->gx};
+    void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->tile_map, d->cal, d->hist,
+                    d->peaks, d->blk, d->gx};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
@@ -675,6 +677,13 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
         const int64_t grid = (n_windows + g.Nb - 1) / g.Nb + n;
         if (grid > 0x7fffffffLL)
             return fail(ENOVA_EUNSUPPORTED, "too many tiles (%lld)", static_cast<long long>(grid));
+        st = ensure(&det->tile_map, &det->tile_map_cap, static_cast<size_t>(grid > 0 ? grid : 1));
+        if (st != ENOVA_OK)
+            return st;
+        e = launch_tile_map(det->tiles, n, grid, det->tile_map, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "tile map kernel");
+        p.tile_stream = det->tile_map;
         if (det->timing)
             (void)hipEventRecord(det->ev[2], stream);
         e = launch_score_mfma(g, p, grid, stream);

@@ -66,7 +66,8 @@ struct ScoreParams {
     const void *x;
     const int64_t *soff;
     const int64_t *woff;
-    const int64_t *tile_off;     // matrix-core kernel only
+    const int64_t *tile_off;     // matrix-core kernel only: first tile of each stream
+    const int *tile_stream;      // matrix-core kernel only: stream of each block (-1: none)
     int n_streams;
     int64_t n_windows;
     const float *mean;
@@ -99,6 +100,9 @@ hipError_t launch_ref_stats(const Geometry &g, const void *x, const int64_t *sof
 // (mode 1) calibration windows of stream s. out has n+1 entries.
 hipError_t launch_stream_scan(const Geometry &g, const int64_t *soff, const int64_t *woff, int n,
                               int mode, int div, int64_t *out, hipStream_t st);
+// map[b] = the stream whose tiles include tile b (tile_off has n+1 entries), -1 for
+// tile_off[n] <= b < grid.
+hipError_t launch_tile_map(const int64_t *tile_off, int n, int64_t grid, int *map, hipStream_t st);
 hipError_t launch_score_valu(const Geometry &g, const ScoreParams &p, hipStream_t st);
 hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st);
 hipError_t launch_flag(const float *scores, int64_t n, float thr, uint8_t *flags, hipStream_t st);

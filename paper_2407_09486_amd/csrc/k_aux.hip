@@ -109,6 +109,29 @@ __global__ __launch_bounds__(256) void k_ref_stats(const void *__restrict__ x,
     }
 }
 
+// Stream of every tile of the matrix-core kernel (one binary search per tile, done once here
+// with full occupancy instead of as a chain of dependent loads at the start of each tile).
+__global__ __launch_bounds__(256) void k_tile_map(const int64_t *__restrict__ tile_off, int n,
+                                                  int64_t grid, int *__restrict__ map)
+{
+    const int64_t total = tile_off[n];
+    for (int64_t b = blockIdx.x * 256LL + threadIdx.x; b < grid; b += static_cast<int64_t>(gridDim.x) * 256) {
+        int s = -1;
+        if (b < total) {
+            int lo = 0, hi = n - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (tile_off[mid] <= b)
+                    lo = mid;
+                else
+                    hi = mid - 1;
+            }
+            s = lo;
+        }
+        map[b] = s;
+    }
+}
+
 // Single-block exclusive scan of a per-stream count.
 __global__ __launch_bounds__(1024) void k_stream_scan(const int64_t *__restrict__ soff,
                                                       const int64_t *__restrict__ woff, int n,
@@ -460,6 +483,18 @@ hipError_t launch_stream_scan(const Geometry &g, const int64_t *soff, const int6
 {
     hipLaunchKernelGGL(k_stream_scan, dim3(1), dim3(1024), 0, st, soff, woff, n, mode, div, g.W,
                        g.S, g.ref_frac, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_map(const int64_t *tile_off, int n, int64_t grid, int *map, hipStream_t st)
+{
+    if (grid <= 0)
+        return hipSuccess;
+    int64_t blocks = (grid + 255) / 256;
+    if (blocks > 65536)
+        blocks = 65536;
+    hipLaunchKernelGGL(k_tile_map, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, tile_off, n,
+                       grid, map);
     return hipGetLastError();
 }
 

@@ -75,19 +75,6 @@ __device__ __forceinline__ float kl_g(float u)
     return expm1f(u) - u;
 }
 
-__device__ __forceinline__ int find_stream(const int64_t *off, int n, int64_t w)
-{
-    int lo = 0, hi = n - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (off[mid] <= w)
-            lo = mid;
-        else
-            hi = mid - 1;
-    }
-    return lo;
-}
-
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
 {
     const __bf16 ha = static_cast<__bf16>(a);
@@ -150,10 +137,9 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
 
     // ---- tile -> (stream, first window)
     const int64_t b = blockIdx.x;
-    const int64_t n_tiles = p.tile_off[p.n_streams];
-    if (b >= n_tiles)
+    const int s = p.tile_stream[b];
+    if (s < 0)
         return;
-    const int s = find_stream(p.tile_off, p.n_streams, b);
     const int64_t k0 = (b - p.tile_off[s]) * NB;
     const int64_t ns = p.woff[s + 1] - p.woff[s];
     const int nv = static_cast<int>(ns - k0 < NB ? ns - k0 : NB);
