@@ -225,88 +225,100 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     const int64_t eavail = (T - step0) * M;        // stream elements from super-row 0 on
     const bool linear = (Mp == M) && (((srow + step0) * M) % EPC == 0);
     const int64_t ebase = (srow + step0) * M;      // element index of super-row 0
-    // Each thread keeps SU chunk loads in flight before normalising them (one load per loop
-    // trip would serialise a full HBM round trip per chunk). Its chunks are tid + i*NT; their
-    // (row, column) advance by (NT / CPR, NT % CPR) with a carry instead of a division each.
+    // Each thread keeps SU chunk loads in flight, and the next SU are issued before the current
+    // ones are normalised (one load per loop trip would serialise a full HBM round trip per
+    // chunk). Its chunks are tid + i*NT; their (row, column) advance by (NT / CPR, NT % CPR)
+    // with a carry instead of a division each.
     constexpr int SU = 8;
     const int n_chunks = nrows * CPR;
     const int dr = NT / CPR, dc = NT - (NT / CPR) * CPR;
     int cr = tid / CPR, ccol = tid - (tid / CPR) * CPR;
-    for (int base = tid; base < n_chunks; base += NT * SU) {
-      uint4 raw[SU];
-      bool vec[SU];
+    auto load_batch = [&](int base, uint4 (&raw)[SU], bool (&vec)[SU]) {
 #pragma unroll
-      for (int u = 0; u < SU; ++u) {
-        const int idx = base + u * NT;
-        vec[u] = idx < n_chunks && linear && static_cast<int64_t>(idx + 1) * EPC <= eavail;
-        if (vec[u]) {
-            const int64_t e0 = ebase + static_cast<int64_t>(idx) * EPC;
-            if constexpr (DT == ENOVA_F32)
-                raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(p.x) + e0);
-            else
-                raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.x) + e0);
+        for (int u = 0; u < SU; ++u) {
+            const int idx = base + u * NT;
+            vec[u] = idx < n_chunks && linear && static_cast<int64_t>(idx + 1) * EPC <= eavail;
+            if (vec[u]) {
+                const int64_t e0 = ebase + static_cast<int64_t>(idx) * EPC;
+                if constexpr (DT == ENOVA_F32)
+                    raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(p.x) + e0);
+                else
+                    raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.x) + e0);
+            }
         }
-      }
+    };
+    auto store_batch = [&](int base, const uint4 (&raw)[SU], const bool (&vec)[SU]) {
 #pragma unroll
-      for (int u = 0; u < SU; ++u) {
-        const int idx = base + u * NT;
-        const int r = cr, c = ccol;
-        ccol += dc;
-        cr += dr;
-        if (ccol >= CPR) {
-            ccol -= CPR;
-            ++cr;
-        }
-        if (idx >= n_chunks)
-            continue;
-        const float *mu = cmean + c * EPC;
-        const float *ri = crinv + c * EPC;
-        float v[EPC];
-        if (vec[u]) {
-            if constexpr (DT == ENOVA_F32) {
-                v[0] = __uint_as_float(raw[u].x);
-                v[1] = __uint_as_float(raw[u].y);
-                v[2] = __uint_as_float(raw[u].z);
-                v[3] = __uint_as_float(raw[u].w);
+        for (int u = 0; u < SU; ++u) {
+            const int idx = base + u * NT;
+            const int r = cr, c = ccol;
+            ccol += dc;
+            cr += dr;
+            if (ccol >= CPR) {
+                ccol -= CPR;
+                ++cr;
+            }
+            if (idx >= n_chunks)
+                continue;
+            const float *mu = cmean + c * EPC;
+            const float *ri = crinv + c * EPC;
+            float v[EPC];
+            if (vec[u]) {
+                if constexpr (DT == ENOVA_F32) {
+                    v[0] = __uint_as_float(raw[u].x);
+                    v[1] = __uint_as_float(raw[u].y);
+                    v[2] = __uint_as_float(raw[u].z);
+                    v[3] = __uint_as_float(raw[u].w);
+                } else {
+                    v[0] = bf16_lo(raw[u].x);
+                    v[1] = bf16_hi(raw[u].x);
+                    v[2] = bf16_lo(raw[u].y);
+                    v[3] = bf16_hi(raw[u].y);
+                    v[4] = bf16_lo(raw[u].z);
+                    v[5] = bf16_hi(raw[u].z);
+                    v[6] = bf16_lo(raw[u].w);
+                    v[7] = bf16_hi(raw[u].w);
+                }
+#pragma unroll
+                for (int e = 0; e < EPC; ++e)
+                    v[e] = (v[e] - mu[e]) * ri[e];
             } else {
-                v[0] = bf16_lo(raw[u].x);
-                v[1] = bf16_hi(raw[u].x);
-                v[2] = bf16_lo(raw[u].y);
-                v[3] = bf16_hi(raw[u].y);
-                v[4] = bf16_lo(raw[u].z);
-                v[5] = bf16_hi(raw[u].z);
-                v[6] = bf16_lo(raw[u].w);
-                v[7] = bf16_hi(raw[u].w);
-            }
+                // padding, the stream's end, or a row start that is not 16-byte aligned
+                const int64_t rel = static_cast<int64_t>(r) * S * M;
 #pragma unroll
-            for (int e = 0; e < EPC; ++e)
-                v[e] = (v[e] - mu[e]) * ri[e];
-        } else {
-            // padding, the stream's end, or a row start that is not 16-byte aligned
-            const int64_t rel = static_cast<int64_t>(r) * S * M;
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                const int off = coff[c * EPC + e];
-                float val = 0.0f;
-                if (off >= 0 && rel + off < eavail)
-                    val = (load_x<DT>(p.x, ebase + rel + off) - mu[e]) * ri[e];
-                v[e] = val;
+                for (int e = 0; e < EPC; ++e) {
+                    const int off = coff[c * EPC + e];
+                    float val = 0.0f;
+                    if (off >= 0 && rel + off < eavail)
+                        val = (load_x<DT>(p.x, ebase + rel + off) - mu[e]) * ri[e];
+                    v[e] = val;
+                }
             }
+            uint4 out;
+            if constexpr (DT == ENOVA_F32) {
+                out.x = __float_as_uint(v[0]);
+                out.y = __float_as_uint(v[1]);
+                out.z = __float_as_uint(v[2]);
+                out.w = __float_as_uint(v[3]);
+            } else {
+                out.x = pack_bf16x2(v[0], v[1]);
+                out.y = pack_bf16x2(v[2], v[3]);
+                out.z = pack_bf16x2(v[4], v[5]);
+                out.w = pack_bf16x2(v[6], v[7]);
+            }
+            seg[r * CPRP + c] = out;
         }
-        uint4 out;
-        if constexpr (DT == ENOVA_F32) {
-            out.x = __float_as_uint(v[0]);
-            out.y = __float_as_uint(v[1]);
-            out.z = __float_as_uint(v[2]);
-            out.w = __float_as_uint(v[3]);
-        } else {
-            out.x = pack_bf16x2(v[0], v[1]);
-            out.y = pack_bf16x2(v[2], v[3]);
-            out.z = pack_bf16x2(v[4], v[5]);
-            out.w = pack_bf16x2(v[6], v[7]);
+    };
+    {
+        uint4 raw0[SU], raw1[SU];
+        bool vec0[SU], vec1[SU];
+        load_batch(tid, raw0, vec0);
+        for (int base = tid; base < n_chunks; base += 2 * NT * SU) {
+            load_batch(base + NT * SU, raw1, vec1);
+            store_batch(base, raw0, vec0);
+            load_batch(base + 2 * NT * SU, raw0, vec0);
+            store_batch(base + NT * SU, raw1, vec1);
         }
-        seg[r * CPRP + c] = out;
-      }
     }
     __syncthreads();
 
