@@ -9,7 +9,8 @@ Section IV-B ("Performance Detection Module") computes, in fp64:
   the Mean-Difference direction from the reconstruction (``core.c``);
 * the peaks-over-threshold threshold (the method of Siffer et al. cited in
   Section IV-B) fitted by maximum likelihood with Grimshaw's reduction, and the
-  "score exceeds threshold" flag.
+  "score exceeds threshold" flag;
+* its streaming form (SPOT, ``Spot``): per-stream thresholds updated score by score.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline leg
 may import this package. It shares no code with the HIP library and never
@@ -336,25 +337,17 @@ def grimshaw(Y):
     return best
 
 
-def pot_threshold(calib_scores, level=0.98, q=1e-3):
-    """Peaks-over-threshold anomaly threshold z_q over calibration scores.
+def pot_fit(t, n, Y, q=1e-3):
+    """z_q from the excesses Y over t among n observations (the tail model of Siffer et al.,
+    the peaks-over-threshold method Section IV-B cites).
 
-    t = the level-quantile (order statistic at ceil(level*n) - 1 of the sorted
-    scores), excesses Y = {c - t : c > t}; the tail above t is modelled by a
-    generalised Pareto distribution (Siffer et al., as cited in Section IV-B) and
+    The tail above t is a generalised Pareto distribution GPD(gamma, sigma) and
         z_q = t + sigma/gamma * ((q n / N_t)^(-gamma) - 1)   (gamma != 0)
         z_q = t - sigma * log(q n / N_t)                      (gamma = 0).
-    N_t >= 10: maximum likelihood (``grimshaw``); 2 <= N_t < 10: method of moments
-    with the unbiased sample variance; N_t <= 1 (or zero variance): z_q = t.
-    Returns (z_q, info dict).
+    N_t >= 10: maximum likelihood (``grimshaw``); 2 <= N_t < 10: method of moments with the
+    unbiased sample variance; N_t <= 1 (or zero variance): z_q = t. Returns (z_q, info dict).
     """
-    C = np.sort(np.asarray(calib_scores, np.float64).ravel())
-    n = C.size
-    if n == 0:
-        raise ValueError("no calibration scores")
-    idx = max(int(math.ceil(level * n)) - 1, 0)
-    t = float(C[idx])
-    Y = C[C > t] - t
+    Y = np.asarray(Y, np.float64)
     Nt = int(Y.size)
     info = {"t": t, "n": n, "n_peaks": Nt, "gamma": None, "sigma": None, "method": None}
     if Nt >= 10:
@@ -379,6 +372,72 @@ def pot_threshold(calib_scores, level=0.98, q=1e-3):
     else:
         z = t + sigma / gamma * (r ** (-gamma) - 1.0)
     return float(z), info
+
+
+def pot_threshold(calib_scores, level=0.98, q=1e-3):
+    """Peaks-over-threshold anomaly threshold z_q over calibration scores.
+
+    t = the level-quantile (order statistic at ceil(level*n) - 1 of the sorted scores),
+    excesses Y = {c - t : c > t}, z_q from ``pot_fit``. Returns (z_q, info dict).
+    """
+    C = np.sort(np.asarray(calib_scores, np.float64).ravel())
+    n = C.size
+    if n == 0:
+        raise ValueError("no calibration scores")
+    idx = max(int(math.ceil(level * n)) - 1, 0)
+    t = float(C[idx])
+    return pot_fit(t, n, C[C > t] - t, q)
+
+
+class Spot:
+    """Streaming peaks-over-threshold of one stream: SPOT of Siffer et al. (the POT method that
+    Section IV-B cites; Section V runs the detector inside a stream-computing job).
+
+    Start: ``pot_threshold`` over the stream's calibration scores gives t, the peaks Y and z_q,
+    with n = the number of calibration scores (no calibration score: t = z_q = +inf and the
+    model never changes, so the stream never flags). Then each new score s, in time order:
+      s > z_q          an alarm (flag 1); the model is left as it is;
+      t < s <= z_q     s - t joins the peaks, n += 1, and z_q is refitted (``pot_fit``) on all
+                       peaks with the new n;
+      s <= t           n += 1 only (z_q changes at the next peak);
+      s is NaN         flag 0, nothing changes.
+    Readings of this build: once ``peak_cap`` peaks are stored the model is frozen (later
+    scores are only compared); a stream's level and q are those of the batch threshold.
+    """
+
+    def __init__(self, calib_scores, level=0.98, q=1e-3, peak_cap=None):
+        C = np.sort(np.asarray(calib_scores, np.float64).ravel())
+        self.q = q
+        self.cap = peak_cap
+        if C.size == 0:
+            self.t = self.z = math.inf
+            self.n = 0
+            self.Y = []
+            return
+        idx = max(int(math.ceil(level * C.size)) - 1, 0)
+        self.t = float(C[idx])
+        self.Y = [float(v) for v in C[C > self.t] - self.t]
+        self.n = int(C.size)
+        if self.cap is not None and len(self.Y) > self.cap:
+            raise ValueError("more calibration peaks than the peak capacity")
+        self.z, _ = pot_fit(self.t, self.n, self.Y, q)
+
+    def frozen(self):
+        return math.isinf(self.t) or (self.cap is not None and len(self.Y) >= self.cap)
+
+    def step(self, s):
+        """Process one score; returns its flag (0/1)."""
+        if math.isnan(s):
+            return 0
+        if s > self.z:
+            return 1
+        if self.frozen():
+            return 0
+        self.n += 1
+        if s > self.t:
+            self.Y.append(s - self.t)
+            self.z, _ = pot_fit(self.t, self.n, self.Y, self.q)
+        return 0
 
 
 def calibration_scores(scores, stream_offsets, *, window, stride, ref_frac=0.5):
