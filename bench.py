@@ -38,7 +38,7 @@ def flops_per_window(cfg) -> int:
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for name in ("k_score_mfma.hip", "internal.h"):
+    for name in ("k_score_mfma.hip", "mfma_common.h", "internal.h"):
         with open(os.path.join(ROOT, "paper_2407_09486_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]

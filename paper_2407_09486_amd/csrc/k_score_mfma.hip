@@ -11,26 +11,17 @@
 // accumulation). Window n's row of V is never materialised: its chunk kappa = q*CPR + c is
 // chunk c of LDS super-row (n + q), so one staged element feeds up to Q windows.
 //
-// The accumulator layout of a 32x32 MFMA block (lane l, register r holds row
-// 8*(r/4) + 4*(l/32) + r%4 and column l%32) is exactly the B-operand layout a following
-// 32x32x2 fp32 MFMA needs when its reduction index is permuted the same way (and, eight
-// registers at a time, the B operand of a 32x32x16 bf16 MFMA), so the rest of the detector
-// chains on the matrix cores without leaving registers:
-//   hidden  h  = act(C + b1)
-//   heads   [mu; logvar] = Wh h + bh          (32 x Hp, Wh pre-permuted on the host)
-//   score   1/2 sum_l (mu_l^2 + e^lv_l - 1 - lv_l)       (lane-pair reduction)
-//   decoder hd = act(Wd1 mu + bd1),  mean(m') = (u . hd + sum bd2) / D
-//   md      mean(v) - mean(m'),  mean(v) from per-super-row sums kept in LDS.
+// The posterior heads, the KL score and the decoder's hidden layer then chain on the matrix
+// cores straight from the accumulators (score_epilogue); the md adds the window mean of the
+// staged inputs from per-super-row sums kept in LDS.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
+#include "mfma_common.h"
 
 namespace enova {
 
 namespace {
-
-typedef float v16f __attribute__((ext_vector_type(16)));
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 struct MfmaShape {
     int M, S, W, Mp, Q, CPR, CPRP, KC;
@@ -38,78 +29,6 @@ struct MfmaShape {
     int tail_rows;   // steps of the window's last super-row that belong to the window
     float inv_d;
 };
-
-template <int DT>
-__device__ __forceinline__ float load_x(const void *x, int64_t idx)
-{
-    if constexpr (DT == ENOVA_F32) {
-        return static_cast<const float *>(x)[idx];
-    } else {
-        uint32_t b = static_cast<const uint16_t *>(x)[idx];
-        return __uint_as_float(b << 16);
-    }
-}
-
-template <int ACT>
-__device__ __forceinline__ float act_fn(float a)
-{
-    if constexpr (ACT == ENOVA_TANH)
-        return tanhf(a);
-    else
-        return a < 0.0f ? 0.0f : a;   // ReLU; a NaN passes through
-}
-
-// e^u - 1 - u without cancellation near 0: Taylor series through u^8 for |u| < 0.5.
-__device__ __forceinline__ float kl_g(float u)
-{
-    if (fabsf(u) < 0.5f) {
-        float p = 1.0f / 40320.0f;
-        p = p * u + 1.0f / 5040.0f;
-        p = p * u + 1.0f / 720.0f;
-        p = p * u + 1.0f / 120.0f;
-        p = p * u + 1.0f / 24.0f;
-        p = p * u + 1.0f / 6.0f;
-        p = p * u + 0.5f;
-        return (u * u) * p;
-    }
-    return expm1f(u) - u;
-}
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
-{
-    const __bf16 ha = static_cast<__bf16>(a);
-    const __bf16 hb = static_cast<__bf16>(b);
-    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, ha)) |
-           (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, hb)) << 16);
-}
-
-__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
-
-// x = hi + lo as two bf16 vectors, lo the rounded remainder. With a bf16 weight split the same
-// way, hi*hi + hi*lo + lo*hi (fp32 accumulation) carries about 16 significant bits: the bf16
-// workload's posterior heads and decoder layer run on three bf16 matrix ops instead of the
-// eight times slower fp32 ones.
-__device__ __forceinline__ void split_bf16x8(const float (&x)[8], v8bf &hi, v8bf &lo)
-{
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const __bf16 h = static_cast<__bf16>(x[t]);
-        hi[t] = h;
-        lo[t] = static_cast<__bf16>(x[t] - static_cast<float>(h));
-    }
-}
-
-__device__ __forceinline__ v16f mfma3_bf16(uint4 a_hi, uint4 a_lo, v8bf b_hi, v8bf b_lo, v16f c)
-{
-    const v8bf ah = __builtin_bit_cast(v8bf, a_hi), al = __builtin_bit_cast(v8bf, a_lo);
-    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b_hi, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, b_lo, c, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, b_hi, c, 0, 0, 0);
-}
-
-// Row of the accumulator register r for lane half g inside a 32x32 block.
-__device__ __forceinline__ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
 // Wave layout: the NW waves form WH groups along the hidden rows and NW/WH groups along the
 // windows. A wave owns HB 32-row hidden blocks and NBW 32-window blocks; with WH > 1 the waves
@@ -156,9 +75,11 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
     constexpr int HP = 32 * HBT;
     constexpr int N_WHP = HBT * 16 * 64, N_WD1P = HBT * 8 * 64;
     constexpr int N_CONST = CL ? N_WHP + N_WD1P + 3 * HP + 32 : 0;
-    constexpr int N_XCHG = WH > 1 ? NW * (NBW > 2 ? 2 : NBW) * (16 + 1) * 64 : 0;   // floats
+    constexpr int N_XCHG = WH > 1 ? epi_xchg_floats(NW, NBW) : 0;   // floats
     float *s_whp = reinterpret_cast<float *>(lds);
     float *s_wd1p = s_whp + N_WHP;
+    const float *e_whp = CL ? s_whp : p.whp;      // epilogue fragments: the copied block, or L2
+    const float *e_wd1p = CL ? s_wd1p : p.wd1p;
     uint4 *seg = lds + N_CONST / 4;
     const int rows_alloc = NB + Q - 1 + g.spare;
     const size_t seg_chunks = static_cast<size_t>(rows_alloc) * CPRP;
@@ -490,187 +411,29 @@ void k_score_mfma(ScoreParams p, MfmaShape g)
             return;
     }
 
-    // ---- epilogue, NG window blocks per pass (weights from LDS, or L2 when the segment needs
-    // the LDS); the NG blocks of a pass run as independent MFMA chains
-    constexpr int NG = NBW > 2 ? 2 : NBW;
-    float *xz = reinterpret_cast<float *>(seg);            // [NW][NG][16][64] head partials
-    float *xd = xz + NW * NG * 16 * 64;                    // [NW][NG][64] decoder partials
+    // ---- epilogue (weights from LDS when CL, else from L2)
     const bool storer = WH == 1 || (wh == 0 && wave_active);
-#pragma unroll
-    for (int g0 = 0; g0 < NBW; g0 += NG) {
-        // hidden activations (bias + act, one 32-row block at a time) feed the posterior heads:
-        // rows 0..15 mean, 16..31 log-variance (this wave's share of the hidden rows)
-        v16f z[NG];
-#pragma unroll
-        for (int i = 0; i < NG; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                z[i][r] = 0.0f;
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-            const int hbg = wh * HB + hb;
-            if constexpr (DT == ENOVA_F32) {
-                // reduction index of matrix op r: hidden rows crow(r, 0), crow(r, 1)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float wv = CL ? s_whp[(hbg * 16 + r) * 64 + lane] : p.whp[(hbg * 16 + r) * 64 + lane];
-                    const float bias = s_b1[hbg * 32 + crow(r, half)];
-#pragma unroll
-                    for (int i = 0; i < NG; ++i)
-                        z[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            wv, act_fn<ACT>(acc[hb][g0 + i][r] + bias), z[i], 0, 0, 0);
-                }
-            } else {
-                // reduction slot (g, t) of op m: hidden row crow(8m + t, g); weights packed as
-                // [hidden block][m][hi, lo][lane] 16-byte fragments
-                const uint4 *wsrc = reinterpret_cast<const uint4 *>(CL ? s_whp : p.whp);
-#pragma unroll
-                for (int m = 0; m < 2; ++m) {
-                    const uint4 wa_hi = wsrc[((hbg * 2 + m) * 2 + 0) * 64 + lane];
-                    const uint4 wa_lo = wsrc[((hbg * 2 + m) * 2 + 1) * 64 + lane];
-#pragma unroll
-                    for (int i = 0; i < NG; ++i) {
-                        float hv[8];
-#pragma unroll
-                        for (int t = 0; t < 8; ++t) {
-                            const int r = 8 * m + t;
-                            const float bias = s_b1[hbg * 32 + crow(r, half)];
-                            hv[t] = act_fn<ACT>(acc[hb][g0 + i][r] + bias);
-                        }
-                        v8bf h_hi, h_lo;
-                        split_bf16x8(hv, h_hi, h_lo);
-                        z[i] = mfma3_bf16(wa_hi, wa_lo, h_hi, h_lo, z[i]);
-                    }
-                }
-            }
+    const EpiArgs ea{e_whp, e_wd1p, s_b1, s_bd1, s_u, s_bh, reinterpret_cast<float *>(seg),
+                     lane, half, wave, wh, wn};
+    score_epilogue<DT, HB, NBW, WH, NW, ACT>(acc, ea, [&](int nb, float sc, float dot) __attribute__((always_inline)) {
+        // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
+        const int n = wn * NBW * 32 + nb * 32 + (lane & 31);
+        float vsum = 0.0f;
+        const int row0 = rb[nb] / CPRP;
+        for (int qq = half; qq < Q - 1; qq += 2)
+            vsum += rs[row0 + qq];
+        if (((Q - 1) & 1) == half)
+            vsum += ps[row0 + Q - 1];
+        vsum += __shfl_xor(vsum, 32);
+        if (storer && half == 0 && n < nv) {
+            const int64_t w = p.woff[s] + k0 + n;
+            p.scores[w] = sc;
+            if (p.md)
+                p.md[w] = vsum * g.inv_d - (dot + p.sum_bd2) * g.inv_d;
+            if (p.write_flags)
+                p.flags[w] = sc > p.threshold ? 1 : 0;
         }
-        if constexpr (WH > 1) {
-            // every wave of the window group adds the WH partials in the same fixed order
-            __syncthreads();          // the segment, or the previous pass's exchange, is no longer read
-#pragma unroll
-            for (int i = 0; i < NG; ++i)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    xz[((wave * NG + i) * 16 + r) * 64 + lane] = z[i][r];
-            __syncthreads();
-#pragma unroll
-            for (int i = 0; i < NG; ++i)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    float t = 0.0f;
-#pragma unroll
-                    for (int w2 = 0; w2 < WH; ++w2)
-                        t += xz[(((wn * WH + w2) * NG + i) * 16 + r) * 64 + lane];
-                    z[i][r] = t;
-                }
-        }
-        float kl[NG];
-#pragma unroll
-        for (int i = 0; i < NG; ++i) {
-            kl[i] = 0.0f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                z[i][r] += s_bh[crow(r, half)];
-                if (r < 8)
-                    kl[i] += z[i][r] * z[i][r];
-                else
-                    kl[i] += kl_g(z[i][r]);
-            }
-            kl[i] += __shfl_xor(kl[i], 32);
-        }
-        // decoder hidden layer at z = mu, dotted with the column sums of Wd2 (mu is held in
-        // registers 0..7: latent crow(r, half))
-        float dot[NG];
-#pragma unroll
-        for (int i = 0; i < NG; ++i)
-            dot[i] = 0.0f;
-        v8bf mu_hi[NG], mu_lo[NG];
-        if constexpr (DT == ENOVA_BF16) {
-#pragma unroll
-            for (int i = 0; i < NG; ++i) {
-                float mv[8];
-#pragma unroll
-                for (int t = 0; t < 8; ++t)
-                    mv[t] = z[i][t];
-                split_bf16x8(mv, mu_hi[i], mu_lo[i]);
-            }
-        }
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-            const int hbg = wh * HB + hb;
-            v16f d[NG];
-#pragma unroll
-            for (int i = 0; i < NG; ++i)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    d[i][r] = 0.0f;
-            if constexpr (DT == ENOVA_F32) {
-#pragma unroll
-                for (int r = 0; r < 8; ++r) {
-                    const float wv = CL ? s_wd1p[(hbg * 8 + r) * 64 + lane] : p.wd1p[(hbg * 8 + r) * 64 + lane];
-#pragma unroll
-                    for (int i = 0; i < NG; ++i)
-                        d[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[i][r], d[i], 0, 0, 0);
-                }
-            } else {
-                // weights packed as [hidden block][hi, lo][lane] 16-byte fragments
-                const uint4 *wsrc = reinterpret_cast<const uint4 *>(CL ? s_wd1p : p.wd1p);
-                const uint4 wd_hi = wsrc[(hbg * 2 + 0) * 64 + lane];
-                const uint4 wd_lo = wsrc[(hbg * 2 + 1) * 64 + lane];
-#pragma unroll
-                for (int i = 0; i < NG; ++i)
-                    d[i] = mfma3_bf16(wd_hi, wd_lo, mu_hi[i], mu_lo[i], d[i]);
-            }
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int h = hbg * 32 + crow(r, half);
-                const float uh = s_u[h];
-                const float bh = s_bd1[h];
-#pragma unroll
-                for (int i = 0; i < NG; ++i)
-                    dot[i] += uh * act_fn<ACT>(d[i][r] + bh);
-            }
-        }
-        if constexpr (WH > 1) {
-#pragma unroll
-            for (int i = 0; i < NG; ++i)
-                xd[(wave * NG + i) * 64 + lane] = dot[i];
-            __syncthreads();
-#pragma unroll
-            for (int i = 0; i < NG; ++i) {
-                float t = 0.0f;
-#pragma unroll
-                for (int w2 = 0; w2 < WH; ++w2)
-                    t += xd[((wn * WH + w2) * NG + i) * 64 + lane];
-                dot[i] = t;
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < NG; ++i) {
-            const int nb = g0 + i;
-            dot[i] += __shfl_xor(dot[i], 32);
-
-            // window mean of the staged inputs: super-rows rb .. rb+Q-1, the last one partially
-            const int n = wn * NBW * 32 + nb * 32 + (lane & 31);
-            float vsum = 0.0f;
-            const int row0 = rb[nb] / CPRP;
-            for (int qq = half; qq < Q - 1; qq += 2)
-                vsum += rs[row0 + qq];
-            if (((Q - 1) & 1) == half)
-                vsum += ps[row0 + Q - 1];
-            vsum += __shfl_xor(vsum, 32);
-
-            if (storer && half == 0 && n < nv) {
-                const int64_t w = p.woff[s] + k0 + n;
-                const float sc = 0.5f * kl[i];
-                p.scores[w] = sc;
-                if (p.md)
-                    p.md[w] = vsum * g.inv_d - (dot[i] + p.sum_bd2) * g.inv_d;
-                if (p.write_flags)
-                    p.flags[w] = sc > p.threshold ? 1 : 0;
-            }
-        }
-    }
+    });
 }
 
 using ScoreKernel = void (*)(ScoreParams, MfmaShape);
