@@ -166,6 +166,67 @@ enova_status enova_detect_threshold(enova_detector det, const float *scores,
                                     float *out_threshold, double *out_info, uint8_t *out_flags,
                                     hipStream_t stream);
 
+/*
+ * Streaming detection. Section V runs the detector inside a stream-computing job, and the
+ * peaks-over-threshold method Section IV-B cites (Siffer et al. 2017) is a streaming one (SPOT).
+ * A streaming set holds n streams that advance together: every enova_stream_push appends one
+ * step of M metrics to each stream; once every stream has seen c = W + k*S steps (k >= 0), the
+ * push scores each stream's newest window (its last W steps, normalised with the reference
+ * statistics given at creation) exactly as enova_detect_score scores that window, and updates
+ * each stream's own threshold by SPOT:
+ *   start   t_s = the order statistic at ceil(level*n_s) - 1 of the stream's n_s calibration
+ *           scores, its peaks {c - t_s : c > t_s} in calibration order, and z_s fitted as by
+ *           enova_detect_threshold over that stream alone (no calibration score: t_s = z_s =
+ *           +inf and the stream never changes, so it never flags);
+ *   s > z_s          flag 1; the stream's model is left as it is (an alarm is not learnt);
+ *   t_s < s <= z_s   flag 0; s - t_s joins the peaks, n_s += 1, z_s is refitted on all peaks;
+ *   s <= t_s         flag 0; n_s += 1 (z_s moves at the next peak);   NaN: flag 0, no change.
+ * Once a stream stores peak_cap peaks its model is frozen (its scores are still compared).
+ * The refits run on the device (one block per stream with a new peak) with the batch fit's
+ * method; a push is asynchronous on `stream`. Calls on one streaming set must not overlap, and
+ * the detector must outlive its streaming sets; the set uses the detector's matrix-core
+ * weights (EUNSUPPORTED for a shape the matrix-core kernel does not take).
+ */
+typedef struct enova_stream_s *enova_stream;   /* opaque; owned by the library */
+
+/*
+ *   n_streams        >= 1
+ *   ref_mean, ref_std  device [n][M] float (e.g. from enova_detect_ref_stats); copied
+ *   calib_scores     device float: stream s's calibration scores at
+ *                    [calib_offsets[s], calib_offsets[s+1]), e.g. its windows inside its
+ *                    reference prefix as scored by enova_detect_score
+ *   calib_offsets    HOST [n+1] int64, [0] = 0, non-decreasing
+ *   level, q         in (0, 1), as for enova_detect_threshold
+ *   peak_cap         >= 1: peaks stored per stream (device memory n * peak_cap * 8 bytes)
+ * Synchronises `stream`. Errors: EINVAL (arguments; a stream whose calibration peaks exceed
+ * peak_cap), ENUMERIC (a non-finite calibration score), EUNSUPPORTED, ENOMEM, EHIP.
+ */
+enova_status enova_stream_create(enova_detector det, int32_t n_streams, const float *ref_mean,
+                                 const float *ref_std, const float *calib_scores,
+                                 const int64_t *calib_offsets, double level, double q,
+                                 int32_t peak_cap, enova_stream *out, hipStream_t stream);
+
+/*
+ *   x_step       device [n][M], the detector's dtype: the next step of every stream
+ *   out_scores   device [n] float or NULL: the newest window's score when a window was due
+ *   out_md       device [n] float or NULL: its md
+ *   out_flags    device [n] uint8 or NULL: 1 where the score exceeds the stream's threshold
+ *                (as it stood before this score)
+ *   out_due      HOST int32 or NULL: 1 if this push scored windows, else 0 (then nothing is
+ *                written to the device outputs)
+ * Asynchronous on `stream`. Errors: EINVAL, EHIP.
+ */
+enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_scores, float *out_md,
+                               uint8_t *out_flags, int32_t *out_due, hipStream_t stream);
+
+/* Per-stream SPOT state into HOST arrays [n] (each may be NULL): t, z, n, stored peaks.
+ * Synchronises `stream`. */
+enova_status enova_stream_state(enova_stream s, double *t, double *z, int64_t *n, int32_t *n_peaks,
+                                hipStream_t stream);
+
+/* Free a streaming set (synchronises the device). NULL is a no-op. */
+enova_status enova_stream_destroy(enova_stream s);
+
 /* flags[i] = scores[i] > threshold for i < n_windows (device pointers). Asynchronous. */
 enova_status enova_detect_flag(enova_detector det, const float *scores, int64_t n_windows,
                                float threshold, uint8_t *out_flags, hipStream_t stream);

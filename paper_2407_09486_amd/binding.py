@@ -24,7 +24,8 @@ ENOVA_KERNEL_AUTO, ENOVA_KERNEL_VALU, ENOVA_KERNEL_MFMA = 0, 1, 2
 EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_offsets",
            "enova_detect_ref_stats", "enova_detect_score", "enova_detect_threshold",
            "enova_detect_flag", "enova_detect_set_timing", "enova_detect_kernel_times",
-           "enova_detect_kernel_kind", "enova_status_str", "enova_last_error"]
+           "enova_detect_kernel_kind", "enova_stream_create", "enova_stream_push",
+           "enova_stream_state", "enova_stream_destroy", "enova_status_str", "enova_last_error"]
 
 
 class EnovaError(RuntimeError):
@@ -69,6 +70,10 @@ def lib():
     L.enova_detect_set_timing.argtypes = [P, I32]
     L.enova_detect_kernel_times.argtypes = [P, P, P]
     L.enova_detect_kernel_kind.argtypes = [P, P]
+    L.enova_stream_create.argtypes = [P, I32, P, P, P, P, D, D, I32, ctypes.POINTER(P), P]
+    L.enova_stream_push.argtypes = [P, P, P, P, P, P, P]
+    L.enova_stream_state.argtypes = [P, P, P, P, P, P]
+    L.enova_stream_destroy.argtypes = [P]
     for name in EXPORTS[:-2]:
         getattr(L, name).restype = st
     L.enova_status_str.argtypes = [st]
@@ -186,6 +191,43 @@ def enova_detect_kernel_kind(handle):
     return k.value
 
 
+def enova_stream_create(handle, n_streams, ref_mean, ref_std, calib_scores, calib_offsets_host,
+                        level=0.98, q=1e-3, peak_cap=4096, stream=None):
+    """Returns the streaming-set handle (int). calib_offsets_host: numpy int64 [n+1]."""
+    off = np.ascontiguousarray(calib_offsets_host, dtype=np.int64)
+    h = ctypes.c_void_p()
+    _check(lib().enova_stream_create(ctypes.c_void_p(handle), int(n_streams), _dptr(ref_mean), _dptr(ref_std),
+                                     _dptr(calib_scores), _hptr(off), float(level), float(q), int(peak_cap),
+                                     ctypes.byref(h), _stream(stream)),
+           "enova_stream_create")
+    return h.value
+
+
+def enova_stream_push(shandle, x_step, out_scores=None, out_md=None, out_flags=None, stream=None):
+    """Returns 1 if the push scored windows, else 0."""
+    due = ctypes.c_int32()
+    _check(lib().enova_stream_push(ctypes.c_void_p(shandle), _dptr(x_step), _dptr(out_scores), _dptr(out_md),
+                                   _dptr(out_flags), ctypes.byref(due), _stream(stream)),
+           "enova_stream_push")
+    return due.value
+
+
+def enova_stream_state(shandle, n_streams, stream=None):
+    """Returns (t, z, n, n_peaks) as numpy arrays."""
+    t = np.zeros(n_streams, np.float64)
+    z = np.zeros(n_streams, np.float64)
+    n = np.zeros(n_streams, np.int64)
+    k = np.zeros(n_streams, np.int32)
+    _check(lib().enova_stream_state(ctypes.c_void_p(shandle), _hptr(t), _hptr(z), _hptr(n), _hptr(k),
+                                    _stream(stream)),
+           "enova_stream_state")
+    return t, z, n, k
+
+
+def enova_stream_destroy(shandle):
+    _check(lib().enova_stream_destroy(ctypes.c_void_p(shandle)), "enova_stream_destroy")
+
+
 # ----------------------------------------------------------------------------- convenience
 def make_config(metrics, window, stride, hidden, latent=16, dtype="f32", act="relu",
                 kernel="auto", ref_frac=0.5) -> enova_detect_config:
@@ -245,6 +287,34 @@ class Detector:
         thr, info = enova_detect_threshold(self.handle, scores, stream_offsets, window_offsets, n, nw,
                                            level, q, fl, stream)
         return thr, info, fl
+
+
+class StreamSet:
+    """Owns one streaming-set handle of a Detector (which must stay open)."""
+
+    def __init__(self, det: Detector, ref_mean, ref_std, calib_scores, calib_offsets_host, level=0.98,
+                 q=1e-3, peak_cap=4096, stream=None):
+        self.det = det
+        self.n = len(calib_offsets_host) - 1
+        self.handle = enova_stream_create(det.handle, self.n, ref_mean, ref_std, calib_scores,
+                                          calib_offsets_host, level, q, peak_cap, stream)
+
+    def push(self, x_step, scores=None, md=None, flags=None, stream=None):
+        return enova_stream_push(self.handle, x_step, scores, md, flags, stream)
+
+    def state(self, stream=None):
+        return enova_stream_state(self.handle, self.n, stream)
+
+    def close(self):
+        if self.handle:
+            enova_stream_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def weights_for_library(wt, dtype="f32") -> dict:

@@ -906,3 +906,199 @@ enova_status enova_detect_kernel_kind(enova_detector det, int32_t *kind)
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------------------------
+// Streaming detection
+// ---------------------------------------------------------------------------------------------
+struct enova_stream_s {
+    enova_detector det = nullptr;
+    int n = 0;
+    int64_t steps = 0;            // steps pushed so far (the same for every stream)
+    double q = 1e-3;
+    void *ring = nullptr;         // [n][2W][M]
+    float *mean = nullptr, *std = nullptr;   // [n][M]
+    float *scores = nullptr;      // [n] when the caller does not ask for scores
+    SpotState spot{};
+};
+
+namespace {
+
+void free_stream(enova_stream s)
+{
+    if (!s)
+        return;
+    void *ptrs[] = {s->ring, s->mean, s->std, s->scores, s->spot.t, s->spot.z, s->spot.cnt,
+                    s->spot.npk, s->spot.peaks, s->spot.mark, s->spot.err};
+    for (void *p : ptrs)
+        if (p)
+            (void)hipFree(p);
+    delete s;
+}
+
+template <typename T>
+enova_status dev_alloc(T **dst, size_t count)
+{
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(dst), std::max<size_t>(count, 1) * sizeof(T));
+    if (e != hipSuccess) {
+        *dst = nullptr;
+        return fail(ENOVA_ENOMEM, "hipMalloc(%zu): %s", count * sizeof(T), hipGetErrorString(e));
+    }
+    return ENOVA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+enova_status enova_stream_create(enova_detector det, int32_t n, const float *ref_mean, const float *ref_std,
+                                 const float *calib_scores, const int64_t *calib_offsets, double level,
+                                 double q, int32_t peak_cap, enova_stream *out, hipStream_t stream)
+{
+    if (!det || !ref_mean || !ref_std || !calib_offsets || !out)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    *out = nullptr;
+    if (n < 1)
+        return fail(ENOVA_EINVAL, "n_streams must be >= 1");
+    if (!(level > 0.0 && level < 1.0) || !(q > 0.0 && q < 1.0))
+        return fail(ENOVA_EINVAL, "level and q must lie in (0, 1)");
+    if (peak_cap < 1)
+        return fail(ENOVA_EINVAL, "peak_cap must be >= 1");
+    if (calib_offsets[0] != 0)
+        return fail(ENOVA_EINVAL, "calib_offsets[0] must be 0");
+    for (int32_t i = 0; i < n; ++i)
+        if (calib_offsets[i + 1] < calib_offsets[i])
+            return fail(ENOVA_EINVAL, "calib_offsets must be non-decreasing");
+    const int64_t n_cal = calib_offsets[n];
+    if (n_cal > 0 && !calib_scores)
+        return fail(ENOVA_EINVAL, "calib_scores is NULL");
+    const Geometry &g = det->g;
+    if (det->kind != 2 || !stream_score_supported(g))
+        return fail(ENOVA_EUNSUPPORTED, "streaming needs the matrix-core kernel's shapes");
+    DeviceGuard dg(det->device);
+    hipError_t e = prepare_stream_score(g);
+    if (e != hipSuccess)
+        return hip_fail(e, "streaming kernel attributes");
+
+    enova_stream s = new (std::nothrow) enova_stream_s;
+    if (!s)
+        return fail(ENOVA_ENOMEM, "host allocation");
+    s->det = det;
+    s->n = n;
+    s->q = q;
+    const size_t esz = g.dtype == ENOVA_F32 ? 4 : 2;
+    const size_t nm = static_cast<size_t>(n) * g.M;
+    enova_status st = ENOVA_OK;
+    int64_t *d_off = nullptr;
+    if ((st = dev_alloc(reinterpret_cast<unsigned char **>(&s->ring), nm * 2 * g.W * esz)) != ENOVA_OK ||
+        (st = dev_alloc(&s->mean, nm)) != ENOVA_OK || (st = dev_alloc(&s->std, nm)) != ENOVA_OK ||
+        (st = dev_alloc(&s->scores, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.t, n)) != ENOVA_OK ||
+        (st = dev_alloc(&s->spot.z, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.cnt, n)) != ENOVA_OK ||
+        (st = dev_alloc(&s->spot.npk, n)) != ENOVA_OK ||
+        (st = dev_alloc(&s->spot.peaks, static_cast<size_t>(n) * peak_cap)) != ENOVA_OK ||
+        (st = dev_alloc(&s->spot.mark, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.err, 1)) != ENOVA_OK ||
+        (st = dev_alloc(&d_off, static_cast<size_t>(n) + 1)) != ENOVA_OK) {
+        (void)hipFree(d_off);
+        free_stream(s);
+        return st;
+    }
+    s->spot.cap = peak_cap;
+    int err = 0;
+    if ((e = hipMemsetAsync(s->ring, 0, nm * 2 * g.W * esz, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(s->mean, ref_mean, nm * sizeof(float), hipMemcpyDeviceToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(s->std, ref_std, nm * sizeof(float), hipMemcpyDeviceToDevice, stream)) != hipSuccess ||
+        (e = hipMemsetAsync(s->spot.err, 0, sizeof(int), stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(d_off, calib_offsets, (static_cast<size_t>(n) + 1) * sizeof(int64_t),
+                            hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = launch_spot_init(n_cal > 0 ? calib_scores : s->scores, d_off, n, level, s->spot, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(&err, s->spot.err, sizeof(int), hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(stream)) != hipSuccess) {
+        (void)hipFree(d_off);
+        free_stream(s);
+        return hip_fail(e, "streaming set start");
+    }
+    (void)hipFree(d_off);
+    if (err == 2) {
+        free_stream(s);
+        return fail(ENOVA_ENUMERIC, "non-finite calibration score");
+    }
+    if (err == 1) {
+        free_stream(s);
+        return fail(ENOVA_EINVAL, "a stream's calibration peaks exceed peak_cap");
+    }
+    if ((e = launch_spot_fit(n, q, s->spot, stream)) != hipSuccess || (e = hipStreamSynchronize(stream)) != hipSuccess) {
+        free_stream(s);
+        return hip_fail(e, "streaming threshold fit");
+    }
+    *out = s;
+    return ENOVA_OK;
+}
+
+enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_scores, float *out_md,
+                               uint8_t *out_flags, int32_t *out_due, hipStream_t stream)
+{
+    if (!s || !x_step)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    enova_detector det = s->det;
+    const Geometry &g = det->g;
+    DeviceGuard dg(det->device);
+    hipError_t e = launch_stream_append(g, x_step, s->n, s->steps, s->ring, stream);
+    if (e != hipSuccess)
+        return hip_fail(e, "streaming append kernel");
+    s->steps += 1;
+    const bool due = s->steps >= g.W && (s->steps - g.W) % g.S == 0;
+    if (out_due)
+        *out_due = due ? 1 : 0;
+    if (!due)
+        return ENOVA_OK;
+    StreamScoreParams p{};
+    p.ring = s->ring;
+    p.n_streams = s->n;
+    p.first_slot = static_cast<int>(s->steps % g.W);
+    p.mean = s->mean;
+    p.std = s->std;
+    p.w1p = static_cast<const uint4 *>(det->w1p);
+    p.whp = det->whp;
+    p.wd1p = det->wd1p;
+    p.b1 = det->b1;
+    p.bd1 = det->bd1;
+    p.u = det->u;
+    p.bh = det->bh;
+    p.sum_bd2 = det->sum_bd2;
+    p.scores = out_scores ? out_scores : s->scores;
+    p.md = out_md;
+    if ((e = launch_stream_score(g, p, stream)) != hipSuccess)
+        return hip_fail(e, "streaming scoring kernel");
+    if ((e = launch_spot_update(p.scores, s->n, s->spot, out_flags, stream)) != hipSuccess ||
+        (e = launch_spot_fit(s->n, s->q, s->spot, stream)) != hipSuccess)
+        return hip_fail(e, "streaming threshold kernels");
+    return ENOVA_OK;
+}
+
+enova_status enova_stream_state(enova_stream s, double *t, double *z, int64_t *n, int32_t *n_peaks,
+                                hipStream_t stream)
+{
+    if (!s)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(s->det->device);
+    const size_t k = static_cast<size_t>(s->n);
+    hipError_t e = hipSuccess;
+    if ((t && (e = hipMemcpyAsync(t, s->spot.t, k * sizeof(double), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
+        (z && (e = hipMemcpyAsync(z, s->spot.z, k * sizeof(double), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
+        (n && (e = hipMemcpyAsync(n, s->spot.cnt, k * sizeof(int64_t), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
+        (n_peaks && (e = hipMemcpyAsync(n_peaks, s->spot.npk, k * sizeof(int32_t), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
+        (e = hipStreamSynchronize(stream)) != hipSuccess)
+        return hip_fail(e, "streaming state copy");
+    return ENOVA_OK;
+}
+
+enova_status enova_stream_destroy(enova_stream s)
+{
+    if (!s)
+        return ENOVA_OK;
+    DeviceGuard dg(s->det->device);
+    (void)hipDeviceSynchronize();
+    free_stream(s);
+    return ENOVA_OK;
+}
+
+}  // extern "C"

@@ -92,6 +92,18 @@ def test_null_arguments_are_rejected():
                                     None, None) == binding.ENOVA_EINVAL
 
 
+def test_streaming_entry_points_reject_null_handles():
+    _ensure_built()
+    L = binding.lib()
+    h = ctypes.c_void_p()
+    off = np.array([0, 0], np.int64)
+    assert L.enova_stream_create(None, 1, None, None, None, off.ctypes.data, 0.98, 1e-3, 16,
+                                 ctypes.byref(h), None) == binding.ENOVA_EINVAL
+    assert L.enova_stream_push(None, None, None, None, None, None, None) == binding.ENOVA_EINVAL
+    assert L.enova_stream_state(None, None, None, None, None, None) == binding.ENOVA_EINVAL
+    assert L.enova_stream_destroy(None) == binding.ENOVA_OK
+
+
 def test_binding_refuses_host_tensors():
     import torch
     with pytest.raises(ValueError):

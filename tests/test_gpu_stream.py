@@ -1,0 +1,160 @@
+"""GPU parity of the streaming path (through the C ABI): every stream's newest window is scored
+as the oracle scores that window of the pushed steps, and each stream's SPOT threshold follows
+the oracle's streaming peaks-over-threshold fed with the same scores."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from harness import TOL, check_md, check_scores, detector, log
+from paper_2407_09486_amd import binding
+from paper_2407_09486_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _split(cfg, n, t_ref, t_live, seed_kind="ragged_mix"):
+    """n streams of t_ref + t_live steps: the reference part and the live part as workloads."""
+    w = wl.generate(cfg, lengths=[t_ref + t_live] * n)
+    v = w.values_f32().reshape(n, t_ref + t_live, cfg.metrics)
+    ref = wl.from_arrays(cfg, v[:, :t_ref].reshape(-1, cfg.metrics), np.arange(n + 1) * t_ref)
+    live = wl.from_arrays(cfg, v[:, t_ref:].reshape(-1, cfg.metrics), np.arange(n + 1) * t_live)
+    return ref, live
+
+
+def _dev(w):
+    import torch
+    if w.cfg.dtype == "bf16":
+        return torch.from_numpy(w.x_bits.view(np.int16)).cuda()
+    return torch.from_numpy(w.x).cuda()
+
+
+def _run(cfg, n=24, t_ref=1200, t_live=150, cal_counts=None, level=0.98, q=1e-3, peak_cap=4096):
+    """Returns everything the checks need: GPU streaming scores/md/flags per due push, the
+    calibration sets, the stats and the final SPOT state."""
+    import torch
+    weights = wl.make_weights(cfg, bias_scale=0.1)
+    det = detector(cfg, weights, "mfma")
+    ref, live = _split(cfg, n, t_ref, t_live)
+    M = cfg.metrics
+    xr = _dev(ref)
+    so_r = torch.from_numpy(ref.stream_offsets).cuda()
+    mean = torch.empty(n * M, dtype=torch.float32, device="cuda")
+    std = torch.empty(n * M, dtype=torch.float32, device="cuda")
+    binding.enova_detect_ref_stats(det.handle, xr, so_r, n, mean, std)
+    woff = det.window_offsets(ref.stream_offsets)
+    wo = torch.from_numpy(woff).cuda()
+    sc_ref, _, _ = det.score(xr, so_r, wo, int(woff[-1]), ref_mean=mean, ref_std=std)
+    sc_ref_h = sc_ref.cpu().numpy()
+    # calibration: the first cal_counts[s] reference windows of stream s
+    counts = np.diff(woff) if cal_counts is None else np.minimum(np.asarray(cal_counts), np.diff(woff))
+    cal = [sc_ref_h[woff[s]:woff[s] + counts[s]] for s in range(n)]
+    cal_off = np.zeros(n + 1, np.int64)
+    np.cumsum(counts, out=cal_off[1:])
+    cal_dev = torch.from_numpy(np.concatenate(cal).astype(np.float32) if cal_off[-1] else np.zeros(1, np.float32)).cuda()
+    ss = binding.StreamSet(det, mean, std, cal_dev, cal_off, level=level, q=q, peak_cap=peak_cap)
+    t0, z0, n0, k0 = ss.state()
+    xl = live.values_f32().reshape(n, t_live, M)
+    steps = torch.from_numpy(np.ascontiguousarray(xl.transpose(1, 0, 2))).cuda()   # [t][n][M] float32
+    if cfg.dtype == "bf16":
+        steps_bits = torch.from_numpy(wl.to_bf16_bits(np.ascontiguousarray(xl.transpose(1, 0, 2))).view(np.int16)).cuda()
+    out_sc, out_md, out_fl = [], [], []
+    scb = torch.empty(n, dtype=torch.float32, device="cuda")
+    mdb = torch.empty(n, dtype=torch.float32, device="cuda")
+    flb = torch.empty(n, dtype=torch.uint8, device="cuda")
+    for t in range(t_live):
+        xs = (steps_bits[t] if cfg.dtype == "bf16" else steps[t]).contiguous()
+        due = ss.push(xs, scb, mdb, flb)
+        expect_due = (t + 1) >= cfg.window and ((t + 1) - cfg.window) % cfg.stride == 0
+        assert due == int(expect_due)
+        if due:
+            out_sc.append(scb.cpu().numpy().copy())
+            out_md.append(mdb.cpu().numpy().copy())
+            out_fl.append(flb.cpu().numpy().copy())
+    state = ss.state()
+    ss.close()
+    det.close()
+    return dict(weights=weights, live=live, mean=mean.cpu().numpy().reshape(n, M),
+                std=std.cpu().numpy().reshape(n, M), cal=cal, start=(t0, z0, n0, k0), state=state,
+                sc=np.array(out_sc), md=np.array(out_md), fl=np.array(out_fl))
+
+
+def _check_scores(cfg, r):
+    o_sc, o_md, info = oracle.score(r["live"].values_f64(), r["live"].stream_offsets, window=cfg.window,
+                                    stride=cfg.stride, weights=r["weights"].as_f64(), act=cfg.act,
+                                    bf16=cfg.dtype == "bf16", ref_mean=r["mean"], ref_std=r["std"],
+                                    return_stats=True)
+    n = len(r["cal"])
+    k = r["sc"].shape[0]
+    woff = info["window_offsets"]
+    assert np.all(np.diff(woff) == k)
+    o_sc = o_sc.reshape(n, k).T
+    o_md = o_md.reshape(n, k).T
+    scale = info["md_scale"].reshape(n, k).T
+    check_scores(r["sc"].ravel(), o_sc.ravel(), cfg.dtype, "stream scores")
+    check_md(r["md"].ravel(), o_md.ravel(), scale.ravel(), cfg.dtype, "stream md")
+
+
+def _check_spot(r, level=0.98, q=1e-3, peak_cap=None):
+    """The oracle's SPOT, fed with the GPU's calibration and streaming scores, against the GPU's
+    flags and final state. A score within 1e-6 of the threshold may flag either way; that
+    stream is compared up to there."""
+    n = len(r["cal"])
+    t_g, z_g, n_g, k_g = r["state"]
+    t0, z0, n0, k0 = r["start"]
+    compared = 0
+    for s in range(n):
+        sp = oracle.Spot(r["cal"][s].astype(np.float64), level=level, q=q, peak_cap=peak_cap)
+        assert t0[s] == sp.t or (math.isinf(sp.t) and math.isinf(t0[s])), (s, t0[s], sp.t)
+        assert n0[s] == sp.n and k0[s] == len(sp.Y)
+        assert z0[s] == pytest.approx(sp.z, rel=1e-6, abs=1e-12) or (math.isinf(sp.z) and math.isinf(z0[s]))
+        ok = True
+        for j in range(r["sc"].shape[0]):
+            x = float(r["sc"][j, s])
+            if abs(x - sp.z) <= 1e-6 * abs(sp.z):
+                ok = False
+                break
+            f = sp.step(x)
+            assert r["fl"][j, s] == f, (s, j, x, sp.z)
+        if ok:
+            compared += 1
+            assert n_g[s] == sp.n and k_g[s] == len(sp.Y), (s, n_g[s], sp.n, k_g[s], len(sp.Y))
+            assert t_g[s] == sp.t or math.isinf(sp.t)
+            assert z_g[s] == pytest.approx(sp.z, rel=1e-6, abs=1e-12) or math.isinf(sp.z), (s, z_g[s], sp.z)
+    assert compared >= n - 1
+    return compared
+
+
+@pytest.mark.parametrize("dtype,act,hidden", [("f32", "relu", 128), ("bf16", "relu", 256),
+                                              ("f32", "tanh", 32), ("bf16", "relu", 64)])
+def test_stream_scores_and_spot(dtype, act, hidden):
+    cfg = wl.CONFIGS["c5"].replace(metrics=8, window=32, stride=2, hidden=hidden, latent=16, dtype=dtype,
+                                   act=act, n_streams=24, kind="ragged_mix")
+    log(f"[stream] {dtype} {act} H={hidden}")
+    # stream 0 without calibration, 1 with one peak, 2 with moments, the rest maximum likelihood
+    counts = [0, 60, 300] + [10 ** 6] * 21
+    r = _run(cfg, n=24, cal_counts=counts)
+    assert r["sc"].shape[0] == (150 - 32) // 2 + 1
+    _check_scores(cfg, r)
+    _check_spot(r)
+    assert math.isinf(r["state"][1][0]) and r["state"][2][0] == 0
+    assert r["fl"][:, 0].sum() == 0
+
+
+def test_stream_spot_freezes_at_the_peak_capacity():
+    cfg = wl.CONFIGS["c5"].replace(metrics=4, window=16, stride=1, hidden=64, latent=16, dtype="f32",
+                                   act="relu", n_streams=8, kind="ragged_mix")
+    r = _run(cfg, n=8, t_ref=900, t_live=200, peak_cap=24, level=0.98)
+    _check_spot(r, peak_cap=24)
+    assert np.all(r["state"][3] <= 24)
+
+
+def test_stream_window_steps_and_stride():
+    # W = 5, S = 3: due after 5, 8, 11, ... steps; the window spans the ring's wrap
+    cfg = wl.CONFIGS["c5"].replace(metrics=3, window=5, stride=3, hidden=32, latent=8, dtype="f32",
+                                   act="relu", n_streams=5, kind="ragged_mix")
+    r = _run(cfg, n=5, t_ref=400, t_live=41)
+    assert r["sc"].shape[0] == (41 - 5) // 3 + 1
+    _check_scores(cfg, r)
+    _check_spot(r)
