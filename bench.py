@@ -7,6 +7,10 @@ the peaks-over-threshold threshold over the calibration windows, and the flags o
 window. Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--config c5]
+
+With --mode stream it measures the streaming path instead: the config's detector shape over
+its number of streams, every push appending one step to each stream, scoring each stream's
+newest window and updating each stream's SPOT threshold (one push is one step).
 """
 from __future__ import annotations
 
@@ -100,6 +104,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="also run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--mode", choices=["batch", "stream"], default="batch")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the detector shards by stream with no collectives, "
@@ -113,6 +118,9 @@ def main():
     from paper_2407_09486_amd import workloads as wl
 
     cfg = wl.CONFIGS[args.config]
+    if args.mode == "stream":
+        stream_main(args, cfg)
+        return
     t_gen = time.perf_counter()
     w = wl.generate(cfg)
     weights = wl.make_weights(cfg)
@@ -207,6 +215,148 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, weights)
+    det.close()
+    print(json.dumps(out), flush=True)
+
+
+STREAM_REF_STEPS = 2048      # reference history per stream: statistics and SPOT calibration
+
+
+def stream_cpu_baseline(cfg, weights, x_ref, x_live, n_streams, pushes):
+    """The oracle on a bounded sample of the streaming work: the newest windows of the first
+    streams scored window by window, then their SPOT steps."""
+    import numpy as np
+
+    import oracle
+    k = min(512, n_streams)
+    W, S, M = cfg.window, cfg.stride, cfg.metrics
+    steps = W - 1 + pushes
+    xs = np.concatenate([x_live[s, :steps] for s in range(k)]).astype(np.float64)
+    offs = np.arange(k + 1, dtype=np.int64) * steps
+    mean = np.array([x_ref[s].mean(axis=0) for s in range(k)])
+    std = np.array([x_ref[s].std(axis=0) for s in range(k)])
+    std[std <= 1e-6] = 1.0
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    sc, _, info = oracle.score(xs, offs, window=W, stride=S, weights=weights.as_f64(), act=cfg.act,
+                               bf16=cfg.dtype == "bf16", ref_mean=mean, ref_std=std, threads=cores,
+                               return_stats=True)
+    sc = sc.reshape(k, -1)
+    for s in range(k):
+        sp = oracle.Spot(np.random.default_rng(s).gamma(2.0, 1.0, 500))
+        for v in sc[s]:
+            sp.step(float(v))
+    dt = time.perf_counter() - t0
+    n = sc.size
+    return {"value": n / dt, "unit": "windows/s", "cores": int(info["threads"]), "kind": "oracle",
+            "sample": f"streams 0..{k - 1}, {sc.shape[1]} pushes each ({n} windows + SPOT steps, {dt:.1f} s)"}
+
+
+def stream_main(args, cfg):
+    import numpy as np
+    import torch
+
+    from paper_2407_09486_amd import binding
+    from paper_2407_09486_amd import workloads as wl
+
+    n = cfg.n_streams
+    W, S, M = cfg.window, cfg.stride, cfg.metrics
+    live_steps = W - 1 + (args.warmup + args.steps) * S
+    scfg = cfg.replace(kind="ragged_mix") if cfg.kind == "ragged_mix" else cfg
+    t_gen = time.perf_counter()
+    w = wl.generate(scfg, lengths=[STREAM_REF_STEPS + live_steps] * n)
+    weights = wl.make_weights(cfg)
+    v = w.values_f32().reshape(n, STREAM_REF_STEPS + live_steps, M)
+    x_ref, x_live = v[:, :STREAM_REF_STEPS], v[:, STREAM_REF_STEPS:]
+    del w
+    print(f"[bench] stream {cfg.name}: {n} streams, {STREAM_REF_STEPS} reference + {live_steps} live steps "
+          f"generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr, flush=True)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+
+    def to_dev(a):
+        a = np.ascontiguousarray(a, np.float32)
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(wl.to_bf16_bits(a).view(np.int16)).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    det = binding.Detector(M, W, S, cfg.hidden, binding.weights_for_library(weights, cfg.dtype),
+                           latent=cfg.latent, dtype=cfg.dtype, act=cfg.act, ref_frac=1.0)
+    so_h = np.arange(n + 1, dtype=np.int64) * STREAM_REF_STEPS
+    xr = to_dev(x_ref.reshape(-1, M))
+    so = torch.from_numpy(so_h).to(dev)
+    mean = torch.empty(n * M, dtype=torch.float32, device=dev)
+    std = torch.empty(n * M, dtype=torch.float32, device=dev)
+    binding.enova_detect_ref_stats(det.handle, xr, so, n, mean, std)
+    woff = det.window_offsets(so_h)
+    sc_ref, _, _ = det.score(xr, so, torch.from_numpy(woff).to(dev), int(woff[-1]), ref_mean=mean,
+                             ref_std=std, md=False)
+    t_c = time.perf_counter()
+    ss = binding.StreamSet(det, mean, std, sc_ref, woff, level=0.98, q=1e-3, peak_cap=4096)
+    t_c = time.perf_counter() - t_c
+    del xr, sc_ref
+    steps = to_dev(np.ascontiguousarray(x_live.transpose(1, 0, 2)))   # [step][n][M]
+    scores = torch.empty(n, dtype=torch.float32, device=dev)
+    md = torch.empty(n, dtype=torch.float32, device=dev)
+    flags = torch.empty(n, dtype=torch.uint8, device=dev)
+    binding.enova_detect_set_timing(det.handle, True)
+    t = 0
+    for _ in range(W - 1):                                  # fill the rings: no window is due yet
+        ss.push(steps[t], scores, md, flags)
+        t += 1
+
+    def push_window():
+        # one scoring push (and the S - 1 non-scoring pushes before it when S > 1)
+        nonlocal t
+        due = 0
+        while not due:
+            due = ss.push(steps[t], scores, md, flags)
+            t += 1
+    for _ in range(args.warmup):
+        push_window()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    score_ms, spot_ms = [], []
+    ev0.record(stream)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        push_window()
+        a, b = ss.kernel_times()
+        score_ms.append(a)
+        spot_ms.append(b)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_push = ev0.elapsed_time(ev1) / args.steps
+    k_ms = float(np.mean(score_ms))
+    fpw = flops_per_window(cfg)
+    achieved = fpw * n / (k_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    t_s, z_s, n_s, k_s = ss.state()
+    out = {
+        "metric": "streaming windows scored/sec (newest window of every stream per push, per-stream SPOT)",
+        "value": round(n / (ms_push / 1e3), 1), "unit": "windows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_push, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+        "data": "synthetic (seeded generators standing in for the paper's industrial series)",
+        "config": {"workload": f"stream {cfg.name} shape: {n} streams x {M} metrics, W={W} S={S}, "
+                               f"H={cfg.hidden}, {cfg.dtype}; one step per stream per push",
+                   "streams": n, "reference_steps": STREAM_REF_STEPS, "pushes_per_step": S,
+                   "wall_windows_per_s": round(n * args.steps / wall, 1),
+                   "create_s": round(t_c, 3), "peaks_stored": int(k_s.sum())},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None, "kernel": "k_stream_score",
+                     "kernel_ms": round(k_ms, 4), "spot_kernels_ms": round(float(np.mean(spot_ms)), 4),
+                     "flops_per_window": fpw, "windows_per_launch": n},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = stream_cpu_baseline(cfg, weights, x_ref, x_live, n, args.steps)
+    ss.close()
     det.close()
     print(json.dumps(out), flush=True)
 

@@ -224,6 +224,11 @@ enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_sc
 enova_status enova_stream_state(enova_stream s, double *t, double *z, int64_t *n, int32_t *n_peaks,
                                 hipStream_t stream);
 
+/* With the detector's kernel timing enabled (enova_detect_set_timing), a push that scored
+ * windows brackets its scoring kernel and its SPOT kernels (update and refit) with HIP events;
+ * this waits for the last such push and reports milliseconds (0 if none ran). */
+enova_status enova_stream_kernel_times(enova_stream s, double *score_kernel_ms, double *spot_kernels_ms);
+
 /* Free a streaming set (synchronises the device). NULL is a no-op. */
 enova_status enova_stream_destroy(enova_stream s);
 

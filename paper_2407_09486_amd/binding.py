@@ -25,7 +25,8 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_detect_ref_stats", "enova_detect_score", "enova_detect_threshold",
            "enova_detect_flag", "enova_detect_set_timing", "enova_detect_kernel_times",
            "enova_detect_kernel_kind", "enova_stream_create", "enova_stream_push",
-           "enova_stream_state", "enova_stream_destroy", "enova_status_str", "enova_last_error"]
+           "enova_stream_state", "enova_stream_kernel_times", "enova_stream_destroy",
+           "enova_status_str", "enova_last_error"]
 
 
 class EnovaError(RuntimeError):
@@ -73,6 +74,7 @@ def lib():
     L.enova_stream_create.argtypes = [P, I32, P, P, P, P, D, D, I32, ctypes.POINTER(P), P]
     L.enova_stream_push.argtypes = [P, P, P, P, P, P, P]
     L.enova_stream_state.argtypes = [P, P, P, P, P, P]
+    L.enova_stream_kernel_times.argtypes = [P, P, P]
     L.enova_stream_destroy.argtypes = [P]
     for name in EXPORTS[:-2]:
         getattr(L, name).restype = st
@@ -224,6 +226,13 @@ def enova_stream_state(shandle, n_streams, stream=None):
     return t, z, n, k
 
 
+def enova_stream_kernel_times(shandle):
+    a, b = ctypes.c_double(), ctypes.c_double()
+    _check(lib().enova_stream_kernel_times(ctypes.c_void_p(shandle), ctypes.byref(a), ctypes.byref(b)),
+           "enova_stream_kernel_times")
+    return a.value, b.value
+
+
 def enova_stream_destroy(shandle):
     _check(lib().enova_stream_destroy(ctypes.c_void_p(shandle)), "enova_stream_destroy")
 
@@ -304,6 +313,9 @@ class StreamSet:
 
     def state(self, stream=None):
         return enova_stream_state(self.handle, self.n, stream)
+
+    def kernel_times(self):
+        return enova_stream_kernel_times(self.handle)
 
     def close(self):
         if self.handle:

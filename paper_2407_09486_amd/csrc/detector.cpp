@@ -919,6 +919,8 @@ struct enova_stream_s {
     float *mean = nullptr, *std = nullptr;   // [n][M]
     float *scores = nullptr;      // [n] when the caller does not ask for scores
     SpotState spot{};
+    hipEvent_t ev[3] = {nullptr, nullptr, nullptr};   // score start, score end / spot start, spot end
+    bool timed = false;           // the last scoring push recorded ev
 };
 
 namespace {
@@ -932,6 +934,9 @@ void free_stream(enova_stream s)
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
+    for (hipEvent_t e : s->ev)
+        if (e)
+            (void)hipEventDestroy(e);
     delete s;
 }
 
@@ -1066,11 +1071,24 @@ enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_sc
     p.sum_bd2 = det->sum_bd2;
     p.scores = out_scores ? out_scores : s->scores;
     p.md = out_md;
+    const bool timed = det->timing;
+    if (timed && !s->ev[0]) {
+        for (hipEvent_t &ev : s->ev)
+            if ((e = hipEventCreate(&ev)) != hipSuccess)
+                return hip_fail(e, "timing events");
+    }
+    if (timed)
+        (void)hipEventRecord(s->ev[0], stream);
     if ((e = launch_stream_score(g, p, stream)) != hipSuccess)
         return hip_fail(e, "streaming scoring kernel");
+    if (timed)
+        (void)hipEventRecord(s->ev[1], stream);
     if ((e = launch_spot_update(p.scores, s->n, s->spot, out_flags, stream)) != hipSuccess ||
         (e = launch_spot_fit(s->n, s->q, s->spot, stream)) != hipSuccess)
         return hip_fail(e, "streaming threshold kernels");
+    if (timed)
+        (void)hipEventRecord(s->ev[2], stream);
+    s->timed = timed;
     return ENOVA_OK;
 }
 
@@ -1088,6 +1106,26 @@ enova_status enova_stream_state(enova_stream s, double *t, double *z, int64_t *n
         (n_peaks && (e = hipMemcpyAsync(n_peaks, s->spot.npk, k * sizeof(int32_t), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
         (e = hipStreamSynchronize(stream)) != hipSuccess)
         return hip_fail(e, "streaming state copy");
+    return ENOVA_OK;
+}
+
+enova_status enova_stream_kernel_times(enova_stream s, double *score_ms, double *spot_ms)
+{
+    if (!s)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(s->det->device);
+    float a = 0.0f, b = 0.0f;
+    hipError_t e;
+    if (s->timed) {
+        if ((e = hipEventSynchronize(s->ev[2])) != hipSuccess ||
+            (e = hipEventElapsedTime(&a, s->ev[0], s->ev[1])) != hipSuccess ||
+            (e = hipEventElapsedTime(&b, s->ev[1], s->ev[2])) != hipSuccess)
+            return hip_fail(e, "streaming kernel timing");
+    }
+    if (score_ms)
+        *score_ms = a;
+    if (spot_ms)
+        *spot_ms = b;
     return ENOVA_OK;
 }
 

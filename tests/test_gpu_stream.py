@@ -140,6 +140,7 @@ def test_stream_scores_and_spot(dtype, act, hidden):
     _check_spot(r)
     assert math.isinf(r["state"][1][0]) and r["state"][2][0] == 0
     assert r["fl"][:, 0].sum() == 0
+    assert np.any(r["state"][3] > r["start"][3]), "no stream took a new peak: refits untested"
 
 
 def test_stream_spot_freezes_at_the_peak_capacity():
