@@ -401,11 +401,13 @@ struct FitShared {
     double xs[2 * kFitGrid];
     double sa[2 * kFitGrid];
     double sb[2 * kFitGrid];
-    double red[256];
+    double red[256], red2[256];
     double blo[kFitMaxBrackets], bhi[kFitMaxBrackets], broot[kFitMaxBrackets];
     int bneg[kFitMaxBrackets], bdone[kFitMaxBrackets], bround[kFitMaxBrackets];
     double roots[2 * kFitMaxBrackets];
     int batch[kFitBatch];
+    int coll[kFitBatch];         // 1: the batch bracket's points are not strictly inside it
+    int scan[256];
     int nbr, nroots, npts, ngrid, nbatch;
     double ysum, ymin, ymax;
 };
@@ -423,22 +425,90 @@ __device__ __forceinline__ double fit_quantile(double t, double gamma, double si
     return t + sigma / gamma * (pow(ratio, -gamma) - 1.0);
 }
 
-// sa/sb at the first npts points of sh.xs, each over all N excesses in order (one point per
-// thread at a time).
+// sa/sb at the first npts (<= 1024) points of sh.xs over all N excesses. Many points: each
+// thread takes up to four; few points: T threads share a point (power of two, T * npts <= 256),
+// each summing every T-th excess, and the T partial sums are added in order. A fixed order
+// either way.
 __device__ void fit_eval(FitShared &sh, const double *y, int N)
 {
-    for (int p = threadIdx.x; p < sh.npts; p += 256) {
-        const double x = sh.xs[p];
-        double a = 0.0, b = 0.0;
-        for (int i = 0; i < N; ++i) {
-            double ta, tb;
-            gpd_terms(x * y[i], ta, tb);
-            a += ta;
-            b += tb;
+    const int np = sh.npts;
+    if (np > 128) {
+        // up to four points per thread, evaluated side by side (independent dependency chains)
+        double x[4], a[4], b[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int p = threadIdx.x + 256 * k;
+            x[k] = p < np ? sh.xs[p] : 0.0;
+            a[k] = 0.0;
+            b[k] = 0.0;
         }
-        sh.sa[p] = a;
-        sh.sb[p] = b;
+        for (int i = 0; i < N; ++i) {
+            const double yi = y[i];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                double ta, tb;
+                gpd_terms(x[k] * yi, ta, tb);
+                a[k] += ta;
+                b[k] += tb;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int p = threadIdx.x + 256 * k;
+            if (p < np) {
+                sh.sa[p] = a[k];
+                sh.sb[p] = b[k];
+            }
+        }
+        __syncthreads();
+        return;
     }
+    int T = 1;
+    while (T < 64 && 2 * T * np <= 256)
+        T *= 2;
+    const int per = 256 / T;
+    const int part = threadIdx.x % T;
+    for (int p0 = 0; p0 < np; p0 += per) {
+        const int p = p0 + static_cast<int>(threadIdx.x) / T;
+        double a = 0.0, b = 0.0;
+        if (p < np) {
+            const double x = sh.xs[p];
+            for (int i = part; i < N; i += T) {
+                double ta, tb;
+                gpd_terms(x * y[i], ta, tb);
+                a += ta;
+                b += tb;
+            }
+        }
+        if (T == 1) {
+            if (p < np) {
+                sh.sa[p] = a;
+                sh.sb[p] = b;
+            }
+        } else {
+            sh.red[threadIdx.x] = a;
+            sh.red2[threadIdx.x] = b;
+            __syncthreads();
+            if (part == 0 && p < np) {
+                double sa = 0.0, sb = 0.0;
+                for (int k = 0; k < T; ++k) {
+                    sa += sh.red[threadIdx.x + k];
+                    sb += sh.red2[threadIdx.x + k];
+                }
+                sh.sa[p] = sa;
+                sh.sb[p] = sb;
+            }
+            __syncthreads();
+        }
+    }
+    __syncthreads();
+}
+
+// w = b - a - a b at the first npts points, into sh.sa (every thread a share).
+__device__ void fit_w_all(FitShared &sh, double n)
+{
+    for (int p = threadIdx.x; p < sh.npts; p += 256)
+        sh.sa[p] = fit_w(sh.sa[p], sh.sb[p], n);
     __syncthreads();
 }
 
@@ -521,38 +591,56 @@ __global__ __launch_bounds__(256) void k_spot_fit(double q, SpotState st)
             }
             __syncthreads();
             fit_eval(sh, y, N);
-            if (tid == 0) {
-                for (int gi = 0; gi < sh.ngrid; ++gi) {
-                    const int base = gi * kFitGrid;
-                    for (int i = 0; i < kFitGrid; ++i) {
-                        const double wi = fit_w(sh.sa[base + i], sh.sb[base + i], Nd);
-                        if (wi == 0.0) {
-                            if (sh.nroots < 2 * kFitMaxBrackets)
-                                sh.roots[sh.nroots++] = sh.xs[base + i];
-                            continue;
-                        }
-                        if (i + 1 < kFitGrid) {
-                            const double wn = fit_w(sh.sa[base + i + 1], sh.sb[base + i + 1], Nd);
-                            if (wi * wn < 0.0 && sh.nbr < kFitMaxBrackets) {
-                                const double x0 = sh.xs[base + i], x1 = sh.xs[base + i + 1];
-                                const int b = sh.nbr++;
-                                sh.blo[b] = x0 < x1 ? x0 : x1;
-                                sh.bhi[b] = x0 < x1 ? x1 : x0;
-                                sh.bneg[b] = x0 < x1 ? (wi < 0.0) : (wn < 0.0);
-                                sh.bdone[b] = 0;
-                                sh.bround[b] = 0;
-                                sh.broot[b] = 0.0;
-                            }
-                        }
-                    }
+            fit_w_all(sh, Nd);
+            // every grid point: an exact root, and/or a sign change to the next point of its grid;
+            // both kept in grid order (ordered compaction over the block)
+            for (int p0 = 0; p0 < sh.npts; p0 += 256) {
+                const int i = p0 + tid;
+                int root = 0, br = 0;
+                if (i < sh.npts) {
+                    const int gi = i % kFitGrid;
+                    const double wi = sh.sa[i];
+                    if (wi == 0.0)
+                        root = 1;
+                    else if (gi + 1 < kFitGrid && wi * sh.sa[i + 1] < 0.0)
+                        br = 1;
                 }
+                sh.scan[tid] = root | (br << 16);
+                __syncthreads();
+                for (int off = 1; off < 256; off <<= 1) {
+                    const int v = tid >= off ? sh.scan[tid - off] : 0;
+                    __syncthreads();
+                    sh.scan[tid] += v;
+                    __syncthreads();
+                }
+                const int incl = sh.scan[tid];
+                const int r_at = sh.nroots + (incl & 0xffff) - root;
+                const int b_at = sh.nbr + (incl >> 16) - br;
+                if (root && r_at < 2 * kFitMaxBrackets)
+                    sh.roots[r_at] = sh.xs[i];
+                if (br && b_at < kFitMaxBrackets) {
+                    const double x0 = sh.xs[i], x1 = sh.xs[i + 1];
+                    const double wi = sh.sa[i], wn = sh.sa[i + 1];
+                    sh.blo[b_at] = x0 < x1 ? x0 : x1;
+                    sh.bhi[b_at] = x0 < x1 ? x1 : x0;
+                    sh.bneg[b_at] = x0 < x1 ? (wi < 0.0) : (wn < 0.0);
+                    sh.bdone[b_at] = 0;
+                    sh.bround[b_at] = 0;
+                    sh.broot[b_at] = 0.0;
+                }
+                __syncthreads();
+                if (tid == 255) {
+                    const int nr = sh.nroots + (incl & 0xffff), nb = sh.nbr + (incl >> 16);
+                    sh.nroots = nr < 2 * kFitMaxBrackets ? nr : 2 * kFitMaxBrackets;
+                    sh.nbr = nb < kFitMaxBrackets ? nb : kFitMaxBrackets;
+                }
+                __syncthreads();
             }
-            __syncthreads();
-            // k-section, up to kFitBatch open brackets per evaluation
+            // k-section, up to kFitBatch open brackets per evaluation: the points and w are
+            // computed by all threads, one thread keeps the brackets
             for (;;) {
                 if (tid == 0) {
                     sh.nbatch = 0;
-                    sh.npts = 0;
                     for (int b = 0; b < sh.nbr && sh.nbatch < kFitBatch; ++b) {
                         if (sh.bdone[b])
                             continue;
@@ -561,39 +649,43 @@ __global__ __launch_bounds__(256) void k_spot_fit(double q, SpotState st)
                             sh.broot[b] = 0.5 * (sh.blo[b] + sh.bhi[b]);
                             continue;
                         }
-                        const double lo = sh.blo[b], hi = sh.bhi[b];
-                        double prev = lo;
-                        bool collapsed = false;
-                        for (int j = 1; j <= kFitInterior; ++j) {
-                            const double pj = lo + (hi - lo) * static_cast<double>(j) / (kFitInterior + 1);
-                            if (!(pj > prev) || !(pj < hi)) {
-                                collapsed = true;
-                                break;
-                            }
-                            prev = pj;
-                        }
-                        if (collapsed) {
-                            sh.bdone[b] = 1;
-                            sh.broot[b] = 0.5 * (lo + hi);
-                            continue;
-                        }
-                        for (int j = 1; j <= kFitInterior; ++j)
-                            sh.xs[sh.npts + j - 1] = lo + (hi - lo) * static_cast<double>(j) / (kFitInterior + 1);
-                        sh.npts += kFitInterior;
+                        sh.coll[sh.nbatch] = 0;
                         sh.batch[sh.nbatch++] = b;
                     }
+                    sh.npts = sh.nbatch * kFitInterior;
                 }
                 __syncthreads();
                 if (sh.nbatch == 0)
                     break;
+                for (int i = tid; i < sh.npts; i += 256) {
+                    const int k = i / kFitInterior, j = i - k * kFitInterior + 1;
+                    const int b = sh.batch[k];
+                    const double lo = sh.blo[b], hi = sh.bhi[b];
+                    sh.xs[i] = lo + (hi - lo) * static_cast<double>(j) / (kFitInterior + 1);
+                }
+                __syncthreads();
+                for (int i = tid; i < sh.npts; i += 256) {
+                    // a bracket that can no longer shrink: its points are not strictly inside
+                    const int k = i / kFitInterior, j = i - k * kFitInterior + 1;
+                    const int b = sh.batch[k];
+                    const double prev = j == 1 ? sh.blo[b] : sh.xs[i - 1];
+                    if (!(sh.xs[i] > prev) || !(sh.xs[i] < sh.bhi[b]))
+                        sh.coll[k] = 1;
+                }
                 fit_eval(sh, y, N);
+                fit_w_all(sh, Nd);
                 if (tid == 0) {
                     for (int k = 0; k < sh.nbatch; ++k) {
                         const int b = sh.batch[k];
+                        if (sh.coll[k]) {
+                            sh.bdone[b] = 1;
+                            sh.broot[b] = 0.5 * (sh.blo[b] + sh.bhi[b]);
+                            continue;
+                        }
                         double new_lo = sh.blo[b], new_hi = sh.bhi[b];
                         for (int j = 0; j < kFitInterior; ++j) {
                             const int pi = k * kFitInterior + j;
-                            const double wj = fit_w(sh.sa[pi], sh.sb[pi], Nd);
+                            const double wj = sh.sa[pi];
                             if (wj == 0.0) {
                                 sh.bdone[b] = 1;
                                 sh.broot[b] = sh.xs[pi];
