@@ -95,48 +95,148 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream_score(StreamScorePara
 #pragma unroll
         for (int r = 0; r < 16; ++r)
             acc[hb][0][r] = 0.0f;
+    v16f acc2[HBW];                                // fp32: the odd reduction slots
+#pragma unroll
+    for (int hb = 0; hb < HBW; ++hb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            acc2[hb][r] = 0.0f;
     float my_sum = 0.0f;                           // thread nl < NBS: window nl's sum of v
 
+    // padding-free windows (M a multiple of the chunk's elements) stage with vector loads
+    const bool linear = Mp == M && M % EPC == 0;
     const uint4 *ap = p.w1p + (wh * HBW) * 64 + lane;
     for (int k0 = 0; k0 < g.KC; k0 += KS) {
         const int ks = g.KC - k0 < KS ? g.KC - k0 : KS;   // a multiple of 16
         __syncthreads();                                   // the previous slice is consumed
-        for (int idx = tid; idx < NBS * ks; idx += NT) {
-            const int w = idx / ks;
-            const int kc = idx - w * ks;
-            const int kappa = k0 + kc;
-            const int q = kappa / CPR;
-            const int c = kappa - q * CPR;
-            const int s = s0 + w;
-            float v[EPC];
+        if (linear) {
+            // chunk kappa is elements [kappa*EPC, +EPC) of the window, contiguous in the ring,
+            // with consecutive metrics: one 16-byte load of x and EPC/4 of mean and std each;
+            // SU chunks per thread in flight
+            constexpr int SU = 4;
+            for (int base = tid; base < NBS * ks; base += NT * SU) {
+                uint4 raw[SU];
+                float4 mu[SU][EPC / 4], sd[SU][EPC / 4];
+                bool ok[SU];
 #pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                const int jj = c * EPC + e;
-                const int tt = jj / Mp;
-                const int m = jj - tt * Mp;
-                const int step = q * S + tt;
-                float val = 0.0f;
-                if (s < p.n_streams && q < Q && m < M && step < W) {
-                    const int64_t at = (static_cast<int64_t>(s) * 2 * W + p.first_slot + step) * M + m;
-                    const float x = load_x<DT>(p.ring, at);
-                    const int64_t sm = static_cast<int64_t>(s) * M + m;
-                    val = (x - p.mean[sm]) * (1.0f / p.std[sm]);
+                for (int u = 0; u < SU; ++u) {
+                    const int idx = base + u * NT;
+                    const int w = idx / ks;
+                    const int kc = idx - w * ks;
+                    const int s = s0 + w;
+                    const int e0 = (k0 + kc) * EPC;
+                    ok[u] = idx < NBS * ks && s < p.n_streams && e0 < W * M;
+                    if (ok[u]) {
+                        const int64_t at = (static_cast<int64_t>(s) * 2 * W + p.first_slot) * M + e0;
+                        if constexpr (DT == ENOVA_F32)
+                            raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(p.ring) + at);
+                        else
+                            raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.ring) + at);
+                        const int64_t sm = static_cast<int64_t>(s) * M + e0 % M;
+#pragma unroll
+                        for (int h = 0; h < EPC / 4; ++h) {
+                            mu[u][h] = reinterpret_cast<const float4 *>(p.mean + sm)[h];
+                            sd[u][h] = reinterpret_cast<const float4 *>(p.std + sm)[h];
+                        }
+                    }
                 }
-                v[e] = val;
+#pragma unroll
+                for (int u = 0; u < SU; ++u) {
+                    const int idx = base + u * NT;
+                    if (idx >= NBS * ks)
+                        continue;
+                    const int w = idx / ks;
+                    const int kc = idx - w * ks;
+                    float v[EPC];
+                    if (ok[u]) {
+                        float xv[EPC], mv[EPC], sv[EPC];
+                        if constexpr (DT == ENOVA_F32) {
+                            xv[0] = __uint_as_float(raw[u].x);
+                            xv[1] = __uint_as_float(raw[u].y);
+                            xv[2] = __uint_as_float(raw[u].z);
+                            xv[3] = __uint_as_float(raw[u].w);
+                        } else {
+                            xv[0] = bf16_lo(raw[u].x);
+                            xv[1] = bf16_hi(raw[u].x);
+                            xv[2] = bf16_lo(raw[u].y);
+                            xv[3] = bf16_hi(raw[u].y);
+                            xv[4] = bf16_lo(raw[u].z);
+                            xv[5] = bf16_hi(raw[u].z);
+                            xv[6] = bf16_lo(raw[u].w);
+                            xv[7] = bf16_hi(raw[u].w);
+                        }
+#pragma unroll
+                        for (int h = 0; h < EPC / 4; ++h) {
+                            mv[4 * h + 0] = mu[u][h].x;
+                            mv[4 * h + 1] = mu[u][h].y;
+                            mv[4 * h + 2] = mu[u][h].z;
+                            mv[4 * h + 3] = mu[u][h].w;
+                            sv[4 * h + 0] = sd[u][h].x;
+                            sv[4 * h + 1] = sd[u][h].y;
+                            sv[4 * h + 2] = sd[u][h].z;
+                            sv[4 * h + 3] = sd[u][h].w;
+                        }
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e)
+                            v[e] = (xv[e] - mv[e]) * (1.0f / sv[e]);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < EPC; ++e)
+                            v[e] = 0.0f;
+                    }
+                    uint4 out;
+                    if constexpr (DT == ENOVA_F32) {
+                        out.x = __float_as_uint(v[0]);
+                        out.y = __float_as_uint(v[1]);
+                        out.z = __float_as_uint(v[2]);
+                        out.w = __float_as_uint(v[3]);
+                    } else {
+                        out.x = pack_bf16x2(v[0], v[1]);
+                        out.y = pack_bf16x2(v[2], v[3]);
+                        out.z = pack_bf16x2(v[4], v[5]);
+                        out.w = pack_bf16x2(v[6], v[7]);
+                    }
+                    buf[w * KCP + kc] = out;
+                }
             }
-            uint4 out;
-            if constexpr (DT == ENOVA_F32) {
-                out.x = __float_as_uint(v[0]);
-                out.y = __float_as_uint(v[1]);
-                out.z = __float_as_uint(v[2]);
-                out.w = __float_as_uint(v[3]);
-            } else {
-                out.x = pack_bf16x2(v[0], v[1]);
-                out.y = pack_bf16x2(v[2], v[3]);
-                out.z = pack_bf16x2(v[4], v[5]);
-                out.w = pack_bf16x2(v[6], v[7]);
+        } else {
+            for (int idx = tid; idx < NBS * ks; idx += NT) {
+                const int w = idx / ks;
+                const int kc = idx - w * ks;
+                const int kappa = k0 + kc;
+                const int q = kappa / CPR;
+                const int c = kappa - q * CPR;
+                const int s = s0 + w;
+                float v[EPC];
+    #pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    const int jj = c * EPC + e;
+                    const int tt = jj / Mp;
+                    const int m = jj - tt * Mp;
+                    const int step = q * S + tt;
+                    float val = 0.0f;
+                    if (s < p.n_streams && q < Q && m < M && step < W) {
+                        const int64_t at = (static_cast<int64_t>(s) * 2 * W + p.first_slot + step) * M + m;
+                        const float x = load_x<DT>(p.ring, at);
+                        const int64_t sm = static_cast<int64_t>(s) * M + m;
+                        val = (x - p.mean[sm]) * (1.0f / p.std[sm]);
+                    }
+                    v[e] = val;
+                }
+                uint4 out;
+                if constexpr (DT == ENOVA_F32) {
+                    out.x = __float_as_uint(v[0]);
+                    out.y = __float_as_uint(v[1]);
+                    out.z = __float_as_uint(v[2]);
+                    out.w = __float_as_uint(v[3]);
+                } else {
+                    out.x = pack_bf16x2(v[0], v[1]);
+                    out.y = pack_bf16x2(v[2], v[3]);
+                    out.z = pack_bf16x2(v[4], v[5]);
+                    out.w = pack_bf16x2(v[6], v[7]);
+                }
+                buf[w * KCP + kc] = out;
             }
-            buf[w * KCP + kc] = out;
         }
         __syncthreads();
         if (tid < NBS) {
@@ -152,40 +252,54 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream_score(StreamScorePara
                 }
             }
         }
-        // contraction over the slice: step i covers chunks 2i (lanes 0..31) and 2i+1 (32..63)
-        const int nsteps = ks / 2;
-        uint4 a_cur[HBW];
+        // contraction over the slice: step i covers chunks 2i (lanes 0..31) and 2i+1 (32..63).
+        // W1 fragments run PD steps ahead in a register ring (a step is only a few matrix ops);
+        // fp32 alternates two accumulators so consecutive ops do not wait on each other.
+        constexpr int PD = 8;
+        static_assert(PD <= kPrefetchSteps, "the packed W1 carries kPrefetchSteps zero steps");
+        const int nsteps = ks / 2;                 // a multiple of PD
+        const int64_t st0 = k0 / 2;
+        uint4 a[PD][HBW];
 #pragma unroll
-        for (int hb = 0; hb < HBW; ++hb)
-            a_cur[hb] = ap[(static_cast<int64_t>(k0 / 2) * HBT + hb) * 64];
-        for (int i = 0; i < nsteps; ++i) {
-            uint4 a_nxt[HBW];
-            const int64_t nxt = static_cast<int64_t>(k0 / 2 + i + 1) * HBT;   // W1 carries zero steps past the end
+        for (int j = 0; j < PD; ++j)
 #pragma unroll
             for (int hb = 0; hb < HBW; ++hb)
-                a_nxt[hb] = ap[(nxt + hb) * 64];
-            const uint4 bq = buf[brow + 2 * i + half];
-            if constexpr (DT == ENOVA_F32) {
+                a[j][hb] = ap[((st0 + j) * HBT + hb) * 64];
+        for (int i = 0; i < nsteps; i += PD) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float bv = __uint_as_float(e == 0 ? bq.x : e == 1 ? bq.y : e == 2 ? bq.z : bq.w);
+            for (int j = 0; j < PD; ++j) {
+                const uint4 bq = buf[brow + 2 * (i + j) + half];
+                if constexpr (DT == ENOVA_F32) {
 #pragma unroll
-                    for (int hb = 0; hb < HBW; ++hb) {
-                        const float av = __uint_as_float(e == 0 ? a_cur[hb].x : e == 1 ? a_cur[hb].y
-                                                        : e == 2 ? a_cur[hb].z : a_cur[hb].w);
-                        acc[hb][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[hb][0], 0, 0, 0);
+                    for (int e = 0; e < 4; ++e) {
+                        const float bv = __uint_as_float(e == 0 ? bq.x : e == 1 ? bq.y : e == 2 ? bq.z : bq.w);
+#pragma unroll
+                        for (int hb = 0; hb < HBW; ++hb) {
+                            const float av = __uint_as_float(e == 0 ? a[j][hb].x : e == 1 ? a[j][hb].y
+                                                            : e == 2 ? a[j][hb].z : a[j][hb].w);
+                            if (e & 1)
+                                acc2[hb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc2[hb], 0, 0, 0);
+                            else
+                                acc[hb][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[hb][0], 0, 0, 0);
+                        }
                     }
+                } else {
+#pragma unroll
+                    for (int hb = 0; hb < HBW; ++hb)
+                        acc[hb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(v8bf, a[j][hb]), __builtin_bit_cast(v8bf, bq), acc[hb][0], 0, 0, 0);
                 }
-            } else {
+                // steps up to KC/2 + PD - 1 are read: the packed W1 carries zero steps past the end
 #pragma unroll
                 for (int hb = 0; hb < HBW; ++hb)
-                    acc[hb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(v8bf, a_cur[hb]), __builtin_bit_cast(v8bf, bq), acc[hb][0], 0, 0, 0);
+                    a[j][hb] = ap[((st0 + i + j + PD) * HBT + hb) * 64];
             }
-#pragma unroll
-            for (int hb = 0; hb < HBW; ++hb)
-                a_cur[hb] = a_nxt[hb];
         }
+    }
+    if constexpr (DT == ENOVA_F32) {
+#pragma unroll
+        for (int hb = 0; hb < HBW; ++hb)
+            acc[hb][0] += acc2[hb];
     }
     __syncthreads();                               // the staging buffer becomes the exchange area
     if (tid < NBS)
