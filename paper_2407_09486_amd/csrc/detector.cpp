@@ -930,7 +930,8 @@ void free_stream(enova_stream s)
     if (!s)
         return;
     void *ptrs[] = {s->ring, s->mean, s->std, s->scores, s->spot.t, s->spot.z, s->spot.cnt,
-                    s->spot.npk, s->spot.peaks, s->spot.mark, s->spot.err};
+                    s->spot.npk, s->spot.peaks, s->spot.mark, s->spot.err, s->spot.list,
+                    s->spot.count};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
@@ -1001,6 +1002,7 @@ enova_status enova_stream_create(enova_detector det, int32_t n, const float *ref
         (st = dev_alloc(&s->spot.npk, n)) != ENOVA_OK ||
         (st = dev_alloc(&s->spot.peaks, static_cast<size_t>(n) * peak_cap)) != ENOVA_OK ||
         (st = dev_alloc(&s->spot.mark, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.err, 1)) != ENOVA_OK ||
+        (st = dev_alloc(&s->spot.list, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.count, 1)) != ENOVA_OK ||
         (st = dev_alloc(&d_off, static_cast<size_t>(n) + 1)) != ENOVA_OK) {
         (void)hipFree(d_off);
         free_stream(s);
@@ -1030,7 +1032,7 @@ enova_status enova_stream_create(enova_detector det, int32_t n, const float *ref
         free_stream(s);
         return fail(ENOVA_EINVAL, "a stream's calibration peaks exceed peak_cap");
     }
-    if ((e = launch_spot_fit(n, q, s->spot, stream)) != hipSuccess || (e = hipStreamSynchronize(stream)) != hipSuccess) {
+    if ((e = launch_spot_fit(n, q, s->spot, true, stream)) != hipSuccess || (e = hipStreamSynchronize(stream)) != hipSuccess) {
         free_stream(s);
         return hip_fail(e, "streaming threshold fit");
     }
@@ -1084,7 +1086,7 @@ enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_sc
     if (timed)
         (void)hipEventRecord(s->ev[1], stream);
     if ((e = launch_spot_update(p.scores, s->n, s->spot, out_flags, stream)) != hipSuccess ||
-        (e = launch_spot_fit(s->n, s->q, s->spot, stream)) != hipSuccess)
+        (e = launch_spot_fit(s->n, s->q, s->spot, false, stream)) != hipSuccess)
         return hip_fail(e, "streaming threshold kernels");
     if (timed)
         (void)hipEventRecord(s->ev[2], stream);

@@ -184,11 +184,14 @@ struct SpotState {
     int cap;
     uint8_t *mark;               // 1: z must be refitted
     int *err;                    // set to 1 if a stream's calibration peaks exceed cap
+    int *list;                   // [n]: streams that took a new peak in this push (any order)
+    int *count;                  // entries of list (cleared before each update)
 };
 hipError_t launch_spot_init(const float *cal, const int64_t *cal_off, int n, double level,
                             const SpotState &s, hipStream_t st);
 hipError_t launch_spot_update(const float *scores, int n, const SpotState &s, uint8_t *flags,
                               hipStream_t st);
-hipError_t launch_spot_fit(int n, double q, const SpotState &s, hipStream_t st);
+// Refits z: every marked stream (all = true), or the streams listed by the last update.
+hipError_t launch_spot_fit(int n, double q, const SpotState &s, bool all, hipStream_t st);
 
 }  // namespace enova

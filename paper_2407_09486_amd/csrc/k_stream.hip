@@ -498,6 +498,7 @@ __global__ __launch_bounds__(256) void k_spot_update(const float *__restrict__ s
                 st.peaks[static_cast<int64_t>(s) * st.cap + np] = xd - t;
                 st.npk[s] = np + 1;
                 st.mark[s] = 1;
+                st.list[atomicAdd(st.count, 1)] = s;
             }
         }
     }
@@ -645,15 +646,11 @@ __device__ double block_reduce(FitShared &sh, double v)
     return r;
 }
 
-// Refit of z for every marked stream, one block per stream: N_t <= 1 gives t; 2 <= N_t < 10 the
-// method of moments with the unbiased sample variance; N_t >= 10 maximum likelihood.
-__global__ __launch_bounds__(256) void k_spot_fit(double q, SpotState st)
+// Refit of z for one marked stream by one block: N_t <= 1 gives t; 2 <= N_t < 10 the method of
+// moments with the unbiased sample variance; N_t >= 10 maximum likelihood.
+__device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState &st)
 {
-    __shared__ FitShared sh;
-    const int s = blockIdx.x;
     const int tid = threadIdx.x;
-    if (!st.mark[s])
-        return;
     const int N = st.npk[s];
     const double t = st.t[s];
     const double n = static_cast<double>(st.cnt[s]);
@@ -853,6 +850,25 @@ __global__ __launch_bounds__(256) void k_spot_fit(double q, SpotState st)
         st.z[s] = z;
         st.mark[s] = 0;
     }
+    __syncthreads();
+}
+
+// One block per stream, the unmarked ones leaving at once (the start of a streaming set).
+__global__ __launch_bounds__(256) void k_spot_fit_all(double q, SpotState st)
+{
+    __shared__ FitShared sh;
+    if (st.mark[blockIdx.x])
+        spot_fit_stream(sh, blockIdx.x, q, st);
+}
+
+// The streams the last update listed, spread over a fixed grid of blocks (a push refits a few
+// percent of the streams; launching a block per stream would mostly launch empty blocks).
+__global__ __launch_bounds__(256) void k_spot_fit_list(double q, SpotState st)
+{
+    __shared__ FitShared sh;
+    const int cnt = *st.count;
+    for (int i = blockIdx.x; i < cnt; i += gridDim.x)
+        spot_fit_stream(sh, st.list[i], q, st);
 }
 
 }  // namespace
@@ -930,16 +946,28 @@ hipError_t launch_spot_update(const float *scores, int n, const SpotState &s, ui
 {
     if (n <= 0)
         return hipSuccess;
+    hipError_t e = hipMemsetAsync(s.count, 0, sizeof(int), st);
+    if (e != hipSuccess)
+        return e;
     hipLaunchKernelGGL(k_spot_update, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, st,
                        scores, n, s, flags);
     return hipGetLastError();
 }
 
-hipError_t launch_spot_fit(int n, double q, const SpotState &s, hipStream_t st)
+hipError_t launch_spot_fit(int n, double q, const SpotState &s, bool all, hipStream_t st)
 {
     if (n <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_spot_fit, dim3(static_cast<unsigned>(n)), dim3(256), 0, st, q, s);
+    if (all) {
+        hipLaunchKernelGGL(k_spot_fit_all, dim3(static_cast<unsigned>(n)), dim3(256), 0, st, q, s);
+    } else {
+        int dev = 0, cus = 256;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            cus = 256;
+        const int blocks = n < 2 * cus ? n : 2 * cus;
+        hipLaunchKernelGGL(k_spot_fit_list, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, q, s);
+    }
     return hipGetLastError();
 }
 
