@@ -15,6 +15,13 @@ PI controller on the batch KL of the normal windows (ControlVAE form: e = KL_set
 P = Kp / (1 + exp(e)), I <- I - Ki e, beta = clamp(P + I + beta_min, beta_min, beta_max));
 Adam on the loss J = -L. Gradients are derived by hand below and pinned in
 ``tests/test_oracle_elbo.py`` against finite differences and torch autograd.
+
+Read literally, L is unbounded above in the anomalous windows' term: -log p grows without
+limit as the decoder drifts away from them (the posterior variance of those windows inflates and
+the loss diverges within tens of Adam steps, even with a few anomalies per thousand windows).
+An optional ``margin`` m bounds that term: an anomalous window contributes
+min(e_i, m) + D/2 log(2 pi) with e_i = 1/2 |v_i - m'_i|^2, so it is pushed away only until its
+reconstruction error reaches m; m = inf is the equation as printed.
 """
 from __future__ import annotations
 
@@ -50,27 +57,35 @@ def forward(p, V, eps, act="relu"):
     f["hd"] = _act(f["a2"], act)
     f["mr"] = f["hd"] @ p["wd2"].T + p["bd2"]
     D = V.shape[1]
-    f["logp"] = -0.5 * np.sum((V - f["mr"]) ** 2, axis=1) - 0.5 * D * math.log(2.0 * math.pi)
+    f["err"] = 0.5 * np.sum((V - f["mr"]) ** 2, axis=1)
+    f["logp"] = -f["err"] - 0.5 * D * math.log(2.0 * math.pi)
     f["kl"] = 0.5 * np.sum(f["mu"] ** 2 + np.exp(f["lv"]) - 1.0 - f["lv"], axis=1)
     return f
 
 
-def objective(p, V, labels, eps, beta, act="relu"):
+def _logp_eff(f, l, margin):
+    """log p of every window, with an anomalous window's -log p capped at margin + D/2 log 2 pi."""
+    const = f["logp"] + f["err"]                       # -D/2 log(2 pi)
+    return np.where(l < 0, -np.minimum(f["err"], margin) + const, f["logp"])
+
+
+def objective(p, V, labels, eps, beta, act="relu", margin=math.inf):
     """L of Eq. (9) for a given beta (the quantity the training maximises)."""
     f = forward(p, V, eps, act)
     l = np.asarray(labels, np.float64)
-    return float(np.mean(l * f["logp"] - 0.5 * (1.0 + l) * beta * f["kl"]))
+    return float(np.mean(l * _logp_eff(f, l, margin) - 0.5 * (1.0 + l) * beta * f["kl"]))
 
 
-def gradients(p, V, labels, eps, beta, act="relu", f=None):
+def gradients(p, V, labels, eps, beta, act="relu", f=None, margin=math.inf):
     """Gradients of J = -L with respect to every parameter (hand-derived backward pass)."""
     if f is None:
         f = forward(p, V, eps, act)
     B = V.shape[0]
     l = np.asarray(labels, np.float64)[:, None]
     g = {}
-    # reconstruction: dJ/dm' = l/B (m' - v)
-    g_mr = l / B * (f["mr"] - V)
+    # reconstruction: dJ/dm' = l/B (m' - v), for an anomalous window only below the margin
+    active = ((l[:, 0] > 0) | (f["err"] < margin))[:, None]
+    g_mr = np.where(active, l / B * (f["mr"] - V), 0.0)
     g["wd2"] = g_mr.T @ f["hd"]
     g["bd2"] = g_mr.sum(axis=0)
     g_a2 = (g_mr @ p["wd2"]) * _dact(f["a2"], act)
@@ -113,7 +128,7 @@ def adam(p, g, m, v, k, lr, b1=0.9, b2=0.999, eps=1e-8):
 
 
 def train_step(p, m, v, k, integ, V, labels, eps, *, act="relu", lr=1e-3, kl_set=3.0, kp=0.01,
-               ki=1e-4, beta_min=0.0, beta_max=1.0):
+               ki=1e-4, beta_min=0.0, beta_max=1.0, margin=math.inf):
     """Step k (>= 1): forward, beta(k) from the batch KL of the normal windows, backward, Adam.
     Returns (p, m, v, integ, info) with info = loss J, mean log p, mean KL, beta."""
     f = forward(p, V, eps, act)
@@ -121,7 +136,7 @@ def train_step(p, m, v, k, integ, V, labels, eps, *, act="relu", lr=1e-3, kl_set
     normal = l > 0
     kl_batch = float(f["kl"][normal].mean()) if normal.any() else 0.0
     beta, integ = pi_beta(kl_batch, integ, kl_set, kp, ki, beta_min, beta_max)
-    g = gradients(p, V, labels, eps, beta, act, f)
-    J = -float(np.mean(l * f["logp"] - 0.5 * (1.0 + l) * beta * f["kl"]))
+    g = gradients(p, V, labels, eps, beta, act, f, margin)
+    J = -float(np.mean(l * _logp_eff(f, l, margin) - 0.5 * (1.0 + l) * beta * f["kl"]))
     p, m, v = adam(p, g, m, v, k, lr)
     return p, m, v, integ, {"loss": J, "logp": float(f["logp"].mean()), "kl": kl_batch, "beta": beta}

@@ -124,3 +124,91 @@ def test_training_lowers_the_loss_on_normal_windows():
         p, m, v, integ, info = elbo.train_step(p, m, v, k, integ, V, labels, eps, act="tanh", lr=1e-2)
         recon.append(-info["logp"] - 4.0 * math.log(2 * math.pi))
     assert np.mean(recon[-20:]) < 0.5 * np.mean(recon[:20])
+
+
+def _margin_between(err, labels):
+    """A margin half-way between two neighbouring anomalous reconstruction errors."""
+    e = np.sort(err[labels < 0])
+    i = len(e) // 2
+    return 0.5 * (e[i - 1] + e[i])
+
+
+def test_margin_gradients_match_finite_differences():
+    p, V, labels, eps = _problem(7, B=16)
+    labels[:6] = -1.0
+    f = elbo.forward(p, V, eps, "tanh")
+    margin = _margin_between(f["err"], labels)
+    beta = 0.3
+    g = elbo.gradients(p, V, labels, eps, beta, "tanh", margin=margin)
+    rng = np.random.default_rng(8)
+    h = 1e-6
+    for name in elbo.PARAMS:
+        for _ in range(4):
+            idx = tuple(rng.integers(0, s) for s in p[name].shape)
+            q1 = {k: v.copy() for k, v in p.items()}
+            q2 = {k: v.copy() for k, v in p.items()}
+            q1[name][idx] += h
+            q2[name][idx] -= h
+            fd = -(elbo.objective(q1, V, labels, eps, beta, "tanh", margin) -
+                   elbo.objective(q2, V, labels, eps, beta, "tanh", margin)) / (2 * h)
+            assert g[name][idx] == pytest.approx(fd, rel=1e-5, abs=1e-8), (name, idx)
+
+
+def test_margin_matches_torch_clamp_and_infinite_margin_is_the_literal_objective():
+    torch = pytest.importorskip("torch")
+    p, V, labels, eps = _problem(10, B=20)
+    labels[::3] = -1.0
+    f = elbo.forward(p, V, eps, "relu")
+    margin = _margin_between(f["err"], labels)
+    g = elbo.gradients(p, V, labels, eps, 0.6, "relu", margin=margin)
+    tp = {k: torch.tensor(v, dtype=torch.float64, requires_grad=True) for k, v in p.items()}
+    Vt, lt, et = (torch.tensor(a, dtype=torch.float64) for a in (V, labels, eps))
+    h = torch.relu(Vt @ tp["w1"].T + tp["b1"])
+    mu = h @ tp["wmu"].T + tp["bmu"]
+    lv = h @ tp["wlv"].T + tp["blv"]
+    z = mu + torch.exp(0.5 * lv) * et
+    mr = torch.relu(z @ tp["wd1"].T + tp["bd1"]) @ tp["wd2"].T + tp["bd2"]
+    err = 0.5 * ((Vt - mr) ** 2).sum(1)
+    c = 0.5 * V.shape[1] * math.log(2 * math.pi)
+    kl = 0.5 * (mu ** 2 + torch.exp(lv) - 1 - lv).sum(1)
+    term = torch.where(lt > 0, -err - c, torch.clamp(err, max=margin) + c)
+    J = -(term - 0.5 * (1 + lt) * 0.6 * kl).mean()
+    J.backward()
+    for name in elbo.PARAMS:
+        np.testing.assert_allclose(g[name], tp[name].grad.numpy(), rtol=1e-10, atol=1e-12)
+    # margin = inf is Eq. (9) as printed
+    g_inf = elbo.gradients(p, V, labels, eps, 0.6, "relu", margin=math.inf)
+    g_lit = elbo.gradients(p, V, labels, eps, 0.6, "relu")
+    for name in elbo.PARAMS:
+        assert np.array_equal(g_inf[name], g_lit[name])
+    assert elbo.objective(p, V, labels, eps, 0.6, "relu", math.inf) == elbo.objective(p, V, labels, eps, 0.6, "relu")
+
+
+def test_margin_keeps_training_bounded_where_the_literal_objective_diverges():
+    """With anomalies in the batch the printed objective has no lower bound on J: Adam inflates
+    the anomalies' posterior variance and J runs away; a margin stops the push at e_i = margin."""
+    p0, V, labels, _ = _problem(11, B=64, D=12, H=16, L=3)
+    labels[:] = 1.0
+    labels[:6] = -1.0
+    rng = np.random.default_rng(12)
+    eps = rng.normal(0, 1, (64, 3))
+    D = V.shape[1]
+    out = {}
+    for margin in (math.inf, 2.0 * D):
+        p = {k: v.copy() for k, v in p0.items()}
+        m = {k: np.zeros_like(v) for k, v in p.items()}
+        v = {k: np.zeros_like(x) for k, x in p.items()}
+        integ = 0.0
+        losses = []
+        with np.errstate(over="ignore", invalid="ignore"):
+            for k in range(1, 101):
+                p, m, v, integ, info = elbo.train_step(p, m, v, k, integ, V, labels, eps, act="relu",
+                                                       lr=1e-2, margin=margin)
+                losses.append(info["loss"])
+        out[margin] = losses
+    c = 0.5 * D * math.log(2 * math.pi)
+    assert out[math.inf][-1] < -1e6
+    # every anomalous term is at most margin + c, and the normal terms are >= 0 in J
+    bounded = out[2.0 * D]
+    assert min(bounded) >= -(6 / 64) * (2.0 * D + c) - 1e-9
+    assert bounded[-1] < 0.5 * bounded[0]
