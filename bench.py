@@ -11,6 +11,10 @@ window. Prints one JSON line.
 With --mode stream it measures the streaming path instead: the config's detector shape over
 its number of streams, every push appending one step to each stream, scoring each stream's
 newest window and updating each stream's SPOT threshold (one push is one step).
+
+With --mode train it measures one semi-supervised ELBO training step of the config's detector
+shape (Eq. (9): forward, PI-controlled KL weight, backward, Adam) on a batch of --batch labelled
+windows resident in HBM (one step is one training step).
 """
 from __future__ import annotations
 
@@ -104,7 +108,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="also run a plain device copy of this size (counter calibration)")
-    ap.add_argument("--mode", choices=["batch", "stream"], default="batch")
+    ap.add_argument("--mode", choices=["batch", "stream", "train"], default="batch")
+    ap.add_argument("--batch", type=int, default=8192, help="windows per training step (--mode train)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the detector shards by stream with no collectives, "
@@ -120,6 +125,9 @@ def main():
     cfg = wl.CONFIGS[args.config]
     if args.mode == "stream":
         stream_main(args, cfg)
+        return
+    if args.mode == "train":
+        train_main(args, cfg)
         return
     t_gen = time.perf_counter()
     w = wl.generate(cfg)
@@ -358,6 +366,105 @@ def stream_main(args, cfg):
         out["cpu_baseline"] = stream_cpu_baseline(cfg, weights, x_ref, x_live, n, args.steps)
     ss.close()
     det.close()
+    print(json.dumps(out), flush=True)
+
+
+def train_flops_per_window(cfg) -> int:
+    """Matrix-product flops of one window in a training step: the forward products
+    (encoder 2HD, heads 4LH, decoder 2LH + 2DH) and the backward ones (weight and input gradients
+    of the same layers, the encoder's input gradient excluded): 2 (5HD + 9HL)."""
+    H, L, D = cfg.hidden, cfg.latent, cfg.d
+    return 2 * (5 * H * D + 9 * H * L)
+
+
+def train_cpu_baseline(cfg, p0, batch, margin, budget_s=10.0):
+    """The oracle's training step on the same batch, repeated for about budget_s seconds."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import elbo
+    p = {k: v.astype(np.float64) for k, v in p0.items()}
+    m = {k: np.zeros_like(v) for k, v in p.items()}
+    v = {k: np.zeros_like(x) for k, x in p.items()}
+    V, lab, eps = (batch.V.astype(np.float64), batch.labels.astype(np.float64), batch.eps.astype(np.float64))
+    integ, k = 0.0, 0
+    t0 = time.perf_counter()
+    while True:
+        k += 1
+        p, m, v, integ, _ = elbo.train_step(p, m, v, k, integ, V, lab, eps, act=cfg.act, margin=margin)
+        dt = time.perf_counter() - t0
+        if dt >= budget_s:
+            break
+    threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    B = V.shape[0]
+    return {"value": round(k * B / dt, 1), "unit": "windows/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{k} fp64 oracle steps on the same {B}-window batch ({dt:.1f} s, numpy BLAS threads)"}
+
+
+def train_main(args, cfg):
+    import numpy as np
+    import torch
+
+    from paper_2407_09486_amd import binding
+    from paper_2407_09486_amd import workloads as wl
+
+    B = args.batch
+    w = wl.make_weights(cfg.replace(dtype="f32"), bias_scale=0.1)
+    p0 = {k: np.asarray(getattr(w, k), np.float32)
+          for k in ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")}
+    batch = wl.training_batch(cfg, B, seed=cfg.data_seed)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    V = torch.from_numpy(batch.V).to(dev)
+    lab = torch.from_numpy(batch.labels).to(dev)
+    eps = torch.from_numpy(batch.eps).to(dev)
+    info = torch.zeros(4, dtype=torch.float32, device=dev)
+    margin = float(cfg.d)      # anomalous windows are pushed up to a reconstruction error of D
+    tr = binding.Trainer(cfg.d, cfg.hidden, cfg.latent, p0, act=cfg.act, margin=margin)
+    for _ in range(args.warmup):
+        tr.step(V, lab, eps, info)
+    tr.set_timing(True)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    gemm_ms, step_ms = [], []
+    ev0.record(stream)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        tr.step(V, lab, eps, info)
+        a, b = tr.kernel_times()
+        gemm_ms.append(a)
+        step_ms.append(b)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    g_ms = float(np.mean(gemm_ms))
+    fpw = train_flops_per_window(cfg)
+    achieved = fpw * B / (g_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS["f32"]
+    inf = info.cpu().numpy()
+    out = {
+        "metric": "windows trained/sec (one semi-supervised ELBO step: forward, backward, Adam)",
+        "value": round(B / (ms / 1e3), 1), "unit": "windows/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded labelled AR(1) windows with injected level shifts)",
+        "config": {"workload": f"train {cfg.name} detector shape: D={cfg.d} (W={cfg.window} x M={cfg.metrics}), "
+                               f"H={cfg.hidden}, L={cfg.latent}, {cfg.act}, batch {B} windows (10% anomalous), "
+                               f"anomaly margin {margin:g}",
+                   "batch": B, "wall_windows_per_s": round(B * args.steps / wall, 1),
+                   "step_kernels_ms": round(float(np.mean(step_ms)), 4),
+                   "last_loss": float(inf[0]), "last_beta": float(inf[3])},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "k_gemm (+ k_sum_splits), all products of a step",
+                     "kernel_ms": round(g_ms, 4), "flops_per_window": fpw, "windows_per_launch": B},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = train_cpu_baseline(cfg, p0, batch, margin)
+    tr.close()
     print(json.dumps(out), flush=True)
 
 

@@ -232,6 +232,70 @@ enova_status enova_stream_kernel_times(enova_stream s, double *score_kernel_ms, 
 /* Free a streaming set (synchronises the device). NULL is a no-op. */
 enova_status enova_stream_destroy(enova_stream s);
 
+/*
+ * Training (Section IV-B, Eq. (9)): one step of semi-supervised ELBO training of the detector's
+ * VAE on a batch of B labelled, normalised windows,
+ *   L = 1/B sum_i [ l_i log p(m_i | z_i) - (1 + l_i)/2 beta(k) KL(q(z | m_i) || p(z)) ],
+ * l_i = +1 (normal) or -1 (anomalous), with z_i = mu_i + exp(lv_i / 2) eps_i one reparameterised
+ * sample (eps given by the caller), a unit-variance Gaussian decoder
+ * (log p = -|v - m'|^2 / 2 - D/2 log 2 pi), beta(k) set before the backward pass by a PI
+ * controller on the mean KL of the batch's normal windows (e = kl_set - KL, P = kp / (1 + e^e),
+ * I <- I - ki e, beta = clamp(P + I + beta_min, beta_min, beta_max), I starts at 0), and an Adam
+ * step (lr, b1, b2, eps; step count k from 1) on J = -L. As printed, L has no upper bound in the
+ * anomalous windows' term -log p (training on anomalies diverges); a finite anomaly_margin m
+ * caps that term at min(e_i, m) + D/2 log 2 pi, e_i = |v_i - m'_i|^2 / 2, so an anomalous window
+ * is pushed away only until its reconstruction error reaches m. Everything runs on the device in fp32
+ * (matrix-core GEMMs with fixed-order reductions, so a step is deterministic); the parameters,
+ * the Adam moments and the controller state live in the trainer.
+ */
+typedef struct enova_trainer_s *enova_trainer;   /* opaque; owned by the library */
+
+typedef struct {
+    int32_t inputs;          /* D >= 1 (W * M of the detector) */
+    int32_t hidden, latent;  /* H >= 1, L >= 1 */
+    int32_t act;             /* enova_act */
+    float lr, adam_b1, adam_b2, adam_eps;            /* e.g. 1e-3, 0.9, 0.999, 1e-8 */
+    float kl_set, kp, ki, beta_min, beta_max;        /* e.g. 3, 0.01, 1e-4, 0, 1 */
+    float anomaly_margin;    /* > 0; +INFINITY: Eq. (9) as printed (see below) */
+} enova_train_config;
+
+/* Parameters or gradients in the layout of enova_detect_weights (w1 always fp32 here). */
+typedef struct {
+    float *w1, *b1, *wmu, *bmu, *wlv, *blv, *wd1, *bd1, *wd2, *bd2;
+} enova_train_params;
+
+/* Create a trainer on the current device from initial HOST weights (w1 fp32). Errors: EINVAL,
+ * ENOMEM, EHIP. */
+enova_status enova_train_init(const enova_train_config *config, const enova_detect_weights *init,
+                              enova_trainer *out);
+
+/*
+ *   V         device [B][D] float: the normalised windows (flattened j = t*M + m)
+ *   labels    device [B] float: +1 or -1
+ *   eps       device [B][L] float: the reparameterisation noise
+ *   out_info  device [4] float or NULL: J, mean log p, mean KL of the normal windows, beta(k)
+ * Asynchronous on `stream`. Errors: EINVAL, ENOMEM, EHIP.
+ */
+enova_status enova_train_step(enova_trainer t, const float *V, const float *labels, const float *eps,
+                              int32_t batch, float *out_info, hipStream_t stream);
+
+/* Copy the current parameters, or the last step's gradients of J, into HOST arrays (each may be
+ * NULL). Synchronises `stream`. */
+enova_status enova_train_params_get(enova_trainer t, const enova_train_params *out, hipStream_t stream);
+enova_status enova_train_grads_get(enova_trainer t, const enova_train_params *out, hipStream_t stream);
+
+/*
+ * Timing: when enabled, every following step brackets each of its matrix products (and the
+ * whole step) with HIP events on its stream; enova_train_kernel_times waits for the last step's
+ * events and reports the summed milliseconds of its products and of the whole step (0 when the
+ * last step was not timed).
+ */
+enova_status enova_train_set_timing(enova_trainer t, int32_t enable);
+enova_status enova_train_kernel_times(enova_trainer t, double *gemm_ms, double *step_ms);
+
+/* Free a trainer (synchronises the device). NULL is a no-op. */
+enova_status enova_train_destroy(enova_trainer t);
+
 /* flags[i] = scores[i] > threshold for i < n_windows (device pointers). Asynchronous. */
 enova_status enova_detect_flag(enova_detector det, const float *scores, int64_t n_windows,
                                float threshold, uint8_t *out_flags, hipStream_t stream);

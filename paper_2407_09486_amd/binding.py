@@ -26,7 +26,8 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_detect_flag", "enova_detect_set_timing", "enova_detect_kernel_times",
            "enova_detect_kernel_kind", "enova_stream_create", "enova_stream_push",
            "enova_stream_state", "enova_stream_kernel_times", "enova_stream_destroy",
-           "enova_status_str", "enova_last_error"]
+           "enova_train_init", "enova_train_step", "enova_train_params_get", "enova_train_grads_get",
+           "enova_train_set_timing", "enova_train_kernel_times", "enova_train_destroy", "enova_status_str", "enova_last_error"]
 
 
 class EnovaError(RuntimeError):
@@ -42,6 +43,19 @@ class enova_detect_config(ctypes.Structure):
 
 
 class enova_detect_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")]
+
+
+class enova_train_config(ctypes.Structure):
+    _fields_ = [("inputs", ctypes.c_int32), ("hidden", ctypes.c_int32), ("latent", ctypes.c_int32),
+                ("act", ctypes.c_int32), ("lr", ctypes.c_float), ("adam_b1", ctypes.c_float),
+                ("adam_b2", ctypes.c_float), ("adam_eps", ctypes.c_float), ("kl_set", ctypes.c_float),
+                ("kp", ctypes.c_float), ("ki", ctypes.c_float), ("beta_min", ctypes.c_float),
+                ("beta_max", ctypes.c_float), ("anomaly_margin", ctypes.c_float)]
+
+
+class enova_train_params(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")]
 
@@ -76,6 +90,14 @@ def lib():
     L.enova_stream_state.argtypes = [P, P, P, P, P, P]
     L.enova_stream_kernel_times.argtypes = [P, P, P]
     L.enova_stream_destroy.argtypes = [P]
+    L.enova_train_init.argtypes = [ctypes.POINTER(enova_train_config), ctypes.POINTER(enova_detect_weights),
+                                   ctypes.POINTER(P)]
+    L.enova_train_step.argtypes = [P, P, P, P, I32, P, P]
+    L.enova_train_params_get.argtypes = [P, ctypes.POINTER(enova_train_params), P]
+    L.enova_train_grads_get.argtypes = [P, ctypes.POINTER(enova_train_params), P]
+    L.enova_train_set_timing.argtypes = [P, I32]
+    L.enova_train_kernel_times.argtypes = [P, P, P]
+    L.enova_train_destroy.argtypes = [P]
     for name in EXPORTS[:-2]:
         getattr(L, name).restype = st
     L.enova_status_str.argtypes = [st]
@@ -237,6 +259,57 @@ def enova_stream_destroy(shandle):
     _check(lib().enova_stream_destroy(ctypes.c_void_p(shandle)), "enova_stream_destroy")
 
 
+TRAIN_PARAMS = ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")
+
+
+def enova_train_init(config: enova_train_config, weights: dict):
+    """weights: host float32 arrays in the layout of enova_detect_weights. Returns the handle."""
+    keep = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in TRAIN_PARAMS}
+    w = enova_detect_weights(**{k: _hptr(keep[k]) for k in TRAIN_PARAMS})
+    h = ctypes.c_void_p()
+    _check(lib().enova_train_init(ctypes.byref(config), ctypes.byref(w), ctypes.byref(h)), "enova_train_init")
+    return h.value
+
+
+def enova_train_step(thandle, V, labels, eps, batch, out_info=None, stream=None):
+    _check(lib().enova_train_step(ctypes.c_void_p(thandle), _dptr(V), _dptr(labels), _dptr(eps), int(batch),
+                                  _dptr(out_info), _stream(stream)),
+           "enova_train_step")
+
+
+def _train_get(fn, name, thandle, shapes, stream):
+    out = {k: np.zeros(shapes[k], np.float32) for k in TRAIN_PARAMS}
+    p = enova_train_params(**{k: _hptr(out[k]) for k in TRAIN_PARAMS})
+    _check(fn(ctypes.c_void_p(thandle), ctypes.byref(p), _stream(stream)), name)
+    return out
+
+
+def enova_train_params_get(thandle, shapes, stream=None):
+    """Returns the current parameters as host float32 arrays of the given shapes."""
+    return _train_get(lib().enova_train_params_get, "enova_train_params_get", thandle, shapes, stream)
+
+
+def enova_train_grads_get(thandle, shapes, stream=None):
+    """Returns the last step's gradients of J as host float32 arrays of the given shapes."""
+    return _train_get(lib().enova_train_grads_get, "enova_train_grads_get", thandle, shapes, stream)
+
+
+def enova_train_set_timing(thandle, enable):
+    _check(lib().enova_train_set_timing(ctypes.c_void_p(thandle), int(bool(enable))), "enova_train_set_timing")
+
+
+def enova_train_kernel_times(thandle):
+    """Returns (milliseconds in the last step's matrix products, milliseconds of the whole step)."""
+    a, b = ctypes.c_double(), ctypes.c_double()
+    _check(lib().enova_train_kernel_times(ctypes.c_void_p(thandle), ctypes.byref(a), ctypes.byref(b)),
+           "enova_train_kernel_times")
+    return a.value, b.value
+
+
+def enova_train_destroy(thandle):
+    _check(lib().enova_train_destroy(ctypes.c_void_p(thandle)), "enova_train_destroy")
+
+
 # ----------------------------------------------------------------------------- convenience
 def make_config(metrics, window, stride, hidden, latent=16, dtype="f32", act="relu",
                 kernel="auto", ref_frac=0.5) -> enova_detect_config:
@@ -320,6 +393,49 @@ class StreamSet:
     def close(self):
         if self.handle:
             enova_stream_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Trainer:
+    """Owns one trainer handle: semi-supervised ELBO steps of a D -> H -> L VAE on the device."""
+
+    def __init__(self, inputs, hidden, latent, weights: dict, act="relu", lr=1e-3, adam_b1=0.9,
+                 adam_b2=0.999, adam_eps=1e-8, kl_set=3.0, kp=0.01, ki=1e-4, beta_min=0.0, beta_max=1.0,
+                 margin=math.inf):
+        self.cfg = enova_train_config(inputs=inputs, hidden=hidden, latent=latent,
+                                      act={"relu": ENOVA_RELU, "tanh": ENOVA_TANH}[act], lr=lr,
+                                      adam_b1=adam_b1, adam_b2=adam_b2, adam_eps=adam_eps, kl_set=kl_set,
+                                      kp=kp, ki=ki, beta_min=beta_min, beta_max=beta_max,
+                                      anomaly_margin=margin)
+        D, H, L = inputs, hidden, latent
+        self.shapes = {"w1": (H, D), "b1": (H,), "wmu": (L, H), "bmu": (L,), "wlv": (L, H), "blv": (L,),
+                       "wd1": (H, L), "bd1": (H,), "wd2": (D, H), "bd2": (D,)}
+        self.handle = enova_train_init(self.cfg, weights)
+
+    def step(self, V, labels, eps, info=None, stream=None):
+        enova_train_step(self.handle, V, labels, eps, V.shape[0], info, stream)
+
+    def params(self, stream=None):
+        return enova_train_params_get(self.handle, self.shapes, stream)
+
+    def set_timing(self, enable=True):
+        enova_train_set_timing(self.handle, enable)
+
+    def kernel_times(self):
+        return enova_train_kernel_times(self.handle)
+
+    def grads(self, stream=None):
+        return enova_train_grads_get(self.handle, self.shapes, stream)
+
+    def close(self):
+        if self.handle:
+            enova_train_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

@@ -19,7 +19,8 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wall", "-Wno-unused-function"]
 
-SOURCES = ["detector.cpp", "pot.cpp", "k_aux.hip", "k_score_valu.hip", "k_score_mfma.hip", "k_stream.hip"]
+SOURCES = ["detector.cpp", "pot.cpp", "k_aux.hip", "k_score_valu.hip", "k_score_mfma.hip", "k_stream.hip",
+           "k_train.hip", "trainer.cpp"]
 
 
 def _compile(src: str) -> str:

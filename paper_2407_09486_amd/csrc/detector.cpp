@@ -14,11 +14,11 @@
 #include "enova_detect.h"
 #include "internal.h"
 
-using namespace enova;
-
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace enova {
 
 enova_status fail(enova_status st, const char *fmt, ...)
 {
@@ -36,22 +36,11 @@ enova_status hip_fail(hipError_t e, const char *what)
     return fail(ENOVA_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Keeps the caller's current device and switches to the detector's for the call's duration.
-struct DeviceGuard {
-    int prev = -1;
-    bool ok = false;
-    explicit DeviceGuard(int dev)
-    {
-        if (hipGetDevice(&prev) != hipSuccess)
-            return;
-        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
-    }
-    ~DeviceGuard()
-    {
-        if (ok && prev >= 0)
-            (void)hipSetDevice(prev);
-    }
-};
+}  // namespace enova
+
+using namespace enova;
+
+namespace {
 
 float bf16_bits_to_float(uint16_t b)
 {

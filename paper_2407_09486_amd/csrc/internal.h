@@ -54,6 +54,27 @@ constexpr size_t kLdsLimit = 160 * 1024;
 constexpr int kPrefetchSteps = 8;
 constexpr int kPrefetchRows = 2;
 
+// Error reporting of the C entry points: records the message returned by enova_last_error().
+enova_status fail(enova_status st, const char *fmt, ...);
+enova_status hip_fail(hipError_t e, const char *what);
+
+// Keeps the caller's current device and switches to another for a call's duration.
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess)
+            return;
+        ok = prev == dev || hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard()
+    {
+        if (ok && prev >= 0)
+            (void)hipSetDevice(prev);
+    }
+};
+
 bool plan_geometry(const enova_detect_config &cfg, Geometry *g);
 // Wave layout of the matrix-core kernel for dtype and hb 32-row hidden blocks: hidden blocks and
 // 32-window blocks per wave, waves along the hidden rows, waves per block.
@@ -193,5 +214,37 @@ hipError_t launch_spot_update(const float *scores, int n, const SpotState &s, ui
                               hipStream_t st);
 // Refits z: every marked stream (all = true), or the streams listed by the last update.
 hipError_t launch_spot_fit(int n, double q, const SpotState &s, bool all, hipStream_t st);
+
+// ---------------------------------------------------------------------------------------------
+// Training (fp32): C(i, j) [+]= sum_k A(i, k) B(k, j), A(i, k) = A[i*ai + k*ak],
+// B(k, j) = B[k*bk + j*bj], C(i, j) = C[i*ldc + j]; and the element-wise steps around it.
+// ---------------------------------------------------------------------------------------------
+struct TrainHyper {
+    float lr, b1, b2, eps;
+    float kl_set, kp, ki, beta_min, beta_max;
+    float margin;   // cap of an anomalous window's reconstruction error (+inf: none)
+};
+// A long reduction over few output tiles is split into slices whose partial tiles go to `work`
+// (gemm_workspace_floats(m, n, k) floats; NULL: no split) and are then summed in slice order.
+int64_t gemm_workspace_floats(int m, int n, int k);
+hipError_t launch_gemm(const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk, int64_t bj,
+                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *work, hipStream_t st);
+hipError_t launch_bias_act(float *pre, const float *bias, float *out, int64_t rows, int cols, int act,
+                           hipStream_t st);
+hipError_t launch_dact(float *g, const float *pre, int64_t total, int act, hipStream_t st);
+hipError_t launch_latent(float *mu, float *lv, const float *bmu, const float *blv, const float *eps, float *sd,
+                         float *z, float *kl, int rows, int L, hipStream_t st);
+hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
+                        int rows, int D, float margin, hipStream_t st);
+hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
+                       const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st);
+hipError_t launch_latent_grad(float *gz, float *glv, const float *mu, const float *lv, const float *sd,
+                              const float *eps, const float *labels, const float *beta, int rows, int L,
+                              hipStream_t st);
+// out[j] = sum over the rows of X[i][j], through colsum_workspace_floats(rows, cols) floats of `work`.
+int64_t colsum_workspace_floats(int64_t rows, int cols);
+hipError_t launch_colsum(const float *X, int64_t rows, int cols, float *out, float *work, hipStream_t st);
+hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
+                       int64_t step, hipStream_t st);
 
 }  // namespace enova

@@ -1,0 +1,349 @@
+// Host side of the training entry points (Section IV-B, Eq. (9)): parameter, gradient and Adam
+// buffers, the batch workspace, and the launch sequence of one ELBO step.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <new>
+
+#include "enova_detect.h"
+#include "internal.h"
+
+using namespace enova;
+
+namespace {
+
+// The parameters in the order of enova_detect_weights, as one flat buffer.
+enum { P_W1, P_B1, P_WMU, P_BMU, P_WLV, P_BLV, P_WD1, P_BD1, P_WD2, P_BD2, P_COUNT };
+
+}  // namespace
+
+struct enova_trainer_s {
+    int device = 0;
+    int D = 0, H = 0, L = 0, act = 0;
+    TrainHyper hyper{};
+    int64_t step = 0;
+    int64_t off[P_COUNT + 1] = {};   // offsets into the flat buffers (floats)
+    float *p = nullptr, *g = nullptr, *m = nullptr, *v = nullptr;
+    float *state = nullptr;          // [0] PI integral, [1] beta of the step
+    // batch workspace
+    int cap = 0;
+    float *a1 = nullptr, *h = nullptr, *a2 = nullptr, *hd = nullptr, *gh = nullptr;   // [B][H]
+    float *mu = nullptr, *lv = nullptr, *sd = nullptr, *z = nullptr;                 // [B][L]
+    float *gmu = nullptr, *glv = nullptr;                                            // [B][L]
+    float *out = nullptr;                                                          // [B][D]
+    float *kl = nullptr, *logp = nullptr;                                          // [B]
+    float *work = nullptr;                                                         // split-reduction partials
+    int64_t work_cap = 0;
+    // timing: an event pair around every product of the last step and around the whole step
+    static constexpr int kMaxEvents = 2 * 16 + 2;
+    bool timed = false;
+    int n_events = 0;
+    hipEvent_t ev[kMaxEvents] = {};
+};
+
+namespace {
+
+void free_trainer(enova_trainer t)
+{
+    if (!t)
+        return;
+    void *ptrs[] = {t->p,  t->g,  t->m,  t->v,  t->state, t->a1,  t->h,   t->a2,  t->hd,  t->gh,
+                    t->mu, t->lv, t->sd, t->z,  t->gmu,   t->glv, t->out, t->kl,  t->logp, t->work};
+    for (void *q : ptrs)
+        if (q)
+            (void)hipFree(q);
+    for (hipEvent_t e : t->ev)
+        if (e)
+            (void)hipEventDestroy(e);
+    delete t;
+}
+
+enova_status alloc_floats(float **dst, size_t n)
+{
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(dst), std::max<size_t>(n, 1) * sizeof(float));
+    if (e != hipSuccess) {
+        *dst = nullptr;
+        return fail(ENOVA_ENOMEM, "hipMalloc(%zu): %s", n * sizeof(float), hipGetErrorString(e));
+    }
+    return ENOVA_OK;
+}
+
+int64_t workspace_floats(const enova_trainer t, int B)
+{
+    // every product of a step, as (m, n, k)
+    const int D = t->D, H = t->H, L = t->L;
+    const int shapes[][3] = {{B, H, D}, {B, L, H}, {B, H, L}, {B, D, H}, {D, H, B}, {B, H, D},
+                             {H, L, B}, {B, L, H}, {L, H, B}, {B, H, L}, {H, D, B}};
+    int64_t ws = 0;
+    for (const auto &sh : shapes)
+        ws = std::max(ws, gemm_workspace_floats(sh[0], sh[1], sh[2]));
+    return std::max(ws, colsum_workspace_floats(B, std::max({D, H, L})));
+}
+
+// Grows the batch buffers to B rows (freeing the old ones synchronises the device).
+enova_status ensure_batch(enova_trainer t, int B)
+{
+    enova_status st;
+    const int64_t ws = workspace_floats(t, B);
+    if (ws > t->work_cap) {
+        (void)hipFree(t->work);
+        t->work = nullptr;
+        t->work_cap = 0;
+        if ((st = alloc_floats(&t->work, static_cast<size_t>(ws))) != ENOVA_OK)
+            return st;
+        t->work_cap = ws;
+    }
+    if (B <= t->cap)
+        return ENOVA_OK;
+    float **bh[] = {&t->a1, &t->h, &t->a2, &t->hd, &t->gh};
+    float **bl[] = {&t->mu, &t->lv, &t->sd, &t->z, &t->gmu, &t->glv};
+    float **b1[] = {&t->kl, &t->logp};
+    for (float **q : bh)
+        (void)hipFree(*q), *q = nullptr;
+    for (float **q : bl)
+        (void)hipFree(*q), *q = nullptr;
+    for (float **q : b1)
+        (void)hipFree(*q), *q = nullptr;
+    (void)hipFree(t->out);
+    t->out = nullptr;
+    t->cap = 0;
+    for (float **q : bh)
+        if ((st = alloc_floats(q, static_cast<size_t>(B) * t->H)) != ENOVA_OK)
+            return st;
+    for (float **q : bl)
+        if ((st = alloc_floats(q, static_cast<size_t>(B) * t->L)) != ENOVA_OK)
+            return st;
+    for (float **q : b1)
+        if ((st = alloc_floats(q, static_cast<size_t>(B))) != ENOVA_OK)
+            return st;
+    if ((st = alloc_floats(&t->out, static_cast<size_t>(B) * t->D)) != ENOVA_OK)
+        return st;
+    t->cap = B;
+    return ENOVA_OK;
+}
+
+enova_status copy_out(enova_trainer t, const float *src, const enova_train_params *out, hipStream_t stream)
+{
+    float *dst[P_COUNT] = {out->w1, out->b1, out->wmu, out->bmu, out->wlv, out->blv, out->wd1, out->bd1,
+                           out->wd2, out->bd2};
+    hipError_t e = hipSuccess;
+    for (int k = 0; k < P_COUNT && e == hipSuccess; ++k)
+        if (dst[k])
+            e = hipMemcpyAsync(dst[k], src + t->off[k], (t->off[k + 1] - t->off[k]) * sizeof(float),
+                               hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(stream);
+    return e == hipSuccess ? ENOVA_OK : hip_fail(e, "trainer copy");
+}
+
+}  // namespace
+
+extern "C" {
+
+enova_status enova_train_init(const enova_train_config *c, const enova_detect_weights *w, enova_trainer *out)
+{
+    if (!c || !w || !out)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    *out = nullptr;
+    if (c->inputs < 1 || c->hidden < 1 || c->latent < 1 || (c->act != ENOVA_RELU && c->act != ENOVA_TANH))
+        return fail(ENOVA_EINVAL, "bad trainer shape");
+    if (!(c->lr > 0.0f) || !(c->adam_b1 >= 0.0f && c->adam_b1 < 1.0f) || !(c->adam_b2 >= 0.0f && c->adam_b2 < 1.0f) ||
+        !(c->adam_eps > 0.0f) || !(c->beta_min <= c->beta_max) || !(c->anomaly_margin > 0.0f))
+        return fail(ENOVA_EINVAL, "bad trainer hyper-parameters");
+    const void *src[P_COUNT] = {w->w1, w->b1, w->wmu, w->bmu, w->wlv, w->blv, w->wd1, w->bd1, w->wd2, w->bd2};
+    for (const void *q : src)
+        if (!q)
+            return fail(ENOVA_EINVAL, "NULL weight array");
+    enova_trainer t = new (std::nothrow) enova_trainer_s;
+    if (!t)
+        return fail(ENOVA_ENOMEM, "host allocation");
+    if (hipGetDevice(&t->device) != hipSuccess) {
+        delete t;
+        return fail(ENOVA_EHIP, "no current HIP device");
+    }
+    t->D = c->inputs;
+    t->H = c->hidden;
+    t->L = c->latent;
+    t->act = c->act;
+    t->hyper = TrainHyper{c->lr,     c->adam_b1,  c->adam_b2,  c->adam_eps,       c->kl_set,
+                          c->kp,     c->ki,       c->beta_min, c->beta_max, c->anomaly_margin};
+    const int64_t D = t->D, H = t->H, L = t->L;
+    const int64_t sizes[P_COUNT] = {H * D, H, L * H, L, L * H, L, H * L, H, D * H, D};
+    for (int k = 0; k < P_COUNT; ++k)
+        t->off[k + 1] = t->off[k] + sizes[k];
+    const size_t total = static_cast<size_t>(t->off[P_COUNT]);
+    enova_status st;
+    if ((st = alloc_floats(&t->p, total)) != ENOVA_OK || (st = alloc_floats(&t->g, total)) != ENOVA_OK ||
+        (st = alloc_floats(&t->m, total)) != ENOVA_OK || (st = alloc_floats(&t->v, total)) != ENOVA_OK ||
+        (st = alloc_floats(&t->state, 2)) != ENOVA_OK) {
+        free_trainer(t);
+        return st;
+    }
+    hipError_t e = hipSuccess;
+    for (int k = 0; k < P_COUNT && e == hipSuccess; ++k)
+        e = hipMemcpy(t->p + t->off[k], src[k], sizes[k] * sizeof(float), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemset(t->m, 0, total * sizeof(float));
+    if (e == hipSuccess)
+        e = hipMemset(t->v, 0, total * sizeof(float));
+    if (e == hipSuccess)
+        e = hipMemset(t->g, 0, total * sizeof(float));
+    if (e == hipSuccess)
+        e = hipMemset(t->state, 0, 2 * sizeof(float));
+    if (e != hipSuccess) {
+        free_trainer(t);
+        return hip_fail(e, "trainer upload");
+    }
+    *out = t;
+    return ENOVA_OK;
+}
+
+enova_status enova_train_step(enova_trainer t, const float *V, const float *labels, const float *eps,
+                              int32_t B, float *info, hipStream_t s)
+{
+    if (!t || !V || !labels || !eps)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    if (B < 1)
+        return fail(ENOVA_EINVAL, "batch must be >= 1");
+    DeviceGuard dg(t->device);
+    enova_status st = ensure_batch(t, B);
+    if (st != ENOVA_OK)
+        return st;
+    const int D = t->D, H = t->H, L = t->L, act = t->act;
+    float *P = t->p, *G = t->g;
+    const int64_t *o = t->off;
+    hipError_t e = hipSuccess;
+    auto run = [&](hipError_t r) {
+        if (e == hipSuccess)
+            e = r;
+    };
+    int ne = 0;
+    auto mark = [&]() {
+        if (t->timed && ne < enova_trainer_s::kMaxEvents)
+            run(hipEventRecord(t->ev[ne++], s));
+    };
+    // every product of the step, bracketed by events when timing is on
+    auto gemm = [&](const float *A, int64_t ai, int64_t ak, const float *Bm, int64_t bk, int64_t bj, float *C,
+                    int64_t ldc, int m, int n, int k, bool acc, float *work, hipStream_t st) {
+        mark();
+        run(launch_gemm(A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, acc, work, st));
+        mark();
+    };
+    mark();
+    // forward: a1 = V W1^T (+ b1), h = act(a1)
+    gemm(V, D, 1, P + o[P_W1], 1, D, t->a1, H, B, H, D, false, t->work, s);
+    run(launch_bias_act(t->a1, P + o[P_B1], t->h, B, H, act, s));
+    // heads, reparameterised latent and KL
+    gemm(t->h, H, 1, P + o[P_WMU], 1, H, t->mu, L, B, L, H, false, t->work, s);
+    gemm(t->h, H, 1, P + o[P_WLV], 1, H, t->lv, L, B, L, H, false, t->work, s);
+    run(launch_latent(t->mu, t->lv, P + o[P_BMU], P + o[P_BLV], eps, t->sd, t->z, t->kl, B, L, s));
+    // decoder: a2 = z Wd1^T (+ bd1), hd = act(a2), m' = hd Wd2^T (+ bd2) -> log p and dJ/dm'
+    gemm(t->z, L, 1, P + o[P_WD1], 1, L, t->a2, H, B, H, L, false, t->work, s);
+    run(launch_bias_act(t->a2, P + o[P_BD1], t->hd, B, H, act, s));
+    gemm(t->hd, H, 1, P + o[P_WD2], 1, H, t->out, D, B, D, H, false, t->work, s);
+    run(launch_recon(t->out, P + o[P_BD2], V, labels, t->logp, B, D, t->hyper.margin, s));
+    // beta(k) from this batch's KL, before the backward pass
+    run(launch_beta(t->kl, t->logp, labels, B, D, t->hyper, t->state, t->state + 1, info, s));
+    // backward through the decoder
+    gemm(t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, false, t->work, s);      // dWd2 = G^T hd
+    run(launch_colsum(t->out, B, D, G + o[P_BD2], t->work, s));
+    gemm(t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, false, t->work, s);      // dJ/dhd = G Wd2
+    run(launch_dact(t->gh, t->a2, static_cast<int64_t>(B) * H, act, s));
+    gemm(t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, false, t->work, s);        // dWd1 = G^T z
+    run(launch_colsum(t->gh, B, H, G + o[P_BD1], t->work, s));
+    gemm(t->gh, H, 1, P + o[P_WD1], L, 1, t->gmu, L, B, L, H, false, t->work, s);      // dJ/dz = G Wd1
+    // latent: dJ/dz becomes dJ/dmu in place; dJ/dlv
+    run(launch_latent_grad(t->gmu, t->glv, t->mu, t->lv, t->sd, eps, labels, t->state + 1, B, L, s));
+    gemm(t->gmu, 1, L, t->h, H, 1, G + o[P_WMU], H, L, H, B, false, t->work, s);      // dWmu = G^T h
+    run(launch_colsum(t->gmu, B, L, G + o[P_BMU], t->work, s));
+    gemm(t->glv, 1, L, t->h, H, 1, G + o[P_WLV], H, L, H, B, false, t->work, s);      // dWlv = G^T h
+    run(launch_colsum(t->glv, B, L, G + o[P_BLV], t->work, s));
+    // backward through the encoder: dJ/dh = G_mu Wmu + G_lv Wlv, times act'(a1)
+    gemm(t->gmu, L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, L, false, t->work, s);
+    gemm(t->glv, L, 1, P + o[P_WLV], H, 1, t->gh, H, B, H, L, true, t->work, s);
+    run(launch_dact(t->gh, t->a1, static_cast<int64_t>(B) * H, act, s));
+    gemm(t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, false, t->work, s);            // dW1 = G^T V
+    run(launch_colsum(t->gh, B, H, G + o[P_B1], t->work, s));
+    // Adam
+    t->step += 1;
+    run(launch_adam(P, G, t->m, t->v, o[P_COUNT], t->hyper, t->step, s));
+    mark();
+    t->n_events = ne;
+    if (e != hipSuccess)
+        return hip_fail(e, "training kernels");
+    return ENOVA_OK;
+}
+
+enova_status enova_train_params_get(enova_trainer t, const enova_train_params *out, hipStream_t stream)
+{
+    if (!t || !out)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(t->device);
+    return copy_out(t, t->p, out, stream);
+}
+
+enova_status enova_train_grads_get(enova_trainer t, const enova_train_params *out, hipStream_t stream)
+{
+    if (!t || !out)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    DeviceGuard dg(t->device);
+    return copy_out(t, t->g, out, stream);
+}
+
+enova_status enova_train_set_timing(enova_trainer t, int32_t enable)
+{
+    if (!t)
+        return fail(ENOVA_EINVAL, "NULL trainer");
+    DeviceGuard dg(t->device);
+    if (enable && !t->ev[0]) {
+        for (hipEvent_t &e : t->ev) {
+            hipError_t r = hipEventCreate(&e);
+            if (r != hipSuccess)
+                return hip_fail(r, "hipEventCreate");
+        }
+    }
+    t->timed = enable != 0;
+    t->n_events = 0;
+    return ENOVA_OK;
+}
+
+enova_status enova_train_kernel_times(enova_trainer t, double *gemm_ms, double *step_ms)
+{
+    if (!t || !gemm_ms || !step_ms)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    *gemm_ms = *step_ms = 0.0;
+    const int ne = t->n_events;
+    if (ne < 2)
+        return ENOVA_OK;
+    DeviceGuard dg(t->device);
+    hipError_t r = hipEventSynchronize(t->ev[ne - 1]);
+    if (r != hipSuccess)
+        return hip_fail(r, "hipEventSynchronize");
+    // events: [step start] (gemm start, gemm end)* [step end]
+    double g = 0.0;
+    for (int i = 1; i + 1 <= ne - 2; i += 2) {
+        float ms = 0.0f;
+        if ((r = hipEventElapsedTime(&ms, t->ev[i], t->ev[i + 1])) != hipSuccess)
+            return hip_fail(r, "hipEventElapsedTime");
+        g += ms;
+    }
+    float all = 0.0f;
+    if ((r = hipEventElapsedTime(&all, t->ev[0], t->ev[ne - 1])) != hipSuccess)
+        return hip_fail(r, "hipEventElapsedTime");
+    *gemm_ms = g;
+    *step_ms = all;
+    return ENOVA_OK;
+}
+
+enova_status enova_train_destroy(enova_trainer t)
+{
+    if (!t)
+        return ENOVA_OK;
+    DeviceGuard dg(t->device);
+    (void)hipDeviceSynchronize();
+    free_trainer(t);
+    return ENOVA_OK;
+}
+
+}  // extern "C"

@@ -406,3 +406,37 @@ def from_arrays(cfg: Config, x, stream_offsets) -> Workload:
         x = None
     return Workload(cfg=cfg, stream_offsets=offs, x=x, x_bits=bits,
                     labels=np.zeros(int(offs[-1]), np.uint8), streams=np.arange(len(offs) - 1))
+
+
+# ----------------------------------------------------------------------------- training batches
+@dataclass
+class TrainBatch:
+    """One labelled batch for a training step: V [B, D] float32 (rows flattened j = t*M + m),
+    labels [B] float32 (+1 normal, -1 anomalous), eps [B, L] float32 (reparameterisation noise)."""
+    V: np.ndarray
+    labels: np.ndarray
+    eps: np.ndarray
+
+
+def training_batch(cfg: Config, batch: int, seed: int = 0, anomaly_frac: float = 0.1) -> TrainBatch:
+    """Windows of W steps of M unit-variance AR(1) metrics (the scale of z-scored metrics).
+
+    A fraction ``anomaly_frac`` of the rows (drawn per row) are anomalous: one random metric takes
+    a level shift of U(3, 6) standard deviations, of random sign, from a random step to the end of
+    the window. eps is standard normal. Every draw comes from ``default_rng(seed)``.
+    """
+    rng = np.random.default_rng(seed)
+    W, M, L = cfg.window, cfg.metrics, cfg.latent
+    e = rng.standard_normal((batch, W, M))
+    e[:, 0] *= SIGMA_MARG
+    x = lfilter([1.0], [1.0, -PHI], e, axis=1) / SIGMA_MARG
+    anomalous = rng.random(batch) < anomaly_frac
+    idx = np.flatnonzero(anomalous)
+    metric = rng.integers(0, M, size=idx.size)
+    start = rng.integers(0, W, size=idx.size)
+    shift = rng.uniform(3.0, 6.0, size=idx.size) * rng.choice([-1.0, 1.0], size=idx.size)
+    for r, m, t0, a in zip(idx, metric, start, shift):
+        x[r, t0:, m] += a
+    labels = np.where(anomalous, -1.0, 1.0).astype(np.float32)
+    eps = rng.standard_normal((batch, L)).astype(np.float32)
+    return TrainBatch(V=np.ascontiguousarray(x.reshape(batch, W * M), dtype=np.float32), labels=labels, eps=eps)

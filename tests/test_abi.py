@@ -104,6 +104,33 @@ def test_streaming_entry_points_reject_null_handles():
     assert L.enova_stream_destroy(None) == binding.ENOVA_OK
 
 
+@pytest.mark.parametrize("over", [dict(inputs=0), dict(hidden=0), dict(latent=0), dict(act=5), dict(lr=0.0),
+                                  dict(adam_b1=1.0), dict(adam_b2=-0.1), dict(adam_eps=0.0),
+                                  dict(beta_min=1.0, beta_max=0.5), dict(anomaly_margin=0.0),
+                                  dict(anomaly_margin=float("nan"))])
+def test_training_entry_points_reject_bad_arguments(over):
+    _ensure_built()
+    L = binding.lib()
+    base = dict(inputs=8, hidden=4, latent=2, act=binding.ENOVA_RELU, lr=1e-3, adam_b1=0.9, adam_b2=0.999,
+                adam_eps=1e-8, kl_set=3.0, kp=0.01, ki=1e-4, beta_min=0.0, beta_max=1.0,
+                anomaly_margin=float("inf"))
+    base.update(over)
+    c = binding.enova_train_config(**base)
+    keep = [np.zeros(64, np.float32) for _ in range(10)]
+    ws = binding.enova_detect_weights(*[ctypes.c_void_p(a.ctypes.data) for a in keep])
+    h = ctypes.c_void_p()
+    assert L.enova_train_init(ctypes.byref(c), ctypes.byref(ws), ctypes.byref(h)) == binding.ENOVA_EINVAL
+    assert not h.value and L.enova_last_error()
+    assert L.enova_train_init(None, None, None) == binding.ENOVA_EINVAL
+    assert L.enova_train_step(None, None, None, None, 4, None, None) == binding.ENOVA_EINVAL
+    assert L.enova_train_params_get(None, None, None) == binding.ENOVA_EINVAL
+    assert L.enova_train_grads_get(None, None, None) == binding.ENOVA_EINVAL
+    assert L.enova_train_set_timing(None, 1) == binding.ENOVA_EINVAL
+    a, b = ctypes.c_double(), ctypes.c_double()
+    assert L.enova_train_kernel_times(None, ctypes.byref(a), ctypes.byref(b)) == binding.ENOVA_EINVAL
+    assert L.enova_train_destroy(None) == binding.ENOVA_OK
+
+
 def test_binding_refuses_host_tensors():
     import torch
     with pytest.raises(ValueError):
