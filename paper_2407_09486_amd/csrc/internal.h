@@ -226,24 +226,24 @@ struct TrainHyper {
 };
 // A long reduction over few output tiles is split into slices whose partial tiles go to `work`
 // (gemm_workspace_floats(m, n, k) floats; NULL: no split) and are then summed in slice order.
+// rowsum (or NULL) receives sum_k A(i, k) for every i < m.
 int64_t gemm_workspace_floats(int m, int n, int k);
 hipError_t launch_gemm(const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk, int64_t bj,
-                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *work, hipStream_t st);
+                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *rowsum, float *work,
+                       hipStream_t st);
 hipError_t launch_bias_act(float *pre, const float *bias, float *out, int64_t rows, int cols, int act,
                            hipStream_t st);
 hipError_t launch_dact(float *g, const float *pre, int64_t total, int act, hipStream_t st);
-hipError_t launch_latent(float *mu, float *lv, const float *bmu, const float *blv, const float *eps, float *sd,
-                         float *z, float *kl, int rows, int L, hipStream_t st);
+// ml: [rows][2L] = [mu | lv] per window (biases bml = [bmu | blv] added in place).
+hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
+                         int L, hipStream_t st);
 hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
                         int rows, int D, float margin, hipStream_t st);
 hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
                        const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st);
-hipError_t launch_latent_grad(float *gz, float *glv, const float *mu, const float *lv, const float *sd,
-                              const float *eps, const float *labels, const float *beta, int rows, int L,
-                              hipStream_t st);
-// out[j] = sum over the rows of X[i][j], through colsum_workspace_floats(rows, cols) floats of `work`.
-int64_t colsum_workspace_floats(int64_t rows, int cols);
-hipError_t launch_colsum(const float *X, int64_t rows, int cols, float *out, float *work, hipStream_t st);
+// gz: [rows][L] = dJ/dz; gml: [rows][2L] = [dJ/dmu | dJ/dlv].
+hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, const float *sd, const float *eps,
+                              const float *labels, const float *beta, int rows, int L, hipStream_t st);
 hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
                        int64_t step, hipStream_t st);
 

@@ -16,88 +16,205 @@ namespace enova {
 
 namespace {
 
-constexpr int kGemmTile = 64;   // C tile of a block (2 x 2 waves of 32 x 32)
-constexpr int kGemmK = 32;      // reduction slice staged in LDS
-constexpr int kGemmPitch = kGemmTile + 4;
-constexpr int kGemmTargetBlocks = 1024;   // split the reduction until a launch has about this many blocks
-constexpr int kGemmMinSlice = 256;        // ... but keep every slice at least this long
-constexpr int kGemmMaxSplits = 64;
-constexpr int kColsumRows = 128;         // rows per block of a column sum ...
-constexpr int kColsumMaxChunks = 64;     // ... in at most this many row chunks
+constexpr int kGemmTile = 128;  // C tile of a block: 2 x 2 waves of 64 x 64 (2 x 2 matrix ops of 32 x 32)
+constexpr int kGemmK = 32;      // reduction slice staged in LDS (double-buffered)
+constexpr int kGemmPitch = kGemmK + 4;   // floats per staged row: 16-byte rows, conflict-free 16-byte reads
+constexpr int kGemmTargetBlocks = 512;   // split the reduction until a launch has about this many blocks
+constexpr int kGemmMinSlice = 128;       // ... but keep every slice at least this long
+constexpr int kGemmMaxSplits = 128;
 constexpr float kLog2Pi = 1.8378770664093453f;   // log(2 pi)
 
-// C(i, j) [+]= sum_k A(i, k) B(k, j) with A(i, k) = A[i*ai + k*ak], B(k, j) = B[k*bk + j*bj],
-// C(i, j) = C[i*ldc + j]; i < m, j < n, k < kk. Two accumulator chains (even and odd k pairs)
-// keep the matrix ops of a wave independent; they are added at the end.
-// blockIdx.z takes the reduction slice [z kc, min(kk, (z + 1) kc)); with several slices each
-// writes its own partial tile to C + z * m * ldc (summed afterwards by k_sum_splits).
-template <bool ACC>
-__global__ __launch_bounds__(256) void k_gemm(const float *__restrict__ A, int64_t ai, int64_t ak,
-                                              const float *__restrict__ B, int64_t bk, int64_t bj,
-                                              float *__restrict__ C, int64_t ldc, int m, int n, int kk, int kc)
+// One operand tile of a slice: 128 rows (i of A, j of B) x 32 reduction indices, staged as
+// rows of the reduction index, S[row][k]. The operand is either "k-contiguous"
+// (X(row, k) = X[row * ld + k]) or "row-contiguous" (X(row, k) = X[k * ld + row]); each thread
+// moves four 4-float groups along the contiguous index.
+template <bool KCONT>
+struct Stage {
+    float4 v[4];
+
+    // Element (row, kx) of thread group q: KCONT walks k fastest (8 groups per row), else rows.
+    static __device__ __forceinline__ void coords(int tid, int q, int &row, int &kx)
+    {
+        const int f = tid + 256 * q;
+        if constexpr (KCONT) {
+            row = f >> 3;
+            kx = (f & 7) * 4;
+        } else {
+            kx = f >> 5;
+            row = (f & 31) * 4;
+        }
+    }
+
+    // full: the whole 128 x 32 tile lies inside the operand and every group is 16-byte aligned
+    // (a uniform branch: one unconditional 16-byte load per group).
+    __device__ __forceinline__ void load(const float *__restrict__ X, int64_t ld, bool full, int r0, int rmax,
+                                         int k0, int kend, int tid)
+    {
+        if (full) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                int row, kx;
+                coords(tid, q, row, kx);
+                const int64_t off = KCONT ? static_cast<int64_t>(r0 + row) * ld + (k0 + kx)
+                                          : static_cast<int64_t>(k0 + kx) * ld + (r0 + row);
+                v[q] = *reinterpret_cast<const float4 *>(X + off);
+            }
+            return;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            int row, kx;
+            coords(tid, q, row, kx);
+            float e[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int gr = r0 + row + (KCONT ? 0 : u), gk = k0 + kx + (KCONT ? u : 0);
+                e[u] = (gr < rmax && gk < kend) ? X[KCONT ? static_cast<int64_t>(gr) * ld + gk
+                                                          : static_cast<int64_t>(gk) * ld + gr]
+                                                : 0.0f;
+            }
+            v[q] = make_float4(e[0], e[1], e[2], e[3]);
+        }
+    }
+
+    __device__ __forceinline__ void store(float (*S)[kGemmPitch], int tid) const
+    {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int f = tid + 256 * q;
+            if constexpr (KCONT) {
+                *reinterpret_cast<float4 *>(&S[f >> 3][(f & 7) * 4]) = v[q];
+            } else {
+                const int kx = f >> 5, row = (f & 31) * 4;
+                S[row][kx] = v[q].x;
+                S[row + 1][kx] = v[q].y;
+                S[row + 2][kx] = v[q].z;
+                S[row + 3][kx] = v[q].w;
+            }
+        }
+    }
+};
+
+// C(i, j) [+]= sum_k A(i, k) B(k, j) for i < m, j < n over the block's reduction slice
+// [z kc, min(kk, (z + 1) kc)), z = blockIdx.z; C(i, j) = C[z m ldc + i ldc + j] (with several
+// slices each writes its own partial tile, summed afterwards in slice order by k_sum_splits).
+// A is k-contiguous when AK (A(i, k) = A[i lda + k]), else row-contiguous (A[k lda + i]); B is
+// k-contiguous when BK (B(k, j) = B[j ldb + k]), else row-contiguous (B[k ldb + j]).
+// With rowsum != NULL the blocks of the first column tile also write sum_k A(i, k) over the slice
+// to rowsum[z m + i] (the bias gradient of a weight-gradient product, read from the staged tiles).
+// Matrix op t of an 8-index group takes, in lane l, the reduction index 4 (l / 32) + t of the
+// group for both operands (a relabelling of the sum), so one 16-byte LDS read feeds four ops.
+// 32 x 32 sub-tiles that lie wholly outside C are skipped (wave-uniform).
+template <bool AK, bool BK, bool ACC>
+__global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, int64_t lda, bool va,
+                                                 const float *__restrict__ B, int64_t ldb, bool vb,
+                                                 float *__restrict__ C, int64_t ldc, float *__restrict__ rowsum,
+                                                 int m, int n, int kk, int kc)
 {
+    __shared__ __align__(16) float As[2][kGemmTile][kGemmPitch];
+    __shared__ __align__(16) float Bs[2][kGemmTile][kGemmPitch];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wy = wave >> 1, wx = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int i0 = blockIdx.y * kGemmTile, j0 = blockIdx.x * kGemmTile;
     const int kbeg = blockIdx.z * kc;
     const int kend = min(kk, kbeg + kc);
     C += static_cast<int64_t>(blockIdx.z) * m * ldc;
-    __shared__ float As[kGemmK][kGemmPitch];
-    __shared__ float Bs[kGemmK][kGemmPitch];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int wy = wave >> 1, wx = wave & 1;
-    const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kGemmTile;
-    const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kGemmTile;
-    v16f acc0, acc1;
+    bool live_a[2], live_b[2];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        acc0[r] = 0.0f;
-        acc1[r] = 0.0f;
+    for (int a = 0; a < 2; ++a) {
+        live_a[a] = i0 + wy * 64 + a * 32 < m;
+        live_b[a] = j0 + wx * 64 + a * 32 < n;
     }
-    for (int k0 = kbeg; k0 < kend; k0 += kGemmK) {
-        // stage both tiles, walking the operand's unit-stride index fastest (coalesced reads)
-        for (int e = tid; e < kGemmTile * kGemmK; e += 256) {
-            int ii, kx;
-            if (ak == 1) {
-                kx = e % kGemmK;
-                ii = e / kGemmK;
-            } else {
-                ii = e % kGemmTile;
-                kx = e / kGemmTile;
+    const bool sums = rowsum != nullptr && blockIdx.x == 0 && wx == 0;
+    v16f acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[a][b][r] = 0.0f;
+    float rs[2] = {0.0f, 0.0f};
+    Stage<AK> sa;
+    Stage<BK> sb;
+    const int ns = kend > kbeg ? (kend - kbeg + kGemmK - 1) / kGemmK : 0;
+    const bool rows_a = va && i0 + kGemmTile <= m, rows_b = vb && j0 + kGemmTile <= n;
+    if (ns > 0) {
+        const bool kin = kbeg + kGemmK <= kend;
+        sa.load(A, lda, rows_a && kin, i0, m, kbeg, kend, tid);
+        sb.load(B, ldb, rows_b && kin, j0, n, kbeg, kend, tid);
+        sa.store(As[0], tid);
+        sb.store(Bs[0], tid);
+    }
+    __syncthreads();
+    for (int s = 0; s < ns; ++s) {
+        const int buf = s & 1;
+        if (s + 1 < ns) {
+            const int k1 = kbeg + (s + 1) * kGemmK;
+            const bool kin = k1 + kGemmK <= kend;
+            sa.load(A, lda, rows_a && kin, i0, m, k1, kend, tid);
+            sb.load(B, ldb, rows_b && kin, j0, n, k1, kend, tid);
+        }
+#pragma unroll
+        for (int g = 0; g < kGemmK / 8; ++g) {
+            float4 av[2], bv[2];
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+                av[a] = *reinterpret_cast<const float4 *>(&As[buf][wy * 64 + a * 32 + l32][g * 8 + 4 * half]);
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                bv[b] = *reinterpret_cast<const float4 *>(&Bs[buf][wx * 64 + b * 32 + l32][g * 8 + 4 * half]);
+            if (sums) {
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    rs[a] += (av[a].x + av[a].y) + (av[a].z + av[a].w);
             }
-            const int64_t gi = i0 + ii, gk = k0 + kx;
-            As[kx][ii] = (gi < m && gk < kend) ? A[gi * ai + gk * ak] : 0.0f;
-            int jj, ky;
-            if (bj == 1) {
-                jj = e % kGemmTile;
-                ky = e / kGemmTile;
-            } else {
-                ky = e % kGemmK;
-                jj = e / kGemmK;
-            }
-            const int64_t gj = j0 + jj, gk2 = k0 + ky;
-            Bs[ky][jj] = (gj < n && gk2 < kend) ? B[gk2 * bk + gj * bj] : 0.0f;
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    if (!(live_a[a] && live_b[b]))
+                        continue;
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].x, bv[b].x, acc[a][b], 0, 0, 0);
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].y, bv[b].y, acc[a][b], 0, 0, 0);
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].z, bv[b].z, acc[a][b], 0, 0, 0);
+                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].w, bv[b].w, acc[a][b], 0, 0, 0);
+                }
+        }
+        if (s + 1 < ns) {
+            sa.store(As[buf ^ 1], tid);
+            sb.store(Bs[buf ^ 1], tid);
         }
         __syncthreads();
-#pragma unroll
-        for (int kp = 0; kp < kGemmK; kp += 4) {
-            const float a0 = As[kp + (lane >> 5)][wy * 32 + (lane & 31)];
-            const float b0 = Bs[kp + (lane >> 5)][wx * 32 + (lane & 31)];
-            const float a1 = As[kp + 2 + (lane >> 5)][wy * 32 + (lane & 31)];
-            const float b1 = Bs[kp + 2 + (lane >> 5)][wx * 32 + (lane & 31)];
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc1, 0, 0, 0);
-        }
-        __syncthreads();
     }
-    const int half = lane >> 5;
+    if (sums) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int64_t gi = i0 + wy * 32 + crow(r, half);
-        const int64_t gj = j0 + wx * 32 + (lane & 31);
-        if (gi < m && gj < n) {
-            const float v = acc0[r] + acc1[r];
-            C[gi * ldc + gj] = ACC ? C[gi * ldc + gj] + v : v;
+        for (int a = 0; a < 2; ++a) {
+            const float other = __shfl_xor(rs[a], 32);
+            const int gi = i0 + wy * 64 + a * 32 + l32;
+            if (half == 0 && gi < m)
+                rowsum[static_cast<int64_t>(blockIdx.z) * m + gi] = rs[a] + other;
         }
     }
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            if (!(live_a[a] && live_b[b]))
+                continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int gi = i0 + wy * 64 + a * 32 + crow(r, half);
+                const int gj = j0 + wx * 64 + b * 32 + l32;
+                if (gi < m && gj < n) {
+                    float *dst = C + static_cast<int64_t>(gi) * ldc + gj;
+                    *dst = ACC ? *dst + acc[a][b][r] : acc[a][b][r];
+                }
+            }
+        }
 }
 
 // C(i, j) [+]= sum over the slices s = 0, 1, ... (in order) of P[s][i][j].
@@ -108,7 +225,17 @@ __global__ __launch_bounds__(256) void k_sum_splits(const float *__restrict__ P,
     const int64_t total = static_cast<int64_t>(m) * n;
     for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
         float v = 0.0f;
-        for (int sp = 0; sp < splits; ++sp)
+        int sp = 0;
+        for (; sp + 8 <= splits; sp += 8) {
+            float t[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                t[u] = P[(sp + u) * total + e];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                v += t[u];
+        }
+        for (; sp < splits; ++sp)
             v += P[sp * total + e];
         const int64_t i = e / n, j = e % n;
         C[i * ldc + j] = ACC ? C[i * ldc + j] + v : v;
@@ -147,24 +274,24 @@ __global__ __launch_bounds__(256) void k_dact(float *__restrict__ g, const float
         g[e] *= dact<ACT>(pre[e]);
 }
 
-// One thread per window: mu, lv (biases added in place), sd = e^(lv/2), z = mu + sd eps and the
-// KL of q(z|m) from N(0, I).
-__global__ __launch_bounds__(256) void k_latent(float *__restrict__ mu, float *__restrict__ lv,
-                                                const float *__restrict__ bmu, const float *__restrict__ blv,
-                                                const float *__restrict__ eps, float *__restrict__ sd,
-                                                float *__restrict__ z, float *__restrict__ kl, int rows, int L)
+// One thread per window. ml holds [mu | lv] per window (2L floats, biases [bmu | blv] added in
+// place); sd = e^(lv/2), z = mu + sd eps and the KL of q(z|m) from N(0, I).
+__global__ __launch_bounds__(64) void k_latent(float *__restrict__ ml, const float *__restrict__ bml,
+                                               const float *__restrict__ eps, float *__restrict__ sd,
+                                               float *__restrict__ z, float *__restrict__ kl, int rows, int L)
 {
-    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int i = blockIdx.x * 64 + threadIdx.x;
     if (i >= rows)
         return;
+    float *mu = ml + static_cast<int64_t>(i) * 2 * L, *lv = mu + L;
     float k = 0.0f;
     for (int l = 0; l < L; ++l) {
         const int64_t e = static_cast<int64_t>(i) * L + l;
-        const float m = mu[e] + bmu[l];
-        const float v = lv[e] + blv[l];
+        const float m = mu[l] + bml[l];
+        const float v = lv[l] + bml[L + l];
         const float s = expf(0.5f * v);
-        mu[e] = m;
-        lv[e] = v;
+        mu[l] = m;
+        lv[l] = v;
         sd[e] = s;
         z[e] = m + s * eps[e];
         k += m * m + kl_g(v);
@@ -174,7 +301,9 @@ __global__ __launch_bounds__(256) void k_latent(float *__restrict__ mu, float *_
 
 // One block per window: m' = out + bd2, e = |v - m'|^2 / 2, log p = -e - D/2 log 2 pi, and in place
 // of out the gradient of J, (l/B)(m' - v); an anomalous window (l < 0) whose e has reached the
-// margin contributes a constant and gets a zero gradient.
+// margin contributes a constant and gets a zero gradient. PER > 0: the window's D <= 256 PER
+// differences stay in registers between the reduction and the write; PER = 0 recomputes them.
+template <int PER>
 __global__ __launch_bounds__(256) void k_recon(float *__restrict__ out, const float *__restrict__ bd2,
                                                const float *__restrict__ V, const float *__restrict__ labels,
                                                float *__restrict__ logp, int D, float inv_b, float margin)
@@ -182,11 +311,22 @@ __global__ __launch_bounds__(256) void k_recon(float *__restrict__ out, const fl
     __shared__ float red[256];
     const int64_t row = blockIdx.x;
     const float l = labels[row];
+    float *o = out + row * D;
+    const float *v = V + row * D;
+    float d[PER > 0 ? PER : 1];
     float sq = 0.0f;
-    for (int j = threadIdx.x; j < D; j += 256) {
-        const int64_t e = row * D + j;
-        const float d = out[e] + bd2[j] - V[e];
-        sq += d * d;
+    if constexpr (PER > 0) {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int j = threadIdx.x + 256 * u;
+            d[u] = j < D ? o[j] + bd2[j] - v[j] : 0.0f;
+            sq += d[u] * d[u];
+        }
+    } else {
+        for (int j = threadIdx.x; j < D; j += 256) {
+            const float t = o[j] + bd2[j] - v[j];
+            sq += t * t;
+        }
     }
     red[threadIdx.x] = sq;
     __syncthreads();
@@ -197,9 +337,16 @@ __global__ __launch_bounds__(256) void k_recon(float *__restrict__ out, const fl
     }
     const float err = 0.5f * red[0];
     const float scale = (l > 0.0f || err < margin) ? l * inv_b : 0.0f;
-    for (int j = threadIdx.x; j < D; j += 256) {
-        const int64_t e = row * D + j;
-        out[e] = scale * (out[e] + bd2[j] - V[e]);
+    if constexpr (PER > 0) {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int j = threadIdx.x + 256 * u;
+            if (j < D)
+                o[j] = scale * d[u];
+        }
+    } else {
+        for (int j = threadIdx.x; j < D; j += 256)
+            o[j] = scale * (o[j] + bd2[j] - v[j]);
     }
     if (threadIdx.x == 0)
         logp[row] = -err - 0.5f * static_cast<float>(D) * kLog2Pi;
@@ -208,16 +355,16 @@ __global__ __launch_bounds__(256) void k_recon(float *__restrict__ out, const fl
 // One block: the KL weight of this step from the PI controller, and the step's summary
 // (J, mean log p, mean KL of the normal windows, beta). State: st[0] = the integral term.
 // An anomalous window enters J through -log p capped at margin + D/2 log 2 pi.
-__global__ __launch_bounds__(256) void k_beta(const float *__restrict__ kl, const float *__restrict__ logp,
+__global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, const float *__restrict__ logp,
                                               const float *__restrict__ labels, int rows, float kl_set,
                                               float kp, float ki, float beta_min, float beta_max,
                                               float margin, float half_d_log2pi,
                                               float *__restrict__ st, float *__restrict__ beta_out,
                                               float *__restrict__ info)
 {
-    __shared__ double r_kl[256], r_n[256], r_lp[256], r_la[256], r_kn[256];
+    __shared__ double r_kl[1024], r_n[1024], r_lp[1024], r_la[1024], r_kn[1024];
     double skl = 0.0, sn = 0.0, slp = 0.0, sla = 0.0, skn = 0.0;
-    for (int i = threadIdx.x; i < rows; i += 256) {
+    for (int i = threadIdx.x; i < rows; i += 1024) {
         const double l = labels[i];
         const double k = kl[i];
         const double lp = logp[i];
@@ -241,7 +388,7 @@ __global__ __launch_bounds__(256) void k_beta(const float *__restrict__ kl, cons
     r_la[threadIdx.x] = sla;
     r_kn[threadIdx.x] = skn;
     __syncthreads();
-    for (int w = 128; w >= 1; w >>= 1) {
+    for (int w = 512; w >= 1; w >>= 1) {
         if (threadIdx.x < w) {
             r_kl[threadIdx.x] += r_kl[threadIdx.x + w];
             r_n[threadIdx.x] += r_n[threadIdx.x + w];
@@ -270,43 +417,24 @@ __global__ __launch_bounds__(256) void k_beta(const float *__restrict__ kl, cons
 }
 
 // Gradients of J at the latent: g_mu = g_z + c mu, g_lv = g_z eps sd/2 + c (e^lv - 1)/2 with
-// c = (1 + l)/2 beta / B; g_z holds dJ/dz on entry and g_mu on exit.
-__global__ __launch_bounds__(256) void k_latent_grad(float *__restrict__ gz, float *__restrict__ glv,
-                                                     const float *__restrict__ mu, const float *__restrict__ lv,
-                                                     const float *__restrict__ sd, const float *__restrict__ eps,
-                                                     const float *__restrict__ labels,
+// c = (1 + l)/2 beta / B, written as [g_mu | g_lv] per window (the layout of ml).
+__global__ __launch_bounds__(256) void k_latent_grad(const float *__restrict__ gz, float *__restrict__ gml,
+                                                     const float *__restrict__ ml, const float *__restrict__ sd,
+                                                     const float *__restrict__ eps, const float *__restrict__ labels,
                                                      const float *__restrict__ beta, int rows, int L, float inv_b)
 {
     const int64_t total = static_cast<int64_t>(rows) * L;
     const float b = beta[0];
     for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
         const int64_t i = e / L;
+        const int l = static_cast<int>(e - i * L);
         const float c = 0.5f * (1.0f + labels[i]) * b * inv_b;
         const float g = gz[e];
-        gz[e] = g + c * mu[e];
-        glv[e] = g * eps[e] * 0.5f * sd[e] + c * 0.5f * expm1f(lv[e]);
+        const float *row = ml + i * 2 * L;
+        float *out = gml + i * 2 * L;
+        out[l] = g + c * row[l];
+        out[L + l] = g * eps[e] * 0.5f * sd[e] + c * 0.5f * expm1f(row[L + l]);
     }
-}
-
-// Column sums in two fixed-order passes: block (x, r) sums rows [r rc, (r + 1) rc) of 64 columns
-// (4 row lanes of 64 threads, combined in lane order) into P[r][j]; k_sum_splits then adds the
-// row chunks in order.
-__global__ __launch_bounds__(256) void k_colsum_part(const float *__restrict__ X, int64_t rows, int cols,
-                                                     int64_t rc, float *__restrict__ P)
-{
-    __shared__ float part[4][64];
-    const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
-    const int j = blockIdx.x * 64 + c;
-    const int64_t r0 = static_cast<int64_t>(blockIdx.y) * rc;
-    const int64_t r1 = r0 + rc < rows ? r0 + rc : rows;
-    float s = 0.0f;
-    if (j < cols)
-        for (int64_t i = r0 + q; i < r1; i += 4)
-            s += X[i * cols + j];
-    part[q][c] = s;
-    __syncthreads();
-    if (q == 0 && j < cols)
-        P[static_cast<int64_t>(blockIdx.y) * cols + j] = ((part[0][c] + part[1][c]) + part[2][c]) + part[3][c];
 }
 
 __global__ __launch_bounds__(256) void k_adam(float *__restrict__ p, const float *__restrict__ g,
@@ -344,31 +472,61 @@ static int gemm_splits(int m, int n, int k)
 int64_t gemm_workspace_floats(int m, int n, int k)
 {
     const int s = gemm_splits(m, n, k);
-    return s > 1 ? static_cast<int64_t>(s) * m * n : 0;
+    return s > 1 ? static_cast<int64_t>(s) * (static_cast<int64_t>(m) * n + m) : 0;
+}
+
+template <bool AK, bool BK>
+void gemm_dispatch(dim3 grid, hipStream_t st, bool acc, const float *A, int64_t lda, bool va, const float *B,
+                   int64_t ldb, bool vb, float *C, int64_t ldc, float *rowsum, int m, int n, int k, int kc)
+{
+    if (acc)
+        hipLaunchKernelGGL((k_gemm<AK, BK, true>), grid, dim3(256), 0, st, A, lda, va, B, ldb, vb, C, ldc, rowsum,
+                           m, n, k, kc);
+    else
+        hipLaunchKernelGGL((k_gemm<AK, BK, false>), grid, dim3(256), 0, st, A, lda, va, B, ldb, vb, C, ldc,
+                           rowsum, m, n, k, kc);
 }
 
 hipError_t launch_gemm(const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk, int64_t bj,
-                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *work, hipStream_t st)
+                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *rowsum, float *work,
+                       hipStream_t st)
 {
     if (m <= 0 || n <= 0)
         return hipSuccess;
+    // each operand needs a unit stride along the reduction index or along its row index
+    if ((ak != 1 && ai != 1) || (bk != 1 && bj != 1))
+        return hipErrorInvalidValue;
+    const bool a_k = ak == 1, b_k = bk == 1;
+    const int64_t lda = a_k ? ai : ak, ldb = b_k ? bj : bk;
+    const bool va = lda % 4 == 0 && reinterpret_cast<uintptr_t>(A) % 16 == 0;
+    const bool vb = ldb % 4 == 0 && reinterpret_cast<uintptr_t>(B) % 16 == 0;
     const int splits = work ? gemm_splits(m, n, k) : 1;
     const int kc = splits > 1 ? ((k + splits - 1) / splits + kGemmK - 1) / kGemmK * kGemmK : std::max(k, 1);
     const int used = splits > 1 ? (k + kc - 1) / kc : 1;
     const dim3 grid(static_cast<unsigned>((n + kGemmTile - 1) / kGemmTile),
                     static_cast<unsigned>((m + kGemmTile - 1) / kGemmTile), static_cast<unsigned>(used));
-    if (used > 1) {
-        hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, st, A, ai, ak, B, bk, bj, work,
-                           static_cast<int64_t>(n), m, n, k, kc);
+    const bool split = used > 1;
+    float *dst = split ? work : C;
+    float *rdst = rowsum && split ? work + static_cast<int64_t>(used) * m * n : rowsum;
+    const int64_t ldd = split ? static_cast<int64_t>(n) : ldc;
+    const bool acc = split ? false : accumulate;
+    if (a_k && b_k)
+        gemm_dispatch<true, true>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
+    else if (a_k)
+        gemm_dispatch<true, false>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
+    else if (b_k)
+        gemm_dispatch<false, true>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
+    else
+        gemm_dispatch<false, false>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
+    if (split) {
         const unsigned b = blocks_for(static_cast<int64_t>(m) * n);
         if (accumulate)
             hipLaunchKernelGGL(k_sum_splits<true>, dim3(b), dim3(256), 0, st, work, used, m, n, C, ldc);
         else
             hipLaunchKernelGGL(k_sum_splits<false>, dim3(b), dim3(256), 0, st, work, used, m, n, C, ldc);
-    } else if (accumulate) {
-        hipLaunchKernelGGL(k_gemm<true>, grid, dim3(256), 0, st, A, ai, ak, B, bk, bj, C, ldc, m, n, k, kc);
-    } else {
-        hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, st, A, ai, ak, B, bk, bj, C, ldc, m, n, k, kc);
+        if (rowsum)
+            hipLaunchKernelGGL(k_sum_splits<false>, dim3(blocks_for(m)), dim3(256), 0, st, rdst, used, 1, m,
+                               rowsum, static_cast<int64_t>(m));
     }
     return hipGetLastError();
 }
@@ -394,57 +552,46 @@ hipError_t launch_dact(float *g, const float *pre, int64_t total, int act, hipSt
     return hipGetLastError();
 }
 
-hipError_t launch_latent(float *mu, float *lv, const float *bmu, const float *blv, const float *eps, float *sd,
-                         float *z, float *kl, int rows, int L, hipStream_t st)
+hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
+                         int L, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_latent, dim3(static_cast<unsigned>((rows + 255) / 256)), dim3(256), 0, st, mu, lv, bmu,
-                       blv, eps, sd, z, kl, rows, L);
+    hipLaunchKernelGGL(k_latent, dim3(static_cast<unsigned>((rows + 63) / 64)), dim3(64), 0, st, ml, bml, eps, sd, z,
+                       kl, rows, L);
     return hipGetLastError();
 }
 
 hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
                         int rows, int D, float margin, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_recon, dim3(static_cast<unsigned>(rows)), dim3(256), 0, st, out, bd2, V, labels, logp,
-                       D, 1.0f / static_cast<float>(rows), margin);
+    const dim3 grid(static_cast<unsigned>(rows));
+    const float inv_b = 1.0f / static_cast<float>(rows);
+    if (D <= 256)
+        hipLaunchKernelGGL(k_recon<1>, grid, dim3(256), 0, st, out, bd2, V, labels, logp, D, inv_b, margin);
+    else if (D <= 512)
+        hipLaunchKernelGGL(k_recon<2>, grid, dim3(256), 0, st, out, bd2, V, labels, logp, D, inv_b, margin);
+    else if (D <= 1024)
+        hipLaunchKernelGGL(k_recon<4>, grid, dim3(256), 0, st, out, bd2, V, labels, logp, D, inv_b, margin);
+    else if (D <= 2048)
+        hipLaunchKernelGGL(k_recon<8>, grid, dim3(256), 0, st, out, bd2, V, labels, logp, D, inv_b, margin);
+    else
+        hipLaunchKernelGGL(k_recon<0>, grid, dim3(256), 0, st, out, bd2, V, labels, logp, D, inv_b, margin);
     return hipGetLastError();
 }
 
 hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
                        const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_beta, dim3(1), dim3(256), 0, st, kl, logp, labels, rows, h.kl_set, h.kp, h.ki,
+    hipLaunchKernelGGL(k_beta, dim3(1), dim3(1024), 0, st, kl, logp, labels, rows, h.kl_set, h.kp, h.ki,
                        h.beta_min, h.beta_max, h.margin, 0.5f * static_cast<float>(D) * kLog2Pi, state, beta,
                        info);
     return hipGetLastError();
 }
 
-hipError_t launch_latent_grad(float *gz, float *glv, const float *mu, const float *lv, const float *sd,
-                              const float *eps, const float *labels, const float *beta, int rows, int L,
-                              hipStream_t st)
+hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, const float *sd, const float *eps,
+                              const float *labels, const float *beta, int rows, int L, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_latent_grad, dim3(blocks_for(static_cast<int64_t>(rows) * L)), dim3(256), 0, st, gz,
-                       glv, mu, lv, sd, eps, labels, beta, rows, L, 1.0f / static_cast<float>(rows));
-    return hipGetLastError();
-}
-
-int64_t colsum_workspace_floats(int64_t rows, int cols)
-{
-    const int64_t chunks = std::min<int64_t>(kColsumMaxChunks, (rows + kColsumRows - 1) / kColsumRows);
-    return std::max<int64_t>(chunks, 1) * cols;
-}
-
-hipError_t launch_colsum(const float *X, int64_t rows, int cols, float *out, float *work, hipStream_t st)
-{
-    if (cols <= 0)
-        return hipSuccess;
-    const int64_t chunks = std::max<int64_t>(1, std::min<int64_t>(kColsumMaxChunks, (rows + kColsumRows - 1) / kColsumRows));
-    const int64_t rc = std::max<int64_t>(1, (rows + chunks - 1) / chunks);
-    const int64_t used = rows > 0 ? (rows + rc - 1) / rc : 1;
-    hipLaunchKernelGGL(k_colsum_part, dim3(static_cast<unsigned>((cols + 63) / 64), static_cast<unsigned>(used)),
-                       dim3(256), 0, st, X, rows, cols, rc, work);
-    hipLaunchKernelGGL(k_sum_splits<false>, dim3(blocks_for(cols)), dim3(256), 0, st, work,
-                       static_cast<int>(used), 1, cols, out, static_cast<int64_t>(cols));
+    hipLaunchKernelGGL(k_latent_grad, dim3(blocks_for(static_cast<int64_t>(rows) * L)), dim3(256), 0, st, gz, gml,
+                       ml, sd, eps, labels, beta, rows, L, 1.0f / static_cast<float>(rows));
     return hipGetLastError();
 }
 

@@ -13,8 +13,11 @@ using namespace enova;
 
 namespace {
 
-// The parameters in the order of enova_detect_weights, as one flat buffer.
+// The parameters in the order of enova_detect_weights. In the flat buffers they are stored as
+// w1, b1, wmu, wlv, bmu, blv, wd1, bd1, wd2, bd2, so that [wmu; wlv] ([2L][H]) and [bmu | blv]
+// form the weights and biases of one fused head product.
 enum { P_W1, P_B1, P_WMU, P_BMU, P_WLV, P_BLV, P_WD1, P_BD1, P_WD2, P_BD2, P_COUNT };
+constexpr int kStoreOrder[P_COUNT] = {P_W1, P_B1, P_WMU, P_WLV, P_BMU, P_BLV, P_WD1, P_BD1, P_WD2, P_BD2};
 
 }  // namespace
 
@@ -23,14 +26,14 @@ struct enova_trainer_s {
     int D = 0, H = 0, L = 0, act = 0;
     TrainHyper hyper{};
     int64_t step = 0;
-    int64_t off[P_COUNT + 1] = {};   // offsets into the flat buffers (floats)
+    int64_t off[P_COUNT] = {}, size[P_COUNT] = {}, total = 0;   // flat-buffer layout (floats)
     float *p = nullptr, *g = nullptr, *m = nullptr, *v = nullptr;
     float *state = nullptr;          // [0] PI integral, [1] beta of the step
     // batch workspace
     int cap = 0;
     float *a1 = nullptr, *h = nullptr, *a2 = nullptr, *hd = nullptr, *gh = nullptr;   // [B][H]
-    float *mu = nullptr, *lv = nullptr, *sd = nullptr, *z = nullptr;                 // [B][L]
-    float *gmu = nullptr, *glv = nullptr;                                            // [B][L]
+    float *ml = nullptr, *gml = nullptr;                                           // [B][2L]: [mu | lv]
+    float *sd = nullptr, *z = nullptr, *gz = nullptr;                              // [B][L]
     float *out = nullptr;                                                          // [B][D]
     float *kl = nullptr, *logp = nullptr;                                          // [B]
     float *work = nullptr;                                                         // split-reduction partials
@@ -48,8 +51,8 @@ void free_trainer(enova_trainer t)
 {
     if (!t)
         return;
-    void *ptrs[] = {t->p,  t->g,  t->m,  t->v,  t->state, t->a1,  t->h,   t->a2,  t->hd,  t->gh,
-                    t->mu, t->lv, t->sd, t->z,  t->gmu,   t->glv, t->out, t->kl,  t->logp, t->work};
+    void *ptrs[] = {t->p,  t->g,  t->m,  t->v,  t->state, t->a1,  t->h,  t->a2,   t->hd,
+                    t->gh, t->ml, t->gml, t->sd, t->z,  t->gz,    t->out, t->kl, t->logp, t->work};
     for (void *q : ptrs)
         if (q)
             (void)hipFree(q);
@@ -73,12 +76,12 @@ int64_t workspace_floats(const enova_trainer t, int B)
 {
     // every product of a step, as (m, n, k)
     const int D = t->D, H = t->H, L = t->L;
-    const int shapes[][3] = {{B, H, D}, {B, L, H}, {B, H, L}, {B, D, H}, {D, H, B}, {B, H, D},
-                             {H, L, B}, {B, L, H}, {L, H, B}, {B, H, L}, {H, D, B}};
+    const int shapes[][3] = {{B, H, D},     {B, 2 * L, H}, {B, H, L}, {B, D, H}, {D, H, B}, {B, H, D},
+                             {H, L, B},     {B, L, H},     {2 * L, H, B}, {B, H, 2 * L}, {H, D, B}};
     int64_t ws = 0;
     for (const auto &sh : shapes)
         ws = std::max(ws, gemm_workspace_floats(sh[0], sh[1], sh[2]));
-    return std::max(ws, colsum_workspace_floats(B, std::max({D, H, L})));
+    return ws;
 }
 
 // Grows the batch buffers to B rows (freeing the old ones synchronises the device).
@@ -97,11 +100,14 @@ enova_status ensure_batch(enova_trainer t, int B)
     if (B <= t->cap)
         return ENOVA_OK;
     float **bh[] = {&t->a1, &t->h, &t->a2, &t->hd, &t->gh};
-    float **bl[] = {&t->mu, &t->lv, &t->sd, &t->z, &t->gmu, &t->glv};
+    float **bl[] = {&t->sd, &t->z, &t->gz};
+    float **b2[] = {&t->ml, &t->gml};
     float **b1[] = {&t->kl, &t->logp};
     for (float **q : bh)
         (void)hipFree(*q), *q = nullptr;
     for (float **q : bl)
+        (void)hipFree(*q), *q = nullptr;
+    for (float **q : b2)
         (void)hipFree(*q), *q = nullptr;
     for (float **q : b1)
         (void)hipFree(*q), *q = nullptr;
@@ -113,6 +119,9 @@ enova_status ensure_batch(enova_trainer t, int B)
             return st;
     for (float **q : bl)
         if ((st = alloc_floats(q, static_cast<size_t>(B) * t->L)) != ENOVA_OK)
+            return st;
+    for (float **q : b2)
+        if ((st = alloc_floats(q, static_cast<size_t>(B) * 2 * t->L)) != ENOVA_OK)
             return st;
     for (float **q : b1)
         if ((st = alloc_floats(q, static_cast<size_t>(B))) != ENOVA_OK)
@@ -130,8 +139,8 @@ enova_status copy_out(enova_trainer t, const float *src, const enova_train_param
     hipError_t e = hipSuccess;
     for (int k = 0; k < P_COUNT && e == hipSuccess; ++k)
         if (dst[k])
-            e = hipMemcpyAsync(dst[k], src + t->off[k], (t->off[k + 1] - t->off[k]) * sizeof(float),
-                               hipMemcpyDeviceToHost, stream);
+            e = hipMemcpyAsync(dst[k], src + t->off[k], t->size[k] * sizeof(float), hipMemcpyDeviceToHost,
+                               stream);
     if (e == hipSuccess)
         e = hipStreamSynchronize(stream);
     return e == hipSuccess ? ENOVA_OK : hip_fail(e, "trainer copy");
@@ -170,9 +179,12 @@ enova_status enova_train_init(const enova_train_config *c, const enova_detect_we
                           c->kp,     c->ki,       c->beta_min, c->beta_max, c->anomaly_margin};
     const int64_t D = t->D, H = t->H, L = t->L;
     const int64_t sizes[P_COUNT] = {H * D, H, L * H, L, L * H, L, H * L, H, D * H, D};
-    for (int k = 0; k < P_COUNT; ++k)
-        t->off[k + 1] = t->off[k] + sizes[k];
-    const size_t total = static_cast<size_t>(t->off[P_COUNT]);
+    for (int q : kStoreOrder) {
+        t->off[q] = t->total;
+        t->size[q] = sizes[q];
+        t->total += sizes[q];
+    }
+    const size_t total = static_cast<size_t>(t->total);
     enova_status st;
     if ((st = alloc_floats(&t->p, total)) != ENOVA_OK || (st = alloc_floats(&t->g, total)) != ENOVA_OK ||
         (st = alloc_floats(&t->m, total)) != ENOVA_OK || (st = alloc_floats(&t->v, total)) != ENOVA_OK ||
@@ -225,49 +237,41 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
     };
     // every product of the step, bracketed by events when timing is on
     auto gemm = [&](const float *A, int64_t ai, int64_t ak, const float *Bm, int64_t bk, int64_t bj, float *C,
-                    int64_t ldc, int m, int n, int k, bool acc, float *work, hipStream_t st) {
+                    int64_t ldc, int m, int n, int k, bool acc, float *rowsum, float *work, hipStream_t st) {
         mark();
-        run(launch_gemm(A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, acc, work, st));
+        run(launch_gemm(A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, acc, rowsum, work, st));
         mark();
     };
     mark();
+    float *W = t->work;
     // forward: a1 = V W1^T (+ b1), h = act(a1)
-    gemm(V, D, 1, P + o[P_W1], 1, D, t->a1, H, B, H, D, false, t->work, s);
+    gemm(V, D, 1, P + o[P_W1], 1, D, t->a1, H, B, H, D, false, nullptr, W, s);
     run(launch_bias_act(t->a1, P + o[P_B1], t->h, B, H, act, s));
-    // heads, reparameterised latent and KL
-    gemm(t->h, H, 1, P + o[P_WMU], 1, H, t->mu, L, B, L, H, false, t->work, s);
-    gemm(t->h, H, 1, P + o[P_WLV], 1, H, t->lv, L, B, L, H, false, t->work, s);
-    run(launch_latent(t->mu, t->lv, P + o[P_BMU], P + o[P_BLV], eps, t->sd, t->z, t->kl, B, L, s));
+    // fused heads [mu | lv] = h [Wmu; Wlv]^T, reparameterised latent and KL
+    gemm(t->h, H, 1, P + o[P_WMU], 1, H, t->ml, 2 * L, B, 2 * L, H, false, nullptr, W, s);
+    run(launch_latent(t->ml, P + o[P_BMU], eps, t->sd, t->z, t->kl, B, L, s));
     // decoder: a2 = z Wd1^T (+ bd1), hd = act(a2), m' = hd Wd2^T (+ bd2) -> log p and dJ/dm'
-    gemm(t->z, L, 1, P + o[P_WD1], 1, L, t->a2, H, B, H, L, false, t->work, s);
+    gemm(t->z, L, 1, P + o[P_WD1], 1, L, t->a2, H, B, H, L, false, nullptr, W, s);
     run(launch_bias_act(t->a2, P + o[P_BD1], t->hd, B, H, act, s));
-    gemm(t->hd, H, 1, P + o[P_WD2], 1, H, t->out, D, B, D, H, false, t->work, s);
+    gemm(t->hd, H, 1, P + o[P_WD2], 1, H, t->out, D, B, D, H, false, nullptr, W, s);
     run(launch_recon(t->out, P + o[P_BD2], V, labels, t->logp, B, D, t->hyper.margin, s));
     // beta(k) from this batch's KL, before the backward pass
     run(launch_beta(t->kl, t->logp, labels, B, D, t->hyper, t->state, t->state + 1, info, s));
-    // backward through the decoder
-    gemm(t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, false, t->work, s);      // dWd2 = G^T hd
-    run(launch_colsum(t->out, B, D, G + o[P_BD2], t->work, s));
-    gemm(t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, false, t->work, s);      // dJ/dhd = G Wd2
+    // backward through the decoder (G = dJ/dm' in out); bias gradients are the row sums of G^T
+    gemm(t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, false, G + o[P_BD2], W, s);   // dWd2 = G^T hd
+    gemm(t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, false, nullptr, W, s);        // dJ/dhd = G Wd2
     run(launch_dact(t->gh, t->a2, static_cast<int64_t>(B) * H, act, s));
-    gemm(t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, false, t->work, s);        // dWd1 = G^T z
-    run(launch_colsum(t->gh, B, H, G + o[P_BD1], t->work, s));
-    gemm(t->gh, H, 1, P + o[P_WD1], L, 1, t->gmu, L, B, L, H, false, t->work, s);      // dJ/dz = G Wd1
-    // latent: dJ/dz becomes dJ/dmu in place; dJ/dlv
-    run(launch_latent_grad(t->gmu, t->glv, t->mu, t->lv, t->sd, eps, labels, t->state + 1, B, L, s));
-    gemm(t->gmu, 1, L, t->h, H, 1, G + o[P_WMU], H, L, H, B, false, t->work, s);      // dWmu = G^T h
-    run(launch_colsum(t->gmu, B, L, G + o[P_BMU], t->work, s));
-    gemm(t->glv, 1, L, t->h, H, 1, G + o[P_WLV], H, L, H, B, false, t->work, s);      // dWlv = G^T h
-    run(launch_colsum(t->glv, B, L, G + o[P_BLV], t->work, s));
-    // backward through the encoder: dJ/dh = G_mu Wmu + G_lv Wlv, times act'(a1)
-    gemm(t->gmu, L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, L, false, t->work, s);
-    gemm(t->glv, L, 1, P + o[P_WLV], H, 1, t->gh, H, B, H, L, true, t->work, s);
+    gemm(t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, false, G + o[P_BD1], W, s);      // dWd1 = G^T z
+    gemm(t->gh, H, 1, P + o[P_WD1], L, 1, t->gz, L, B, L, H, false, nullptr, W, s);          // dJ/dz = G Wd1
+    // latent: [dJ/dmu | dJ/dlv], then the fused heads' gradients and dJ/dh = G_ml [Wmu; Wlv]
+    run(launch_latent_grad(t->gz, t->gml, t->ml, t->sd, eps, labels, t->state + 1, B, L, s));
+    gemm(t->gml, 1, 2 * L, t->h, H, 1, G + o[P_WMU], H, 2 * L, H, B, false, G + o[P_BMU], W, s);
+    gemm(t->gml, 2 * L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, 2 * L, false, nullptr, W, s);
     run(launch_dact(t->gh, t->a1, static_cast<int64_t>(B) * H, act, s));
-    gemm(t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, false, t->work, s);            // dW1 = G^T V
-    run(launch_colsum(t->gh, B, H, G + o[P_B1], t->work, s));
+    gemm(t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, false, G + o[P_B1], W, s);            // dW1 = G^T V
     // Adam
     t->step += 1;
-    run(launch_adam(P, G, t->m, t->v, o[P_COUNT], t->hyper, t->step, s));
+    run(launch_adam(P, G, t->m, t->v, t->total, t->hyper, t->step, s));
     mark();
     t->n_events = ne;
     if (e != hipSuccess)
