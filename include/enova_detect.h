@@ -285,10 +285,11 @@ enova_status enova_train_params_get(enova_trainer t, const enova_train_params *o
 enova_status enova_train_grads_get(enova_trainer t, const enova_train_params *out, hipStream_t stream);
 
 /*
- * Timing: when enabled, every following step brackets each of its matrix products (and the
- * whole step) with HIP events on its stream; enova_train_kernel_times waits for the last step's
- * events and reports the summed milliseconds of its products and of the whole step (0 when the
- * last step was not timed).
+ * Timing: when enabled, every following step brackets the kernel of each of its matrix products
+ * (not the pass that adds the partial results of a split product) and the whole step with HIP
+ * events on its stream; enova_train_kernel_times waits for the last step's events and reports
+ * the summed milliseconds of those kernels and of the whole step (0 when the last step was not
+ * timed).
  */
 enova_status enova_train_set_timing(enova_trainer t, int32_t enable);
 enova_status enova_train_kernel_times(enova_trainer t, double *gemm_ms, double *step_ms);

@@ -226,14 +226,22 @@ struct TrainHyper {
 };
 // A long reduction over few output tiles is split into slices whose partial tiles go to `work`
 // (gemm_workspace_floats(m, n, k) floats; NULL: no split) and are then summed in slice order.
-// rowsum (or NULL) receives sum_k A(i, k) for every i < m.
+// rowsum (or NULL) receives sum_k A(i, k) for every i < m. The epilogue fuses the element-wise
+// step that follows a product: store; C = product + bias[j] with out2 = act(C); or
+// C = product * act'(pre) (pre in C's layout).
+enum { kEpiStore = 0, kEpiBiasAct = 1, kEpiDact = 2 };
+struct GemmEpilogue {
+    int kind = kEpiStore;
+    int act = ENOVA_RELU;
+    const float *bias = nullptr;
+    float *out2 = nullptr;
+    const float *pre = nullptr;
+};
 int64_t gemm_workspace_floats(int m, int n, int k);
-hipError_t launch_gemm(const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk, int64_t bj,
-                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *rowsum, float *work,
-                       hipStream_t st);
-hipError_t launch_bias_act(float *pre, const float *bias, float *out, int64_t rows, int cols, int act,
-                           hipStream_t st);
-hipError_t launch_dact(float *g, const float *pre, int64_t total, int act, hipStream_t st);
+// ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
+hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
+                       int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
+                       hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // ml: [rows][2L] = [mu | lv] per window (biases bml = [bmu | blv] added in place).
 hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
                          int L, hipStream_t st);

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 #include "mfma_common.h"
@@ -18,8 +19,15 @@ namespace {
 
 constexpr int kGemmTile = 128;  // C tile of a block: 2 x 2 waves of 64 x 64 (2 x 2 matrix ops of 32 x 32)
 constexpr int kGemmK = 32;      // reduction slice staged in LDS (double-buffered)
-constexpr int kGemmPitch = kGemmK + 4;   // floats per staged row: 16-byte rows, conflict-free 16-byte reads
-constexpr int kGemmTargetBlocks = 512;   // split the reduction until a launch has about this many blocks
+// LDS image of one operand slice. A k-contiguous operand is staged row-major, S[row][k] with a
+// pitch of kGemmK + 4 floats (16-byte rows, conflict-free 16-byte reads along k); a
+// row-contiguous operand is staged k-major, S[k][row] with a pitch of kGemmTile + 4 floats
+// (16-byte writes along rows, conflict-free 4-byte reads across lanes).
+constexpr int kGemmPitch = kGemmK + 4;
+constexpr int kGemmPitchT = kGemmTile + 4;
+constexpr int kGemmStage = kGemmTile * kGemmPitch > kGemmK * kGemmPitchT ? kGemmTile * kGemmPitch
+                                                                         : kGemmK * kGemmPitchT;
+constexpr int kGemmTargetBlocks = 256;   // split the reduction until a launch has about this many blocks
 constexpr int kGemmMinSlice = 128;       // ... but keep every slice at least this long
 constexpr int kGemmMaxSplits = 128;
 constexpr float kLog2Pi = 1.8378770664093453f;   // log(2 pi)
@@ -45,8 +53,22 @@ struct Stage {
         }
     }
 
-    // full: the whole 128 x 32 tile lies inside the operand and every group is 16-byte aligned
-    // (a uniform branch: one unconditional 16-byte load per group).
+    // The whole 128 x 32 tile lies inside the operand and every group is 16-byte aligned: one
+    // unconditional 16-byte load per group (a fixed instruction count, so the waits that follow
+    // can count exactly how many loads are still in flight).
+    __device__ __forceinline__ void load_full(const float *__restrict__ X, int64_t ld, int r0, int k0, int tid)
+    {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            int row, kx;
+            coords(tid, q, row, kx);
+            const int64_t off = KCONT ? static_cast<int64_t>(r0 + row) * ld + (k0 + kx)
+                                      : static_cast<int64_t>(k0 + kx) * ld + (r0 + row);
+            v[q] = *reinterpret_cast<const float4 *>(X + off);
+        }
+    }
+
+    // full: as load_full (a uniform branch); otherwise element by element with bounds checks.
     __device__ __forceinline__ void load(const float *__restrict__ X, int64_t ld, bool full, int r0, int rmax,
                                          int k0, int kend, int tid)
     {
@@ -77,42 +99,117 @@ struct Stage {
         }
     }
 
-    __device__ __forceinline__ void store(float (*S)[kGemmPitch], int tid) const
+    __device__ __forceinline__ void store(float *S, int tid) const
     {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int f = tid + 256 * q;
-            if constexpr (KCONT) {
-                *reinterpret_cast<float4 *>(&S[f >> 3][(f & 7) * 4]) = v[q];
-            } else {
-                const int kx = f >> 5, row = (f & 31) * 4;
-                S[row][kx] = v[q].x;
-                S[row + 1][kx] = v[q].y;
-                S[row + 2][kx] = v[q].z;
-                S[row + 3][kx] = v[q].w;
-            }
+            int row, kx;
+            coords(tid, q, row, kx);
+            if constexpr (KCONT)
+                *reinterpret_cast<float4 *>(&S[row * kGemmPitch + kx]) = v[q];
+            else
+                *reinterpret_cast<float4 *>(&S[kx * kGemmPitchT + row]) = v[q];
+        }
+    }
+
+    // The four reduction indices g*8 + 4*half + t (t = 0..3) of staged row `row`.
+    static __device__ __forceinline__ float4 operand(const float *S, int row, int g, int half)
+    {
+        const int k = g * 8 + 4 * half;
+        if constexpr (KCONT) {
+            return *reinterpret_cast<const float4 *>(&S[row * kGemmPitch + k]);
+        } else {
+            return make_float4(S[k * kGemmPitchT + row], S[(k + 1) * kGemmPitchT + row],
+                               S[(k + 2) * kGemmPitchT + row], S[(k + 3) * kGemmPitchT + row]);
         }
     }
 };
 
+// What a product does with C(i, j) once it is complete (fused element-wise steps):
+//   kEpiStore:     C = v
+//   kEpiBiasAct:   C = v + bias[j] (the pre-activation, kept for the backward pass), out2 = act(C)
+//   kEpiDact:      C = v * act'(pre[i][j]) (pre has C's layout)
+struct EpiParams {
+    const float *bias;   // kEpiBiasAct
+    float *out2;         // kEpiBiasAct: act(C), C's layout
+    const float *pre;    // kEpiDact
+};
+
+template <int ACT>
+__device__ __forceinline__ float dact_of(float a)
+{
+    if constexpr (ACT == ENOVA_TANH) {
+        const float t = tanhf(a);
+        return 1.0f - t * t;
+    } else {
+        return a > 0.0f ? 1.0f : 0.0f;
+    }
+}
+
+template <int EPI, int ACT>
+__device__ __forceinline__ void epi_store(float *__restrict__ C, int64_t ldc, int64_t i, int64_t j, float v,
+                                          const EpiParams &ep)
+{
+    const int64_t e = i * ldc + j;
+    if constexpr (EPI == kEpiBiasAct) {
+        const float a = v + ep.bias[j];
+        C[e] = a;
+        ep.out2[e] = act_fn<ACT>(a);
+    } else if constexpr (EPI == kEpiDact) {
+        C[e] = v * dact_of<ACT>(ep.pre[e]);
+    } else {
+        C[e] = v;
+    }
+}
+
+// A whole 32 x 32 sub-tile (rows si + crow(r, half), column gj of this lane): loads first, then
+// the element-wise step and the stores.
+template <int EPI, int ACT>
+__device__ __forceinline__ void epi_tile(float *__restrict__ C, int64_t ldc, int si, int gj, int half, const v16f &v,
+                                         const EpiParams &ep)
+{
+    if constexpr (EPI == kEpiBiasAct) {
+        const float bj = ep.bias[gj];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int64_t e = static_cast<int64_t>(si + crow(r, half)) * ldc + gj;
+            const float a = v[r] + bj;
+            C[e] = a;
+            ep.out2[e] = act_fn<ACT>(a);
+        }
+    } else if constexpr (EPI == kEpiDact) {
+        float pre[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            pre[r] = ep.pre[static_cast<int64_t>(si + crow(r, half)) * ldc + gj];
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            C[static_cast<int64_t>(si + crow(r, half)) * ldc + gj] = v[r] * dact_of<ACT>(pre[r]);
+    } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            C[static_cast<int64_t>(si + crow(r, half)) * ldc + gj] = v[r];
+    }
+}
+
 // C(i, j) [+]= sum_k A(i, k) B(k, j) for i < m, j < n over the block's reduction slice
 // [z kc, min(kk, (z + 1) kc)), z = blockIdx.z; C(i, j) = C[z m ldc + i ldc + j] (with several
-// slices each writes its own partial tile, summed afterwards in slice order by k_sum_splits).
+// slices each writes its own partial tile, summed afterwards in slice order by k_sum_splits,
+// which then applies the epilogue EPI; a single slice applies it here).
 // A is k-contiguous when AK (A(i, k) = A[i lda + k]), else row-contiguous (A[k lda + i]); B is
 // k-contiguous when BK (B(k, j) = B[j ldb + k]), else row-contiguous (B[k ldb + j]).
 // With rowsum != NULL the blocks of the first column tile also write sum_k A(i, k) over the slice
 // to rowsum[z m + i] (the bias gradient of a weight-gradient product, read from the staged tiles).
 // Matrix op t of an 8-index group takes, in lane l, the reduction index 4 (l / 32) + t of the
 // group for both operands (a relabelling of the sum), so one 16-byte LDS read feeds four ops.
-// 32 x 32 sub-tiles that lie wholly outside C are skipped (wave-uniform).
-template <bool AK, bool BK, bool ACC>
+template <bool AK, bool BK, int EPI, int ACT>
 __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, int64_t lda, bool va,
                                                  const float *__restrict__ B, int64_t ldb, bool vb,
                                                  float *__restrict__ C, int64_t ldc, float *__restrict__ rowsum,
-                                                 int m, int n, int kk, int kc)
+                                                 EpiParams ep, int m, int n, int kk, int kc)
 {
-    __shared__ __align__(16) float As[2][kGemmTile][kGemmPitch];
-    __shared__ __align__(16) float Bs[2][kGemmTile][kGemmPitch];
+    __shared__ __align__(16) float As[2][kGemmStage];
+    __shared__ __align__(16) float Bs[2][kGemmStage];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -138,58 +235,97 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
             for (int r = 0; r < 16; ++r)
                 acc[a][b][r] = 0.0f;
     float rs[2] = {0.0f, 0.0f};
-    Stage<AK> sa;
-    Stage<BK> sb;
+    // Two register stages: the global loads of slice s + 2 are issued before slice s is computed,
+    // so each load has two slices of matrix work to arrive in.
+    Stage<AK> sa[2];
+    Stage<BK> sb[2];
     const int ns = kend > kbeg ? (kend - kbeg + kGemmK - 1) / kGemmK : 0;
     const bool rows_a = va && i0 + kGemmTile <= m, rows_b = vb && j0 + kGemmTile <= n;
-    if (ns > 0) {
-        const bool kin = kbeg + kGemmK <= kend;
-        sa.load(A, lda, rows_a && kin, i0, m, kbeg, kend, tid);
-        sb.load(B, ldb, rows_b && kin, j0, n, kbeg, kend, tid);
-        sa.store(As[0], tid);
-        sb.store(Bs[0], tid);
-    }
-    __syncthreads();
-    for (int s = 0; s < ns; ++s) {
-        const int buf = s & 1;
-        if (s + 1 < ns) {
-            const int k1 = kbeg + (s + 1) * kGemmK;
-            const bool kin = k1 + kGemmK <= kend;
-            sa.load(A, lda, rows_a && kin, i0, m, k1, kend, tid);
-            sb.load(B, ldb, rows_b && kin, j0, n, k1, kend, tid);
+    auto compute = [&](int buf) __attribute__((always_inline)) {
+        // every operand read of the slice is issued before the first matrix op
+        float4 av[kGemmK / 8][2], bv[kGemmK / 8][2];
+#pragma unroll
+        for (int g = 0; g < kGemmK / 8; ++g) {
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+                av[g][a] = Stage<AK>::operand(As[buf], wy * 64 + a * 32 + l32, g, half);
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                bv[g][b] = Stage<BK>::operand(Bs[buf], wx * 64 + b * 32 + l32, g, half);
         }
 #pragma unroll
         for (int g = 0; g < kGemmK / 8; ++g) {
-            float4 av[2], bv[2];
+            // row sums of A (used only when requested; cheaper to always form than to branch)
 #pragma unroll
             for (int a = 0; a < 2; ++a)
-                av[a] = *reinterpret_cast<const float4 *>(&As[buf][wy * 64 + a * 32 + l32][g * 8 + 4 * half]);
+                rs[a] += (av[g][a].x + av[g][a].y) + (av[g][a].z + av[g][a].w);
+            // the four ops of one accumulator are interleaved with the other accumulators' ops
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-                bv[b] = *reinterpret_cast<const float4 *>(&Bs[buf][wx * 64 + b * 32 + l32][g * 8 + 4 * half]);
-            if (sums) {
+            for (int t = 0; t < 4; ++t)
 #pragma unroll
                 for (int a = 0; a < 2; ++a)
-                    rs[a] += (av[a].x + av[a].y) + (av[a].z + av[a].w);
-            }
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    if (!(live_a[a] && live_b[b]))
-                        continue;
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].x, bv[b].x, acc[a][b], 0, 0, 0);
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].y, bv[b].y, acc[a][b], 0, 0, 0);
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].z, bv[b].z, acc[a][b], 0, 0, 0);
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a].w, bv[b].w, acc[a][b], 0, 0, 0);
-                }
+                    for (int b = 0; b < 2; ++b) {
+                        const float4 &x4 = av[g][a], &y4 = bv[g][b];
+                        const float x = t == 0 ? x4.x : t == 1 ? x4.y : t == 2 ? x4.z : x4.w;
+                        const float y = t == 0 ? y4.x : t == 1 ? y4.y : t == 2 ? y4.z : y4.w;
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(x, y, acc[a][b], 0, 0, 0);
+                    }
         }
-        if (s + 1 < ns) {
-            sa.store(As[buf ^ 1], tid);
-            sb.store(Bs[buf ^ 1], tid);
+    };
+    // The slice loop, with unconditional loads when every slice of the block is a full tile
+    // (FULL) and bounds-checked loads otherwise.
+    auto run = [&](auto full_tag) __attribute__((always_inline)) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        auto fetch = [&](int sl, Stage<AK> &ra, Stage<BK> &rb) __attribute__((always_inline)) {
+            const int k1 = kbeg + sl * kGemmK;
+            if constexpr (FULL) {
+                ra.load_full(A, lda, i0, k1, tid);
+                rb.load_full(B, ldb, j0, k1, tid);
+            } else {
+                const bool kin = k1 + kGemmK <= kend;
+                ra.load(A, lda, rows_a && kin, i0, m, k1, kend, tid);
+                rb.load(B, ldb, rows_b && kin, j0, n, k1, kend, tid);
+            }
+        };
+        // one slice: slice s is in LDS buffer s & 1 and slice s + 1 in registers `nx`; `fr` is free
+        // With FULL every step issues the same loads and stores (past the end it re-reads the last
+        // slice and fills a buffer nobody reads), so the wait before the stores counts exactly the
+        // eight loads just issued and lets them stay in flight.
+        auto step = [&](int s, Stage<AK> &nxa, Stage<BK> &nxb, Stage<AK> &fra, Stage<BK> &frb)
+                        __attribute__((always_inline)) {
+            if (FULL)
+                fetch(min(s + 2, ns - 1), fra, frb);
+            else if (s + 2 < ns)
+                fetch(s + 2, fra, frb);
+            // keep the loads ahead of the matrix work (the scheduler would sink them to their use)
+            __builtin_amdgcn_sched_barrier(0);
+            compute(s & 1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (FULL || s + 1 < ns) {
+                nxa.store(As[(s + 1) & 1], tid);
+                nxb.store(Bs[(s + 1) & 1], tid);
+            }
+            __syncthreads();
+        };
+        if (ns > 0) {
+            fetch(0, sa[0], sb[0]);
+            if (FULL || ns > 1)
+                fetch(min(1, ns - 1), sa[1], sb[1]);
+            sa[0].store(As[0], tid);
+            sb[0].store(Bs[0], tid);
         }
         __syncthreads();
-    }
+        for (int s = 0; s < ns; s += 2) {
+            step(s, sa[1], sb[1], sa[0], sb[0]);
+            if (s + 1 < ns)
+                step(s + 1, sa[0], sb[0], sa[1], sb[1]);
+        }
+    };
+    if (rows_a && rows_b && (kend - kbeg) % kGemmK == 0)
+        run(std::true_type{});
+    else
+        run(std::false_type{});
     if (sums) {
 #pragma unroll
         for (int a = 0; a < 2; ++a) {
@@ -205,73 +341,52 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
         for (int b = 0; b < 2; ++b) {
             if (!(live_a[a] && live_b[b]))
                 continue;
+            const int si = i0 + wy * 64 + a * 32, gj = j0 + wx * 64 + b * 32 + l32;
+            if (si + 32 <= m && j0 + wx * 64 + b * 32 + 32 <= n) {
+                // whole sub-tile inside C: the epilogue's reads are issued together
+                epi_tile<EPI, ACT>(C, ldc, si, gj, half, acc[a][b], ep);
+            } else {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int gi = i0 + wy * 64 + a * 32 + crow(r, half);
-                const int gj = j0 + wx * 64 + b * 32 + l32;
-                if (gi < m && gj < n) {
-                    float *dst = C + static_cast<int64_t>(gi) * ldc + gj;
-                    *dst = ACC ? *dst + acc[a][b][r] : acc[a][b][r];
+                for (int r = 0; r < 16; ++r) {
+                    const int gi = si + crow(r, half);
+                    if (gi < m && gj < n)
+                        epi_store<EPI, ACT>(C, ldc, gi, gj, acc[a][b][r], ep);
                 }
             }
         }
 }
 
-// C(i, j) [+]= sum over the slices s = 0, 1, ... (in order) of P[s][i][j].
-template <bool ACC>
-__global__ __launch_bounds__(256) void k_sum_splits(const float *__restrict__ P, int splits, int m, int n,
-                                                    float *__restrict__ C, int64_t ldc)
+// C(i, j) = epilogue(sum over the slices s = 0, 1, ... (in order) of P[s][i][j]) for i < m, j < n,
+// and, with rowsum != NULL, rowsum[i] = sum over the slices of R[s][i].
+template <int EPI, int ACT>
+__global__ __launch_bounds__(256) void k_sum_splits(const float *__restrict__ P, const float *__restrict__ R,
+                                                    int splits, int m, int n, float *__restrict__ C, int64_t ldc,
+                                                    float *__restrict__ rowsum, EpiParams ep)
 {
     const int64_t total = static_cast<int64_t>(m) * n;
-    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t all = total + (rowsum ? m : 0);
+    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < all; e += static_cast<int64_t>(gridDim.x) * 256) {
+        const bool main = e < total;
+        const float *src = main ? P + e : R + (e - total);
+        const int64_t stride = main ? total : m;
         float v = 0.0f;
         int sp = 0;
         for (; sp + 8 <= splits; sp += 8) {
             float t[8];
 #pragma unroll
             for (int u = 0; u < 8; ++u)
-                t[u] = P[(sp + u) * total + e];
+                t[u] = src[(sp + u) * stride];
 #pragma unroll
             for (int u = 0; u < 8; ++u)
                 v += t[u];
         }
         for (; sp < splits; ++sp)
-            v += P[sp * total + e];
-        const int64_t i = e / n, j = e % n;
-        C[i * ldc + j] = ACC ? C[i * ldc + j] + v : v;
+            v += src[sp * stride];
+        if (main)
+            epi_store<EPI, ACT>(C, ldc, e / n, e % n, v, ep);
+        else
+            rowsum[e - total] = v;
     }
-}
-
-template <int ACT>
-__device__ __forceinline__ float dact(float a)
-{
-    if constexpr (ACT == ENOVA_TANH) {
-        const float t = tanhf(a);
-        return 1.0f - t * t;
-    } else {
-        return a > 0.0f ? 1.0f : 0.0f;
-    }
-}
-
-// pre[i][j] += bias[j]; out[i][j] = act(pre[i][j])
-template <int ACT>
-__global__ __launch_bounds__(256) void k_bias_act(float *__restrict__ pre, const float *__restrict__ bias,
-                                                  float *__restrict__ out, int64_t rows, int cols)
-{
-    const int64_t total = rows * cols;
-    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
-        const float a = pre[e] + bias[e % cols];
-        pre[e] = a;
-        out[e] = act_fn<ACT>(a);
-    }
-}
-
-// g[e] *= act'(pre[e])
-template <int ACT>
-__global__ __launch_bounds__(256) void k_dact(float *__restrict__ g, const float *__restrict__ pre, int64_t total)
-{
-    for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256)
-        g[e] *= dact<ACT>(pre[e]);
 }
 
 // One thread per window. ml holds [mu | lv] per window (2L floats, biases [bmu | blv] added in
@@ -475,21 +590,81 @@ int64_t gemm_workspace_floats(int m, int n, int k)
     return s > 1 ? static_cast<int64_t>(s) * (static_cast<int64_t>(m) * n + m) : 0;
 }
 
-template <bool AK, bool BK>
-void gemm_dispatch(dim3 grid, hipStream_t st, bool acc, const float *A, int64_t lda, bool va, const float *B,
-                   int64_t ldb, bool vb, float *C, int64_t ldc, float *rowsum, int m, int n, int k, int kc)
+namespace {
+
+template <bool AK, bool BK, int EPI, int ACT>
+void gemm_run(dim3 grid, hipStream_t st, const float *A, int64_t lda, bool va, const float *B, int64_t ldb, bool vb,
+              float *C, int64_t ldc, float *rowsum, const EpiParams &ep, int m, int n, int k, int kc)
 {
-    if (acc)
-        hipLaunchKernelGGL((k_gemm<AK, BK, true>), grid, dim3(256), 0, st, A, lda, va, B, ldb, vb, C, ldc, rowsum,
-                           m, n, k, kc);
-    else
-        hipLaunchKernelGGL((k_gemm<AK, BK, false>), grid, dim3(256), 0, st, A, lda, va, B, ldb, vb, C, ldc,
-                           rowsum, m, n, k, kc);
+    hipLaunchKernelGGL((k_gemm<AK, BK, EPI, ACT>), grid, dim3(256), 0, st, A, lda, va, B, ldb, vb, C, ldc, rowsum,
+                       ep, m, n, k, kc);
 }
 
-hipError_t launch_gemm(const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk, int64_t bj,
-                       float *C, int64_t ldc, int m, int n, int k, bool accumulate, float *rowsum, float *work,
-                       hipStream_t st)
+template <int EPI, int ACT>
+void gemm_layouts(bool a_k, bool b_k, dim3 grid, hipStream_t st, const float *A, int64_t lda, bool va,
+                  const float *B, int64_t ldb, bool vb, float *C, int64_t ldc, float *rowsum, const EpiParams &ep,
+                  int m, int n, int k, int kc)
+{
+    if (a_k && b_k)
+        gemm_run<true, true, EPI, ACT>(grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
+    else if (a_k)
+        gemm_run<true, false, EPI, ACT>(grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
+    else if (b_k)
+        gemm_run<false, true, EPI, ACT>(grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
+    else
+        gemm_run<false, false, EPI, ACT>(grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
+}
+
+template <int EPI, int ACT>
+void sum_run(unsigned blocks, hipStream_t st, const float *P, const float *R, int splits, int m, int n, float *C,
+             int64_t ldc, float *rowsum, const EpiParams &ep)
+{
+    hipLaunchKernelGGL((k_sum_splits<EPI, ACT>), dim3(blocks), dim3(256), 0, st, P, R, splits, m, n, C, ldc, rowsum,
+                       ep);
+}
+
+// The epilogue kind and activation as template arguments.
+template <template <int, int> class F, typename... Args>
+void with_epilogue(int kind, int act, Args &&...args)
+{
+    if (kind == kEpiBiasAct) {
+        if (act == ENOVA_TANH)
+            F<kEpiBiasAct, ENOVA_TANH>::run(args...);
+        else
+            F<kEpiBiasAct, ENOVA_RELU>::run(args...);
+    } else if (kind == kEpiDact) {
+        if (act == ENOVA_TANH)
+            F<kEpiDact, ENOVA_TANH>::run(args...);
+        else
+            F<kEpiDact, ENOVA_RELU>::run(args...);
+    } else {
+        F<kEpiStore, ENOVA_RELU>::run(args...);
+    }
+}
+
+template <int EPI, int ACT>
+struct GemmF {
+    template <typename... Args>
+    static void run(Args &&...args)
+    {
+        gemm_layouts<EPI, ACT>(args...);
+    }
+};
+
+template <int EPI, int ACT>
+struct SumF {
+    template <typename... Args>
+    static void run(Args &&...args)
+    {
+        sum_run<EPI, ACT>(args...);
+    }
+};
+
+}  // namespace
+
+hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
+                       int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
+                       hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
 {
     if (m <= 0 || n <= 0)
         return hipSuccess;
@@ -505,50 +680,28 @@ hipError_t launch_gemm(const float *A, int64_t ai, int64_t ak, const float *B, i
     const int used = splits > 1 ? (k + kc - 1) / kc : 1;
     const dim3 grid(static_cast<unsigned>((n + kGemmTile - 1) / kGemmTile),
                     static_cast<unsigned>((m + kGemmTile - 1) / kGemmTile), static_cast<unsigned>(used));
-    const bool split = used > 1;
-    float *dst = split ? work : C;
-    float *rdst = rowsum && split ? work + static_cast<int64_t>(used) * m * n : rowsum;
-    const int64_t ldd = split ? static_cast<int64_t>(n) : ldc;
-    const bool acc = split ? false : accumulate;
-    if (a_k && b_k)
-        gemm_dispatch<true, true>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
-    else if (a_k)
-        gemm_dispatch<true, false>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
-    else if (b_k)
-        gemm_dispatch<false, true>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
-    else
-        gemm_dispatch<false, false>(grid, st, acc, A, lda, va, B, ldb, vb, dst, ldd, rdst, m, n, k, kc);
-    if (split) {
-        const unsigned b = blocks_for(static_cast<int64_t>(m) * n);
-        if (accumulate)
-            hipLaunchKernelGGL(k_sum_splits<true>, dim3(b), dim3(256), 0, st, work, used, m, n, C, ldc);
-        else
-            hipLaunchKernelGGL(k_sum_splits<false>, dim3(b), dim3(256), 0, st, work, used, m, n, C, ldc);
-        if (rowsum)
-            hipLaunchKernelGGL(k_sum_splits<false>, dim3(blocks_for(m)), dim3(256), 0, st, rdst, used, 1, m,
-                               rowsum, static_cast<int64_t>(m));
+    const EpiParams ep{epi.bias, epi.out2, epi.pre};
+    hipError_t e = hipSuccess;
+    if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess)
+        return e;
+    if (used == 1) {
+        with_epilogue<GemmF>(epi.kind, epi.act, a_k, b_k, grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, ep, m, n,
+                             k, kc);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        return ev1 ? hipEventRecord(ev1, st) : hipSuccess;
     }
-    return hipGetLastError();
-}
-
-hipError_t launch_bias_act(float *pre, const float *bias, float *out, int64_t rows, int cols, int act,
-                           hipStream_t st)
-{
-    const unsigned b = blocks_for(rows * cols);
-    if (act == ENOVA_TANH)
-        hipLaunchKernelGGL(k_bias_act<ENOVA_TANH>, dim3(b), dim3(256), 0, st, pre, bias, out, rows, cols);
-    else
-        hipLaunchKernelGGL(k_bias_act<ENOVA_RELU>, dim3(b), dim3(256), 0, st, pre, bias, out, rows, cols);
-    return hipGetLastError();
-}
-
-hipError_t launch_dact(float *g, const float *pre, int64_t total, int act, hipStream_t st)
-{
-    const unsigned b = blocks_for(total);
-    if (act == ENOVA_TANH)
-        hipLaunchKernelGGL(k_dact<ENOVA_TANH>, dim3(b), dim3(256), 0, st, g, pre, total);
-    else
-        hipLaunchKernelGGL(k_dact<ENOVA_RELU>, dim3(b), dim3(256), 0, st, g, pre, total);
+    // partial tiles, then one pass that sums them in slice order and applies the epilogue
+    float *part_rows = rowsum ? work + static_cast<int64_t>(used) * m * n : nullptr;
+    gemm_layouts<kEpiStore, ENOVA_RELU>(a_k, b_k, grid, st, A, lda, va, B, ldb, vb, work, static_cast<int64_t>(n),
+                                        part_rows, EpiParams{}, m, n, k, kc);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess)
+        return e;
+    const unsigned blocks = blocks_for(static_cast<int64_t>(m) * n + (rowsum ? m : 0));
+    with_epilogue<SumF>(epi.kind, epi.act, blocks, st, static_cast<const float *>(work),
+                        static_cast<const float *>(part_rows), used, m, n, C, ldc, rowsum, ep);
     return hipGetLastError();
 }
 

@@ -236,39 +236,54 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
             run(hipEventRecord(t->ev[ne++], s));
     };
     // every product of the step, bracketed by events when timing is on
-    auto gemm = [&](const float *A, int64_t ai, int64_t ak, const float *Bm, int64_t bk, int64_t bj, float *C,
-                    int64_t ldc, int m, int n, int k, bool acc, float *rowsum, float *work, hipStream_t st) {
-        mark();
-        run(launch_gemm(A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, acc, rowsum, work, st));
-        mark();
+    // every product of the step; with timing on, its product kernel is bracketed by two events
+    auto gemm = [&](const GemmEpilogue &ep, const float *A, int64_t ai, int64_t ak, const float *Bm, int64_t bk,
+                    int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum) {
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (t->timed && ne + 2 < enova_trainer_s::kMaxEvents) {
+            e0 = t->ev[ne++];
+            e1 = t->ev[ne++];
+        }
+        run(launch_gemm(ep, A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, rowsum, t->work, s, e0, e1));
+    };
+    const GemmEpilogue plain{};
+    auto bias_act = [&](const float *bias, float *out) {
+        GemmEpilogue e;
+        e.kind = kEpiBiasAct;
+        e.act = act;
+        e.bias = bias;
+        e.out2 = out;
+        return e;
+    };
+    auto dact = [&](const float *pre) {
+        GemmEpilogue e;
+        e.kind = kEpiDact;
+        e.act = act;
+        e.pre = pre;
+        return e;
     };
     mark();
-    float *W = t->work;
-    // forward: a1 = V W1^T (+ b1), h = act(a1)
-    gemm(V, D, 1, P + o[P_W1], 1, D, t->a1, H, B, H, D, false, nullptr, W, s);
-    run(launch_bias_act(t->a1, P + o[P_B1], t->h, B, H, act, s));
+    // forward: a1 = V W1^T + b1, h = act(a1)
+    gemm(bias_act(P + o[P_B1], t->h), V, D, 1, P + o[P_W1], 1, D, t->a1, H, B, H, D, nullptr);
     // fused heads [mu | lv] = h [Wmu; Wlv]^T, reparameterised latent and KL
-    gemm(t->h, H, 1, P + o[P_WMU], 1, H, t->ml, 2 * L, B, 2 * L, H, false, nullptr, W, s);
+    gemm(plain, t->h, H, 1, P + o[P_WMU], 1, H, t->ml, 2 * L, B, 2 * L, H, nullptr);
     run(launch_latent(t->ml, P + o[P_BMU], eps, t->sd, t->z, t->kl, B, L, s));
-    // decoder: a2 = z Wd1^T (+ bd1), hd = act(a2), m' = hd Wd2^T (+ bd2) -> log p and dJ/dm'
-    gemm(t->z, L, 1, P + o[P_WD1], 1, L, t->a2, H, B, H, L, false, nullptr, W, s);
-    run(launch_bias_act(t->a2, P + o[P_BD1], t->hd, B, H, act, s));
-    gemm(t->hd, H, 1, P + o[P_WD2], 1, H, t->out, D, B, D, H, false, nullptr, W, s);
+    // decoder: a2 = z Wd1^T + bd1, hd = act(a2), m' = hd Wd2^T (+ bd2) -> log p and dJ/dm'
+    gemm(bias_act(P + o[P_BD1], t->hd), t->z, L, 1, P + o[P_WD1], 1, L, t->a2, H, B, H, L, nullptr);
+    gemm(plain, t->hd, H, 1, P + o[P_WD2], 1, H, t->out, D, B, D, H, nullptr);
     run(launch_recon(t->out, P + o[P_BD2], V, labels, t->logp, B, D, t->hyper.margin, s));
     // beta(k) from this batch's KL, before the backward pass
     run(launch_beta(t->kl, t->logp, labels, B, D, t->hyper, t->state, t->state + 1, info, s));
     // backward through the decoder (G = dJ/dm' in out); bias gradients are the row sums of G^T
-    gemm(t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, false, G + o[P_BD2], W, s);   // dWd2 = G^T hd
-    gemm(t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, false, nullptr, W, s);        // dJ/dhd = G Wd2
-    run(launch_dact(t->gh, t->a2, static_cast<int64_t>(B) * H, act, s));
-    gemm(t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, false, G + o[P_BD1], W, s);      // dWd1 = G^T z
-    gemm(t->gh, H, 1, P + o[P_WD1], L, 1, t->gz, L, B, L, H, false, nullptr, W, s);          // dJ/dz = G Wd1
-    // latent: [dJ/dmu | dJ/dlv], then the fused heads' gradients and dJ/dh = G_ml [Wmu; Wlv]
+    gemm(plain, t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, G + o[P_BD2]);    // dWd2 = G^T hd
+    gemm(dact(t->a2), t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, nullptr);   // dJ/da2
+    gemm(plain, t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, G + o[P_BD1]);      // dWd1 = G^T z
+    gemm(plain, t->gh, H, 1, P + o[P_WD1], L, 1, t->gz, L, B, L, H, nullptr);          // dJ/dz = G Wd1
+    // latent: [dJ/dmu | dJ/dlv], then the fused heads' gradients and dJ/da1 = (G_ml [Wmu; Wlv]) act'(a1)
     run(launch_latent_grad(t->gz, t->gml, t->ml, t->sd, eps, labels, t->state + 1, B, L, s));
-    gemm(t->gml, 1, 2 * L, t->h, H, 1, G + o[P_WMU], H, 2 * L, H, B, false, G + o[P_BMU], W, s);
-    gemm(t->gml, 2 * L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, 2 * L, false, nullptr, W, s);
-    run(launch_dact(t->gh, t->a1, static_cast<int64_t>(B) * H, act, s));
-    gemm(t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, false, G + o[P_B1], W, s);            // dW1 = G^T V
+    gemm(plain, t->gml, 1, 2 * L, t->h, H, 1, G + o[P_WMU], H, 2 * L, H, B, G + o[P_BMU]);
+    gemm(dact(t->a1), t->gml, 2 * L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, 2 * L, nullptr);
+    gemm(plain, t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, G + o[P_B1]);            // dW1 = G^T V
     // Adam
     t->step += 1;
     run(launch_adam(P, G, t->m, t->v, t->total, t->hyper, t->step, s));
