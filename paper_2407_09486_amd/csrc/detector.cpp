@@ -13,6 +13,7 @@
 
 #include "enova_detect.h"
 #include "internal.h"
+#include "stream_internal.h"
 
 namespace {
 thread_local std::string g_last_error;

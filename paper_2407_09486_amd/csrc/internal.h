@@ -171,88 +171,4 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
 // Method of moments / degenerate cases (n_peaks < 10) from the excesses on the host.
 PotResult pot_small(double t, int64_t n, const double *excess, int64_t n_peaks, double q);
 
-// ---------------------------------------------------------------------------------------------
-// Streaming detection: n streams advance one step per push; each keeps its last W steps in a
-// ring of 2W slots (every step is written twice, at slot c % W and c % W + W, so the newest W
-// steps are always contiguous), and its own SPOT threshold.
-// ---------------------------------------------------------------------------------------------
-struct StreamScoreParams {
-    const void *ring;            // [n][2W][M], the detector's dtype
-    int n_streams;
-    int first_slot;              // slot of the newest window's first step (the same in every stream)
-    const float *mean, *std;     // [n][M]
-    const uint4 *w1p;            // the detector's packed W1 fragments
-    const float *whp, *wd1p;     // the detector's epilogue fragments
-    const float *b1, *bd1, *u, *bh;
-    float sum_bd2;
-    float *scores;               // [n]
-    float *md;                   // [n] or null
-};
-// x_step [n][M] becomes step number `step` (0-based) of every stream.
-hipError_t launch_stream_append(const Geometry &g, const void *x_step, int n, int64_t step, void *ring,
-                                hipStream_t st);
-// Lets the streaming scoring kernel of g use the LDS it needs; false if g does not fit.
-bool stream_score_supported(const Geometry &g);
-hipError_t prepare_stream_score(const Geometry &g);
-hipError_t launch_stream_score(const Geometry &g, const StreamScoreParams &p, hipStream_t st);
-
-// Per-stream SPOT state (device arrays of n entries; peaks [n][cap]).
-struct SpotState {
-    double *t, *z;               // level quantile and threshold (+inf: no calibration)
-    int64_t *cnt;                // observations counted (calibration + later non-alarms)
-    int *npk;                    // stored peaks
-    double *peaks;               // excesses over t, arrival order
-    int cap;
-    uint8_t *mark;               // 1: z must be refitted
-    int *err;                    // set to 1 if a stream's calibration peaks exceed cap
-    int *list;                   // [n]: streams that took a new peak in this push (any order)
-    int *count;                  // entries of list (cleared before each update)
-};
-hipError_t launch_spot_init(const float *cal, const int64_t *cal_off, int n, double level,
-                            const SpotState &s, hipStream_t st);
-hipError_t launch_spot_update(const float *scores, int n, const SpotState &s, uint8_t *flags,
-                              hipStream_t st);
-// Refits z: every marked stream (all = true), or the streams listed by the last update.
-hipError_t launch_spot_fit(int n, double q, const SpotState &s, bool all, hipStream_t st);
-
-// ---------------------------------------------------------------------------------------------
-// Training (fp32): C(i, j) [+]= sum_k A(i, k) B(k, j), A(i, k) = A[i*ai + k*ak],
-// B(k, j) = B[k*bk + j*bj], C(i, j) = C[i*ldc + j]; and the element-wise steps around it.
-// ---------------------------------------------------------------------------------------------
-struct TrainHyper {
-    float lr, b1, b2, eps;
-    float kl_set, kp, ki, beta_min, beta_max;
-    float margin;   // cap of an anomalous window's reconstruction error (+inf: none)
-};
-// A long reduction over few output tiles is split into slices whose partial tiles go to `work`
-// (gemm_workspace_floats(m, n, k) floats; NULL: no split) and are then summed in slice order.
-// rowsum (or NULL) receives sum_k A(i, k) for every i < m. The epilogue fuses the element-wise
-// step that follows a product: store; C = product + bias[j] with out2 = act(C); or
-// C = product * act'(pre) (pre in C's layout).
-enum { kEpiStore = 0, kEpiBiasAct = 1, kEpiDact = 2 };
-struct GemmEpilogue {
-    int kind = kEpiStore;
-    int act = ENOVA_RELU;
-    const float *bias = nullptr;
-    float *out2 = nullptr;
-    const float *pre = nullptr;
-};
-int64_t gemm_workspace_floats(int m, int n, int k);
-// ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
-hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
-                       int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
-                       hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
-// ml: [rows][2L] = [mu | lv] per window (biases bml = [bmu | blv] added in place).
-hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
-                         int L, hipStream_t st);
-hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
-                        int rows, int D, float margin, hipStream_t st);
-hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
-                       const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st);
-// gz: [rows][L] = dJ/dz; gml: [rows][2L] = [dJ/dmu | dJ/dlv].
-hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, const float *sd, const float *eps,
-                              const float *labels, const float *beta, int rows, int L, hipStream_t st);
-hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
-                       int64_t step, hipStream_t st);
-
 }  // namespace enova

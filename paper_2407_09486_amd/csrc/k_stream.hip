@@ -17,7 +17,7 @@
 #include <cmath>
 
 #include "gpd_math.h"
-#include "internal.h"
+#include "stream_internal.h"
 #include "mfma_common.h"
 
 namespace enova {

@@ -10,7 +10,7 @@
 #include <cmath>
 #include <type_traits>
 
-#include "internal.h"
+#include "train_internal.h"
 #include "mfma_common.h"
 
 namespace enova {

@@ -1,0 +1,52 @@
+// Internal declarations of the streaming path (per-stream rings, newest-window scoring, SPOT).
+#pragma once
+
+#include "internal.h"
+
+namespace enova {
+
+// ---------------------------------------------------------------------------------------------
+// Streaming detection: n streams advance one step per push; each keeps its last W steps in a
+// ring of 2W slots (every step is written twice, at slot c % W and c % W + W, so the newest W
+// steps are always contiguous), and its own SPOT threshold.
+// ---------------------------------------------------------------------------------------------
+struct StreamScoreParams {
+    const void *ring;            // [n][2W][M], the detector's dtype
+    int n_streams;
+    int first_slot;              // slot of the newest window's first step (the same in every stream)
+    const float *mean, *std;     // [n][M]
+    const uint4 *w1p;            // the detector's packed W1 fragments
+    const float *whp, *wd1p;     // the detector's epilogue fragments
+    const float *b1, *bd1, *u, *bh;
+    float sum_bd2;
+    float *scores;               // [n]
+    float *md;                   // [n] or null
+};
+// x_step [n][M] becomes step number `step` (0-based) of every stream.
+hipError_t launch_stream_append(const Geometry &g, const void *x_step, int n, int64_t step, void *ring,
+                                hipStream_t st);
+// Lets the streaming scoring kernel of g use the LDS it needs; false if g does not fit.
+bool stream_score_supported(const Geometry &g);
+hipError_t prepare_stream_score(const Geometry &g);
+hipError_t launch_stream_score(const Geometry &g, const StreamScoreParams &p, hipStream_t st);
+
+// Per-stream SPOT state (device arrays of n entries; peaks [n][cap]).
+struct SpotState {
+    double *t, *z;               // level quantile and threshold (+inf: no calibration)
+    int64_t *cnt;                // observations counted (calibration + later non-alarms)
+    int *npk;                    // stored peaks
+    double *peaks;               // excesses over t, arrival order
+    int cap;
+    uint8_t *mark;               // 1: z must be refitted
+    int *err;                    // set to 1 if a stream's calibration peaks exceed cap
+    int *list;                   // [n]: streams that took a new peak in this push (any order)
+    int *count;                  // entries of list (cleared before each update)
+};
+hipError_t launch_spot_init(const float *cal, const int64_t *cal_off, int n, double level,
+                            const SpotState &s, hipStream_t st);
+hipError_t launch_spot_update(const float *scores, int n, const SpotState &s, uint8_t *flags,
+                              hipStream_t st);
+// Refits z: every marked stream (all = true), or the streams listed by the last update.
+hipError_t launch_spot_fit(int n, double q, const SpotState &s, bool all, hipStream_t st);
+
+}  // namespace enova

@@ -1,0 +1,48 @@
+// Internal declarations of the training step (matrix-core products and element-wise kernels).
+#pragma once
+
+#include "internal.h"
+
+namespace enova {
+
+// ---------------------------------------------------------------------------------------------
+// Training (fp32): C(i, j) [+]= sum_k A(i, k) B(k, j), A(i, k) = A[i*ai + k*ak],
+// B(k, j) = B[k*bk + j*bj], C(i, j) = C[i*ldc + j]; and the element-wise steps around it.
+// ---------------------------------------------------------------------------------------------
+struct TrainHyper {
+    float lr, b1, b2, eps;
+    float kl_set, kp, ki, beta_min, beta_max;
+    float margin;   // cap of an anomalous window's reconstruction error (+inf: none)
+};
+// A long reduction over few output tiles is split into slices whose partial tiles go to `work`
+// (gemm_workspace_floats(m, n, k) floats; NULL: no split) and are then summed in slice order.
+// rowsum (or NULL) receives sum_k A(i, k) for every i < m. The epilogue fuses the element-wise
+// step that follows a product: store; C = product + bias[j] with out2 = act(C); or
+// C = product * act'(pre) (pre in C's layout).
+enum { kEpiStore = 0, kEpiBiasAct = 1, kEpiDact = 2 };
+struct GemmEpilogue {
+    int kind = kEpiStore;
+    int act = ENOVA_RELU;
+    const float *bias = nullptr;
+    float *out2 = nullptr;
+    const float *pre = nullptr;
+};
+int64_t gemm_workspace_floats(int m, int n, int k);
+// ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
+hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
+                       int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
+                       hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// ml: [rows][2L] = [mu | lv] per window (biases bml = [bmu | blv] added in place).
+hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
+                         int L, hipStream_t st);
+hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
+                        int rows, int D, float margin, hipStream_t st);
+hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
+                       const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st);
+// gz: [rows][L] = dJ/dz; gml: [rows][2L] = [dJ/dmu | dJ/dlv].
+hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, const float *sd, const float *eps,
+                              const float *labels, const float *beta, int rows, int L, hipStream_t st);
+hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
+                       int64_t step, hipStream_t st);
+
+}  // namespace enova

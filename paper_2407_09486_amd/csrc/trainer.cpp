@@ -7,7 +7,7 @@
 #include <new>
 
 #include "enova_detect.h"
-#include "internal.h"
+#include "train_internal.h"
 
 using namespace enova;
 
