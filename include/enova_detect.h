@@ -297,6 +297,68 @@ enova_status enova_train_kernel_times(enova_trainer t, double *gemm_ms, double *
 /* Free a trainer (synchronises the device). NULL is a no-op. */
 enova_status enova_train_destroy(enova_trainer t);
 
+/*
+ * Configuration scans (Section IV-A, Eqs. (2)-(3), Table III) over the same monitoring series.
+ * Whether the finished-request rate n^f still depends on the number of running requests n^r is
+ * decided per window by an ordinary-least-squares fit n^f = a + b n^r and a two-sided t-test of
+ * the slope at level alpha (t = b / sqrt(RSS / ((W - 2) Sxx)), significant iff
+ * |t| > t_{1-alpha/2, W-2}; a window with constant n^r has b = 0, a = mean n^f, t = 0); the
+ * GPU memory relation m^u = g0 + g1 n^r is fitted by OLS on the same window. Per stream, the last
+ * window then gives n_limit and t^r_limit as quantiles of a Gaussian kernel density estimate
+ * (Silverman's bandwidth 0.9 min(sd, IQR/1.34) W^(-1/5), sd if IQR = 0, a point mass if the window
+ * is constant) of n^f and of t^r: at level q_extreme when the relation is significant (n^f has not
+ * reached its limit, so the limit lies in the upper tail), at 0.5 otherwise (n^f sits at its
+ * limit); max_num_seqs = n_limit t^r_limit (Eq. (2)) and gpu_memory = g0 + g1 max_num_seqs
+ * (Eq. (3)). Windows are the detector's: W steps, stride S, from step 0 of each stream. All
+ * statistics are computed in fp64.
+ */
+typedef struct enova_config_s *enova_config;   /* opaque; owned by the library */
+
+typedef struct {
+    int32_t metrics, window, stride;   /* M >= 1; 3 <= W <= 4096; S >= 1 */
+    int32_t dtype;                     /* enova_dtype of x */
+    int32_t col_finished, col_running, col_exec_time, col_mem_util;   /* metric columns of n^f, n^r, t^r, m^u */
+    double alpha;                      /* in (0, 1), e.g. 0.05 */
+    double q_extreme;                  /* in (0, 1), e.g. 0.99 */
+} enova_config_params;
+
+/* Two-sided critical value t_{1-alpha/2, dof} of Student's t (host helper). Errors: EINVAL. */
+enova_status enova_config_t_critical(double alpha, int32_t dof, double *out);
+
+/* Create a configuration scanner on the current device. Errors: EINVAL, ENOMEM, EHIP. */
+enova_status enova_config_init(const enova_config_params *params, enova_config *out);
+enova_status enova_config_destroy(enova_config c);
+
+/* Host helper: the window CSR of the scanner's W and S (as enova_detect_window_offsets). */
+enova_status enova_config_window_offsets(enova_config c, const int64_t *stream_offsets_host,
+                                         int32_t n_streams, int64_t *window_offsets_host);
+
+/*
+ * Every window of every stream (device pointers; outputs [n_windows] float or uint8, any may be
+ * NULL): OLS of n^f on n^r (intercept, slope, t statistic, significant), OLS of m^u on n^r
+ * (intercept, slope). x: [stream_offsets[n]][M] in the scanner's dtype. Asynchronous.
+ * Errors: EINVAL, ENOMEM, EHIP.
+ */
+enova_status enova_config_scan(enova_config c, const void *x, const int64_t *stream_offsets,
+                               const int64_t *window_offsets, int32_t n_streams, int64_t n_windows,
+                               float *out_intercept, float *out_slope, float *out_t,
+                               uint8_t *out_significant, float *out_mem_intercept, float *out_mem_slope,
+                               hipStream_t stream);
+
+/*
+ * The configuration read off each stream's last window (device outputs [n_streams], any may be
+ * NULL): significant (0/1), n_limit, t^r_limit, max_num_seqs, gpu_memory (NaN and 0 for a stream
+ * shorter than W). Asynchronous. Errors: EINVAL, EHIP.
+ */
+enova_status enova_config_recommend(enova_config c, const void *x, const int64_t *stream_offsets,
+                                    int32_t n_streams, uint8_t *out_significant, double *out_n_limit,
+                                    double *out_t_limit, double *out_max_num_seqs, double *out_gpu_memory,
+                                    hipStream_t stream);
+
+/* Kernel timing of the last enova_config_scan (its scan kernel) when enabled, milliseconds. */
+enova_status enova_config_set_timing(enova_config c, int32_t enable);
+enova_status enova_config_kernel_time(enova_config c, double *scan_kernel_ms);
+
 /* flags[i] = scores[i] > threshold for i < n_windows (device pointers). Asynchronous. */
 enova_status enova_detect_flag(enova_detector det, const float *scores, int64_t n_windows,
                                float threshold, uint8_t *out_flags, hipStream_t stream);

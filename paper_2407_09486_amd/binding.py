@@ -27,7 +27,9 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_detect_kernel_kind", "enova_stream_create", "enova_stream_push",
            "enova_stream_state", "enova_stream_kernel_times", "enova_stream_destroy",
            "enova_train_init", "enova_train_step", "enova_train_params_get", "enova_train_grads_get",
-           "enova_train_set_timing", "enova_train_kernel_times", "enova_train_destroy", "enova_status_str", "enova_last_error"]
+           "enova_train_set_timing", "enova_train_kernel_times", "enova_train_destroy",
+           "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
+           "enova_config_scan", "enova_config_recommend", "enova_config_set_timing", "enova_config_kernel_time", "enova_status_str", "enova_last_error"]
 
 
 class EnovaError(RuntimeError):
@@ -53,6 +55,13 @@ class enova_train_config(ctypes.Structure):
                 ("adam_b2", ctypes.c_float), ("adam_eps", ctypes.c_float), ("kl_set", ctypes.c_float),
                 ("kp", ctypes.c_float), ("ki", ctypes.c_float), ("beta_min", ctypes.c_float),
                 ("beta_max", ctypes.c_float), ("anomaly_margin", ctypes.c_float)]
+
+
+class enova_config_params(ctypes.Structure):
+    _fields_ = [("metrics", ctypes.c_int32), ("window", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("col_finished", ctypes.c_int32), ("col_running", ctypes.c_int32),
+                ("col_exec_time", ctypes.c_int32), ("col_mem_util", ctypes.c_int32), ("alpha", ctypes.c_double),
+                ("q_extreme", ctypes.c_double)]
 
 
 class enova_train_params(ctypes.Structure):
@@ -98,6 +107,14 @@ def lib():
     L.enova_train_set_timing.argtypes = [P, I32]
     L.enova_train_kernel_times.argtypes = [P, P, P]
     L.enova_train_destroy.argtypes = [P]
+    L.enova_config_t_critical.argtypes = [D, I32, P]
+    L.enova_config_init.argtypes = [ctypes.POINTER(enova_config_params), ctypes.POINTER(P)]
+    L.enova_config_destroy.argtypes = [P]
+    L.enova_config_window_offsets.argtypes = [P, P, I32, P]
+    L.enova_config_scan.argtypes = [P, P, P, P, I32, I64, P, P, P, P, P, P, P]
+    L.enova_config_recommend.argtypes = [P, P, P, I32, P, P, P, P, P, P]
+    L.enova_config_set_timing.argtypes = [P, I32]
+    L.enova_config_kernel_time.argtypes = [P, P]
     for name in EXPORTS[:-2]:
         getattr(L, name).restype = st
     L.enova_status_str.argtypes = [st]
@@ -308,6 +325,80 @@ def enova_train_kernel_times(thandle):
 
 def enova_train_destroy(thandle):
     _check(lib().enova_train_destroy(ctypes.c_void_p(thandle)), "enova_train_destroy")
+
+
+def enova_config_t_critical(alpha, dof):
+    v = ctypes.c_double()
+    _check(lib().enova_config_t_critical(float(alpha), int(dof), ctypes.byref(v)), "enova_config_t_critical")
+    return v.value
+
+
+class ConfigScanner:
+    """Owns one configuration-scan handle (Section IV-A scans); methods call the C entry points."""
+
+    def __init__(self, metrics, window, stride, col_finished, col_running, col_exec_time, col_mem_util,
+                 dtype="f32", alpha=0.05, q_extreme=0.99):
+        self.params = enova_config_params(metrics=metrics, window=window, stride=stride,
+                                          dtype={"f32": ENOVA_F32, "bf16": ENOVA_BF16}[dtype],
+                                          col_finished=col_finished, col_running=col_running,
+                                          col_exec_time=col_exec_time, col_mem_util=col_mem_util,
+                                          alpha=alpha, q_extreme=q_extreme)
+        h = ctypes.c_void_p()
+        _check(lib().enova_config_init(ctypes.byref(self.params), ctypes.byref(h)), "enova_config_init")
+        self.handle = h.value
+
+    def window_offsets(self, stream_offsets_host):
+        so = np.ascontiguousarray(stream_offsets_host, dtype=np.int64)
+        out = np.zeros(len(so), np.int64)
+        _check(lib().enova_config_window_offsets(ctypes.c_void_p(self.handle), _hptr(so), len(so) - 1, _hptr(out)),
+               "enova_config_window_offsets")
+        return out
+
+    def scan(self, x, stream_offsets, window_offsets, n_windows, stream=None):
+        """Returns device tensors (intercept, slope, t, significant, mem_intercept, mem_slope)."""
+        import torch
+        dev = x.device
+        n = stream_offsets.numel() - 1
+        f = [torch.empty(max(n_windows, 1), dtype=torch.float32, device=dev)[:n_windows] for _ in range(5)]
+        sig = torch.empty(max(n_windows, 1), dtype=torch.uint8, device=dev)[:n_windows]
+        _check(lib().enova_config_scan(ctypes.c_void_p(self.handle), _dptr(x), _dptr(stream_offsets),
+                                       _dptr(window_offsets), n, int(n_windows), _dptr(f[0]), _dptr(f[1]),
+                                       _dptr(f[2]), _dptr(sig), _dptr(f[3]), _dptr(f[4]), _stream(stream)),
+               "enova_config_scan")
+        return f[0], f[1], f[2], sig, f[3], f[4]
+
+    def recommend(self, x, stream_offsets, stream=None):
+        """Returns device tensors (significant, n_limit, t_limit, max_num_seqs, gpu_memory)."""
+        import torch
+        dev = x.device
+        n = stream_offsets.numel() - 1
+        sig = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)[:n]
+        d = [torch.empty(max(n, 1), dtype=torch.float64, device=dev)[:n] for _ in range(4)]
+        _check(lib().enova_config_recommend(ctypes.c_void_p(self.handle), _dptr(x), _dptr(stream_offsets), n,
+                                            _dptr(sig), _dptr(d[0]), _dptr(d[1]), _dptr(d[2]), _dptr(d[3]),
+                                            _stream(stream)),
+               "enova_config_recommend")
+        return sig, d[0], d[1], d[2], d[3]
+
+    def set_timing(self, enable=True):
+        _check(lib().enova_config_set_timing(ctypes.c_void_p(self.handle), int(bool(enable))),
+               "enova_config_set_timing")
+
+    def kernel_time(self):
+        v = ctypes.c_double()
+        _check(lib().enova_config_kernel_time(ctypes.c_void_p(self.handle), ctypes.byref(v)), "enova_config_kernel_time")
+        return v.value
+
+    def close(self):
+        if self.handle:
+            _check(lib().enova_config_destroy(ctypes.c_void_p(self.handle)), "enova_config_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # ----------------------------------------------------------------------------- convenience

@@ -1,0 +1,314 @@
+// Configuration scans (Section IV-A, Eqs. (2)-(3)): per-window OLS fits with the slope's t-test,
+// and per-stream KDE quantiles of the last window. All statistics in fp64, every reduction in a
+// fixed order.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "config_internal.h"
+
+namespace enova {
+
+namespace {
+
+constexpr int kCfgThreads = 256;
+constexpr int kCfgMaxW = 4096;   // the per-stream kernel holds one window of four columns in LDS
+constexpr size_t kCfgScanLds = 48 * 1024;
+
+template <int DT>
+__device__ __forceinline__ float load_value(const void *x, int64_t idx)
+{
+    if constexpr (DT == ENOVA_BF16)
+        return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t *>(x)[idx]) << 16);
+    else
+        return static_cast<const float *>(x)[idx];
+}
+
+// One thread per window: two passes over the window's samples in LDS (means, then centred sums).
+template <int DT>
+__global__ __launch_bounds__(kCfgThreads) void k_cfg_scan(CfgParams c, int nb, const void *__restrict__ x,
+                                                          const int64_t *__restrict__ soff,
+                                                          const int64_t *__restrict__ woff,
+                                                          const int64_t *__restrict__ tile_off,
+                                                          const int *__restrict__ tile_stream, CfgScanOut o)
+{
+    extern __shared__ float sm[];
+    const int s = tile_stream[blockIdx.x];
+    if (s < 0)
+        return;
+    const int64_t k0 = (static_cast<int64_t>(blockIdx.x) - tile_off[s]) * nb;
+    const int64_t nwin = woff[s + 1] - woff[s];
+    const int nw = static_cast<int>(nwin - k0 < nb ? nwin - k0 : nb);
+    const int W = c.W, S = c.S, M = c.M;
+    const int seg = (nw - 1) * S + W;
+    const int pitch = (nb - 1) * S + W;
+    float *xr = sm, *xf = sm + pitch, *xm = sm + 2 * pitch;
+    const int64_t row0 = soff[s] + k0 * S;
+    for (int i = threadIdx.x; i < seg; i += kCfgThreads) {
+        const int64_t base = (row0 + i) * M;
+        xr[i] = load_value<DT>(x, base + c.col_r);
+        xf[i] = load_value<DT>(x, base + c.col_f);
+        xm[i] = load_value<DT>(x, base + c.col_m);
+    }
+    __syncthreads();
+    const int w = threadIdx.x;
+    if (w >= nw)
+        return;
+    const float *r = xr + w * S, *f = xf + w * S, *m = xm + w * S;
+    double sr = 0.0, sf = 0.0, smu = 0.0;
+    for (int j = 0; j < W; ++j) {
+        sr += r[j];
+        sf += f[j];
+        smu += m[j];
+    }
+    const double rm = sr / W, fm = sf / W, mm = smu / W;
+    double sxx = 0.0, sxy = 0.0, syy = 0.0, sxz = 0.0;
+    for (int j = 0; j < W; ++j) {
+        const double dx = r[j] - rm, dy = f[j] - fm, dz = m[j] - mm;
+        sxx = fma(dx, dx, sxx);
+        sxy = fma(dx, dy, sxy);
+        syy = fma(dy, dy, syy);
+        sxz = fma(dx, dz, sxz);
+    }
+    double a, b, t, g0, g1;
+    if (sxx == 0.0) {
+        a = fm;
+        b = 0.0;
+        t = 0.0;
+        g0 = mm;
+        g1 = 0.0;
+    } else {
+        b = sxy / sxx;
+        a = fm - b * rm;
+        const double rss = fmax(syy - b * sxy, 0.0);
+        t = b == 0.0 ? 0.0 : (rss == 0.0 ? copysign(HUGE_VAL, b) : b * sqrt((W - 2) * sxx / rss));
+        g1 = sxz / sxx;
+        g0 = mm - g1 * rm;
+    }
+    const int64_t out = woff[s] + k0 + w;
+    if (o.a)
+        o.a[out] = static_cast<float>(a);
+    if (o.b)
+        o.b[out] = static_cast<float>(b);
+    if (o.t)
+        o.t[out] = static_cast<float>(t);
+    if (o.sig)
+        o.sig[out] = fabs(t) > c.t_crit ? 1 : 0;
+    if (o.g0)
+        o.g0[out] = static_cast<float>(g0);
+    if (o.g1)
+        o.g1[out] = static_cast<float>(g1);
+}
+
+// Fixed-order block sum (tree over the threads' partials); every thread gets the total.
+__device__ double block_sum(double v, double *red)
+{
+    red[threadIdx.x] = v;
+    __syncthreads();
+    for (int w = kCfgThreads / 2; w >= 1; w >>= 1) {
+        if (threadIdx.x < w)
+            red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const double r = red[0];
+    __syncthreads();
+    return r;
+}
+
+// Linearly interpolated sample quantile of sorted v[0..n).
+__device__ double sorted_quantile(const float *v, int n, double p)
+{
+    const double h = (n - 1) * p;
+    const int lo = static_cast<int>(floor(h));
+    const int hi = lo + 1 < n ? lo + 1 : n - 1;
+    return static_cast<double>(v[lo]) + (h - lo) * (static_cast<double>(v[hi]) - static_cast<double>(v[lo]));
+}
+
+// Quantile at level q of the Gaussian KDE of v[0..n) (Silverman's bandwidth), by bisection on its
+// distribution function. `sorted` is scratch of np2 floats (np2: a power of two >= n).
+__device__ double kde_quantile(const float *v, int n, int np2, double q, float *sorted, double *red)
+{
+    for (int i = threadIdx.x; i < np2; i += kCfgThreads)
+        sorted[i] = i < n ? v[i] : INFINITY;
+    __syncthreads();
+    // bitonic sort, ascending
+    for (int k = 2; k <= np2; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < np2; i += kCfgThreads) {
+                const int l = i ^ j;
+                if (l > i) {
+                    const bool up = (i & k) == 0;
+                    const float x = sorted[i], y = sorted[l];
+                    if ((x > y) == up) {
+                        sorted[i] = y;
+                        sorted[l] = x;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    double part = 0.0;
+    for (int i = threadIdx.x; i < n; i += kCfgThreads)
+        part += v[i];
+    const double mean = block_sum(part, red) / n;
+    part = 0.0;
+    for (int i = threadIdx.x; i < n; i += kCfgThreads) {
+        const double d = v[i] - mean;
+        part = fma(d, d, part);
+    }
+    const double ss = block_sum(part, red);
+    const double sd = n > 1 ? sqrt(ss / (n - 1)) : 0.0;
+    const double iqr = sorted_quantile(sorted, n, 0.75) - sorted_quantile(sorted, n, 0.25);
+    const double spread = iqr > 0.0 ? fmin(sd, iqr / 1.34) : sd;
+    const double h = 0.9 * spread * pow(static_cast<double>(n), -0.2);
+    if (h == 0.0)
+        return v[0];
+    double lo = sorted[0] - 10.0 * h, hi = sorted[n - 1] + 10.0 * h;
+    const double scale = 1.0 / (h * 1.4142135623730951);
+    for (int it = 0; it < 200; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        if (mid <= lo || mid >= hi)
+            break;
+        part = 0.0;
+        for (int i = threadIdx.x; i < n; i += kCfgThreads)
+            part += 0.5 * erfc(-(mid - v[i]) * scale);
+        const double F = block_sum(part, red) / n;
+        if (F < q)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return 0.5 * (lo + hi);
+}
+
+// One block per stream: the last window's fits, the regime and the KDE limits.
+template <int DT>
+__global__ __launch_bounds__(kCfgThreads) void k_cfg_stream(CfgParams c, const void *__restrict__ x,
+                                                            const int64_t *__restrict__ soff, CfgStreamOut o)
+{
+    __shared__ float vr[kCfgMaxW], vf[kCfgMaxW], vt[kCfgMaxW], vm[kCfgMaxW], sorted[kCfgMaxW];
+    __shared__ double red[kCfgThreads];
+    const int s = blockIdx.x;
+    const int W = c.W, S = c.S, M = c.M;
+    const int64_t T = soff[s + 1] - soff[s];
+    const int64_t nw = T >= W ? (T - W) / S + 1 : 0;
+    if (nw == 0) {
+        if (threadIdx.x == 0) {
+            if (o.sig)
+                o.sig[s] = 0;
+            if (o.n_limit)
+                o.n_limit[s] = NAN;
+            if (o.t_limit)
+                o.t_limit[s] = NAN;
+            if (o.max_num_seqs)
+                o.max_num_seqs[s] = NAN;
+            if (o.gpu_memory)
+                o.gpu_memory[s] = NAN;
+        }
+        return;
+    }
+    const int64_t row0 = soff[s] + (nw - 1) * S;
+    for (int i = threadIdx.x; i < W; i += kCfgThreads) {
+        const int64_t base = (row0 + i) * M;
+        vr[i] = load_value<DT>(x, base + c.col_r);
+        vf[i] = load_value<DT>(x, base + c.col_f);
+        vt[i] = load_value<DT>(x, base + c.col_t);
+        vm[i] = load_value<DT>(x, base + c.col_m);
+    }
+    __syncthreads();
+    double p0 = 0.0, p1 = 0.0, p2 = 0.0;
+    for (int i = threadIdx.x; i < W; i += kCfgThreads) {
+        p0 += vr[i];
+        p1 += vf[i];
+        p2 += vm[i];
+    }
+    const double rm = block_sum(p0, red) / W, fm = block_sum(p1, red) / W, mm = block_sum(p2, red) / W;
+    double q0 = 0.0, q1 = 0.0, q2 = 0.0, q3 = 0.0;
+    for (int i = threadIdx.x; i < W; i += kCfgThreads) {
+        const double dx = vr[i] - rm, dy = vf[i] - fm, dz = vm[i] - mm;
+        q0 = fma(dx, dx, q0);
+        q1 = fma(dx, dy, q1);
+        q2 = fma(dy, dy, q2);
+        q3 = fma(dx, dz, q3);
+    }
+    const double sxx = block_sum(q0, red), sxy = block_sum(q1, red), syy = block_sum(q2, red),
+                 sxz = block_sum(q3, red);
+    double t = 0.0, g0 = mm, g1 = 0.0;
+    if (sxx != 0.0) {
+        const double b = sxy / sxx;
+        const double rss = fmax(syy - b * sxy, 0.0);
+        t = b == 0.0 ? 0.0 : (rss == 0.0 ? copysign(HUGE_VAL, b) : b * sqrt((W - 2) * sxx / rss));
+        g1 = sxz / sxx;
+        g0 = mm - g1 * rm;
+    }
+    const bool sig = fabs(t) > c.t_crit;
+    const double q = sig ? c.q_extreme : 0.5;
+    int np2 = 1;
+    while (np2 < W)
+        np2 <<= 1;
+    const double nl = kde_quantile(vf, W, np2, q, sorted, red);
+    const double tl = kde_quantile(vt, W, np2, q, sorted, red);
+    if (threadIdx.x == 0) {
+        const double mns = nl * tl;
+        if (o.sig)
+            o.sig[s] = sig ? 1 : 0;
+        if (o.n_limit)
+            o.n_limit[s] = nl;
+        if (o.t_limit)
+            o.t_limit[s] = tl;
+        if (o.max_num_seqs)
+            o.max_num_seqs[s] = mns;
+        if (o.gpu_memory)
+            o.gpu_memory[s] = g0 + g1 * mns;
+    }
+}
+
+}  // namespace
+
+int cfg_scan_windows_per_block(const CfgParams &c)
+{
+    for (int nb = kCfgThreads; nb >= 1; nb >>= 1)
+        if (cfg_scan_lds_bytes(c, nb) <= kCfgScanLds)
+            return nb;
+    return 0;
+}
+
+size_t cfg_scan_lds_bytes(const CfgParams &c, int nb)
+{
+    return 3 * sizeof(float) * (static_cast<size_t>(nb - 1) * c.S + c.W);
+}
+
+hipError_t launch_cfg_scan(const CfgParams &c, int nb, const void *x, const int64_t *soff, const int64_t *woff,
+                           const int64_t *tile_off, const int *tile_stream, int64_t grid, const CfgScanOut &o,
+                           hipStream_t st)
+{
+    if (grid <= 0)
+        return hipSuccess;
+    const size_t lds = cfg_scan_lds_bytes(c, nb);
+    if (c.dtype == ENOVA_BF16)
+        hipLaunchKernelGGL(k_cfg_scan<ENOVA_BF16>, dim3(static_cast<unsigned>(grid)), dim3(kCfgThreads), lds, st, c,
+                           nb, x, soff, woff, tile_off, tile_stream, o);
+    else
+        hipLaunchKernelGGL(k_cfg_scan<ENOVA_F32>, dim3(static_cast<unsigned>(grid)), dim3(kCfgThreads), lds, st, c,
+                           nb, x, soff, woff, tile_off, tile_stream, o);
+    return hipGetLastError();
+}
+
+hipError_t launch_cfg_stream(const CfgParams &c, const void *x, const int64_t *soff, int n, const CfgStreamOut &o,
+                             hipStream_t st)
+{
+    if (n <= 0)
+        return hipSuccess;
+    if (c.W > kCfgMaxW)
+        return hipErrorInvalidValue;
+    if (c.dtype == ENOVA_BF16)
+        hipLaunchKernelGGL(k_cfg_stream<ENOVA_BF16>, dim3(static_cast<unsigned>(n)), dim3(kCfgThreads), 0, st, c, x,
+                           soff, o);
+    else
+        hipLaunchKernelGGL(k_cfg_stream<ENOVA_F32>, dim3(static_cast<unsigned>(n)), dim3(kCfgThreads), 0, st, c, x,
+                           soff, o);
+    return hipGetLastError();
+}
+
+}  // namespace enova

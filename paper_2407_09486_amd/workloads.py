@@ -440,3 +440,46 @@ def training_batch(cfg: Config, batch: int, seed: int = 0, anomaly_frac: float =
     labels = np.where(anomalous, -1.0, 1.0).astype(np.float32)
     eps = rng.standard_normal((batch, L)).astype(np.float32)
     return TrainBatch(V=np.ascontiguousarray(x.reshape(batch, W * M), dtype=np.float32), labels=labels, eps=eps)
+
+
+# ----------------------------------------------------------------------------- configuration series
+CONFIG_METRICS = ("n_f", "n_r", "n_a", "n_p", "t_r", "m_u", "g_u")   # Table III order
+
+
+def config_series(n_streams: int, T: int, seed: int = 0) -> Workload:
+    """Serving metrics of n_streams services over T steps (one step = one minute), Table III order.
+
+    Arrivals n^a ~ Poisson(lambda_t), lambda_t = base (1 + 0.5 sin(2 pi (t + phase) / 1440)).
+    Even streams have capacity C = 3 base (never saturated), odd streams C = 0.8 base (saturated
+    around the daily peak). Execution time t^r = t0 (1 + 0.5 min(lambda_t / C, 1.5)) LogNormal(0, 0.05).
+    Below capacity the running requests n^r ~ Poisson(lambda_t t^r) and the finished rate follows
+    them (Little's law), n^f = n^r / t^r + N(0, 0.02 base); at capacity n^r ~ Poisson(C t^r)
+    fluctuates around the concurrency limit and n^f = C + N(0, 0.05 C) does not follow it.
+    Pending n^p ~ Poisson(5 max(0, lambda_t - C)); GPU memory use
+    m^u = 0.05 + 0.9 min(1, n^r / R) + N(0, 0.005) with R = 2 C t0; GPU use
+    g^u = logistic(4 (lambda_t / C - 0.7)) + N(0, 0.02), clipped to [0, 1].
+    """
+    rng = np.random.default_rng(seed)
+    x = np.empty((n_streams * T, len(CONFIG_METRICS)), np.float32)
+    t = np.arange(T, dtype=np.float64)
+    for s in range(n_streams):
+        base = rng.uniform(20.0, 80.0)
+        phase = rng.uniform(0.0, 1440.0)
+        cap = base * (3.0 if s % 2 == 0 else 0.8)
+        t0 = rng.uniform(1.0, 4.0)
+        lam = base * (1.0 + 0.5 * np.sin(2.0 * math.pi * (t + phase) / 1440.0))
+        sat = lam >= cap
+        n_a = rng.poisson(lam)
+        t_r = t0 * (1.0 + 0.5 * np.minimum(lam / cap, 1.5)) * rng.lognormal(0.0, 0.05, T)
+        n_r = rng.poisson(np.minimum(lam, cap) * t_r).astype(np.float64)
+        n_f = np.where(sat, cap + rng.normal(0.0, 0.05 * cap, T), n_r / t_r + rng.normal(0.0, 0.02 * base, T))
+        n_p = rng.poisson(5.0 * np.maximum(0.0, lam - cap))
+        m_u = 0.05 + 0.9 * np.minimum(1.0, n_r / (2.0 * cap * t0)) + rng.normal(0.0, 0.005, T)
+        g_u = np.clip(1.0 / (1.0 + np.exp(-4.0 * (lam / cap - 0.7))) + rng.normal(0.0, 0.02, T), 0.0, 1.0)
+        x[s * T:(s + 1) * T] = np.stack([n_f, n_r, n_a, n_p, t_r, m_u, g_u], axis=1)
+    offs = np.arange(n_streams + 1, dtype=np.int64) * T
+    cfg = Config(name="config", n_streams=n_streams, metrics=len(CONFIG_METRICS), t_len=T, t_min=0, t_max=0,
+                 window=64, stride=1, hidden=1, latent=1, dtype="f32", act="relu", ref_frac=0.5,
+                 kind="config_series", data_seed=seed, weight_seed=0)
+    return Workload(cfg=cfg, stream_offsets=offs, x=x, x_bits=None,
+                    labels=np.zeros(n_streams * T, np.uint8), streams=np.arange(n_streams))

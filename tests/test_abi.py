@@ -135,3 +135,34 @@ def test_binding_refuses_host_tensors():
     import torch
     with pytest.raises(ValueError):
         binding._dptr(torch.zeros(3))
+
+
+def test_config_t_critical_matches_scipy():
+    _ensure_built()
+    from scipy import stats
+    for alpha in (0.05, 0.01, 0.2):
+        for dof in (1, 2, 3, 10, 62, 1000, 100000):
+            v = binding.enova_config_t_critical(alpha, dof)
+            # lgamma of large arguments limits the library to ~1e-10 relative at dof ~ 1e5
+            assert v == pytest.approx(stats.t.ppf(1 - alpha / 2, dof), rel=1e-9)
+
+
+@pytest.mark.parametrize("over", [dict(window=2), dict(window=4097), dict(stride=0), dict(metrics=0),
+                                  dict(col_running=7), dict(col_mem_util=-1), dict(alpha=0.0), dict(alpha=1.0),
+                                  dict(q_extreme=1.0), dict(dtype=5)])
+def test_config_init_rejects_bad_params(over):
+    _ensure_built()
+    L = binding.lib()
+    base = dict(metrics=7, window=64, stride=1, dtype=binding.ENOVA_F32, col_finished=0, col_running=1,
+                col_exec_time=4, col_mem_util=5, alpha=0.05, q_extreme=0.99)
+    base.update(over)
+    p = binding.enova_config_params(**base)
+    h = ctypes.c_void_p()
+    assert L.enova_config_init(ctypes.byref(p), ctypes.byref(h)) == binding.ENOVA_EINVAL and not h.value
+    assert L.enova_config_init(None, None) == binding.ENOVA_EINVAL
+    assert L.enova_config_scan(None, None, None, None, 1, 1, None, None, None, None, None, None,
+                               None) == binding.ENOVA_EINVAL
+    assert L.enova_config_recommend(None, None, None, 1, None, None, None, None, None, None) == binding.ENOVA_EINVAL
+    v = ctypes.c_double()
+    assert L.enova_config_t_critical(0.05, 0, ctypes.byref(v)) == binding.ENOVA_EINVAL
+    assert L.enova_config_destroy(None) == binding.ENOVA_OK
