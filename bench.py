@@ -16,6 +16,10 @@ With --mode train it measures one semi-supervised ELBO training step of the conf
 shape (Eq. (9): forward, PI-controlled KL weight, backward, Adam) on a batch of --batch labelled
 windows resident in HBM (one step is one training step).
 
+With --mode variants it measures the detector-output variants on the config's workload: every
+window normalised against itself (--norm window, default) or its reference prefix, with its KL
+score, md, per-metric md vector and reconstruction error (one step is one call).
+
 With --mode config it measures the configuration scans (Section IV-A, Eqs. (2)-(3)) over 1024
 services x 16384 one-minute steps of the Table III metrics: every window's OLS fits and t-test,
 then each service's KDE limits and configuration (one step is both calls).
@@ -112,7 +116,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="also run a plain device copy of this size (counter calibration)")
-    ap.add_argument("--mode", choices=["batch", "stream", "train", "config"], default="batch")
+    ap.add_argument("--mode", choices=["batch", "stream", "train", "config", "variants"], default="batch")
+    ap.add_argument("--norm", choices=["window", "reference"], default="window",
+                    help="normalisation of --mode variants")
     ap.add_argument("--batch", type=int, default=8192, help="windows per training step (--mode train)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -135,6 +141,9 @@ def main():
         return
     if args.mode == "config":
         config_main(args)
+        return
+    if args.mode == "variants":
+        variants_main(args, cfg)
         return
     t_gen = time.perf_counter()
     w = wl.generate(cfg)
@@ -472,6 +481,107 @@ def train_main(args, cfg):
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = train_cpu_baseline(cfg, p0, batch, margin)
     tr.close()
+    print(json.dumps(out), flush=True)
+
+
+def variants_flops_per_window(cfg) -> int:
+    """Matrix-product flops of one window's variants: encoder 2HD, heads 4LH, decoder hidden 2LH,
+    decoder output 2DH."""
+    H, L, D = cfg.hidden, cfg.latent, cfg.d
+    return 4 * H * D + 6 * L * H
+
+
+def variants_cpu_baseline(cfg, w, work, norm, budget_s=10.0):
+    import numpy as np
+
+    from oracle import variants as ov
+    wts = {k: np.asarray(getattr(w, k), np.float64) for k in
+           ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")}
+    import oracle
+    x = work.values_f64()
+    offs = work.stream_offsets
+    nw = oracle.window_count(np.diff(offs), cfg.window, cfg.stride)
+    n, t0 = 0, time.perf_counter()
+    k = 0
+    while time.perf_counter() - t0 < budget_s and k < int(nw.max()):
+        pairs = [(s, k) for s in range(min(64, work.n_streams)) if k < nw[s]]
+        r = ov.score_ext(x, offs, window=cfg.window, stride=cfg.stride, weights=wts, act=cfg.act, norm=norm,
+                         ref_frac=cfg.ref_frac, bf16=cfg.dtype == "bf16", pairs=pairs)
+        n += len(r["score"])
+        k += 1
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 1), "unit": "windows/s", "cores": 1, "kind": "oracle",
+            "sample": f"windows 0..{k - 1} of streams 0..63 ({n} windows, {dt:.1f} s, fp64, one core)"}
+
+
+def variants_main(args, cfg):
+    import numpy as np
+    import torch
+
+    from paper_2407_09486_amd import binding
+    from paper_2407_09486_amd import workloads as wl
+
+    t_gen = time.perf_counter()
+    work = wl.generate(cfg)
+    w = wl.make_weights(cfg)
+    print(f"[bench] variants {cfg.name}: generated in {time.perf_counter() - t_gen:.1f} s", file=sys.stderr,
+          flush=True)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    det = binding.Detector(cfg.metrics, cfg.window, cfg.stride, cfg.hidden, binding.weights_for_library(w, cfg.dtype),
+                           latent=cfg.latent, dtype=cfg.dtype, act=cfg.act, ref_frac=cfg.ref_frac)
+    if cfg.dtype == "bf16":
+        x = torch.from_numpy(work.x_bits.view(np.int16)).to(dev)
+    else:
+        x = torch.from_numpy(work.x).to(dev)
+    so = torch.from_numpy(work.stream_offsets).to(dev)
+    woff = det.window_offsets(work.stream_offsets)
+    wo = torch.from_numpy(woff).to(dev)
+    N = int(woff[-1])
+    M = cfg.metrics
+    sc = torch.empty(N, dtype=torch.float32, device=dev)
+    md = torch.empty(N, dtype=torch.float32, device=dev)
+    mdm = torch.empty((N, M), dtype=torch.float32, device=dev)
+    rec = torch.empty(N, dtype=torch.float32, device=dev)
+    norm = {"window": binding.ENOVA_NORM_WINDOW, "reference": binding.ENOVA_NORM_REFERENCE}[args.norm]
+
+    def step():
+        binding.enova_detect_score_ext(det.handle, x, so, wo, work.n_streams, N, None, None, norm, sc, md, mdm, rec)
+    for _ in range(args.warmup):
+        step()
+    binding.enova_detect_set_timing(det.handle, True)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    k_ms = []
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+        k_ms.append(binding.enova_detect_ext_time(det.handle))
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    km = float(np.mean(k_ms))
+    fpw = variants_flops_per_window(cfg)
+    achieved = fpw * N / (km / 1e3) / 1e12
+    out = {
+        "metric": "windows evaluated/sec (KL score, md, per-metric md vector, reconstruction error)",
+        "value": round(N / (ms / 1e3), 1), "unit": "windows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded generators standing in for the paper's industrial series)",
+        "config": {"workload": f"variants on {cfg.name}: {work.n_streams} streams x {M} metrics, W={cfg.window} "
+                               f"S={cfg.stride}, H={cfg.hidden}, {cfg.dtype} ({N} windows), {args.norm} normalisation",
+                   "windows": N},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_TFLOPS["f32"], "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_TFLOPS["f32"], 4), "traffic": None,
+                     "kernel": "the whole variant pass (staging, 4 products, latent, reductions)",
+                     "kernel_ms": round(km, 4), "flops_per_window": fpw, "windows_per_launch": N},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = variants_cpu_baseline(cfg, w, work, args.norm)
+    det.close()
     print(json.dumps(out), flush=True)
 
 

@@ -298,6 +298,31 @@ enova_status enova_train_kernel_times(enova_trainer t, double *gemm_ms, double *
 enova_status enova_train_destroy(enova_trainer t);
 
 /*
+ * Detector-output variants (Section IV-B). The windows are evaluated densely, in chunks: each is
+ * normalised against its stream's reference statistics (ENOVA_NORM_REFERENCE, as
+ * enova_detect_score) or against itself (ENOVA_NORM_WINDOW: per metric the window's own mean and
+ * population std, a std <= 1e-6 max(1, |mean|) counting as 1 -- the literal reading of
+ * per-window normalisation); then the encoder, the KL score, and the decoder's full output
+ * m' = Wd2 act(Wd1 mu + bd1) + bd2 at z = mu. Per window: out_scores (the KL score),
+ * out_md = mean_j (v_j - m'_j), out_md_metric [N][M] = mean over the W steps of (v - m') per
+ * metric, out_recon_err = mean_j (v_j - m'_j)^2 (device outputs; any may be NULL). ref_mean /
+ * ref_std as in enova_detect_score (NULL: computed; ignored for ENOVA_NORM_WINDOW). M <= 4096.
+ * The products run in fp32 on the matrix cores (x and W1 of a bf16 detector are bf16 values;
+ * v is rounded to bf16 as in enova_detect_score). Asynchronous. Errors: EINVAL, EUNSUPPORTED,
+ * ENOMEM, EHIP.
+ */
+typedef enum { ENOVA_NORM_REFERENCE = 0, ENOVA_NORM_WINDOW = 1 } enova_norm;
+
+enova_status enova_detect_score_ext(enova_detector det, const void *x, const int64_t *stream_offsets,
+                                    const int64_t *window_offsets, int32_t n_streams, int64_t n_windows,
+                                    const float *ref_mean, const float *ref_std, int32_t norm, float *out_scores,
+                                    float *out_md, float *out_md_metric, float *out_recon_err, hipStream_t stream);
+
+/* With timing enabled (enova_detect_set_timing), the last enova_detect_score_ext call's duration
+ * from its first to its last kernel, milliseconds. */
+enova_status enova_detect_ext_time(enova_detector det, double *ms);
+
+/*
  * Configuration scans (Section IV-A, Eqs. (2)-(3), Table III) over the same monitoring series.
  * Whether the finished-request rate n^f still depends on the number of running requests n^r is
  * decided per window by an ordinary-least-squares fit n^f = a + b n^r and a two-sided t-test of

@@ -35,7 +35,8 @@ def window_stats(xw):
 def score_ext(x, stream_offsets, *, window, stride, weights, act="relu", norm="reference", ref_frac=0.5,
               bf16=False, ref_mean=None, ref_std=None, pairs=None):
     """Variants of every window (or of the (stream, k) pairs given). Returns dict of arrays:
-    score, md, md_metric [., M], recon (window order = stream order, then window index)."""
+    score, md, md_metric [., M], recon, and scale = mean|v| + mean|m'| (the magnitude the mean
+    differences are measured against); window order = stream order, then window index."""
     x = np.asarray(x, np.float64)
     offs = np.asarray(stream_offsets, np.int64)
     n = len(offs) - 1
@@ -49,7 +50,7 @@ def score_ext(x, stream_offsets, *, window, stride, weights, act="relu", norm="r
             rs = np.asarray(ref_std, np.float64).reshape(n, M)
     if pairs is None:
         pairs = [(s, k) for s in range(n) for k in range(int(window_count(int(offs[s + 1] - offs[s]), W, S)))]
-    out = {"score": [], "md": [], "md_metric": [], "recon": []}
+    out = {"score": [], "md": [], "md_metric": [], "recon": [], "scale": []}
     for s, k in pairs:
         xs = x[offs[s]:offs[s + 1]]
         if norm == "window":
@@ -62,6 +63,7 @@ def score_ext(x, stream_offsets, *, window, stride, weights, act="relu", norm="r
         out["md"].append(d.mean())
         out["md_metric"].append(d.reshape(W, M).mean(axis=0))
         out["recon"].append((d * d).mean())
+        out["scale"].append(np.abs(dbg["v"]).mean() + np.abs(dbg["mrec"]).mean())
     res = {k: np.asarray(v, np.float64) for k, v in out.items()}
     if res["md_metric"].size == 0:
         res["md_metric"] = np.zeros((0, M))

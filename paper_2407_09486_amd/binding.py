@@ -28,7 +28,7 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_stream_state", "enova_stream_kernel_times", "enova_stream_destroy",
            "enova_train_init", "enova_train_step", "enova_train_params_get", "enova_train_grads_get",
            "enova_train_set_timing", "enova_train_kernel_times", "enova_train_destroy",
-           "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
+           "enova_detect_score_ext", "enova_detect_ext_time", "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
            "enova_config_scan", "enova_config_recommend", "enova_config_set_timing", "enova_config_kernel_time", "enova_status_str", "enova_last_error"]
 
 
@@ -107,6 +107,8 @@ def lib():
     L.enova_train_set_timing.argtypes = [P, I32]
     L.enova_train_kernel_times.argtypes = [P, P, P]
     L.enova_train_destroy.argtypes = [P]
+    L.enova_detect_score_ext.argtypes = [P, P, P, P, I32, I64, P, P, I32, P, P, P, P, P]
+    L.enova_detect_ext_time.argtypes = [P, P]
     L.enova_config_t_critical.argtypes = [D, I32, P]
     L.enova_config_init.argtypes = [ctypes.POINTER(enova_config_params), ctypes.POINTER(P)]
     L.enova_config_destroy.argtypes = [P]
@@ -327,6 +329,24 @@ def enova_train_destroy(thandle):
     _check(lib().enova_train_destroy(ctypes.c_void_p(thandle)), "enova_train_destroy")
 
 
+ENOVA_NORM_REFERENCE, ENOVA_NORM_WINDOW = 0, 1
+
+
+def enova_detect_score_ext(handle, x, stream_offsets, window_offsets, n_streams, n_windows, ref_mean, ref_std, norm,
+                           out_scores=None, out_md=None, out_md_metric=None, out_recon=None, stream=None):
+    _check(lib().enova_detect_score_ext(ctypes.c_void_p(handle), _dptr(x), _dptr(stream_offsets),
+                                        _dptr(window_offsets), int(n_streams), int(n_windows), _dptr(ref_mean),
+                                        _dptr(ref_std), int(norm), _dptr(out_scores), _dptr(out_md),
+                                        _dptr(out_md_metric), _dptr(out_recon), _stream(stream)),
+           "enova_detect_score_ext")
+
+
+def enova_detect_ext_time(handle):
+    v = ctypes.c_double()
+    _check(lib().enova_detect_ext_time(ctypes.c_void_p(handle), ctypes.byref(v)), "enova_detect_ext_time")
+    return v.value
+
+
 def enova_config_t_critical(alpha, dof):
     v = ctypes.c_double()
     _check(lib().enova_config_t_critical(float(alpha), int(dof), ctypes.byref(v)), "enova_config_t_critical")
@@ -450,6 +470,20 @@ class Detector:
         enova_detect_score(self.handle, x, stream_offsets, window_offsets, n, n_windows, ref_mean, ref_std,
                            threshold, scores, mdv, fl, stream)
         return scores, mdv, fl
+
+    def score_ext(self, x, stream_offsets, window_offsets, n_windows, norm="reference", ref_mean=None,
+                  ref_std=None, stream=None):
+        """Output variants: returns device tensors (scores, md, md_metric [N, M], recon_err)."""
+        import torch
+        dev = x.device
+        n = stream_offsets.numel() - 1
+        M = self.cfg.metrics
+        f = [torch.empty(max(n_windows, 1), dtype=torch.float32, device=dev)[:n_windows] for _ in range(3)]
+        mdm = torch.empty((max(n_windows, 1), M), dtype=torch.float32, device=dev)[:n_windows]
+        enova_detect_score_ext(self.handle, x, stream_offsets, window_offsets, n, n_windows, ref_mean, ref_std,
+                               {"reference": ENOVA_NORM_REFERENCE, "window": ENOVA_NORM_WINDOW}[norm], f[0], f[1],
+                               mdm, f[2], stream)
+        return f[0], f[1], mdm, f[2]
 
     def threshold(self, scores, stream_offsets, window_offsets, level=0.98, q=1e-3, flags=False,
                   stream=None):

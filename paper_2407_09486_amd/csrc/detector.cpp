@@ -14,6 +14,7 @@
 #include "enova_detect.h"
 #include "internal.h"
 #include "stream_internal.h"
+#include "variants_internal.h"
 
 namespace {
 thread_local std::string g_last_error;
@@ -92,10 +93,19 @@ struct enova_detector_s {
     size_t blk_cap = 0;
     double *gx = nullptr;         // evaluation points of the GPD likelihood sums, then the sums
     size_t gx_cap = 0;
+    // dense fp32 weights of the output variants: W1 [H][D], [Wmu; Wlv] [2L][H], [bmu | blv] [2L],
+    // Wd1 [H][L], Wd2 [D][H], bd2 [D] (one allocation)
+    float *dense = nullptr;
+    float *d_w1 = nullptr, *d_wml = nullptr, *d_bml = nullptr, *d_wd1 = nullptr, *d_wd2 = nullptr,
+          *d_bd2 = nullptr;
+    // workspace of the output variants (one chunk of windows)
+    float *ext_ws = nullptr;
+    size_t ext_ws_cap = 0;        // floats
     // timing
     bool timing = false;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
-    bool ran_stats = false, ran_score = false;
+    hipEvent_t ext_ev[2] = {nullptr, nullptr};
+    bool ran_stats = false, ran_score = false, ran_ext = false;
 };
 
 namespace enova {
@@ -198,11 +208,14 @@ void free_detector(enova_detector d)
     if (!d)
         return;
     void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->tile_map, d->cal, d->hist,
-                    d->peaks, d->blk, d->gx};
+                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
     for (hipEvent_t e : d->ev)
+        if (e)
+            (void)hipEventDestroy(e);
+    for (hipEvent_t e : d->ext_ev)
         if (e)
             (void)hipEventDestroy(e);
     delete d;
@@ -470,6 +483,41 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
     d->whp = d->small + o_whp;
     d->wd1p = d->small + o_wd1p;
 
+    {
+        // dense fp32 copies for the output variants (16-byte aligned sub-arrays)
+        size_t od = 0;
+        auto takd = [&od](size_t n) {
+            const size_t at = od;
+            od += (n + 3) / 4 * 4;
+            return at;
+        };
+        const size_t p_w1 = takd(static_cast<size_t>(H) * D), p_wml = takd(2 * static_cast<size_t>(L) * H),
+                     p_bml = takd(2 * static_cast<size_t>(L)), p_wd1 = takd(static_cast<size_t>(H) * L),
+                     p_wd2 = takd(static_cast<size_t>(D) * H), p_bd2 = takd(D);
+        std::vector<float> dn(od, 0.0f);
+        for (int h = 0; h < H; ++h)
+            for (int j = 0; j < D; ++j)
+                dn[p_w1 + static_cast<size_t>(h) * D + j] = w1v(h, j);
+        std::memcpy(&dn[p_wml], w->wmu, sizeof(float) * L * H);
+        std::memcpy(&dn[p_wml + static_cast<size_t>(L) * H], w->wlv, sizeof(float) * L * H);
+        std::memcpy(&dn[p_bml], w->bmu, sizeof(float) * L);
+        std::memcpy(&dn[p_bml + L], w->blv, sizeof(float) * L);
+        std::memcpy(&dn[p_wd1], w->wd1, sizeof(float) * H * L);
+        std::memcpy(&dn[p_wd2], w->wd2, sizeof(float) * static_cast<size_t>(D) * H);
+        std::memcpy(&dn[p_bd2], w->bd2, sizeof(float) * D);
+        st = dev_upload(&d->dense, dn.data(), dn.size() * sizeof(float));
+        if (st != ENOVA_OK) {
+            free_detector(d);
+            return st;
+        }
+        d->d_w1 = d->dense + p_w1;
+        d->d_wml = d->dense + p_wml;
+        d->d_bml = d->dense + p_bml;
+        d->d_wd1 = d->dense + p_wd1;
+        d->d_wd2 = d->dense + p_wd2;
+        d->d_bd2 = d->dense + p_bd2;
+    }
+
     if (d->kind == 1) {
         // transposed W1 [D][H] in the storage type
         const size_t esz = bf ? 2 : 4;
@@ -689,6 +737,130 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
     if (det->timing)
         (void)hipEventRecord(det->ev[3], stream);
     det->ran_score = true;
+    return ENOVA_OK;
+}
+
+// Windows per chunk of the output variants: V and the decoder output ([chunk][D] each) within
+// about 512 MiB.
+static int ext_chunk(const Geometry &g, int64_t n_windows)
+{
+    int64_t c = (int64_t{1} << 26) / g.D;
+    c = std::max<int64_t>(256, std::min<int64_t>(c, 65536));
+    return static_cast<int>(std::min<int64_t>(c, std::max<int64_t>(n_windows, 1)));
+}
+
+enova_status enova_detect_score_ext(enova_detector det, const void *x, const int64_t *soff, const int64_t *woff,
+                                    int32_t n, int64_t n_windows, const float *ref_mean, const float *ref_std,
+                                    int32_t norm, float *out_scores, float *out_md, float *out_md_metric,
+                                    float *out_recon, hipStream_t stream)
+{
+    if (!det)
+        return fail(ENOVA_EINVAL, "detector is NULL");
+    if (n < 0 || n_windows < 0)
+        return fail(ENOVA_EINVAL, "n_streams and n_windows must be >= 0");
+    if (norm != ENOVA_NORM_REFERENCE && norm != ENOVA_NORM_WINDOW)
+        return fail(ENOVA_EINVAL, "bad normalisation mode");
+    if ((ref_mean == nullptr) != (ref_std == nullptr))
+        return fail(ENOVA_EINVAL, "ref_mean and ref_std must both be given or both be NULL");
+    det->ran_ext = false;
+    if (n == 0 || n_windows == 0)
+        return ENOVA_OK;
+    if (!x || !soff || !woff)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    const Geometry &g = det->g;
+    if (g.M > kExtMaxM)
+        return fail(ENOVA_EUNSUPPORTED, "output variants support at most %d metrics", kExtMaxM);
+    DeviceGuard dg(det->device);
+    if (!dg.ok)
+        return fail(ENOVA_EHIP, "cannot select the detector's device");
+    hipError_t e;
+    if (det->timing && !det->ext_ev[0]) {
+        for (auto &ev : det->ext_ev)
+            if ((e = hipEventCreate(&ev)) != hipSuccess)
+                return hip_fail(e, "hipEventCreate");
+    }
+    const int D = g.D, H = g.H, L = g.L, M = g.M;
+    const int B = ext_chunk(g, n_windows);
+    // workspace: V, out [B][D]; a1, h, a2, hd [B][H]; ml [B][2L]; the products' split partials
+    // split partials of the products, for a full chunk and for the last, shorter one
+    int64_t wsg = 0;
+    const int last = static_cast<int>(n_windows - (n_windows - 1) / B * B);
+    for (const int rows : {B, last}) {
+        const int shapes[][3] = {{rows, H, D}, {rows, 2 * L, H}, {rows, H, L}, {rows, D, H}};
+        for (const auto &sh : shapes)
+            wsg = std::max(wsg, gemm_workspace_floats(sh[0], sh[1], sh[2]));
+    }
+    auto up4 = [](size_t v) { return (v + 3) / 4 * 4; };   // every sub-buffer 16-byte aligned
+    const size_t nBD = up4(static_cast<size_t>(B) * D), nBH = up4(static_cast<size_t>(B) * H),
+                 nML = up4(static_cast<size_t>(B) * 2 * L);
+    const size_t need = 2 * nBD + 4 * nBH + nML + static_cast<size_t>(wsg) + 16;
+    enova_status st = ensure(&det->ext_ws, &det->ext_ws_cap, need);
+    if (st != ENOVA_OK)
+        return st;
+    float *V = det->ext_ws, *out = V + nBD, *a1 = out + nBD, *h = a1 + nBH, *a2 = h + nBH, *hd = a2 + nBH,
+          *ml = hd + nBH, *gw = ml + nML;
+    if (det->timing)
+        (void)hipEventRecord(det->ext_ev[0], stream);
+    if (norm == ENOVA_NORM_REFERENCE && !ref_mean) {
+        st = ensure(&det->stats, &det->stats_cap, 2 * static_cast<size_t>(n) * M);
+        if (st != ENOVA_OK)
+            return st;
+        ref_mean = det->stats;
+        ref_std = det->stats + static_cast<size_t>(n) * M;
+        if ((e = launch_ref_stats(g, x, soff, n, det->stats, det->stats + static_cast<size_t>(n) * M, stream)) !=
+            hipSuccess)
+            return hip_fail(e, "reference statistics kernel");
+    }
+    GemmEpilogue plain{};
+    GemmEpilogue enc;
+    enc.kind = kEpiBiasAct;
+    enc.act = g.act;
+    enc.bias = det->b1;
+    enc.out2 = h;
+    GemmEpilogue dec = enc;
+    dec.bias = det->bd1;
+    dec.out2 = hd;
+    for (int64_t w0 = 0; w0 < n_windows; w0 += B) {
+        const int rows = static_cast<int>(std::min<int64_t>(B, n_windows - w0));
+        e = launch_ext_stage(x, g.dtype, soff, woff, n, w0, rows, M, g.W, g.S, norm, ref_mean, ref_std, V, stream);
+        if (e == hipSuccess)   // a1 = V W1^T + b1, h = act(a1)
+            e = launch_gemm(enc, V, D, 1, det->d_w1, 1, D, a1, H, rows, H, D, nullptr, gw, wsg, stream);
+        if (e == hipSuccess)   // [mu | lv] = h [Wmu; Wlv]^T
+            e = launch_gemm(plain, h, H, 1, det->d_wml, 1, H, ml, 2 * L, rows, 2 * L, H, nullptr, gw, wsg, stream);
+        if (e == hipSuccess)
+            e = launch_ext_latent(ml, det->d_bml, rows, L, out_scores ? out_scores + w0 : nullptr, stream);
+        if (e == hipSuccess)   // a2 = mu Wd1^T + bd1, hd = act(a2)
+            e = launch_gemm(dec, ml, 2 * L, 1, det->d_wd1, 1, L, a2, H, rows, H, L, nullptr, gw, wsg, stream);
+        if (e == hipSuccess)   // decoder output without bd2
+            e = launch_gemm(plain, hd, H, 1, det->d_wd2, 1, H, out, D, rows, D, H, nullptr, gw, wsg, stream);
+        if (e == hipSuccess)
+            e = launch_ext_reduce(V, out, det->d_bd2, rows, M, g.W, out_md ? out_md + w0 : nullptr,
+                                  out_md_metric ? out_md_metric + w0 * M : nullptr,
+                                  out_recon ? out_recon + w0 : nullptr, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "output-variant kernels");
+    }
+    if (det->timing)
+        (void)hipEventRecord(det->ext_ev[1], stream);
+    det->ran_ext = true;
+    return ENOVA_OK;
+}
+
+enova_status enova_detect_ext_time(enova_detector det, double *ms)
+{
+    if (!det || !ms)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    *ms = 0.0;
+    if (!det->timing || !det->ran_ext || !det->ext_ev[1])
+        return ENOVA_OK;
+    DeviceGuard dg(det->device);
+    hipError_t e = hipEventSynchronize(det->ext_ev[1]);
+    float f = 0.0f;
+    if (e == hipSuccess)
+        e = hipEventElapsedTime(&f, det->ext_ev[0], det->ext_ev[1]);
+    if (e != hipSuccess)
+        return hip_fail(e, "event timing");
+    *ms = f;
     return ENOVA_OK;
 }
 

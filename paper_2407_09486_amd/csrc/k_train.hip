@@ -664,7 +664,7 @@ struct SumF {
 
 hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
                        int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
-                       hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
+                       int64_t work_floats, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
 {
     if (m <= 0 || n <= 0)
         return hipSuccess;
@@ -675,7 +675,11 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
     const int64_t lda = a_k ? ai : ak, ldb = b_k ? bj : bk;
     const bool va = lda % 4 == 0 && reinterpret_cast<uintptr_t>(A) % 16 == 0;
     const bool vb = ldb % 4 == 0 && reinterpret_cast<uintptr_t>(B) % 16 == 0;
-    const int splits = work ? gemm_splits(m, n, k) : 1;
+    // never more slices than the caller's workspace holds
+    int splits = work ? gemm_splits(m, n, k) : 1;
+    const int64_t per_slice = static_cast<int64_t>(m) * n + m;
+    while (splits > 1 && static_cast<int64_t>(splits) * per_slice > work_floats)
+        --splits;
     const int kc = splits > 1 ? ((k + splits - 1) / splits + kGemmK - 1) / kGemmK * kGemmK : std::max(k, 1);
     const int used = splits > 1 ? (k + kc - 1) / kc : 1;
     const dim3 grid(static_cast<unsigned>((n + kGemmTile - 1) / kGemmTile),

@@ -1,0 +1,233 @@
+// Detector-output variants (Section IV-B): windows materialised in chunks, normalised against the
+// reference prefix or against the window itself; the encoder, heads and the decoder's full output
+// run as matrix-core products (the training step's GEMM); these kernels are the pieces around
+// them: staging, the latent and its KL score, and the per-window reductions of v - m'.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "mfma_common.h"
+#include "variants_internal.h"
+
+namespace enova {
+
+namespace {
+
+constexpr int kExtThreads = 256;
+
+template <int DT>
+__device__ __forceinline__ float load_value(const void *x, int64_t idx)
+{
+    if constexpr (DT == ENOVA_BF16)
+        return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t *>(x)[idx]) << 16);
+    else
+        return static_cast<const float *>(x)[idx];
+}
+
+// bf16 round to nearest even, returned as the float it represents (NaN kept).
+__device__ __forceinline__ float round_bf16(float v)
+{
+    uint32_t u = __float_as_uint(v);
+    if ((u & 0x7fffffffu) > 0x7f800000u)
+        return v;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return __uint_as_float(u & 0xffff0000u);
+}
+
+// One block per window of the chunk: the window's stream (binary search of the window CSR), its
+// normalisation (reference statistics, or the window's own fp64 mean and population std with the
+// reference path's guard), and its D normalised values as row i of V.
+template <int DT>
+__global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restrict__ x, const int64_t *__restrict__ soff,
+                                                           const int64_t *__restrict__ woff, int n, int64_t w0, int M,
+                                                           int W, int S, int norm, const float *__restrict__ mean,
+                                                           const float *__restrict__ std, float *__restrict__ V)
+{
+    __shared__ float s_mean[kExtMaxM], s_rinv[kExtMaxM];
+    const int64_t gw = w0 + blockIdx.x;
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (woff[mid] <= gw)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    const int s = lo;
+    const int64_t row0 = soff[s] + (gw - woff[s]) * S;
+    if (norm == ENOVA_NORM_WINDOW) {
+        // G threads per metric (M <= 256; else one), each over every G-th step; their partial
+        // sums are combined in thread order
+        __shared__ double part[kExtThreads];
+        const int G = M <= kExtThreads ? kExtThreads / M : 1;
+        for (int m0 = 0; m0 < M; m0 += kExtThreads / G) {
+            const int m = m0 + threadIdx.x / G, g = threadIdx.x % G;
+            const bool on = threadIdx.x / G < kExtThreads / G && m < M;
+            double a = 0.0;
+            if (on)
+                for (int t = g; t < W; t += G)
+                    a += load_value<DT>(x, (row0 + t) * M + m);
+            part[threadIdx.x] = a;
+            __syncthreads();
+            double mu = 0.0;
+            if (on) {
+                for (int i = 0; i < G; ++i)
+                    mu += part[(threadIdx.x / G) * G + i];
+                mu /= W;
+            }
+            __syncthreads();
+            double q = 0.0;
+            if (on)
+                for (int t = g; t < W; t += G) {
+                    const double d = load_value<DT>(x, (row0 + t) * M + m) - mu;
+                    q = fma(d, d, q);
+                }
+            part[threadIdx.x] = q;
+            __syncthreads();
+            if (on && g == 0) {
+                double ss = 0.0;
+                for (int i = 0; i < G; ++i)
+                    ss += part[threadIdx.x + i];
+                double sd = sqrt(ss / W);
+                if (sd <= 1e-6 * fmax(1.0, fabs(mu)))
+                    sd = 1.0;
+                s_mean[m] = static_cast<float>(mu);
+                s_rinv[m] = 1.0f / static_cast<float>(sd);
+            }
+            __syncthreads();
+        }
+    } else {
+        for (int m = threadIdx.x; m < M; m += kExtThreads) {
+            s_mean[m] = mean[static_cast<int64_t>(s) * M + m];
+            s_rinv[m] = 1.0f / std[static_cast<int64_t>(s) * M + m];
+        }
+        __syncthreads();
+    }
+    const int D = W * M;
+    float *out = V + static_cast<int64_t>(blockIdx.x) * D;
+    for (int j = threadIdx.x; j < D; j += kExtThreads) {
+        const int t = j / M, m = j - t * M;
+        const float v = (load_value<DT>(x, (row0 + t) * M + m) - s_mean[m]) * s_rinv[m];
+        out[j] = DT == ENOVA_BF16 ? round_bf16(v) : v;
+    }
+}
+
+// One thread per window: mu and lv (biases [bmu | blv] added in place in ml = [mu | lv]) and
+// the KL score of the posterior from N(0, I).
+__global__ __launch_bounds__(64) void k_ext_latent(float *__restrict__ ml, const float *__restrict__ bml, int rows,
+                                                   int L, float *__restrict__ score)
+{
+    const int i = blockIdx.x * 64 + threadIdx.x;
+    if (i >= rows)
+        return;
+    float *mu = ml + static_cast<int64_t>(i) * 2 * L, *lv = mu + L;
+    float k = 0.0f;
+    for (int l = 0; l < L; ++l) {
+        const float m = mu[l] + bml[l];
+        const float v = lv[l] + bml[L + l];
+        mu[l] = m;
+        lv[l] = v;
+        k += m * m + kl_g(v);
+    }
+    if (score)
+        score[i] = 0.5f * k;
+}
+
+// One block per window: d = v - (out + bd2) over the window's D values; per metric the mean of d
+// over the W steps, and the window's mean of d and of d^2. G threads per metric (M <= 256) each
+// sum every G-th step; partials are combined in thread order, the metrics' totals by a tree.
+__global__ __launch_bounds__(kExtThreads) void k_ext_reduce(const float *__restrict__ V, const float *__restrict__ out,
+                                                            const float *__restrict__ bd2, int M, int W,
+                                                            float *__restrict__ md, float *__restrict__ md_metric,
+                                                            float *__restrict__ recon)
+{
+    __shared__ float pa[kExtThreads], pq[kExtThreads];
+    const int D = W * M;
+    const float *v = V + static_cast<int64_t>(blockIdx.x) * D;
+    const float *o = out + static_cast<int64_t>(blockIdx.x) * D;
+    const int G = M <= kExtThreads ? kExtThreads / M : 1;
+    float sd = 0.0f, sq = 0.0f;   // thread g == 0 of a metric: running totals over its metrics
+    for (int m0 = 0; m0 < M; m0 += kExtThreads / G) {
+        const int m = m0 + threadIdx.x / G, g = threadIdx.x % G;
+        const bool on = threadIdx.x / G < kExtThreads / G && m < M;
+        float a = 0.0f, q = 0.0f;
+        if (on)
+            for (int t = g; t < W; t += G) {
+                const int j = t * M + m;
+                const float d = v[j] - (o[j] + bd2[j]);
+                a += d;
+                q = fmaf(d, d, q);
+            }
+        pa[threadIdx.x] = a;
+        pq[threadIdx.x] = q;
+        __syncthreads();
+        if (on && g == 0) {
+            float ta = 0.0f, tq = 0.0f;
+            for (int i = 0; i < G; ++i) {
+                ta += pa[threadIdx.x + i];
+                tq += pq[threadIdx.x + i];
+            }
+            if (md_metric)
+                md_metric[static_cast<int64_t>(blockIdx.x) * M + m] = ta / W;
+            sd += ta;
+            sq += tq;
+        }
+        __syncthreads();
+    }
+    pa[threadIdx.x] = sd;
+    pq[threadIdx.x] = sq;
+    __syncthreads();
+    for (int w = kExtThreads / 2; w >= 1; w >>= 1) {
+        if (threadIdx.x < w) {
+            pa[threadIdx.x] += pa[threadIdx.x + w];
+            pq[threadIdx.x] += pq[threadIdx.x + w];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        if (md)
+            md[blockIdx.x] = pa[0] / D;
+        if (recon)
+            recon[blockIdx.x] = pq[0] / D;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const int64_t *woff, int n, int64_t w0,
+                            int rows, int M, int W, int S, int norm, const float *mean, const float *std, float *V,
+                            hipStream_t st)
+{
+    if (rows <= 0)
+        return hipSuccess;
+    if (M > kExtMaxM)
+        return hipErrorInvalidValue;
+    if (dtype == ENOVA_BF16)
+        hipLaunchKernelGGL(k_ext_stage<ENOVA_BF16>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), 0, st, x,
+                           soff, woff, n, w0, M, W, S, norm, mean, std, V);
+    else
+        hipLaunchKernelGGL(k_ext_stage<ENOVA_F32>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), 0, st, x,
+                           soff, woff, n, w0, M, W, S, norm, mean, std, V);
+    return hipGetLastError();
+}
+
+hipError_t launch_ext_latent(float *ml, const float *bml, int rows, int L, float *score, hipStream_t st)
+{
+    if (rows <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_ext_latent, dim3(static_cast<unsigned>((rows + 63) / 64)), dim3(64), 0, st, ml, bml, rows, L,
+                       score);
+    return hipGetLastError();
+}
+
+hipError_t launch_ext_reduce(const float *V, const float *out, const float *bd2, int rows, int M, int W, float *md,
+                             float *md_metric, float *recon, hipStream_t st)
+{
+    if (rows <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_ext_reduce, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), 0, st, V, out, bd2, M, W,
+                       md, md_metric, recon);
+    return hipGetLastError();
+}
+
+}  // namespace enova

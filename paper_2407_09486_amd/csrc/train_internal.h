@@ -29,9 +29,11 @@ struct GemmEpilogue {
 };
 int64_t gemm_workspace_floats(int m, int n, int k);
 // ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
+// `work` holds work_floats floats; a product splits only as far as they allow (none when work is
+// NULL).
 hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
                        int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
-                       hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                       int64_t work_floats, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // ml: [rows][2L] = [mu | lv] per window (biases bml = [bmu | blv] added in place).
 hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
                          int L, hipStream_t st);

@@ -244,7 +244,7 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
             e0 = t->ev[ne++];
             e1 = t->ev[ne++];
         }
-        run(launch_gemm(ep, A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, rowsum, t->work, s, e0, e1));
+        run(launch_gemm(ep, A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, rowsum, t->work, t->work_cap, s, e0, e1));
     };
     const GemmEpilogue plain{};
     auto bias_act = [&](const float *bias, float *out) {

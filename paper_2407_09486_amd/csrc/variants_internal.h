@@ -1,0 +1,23 @@
+// Internal declarations of the detector-output variants (chunked dense evaluation of windows).
+#pragma once
+
+#include "train_internal.h"
+
+namespace enova {
+
+constexpr int kExtMaxM = 4096;   // metrics whose normalisation a staging block keeps in LDS
+
+// Rows i < rows of V [rows][W*M] = window w0 + i (global window index) normalised per `norm`
+// (ENOVA_NORM_REFERENCE: mean/std [n][M]; ENOVA_NORM_WINDOW: the window's own statistics).
+hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const int64_t *woff, int n, int64_t w0,
+                            int rows, int M, int W, int S, int norm, const float *mean, const float *std, float *V,
+                            hipStream_t st);
+// ml [rows][2L] = [mu | lv] without biases; adds bml = [bmu | blv] in place and writes the KL
+// score of each row (score may be NULL).
+hipError_t launch_ext_latent(float *ml, const float *bml, int rows, int L, float *score, hipStream_t st);
+// Per row: md = mean(v - m'), md_metric [rows][M] = mean over the steps per metric, recon =
+// mean((v - m')^2), with m' = out + bd2 (any output may be NULL).
+hipError_t launch_ext_reduce(const float *V, const float *out, const float *bd2, int rows, int M, int W, float *md,
+                             float *md_metric, float *recon, hipStream_t st);
+
+}  // namespace enova

@@ -166,3 +166,12 @@ def test_config_init_rejects_bad_params(over):
     v = ctypes.c_double()
     assert L.enova_config_t_critical(0.05, 0, ctypes.byref(v)) == binding.ENOVA_EINVAL
     assert L.enova_config_destroy(None) == binding.ENOVA_OK
+
+
+def test_output_variants_reject_bad_arguments():
+    _ensure_built()
+    L = binding.lib()
+    assert L.enova_detect_score_ext(None, None, None, None, 1, 1, None, None, 0, None, None, None, None,
+                                    None) == binding.ENOVA_EINVAL
+    v = ctypes.c_double()
+    assert L.enova_detect_ext_time(None, ctypes.byref(v)) == binding.ENOVA_EINVAL

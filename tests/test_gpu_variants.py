@@ -1,0 +1,131 @@
+"""GPU parity of the detector-output variants (Section IV-B) through the C ABI: KL score, md, the
+per-metric md vector and the reconstruction error of every window, for both normalisations,
+against the fp64 oracle ``oracle/variants.py``.
+
+Tolerances: the scores as the batch path (1e-4 relative in fp32, 1e-2 for the bf16 detector);
+md and every md_m within that fraction of the window's scale mean|v| + mean|m'|; the
+reconstruction error within that fraction of (error + scale^2), since it is a mean of squared
+differences of quantities of that scale.
+"""
+import numpy as np
+import pytest
+
+from harness import TOL, check_scores, detector, log, upload
+from oracle import variants as ov
+from paper_2407_09486_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _weights_f64(w):
+    return {k: np.asarray(getattr(w, k), np.float64) for k in
+            ("w1", "b1", "wmu", "bmu", "wlv", "blv", "wd1", "bd1", "wd2", "bd2")}
+
+
+def _run(cfg, w, work, norm):
+    import torch
+    det = detector(cfg, w, "mfma")
+    x, so = upload(work)
+    woff = det.window_offsets(work.stream_offsets)
+    N = int(woff[-1])
+    out = det.score_ext(x, so, torch.from_numpy(woff).cuda(), N, norm=norm)
+    torch.cuda.synchronize()
+    res = [o.cpu().numpy() for o in out]
+    det.close()
+    return res, woff
+
+
+def _check(g, ref, dtype, what, idx=None):
+    sc, md, mdm, rec = g
+    if idx is not None:
+        sc, md, mdm, rec = sc[idx], md[idx], mdm[idx], rec[idx]
+    rel, _ = TOL[dtype]
+    check_scores(sc, ref["score"], dtype, what + " score")
+    scale = ref["scale"]
+    assert np.all(np.abs(md - ref["md"]) <= rel * scale), what + " md"
+    assert np.all(np.abs(mdm - ref["md_metric"]) <= rel * scale[:, None]), what + " md_metric"
+    assert np.all(np.abs(rec - ref["recon"]) <= rel * (ref["recon"] + scale ** 2)), what + " recon"
+
+
+@pytest.mark.parametrize("norm", ["reference", "window"])
+@pytest.mark.parametrize("shape", [dict(metrics=8, window=32, stride=1, hidden=32, latent=16, act="relu"),
+                                   dict(metrics=5, window=7, stride=3, hidden=40, latent=3, act="tanh")])
+def test_variants_match_oracle(norm, shape):
+    cfg = wl.CONFIGS["c1"].replace(n_streams=5, t_len=0, t_min=20, t_max=900, kind="ragged_mix", **shape)
+    w = wl.make_weights(cfg, bias_scale=0.1)
+    work = wl.generate(cfg, lengths=[900, 5, 40, 333, 700])
+    log(f"variants {norm} {shape}")
+    g, woff = _run(cfg, w, work, norm)
+    ref = ov.score_ext(work.values_f64(), work.stream_offsets, window=cfg.window, stride=cfg.stride,
+                       weights=_weights_f64(w), act=cfg.act, norm=norm, ref_frac=cfg.ref_frac)
+    assert len(ref["score"]) == woff[-1]
+    _check(g, ref, "f32", f"{norm} {shape}")
+
+
+@pytest.mark.parametrize("norm", ["reference", "window"])
+def test_variants_bf16_detector(norm):
+    cfg = wl.CONFIGS["c4"].replace(n_streams=3, t_len=300, metrics=8, window=16, stride=2, hidden=64)
+    w = wl.make_weights(cfg, bias_scale=0.1)
+    work = wl.generate(cfg)
+    log(f"variants bf16 {norm}")
+    g, woff = _run(cfg, w, work, norm)
+    ref = ov.score_ext(work.values_f64(), work.stream_offsets, window=cfg.window, stride=cfg.stride,
+                       weights=_weights_f64(w), act=cfg.act, norm=norm, ref_frac=cfg.ref_frac, bf16=True)
+    _check(g, ref, "bf16", f"bf16 {norm}")
+
+
+def test_reference_variants_agree_with_the_batch_path():
+    import torch
+    cfg = wl.CONFIGS["c2"].replace(n_streams=4, t_len=3000)
+    w = wl.make_weights(cfg)
+    work = wl.generate(cfg)
+    det = detector(cfg, w, "mfma")
+    x, so = upload(work)
+    woff = det.window_offsets(work.stream_offsets)
+    N = int(woff[-1])
+    wo = torch.from_numpy(woff).cuda()
+    sc, md, _ = det.score(x, so, wo, N)
+    sc2, md2, _, _ = det.score_ext(x, so, wo, N)
+    torch.cuda.synchronize()
+    a, b = sc.cpu().numpy().astype(np.float64), sc2.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(a - b) <= 2e-4 * np.abs(a) + 1e-6)
+    det.close()
+
+
+def test_windows_across_chunks_and_constant_metrics():
+    """More windows than one chunk (65536 for D = 256): windows on both sides of every chunk
+    boundary, and a metric that is constant inside some windows (the per-window guard)."""
+    cfg = wl.CONFIGS["c1"].replace(n_streams=3, t_len=30000)
+    w = wl.make_weights(cfg, bias_scale=0.1)
+    work = wl.generate(cfg)
+    xv = work.x.copy()
+    xv[1000:1100, 3] = 2.5                           # constant inside windows of stream 0
+    work = wl.from_arrays(cfg, xv, work.stream_offsets)
+    for norm in ("window", "reference"):
+        g, woff = _run(cfg, w, work, norm)
+        N = int(woff[-1])
+        assert N > 65536
+        glob = sorted({0, 1000, 1030, 65535, 65536, 65537, N - 1} | set(range(1040, 1060)))
+        pairs = []
+        for gi in glob:
+            s = int(np.searchsorted(woff, gi, side="right") - 1)
+            pairs.append((s, gi - int(woff[s])))
+        ref = ov.score_ext(work.values_f64(), work.stream_offsets, window=cfg.window, stride=cfg.stride,
+                           weights=_weights_f64(w), act=cfg.act, norm=norm, ref_frac=cfg.ref_frac, pairs=pairs)
+        _check(g, ref, "f32", f"chunks {norm}", idx=np.asarray(glob))
+
+
+def test_short_last_chunk_splits_its_products():
+    """65536 + 300 windows of D = 256: the last chunk's encoder product has few output tiles and
+    splits its reduction; its windows must match the oracle like the others."""
+    cfg = wl.CONFIGS["c1"].replace(n_streams=1, t_len=65867)
+    w = wl.make_weights(cfg, bias_scale=0.1)
+    work = wl.generate(cfg)
+    g, woff = _run(cfg, w, work, "window")
+    N = int(woff[-1])
+    assert N == 65536 + 300
+    glob = [0, 65535] + list(range(65536, N, 7)) + [N - 1]
+    ref = ov.score_ext(work.values_f64(), work.stream_offsets, window=cfg.window, stride=cfg.stride,
+                       weights=_weights_f64(w), act=cfg.act, norm="window", ref_frac=cfg.ref_frac,
+                       pairs=[(0, k) for k in glob])
+    _check(g, ref, "f32", "short last chunk", idx=np.asarray(glob))
