@@ -793,12 +793,14 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
     auto up4 = [](size_t v) { return (v + 3) / 4 * 4; };   // every sub-buffer 16-byte aligned
     const size_t nBD = up4(static_cast<size_t>(B) * D), nBH = up4(static_cast<size_t>(B) * H),
                  nML = up4(static_cast<size_t>(B) * 2 * L);
-    const size_t need = 2 * nBD + 4 * nBH + nML + static_cast<size_t>(wsg) + 16;
+    const size_t nMap = up4(static_cast<size_t>(B));   // the chunk's window -> stream map (ints)
+    const size_t need = 2 * nBD + 4 * nBH + nML + nMap + static_cast<size_t>(wsg) + 16;
     enova_status st = ensure(&det->ext_ws, &det->ext_ws_cap, need);
     if (st != ENOVA_OK)
         return st;
     float *V = det->ext_ws, *out = V + nBD, *a1 = out + nBD, *h = a1 + nBH, *a2 = h + nBH, *hd = a2 + nBH,
-          *ml = hd + nBH, *gw = ml + nML;
+          *ml = hd + nBH, *mapf = ml + nML, *gw = mapf + nMap;
+    int *wmap = reinterpret_cast<int *>(mapf);
     if (det->timing)
         (void)hipEventRecord(det->ext_ev[0], stream);
     if (norm == ENOVA_NORM_REFERENCE && !ref_mean) {
@@ -822,7 +824,8 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
     dec.out2 = hd;
     for (int64_t w0 = 0; w0 < n_windows; w0 += B) {
         const int rows = static_cast<int>(std::min<int64_t>(B, n_windows - w0));
-        e = launch_ext_stage(x, g.dtype, soff, woff, n, w0, rows, M, g.W, g.S, norm, ref_mean, ref_std, V, stream);
+        e = launch_ext_stage(x, g.dtype, soff, woff, n, w0, rows, M, g.W, g.S, norm, ref_mean, ref_std, wmap, V,
+                             stream);
         if (e == hipSuccess)   // a1 = V W1^T + b1, h = act(a1)
             e = launch_gemm(enc, V, D, 1, det->d_w1, 1, D, a1, H, rows, H, D, nullptr, gw, wsg, stream);
         if (e == hipSuccess)   // [mu | lv] = h [Wmu; Wlv]^T

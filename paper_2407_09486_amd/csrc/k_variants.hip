@@ -34,17 +34,18 @@ __device__ __forceinline__ float round_bf16(float v)
     return __uint_as_float(u & 0xffff0000u);
 }
 
-// One block per window of the chunk: the window's stream (binary search of the window CSR), its
+// One block per window of the chunk: the window's stream (from k_ext_map), its
 // normalisation (reference statistics, or the window's own fp64 mean and population std with the
 // reference path's guard), and its D normalised values as row i of V.
-template <int DT>
-__global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restrict__ x, const int64_t *__restrict__ soff,
-                                                           const int64_t *__restrict__ woff, int n, int64_t w0, int M,
-                                                           int W, int S, int norm, const float *__restrict__ mean,
-                                                           const float *__restrict__ std, float *__restrict__ V)
+// map[i] = the stream of window w0 + i (the last s with woff[s] <= w0 + i), one thread per window:
+// the binary searches run in parallel instead of heading every staging block.
+__global__ __launch_bounds__(kExtThreads) void k_ext_map(const int64_t *__restrict__ woff, int n, int64_t w0, int rows,
+                                                         int *__restrict__ map)
 {
-    __shared__ float s_mean[kExtMaxM], s_rinv[kExtMaxM];
-    const int64_t gw = w0 + blockIdx.x;
+    const int i = blockIdx.x * kExtThreads + threadIdx.x;
+    if (i >= rows)
+        return;
+    const int64_t gw = w0 + i;
     int lo = 0, hi = n - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
@@ -53,16 +54,31 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restric
         else
             hi = mid - 1;
     }
-    const int s = lo;
+    map[i] = lo;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restrict__ x, const int64_t *__restrict__ soff,
+                                                           const int64_t *__restrict__ woff, const int *__restrict__ map,
+                                                           int64_t w0, int M, int W, int S, int norm,
+                                                           const float *__restrict__ mean,
+                                                           const float *__restrict__ std, float *__restrict__ V)
+{
+    extern __shared__ float s_norm[];   // mean [M], then 1/std [M]
+    float *s_mean = s_norm, *s_rinv = s_norm + M;
+    const int64_t gw = w0 + blockIdx.x;
+    const int s = map[blockIdx.x];
     const int64_t row0 = soff[s] + (gw - woff[s]) * S;
     if (norm == ENOVA_NORM_WINDOW) {
-        // G threads per metric (M <= 256; else one), each over every G-th step; their partial
-        // sums are combined in thread order
+        // G = 256 / MB threads per metric for a batch of MB = min(M, 256) metrics: thread
+        // (g, m) = (tid / MB, tid % MB) takes every G-th step (consecutive threads read
+        // consecutive metrics of a step); the G partial sums of a metric are combined in g order
         __shared__ double part[kExtThreads];
-        const int G = M <= kExtThreads ? kExtThreads / M : 1;
-        for (int m0 = 0; m0 < M; m0 += kExtThreads / G) {
-            const int m = m0 + threadIdx.x / G, g = threadIdx.x % G;
-            const bool on = threadIdx.x / G < kExtThreads / G && m < M;
+        const int MB = M < kExtThreads ? M : kExtThreads;
+        const int G = kExtThreads / MB;
+        for (int m0 = 0; m0 < M; m0 += MB) {
+            const int m = m0 + threadIdx.x % MB, g = threadIdx.x / MB;
+            const bool on = g < G && m < M;
             double a = 0.0;
             if (on)
                 for (int t = g; t < W; t += G)
@@ -72,7 +88,7 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restric
             double mu = 0.0;
             if (on) {
                 for (int i = 0; i < G; ++i)
-                    mu += part[(threadIdx.x / G) * G + i];
+                    mu += part[i * MB + threadIdx.x % MB];
                 mu /= W;
             }
             __syncthreads();
@@ -87,7 +103,7 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restric
             if (on && g == 0) {
                 double ss = 0.0;
                 for (int i = 0; i < G; ++i)
-                    ss += part[threadIdx.x + i];
+                    ss += part[i * MB + threadIdx.x];
                 double sd = sqrt(ss / W);
                 if (sd <= 1e-6 * fmax(1.0, fabs(mu)))
                     sd = 1.0;
@@ -134,8 +150,9 @@ __global__ __launch_bounds__(64) void k_ext_latent(float *__restrict__ ml, const
 }
 
 // One block per window: d = v - (out + bd2) over the window's D values; per metric the mean of d
-// over the W steps, and the window's mean of d and of d^2. G threads per metric (M <= 256) each
-// sum every G-th step; partials are combined in thread order, the metrics' totals by a tree.
+// over the W steps, and the window's mean of d and of d^2. Thread (g, m) = (tid / MB, tid % MB)
+// sums every G-th step of metric m (MB = min(M, 256), G = 256 / MB); a metric's partials are
+// combined in g order, the metrics' totals by a tree.
 __global__ __launch_bounds__(kExtThreads) void k_ext_reduce(const float *__restrict__ V, const float *__restrict__ out,
                                                             const float *__restrict__ bd2, int M, int W,
                                                             float *__restrict__ md, float *__restrict__ md_metric,
@@ -145,11 +162,12 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_reduce(const float *__restr
     const int D = W * M;
     const float *v = V + static_cast<int64_t>(blockIdx.x) * D;
     const float *o = out + static_cast<int64_t>(blockIdx.x) * D;
-    const int G = M <= kExtThreads ? kExtThreads / M : 1;
+    const int MB = M < kExtThreads ? M : kExtThreads;
+    const int G = kExtThreads / MB;
     float sd = 0.0f, sq = 0.0f;   // thread g == 0 of a metric: running totals over its metrics
-    for (int m0 = 0; m0 < M; m0 += kExtThreads / G) {
-        const int m = m0 + threadIdx.x / G, g = threadIdx.x % G;
-        const bool on = threadIdx.x / G < kExtThreads / G && m < M;
+    for (int m0 = 0; m0 < M; m0 += MB) {
+        const int m = m0 + threadIdx.x % MB, g = threadIdx.x / MB;
+        const bool on = g < G && m < M;
         float a = 0.0f, q = 0.0f;
         if (on)
             for (int t = g; t < W; t += G) {
@@ -164,8 +182,8 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_reduce(const float *__restr
         if (on && g == 0) {
             float ta = 0.0f, tq = 0.0f;
             for (int i = 0; i < G; ++i) {
-                ta += pa[threadIdx.x + i];
-                tq += pq[threadIdx.x + i];
+                ta += pa[i * MB + threadIdx.x];
+                tq += pq[i * MB + threadIdx.x];
             }
             if (md_metric)
                 md_metric[static_cast<int64_t>(blockIdx.x) * M + m] = ta / W;
@@ -195,19 +213,22 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_reduce(const float *__restr
 }  // namespace
 
 hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const int64_t *woff, int n, int64_t w0,
-                            int rows, int M, int W, int S, int norm, const float *mean, const float *std, float *V,
-                            hipStream_t st)
+                            int rows, int M, int W, int S, int norm, const float *mean, const float *std, int *map,
+                            float *V, hipStream_t st)
 {
     if (rows <= 0)
         return hipSuccess;
     if (M > kExtMaxM)
         return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_ext_map, dim3(static_cast<unsigned>((rows + kExtThreads - 1) / kExtThreads)),
+                       dim3(kExtThreads), 0, st, woff, n, w0, rows, map);
+    const size_t lds = 2 * sizeof(float) * static_cast<size_t>(M);
     if (dtype == ENOVA_BF16)
-        hipLaunchKernelGGL(k_ext_stage<ENOVA_BF16>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), 0, st, x,
-                           soff, woff, n, w0, M, W, S, norm, mean, std, V);
+        hipLaunchKernelGGL(k_ext_stage<ENOVA_BF16>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), lds, st, x,
+                           soff, woff, map, w0, M, W, S, norm, mean, std, V);
     else
-        hipLaunchKernelGGL(k_ext_stage<ENOVA_F32>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), 0, st, x,
-                           soff, woff, n, w0, M, W, S, norm, mean, std, V);
+        hipLaunchKernelGGL(k_ext_stage<ENOVA_F32>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), lds, st, x,
+                           soff, woff, map, w0, M, W, S, norm, mean, std, V);
     return hipGetLastError();
 }
 

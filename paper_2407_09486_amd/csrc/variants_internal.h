@@ -5,13 +5,14 @@
 
 namespace enova {
 
-constexpr int kExtMaxM = 4096;   // metrics whose normalisation a staging block keeps in LDS
+constexpr int kExtMaxM = 4096;   // metrics whose normalisation (2M floats) a staging block keeps in LDS
 
 // Rows i < rows of V [rows][W*M] = window w0 + i (global window index) normalised per `norm`
-// (ENOVA_NORM_REFERENCE: mean/std [n][M]; ENOVA_NORM_WINDOW: the window's own statistics).
+// (ENOVA_NORM_REFERENCE: mean/std [n][M]; ENOVA_NORM_WINDOW: the window's own statistics);
+// map holds `rows` ints of scratch (each window's stream).
 hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const int64_t *woff, int n, int64_t w0,
-                            int rows, int M, int W, int S, int norm, const float *mean, const float *std, float *V,
-                            hipStream_t st);
+                            int rows, int M, int W, int S, int norm, const float *mean, const float *std, int *map,
+                            float *V, hipStream_t st);
 // ml [rows][2L] = [mu | lv] without biases; adds bml = [bmu | blv] in place and writes the KL
 // score of each row (score may be NULL).
 hipError_t launch_ext_latent(float *ml, const float *bml, int rows, int L, float *score, hipStream_t st);
