@@ -12,7 +12,7 @@ namespace enova {
 namespace {
 
 constexpr int kCfgThreads = 256;
-constexpr int kCfgMaxW = 4096;   // the per-stream kernel holds one window of four columns in LDS
+constexpr int kCfgMaxW = 4096;   // the per-stream kernel holds one window of four columns in LDS (80 KiB at most)
 constexpr size_t kCfgScanLds = 48 * 1024;
 
 template <int DT>
@@ -115,6 +115,24 @@ __device__ double block_sum(double v, double *red)
     return r;
 }
 
+// Two fixed-order block sums at once (red holds 2 * kCfgThreads doubles).
+__device__ void block_sum2(double a, double b, double *red, double &ra, double &rb)
+{
+    red[threadIdx.x] = a;
+    red[kCfgThreads + threadIdx.x] = b;
+    __syncthreads();
+    for (int w = kCfgThreads / 2; w >= 1; w >>= 1) {
+        if (threadIdx.x < w) {
+            red[threadIdx.x] += red[threadIdx.x + w];
+            red[kCfgThreads + threadIdx.x] += red[kCfgThreads + threadIdx.x + w];
+        }
+        __syncthreads();
+    }
+    ra = red[0];
+    rb = red[kCfgThreads];
+    __syncthreads();
+}
+
 // Linearly interpolated sample quantile of sorted v[0..n).
 __device__ double sorted_quantile(const float *v, int n, double p)
 {
@@ -124,8 +142,8 @@ __device__ double sorted_quantile(const float *v, int n, double p)
     return static_cast<double>(v[lo]) + (h - lo) * (static_cast<double>(v[hi]) - static_cast<double>(v[lo]));
 }
 
-// Quantile at level q of the Gaussian KDE of v[0..n) (Silverman's bandwidth), by bisection on its
-// distribution function. `sorted` is scratch of np2 floats (np2: a power of two >= n).
+// Quantile at level q of the Gaussian KDE of v[0..n) (Silverman's bandwidth): the root of its
+// distribution function minus q. `sorted` is scratch of np2 floats (np2: a power of two >= n).
 __device__ double kde_quantile(const float *v, int n, int np2, double q, float *sorted, double *red)
 {
     for (int i = threadIdx.x; i < np2; i += kCfgThreads)
@@ -164,22 +182,36 @@ __device__ double kde_quantile(const float *v, int n, int np2, double q, float *
     const double h = 0.9 * spread * pow(static_cast<double>(n), -0.2);
     if (h == 0.0)
         return v[0];
+    // Safeguarded Newton on F(x) - q (F' is the KDE density): every evaluation also tightens the
+    // bracket [lo, hi], and a step that would leave it becomes a bisection step; stops when the
+    // bracket can no longer shrink or the step vanishes.
     double lo = sorted[0] - 10.0 * h, hi = sorted[n - 1] + 10.0 * h;
     const double scale = 1.0 / (h * 1.4142135623730951);
+    const double dens = 1.0 / (h * 2.5066282746310002 * n);   // 1 / (h sqrt(2 pi) n)
+    double x = 0.5 * (lo + hi);
     for (int it = 0; it < 200; ++it) {
-        const double mid = 0.5 * (lo + hi);
-        if (mid <= lo || mid >= hi)
-            break;
-        part = 0.0;
-        for (int i = threadIdx.x; i < n; i += kCfgThreads)
-            part += 0.5 * erfc(-(mid - v[i]) * scale);
-        const double F = block_sum(part, red) / n;
+        double pf = 0.0, pd = 0.0;
+        for (int i = threadIdx.x; i < n; i += kCfgThreads) {
+            const double u = (x - v[i]) * scale;
+            pf += 0.5 * erfc(-u);
+            pd += exp(-u * u);
+        }
+        double F, f1;
+        block_sum2(pf, pd, red, F, f1);
+        F /= n;
+        f1 *= dens;
         if (F < q)
-            lo = mid;
+            lo = x;
         else
-            hi = mid;
+            hi = x;
+        double nx = f1 > 0.0 ? x - (F - q) / f1 : 0.5 * (lo + hi);
+        if (!(nx > lo && nx < hi))
+            nx = 0.5 * (lo + hi);
+        if (nx == x || !(0.5 * (lo + hi) > lo && 0.5 * (lo + hi) < hi))
+            break;
+        x = nx;
     }
-    return 0.5 * (lo + hi);
+    return x;
 }
 
 // One block per stream: the last window's fits, the regime and the KDE limits.
@@ -187,10 +219,11 @@ template <int DT>
 __global__ __launch_bounds__(kCfgThreads) void k_cfg_stream(CfgParams c, const void *__restrict__ x,
                                                             const int64_t *__restrict__ soff, CfgStreamOut o)
 {
-    __shared__ float vr[kCfgMaxW], vf[kCfgMaxW], vt[kCfgMaxW], vm[kCfgMaxW], sorted[kCfgMaxW];
-    __shared__ double red[kCfgThreads];
+    extern __shared__ float cfg_dyn[];   // four columns of the window [W] each, sort scratch [np2]
+    __shared__ double red[2 * kCfgThreads];
     const int s = blockIdx.x;
     const int W = c.W, S = c.S, M = c.M;
+    float *vr = cfg_dyn, *vf = vr + W, *vt = vf + W, *vm = vt + W, *sorted = vm + W;
     const int64_t T = soff[s + 1] - soff[s];
     const int64_t nw = T >= W ? (T - W) / S + 1 : 0;
     if (nw == 0) {
@@ -302,11 +335,22 @@ hipError_t launch_cfg_stream(const CfgParams &c, const void *x, const int64_t *s
         return hipSuccess;
     if (c.W > kCfgMaxW)
         return hipErrorInvalidValue;
+    int np2 = 1;
+    while (np2 < c.W)
+        np2 <<= 1;
+    const size_t lds = sizeof(float) * (4 * static_cast<size_t>(c.W) + np2);
+    const void *fn = c.dtype == ENOVA_BF16 ? reinterpret_cast<const void *>(k_cfg_stream<ENOVA_BF16>)
+                                           : reinterpret_cast<const void *>(k_cfg_stream<ENOVA_F32>);
+    if (lds > 64 * 1024) {   // windows beyond 3276 steps need more than the default dynamic LDS
+        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (e != hipSuccess)
+            return e;
+    }
     if (c.dtype == ENOVA_BF16)
-        hipLaunchKernelGGL(k_cfg_stream<ENOVA_BF16>, dim3(static_cast<unsigned>(n)), dim3(kCfgThreads), 0, st, c, x,
+        hipLaunchKernelGGL(k_cfg_stream<ENOVA_BF16>, dim3(static_cast<unsigned>(n)), dim3(kCfgThreads), lds, st, c, x,
                            soff, o);
     else
-        hipLaunchKernelGGL(k_cfg_stream<ENOVA_F32>, dim3(static_cast<unsigned>(n)), dim3(kCfgThreads), 0, st, c, x,
+        hipLaunchKernelGGL(k_cfg_stream<ENOVA_F32>, dim3(static_cast<unsigned>(n)), dim3(kCfgThreads), lds, st, c, x,
                            soff, o);
     return hipGetLastError();
 }

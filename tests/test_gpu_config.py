@@ -172,3 +172,21 @@ def test_full_size_sampled():
     assert np.array_equal(rs[0][pick], ref["sig"])
     for got, key in zip(rs[1:], ("n_limit", "t_limit", "max_num_seqs", "gpu_memory")):
         np.testing.assert_allclose(got[pick], ref[key], rtol=1e-9, atol=0)
+
+
+def test_recommend_longest_window():
+    """W = 4096 (the largest window the per-service kernel holds): more than the default dynamic
+    LDS, a non-trivial sort and KDE over 4096 values."""
+    import torch
+    W = 4096
+    x, offs = _series([5000, 4500, 4096, 4095], seed=77)
+    log(f"config recommend W={W}")
+    sc = _scanner(W, 3)
+    sig, nl, tl, mns, gm = (v.cpu().numpy() for v in sc.recommend(_upload(x, "f32"), torch.from_numpy(offs).cuda()))
+    sc.close()
+    ref = cs.stream_config(x.astype(np.float64), offs, window=W, stride=3, **COLS)
+    assert np.array_equal(sig, ref["sig"])
+    for got, exp in ((nl, ref["n_limit"]), (tl, ref["t_limit"]), (mns, ref["max_num_seqs"]), (gm, ref["gpu_memory"])):
+        assert np.array_equal(np.isnan(got), np.isnan(exp))
+        ok = ~np.isnan(exp)
+        np.testing.assert_allclose(got[ok], exp[ok], rtol=1e-9, atol=0)
