@@ -274,10 +274,19 @@ enova_status enova_train_init(const enova_train_config *config, const enova_dete
  *   labels    device [B] float: +1 or -1
  *   eps       device [B][L] float: the reparameterisation noise
  *   out_info  device [4] float or NULL: J, mean log p, mean KL of the normal windows, beta(k)
- * Asynchronous on `stream`. Errors: EINVAL, ENOMEM, EHIP.
+ * Asynchronous on `stream`. The step's launches are captured once into a HIP graph (on a stream
+ * of the trainer's own) and the graph is replayed while V, labels, eps, out_info and the batch
+ * size stay the same (the contents may change between steps); any other arguments capture it
+ * again, which first waits for the device. Steps taken with timing on, or with graph replay
+ * off, launch their kernels one by one on `stream`; a caller that captures the step into a
+ * graph of its own turns replay off. Errors: EINVAL, ENOMEM, EHIP.
  */
 enova_status enova_train_step(enova_trainer t, const float *V, const float *labels, const float *eps,
                               int32_t batch, float *out_info, hipStream_t stream);
+
+/* Graph replay of the step (see enova_train_step): on (non-zero, the default) or off. Turning it
+ * off frees the captured graph (waiting for the device). Errors: EINVAL. */
+enova_status enova_train_set_graph(enova_trainer t, int32_t enable);
 
 /* Copy the current parameters, or the last step's gradients of J, into HOST arrays (each may be
  * NULL). Synchronises `stream`. */

@@ -27,7 +27,7 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_detect_kernel_kind", "enova_stream_create", "enova_stream_push",
            "enova_stream_state", "enova_stream_kernel_times", "enova_stream_destroy",
            "enova_train_init", "enova_train_step", "enova_train_params_get", "enova_train_grads_get",
-           "enova_train_set_timing", "enova_train_kernel_times", "enova_train_destroy",
+           "enova_train_set_timing", "enova_train_set_graph", "enova_train_kernel_times", "enova_train_destroy",
            "enova_detect_score_ext", "enova_detect_ext_time", "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
            "enova_config_scan", "enova_config_recommend", "enova_config_set_timing", "enova_config_kernel_time", "enova_status_str", "enova_last_error"]
 
@@ -105,6 +105,7 @@ def lib():
     L.enova_train_params_get.argtypes = [P, ctypes.POINTER(enova_train_params), P]
     L.enova_train_grads_get.argtypes = [P, ctypes.POINTER(enova_train_params), P]
     L.enova_train_set_timing.argtypes = [P, I32]
+    L.enova_train_set_graph.argtypes = [P, I32]
     L.enova_train_kernel_times.argtypes = [P, P, P]
     L.enova_train_destroy.argtypes = [P]
     L.enova_detect_score_ext.argtypes = [P, P, P, P, I32, I64, P, P, I32, P, P, P, P, P]
@@ -315,6 +316,10 @@ def enova_train_grads_get(thandle, shapes, stream=None):
 
 def enova_train_set_timing(thandle, enable):
     _check(lib().enova_train_set_timing(ctypes.c_void_p(thandle), int(bool(enable))), "enova_train_set_timing")
+
+
+def enova_train_set_graph(thandle, enable):
+    _check(lib().enova_train_set_graph(ctypes.c_void_p(thandle), int(bool(enable))), "enova_train_set_graph")
 
 
 def enova_train_kernel_times(thandle):
@@ -551,6 +556,9 @@ class Trainer:
 
     def set_timing(self, enable=True):
         enova_train_set_timing(self.handle, enable)
+
+    def set_graph(self, enable=True):
+        enova_train_set_graph(self.handle, enable)
 
     def kernel_times(self):
         return enova_train_kernel_times(self.handle)

@@ -470,12 +470,15 @@ __global__ __launch_bounds__(256) void k_recon(float *__restrict__ out, const fl
 // One block: the KL weight of this step from the PI controller, and the step's summary
 // (J, mean log p, mean KL of the normal windows, beta). State: st[0] = the integral term.
 // An anomalous window enters J through -log p capped at margin + D/2 log 2 pi.
+// It also advances the Adam step count k (held on the device, so a step's launches carry no
+// per-step host value) and writes the bias corrections 1/(1 - b1^k), 1/(1 - b2^k) to corr.
 __global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, const float *__restrict__ logp,
                                               const float *__restrict__ labels, int rows, float kl_set,
                                               float kp, float ki, float beta_min, float beta_max,
                                               float margin, float half_d_log2pi,
                                               float *__restrict__ st, float *__restrict__ beta_out,
-                                              float *__restrict__ info)
+                                              float *__restrict__ info, float b1, float b2,
+                                              long long *__restrict__ step, float *__restrict__ corr)
 {
     __shared__ double r_kl[1024], r_n[1024], r_lp[1024], r_la[1024], r_kn[1024];
     double skl = 0.0, sn = 0.0, slp = 0.0, sla = 0.0, skn = 0.0;
@@ -522,6 +525,10 @@ __global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, con
         b = b < beta_min ? beta_min : (b > beta_max ? beta_max : b);
         st[0] = static_cast<float>(integ);
         beta_out[0] = static_cast<float>(b);
+        const long long k_adam = step[0] + 1;
+        step[0] = k_adam;
+        corr[0] = static_cast<float>(1.0 / (1.0 - pow(static_cast<double>(b1), static_cast<double>(k_adam))));
+        corr[1] = static_cast<float>(1.0 / (1.0 - pow(static_cast<double>(b2), static_cast<double>(k_adam))));
         if (info) {
             info[0] = static_cast<float>(-(r_la[0] - b * r_kn[0]) / rows);
             info[1] = static_cast<float>(r_lp[0] / rows);
@@ -554,8 +561,10 @@ __global__ __launch_bounds__(256) void k_latent_grad(const float *__restrict__ g
 
 __global__ __launch_bounds__(256) void k_adam(float *__restrict__ p, const float *__restrict__ g,
                                               float *__restrict__ m, float *__restrict__ v, int64_t total,
-                                              float lr, float b1, float b2, float eps, float c1, float c2)
+                                              float lr, float b1, float b2, float eps,
+                                              const float *__restrict__ corr)
 {
+    const float c1 = corr[0], c2 = corr[1];
     for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
         const float ge = g[e];
         const float me = b1 * m[e] + (1.0f - b1) * ge;
@@ -736,11 +745,12 @@ hipError_t launch_recon(float *out, const float *bd2, const float *V, const floa
 }
 
 hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
-                       const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st)
+                       const TrainHyper &h, float *state, float *beta, float *info, long long *step, float *corr,
+                       hipStream_t st)
 {
     hipLaunchKernelGGL(k_beta, dim3(1), dim3(1024), 0, st, kl, logp, labels, rows, h.kl_set, h.kp, h.ki,
                        h.beta_min, h.beta_max, h.margin, 0.5f * static_cast<float>(D) * kLog2Pi, state, beta,
-                       info);
+                       info, h.b1, h.b2, step, corr);
     return hipGetLastError();
 }
 
@@ -753,12 +763,10 @@ hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, cons
 }
 
 hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
-                       int64_t step, hipStream_t st)
+                       const float *corr, hipStream_t st)
 {
-    const double c1 = 1.0 / (1.0 - std::pow(static_cast<double>(h.b1), static_cast<double>(step)));
-    const double c2 = 1.0 / (1.0 - std::pow(static_cast<double>(h.b2), static_cast<double>(step)));
     hipLaunchKernelGGL(k_adam, dim3(blocks_for(total)), dim3(256), 0, st, p, g, m, v, total, h.lr, h.b1, h.b2,
-                       h.eps, static_cast<float>(c1), static_cast<float>(c2));
+                       h.eps, corr);
     return hipGetLastError();
 }
 

@@ -39,12 +39,15 @@ hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *s
                          int L, hipStream_t st);
 hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
                         int rows, int D, float margin, hipStream_t st);
+// state[0] = the controller's integral term, beta = this step's KL weight; step = the Adam step
+// count (advanced here), corr [2] = its bias corrections for launch_adam.
 hipError_t launch_beta(const float *kl, const float *logp, const float *labels, int rows, int D,
-                       const TrainHyper &h, float *state, float *beta, float *info, hipStream_t st);
+                       const TrainHyper &h, float *state, float *beta, float *info, long long *step, float *corr,
+                       hipStream_t st);
 // gz: [rows][L] = dJ/dz; gml: [rows][2L] = [dJ/dmu | dJ/dlv].
 hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, const float *sd, const float *eps,
                               const float *labels, const float *beta, int rows, int L, hipStream_t st);
 hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
-                       int64_t step, hipStream_t st);
+                       const float *corr, hipStream_t st);
 
 }  // namespace enova

@@ -1,9 +1,10 @@
 // Host side of the training entry points (Section IV-B, Eq. (9)): parameter, gradient and Adam
-// buffers, the batch workspace, and the launch sequence of one ELBO step.
+// buffers, the batch workspace, and the launch sequence of one ELBO step, replayed as a HIP graph.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
+#include <cstdint>
 #include <new>
 
 #include "enova_detect.h"
@@ -25,10 +26,10 @@ struct enova_trainer_s {
     int device = 0;
     int D = 0, H = 0, L = 0, act = 0;
     TrainHyper hyper{};
-    int64_t step = 0;
     int64_t off[P_COUNT] = {}, size[P_COUNT] = {}, total = 0;   // flat-buffer layout (floats)
     float *p = nullptr, *g = nullptr, *m = nullptr, *v = nullptr;
-    float *state = nullptr;          // [0] PI integral, [1] beta of the step
+    float *state = nullptr;          // [0] PI integral, [1] beta of the step, [2..3] Adam bias corrections
+    long long *step = nullptr;       // Adam step count, advanced on the device
     // batch workspace
     int cap = 0;
     float *a1 = nullptr, *h = nullptr, *a2 = nullptr, *hd = nullptr, *gh = nullptr;   // [B][H]
@@ -43,6 +44,15 @@ struct enova_trainer_s {
     bool timed = false;
     int n_events = 0;
     hipEvent_t ev[kMaxEvents] = {};
+    // graph replay: the launches of one step, captured on the private stream `gstream` for one set of
+    // step arguments and buffer generation, replayed while both stay the same
+    bool use_graph = true;
+    hipStream_t gstream = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    const void *key[4] = {};         // V, labels, eps, out_info of the captured step
+    int key_batch = 0;
+    uint64_t gen = 1, key_gen = 0;   // gen advances with every reallocation of a step buffer
 };
 
 namespace {
@@ -51,8 +61,14 @@ void free_trainer(enova_trainer t)
 {
     if (!t)
         return;
-    void *ptrs[] = {t->p,  t->g,  t->m,  t->v,  t->state, t->a1,  t->h,  t->a2,   t->hd,
-                    t->gh, t->ml, t->gml, t->sd, t->z,  t->gz,    t->out, t->kl, t->logp, t->work};
+    if (t->exec)
+        (void)hipGraphExecDestroy(t->exec);
+    if (t->graph)
+        (void)hipGraphDestroy(t->graph);
+    if (t->gstream)
+        (void)hipStreamDestroy(t->gstream);
+    void *ptrs[] = {t->p,  t->g,  t->m,  t->v,  t->state, t->step, t->a1,  t->h,  t->a2,   t->hd,
+                    t->gh, t->ml, t->gml, t->sd, t->z,  t->gz,    t->out,  t->kl, t->logp, t->work};
     for (void *q : ptrs)
         if (q)
             (void)hipFree(q);
@@ -90,6 +106,7 @@ enova_status ensure_batch(enova_trainer t, int B)
     enova_status st;
     const int64_t ws = workspace_floats(t, B);
     if (ws > t->work_cap) {
+        ++t->gen;
         (void)hipFree(t->work);
         t->work = nullptr;
         t->work_cap = 0;
@@ -99,6 +116,7 @@ enova_status ensure_batch(enova_trainer t, int B)
     }
     if (B <= t->cap)
         return ENOVA_OK;
+    ++t->gen;
     float **bh[] = {&t->a1, &t->h, &t->a2, &t->hd, &t->gh};
     float **bl[] = {&t->sd, &t->z, &t->gz};
     float **b2[] = {&t->ml, &t->gml};
@@ -188,11 +206,16 @@ enova_status enova_train_init(const enova_train_config *c, const enova_detect_we
     enova_status st;
     if ((st = alloc_floats(&t->p, total)) != ENOVA_OK || (st = alloc_floats(&t->g, total)) != ENOVA_OK ||
         (st = alloc_floats(&t->m, total)) != ENOVA_OK || (st = alloc_floats(&t->v, total)) != ENOVA_OK ||
-        (st = alloc_floats(&t->state, 2)) != ENOVA_OK) {
+        (st = alloc_floats(&t->state, 4)) != ENOVA_OK) {
         free_trainer(t);
         return st;
     }
-    hipError_t e = hipSuccess;
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&t->step), sizeof(long long));
+    if (e != hipSuccess) {
+        t->step = nullptr;
+        free_trainer(t);
+        return fail(ENOVA_ENOMEM, "hipMalloc(step count): %s", hipGetErrorString(e));
+    }
     for (int k = 0; k < P_COUNT && e == hipSuccess; ++k)
         e = hipMemcpy(t->p + t->off[k], src[k], sizes[k] * sizeof(float), hipMemcpyHostToDevice);
     if (e == hipSuccess)
@@ -202,7 +225,11 @@ enova_status enova_train_init(const enova_train_config *c, const enova_detect_we
     if (e == hipSuccess)
         e = hipMemset(t->g, 0, total * sizeof(float));
     if (e == hipSuccess)
-        e = hipMemset(t->state, 0, 2 * sizeof(float));
+        e = hipMemset(t->state, 0, 4 * sizeof(float));
+    if (e == hipSuccess)
+        e = hipMemset(t->step, 0, sizeof(long long));
+    if (e == hipSuccess)
+        e = hipStreamCreateWithFlags(&t->gstream, hipStreamNonBlocking);
     if (e != hipSuccess) {
         free_trainer(t);
         return hip_fail(e, "trainer upload");
@@ -211,17 +238,14 @@ enova_status enova_train_init(const enova_train_config *c, const enova_detect_we
     return ENOVA_OK;
 }
 
-enova_status enova_train_step(enova_trainer t, const float *V, const float *labels, const float *eps,
-                              int32_t B, float *info, hipStream_t s)
+}  // extern "C"
+
+namespace {
+
+// The launches of one step on stream s (events around the products when timing is on).
+hipError_t enqueue_step(enova_trainer t, const float *V, const float *labels, const float *eps, int B,
+                        float *info, hipStream_t s)
 {
-    if (!t || !V || !labels || !eps)
-        return fail(ENOVA_EINVAL, "NULL argument");
-    if (B < 1)
-        return fail(ENOVA_EINVAL, "batch must be >= 1");
-    DeviceGuard dg(t->device);
-    enova_status st = ensure_batch(t, B);
-    if (st != ENOVA_OK)
-        return st;
     const int D = t->D, H = t->H, L = t->L, act = t->act;
     float *P = t->p, *G = t->g;
     const int64_t *o = t->off;
@@ -235,7 +259,6 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
         if (t->timed && ne < enova_trainer_s::kMaxEvents)
             run(hipEventRecord(t->ev[ne++], s));
     };
-    // every product of the step, bracketed by events when timing is on
     // every product of the step; with timing on, its product kernel is bracketed by two events
     auto gemm = [&](const GemmEpilogue &ep, const float *A, int64_t ai, int64_t ak, const float *Bm, int64_t bk,
                     int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum) {
@@ -248,19 +271,19 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
     };
     const GemmEpilogue plain{};
     auto bias_act = [&](const float *bias, float *out) {
-        GemmEpilogue e;
-        e.kind = kEpiBiasAct;
-        e.act = act;
-        e.bias = bias;
-        e.out2 = out;
-        return e;
+        GemmEpilogue ep;
+        ep.kind = kEpiBiasAct;
+        ep.act = act;
+        ep.bias = bias;
+        ep.out2 = out;
+        return ep;
     };
     auto dact = [&](const float *pre) {
-        GemmEpilogue e;
-        e.kind = kEpiDact;
-        e.act = act;
-        e.pre = pre;
-        return e;
+        GemmEpilogue ep;
+        ep.kind = kEpiDact;
+        ep.act = act;
+        ep.pre = pre;
+        return ep;
     };
     mark();
     // forward: a1 = V W1^T + b1, h = act(a1)
@@ -272,8 +295,9 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
     gemm(bias_act(P + o[P_BD1], t->hd), t->z, L, 1, P + o[P_WD1], 1, L, t->a2, H, B, H, L, nullptr);
     gemm(plain, t->hd, H, 1, P + o[P_WD2], 1, H, t->out, D, B, D, H, nullptr);
     run(launch_recon(t->out, P + o[P_BD2], V, labels, t->logp, B, D, t->hyper.margin, s));
-    // beta(k) from this batch's KL, before the backward pass
-    run(launch_beta(t->kl, t->logp, labels, B, D, t->hyper, t->state, t->state + 1, info, s));
+    // beta(k) from this batch's KL, before the backward pass; the Adam step count and corrections
+    run(launch_beta(t->kl, t->logp, labels, B, D, t->hyper, t->state, t->state + 1, info, t->step, t->state + 2,
+                    s));
     // backward through the decoder (G = dJ/dm' in out); bias gradients are the row sums of G^T
     gemm(plain, t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, G + o[P_BD2]);    // dWd2 = G^T hd
     gemm(dact(t->a2), t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, nullptr);   // dJ/da2
@@ -285,13 +309,87 @@ enova_status enova_train_step(enova_trainer t, const float *V, const float *labe
     gemm(dact(t->a1), t->gml, 2 * L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, 2 * L, nullptr);
     gemm(plain, t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, G + o[P_B1]);            // dW1 = G^T V
     // Adam
-    t->step += 1;
-    run(launch_adam(P, G, t->m, t->v, t->total, t->hyper, t->step, s));
+    run(launch_adam(P, G, t->m, t->v, t->total, t->hyper, t->state + 2, s));
     mark();
     t->n_events = ne;
+    return e;
+}
+
+// Free the captured graph; a replay of it may still be in flight, so the device is drained first.
+void drop_graph(enova_trainer t)
+{
+    if (t->exec) {
+        (void)hipDeviceSynchronize();
+        (void)hipGraphExecDestroy(t->exec);
+    }
+    if (t->graph)
+        (void)hipGraphDestroy(t->graph);
+    t->exec = nullptr;
+    t->graph = nullptr;
+    t->key_gen = 0;
+}
+
+// Capture the step's launches on the private stream (nothing runs while capturing) and
+// instantiate them; on any failure no graph is kept.
+hipError_t capture_step(enova_trainer t, const float *V, const float *labels, const float *eps, int B, float *info)
+{
+    drop_graph(t);
+    hipError_t e = hipStreamBeginCapture(t->gstream, hipStreamCaptureModeThreadLocal);
     if (e != hipSuccess)
-        return hip_fail(e, "training kernels");
-    return ENOVA_OK;
+        return e;
+    const hipError_t le = enqueue_step(t, V, labels, eps, B, info, t->gstream);
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(t->gstream, &g);
+    if (le != hipSuccess || e != hipSuccess) {
+        if (g)
+            (void)hipGraphDestroy(g);
+        return le != hipSuccess ? le : e;
+    }
+    hipGraphExec_t x = nullptr;
+    if ((e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0)) != hipSuccess) {
+        (void)hipGraphDestroy(g);
+        return e;
+    }
+    t->graph = g;
+    t->exec = x;
+    t->key[0] = V;
+    t->key[1] = labels;
+    t->key[2] = eps;
+    t->key[3] = info;
+    t->key_batch = B;
+    t->key_gen = t->gen;
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+enova_status enova_train_step(enova_trainer t, const float *V, const float *labels, const float *eps,
+                              int32_t B, float *info, hipStream_t s)
+{
+    if (!t || !V || !labels || !eps)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    if (B < 1)
+        return fail(ENOVA_EINVAL, "batch must be >= 1");
+    DeviceGuard dg(t->device);
+    enova_status st = ensure_batch(t, B);
+    if (st != ENOVA_OK)
+        return st;
+    if (t->timed || !t->use_graph) {
+        const hipError_t e = enqueue_step(t, V, labels, eps, B, info, s);
+        return e == hipSuccess ? ENOVA_OK : hip_fail(e, "training kernels");
+    }
+    t->n_events = 0;
+    const bool same = t->exec && t->key_gen == t->gen && t->key_batch == B && t->key[0] == V &&
+                      t->key[1] == labels && t->key[2] == eps && t->key[3] == info;
+    if (!same) {
+        const hipError_t e = capture_step(t, V, labels, eps, B, info);
+        if (e != hipSuccess)
+            return hip_fail(e, "capturing the training step");
+    }
+    const hipError_t e = hipGraphLaunch(t->exec, s);
+    return e == hipSuccess ? ENOVA_OK : hip_fail(e, "hipGraphLaunch");
 }
 
 enova_status enova_train_params_get(enova_trainer t, const enova_train_params *out, hipStream_t stream)
@@ -308,6 +406,17 @@ enova_status enova_train_grads_get(enova_trainer t, const enova_train_params *ou
         return fail(ENOVA_EINVAL, "NULL argument");
     DeviceGuard dg(t->device);
     return copy_out(t, t->g, out, stream);
+}
+
+enova_status enova_train_set_graph(enova_trainer t, int32_t enable)
+{
+    if (!t)
+        return fail(ENOVA_EINVAL, "NULL trainer");
+    DeviceGuard dg(t->device);
+    t->use_graph = enable != 0;
+    if (!t->use_graph)
+        drop_graph(t);
+    return ENOVA_OK;
 }
 
 enova_status enova_train_set_timing(enova_trainer t, int32_t enable)

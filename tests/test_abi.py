@@ -126,6 +126,7 @@ def test_training_entry_points_reject_bad_arguments(over):
     assert L.enova_train_params_get(None, None, None) == binding.ENOVA_EINVAL
     assert L.enova_train_grads_get(None, None, None) == binding.ENOVA_EINVAL
     assert L.enova_train_set_timing(None, 1) == binding.ENOVA_EINVAL
+    assert L.enova_train_set_graph(None, 1) == binding.ENOVA_EINVAL
     a, b = ctypes.c_double(), ctypes.c_double()
     assert L.enova_train_kernel_times(None, ctypes.byref(a), ctypes.byref(b)) == binding.ENOVA_EINVAL
     assert L.enova_train_destroy(None) == binding.ENOVA_OK

@@ -232,3 +232,44 @@ def test_batch_size_may_change_between_steps():
                                               act=cfg.act, **HYPER)
         _check_info(info.cpu().numpy().astype(np.float64), ref, 1e-4, f"B={B}")
     tr.close()
+
+
+def test_graph_replay_matches_eager_steps():
+    """The default step replays a captured HIP graph; a second trainer launches every kernel
+    eagerly. Same seeded batches, same order: after every step the summary, and at the end the
+    parameters and gradients, are bit-identical. Between replays the stream also runs unrelated
+    eager work and the host synchronises; new batch pointers and a new batch size re-capture."""
+    import torch
+    cfg = _cfg(8, 32, 64, 16, "relu")
+    p0 = _init(cfg)
+    ga, eb = _trainer(cfg, p0), _trainer(cfg, p0)
+    eb.set_graph(False)
+    b1 = wl.training_batch(cfg, 2000, seed=401)
+    b2 = wl.training_batch(cfg, 700, seed=402)
+    d1 = [_dev(a) for a in (b1.V, b1.labels, b1.eps)]
+    d2 = [_dev(a) for a in (b2.V, b2.labels, b2.eps)]
+    ia = torch.zeros(4, dtype=torch.float32, device="cuda")
+    ib = torch.zeros(4, dtype=torch.float32, device="cuda")
+    junk = torch.randn(1 << 20, device="cuda")
+    plan = [d1, d1, d1, d2, d2, d1, d1]
+    for k, d in enumerate(plan):
+        log(f"graph replay step {k} batch {d[0].shape[0]}")
+        ga.step(*d, ia)
+        junk.mul_(0.5).add_(1.0)                      # eager work between replays
+        eb.step(*d, ib)
+        torch.cuda.synchronize()
+        if k == 2:                                    # same pointers, contents rewritten in place
+            d1[0].copy_(_dev(wl.training_batch(cfg, 2000, seed=403).V))
+        assert np.array_equal(ia.cpu().numpy(), ib.cpu().numpy()), k
+    pa, pb = ga.params(), eb.params()
+    qa, qb = ga.grads(), eb.grads()
+    for name in elbo.PARAMS:
+        assert np.array_equal(pa[name], pb[name]), name
+        assert np.array_equal(qa[name], qb[name]), name
+    ga.set_graph(False)                               # frees the graph; eager steps continue from the same state
+    ga.step(*d2, ia)
+    eb.step(*d2, ib)
+    torch.cuda.synchronize()
+    assert np.array_equal(ia.cpu().numpy(), ib.cpu().numpy())
+    ga.close()
+    eb.close()
