@@ -17,28 +17,34 @@ namespace enova {
 
 namespace {
 
-constexpr int kGemmTile = 128;  // C tile of a block: 2 x 2 waves of 64 x 64 (2 x 2 matrix ops of 32 x 32)
+// C tile of a block (4 waves, each a grid of 32 x 32 matrix ops): 128 x 128 as 2 x 2 waves of
+// 64 x 64; for a product with at most 32 columns 128 x 32 as 4 x 1 waves of 32 x 32, and with at
+// most 32 rows (and more columns) 32 x 128 as 1 x 4 waves, so a thin product does no padded work.
+constexpr int kGemmTile = 128;
+constexpr int kGemmThin = 32;
 constexpr int kGemmK = 32;      // reduction slice staged in LDS (double-buffered)
 // LDS image of one operand slice. A k-contiguous operand is staged row-major, S[row][k] with a
 // pitch of kGemmK + 4 floats (16-byte rows, conflict-free 16-byte reads along k); a
-// row-contiguous operand is staged k-major, S[k][row] with a pitch of kGemmTile + 4 floats
+// row-contiguous operand is staged k-major, S[k][row] with a pitch of ROWS + 4 floats
 // (16-byte writes along rows, conflict-free 4-byte reads across lanes).
 constexpr int kGemmPitch = kGemmK + 4;
-constexpr int kGemmPitchT = kGemmTile + 4;
-constexpr int kGemmStage = kGemmTile * kGemmPitch > kGemmK * kGemmPitchT ? kGemmTile * kGemmPitch
-                                                                         : kGemmK * kGemmPitchT;
+constexpr int stage_floats(int rows, bool kcont)
+{
+    return kcont ? rows * kGemmPitch : kGemmK * (rows + 4);
+}
 constexpr int kGemmTargetBlocks = 256;   // split the reduction until a launch has about this many blocks
 constexpr int kGemmMinSlice = 128;       // ... but keep every slice at least this long
 constexpr int kGemmMaxSplits = 128;
 constexpr float kLog2Pi = 1.8378770664093453f;   // log(2 pi)
 
-// One operand tile of a slice: 128 rows (i of A, j of B) x 32 reduction indices, staged as
-// rows of the reduction index, S[row][k]. The operand is either "k-contiguous"
-// (X(row, k) = X[row * ld + k]) or "row-contiguous" (X(row, k) = X[k * ld + row]); each thread
-// moves four 4-float groups along the contiguous index.
-template <bool KCONT>
+// One operand tile of a slice: ROWS rows (i of A, j of B) x 32 reduction indices. The operand is
+// either "k-contiguous" (X(row, k) = X[row * ld + k]) or "row-contiguous" (X(row, k) =
+// X[k * ld + row]); each thread moves ROWS / 32 4-float groups along the contiguous index.
+template <bool KCONT, int ROWS>
 struct Stage {
-    float4 v[4];
+    static constexpr int kGroups = ROWS / 32;
+    static constexpr int kPitchT = ROWS + 4;
+    float4 v[kGroups];
 
     // Element (row, kx) of thread group q: KCONT walks k fastest (8 groups per row), else rows.
     static __device__ __forceinline__ void coords(int tid, int q, int &row, int &kx)
@@ -48,18 +54,18 @@ struct Stage {
             row = f >> 3;
             kx = (f & 7) * 4;
         } else {
-            kx = f >> 5;
-            row = (f & 31) * 4;
+            kx = f / (ROWS / 4);
+            row = (f % (ROWS / 4)) * 4;
         }
     }
 
-    // The whole 128 x 32 tile lies inside the operand and every group is 16-byte aligned: one
+    // The whole ROWS x 32 tile lies inside the operand and every group is 16-byte aligned: one
     // unconditional 16-byte load per group (a fixed instruction count, so the waits that follow
     // can count exactly how many loads are still in flight).
     __device__ __forceinline__ void load_full(const float *__restrict__ X, int64_t ld, int r0, int k0, int tid)
     {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < kGroups; ++q) {
             int row, kx;
             coords(tid, q, row, kx);
             const int64_t off = KCONT ? static_cast<int64_t>(r0 + row) * ld + (k0 + kx)
@@ -74,7 +80,7 @@ struct Stage {
     {
         if (full) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
+            for (int q = 0; q < kGroups; ++q) {
                 int row, kx;
                 coords(tid, q, row, kx);
                 const int64_t off = KCONT ? static_cast<int64_t>(r0 + row) * ld + (k0 + kx)
@@ -84,7 +90,7 @@ struct Stage {
             return;
         }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < kGroups; ++q) {
             int row, kx;
             coords(tid, q, row, kx);
             float e[4];
@@ -102,13 +108,13 @@ struct Stage {
     __device__ __forceinline__ void store(float *S, int tid) const
     {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < kGroups; ++q) {
             int row, kx;
             coords(tid, q, row, kx);
             if constexpr (KCONT)
                 *reinterpret_cast<float4 *>(&S[row * kGemmPitch + kx]) = v[q];
             else
-                *reinterpret_cast<float4 *>(&S[kx * kGemmPitchT + row]) = v[q];
+                *reinterpret_cast<float4 *>(&S[kx * kPitchT + row]) = v[q];
         }
     }
 
@@ -119,8 +125,8 @@ struct Stage {
         if constexpr (KCONT) {
             return *reinterpret_cast<const float4 *>(&S[row * kGemmPitch + k]);
         } else {
-            return make_float4(S[k * kGemmPitchT + row], S[(k + 1) * kGemmPitchT + row],
-                               S[(k + 2) * kGemmPitchT + row], S[(k + 3) * kGemmPitchT + row]);
+            return make_float4(S[k * kPitchT + row], S[(k + 1) * kPitchT + row], S[(k + 2) * kPitchT + row],
+                               S[(k + 3) * kPitchT + row]);
         }
     }
 };
@@ -202,70 +208,82 @@ __device__ __forceinline__ void epi_tile(float *__restrict__ C, int64_t ldc, int
 // to rowsum[z m + i] (the bias gradient of a weight-gradient product, read from the staged tiles).
 // Matrix op t of an 8-index group takes, in lane l, the reduction index 4 (l / 32) + t of the
 // group for both operands (a relabelling of the sum), so one 16-byte LDS read feeds four ops.
-template <bool AK, bool BK, int EPI, int ACT>
+template <bool AK, bool BK, int EPI, int ACT, int TM, int TN>
 __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, int64_t lda, bool va,
                                                  const float *__restrict__ B, int64_t ldb, bool vb,
                                                  float *__restrict__ C, int64_t ldc, float *__restrict__ rowsum,
                                                  EpiParams ep, int m, int n, int kk, int kc)
 {
-    __shared__ __align__(16) float As[2][kGemmStage];
-    __shared__ __align__(16) float Bs[2][kGemmStage];
+    // waves along the rows (WM) and columns (WN) of the tile; each covers RW x CW as MA x MB ops
+    constexpr int WM = TN == kGemmTile ? (TM == kGemmTile ? 2 : 1) : 4;
+    constexpr int WN = 4 / WM;
+    constexpr int RW = TM / WM, CW = TN / WN;
+    constexpr int MA = RW / 32, MB = CW / 32;
+    static_assert(MA >= 1 && MB >= 1 && WM * WN == 4, "tile shape");
+    __shared__ __align__(16) float As[2][stage_floats(TM, AK)];
+    __shared__ __align__(16) float Bs[2][stage_floats(TN, BK)];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wy = wave >> 1, wx = wave & 1;
+    const int wy = wave / WN, wx = wave % WN;
     const int half = lane >> 5, l32 = lane & 31;
-    const int i0 = blockIdx.y * kGemmTile, j0 = blockIdx.x * kGemmTile;
+    const int i0 = blockIdx.y * TM, j0 = blockIdx.x * TN;
     const int kbeg = blockIdx.z * kc;
     const int kend = min(kk, kbeg + kc);
     C += static_cast<int64_t>(blockIdx.z) * m * ldc;
-    bool live_a[2], live_b[2];
+    bool live_a[MA], live_b[MB];
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
-        live_a[a] = i0 + wy * 64 + a * 32 < m;
-        live_b[a] = j0 + wx * 64 + a * 32 < n;
-    }
+    for (int a = 0; a < MA; ++a)
+        live_a[a] = i0 + wy * RW + a * 32 < m;
+#pragma unroll
+    for (int b = 0; b < MB; ++b)
+        live_b[b] = j0 + wx * CW + b * 32 < n;
     const bool sums = rowsum != nullptr && blockIdx.x == 0 && wx == 0;
-    v16f acc[2][2];
+    v16f acc[MA][MB];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < MA; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < MB; ++b)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
                 acc[a][b][r] = 0.0f;
-    float rs[2] = {0.0f, 0.0f};
+    float rs[MA];
+#pragma unroll
+    for (int a = 0; a < MA; ++a)
+        rs[a] = 0.0f;
     // Two register stages: the global loads of slice s + 2 are issued before slice s is computed,
     // so each load has two slices of matrix work to arrive in.
-    Stage<AK> sa[2];
-    Stage<BK> sb[2];
+    using SA = Stage<AK, TM>;
+    using SB = Stage<BK, TN>;
+    SA sa[2];
+    SB sb[2];
     const int ns = kend > kbeg ? (kend - kbeg + kGemmK - 1) / kGemmK : 0;
-    const bool rows_a = va && i0 + kGemmTile <= m, rows_b = vb && j0 + kGemmTile <= n;
+    const bool rows_a = va && i0 + TM <= m, rows_b = vb && j0 + TN <= n;
     auto compute = [&](int buf) __attribute__((always_inline)) {
         // every operand read of the slice is issued before the first matrix op
-        float4 av[kGemmK / 8][2], bv[kGemmK / 8][2];
+        float4 av[kGemmK / 8][MA], bv[kGemmK / 8][MB];
 #pragma unroll
         for (int g = 0; g < kGemmK / 8; ++g) {
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
-                av[g][a] = Stage<AK>::operand(As[buf], wy * 64 + a * 32 + l32, g, half);
+            for (int a = 0; a < MA; ++a)
+                av[g][a] = SA::operand(As[buf], wy * RW + a * 32 + l32, g, half);
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-                bv[g][b] = Stage<BK>::operand(Bs[buf], wx * 64 + b * 32 + l32, g, half);
+            for (int b = 0; b < MB; ++b)
+                bv[g][b] = SB::operand(Bs[buf], wx * CW + b * 32 + l32, g, half);
         }
 #pragma unroll
         for (int g = 0; g < kGemmK / 8; ++g) {
             // row sums of A (used only when requested; cheaper to always form than to branch)
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < MA; ++a)
                 rs[a] += (av[g][a].x + av[g][a].y) + (av[g][a].z + av[g][a].w);
             // the four ops of one accumulator are interleaved with the other accumulators' ops
 #pragma unroll
             for (int t = 0; t < 4; ++t)
 #pragma unroll
-                for (int a = 0; a < 2; ++a)
+                for (int a = 0; a < MA; ++a)
 #pragma unroll
-                    for (int b = 0; b < 2; ++b) {
+                    for (int b = 0; b < MB; ++b) {
                         const float4 &x4 = av[g][a], &y4 = bv[g][b];
                         const float x = t == 0 ? x4.x : t == 1 ? x4.y : t == 2 ? x4.z : x4.w;
                         const float y = t == 0 ? y4.x : t == 1 ? y4.y : t == 2 ? y4.z : y4.w;
@@ -277,7 +295,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
     // (FULL) and bounds-checked loads otherwise.
     auto run = [&](auto full_tag) __attribute__((always_inline)) {
         constexpr bool FULL = decltype(full_tag)::value;
-        auto fetch = [&](int sl, Stage<AK> &ra, Stage<BK> &rb) __attribute__((always_inline)) {
+        auto fetch = [&](int sl, SA &ra, SB &rb) __attribute__((always_inline)) {
             const int k1 = kbeg + sl * kGemmK;
             if constexpr (FULL) {
                 ra.load_full(A, lda, i0, k1, tid);
@@ -291,9 +309,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
         // one slice: slice s is in LDS buffer s & 1 and slice s + 1 in registers `nx`; `fr` is free
         // With FULL every step issues the same loads and stores (past the end it re-reads the last
         // slice and fills a buffer nobody reads), so the wait before the stores counts exactly the
-        // eight loads just issued and lets them stay in flight.
-        auto step = [&](int s, Stage<AK> &nxa, Stage<BK> &nxb, Stage<AK> &fra, Stage<BK> &frb)
-                        __attribute__((always_inline)) {
+        // loads just issued and lets them stay in flight.
+        auto step = [&](int s, SA &nxa, SB &nxb, SA &fra, SB &frb) __attribute__((always_inline)) {
             if (FULL)
                 fetch(min(s + 2, ns - 1), fra, frb);
             else if (s + 2 < ns)
@@ -328,21 +345,21 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
         run(std::false_type{});
     if (sums) {
 #pragma unroll
-        for (int a = 0; a < 2; ++a) {
+        for (int a = 0; a < MA; ++a) {
             const float other = __shfl_xor(rs[a], 32);
-            const int gi = i0 + wy * 64 + a * 32 + l32;
+            const int gi = i0 + wy * RW + a * 32 + l32;
             if (half == 0 && gi < m)
                 rowsum[static_cast<int64_t>(blockIdx.z) * m + gi] = rs[a] + other;
         }
     }
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < MA; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+        for (int b = 0; b < MB; ++b) {
             if (!(live_a[a] && live_b[b]))
                 continue;
-            const int si = i0 + wy * 64 + a * 32, gj = j0 + wx * 64 + b * 32 + l32;
-            if (si + 32 <= m && j0 + wx * 64 + b * 32 + 32 <= n) {
+            const int si = i0 + wy * RW + a * 32, sj = j0 + wx * CW + b * 32, gj = sj + l32;
+            if (si + 32 <= m && sj + 32 <= n) {
                 // whole sub-tile inside C: the epilogue's reads are issued together
                 epi_tile<EPI, ACT>(C, ldc, si, gj, half, acc[a][b], ep);
             } else {
@@ -583,9 +600,22 @@ unsigned blocks_for(int64_t total)
 
 }  // namespace
 
+// The block tile of an m x n product (rows, columns): thin products get a 32-wide side.
+static void gemm_tile(int m, int n, int &tm, int &tn)
+{
+    tm = kGemmTile;
+    tn = kGemmTile;
+    if (n <= kGemmThin)
+        tn = kGemmThin;
+    else if (m <= kGemmThin)
+        tm = kGemmThin;
+}
+
 static int gemm_splits(int m, int n, int k)
 {
-    const int64_t tiles = static_cast<int64_t>((m + kGemmTile - 1) / kGemmTile) * ((n + kGemmTile - 1) / kGemmTile);
+    int tm, tn;
+    gemm_tile(m, n, tm, tn);
+    const int64_t tiles = static_cast<int64_t>((m + tm - 1) / tm) * ((n + tn - 1) / tn);
     if (tiles >= kGemmTargetBlocks / 2)
         return 1;
     const int by_k = (k + kGemmMinSlice - 1) / kGemmMinSlice;
@@ -605,8 +635,17 @@ template <bool AK, bool BK, int EPI, int ACT>
 void gemm_run(dim3 grid, hipStream_t st, const float *A, int64_t lda, bool va, const float *B, int64_t ldb, bool vb,
               float *C, int64_t ldc, float *rowsum, const EpiParams &ep, int m, int n, int k, int kc)
 {
-    hipLaunchKernelGGL((k_gemm<AK, BK, EPI, ACT>), grid, dim3(256), 0, st, A, lda, va, B, ldb, vb, C, ldc, rowsum,
-                       ep, m, n, k, kc);
+    int tm, tn;
+    gemm_tile(m, n, tm, tn);
+    if (tn == kGemmThin)
+        hipLaunchKernelGGL((k_gemm<AK, BK, EPI, ACT, kGemmTile, kGemmThin>), grid, dim3(256), 0, st, A, lda, va, B,
+                           ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
+    else if (tm == kGemmThin)
+        hipLaunchKernelGGL((k_gemm<AK, BK, EPI, ACT, kGemmThin, kGemmTile>), grid, dim3(256), 0, st, A, lda, va, B,
+                           ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
+    else
+        hipLaunchKernelGGL((k_gemm<AK, BK, EPI, ACT, kGemmTile, kGemmTile>), grid, dim3(256), 0, st, A, lda, va, B,
+                           ldb, vb, C, ldc, rowsum, ep, m, n, k, kc);
 }
 
 template <int EPI, int ACT>
@@ -691,8 +730,10 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
         --splits;
     const int kc = splits > 1 ? ((k + splits - 1) / splits + kGemmK - 1) / kGemmK * kGemmK : std::max(k, 1);
     const int used = splits > 1 ? (k + kc - 1) / kc : 1;
-    const dim3 grid(static_cast<unsigned>((n + kGemmTile - 1) / kGemmTile),
-                    static_cast<unsigned>((m + kGemmTile - 1) / kGemmTile), static_cast<unsigned>(used));
+    int tm, tn;
+    gemm_tile(m, n, tm, tn);
+    const dim3 grid(static_cast<unsigned>((n + tn - 1) / tn), static_cast<unsigned>((m + tm - 1) / tm),
+                    static_cast<unsigned>(used));
     const EpiParams ep{epi.bias, epi.out2, epi.pre};
     hipError_t e = hipSuccess;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess)
