@@ -600,15 +600,26 @@ unsigned blocks_for(int64_t total)
 
 }  // namespace
 
-// The block tile of an m x n product (rows, columns): thin products get a 32-wide side.
+// The block tile of an m x n product (rows, columns): thin products get a 32-wide side, and so
+// does one whose 128 x 128 tiles would leave most of the chip idle (its longer side is cut into
+// 4x as many tiles, so it needs fewer reduction slices, or none).
 static void gemm_tile(int m, int n, int &tm, int &tn)
 {
     tm = kGemmTile;
     tn = kGemmTile;
-    if (n <= kGemmThin)
+    if (n <= kGemmThin) {
         tn = kGemmThin;
-    else if (m <= kGemmThin)
+    } else if (m <= kGemmThin) {
         tm = kGemmThin;
+    } else {
+        const int64_t tiles = static_cast<int64_t>((m + kGemmTile - 1) / kGemmTile) * ((n + kGemmTile - 1) / kGemmTile);
+        if (tiles < kGemmTargetBlocks / 2) {
+            if (m >= n)
+                tm = kGemmThin;
+            else
+                tn = kGemmThin;
+        }
+    }
 }
 
 static int gemm_splits(int m, int n, int k)
