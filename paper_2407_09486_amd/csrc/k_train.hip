@@ -28,6 +28,9 @@ constexpr int kGemmK = 32;      // reduction slice staged in LDS (double-buffere
 // row-contiguous operand is staged k-major, S[k][row] with a pitch of ROWS + 4 floats
 // (16-byte writes along rows, conflict-free 4-byte reads across lanes).
 constexpr int kGemmPitch = kGemmK + 4;
+// Largest leading dimension of an operand loaded with 32-bit in-tile offsets (128 rows or 32
+// reduction indices of it stay below 2^31 elements); larger ones take the bounds-checked loads.
+constexpr int64_t kGemmMaxLd32 = int64_t(1) << 24;
 constexpr int stage_floats(int rows, bool kcont)
 {
     return kcont ? rows * kGemmPitch : kGemmK * (rows + 4);
@@ -62,15 +65,19 @@ struct Stage {
     // The whole ROWS x 32 tile lies inside the operand and every group is 16-byte aligned: one
     // unconditional 16-byte load per group (a fixed instruction count, so the waits that follow
     // can count exactly how many loads are still in flight).
+    // The tile's first element is a uniform base; each group adds a 32-bit offset that does not
+    // change between slices (the caller guarantees ld <= kGemmMaxLd32), so a slice's loads need
+    // no per-load 64-bit address arithmetic.
     __device__ __forceinline__ void load_full(const float *__restrict__ X, int64_t ld, int r0, int k0, int tid)
     {
+        const float *base = KCONT ? X + static_cast<int64_t>(r0) * ld + k0 : X + static_cast<int64_t>(k0) * ld + r0;
+        const int ld32 = static_cast<int>(ld);
 #pragma unroll
         for (int q = 0; q < kGroups; ++q) {
             int row, kx;
             coords(tid, q, row, kx);
-            const int64_t off = KCONT ? static_cast<int64_t>(r0 + row) * ld + (k0 + kx)
-                                      : static_cast<int64_t>(k0 + kx) * ld + (r0 + row);
-            v[q] = *reinterpret_cast<const float4 *>(X + off);
+            const int off = KCONT ? row * ld32 + kx : kx * ld32 + row;
+            v[q] = *reinterpret_cast<const float4 *>(base + off);
         }
     }
 
@@ -79,14 +86,7 @@ struct Stage {
                                          int k0, int kend, int tid)
     {
         if (full) {
-#pragma unroll
-            for (int q = 0; q < kGroups; ++q) {
-                int row, kx;
-                coords(tid, q, row, kx);
-                const int64_t off = KCONT ? static_cast<int64_t>(r0 + row) * ld + (k0 + kx)
-                                          : static_cast<int64_t>(k0 + kx) * ld + (r0 + row);
-                v[q] = *reinterpret_cast<const float4 *>(X + off);
-            }
+            load_full(X, ld, r0, k0, tid);
             return;
         }
 #pragma unroll
@@ -332,12 +332,21 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
             sa[0].store(As[0], tid);
             sb[0].store(Bs[0], tid);
         }
+        // FULL: let the prologue's loads land (vmcnt(0), once per block). Otherwise the wait
+        // counters merged at the head of the slice loop still see them, and a register the loop
+        // reuses for addresses makes every trip wait for all loads in flight.
+        if constexpr (FULL)
+            __builtin_amdgcn_s_waitcnt(0x0F70);
         __syncthreads();
-        for (int s = 0; s < ns; s += 2) {
+        // pairs of steps as straight-line code (a conditional second step lets the compiler
+        // merge both steps' loads at the top of the pair, which shortens the prefetch distance)
+        int s = 0;
+        for (; s + 1 < ns; s += 2) {
             step(s, sa[1], sb[1], sa[0], sb[0]);
-            if (s + 1 < ns)
-                step(s + 1, sa[0], sb[0], sa[1], sb[1]);
+            step(s + 1, sa[0], sb[0], sa[1], sb[1]);
         }
+        if (s < ns)
+            step(s, sa[1], sb[1], sa[0], sb[0]);
     };
     if (rows_a && rows_b && (kend - kbeg) % kGemmK == 0)
         run(std::true_type{});
@@ -732,8 +741,8 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
         return hipErrorInvalidValue;
     const bool a_k = ak == 1, b_k = bk == 1;
     const int64_t lda = a_k ? ai : ak, ldb = b_k ? bj : bk;
-    const bool va = lda % 4 == 0 && reinterpret_cast<uintptr_t>(A) % 16 == 0;
-    const bool vb = ldb % 4 == 0 && reinterpret_cast<uintptr_t>(B) % 16 == 0;
+    const bool va = lda % 4 == 0 && lda <= kGemmMaxLd32 && reinterpret_cast<uintptr_t>(A) % 16 == 0;
+    const bool vb = ldb % 4 == 0 && ldb <= kGemmMaxLd32 && reinterpret_cast<uintptr_t>(B) % 16 == 0;
     // never more slices than the caller's workspace holds
     int splits = work ? gemm_splits(m, n, k) : 1;
     const int64_t per_slice = static_cast<int64_t>(m) * n + m;
