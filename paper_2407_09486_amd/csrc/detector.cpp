@@ -790,15 +790,21 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
         for (const auto &sh : shapes)
             wsg = std::max(wsg, gemm_workspace_floats(sh[0], sh[1], sh[2]));
     }
+    // With M a power of two <= 32 the decoder-output product reduces v - m' in its epilogue
+    // (per window, metric and column slot) instead of writing m'; `out` then holds those sums.
+    const bool fused = M <= 32 && (M & (M - 1)) == 0;
+    const int slots = fused ? std::max(gemm_reduce_slots(B, D), gemm_reduce_slots(last, D)) : 0;
     auto up4 = [](size_t v) { return (v + 3) / 4 * 4; };   // every sub-buffer 16-byte aligned
     const size_t nBD = up4(static_cast<size_t>(B) * D), nBH = up4(static_cast<size_t>(B) * H),
                  nML = up4(static_cast<size_t>(B) * 2 * L);
+    const size_t nP = up4(static_cast<size_t>(B) * slots * M), nQ = up4(static_cast<size_t>(B) * slots);
+    const size_t nOut = fused ? nP + nQ : nBD;
     const size_t nMap = up4(static_cast<size_t>(B));   // the chunk's window -> stream map (ints)
-    const size_t need = 2 * nBD + 4 * nBH + nML + nMap + static_cast<size_t>(wsg) + 16;
+    const size_t need = nBD + nOut + 4 * nBH + nML + nMap + static_cast<size_t>(wsg) + 16;
     enova_status st = ensure(&det->ext_ws, &det->ext_ws_cap, need);
     if (st != ENOVA_OK)
         return st;
-    float *V = det->ext_ws, *out = V + nBD, *a1 = out + nBD, *h = a1 + nBH, *a2 = h + nBH, *hd = a2 + nBH,
+    float *V = det->ext_ws, *out = V + nBD, *a1 = out + nOut, *h = a1 + nBH, *a2 = h + nBH, *hd = a2 + nBH,
           *ml = hd + nBH, *mapf = ml + nML, *gw = mapf + nMap;
     int *wmap = reinterpret_cast<int *>(mapf);
     if (det->timing)
@@ -822,6 +828,14 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
     GemmEpilogue dec = enc;
     dec.bias = det->bd1;
     dec.out2 = hd;
+    GemmEpilogue red;   // fused reductions of d = v - (product + bd2)
+    red.kind = kEpiRowReduce;
+    red.bias = det->d_bd2;
+    red.pre = V;
+    red.ldv = D;
+    red.groups = M;
+    red.out2 = out;
+    red.sq = out + nP;
     for (int64_t w0 = 0; w0 < n_windows; w0 += B) {
         const int rows = static_cast<int>(std::min<int64_t>(B, n_windows - w0));
         e = launch_ext_stage(x, g.dtype, soff, woff, n, w0, rows, M, g.W, g.S, norm, ref_mean, ref_std, wmap, V,
@@ -834,12 +848,20 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
             e = launch_ext_latent(ml, det->d_bml, rows, L, out_scores ? out_scores + w0 : nullptr, stream);
         if (e == hipSuccess)   // a2 = mu Wd1^T + bd1, hd = act(a2)
             e = launch_gemm(dec, ml, 2 * L, 1, det->d_wd1, 1, L, a2, H, rows, H, L, nullptr, gw, wsg, stream);
-        if (e == hipSuccess)   // decoder output without bd2
-            e = launch_gemm(plain, hd, H, 1, det->d_wd2, 1, H, out, D, rows, D, H, nullptr, gw, wsg, stream);
-        if (e == hipSuccess)
-            e = launch_ext_reduce(V, out, det->d_bd2, rows, M, g.W, out_md ? out_md + w0 : nullptr,
-                                  out_md_metric ? out_md_metric + w0 * M : nullptr,
-                                  out_recon ? out_recon + w0 : nullptr, stream);
+        float *o_md = out_md ? out_md + w0 : nullptr, *o_mdm = out_md_metric ? out_md_metric + w0 * M : nullptr,
+              *o_rec = out_recon ? out_recon + w0 : nullptr;
+        if (fused) {
+            if (e == hipSuccess)   // decoder output, reduced against V in the epilogue
+                e = launch_gemm(red, hd, H, 1, det->d_wd2, 1, H, out, D, rows, D, H, nullptr, gw, wsg, stream);
+            if (e == hipSuccess)
+                e = launch_ext_finish(out, out + nP, rows, gemm_reduce_slots(rows, D), M, g.W, o_md, o_mdm, o_rec,
+                                      stream);
+        } else {
+            if (e == hipSuccess)   // decoder output without bd2
+                e = launch_gemm(plain, hd, H, 1, det->d_wd2, 1, H, out, D, rows, D, H, nullptr, gw, wsg, stream);
+            if (e == hipSuccess)
+                e = launch_ext_reduce(V, out, det->d_bd2, rows, M, g.W, o_md, o_mdm, o_rec, stream);
+        }
         if (e != hipSuccess)
             return hip_fail(e, "output-variant kernels");
     }

@@ -136,10 +136,18 @@ struct Stage {
 //   kEpiBiasAct:   C = v + bias[j] (the pre-activation, kept for the backward pass), out2 = act(C)
 //   kEpiDact:      C = v * act'(pre[i][j]) (pre has C's layout)
 struct EpiParams {
-    const float *bias;   // kEpiBiasAct
-    float *out2;         // kEpiBiasAct: act(C), C's layout
-    const float *pre;    // kEpiDact
+    const float *bias;   // kEpiBiasAct, kEpiRowReduce
+    float *out2;         // kEpiBiasAct: act(C), C's layout; kEpiRowReduce: group sums
+    const float *pre;    // kEpiDact; kEpiRowReduce: the minuend, leading dimension ldv
+    float *sq;           // kEpiRowReduce: sums of squares
+    int ldv, groups;     // kEpiRowReduce
 };
+
+// Waves of a TM x TN block tile along its columns.
+constexpr int gemm_waves_n(int tm, int tn)
+{
+    return 4 / (tn == kGemmTile ? (tm == kGemmTile ? 2 : 1) : 4);
+}
 
 template <int ACT>
 __device__ __forceinline__ float dact_of(float a)
@@ -163,7 +171,7 @@ __device__ __forceinline__ void epi_store(float *__restrict__ C, int64_t ldc, in
         ep.out2[e] = act_fn<ACT>(a);
     } else if constexpr (EPI == kEpiDact) {
         C[e] = v * dact_of<ACT>(ep.pre[e]);
-    } else {
+    } else if constexpr (EPI == kEpiStore) {
         C[e] = v;
     }
 }
@@ -191,7 +199,7 @@ __device__ __forceinline__ void epi_tile(float *__restrict__ C, int64_t ldc, int
 #pragma unroll
         for (int r = 0; r < 16; ++r)
             C[static_cast<int64_t>(si + crow(r, half)) * ldc + gj] = v[r] * dact_of<ACT>(pre[r]);
-    } else {
+    } else if constexpr (EPI == kEpiStore) {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
             C[static_cast<int64_t>(si + crow(r, half)) * ldc + gj] = v[r];
@@ -215,8 +223,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
                                                  EpiParams ep, int m, int n, int kk, int kc)
 {
     // waves along the rows (WM) and columns (WN) of the tile; each covers RW x CW as MA x MB ops
-    constexpr int WM = TN == kGemmTile ? (TM == kGemmTile ? 2 : 1) : 4;
-    constexpr int WN = 4 / WM;
+    constexpr int WN = gemm_waves_n(TM, TN);
+    constexpr int WM = 4 / WN;
     constexpr int RW = TM / WM, CW = TN / WN;
     constexpr int MA = RW / 32, MB = CW / 32;
     static_assert(MA >= 1 && MB >= 1 && WM * WN == 4, "tile shape");
@@ -360,6 +368,68 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
             if (half == 0 && gi < m)
                 rowsum[static_cast<int64_t>(blockIdx.z) * m + gi] = rs[a] + other;
         }
+    }
+    if constexpr (EPI == kEpiRowReduce) {
+        // d = pre - (C + bias) summed per row: over the wave's MB sub-tiles in registers, then
+        // across lanes of the same column group (xor of the lane bits at and above `groups`),
+        // then the rest of the lanes for the squares. One slot per wave column group.
+        const int slot = blockIdx.x * WN + wx;
+        if (j0 + wx * CW >= n)
+            return;
+        const int slots = (n + CW - 1) / CW;
+#pragma unroll
+        for (int a = 0; a < MA; ++a) {
+            if (!live_a[a])
+                continue;
+            const int si = i0 + wy * RW + a * 32;
+            // the 16 rows of a lane in two halves of 8 (fewer registers next to the accumulators)
+#pragma unroll
+            for (int rh = 0; rh < 16; rh += 8) {
+                float sd[8], sq[8];
+#pragma unroll
+                for (int r = 0; r < 8; ++r)
+                    sd[r] = sq[r] = 0.0f;
+#pragma unroll
+                for (int b = 0; b < MB; ++b) {
+                    const int gj = j0 + wx * CW + b * 32 + l32;
+                    const bool col = gj < n;
+                    const float bj = col ? ep.bias[gj] : 0.0f;
+                    float v[8];
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) {
+                        const int gi = si + crow(rh + r, half);
+                        v[r] = col && gi < m ? ep.pre[static_cast<int64_t>(gi) * ep.ldv + gj] : 0.0f;
+                    }
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) {
+                        const int gi = si + crow(rh + r, half);
+                        const float d = col && gi < m ? v[r] - (acc[a][b][rh + r] + bj) : 0.0f;
+                        sd[r] += d;
+                        sq[r] = fmaf(d, d, sq[r]);
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    for (int off = 16; off >= ep.groups; off >>= 1)
+                        sd[r] += __shfl_xor(sd[r], off);
+#pragma unroll
+                    for (int off = 16; off >= 1; off >>= 1)
+                        sq[r] += __shfl_xor(sq[r], off);
+                }
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const int gi = si + crow(rh + r, half);
+                    if (gi < m) {
+                        const int64_t row = static_cast<int64_t>(gi) * slots + slot;
+                        if (l32 < ep.groups)
+                            ep.out2[row * ep.groups + l32] = sd[r];
+                        if (l32 == 0)
+                            ep.sq[row] = sq[r];
+                    }
+                }
+            }
+        }
+        return;
     }
 #pragma unroll
     for (int a = 0; a < MA; ++a)
@@ -643,6 +713,14 @@ static int gemm_splits(int m, int n, int k)
     return std::max(1, std::min({by_k, by_grid, kGemmMaxSplits}));
 }
 
+int gemm_reduce_slots(int m, int n)
+{
+    int tm, tn;
+    gemm_tile(m, n, tm, tn);
+    const int cw = tn / gemm_waves_n(tm, tn);
+    return (n + cw - 1) / cw;
+}
+
 int64_t gemm_workspace_floats(int m, int n, int k)
 {
     const int s = gemm_splits(m, n, k);
@@ -705,6 +783,8 @@ void with_epilogue(int kind, int act, Args &&...args)
             F<kEpiDact, ENOVA_TANH>::run(args...);
         else
             F<kEpiDact, ENOVA_RELU>::run(args...);
+    } else if (kind == kEpiRowReduce) {
+        F<kEpiRowReduce, ENOVA_RELU>::run(args...);
     } else {
         F<kEpiStore, ENOVA_RELU>::run(args...);
     }
@@ -743,8 +823,11 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
     const int64_t lda = a_k ? ai : ak, ldb = b_k ? bj : bk;
     const bool va = lda % 4 == 0 && lda <= kGemmMaxLd32 && reinterpret_cast<uintptr_t>(A) % 16 == 0;
     const bool vb = ldb % 4 == 0 && ldb <= kGemmMaxLd32 && reinterpret_cast<uintptr_t>(B) % 16 == 0;
-    // never more slices than the caller's workspace holds
-    int splits = work ? gemm_splits(m, n, k) : 1;
+    if (epi.kind == kEpiRowReduce &&
+        (epi.groups < 1 || epi.groups > 32 || (epi.groups & (epi.groups - 1)) != 0 || !epi.sq || !epi.out2))
+        return hipErrorInvalidValue;
+    // never more slices than the caller's workspace holds (a row reduction is never split)
+    int splits = work && epi.kind != kEpiRowReduce ? gemm_splits(m, n, k) : 1;
     const int64_t per_slice = static_cast<int64_t>(m) * n + m;
     while (splits > 1 && static_cast<int64_t>(splits) * per_slice > work_floats)
         --splits;
@@ -754,7 +837,7 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
     gemm_tile(m, n, tm, tn);
     const dim3 grid(static_cast<unsigned>((n + tn - 1) / tn), static_cast<unsigned>((m + tm - 1) / tm),
                     static_cast<unsigned>(used));
-    const EpiParams ep{epi.bias, epi.out2, epi.pre};
+    const EpiParams ep{epi.bias, epi.out2, epi.pre, epi.sq, epi.ldv, epi.groups};
     hipError_t e = hipSuccess;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess)
         return e;

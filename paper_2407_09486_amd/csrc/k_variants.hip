@@ -210,7 +210,58 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_reduce(const float *__restr
     }
 }
 
+// The reductions of k_ext_reduce from the partial sums of the decoder-output product's fused
+// epilogue: P [rows][slots][M] (sums of d per metric and column slot), Q [rows][slots] (sums of
+// d^2). M lanes per window (M a power of two <= 32): lane m adds its metric's slots in order, the
+// window's total is a butterfly over the M lanes, and lane 0 adds the squares.
+__global__ __launch_bounds__(kExtThreads) void k_ext_finish(const float *__restrict__ P, const float *__restrict__ Q,
+                                                            int rows, int slots, int M, int W,
+                                                            float *__restrict__ md, float *__restrict__ md_metric,
+                                                            float *__restrict__ recon)
+{
+    const int per = kExtThreads / M;
+    const int i = blockIdx.x * per + static_cast<int>(threadIdx.x) / M;
+    const int m = threadIdx.x % M;
+    const bool on = i < rows;
+    float s = 0.0f;
+    if (on) {
+        const float *p = P + static_cast<int64_t>(i) * slots * M + m;
+        for (int k = 0; k < slots; ++k)
+            s += p[static_cast<int64_t>(k) * M];
+        if (md_metric)
+            md_metric[static_cast<int64_t>(i) * M + m] = s / W;
+    }
+    float t = s;
+    for (int off = 1; off < M; off <<= 1)
+        t += __shfl_xor(t, off);
+    if (on && m == 0) {
+        const float D = static_cast<float>(W) * static_cast<float>(M);
+        if (md)
+            md[i] = t / D;
+        if (recon) {
+            float q = 0.0f;
+            const float *qq = Q + static_cast<int64_t>(i) * slots;
+            for (int k = 0; k < slots; ++k)
+                q += qq[k];
+            recon[i] = q / D;
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_ext_finish(const float *P, const float *Q, int rows, int slots, int M, int W, float *md,
+                             float *md_metric, float *recon, hipStream_t st)
+{
+    if (rows <= 0)
+        return hipSuccess;
+    if (M < 1 || M > 32 || (M & (M - 1)) != 0)
+        return hipErrorInvalidValue;
+    const int per = kExtThreads / M;
+    hipLaunchKernelGGL(k_ext_finish, dim3(static_cast<unsigned>((rows + per - 1) / per)), dim3(kExtThreads), 0, st, P,
+                       Q, rows, slots, M, W, md, md_metric, recon);
+    return hipGetLastError();
+}
 
 hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const int64_t *woff, int n, int64_t w0,
                             int rows, int M, int W, int S, int norm, const float *mean, const float *std, int *map,

@@ -19,15 +19,26 @@ struct TrainHyper {
 // rowsum (or NULL) receives sum_k A(i, k) for every i < m. The epilogue fuses the element-wise
 // step that follows a product: store; C = product + bias[j] with out2 = act(C); or
 // C = product * act'(pre) (pre in C's layout).
-enum { kEpiStore = 0, kEpiBiasAct = 1, kEpiDact = 2 };
+// kEpiRowReduce writes no C: with d(i, j) = pre[i*ldv + j] - (product + bias[j]) and column j
+// belonging to group j mod groups (groups a power of two <= 32), it writes for every row i and
+// column slot s (gemm_reduce_slots(m, n) slots of consecutive columns)
+//   out2[(i*slots + s)*groups + c] = sum of d over the slot's columns of group c,
+//   sq[i*slots + s]                = sum of d^2 over the slot's columns;
+// such a product is never split.
+enum { kEpiStore = 0, kEpiBiasAct = 1, kEpiDact = 2, kEpiRowReduce = 3 };
 struct GemmEpilogue {
     int kind = kEpiStore;
     int act = ENOVA_RELU;
     const float *bias = nullptr;
     float *out2 = nullptr;
     const float *pre = nullptr;
+    float *sq = nullptr;    // kEpiRowReduce
+    int ldv = 0;            // kEpiRowReduce: leading dimension of pre
+    int groups = 0;         // kEpiRowReduce
 };
 int64_t gemm_workspace_floats(int m, int n, int k);
+// Column slots of an m x n kEpiRowReduce product (at most (n + 31) / 32).
+int gemm_reduce_slots(int m, int n);
 // ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
 // `work` holds work_floats floats; a product splits only as far as they allow (none when work is
 // NULL).

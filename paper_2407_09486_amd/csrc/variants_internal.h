@@ -18,6 +18,10 @@ hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const
 hipError_t launch_ext_latent(float *ml, const float *bml, int rows, int L, float *score, hipStream_t st);
 // Per row: md = mean(v - m'), md_metric [rows][M] = mean over the steps per metric, recon =
 // mean((v - m')^2), with m' = out + bd2 (any output may be NULL).
+// The same outputs from the partial sums of a kEpiRowReduce decoder-output product with M
+// column groups (M a power of two <= 32): P [rows][slots][M], Q [rows][slots].
+hipError_t launch_ext_finish(const float *P, const float *Q, int rows, int slots, int M, int W, float *md,
+                             float *md_metric, float *recon, hipStream_t st);
 hipError_t launch_ext_reduce(const float *V, const float *out, const float *bd2, int rows, int M, int W, float *md,
                              float *md_metric, float *recon, hipStream_t st);
 

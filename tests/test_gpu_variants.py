@@ -49,9 +49,15 @@ def _check(g, ref, dtype, what, idx=None):
 
 @pytest.mark.parametrize("norm", ["reference", "window"])
 @pytest.mark.parametrize("shape", [dict(metrics=8, window=32, stride=1, hidden=32, latent=16, act="relu"),
-                                   dict(metrics=5, window=7, stride=3, hidden=40, latent=3, act="tanh")])
+                                   dict(metrics=5, window=7, stride=3, hidden=40, latent=3, act="tanh"),
+                                   # power-of-two M: the decoder-output product reduces in its
+                                   # epilogue; D = 28 (one partial column slot), M = 1, M = 32
+                                   dict(metrics=4, window=7, stride=2, hidden=40, latent=3, act="tanh"),
+                                   dict(metrics=1, window=50, stride=1, hidden=64, latent=8, act="relu",
+                                        kind="ar1_spikes"),
+                                   dict(metrics=32, window=5, stride=1, hidden=48, latent=16, act="relu")])
 def test_variants_match_oracle(norm, shape):
-    cfg = wl.CONFIGS["c1"].replace(n_streams=5, t_len=0, t_min=20, t_max=900, kind="ragged_mix", **shape)
+    cfg = wl.CONFIGS["c1"].replace(n_streams=5, t_len=0, t_min=20, t_max=900, **{"kind": "ragged_mix", **shape})
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg, lengths=[900, 5, 40, 333, 700])
     log(f"variants {norm} {shape}")
