@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdint>
+#include <type_traits>
 
 #include "mfma_common.h"
 #include "variants_internal.h"
@@ -125,6 +127,104 @@ __global__ __launch_bounds__(kExtThreads) void k_ext_stage(const void *__restric
         const int t = j / M, m = j - t * M;
         const float v = (load_value<DT>(x, (row0 + t) * M + m) - s_mean[m]) * s_rinv[m];
         out[j] = DT == ENOVA_BF16 ? round_bf16(v) : v;
+    }
+}
+
+// The same rows as k_ext_stage, one wave per window (four per block, no LDS, no barriers), when
+// M is a power of two in [4, 256] and D = 256 Q: lane l holds the 4 Q values
+// j = 256 q + 4 l + u (metric (4 l + u) mod M) in registers. The lanes that hold a metric are
+// those with equal l mod (M / 4), so a butterfly over the other lane bits completes each metric's
+// fp64 sum (then its centred sum of squares) in every lane that needs it.
+template <int DT, int Q>
+__global__ __launch_bounds__(kExtThreads) void k_ext_stage_wave(const void *__restrict__ x,
+                                                                const int64_t *__restrict__ soff,
+                                                                const int64_t *__restrict__ woff,
+                                                                const int *__restrict__ map, int64_t w0, int rows,
+                                                                int M, int W, int S, int norm,
+                                                                const float *__restrict__ mean,
+                                                                const float *__restrict__ std, float *__restrict__ V)
+{
+    const int lane = threadIdx.x & 63;
+    const int i = blockIdx.x * (kExtThreads / 64) + static_cast<int>(threadIdx.x >> 6);
+    if (i >= rows)
+        return;
+    const int s = map[i];
+    const int64_t row0 = soff[s] + (w0 + i - woff[s]) * S;
+    const int64_t base = row0 * M + 4 * lane;
+    float v[Q][4];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        if constexpr (DT == ENOVA_BF16) {
+            const uint2 p = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(x) + base + 256 * q);
+            v[q][0] = __uint_as_float(p.x << 16);
+            v[q][1] = __uint_as_float(p.x & 0xffff0000u);
+            v[q][2] = __uint_as_float(p.y << 16);
+            v[q][3] = __uint_as_float(p.y & 0xffff0000u);
+        } else {
+            const float4 p = *reinterpret_cast<const float4 *>(static_cast<const float *>(x) + base + 256 * q);
+            v[q][0] = p.x;
+            v[q][1] = p.y;
+            v[q][2] = p.z;
+            v[q][3] = p.w;
+        }
+    }
+    float mu[4], ri[4];
+    if (norm == ENOVA_NORM_WINDOW) {
+        const int g = M / 4;   // lanes l and l ^ (k g) hold the same metrics
+        double a[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            a[u] = 0.0;
+#pragma unroll
+            for (int q = 0; q < Q; ++q)
+                a[u] += v[q][u];
+        }
+        for (int off = g; off < 64; off <<= 1)
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                a[u] += __shfl_xor(a[u], off);
+        double c[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            a[u] /= W;
+            c[u] = 0.0;
+#pragma unroll
+            for (int q = 0; q < Q; ++q) {
+                const double d = v[q][u] - a[u];
+                c[u] = fma(d, d, c[u]);
+            }
+        }
+        for (int off = g; off < 64; off <<= 1)
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                c[u] += __shfl_xor(c[u], off);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            double sd = sqrt(c[u] / W);
+            if (sd <= 1e-6 * fmax(1.0, fabs(a[u])))
+                sd = 1.0;
+            mu[u] = static_cast<float>(a[u]);
+            ri[u] = 1.0f / static_cast<float>(sd);
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t e = static_cast<int64_t>(s) * M + ((4 * lane + u) & (M - 1));
+            mu[u] = mean[e];
+            ri[u] = 1.0f / std[e];
+        }
+    }
+    float *out = V + static_cast<int64_t>(i) * (256 * Q) + 4 * lane;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        float o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            o[u] = (v[q][u] - mu[u]) * ri[u];
+            if constexpr (DT == ENOVA_BF16)
+                o[u] = round_bf16(o[u]);
+        }
+        *reinterpret_cast<float4 *>(out + 256 * q) = make_float4(o[0], o[1], o[2], o[3]);
     }
 }
 
@@ -273,6 +373,35 @@ hipError_t launch_ext_stage(const void *x, int dtype, const int64_t *soff, const
         return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_ext_map, dim3(static_cast<unsigned>((rows + kExtThreads - 1) / kExtThreads)),
                        dim3(kExtThreads), 0, st, woff, n, w0, rows, map);
+    const int D = W * M;
+    const int q = D / 256;
+    const bool aligned = reinterpret_cast<uintptr_t>(x) % (dtype == ENOVA_BF16 ? 8 : 16) == 0 &&
+                         reinterpret_cast<uintptr_t>(V) % 16 == 0;
+    if (aligned && M >= 4 && M <= 256 && (M & (M - 1)) == 0 && D % 256 == 0 && q >= 1 && q <= 8) {
+        const dim3 grid(static_cast<unsigned>((rows + kExtThreads / 64 - 1) / (kExtThreads / 64)));
+        auto go = [&](auto dt_tag, auto q_tag) {
+            constexpr int DT = decltype(dt_tag)::value, QQ = decltype(q_tag)::value;
+            hipLaunchKernelGGL((k_ext_stage_wave<DT, QQ>), grid, dim3(kExtThreads), 0, st, x, soff, woff, map, w0,
+                               rows, M, W, S, norm, mean, std, V);
+        };
+        auto by_q = [&](auto dt_tag) {
+            switch (q) {
+            case 1: go(dt_tag, std::integral_constant<int, 1>{}); break;
+            case 2: go(dt_tag, std::integral_constant<int, 2>{}); break;
+            case 3: go(dt_tag, std::integral_constant<int, 3>{}); break;
+            case 4: go(dt_tag, std::integral_constant<int, 4>{}); break;
+            case 5: go(dt_tag, std::integral_constant<int, 5>{}); break;
+            case 6: go(dt_tag, std::integral_constant<int, 6>{}); break;
+            case 7: go(dt_tag, std::integral_constant<int, 7>{}); break;
+            default: go(dt_tag, std::integral_constant<int, 8>{}); break;
+            }
+        };
+        if (dtype == ENOVA_BF16)
+            by_q(std::integral_constant<int, ENOVA_BF16>{});
+        else
+            by_q(std::integral_constant<int, ENOVA_F32>{});
+        return hipGetLastError();
+    }
     const size_t lds = 2 * sizeof(float) * static_cast<size_t>(M);
     if (dtype == ENOVA_BF16)
         hipLaunchKernelGGL(k_ext_stage<ENOVA_BF16>, dim3(static_cast<unsigned>(rows)), dim3(kExtThreads), lds, st, x,

@@ -55,7 +55,9 @@ def _check(g, ref, dtype, what, idx=None):
                                    dict(metrics=4, window=7, stride=2, hidden=40, latent=3, act="tanh"),
                                    dict(metrics=1, window=50, stride=1, hidden=64, latent=8, act="relu",
                                         kind="ar1_spikes"),
-                                   dict(metrics=32, window=5, stride=1, hidden=48, latent=16, act="relu")])
+                                   dict(metrics=32, window=5, stride=1, hidden=48, latent=16, act="relu"),
+                                   # the detector's c5 window shape (M = 16, D = 1024)
+                                   dict(metrics=16, window=64, stride=1, hidden=32, latent=16, act="relu")])
 def test_variants_match_oracle(norm, shape):
     cfg = wl.CONFIGS["c1"].replace(n_streams=5, t_len=0, t_min=20, t_max=900, **{"kind": "ragged_mix", **shape})
     w = wl.make_weights(cfg, bias_scale=0.1)
@@ -68,12 +70,13 @@ def test_variants_match_oracle(norm, shape):
     _check(g, ref, "f32", f"{norm} {shape}")
 
 
+@pytest.mark.parametrize("window", [16, 32])
 @pytest.mark.parametrize("norm", ["reference", "window"])
-def test_variants_bf16_detector(norm):
-    cfg = wl.CONFIGS["c4"].replace(n_streams=3, t_len=300, metrics=8, window=16, stride=2, hidden=64)
+def test_variants_bf16_detector(norm, window):
+    cfg = wl.CONFIGS["c4"].replace(n_streams=3, t_len=300, metrics=8, window=window, stride=2, hidden=64)
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg)
-    log(f"variants bf16 {norm}")
+    log(f"variants bf16 {norm} W={window}")
     g, woff = _run(cfg, w, work, norm)
     ref = ov.score_ext(work.values_f64(), work.stream_offsets, window=cfg.window, stride=cfg.stride,
                        weights=_weights_f64(w), act=cfg.act, norm=norm, ref_frac=cfg.ref_frac, bf16=True)
