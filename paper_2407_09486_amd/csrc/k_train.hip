@@ -510,6 +510,81 @@ __global__ __launch_bounds__(64) void k_latent(float *__restrict__ ml, const flo
     kl[i] = 0.5f * k;
 }
 
+// The same with one thread per (window, latent index) when L is a power of two <= 64: coalesced
+// accesses, and the window's KL summed over its L lanes by a butterfly.
+__global__ __launch_bounds__(256) void k_latent_lanes(float *__restrict__ ml, const float *__restrict__ bml,
+                                                      const float *__restrict__ eps, float *__restrict__ sd,
+                                                      float *__restrict__ z, float *__restrict__ kl, int rows, int L)
+{
+    const int64_t t = blockIdx.x * 256LL + threadIdx.x;
+    const int64_t i = t / L;
+    const int l = static_cast<int>(t - i * L);
+    const bool on = i < rows;
+    float k = 0.0f;
+    if (on) {
+        float *mu = ml + i * 2 * L;
+        const float m = mu[l] + bml[l];
+        const float v = mu[L + l] + bml[L + l];
+        const float s = expf(0.5f * v);
+        mu[l] = m;
+        mu[L + l] = v;
+        sd[t] = s;
+        z[t] = m + s * eps[t];
+        k = m * m + kl_g(v);
+    }
+    for (int off = 1; off < L; off <<= 1)
+        k += __shfl_xor(k, off);
+    if (on && l == 0)
+        kl[i] = 0.5f * k;
+}
+
+// One wave per window (four per block) when D is a multiple of 4 and at most 2048: lane l holds
+// the differences j = 256 q + 4 l + u in registers, the window's error is a butterfly over the
+// wave, and no LDS or barrier is involved. Same outputs as k_recon.
+template <int Q>
+__global__ __launch_bounds__(256) void k_recon_wave(float *__restrict__ out, const float *__restrict__ bd2,
+                                                    const float *__restrict__ V, const float *__restrict__ labels,
+                                                    float *__restrict__ logp, int rows, int D, float inv_b,
+                                                    float margin)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t row = blockIdx.x * 4LL + (threadIdx.x >> 6);
+    if (row >= rows)
+        return;
+    float *o = out + row * D;
+    const float *v = V + row * D;
+    float4 d[Q];
+    float sq = 0.0f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int j = 256 * q + 4 * lane;
+        if (j < D) {
+            const float4 a = *reinterpret_cast<const float4 *>(o + j);
+            const float4 b = *reinterpret_cast<const float4 *>(bd2 + j);
+            const float4 c = *reinterpret_cast<const float4 *>(v + j);
+            d[q] = make_float4(a.x + b.x - c.x, a.y + b.y - c.y, a.z + b.z - c.z, a.w + b.w - c.w);
+        } else {
+            d[q] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        }
+        sq += (d[q].x * d[q].x + d[q].y * d[q].y) + (d[q].z * d[q].z + d[q].w * d[q].w);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        sq += __shfl_xor(sq, off);
+    const float l = labels[row];
+    const float err = 0.5f * sq;
+    const float scale = (l > 0.0f || err < margin) ? l * inv_b : 0.0f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int j = 256 * q + 4 * lane;
+        if (j < D)
+            *reinterpret_cast<float4 *>(o + j) =
+                make_float4(scale * d[q].x, scale * d[q].y, scale * d[q].z, scale * d[q].w);
+    }
+    if (lane == 0)
+        logp[row] = -err - 0.5f * static_cast<float>(D) * kLog2Pi;
+}
+
 // One block per window: m' = out + bd2, e = |v - m'|^2 / 2, log p = -e - D/2 log 2 pi, and in place
 // of out the gradient of J, (l/B)(m' - v); an anomalous window (l < 0) whose e has reached the
 // margin contributes a constant and gets a zero gradient. PER > 0: the window's D <= 256 PER
@@ -576,44 +651,47 @@ __global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, con
                                               float *__restrict__ info, float b1, float b2,
                                               long long *__restrict__ step, float *__restrict__ corr)
 {
-    __shared__ double r_kl[1024], r_n[1024], r_lp[1024], r_la[1024], r_kn[1024];
-    double skl = 0.0, sn = 0.0, slp = 0.0, sla = 0.0, skn = 0.0;
+    // per thread (fixed stride), per wave (butterfly), then the 16 wave sums in wave order
+    __shared__ double r[5][16];
+    double a[5] = {0.0, 0.0, 0.0, 0.0, 0.0};   // KL of normal windows, their count, log p, J terms, KL terms
     for (int i = threadIdx.x; i < rows; i += 1024) {
         const double l = labels[i];
         const double k = kl[i];
         const double lp = logp[i];
         if (l > 0.0) {
-            skl += k;
-            sn += 1.0;
+            a[0] += k;
+            a[1] += 1.0;
         }
-        slp += lp;
+        a[2] += lp;
         if (l < 0.0) {
             // anomalous: -log p capped at margin + D/2 log 2 pi
             const double err = -lp - static_cast<double>(half_d_log2pi);
-            sla += (err < margin ? err : static_cast<double>(margin)) + static_cast<double>(half_d_log2pi);
+            a[3] += (err < margin ? err : static_cast<double>(margin)) + static_cast<double>(half_d_log2pi);
         } else {
-            sla += l * lp;
+            a[3] += l * lp;
         }
-        skn += 0.5 * (1.0 + l) * k;
+        a[4] += 0.5 * (1.0 + l) * k;
     }
-    r_kl[threadIdx.x] = skl;
-    r_n[threadIdx.x] = sn;
-    r_lp[threadIdx.x] = slp;
-    r_la[threadIdx.x] = sla;
-    r_kn[threadIdx.x] = skn;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+            a[q] += __shfl_xor(a[q], off);
+    if ((threadIdx.x & 63) == 0)
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+            r[q][threadIdx.x >> 6] = a[q];
     __syncthreads();
-    for (int w = 512; w >= 1; w >>= 1) {
-        if (threadIdx.x < w) {
-            r_kl[threadIdx.x] += r_kl[threadIdx.x + w];
-            r_n[threadIdx.x] += r_n[threadIdx.x + w];
-            r_lp[threadIdx.x] += r_lp[threadIdx.x + w];
-            r_la[threadIdx.x] += r_la[threadIdx.x + w];
-            r_kn[threadIdx.x] += r_kn[threadIdx.x + w];
-        }
-        __syncthreads();
-    }
     if (threadIdx.x == 0) {
-        const double mkl = r_n[0] > 0.0 ? r_kl[0] / r_n[0] : 0.0;
+        double s_kl = 0.0, s_n = 0.0, s_lp = 0.0, s_la = 0.0, s_kn = 0.0;
+        for (int w = 0; w < 16; ++w) {
+            s_kl += r[0][w];
+            s_n += r[1][w];
+            s_lp += r[2][w];
+            s_la += r[3][w];
+            s_kn += r[4][w];
+        }
+        const double mkl = s_n > 0.0 ? s_kl / s_n : 0.0;
         const double e = static_cast<double>(kl_set) - mkl;
         const double integ = static_cast<double>(st[0]) - static_cast<double>(ki) * e;
         const double p = e < 700.0 ? static_cast<double>(kp) / (1.0 + exp(e)) : 0.0;
@@ -626,8 +704,8 @@ __global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, con
         corr[0] = static_cast<float>(1.0 / (1.0 - pow(static_cast<double>(b1), static_cast<double>(k_adam))));
         corr[1] = static_cast<float>(1.0 / (1.0 - pow(static_cast<double>(b2), static_cast<double>(k_adam))));
         if (info) {
-            info[0] = static_cast<float>(-(r_la[0] - b * r_kn[0]) / rows);
-            info[1] = static_cast<float>(r_lp[0] / rows);
+            info[0] = static_cast<float>(-(s_la - b * s_kn) / rows);
+            info[1] = static_cast<float>(s_lp / rows);
             info[2] = static_cast<float>(mkl);
             info[3] = static_cast<float>(b);
         }
@@ -865,6 +943,12 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
 hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
                          int L, hipStream_t st)
 {
+    if (L <= 64 && (L & (L - 1)) == 0) {
+        const int64_t threads = static_cast<int64_t>(rows) * L;
+        hipLaunchKernelGGL(k_latent_lanes, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st, ml, bml,
+                           eps, sd, z, kl, rows, L);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(k_latent, dim3(static_cast<unsigned>((rows + 63) / 64)), dim3(64), 0, st, ml, bml, eps, sd, z,
                        kl, rows, L);
     return hipGetLastError();
@@ -873,8 +957,25 @@ hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *s
 hipError_t launch_recon(float *out, const float *bd2, const float *V, const float *labels, float *logp,
                         int rows, int D, float margin, hipStream_t st)
 {
-    const dim3 grid(static_cast<unsigned>(rows));
     const float inv_b = 1.0f / static_cast<float>(rows);
+    const bool vec = D % 4 == 0 && D <= 2048 && reinterpret_cast<uintptr_t>(out) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(V) % 16 == 0 && reinterpret_cast<uintptr_t>(bd2) % 16 == 0;
+    if (vec) {
+        const dim3 wgrid(static_cast<unsigned>((rows + 3) / 4));
+        const int q = (D + 255) / 256;
+        switch (q) {
+        case 1: hipLaunchKernelGGL(k_recon_wave<1>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        case 2: hipLaunchKernelGGL(k_recon_wave<2>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        case 3: hipLaunchKernelGGL(k_recon_wave<3>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        case 4: hipLaunchKernelGGL(k_recon_wave<4>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        case 5: hipLaunchKernelGGL(k_recon_wave<5>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        case 6: hipLaunchKernelGGL(k_recon_wave<6>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        case 7: hipLaunchKernelGGL(k_recon_wave<7>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        default: hipLaunchKernelGGL(k_recon_wave<8>, wgrid, dim3(256), 0, st, out, bd2, V, labels, logp, rows, D, inv_b, margin); break;
+        }
+        return hipGetLastError();
+    }
+    const dim3 grid(static_cast<unsigned>(rows));
     if (D <= 256)
         hipLaunchKernelGGL(k_recon<1>, grid, dim3(256), 0, st, out, bd2, V, labels, logp, D, inv_b, margin);
     else if (D <= 512)
