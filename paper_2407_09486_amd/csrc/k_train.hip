@@ -654,23 +654,34 @@ __global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, con
     // per thread (fixed stride), per wave (butterfly), then the 16 wave sums in wave order
     __shared__ double r[5][16];
     double a[5] = {0.0, 0.0, 0.0, 0.0, 0.0};   // KL of normal windows, their count, log p, J terms, KL terms
-    for (int i = threadIdx.x; i < rows; i += 1024) {
-        const double l = labels[i];
-        const double k = kl[i];
-        const double lp = logp[i];
-        if (l > 0.0) {
-            a[0] += k;
-            a[1] += 1.0;
+    // 8 elements per thread per round, all loaded before any is added
+    for (int i0 = 0; i0 < rows; i0 += 8 * 1024) {
+        float fl[8], fk[8], fp[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * 1024 + static_cast<int>(threadIdx.x);
+            const bool in = i < rows;
+            fl[u] = in ? labels[i] : 0.0f;   // a zero label adds nothing below
+            fk[u] = in ? kl[i] : 0.0f;
+            fp[u] = in ? logp[i] : 0.0f;
         }
-        a[2] += lp;
-        if (l < 0.0) {
-            // anomalous: -log p capped at margin + D/2 log 2 pi
-            const double err = -lp - static_cast<double>(half_d_log2pi);
-            a[3] += (err < margin ? err : static_cast<double>(margin)) + static_cast<double>(half_d_log2pi);
-        } else {
-            a[3] += l * lp;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const double l = fl[u], k = fk[u], lp = fp[u];
+            if (l > 0.0) {
+                a[0] += k;
+                a[1] += 1.0;
+            }
+            a[2] += lp;
+            if (l < 0.0) {
+                // anomalous: -log p capped at margin + D/2 log 2 pi
+                const double err = -lp - static_cast<double>(half_d_log2pi);
+                a[3] += (err < margin ? err : static_cast<double>(margin)) + static_cast<double>(half_d_log2pi);
+            } else {
+                a[3] += l * lp;
+            }
+            a[4] += 0.5 * (1.0 + l) * k;
         }
-        a[4] += 0.5 * (1.0 + l) * k;
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1)
