@@ -314,7 +314,8 @@ enova_status enova_train_destroy(enova_trainer t);
  * per-window normalisation); then the encoder, the KL score, and the decoder's full output
  * m' = Wd2 act(Wd1 mu + bd1) + bd2 at z = mu. Per window: out_scores (the KL score),
  * out_md = mean_j (v_j - m'_j), out_md_metric [N][M] = mean over the W steps of (v - m') per
- * metric, out_recon_err = mean_j (v_j - m'_j)^2 (device outputs; any may be NULL). ref_mean /
+ * metric, out_recon_err = mean_j (v_j - m'_j)^2 (device outputs; any may be NULL; with the last
+ * three NULL the decoder is not evaluated). ref_mean /
  * ref_std as in enova_detect_score (NULL: computed; ignored for ENOVA_NORM_WINDOW). M <= 4096.
  * The products run in fp32 on the matrix cores (x and W1 of a bf16 detector are bf16 values;
  * v is rounded to bf16 as in enova_detect_score). Asynchronous. Errors: EINVAL, EUNSUPPORTED,

@@ -477,14 +477,17 @@ class Detector:
         return scores, mdv, fl
 
     def score_ext(self, x, stream_offsets, window_offsets, n_windows, norm="reference", ref_mean=None,
-                  ref_std=None, stream=None):
-        """Output variants: returns device tensors (scores, md, md_metric [N, M], recon_err)."""
+                  ref_std=None, stream=None, scores_only=False):
+        """Output variants: returns device tensors (scores, md, md_metric [N, M], recon_err); with
+        scores_only the last three are None (the decoder is then not evaluated)."""
         import torch
         dev = x.device
         n = stream_offsets.numel() - 1
         M = self.cfg.metrics
-        f = [torch.empty(max(n_windows, 1), dtype=torch.float32, device=dev)[:n_windows] for _ in range(3)]
-        mdm = torch.empty((max(n_windows, 1), M), dtype=torch.float32, device=dev)[:n_windows]
+        k = 1 if scores_only else 3
+        f = [torch.empty(max(n_windows, 1), dtype=torch.float32, device=dev)[:n_windows] for _ in range(k)]
+        f += [None] * (3 - k)
+        mdm = None if scores_only else torch.empty((max(n_windows, 1), M), dtype=torch.float32, device=dev)[:n_windows]
         enova_detect_score_ext(self.handle, x, stream_offsets, window_offsets, n, n_windows, ref_mean, ref_std,
                                {"reference": ENOVA_NORM_REFERENCE, "window": ENOVA_NORM_WINDOW}[norm], f[0], f[1],
                                mdm, f[2], stream)

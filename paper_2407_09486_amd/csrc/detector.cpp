@@ -793,6 +793,7 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
     // With M a power of two <= 32 the decoder-output product reduces v - m' in its epilogue
     // (per window, metric and column slot) instead of writing m'; `out` then holds those sums.
     const bool fused = M <= 32 && (M & (M - 1)) == 0;
+    const bool decode = out_md || out_md_metric || out_recon;
     const int slots = fused ? std::max(gemm_reduce_slots(B, D), gemm_reduce_slots(last, D)) : 0;
     auto up4 = [](size_t v) { return (v + 3) / 4 * 4; };   // every sub-buffer 16-byte aligned
     const size_t nBD = up4(static_cast<size_t>(B) * D), nBH = up4(static_cast<size_t>(B) * H),
@@ -846,6 +847,10 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
             e = launch_gemm(plain, h, H, 1, det->d_wml, 1, H, ml, 2 * L, rows, 2 * L, H, nullptr, gw, wsg, stream);
         if (e == hipSuccess)
             e = launch_ext_latent(ml, det->d_bml, rows, L, out_scores ? out_scores + w0 : nullptr, stream);
+        if (e != hipSuccess)
+            return hip_fail(e, "output-variant kernels");
+        if (!decode)   // only scores requested: the decoder is not needed
+            continue;
         if (e == hipSuccess)   // a2 = mu Wd1^T + bd1, hd = act(a2)
             e = launch_gemm(dec, ml, 2 * L, 1, det->d_wd1, 1, L, a2, H, rows, H, L, nullptr, gw, wsg, stream);
         float *o_md = out_md ? out_md + w0 : nullptr, *o_mdm = out_md_metric ? out_md_metric + w0 * M : nullptr,

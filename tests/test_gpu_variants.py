@@ -138,3 +138,26 @@ def test_short_last_chunk_splits_its_products():
                        weights=_weights_f64(w), act=cfg.act, norm="window", ref_frac=cfg.ref_frac,
                        pairs=[(0, k) for k in glob])
     _check(g, ref, "f32", "short last chunk", idx=np.asarray(glob))
+
+
+def test_scores_only_skip_the_decoder():
+    """With md, md_m and the error all NULL the decoder products are skipped; the scores are the
+    same kernels' output, so they match a full call bit for bit. No windows: nothing to do."""
+    import torch
+    cfg = wl.CONFIGS["c2"].replace(n_streams=3, t_len=2000)
+    w = wl.make_weights(cfg, bias_scale=0.1)
+    work = wl.generate(cfg)
+    det = detector(cfg, w, "mfma")
+    x, so = upload(work)
+    woff = det.window_offsets(work.stream_offsets)
+    N = int(woff[-1])
+    wo = torch.from_numpy(woff).cuda()
+    log("variants scores only")
+    full = det.score_ext(x, so, wo, N, norm="window")[0]
+    only, md, mdm, rec = det.score_ext(x, so, wo, N, norm="window", scores_only=True)
+    assert md is None and mdm is None and rec is None
+    empty = det.score_ext(x, so, wo, 0, norm="window")
+    torch.cuda.synchronize()
+    assert np.array_equal(full.cpu().numpy(), only.cpu().numpy())
+    assert all(t.numel() == 0 for t in empty)
+    det.close()
