@@ -742,10 +742,12 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
 
 // Windows per chunk of the output variants: V and the decoder output ([chunk][D] each) within
 // about 512 MiB.
+// Windows per chunk of the variant pass: about 1 GiB of V (every chunk pays each kernel's fixed
+// launch cost once), at most 262144.
 static int ext_chunk(const Geometry &g, int64_t n_windows)
 {
-    int64_t c = (int64_t{1} << 26) / g.D;
-    c = std::max<int64_t>(256, std::min<int64_t>(c, 65536));
+    int64_t c = (int64_t{1} << 28) / g.D;
+    c = std::max<int64_t>(256, std::min<int64_t>(c, 262144));
     return static_cast<int>(std::min<int64_t>(c, std::max<int64_t>(n_windows, 1)));
 }
 

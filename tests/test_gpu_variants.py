@@ -102,13 +102,14 @@ def test_reference_variants_agree_with_the_batch_path():
 
 
 def test_windows_across_chunks_and_constant_metrics():
-    """More windows than one chunk (65536 for D = 256): windows on both sides of every chunk
-    boundary, and a metric that is constant inside some windows (the per-window guard)."""
-    cfg = wl.CONFIGS["c1"].replace(n_streams=3, t_len=30000)
+    """More windows than one chunk (2^28 / D = 65536 windows for D = 512 x 8): windows on both
+    sides of every chunk boundary, and a metric that is constant inside some windows (the
+    per-window guard)."""
+    cfg = wl.CONFIGS["c1"].replace(n_streams=3, t_len=30000, window=512)
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg)
     xv = work.x.copy()
-    xv[1000:1100, 3] = 2.5                           # constant inside windows of stream 0
+    xv[1000:1700, 3] = 2.5                           # constant inside windows 1000..1188 of stream 0
     work = wl.from_arrays(cfg, xv, work.stream_offsets)
     for norm in ("window", "reference"):
         g, woff = _run(cfg, w, work, norm)
@@ -125,9 +126,9 @@ def test_windows_across_chunks_and_constant_metrics():
 
 
 def test_short_last_chunk_splits_its_products():
-    """65536 + 300 windows of D = 256: the last chunk's encoder product has few output tiles and
-    splits its reduction; its windows must match the oracle like the others."""
-    cfg = wl.CONFIGS["c1"].replace(n_streams=1, t_len=65867)
+    """65536 + 300 windows of D = 512 x 8 (chunks of 65536): the last chunk's encoder product has
+    few output tiles and splits its reduction; its windows must match the oracle like the others."""
+    cfg = wl.CONFIGS["c1"].replace(n_streams=1, t_len=65536 + 300 + 511, window=512)
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg)
     g, woff = _run(cfg, w, work, "window")
