@@ -162,3 +162,35 @@ def test_scores_only_skip_the_decoder():
     assert np.array_equal(full.cpu().numpy(), only.cpu().numpy())
     assert all(t.numel() == 0 for t in empty)
     det.close()
+
+
+def test_variants_full_size_sampled():
+    """The benchmarked workload (c5, per-window normalisation, every output) at its real size,
+    launched as bench.py launches it; sampled windows (random ones, stream edges and both sides
+    of every chunk boundary) against the oracle."""
+    import torch
+    from test_gpu_fullsize import _sample, _sub_workload
+    cfg = wl.CONFIGS["c5"]
+    w = wl.make_weights(cfg)
+    work = wl.generate(cfg)
+    det = detector(cfg, w, "mfma")
+    x, so = upload(work)
+    woff = det.window_offsets(work.stream_offsets)
+    N = int(woff[-1])
+    log(f"variants full size: {N} windows")
+    sc, md, mdm, rec = det.score_ext(x, so, torch.from_numpy(woff).cuda(), N, norm="window")
+    g, s, k = _sample(woff, 128, np.random.default_rng(7), n_random=500, n_streams=20)
+    chunk = (1 << 28) // cfg.d                       # windows per chunk of the variant pass
+    edges = [e for c in range(chunk, N, chunk) for e in (c - 1, c)]
+    g = np.array(sorted(set(g.tolist()) | set(edges)), np.int64)
+    s = np.searchsorted(woff, g, side="right") - 1
+    k = g - woff[s]
+    gi = torch.from_numpy(g).cuda()
+    got = [t[gi].cpu().numpy() for t in (sc, md, mdm, rec)]
+    streams = np.unique(s)
+    xs, offs = _sub_workload(work, streams)
+    sub = np.searchsorted(streams, s)
+    ref = ov.score_ext(xs, offs, window=cfg.window, stride=cfg.stride, weights=_weights_f64(w), act=cfg.act,
+                       norm="window", ref_frac=cfg.ref_frac, pairs=list(zip(sub.tolist(), k.tolist())))
+    _check(got, ref, "f32", "variants full size")
+    det.close()
