@@ -80,6 +80,11 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2407_09486_amd.build` "
                            "(or __graft_entry__.build())")
+    # torch's GPU runtime first: the library then binds to the HIP runtime already in the process
+    # (the one that owns the tensors and streams it is given). Loaded and initialised the other
+    # way round, torch can fail to find the device.
+    import torch
+    torch.cuda.is_available()
     L = ctypes.CDLL(LIB_PATH)
     P, I32, I64, F, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
     st = ctypes.c_int

@@ -93,6 +93,8 @@ struct enova_detector_s {
     size_t blk_cap = 0;
     double *gx = nullptr;         // evaluation points of the GPD likelihood sums, then the sums
     size_t gx_cap = 0;
+    double *gpin = nullptr;       // pinned host staging of those points and sums
+    size_t gpin_cap = 0;
     // dense fp32 weights of the output variants: W1 [H][D], [Wmu; Wlv] [2L][H], [bmu | blv] [2L],
     // Wd1 [H][L], Wd2 [D][H], bd2 [D] (one allocation)
     float *dense = nullptr;
@@ -212,6 +214,8 @@ void free_detector(enova_detector d)
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
+    if (d->gpin)
+        (void)hipHostFree(d->gpin);
     for (hipEvent_t e : d->ev)
         if (e)
             (void)hipEventDestroy(e);
@@ -260,31 +264,37 @@ struct DeviceGpdSums : GpdSums {
             return true;
         const int ns = gpd_split(n, nx);
         const size_t np = static_cast<size_t>(nx) * ns;
-        status = ensure(&d->gx, &d->gx_cap, static_cast<size_t>(nx) + 2 * np);
+        status = ensure(&d->gx, &d->gx_cap, 3 * static_cast<size_t>(nx) + 2 * np);
         if (status != ENOVA_OK)
             return false;
-        double *dx = d->gx, *dpa = d->gx + nx, *dpb = dpa + np;
-        std::vector<double> pa(np), pb(np);
+        // pinned host staging: the points, then the two sums per point (3 nx doubles)
+        if (d->gpin_cap < 3 * static_cast<size_t>(nx)) {
+            if (d->gpin)
+                (void)hipHostFree(d->gpin);
+            d->gpin = nullptr;
+            d->gpin_cap = 0;
+            const size_t cap = std::max<size_t>(3 * static_cast<size_t>(nx), 3 * 1024);
+            if (hipHostMalloc(reinterpret_cast<void **>(&d->gpin), cap * sizeof(double)) != hipSuccess) {
+                d->gpin = nullptr;
+                status = fail(ENOVA_ENOMEM, "pinned host buffer of %zu doubles", cap);
+                return false;
+            }
+            d->gpin_cap = cap;
+        }
+        double *dx = d->gx, *dsa = dx + nx, *dsb = dsa + nx, *dpa = dsb + nx, *dpb = dpa + np;
+        double *hx = d->gpin, *hsa = hx + nx, *hsb = hsa + nx;
+        std::copy(xs, xs + nx, hx);
         hipError_t e;
-        if ((e = hipMemcpyAsync(dx, xs, sizeof(double) * nx, hipMemcpyHostToDevice, st)) != hipSuccess ||
+        if ((e = hipMemcpyAsync(dx, hx, sizeof(double) * nx, hipMemcpyHostToDevice, st)) != hipSuccess ||
             (e = launch_gpd_sums(y, n, dx, nx, ns, dpa, dpb, st)) != hipSuccess ||
-            (e = hipMemcpyAsync(pa.data(), dpa, sizeof(double) * np, hipMemcpyDeviceToHost, st)) !=
-                hipSuccess ||
-            (e = hipMemcpyAsync(pb.data(), dpb, sizeof(double) * np, hipMemcpyDeviceToHost, st)) !=
-                hipSuccess ||
+            (e = launch_gpd_reduce(dpa, dpb, nx, ns, dsa, dsb, st)) != hipSuccess ||
+            (e = hipMemcpyAsync(hsa, dsa, sizeof(double) * 2 * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
             (e = hipStreamSynchronize(st)) != hipSuccess) {
             status = hip_fail(e, "GPD likelihood sums");
             return false;
         }
-        for (int i = 0; i < nx; ++i) {
-            double a = 0.0, b = 0.0;
-            for (int j = 0; j < ns; ++j) {
-                a += pa[static_cast<size_t>(i) * ns + j];
-                b += pb[static_cast<size_t>(i) * ns + j];
-            }
-            sa[i] = a;
-            sb[i] = b;
-        }
+        std::copy(hsa, hsa + nx, sa);
+        std::copy(hsb, hsb + nx, sb);
         return true;
     }
 };

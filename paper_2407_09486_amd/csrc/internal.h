@@ -149,6 +149,9 @@ hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream
 int gpd_split(int64_t n, int nx);
 hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
                            double *pa, double *pb, hipStream_t st);
+// sa[i], sb[i] = the chunk partials of point i added in chunk order.
+hipError_t launch_gpd_reduce(const double *pa, const double *pb, int nx, int nsplit, double *sa, double *sb,
+                             hipStream_t st);
 // out = {sum y, min y, max y}; work holds 3 * kPeakBlocks doubles of block partials
 constexpr int kPeakBlocks = 256;
 hipError_t launch_peak_stats(const double *y, int64_t n, double *out, double *work, hipStream_t st);

@@ -555,6 +555,35 @@ hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream
     return hipGetLastError();
 }
 
+// sa[i] = sum over j = 0, 1, ... (in order) of pa[i*nsplit + j], likewise sb from pb: the same
+// fp64 additions in the same order as the host adding the chunks.
+__global__ __launch_bounds__(256) void k_gpd_reduce(const double *__restrict__ pa, const double *__restrict__ pb,
+                                                    int nx, int nsplit, double *__restrict__ sa,
+                                                    double *__restrict__ sb)
+{
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= nx)
+        return;
+    const double *a = pa + static_cast<int64_t>(i) * nsplit, *b = pb + static_cast<int64_t>(i) * nsplit;
+    double ta = 0.0, tb = 0.0;
+    for (int j = 0; j < nsplit; ++j) {
+        ta += a[j];
+        tb += b[j];
+    }
+    sa[i] = ta;
+    sb[i] = tb;
+}
+
+hipError_t launch_gpd_reduce(const double *pa, const double *pb, int nx, int nsplit, double *sa, double *sb,
+                             hipStream_t st)
+{
+    if (nx <= 0)
+        return hipSuccess;
+    hipLaunchKernelGGL(k_gpd_reduce, dim3(static_cast<unsigned>((nx + 255) / 256)), dim3(256), 0, st, pa, pb, nx,
+                       nsplit, sa, sb);
+    return hipGetLastError();
+}
+
 int gpd_split(int64_t n, int nx)
 {
     // about 2048 blocks in all (eight per compute unit: the fp64 division and log1p chains need
