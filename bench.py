@@ -128,7 +128,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the detector shards by stream with no collectives, "
-              "and this build measures the single-GPU kernel (use --gpus 1).", file=sys.stderr)
+              "and the bench measures the single-GPU kernel (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -46,7 +46,7 @@ typedef enum {
     ENOVA_ESHAPE = 2,        /* shapes are valid but the request has no data to act on */
     ENOVA_ENOMEM = 3,        /* device or host allocation failed */
     ENOVA_EHIP = 4,          /* a HIP runtime call or a kernel launch failed */
-    ENOVA_EUNSUPPORTED = 5,  /* a valid request this build does not implement */
+    ENOVA_EUNSUPPORTED = 5,  /* a valid request this library does not implement */
     ENOVA_ENUMERIC = 6       /* non-finite values where finite ones are required */
 } enova_status;
 

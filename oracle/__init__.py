@@ -401,7 +401,7 @@ class Spot:
                        peaks with the new n;
       s <= t           n += 1 only (z_q changes at the next peak);
       s is NaN         flag 0, nothing changes.
-    Readings of this build: once ``peak_cap`` peaks are stored the model is frozen (later
+    Readings taken here (the paper is silent): once ``peak_cap`` peaks are stored the model is frozen (later
     scores are only compared); a stream's level and q are those of the batch threshold.
     """
 

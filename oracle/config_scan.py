@@ -10,7 +10,7 @@ and they come from the centre of a normal-like distribution. Both are read off a
 estimate of the window's observations. The GPU memory is then g(max_num_seqs) for an OLS fit
 m^u = g(n^r) (Eq. (3)).
 
-Readings of this build (the paper fixes none of them):
+Readings taken here (the paper fixes none of them):
 
 * windows are the detector's: W steps, stride S, from step 0 of every stream (Table II);
 * the t-test is two-sided at level alpha on the slope, with W - 2 degrees of freedom:

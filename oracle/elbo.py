@@ -8,7 +8,7 @@ labelled windows by maximising
     L = 1/B sum_i [ l_i * E_q log p(m_i | z)  -  (1 + l_i)/2 * beta(k) * KL(q(z | m_i) || p(z)) ]
 
 with l_i = +1 for a normal window and -1 for an anomalous one, so the KL term acts on normal
-windows only and the reconstruction term pushes anomalies away. Readings of this build (the
+windows only and the reconstruction term pushes anomalies away. Readings taken here (the
 paper fixes none of them): one reparameterised sample z = mu + exp(lv/2) * eps with eps given;
 a unit-variance Gaussian decoder, log p(m|z) = -1/2 |v - m'|^2 - D/2 log(2 pi); beta(k) from a
 PI controller on the batch KL of the normal windows (ControlVAE form: e = KL_set - KL,
