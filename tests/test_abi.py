@@ -176,3 +176,16 @@ def test_output_variants_reject_bad_arguments():
                                     None) == binding.ENOVA_EINVAL
     v = ctypes.c_double()
     assert L.enova_detect_ext_time(None, ctypes.byref(v)) == binding.ENOVA_EINVAL
+
+
+@pytest.mark.parametrize("argv", [["--gpus", "2"], ["--gpus", "8", "--steps", "1"]])
+def test_bench_refuses_more_than_one_gpu(argv):
+    """The bench measures one GPU's share; asked for several it exits with status 2 and says so
+    before touching a device."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv], capture_output=True,
+                       text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr
+    assert r.stdout == ""
