@@ -106,9 +106,18 @@ def cpu_baseline(cfg, weights, budget_s=10.0):
         n_done += int(np.isfinite(sc).sum())
         threads = int(info["threads"])
         s0 = int(streams[-1]) + 1
+    # the same oracle on one thread, over the first stream's sampled windows
+    w1 = wl.generate(cfg, streams=np.arange(0, 1))
+    t0 = time.perf_counter()
+    sc1 = oracle.score(w1.values_f64(), w1.stream_offsets, window=cfg.window, stride=cfg.stride,
+                       weights=weights.as_f64(), act=cfg.act, ref_frac=cfg.ref_frac,
+                       bf16=cfg.dtype == "bf16", max_windows=max_w, threads=1, return_stats=True)[0]
+    dt1 = time.perf_counter() - t0
+    n1 = int(np.isfinite(sc1).sum())
     sample = (f"{cfg.name}: streams 0..{s0 - 1}, "
               + (f"first {max_w} windows each" if max_w else "all windows")
-              + f" ({n_done} windows, {dt:.1f} s of fp64 oracle incl. reference statistics)")
+              + f" ({n_done} windows, {dt:.1f} s of fp64 oracle incl. reference statistics); "
+              + f"on 1 thread {n1 / dt1:.4g} windows/s (stream 0, {n1} windows, {dt1:.1f} s)")
     return {"value": n_done / dt, "unit": "windows/s", "cores": threads, "kind": "oracle", "sample": sample}
 
 
