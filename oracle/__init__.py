@@ -68,6 +68,8 @@ def _load():
     lib.oracle_score_pairs.argtypes = ([P, P, I, I, I, I, I, I, I, P] + [P] * 10 +
                                        [I, P, P, P, P, I64, P, P, P, I])
     lib.oracle_score_pairs.restype = I
+    lib.oracle_bf16_round_array.argtypes = [P, P, I64]
+    lib.oracle_bf16_round_array.restype = None
     _lib = lib
     return lib
 
@@ -108,6 +110,20 @@ def ref_len(T, ref_frac):
 def calibration_count(T, W, S, ref_frac):
     """Windows lying wholly inside the reference prefix: k*S + W <= R."""
     return window_count(ref_len(T, ref_frac), W, S)
+
+
+def bf16_round(a):
+    """Nearest bfloat16 value of each fp64 entry, ties to even, rounded once from fp64.
+
+    The bf16 workload stores the normalised inputs as bfloat16; step 3 of the window
+    evaluation applies this to v = (x - mean) / std computed in fp64.
+    """
+    lib = _load()
+    a = _f64(a)
+    out = np.empty_like(a)
+    if a.size:
+        lib.oracle_bf16_round_array(_ptr(a), _ptr(out), a.size)
+    return out
 
 
 # ----------------------------------------------------------------------------- statistics

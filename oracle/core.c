@@ -19,10 +19,9 @@
  *      md = (1/D) sum_j (v_j - m'_j)  (the decoder is materialised in full here).
  * Thresholding (peaks-over-threshold) is in the Python half of the oracle.
  *
- * For the bf16 workload the kernel stores the normalised value v as bfloat16;
- * the quantisation decision is taken in the kernel's precision (fp32):
- * mean32 = fp32(mean), std32 = fp32(std), v32 = fp32(x - mean32) * fp32(1/std32),
- * v = bf16_rne(v32). Everything after that stays fp64 here.
+ * For the bf16 workload the normalised value is stored as bfloat16: step 3 is
+ * evaluated in fp64, v = (x - mean) / std, and v is then rounded once to the
+ * nearest bfloat16 (ties to even). Everything after that stays fp64 here.
  */
 #include <math.h>
 #include <stdint.h>
@@ -42,17 +41,36 @@ static double act_fn(double a, int kind)
     return a < 0.0 ? 0.0 : a;      /* ReLU; a NaN passes through */
 }
 
-static float bf16_round(float f)
+/*
+ * Nearest bfloat16 value of a double, ties to the even significand (one rounding
+ * straight from fp64, never through fp32). bfloat16 keeps 8 significant bits and
+ * fp32's exponent range: the spacing of representable values at |d| in
+ * [2^(e-1), 2^e) is 2^(e-8), and below the smallest normal (2^-126) the spacing is
+ * the subnormal step 2^-133. A result beyond the largest finite bfloat16
+ * (0x7f7f = (2 - 2^-7) * 2^127) is an infinity of the same sign, as in IEEE
+ * round-to-nearest.
+ */
+double oracle_bf16_round(double d)
 {
-    uint32_t u;
-    memcpy(&u, &f, 4);
-    if ((u & 0x7fffffffu) > 0x7f800000u)
-        return f;                                   /* NaN stays NaN */
-    u += 0x7fffu + ((u >> 16) & 1u);                /* round to nearest, ties to even */
-    u &= 0xffff0000u;
-    float r;
-    memcpy(&r, &u, 4);
+    if (!isfinite(d) || d == 0.0)
+        return d;
+    int e;
+    frexp(d, &e);                                   /* |d| = f * 2^e, f in [0.5, 1) */
+    int qe = e - 8;
+    if (qe < -133)
+        qe = -133;
+    double q = ldexp(1.0, qe);
+    double r = nearbyint(d / q) * q;                /* d / q is exact; default mode ties to even */
+    const double maxbf = ldexp(255.0, 120);         /* (2 - 2^-7) * 2^127 */
+    if (fabs(r) > maxbf)
+        return d > 0 ? INFINITY : -INFINITY;
     return r;
+}
+
+void oracle_bf16_round_array(const double *in, double *out, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = oracle_bf16_round(in[i]);
 }
 
 /* Reference statistics over x[0..R) of one stream (row-major [T][M]). */
@@ -99,19 +117,8 @@ static void score_window(const double *xs, int M, int W, int S, int64_t k, int H
     /* step 3: normalise */
     for (int t = 0; t < W; ++t) {
         for (int m = 0; m < M; ++m) {
-            double xv = xs[(k * S + t) * M + m];
-            double val;
-            if (bf16) {
-                float mu32 = (float)mean[m];
-                float sd32 = (float)std[m];
-                float rinv = 1.0f / sd32;
-                float d = (float)xv - mu32;
-                float v32 = d * rinv;
-                val = (double)bf16_round(v32);
-            } else {
-                val = (xv - mean[m]) / std[m];
-            }
-            v[t * M + m] = val;
+            double val = (xs[(k * S + t) * M + m] - mean[m]) / std[m];
+            v[t * M + m] = bf16 ? oracle_bf16_round(val) : val;
         }
     }
     /* step 4: encoder */

@@ -117,8 +117,67 @@ def test_md_column_sum_identity():
     assert d["md"] == pytest.approx(d["v"].mean() - mean_rec, rel=1e-12, abs=1e-14)
 
 
+def _bf16_table():
+    """Every non-negative bfloat16 value in bit-pattern order (patterns 0 .. 0x7f80). The last
+    entry, pattern 0x7f80 (+inf), stands at 2^128: IEEE rounding overflows to infinity exactly
+    where the nearest value of an unbounded exponent range would be 2^128."""
+    bits = np.arange(0, 0x7f81, dtype=np.uint32) << 16
+    tab = bits.view(np.float32).astype(np.float64)
+    tab[-1] = 2.0 ** 128
+    return tab
+
+
+def _nearest_bf16(d):
+    """Brute force: the nearest entry of the full bfloat16 table, ties to the even bit pattern."""
+    tab = _bf16_table()
+    d = np.asarray(d, np.float64)
+    a = np.abs(d)
+    hi = np.searchsorted(tab, a, side="left")           # tab[hi-1] < a <= tab[hi]
+    hi = np.clip(hi, 1, len(tab) - 1)
+    lo = hi - 1
+    dlo, dhi = a - tab[lo], tab[hi] - a
+    pick = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi)))
+    r = np.where(a == 0, 0.0, tab[pick])
+    r = np.where((r == 2.0 ** 128) | (a >= 2.0 ** 128), np.inf, r)
+    return np.copysign(r, d)
+
+
+def _bf16_probe_values():
+    rng = np.random.default_rng(11)
+    tab = _bf16_table()[:-1]                            # finite values only
+    mag = np.exp2(rng.uniform(-140, 129, 20000))
+    i = rng.integers(0, len(tab) - 1, 4000)
+    mids = 0.5 * (tab[i] + tab[i + 1])                   # exact ties
+    near = np.concatenate([mids * (1 + 2.0 ** -40), mids * (1 - 2.0 ** -40)])  # off-tie by less than fp32 resolves
+    special = np.array([0.0, 2.0 ** -133, 2.0 ** -134, 3 * 2.0 ** -135, 2.0 ** -126, tab[-1],
+                        0.5 * (tab[-1] + 2.0 ** 128), 0.5 * (tab[-1] + 2.0 ** 128) * (1 - 2.0 ** -30)])
+    v = np.concatenate([mag, mids, near, special])
+    sign = np.where(rng.random(len(v)) < 0.5, -1.0, 1.0)
+    return v * sign
+
+
+def test_bf16_round_is_the_nearest_bf16_value():
+    """The oracle's fp64 -> bfloat16 rounding is the nearest representable value, ties to even,
+    including values that a detour through fp32 would round to a tie (1 +- 2^-40 off a midpoint)."""
+    v = _bf16_probe_values()
+    got = oracle.bf16_round(v)
+    exp = _nearest_bf16(v)
+    bad = ~((got == exp) | (np.isinf(got) & np.isinf(exp) & (np.sign(got) == np.sign(exp))))
+    assert not bad.any(), (v[bad][:5], got[bad][:5], exp[bad][:5])
+
+
+def test_bf16_round_matches_torch_on_fp32_values():
+    """On fp32-representable inputs one rounding from fp64 equals torch's float32 -> bfloat16
+    conversion (round to nearest even)."""
+    rng = np.random.default_rng(12)
+    v = (rng.standard_normal(50000) * np.exp2(rng.integers(-30, 30, 50000))).astype(np.float32)
+    exp = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(oracle.bf16_round(v.astype(np.float64)), exp)
+
+
 def test_bf16_mode_rounds_normalised_values():
-    """bf16 workload: staged v is bf16(fp32(x - mean) * fp32(1/std)); the rest is fp64."""
+    """bf16 workload: the staged v is (x - mean) / std evaluated in fp64, then rounded once to
+    the nearest bfloat16; the rest of the window stays fp64."""
     cfg = wl.CONFIGS["c4"].replace(n_streams=1, t_len=64, window=8, stride=2, metrics=4, hidden=8)
     w = wl.generate(cfg)
     Wt = wl.make_weights(cfg)
@@ -126,7 +185,11 @@ def test_bf16_mode_rounds_normalised_values():
     mean = np.array([0.1, -0.3, 2.0, 0.0])
     std = np.array([1.3, 0.7, 3.1, 1.0])
     d = oracle.window_debug(x, 2, window=8, stride=2, weights=Wt.as_f64(), mean=mean, std=std, bf16=True)
-    seg = x[4:12].astype(np.float32)
-    v32 = (seg - mean.astype(np.float32)) * (np.float32(1.0) / std.astype(np.float32))
-    vb = wl.bf16_bits_to_f32(wl.to_bf16_bits(v32.astype(np.float32))).reshape(-1)
-    assert np.array_equal(d["v"], vb.astype(np.float64))
+    v = ((x[4:12] - mean) / std).reshape(-1)
+    assert np.array_equal(d["v"], _nearest_bf16(v))
+    d32 = oracle.window_debug(x, 2, window=8, stride=2, weights=Wt.as_f64(), mean=mean, std=std)
+    assert np.array_equal(d32["v"], v)
+    # the encoder runs on the rounded values in fp64
+    w1 = Wt.as_f64()
+    a = w1["w1"] @ d["v"] + w1["b1"]
+    np.testing.assert_allclose(d["h"], np.maximum(a, 0.0), rtol=1e-12, atol=1e-14)
