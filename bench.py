@@ -20,8 +20,8 @@ With --mode variants it measures the detector-output variants on the config's wo
 window normalised against itself (--norm window, default) or its reference prefix, with its KL
 score, md, per-metric md vector and reconstruction error (one step is one call).
 
-With --mode config it measures the configuration scans (Section IV-A, Eqs. (2)-(3)) over 1024
-services x 16384 one-minute steps of the Table III metrics: every window's OLS fits and t-test,
+With --mode config it measures the configuration scans (Section IV-A, Eqs. (4)-(6)) over 1024
+services x 16384 one-minute steps of the Table II metrics: every window's OLS fits and t-test,
 then each service's KDE limits and configuration (one step is both calls).
 """
 from __future__ import annotations
@@ -681,7 +681,7 @@ def config_main(args):
         "value": round(N / (ms / 1e3), 1), "unit": "windows/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f64",
-        "data": "synthetic (seeded serving metrics of Table III, half the services saturating)",
+        "data": "synthetic (seeded serving metrics of Table II, half the services saturating)",
         "config": {"workload": f"config scans: {CONFIG_STREAMS} services x {CONFIG_STEPS} one-minute steps x {M} "
                                f"metrics, W={W} S=1 ({N} windows)", "windows": N},
         "roofline": {"bound": "alu", "achieved": round(achieved, 3), "peak": 78.6, "unit": "TFLOP/s",

@@ -333,9 +333,9 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
 enova_status enova_detect_ext_time(enova_detector det, double *ms);
 
 /*
- * Configuration scans (Section IV-A, Eqs. (2)-(3), Table III) over the same monitoring series.
+ * Configuration scans (Section IV-A, Eqs. (4)-(6), Table II) over the same monitoring series.
  * Whether the finished-request rate n^f still depends on the number of running requests n^r is
- * decided per window by an ordinary-least-squares fit n^f = a + b n^r and a two-sided t-test of
+ * decided per window by an ordinary-least-squares fit n^f = a + b n^r (the relation n^f = f(n^r) of Eq. (5)) and a two-sided t-test of
  * the slope at level alpha (t = b / sqrt(RSS / ((W - 2) Sxx)), significant iff
  * |t| > t_{1-alpha/2, W-2}; a window with constant n^r has b = 0, a = mean n^f, t = 0); the
  * GPU memory relation m^u = g0 + g1 n^r is fitted by OLS on the same window. Per stream, the last
@@ -343,8 +343,8 @@ enova_status enova_detect_ext_time(enova_detector det, double *ms);
  * (Silverman's bandwidth 0.9 min(sd, IQR/1.34) W^(-1/5), sd if IQR = 0, a point mass if the window
  * is constant) of n^f and of t^r: at level q_extreme when the relation is significant (n^f has not
  * reached its limit, so the limit lies in the upper tail), at 0.5 otherwise (n^f sits at its
- * limit); max_num_seqs = n_limit t^r_limit (Eq. (2)) and gpu_memory = g0 + g1 max_num_seqs
- * (Eq. (3)). Windows are the detector's: W steps, stride S, from step 0 of each stream. All
+ * limit); max_num_seqs = n_limit t^r_limit (Eq. (4)) and gpu_memory = g0 + g1 max_num_seqs
+ * (Eq. (6)). Windows are the detector's: W steps, stride S, from step 0 of each stream. All
  * statistics are computed in fp64.
  */
 typedef struct enova_config_s *enova_config;   /* opaque; owned by the library */

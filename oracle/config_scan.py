@@ -1,14 +1,14 @@
-"""Oracle of the configuration module's scans (Section IV-A, Eqs. (2)-(3), Table III) -- TEST
+"""Oracle of the configuration module's scans (Section IV-A, Eqs. (4)-(6), Table II) -- TEST
 INFRASTRUCTURE ONLY, plain fp64 Python/numpy.
 
-Section IV-A sets max_num_seqs ~ n_limit * t^r_limit (Eq. (2)) from the monitoring series of a
+Section IV-A sets max_num_seqs ~ n_limit * t^r_limit (Eq. (4)) from the monitoring series of a
 service: it first asks whether the finished-request rate n^f still depends on the number of
-running requests n^r, by an ordinary-least-squares fit n^f = f(n^r) and a t-test of its slope.
+running requests n^r, by an ordinary-least-squares fit n^f = f(n^r) (Eq. (5)) and a t-test of its slope.
 A significant relation means n^f has not yet reached its limit, so n_limit and t^r_limit are
 taken from the extreme values of the observed window; no relation means n^f sits at its limit
 and they come from the centre of a normal-like distribution. Both are read off a kernel density
 estimate of the window's observations. The GPU memory is then g(max_num_seqs) for an OLS fit
-m^u = g(n^r) (Eq. (3)).
+m^u = g(n^r) (Eq. (6)).
 
 Readings taken here (the paper fixes none of them):
 
@@ -139,7 +139,7 @@ def kde_quantile(v, q):
 
 def stream_config(x, stream_offsets, *, window, stride, col_f, col_r, col_t, col_m, alpha=0.05,
                   q_extreme=0.99):
-    """The configuration read off each stream's last window (Eqs. (2)-(3)). Returns dict of arrays
+    """The configuration read off each stream's last window (Eqs. (4)-(6)). Returns dict of arrays
     [n_streams]: sig, n_limit, t_limit, max_num_seqs, gpu_memory (NaN for a stream without a
     window)."""
     x = np.asarray(x, np.float64)

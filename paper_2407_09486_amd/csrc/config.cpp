@@ -1,4 +1,4 @@
-// Host side of the configuration scans (Section IV-A, Eqs. (2)-(3)): parameter checks, the
+// Host side of the configuration scans (Section IV-A, Eqs. (4)-(6)): parameter checks, the
 // critical value of the slope's t-test, tile bookkeeping and the launches.
 #include <hip/hip_runtime.h>
 

@@ -750,8 +750,6 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
     return ENOVA_OK;
 }
 
-// Windows per chunk of the output variants: V and the decoder output ([chunk][D] each) within
-// about 512 MiB.
 // Windows per chunk of the variant pass: about 1 GiB of V (every chunk pays each kernel's fixed
 // launch cost once), at most 262144.
 static int ext_chunk(const Geometry &g, int64_t n_windows)

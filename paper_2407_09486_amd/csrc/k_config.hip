@@ -1,4 +1,4 @@
-// Configuration scans (Section IV-A, Eqs. (2)-(3)): per-window OLS fits with the slope's t-test,
+// Configuration scans (Section IV-A, Eqs. (4)-(6)): per-window OLS fits with the slope's t-test,
 // and per-stream KDE quantiles of the last window. All statistics in fp64, every reduction in a
 // fixed order.
 #include <hip/hip_runtime.h>

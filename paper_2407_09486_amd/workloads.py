@@ -443,11 +443,11 @@ def training_batch(cfg: Config, batch: int, seed: int = 0, anomaly_frac: float =
 
 
 # ----------------------------------------------------------------------------- configuration series
-CONFIG_METRICS = ("n_f", "n_r", "n_a", "n_p", "t_r", "m_u", "g_u")   # Table III order
+CONFIG_METRICS = ("n_f", "n_r", "n_a", "n_p", "t_r", "m_u", "g_u")   # Table II order
 
 
 def config_series(n_streams: int, T: int, seed: int = 0) -> Workload:
-    """Serving metrics of n_streams services over T steps (one step = one minute), Table III order.
+    """Serving metrics of n_streams services over T steps (one step = one minute), Table II order.
 
     Arrivals n^a ~ Poisson(lambda_t), lambda_t = base (1 + 0.5 sin(2 pi (t + phase) / 1440)).
     Even streams have capacity C = 3 base (never saturated), odd streams C = 0.8 base (saturated

@@ -1,4 +1,4 @@
-"""GPU parity of the configuration scans (Section IV-A, Eqs. (2)-(3)) through the C ABI: every
+"""GPU parity of the configuration scans (Section IV-A, Eqs. (4)-(6)) through the C ABI: every
 window's OLS fits and t-test, and each stream's KDE limits and configuration, against the fp64
 oracle ``oracle/config_scan.py`` on the same seeded series.
 

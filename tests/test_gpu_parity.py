@@ -46,13 +46,18 @@ def test_subset_parity(name, n, kernel):
     det.close()
 
 
-@pytest.mark.parametrize("name,n", [("c1", 1), ("c2", 3), ("c3", 4)])
+# Every config, each subset scored as its own batch so the calibration sets match: c4 with four
+# full streams (900 calibration windows, an MLE fit), c5 with three streams at their real ragged
+# lengths (45554, 9528 and 29047 steps: 84 K windows, many 256-window tiles per stream).
+@pytest.mark.parametrize("name,n", [("c1", 1), ("c2", 3), ("c3", 4), ("c4", 4), ("c5", 3)])
 def test_threshold_and_flags(name, n):
     cfg, w = _subset(name, n)
     weights = wl.make_weights(cfg)
+    log(f"[threshold] {name} streams={w.streams.tolist()} lengths={np.diff(w.stream_offsets).tolist()}")
     det = detector(cfg, weights)
     sc, md, _, woff = gpu_score(det, w)
     o_sc, _, _ = oracle_score(cfg, w, weights)
+    check_scores(sc, o_sc, cfg.dtype, f"{name} threshold subset")
     import torch
     scores_t = torch.from_numpy(sc).cuda()
     so_t = torch.from_numpy(w.stream_offsets).cuda()

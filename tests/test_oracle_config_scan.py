@@ -1,4 +1,4 @@
-"""Pins of the configuration-scan oracle (Section IV-A, Eqs. (2)-(3)): OLS against least squares
+"""Pins of the configuration-scan oracle (Section IV-A, Eqs. (4)-(6)): OLS against least squares
 and scipy's linregress, the t-test decision against the p-value, critical values against printed
 table values, Silverman's bandwidth on a hand example, the KDE against scipy's gaussian_kde, the
 quantile by its defining equation, and the regime logic on series built to have or lack a
