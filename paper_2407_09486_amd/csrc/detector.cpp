@@ -750,15 +750,6 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
     return ENOVA_OK;
 }
 
-// Windows per chunk of the variant pass: about 1 GiB of V (every chunk pays each kernel's fixed
-// launch cost once), at most 262144.
-static int ext_chunk(const Geometry &g, int64_t n_windows)
-{
-    int64_t c = (int64_t{1} << 28) / g.D;
-    c = std::max<int64_t>(256, std::min<int64_t>(c, 262144));
-    return static_cast<int>(std::min<int64_t>(c, std::max<int64_t>(n_windows, 1)));
-}
-
 enova_status enova_detect_score_ext(enova_detector det, const void *x, const int64_t *soff, const int64_t *woff,
                                     int32_t n, int64_t n_windows, const float *ref_mean, const float *ref_std,
                                     int32_t norm, float *out_scores, float *out_md, float *out_md_metric,
@@ -790,16 +781,11 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
                 return hip_fail(e, "hipEventCreate");
     }
     const int D = g.D, H = g.H, L = g.L, M = g.M;
-    const int B = ext_chunk(g, n_windows);
-    // workspace: V, out [B][D]; a1, h, a2, hd [B][H]; ml [B][2L]; the products' split partials
-    // split partials of the products, for a full chunk and for the last, shorter one
-    int64_t wsg = 0;
-    const int last = static_cast<int>(n_windows - (n_windows - 1) / B * B);
-    for (const int rows : {B, last}) {
-        const int shapes[][3] = {{rows, H, D}, {rows, 2 * L, H}, {rows, H, L}, {rows, D, H}};
-        for (const auto &sh : shapes)
-            wsg = std::max(wsg, gemm_workspace_floats(sh[0], sh[1], sh[2]));
-    }
+    const int B = variants_chunk(D, n_windows);
+    // workspace: V, out [B][D]; a1, h, a2, hd [B][H]; ml [B][2L]; the products' split partials,
+    // for a full chunk and for the last, shorter one
+    const int last = variants_last_rows(n_windows, B);
+    const int64_t wsg = variants_gemm_workspace(B, last, D, H, L);
     // With M a power of two <= 32 the decoder-output product reduces v - m' in its epilogue
     // (per window, metric and column slot) instead of writing m'; `out` then holds those sums.
     const bool fused = M <= 32 && (M & (M - 1)) == 0;

@@ -10,6 +10,7 @@
 #include <cmath>
 #include <type_traits>
 
+#include "gemm_plan.h"
 #include "train_internal.h"
 #include "mfma_common.h"
 
@@ -17,12 +18,7 @@ namespace enova {
 
 namespace {
 
-// C tile of a block (4 waves, each a grid of 32 x 32 matrix ops): 128 x 128 as 2 x 2 waves of
-// 64 x 64; for a product with at most 32 columns 128 x 32 as 4 x 1 waves of 32 x 32, and with at
-// most 32 rows (and more columns) 32 x 128 as 1 x 4 waves, so a thin product does no padded work.
-constexpr int kGemmTile = 128;
-constexpr int kGemmThin = 32;
-constexpr int kGemmK = 32;      // reduction slice staged in LDS (double-buffered)
+// Block tiles, slice length and split limits are in gemm_plan.h.
 // LDS image of one operand slice. A k-contiguous operand is staged row-major, S[row][k] with a
 // pitch of kGemmK + 4 floats (16-byte rows, conflict-free 16-byte reads along k); a
 // row-contiguous operand is staged k-major, S[k][row] with a pitch of ROWS + 4 floats
@@ -35,9 +31,6 @@ constexpr int stage_floats(int rows, bool kcont)
 {
     return kcont ? rows * kGemmPitch : kGemmK * (rows + 4);
 }
-constexpr int kGemmTargetBlocks = 256;   // split the reduction until a launch has about this many blocks
-constexpr int kGemmMinSlice = 128;       // ... but keep every slice at least this long
-constexpr int kGemmMaxSplits = 128;
 constexpr float kLog2Pi = 1.8378770664093453f;   // log(2 pi)
 
 // One operand tile of a slice: ROWS rows (i of A, j of B) x 32 reduction indices. The operand is
@@ -142,12 +135,6 @@ struct EpiParams {
     float *sq;           // kEpiRowReduce: sums of squares
     int ldv, groups;     // kEpiRowReduce
 };
-
-// Waves of a TM x TN block tile along its columns.
-constexpr int gemm_waves_n(int tm, int tn)
-{
-    return 4 / (tn == kGemmTile ? (tm == kGemmTile ? 2 : 1) : 4);
-}
 
 template <int ACT>
 __device__ __forceinline__ float dact_of(float a)
@@ -768,54 +755,6 @@ unsigned blocks_for(int64_t total)
 
 }  // namespace
 
-// The block tile of an m x n product (rows, columns): thin products get a 32-wide side, and so
-// does one whose 128 x 128 tiles would leave most of the chip idle (its longer side is cut into
-// 4x as many tiles, so it needs fewer reduction slices, or none).
-static void gemm_tile(int m, int n, int &tm, int &tn)
-{
-    tm = kGemmTile;
-    tn = kGemmTile;
-    if (n <= kGemmThin) {
-        tn = kGemmThin;
-    } else if (m <= kGemmThin) {
-        tm = kGemmThin;
-    } else {
-        const int64_t tiles = static_cast<int64_t>((m + kGemmTile - 1) / kGemmTile) * ((n + kGemmTile - 1) / kGemmTile);
-        if (tiles < kGemmTargetBlocks / 2) {
-            if (m >= n)
-                tm = kGemmThin;
-            else
-                tn = kGemmThin;
-        }
-    }
-}
-
-static int gemm_splits(int m, int n, int k)
-{
-    int tm, tn;
-    gemm_tile(m, n, tm, tn);
-    const int64_t tiles = static_cast<int64_t>((m + tm - 1) / tm) * ((n + tn - 1) / tn);
-    if (tiles >= kGemmTargetBlocks / 2)
-        return 1;
-    const int by_k = (k + kGemmMinSlice - 1) / kGemmMinSlice;
-    const int by_grid = static_cast<int>((kGemmTargetBlocks + tiles - 1) / tiles);
-    return std::max(1, std::min({by_k, by_grid, kGemmMaxSplits}));
-}
-
-int gemm_reduce_slots(int m, int n)
-{
-    int tm, tn;
-    gemm_tile(m, n, tm, tn);
-    const int cw = tn / gemm_waves_n(tm, tn);
-    return (n + cw - 1) / cw;
-}
-
-int64_t gemm_workspace_floats(int m, int n, int k)
-{
-    const int s = gemm_splits(m, n, k);
-    return s > 1 ? static_cast<int64_t>(s) * (static_cast<int64_t>(m) * n + m) : 0;
-}
-
 namespace {
 
 template <bool AK, bool BK, int EPI, int ACT>
@@ -916,15 +855,9 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
         (epi.groups < 1 || epi.groups > 32 || (epi.groups & (epi.groups - 1)) != 0 || !epi.sq || !epi.out2))
         return hipErrorInvalidValue;
     // never more slices than the caller's workspace holds (a row reduction is never split)
-    int splits = work && epi.kind != kEpiRowReduce ? gemm_splits(m, n, k) : 1;
-    const int64_t per_slice = static_cast<int64_t>(m) * n + m;
-    while (splits > 1 && static_cast<int64_t>(splits) * per_slice > work_floats)
-        --splits;
-    const int kc = splits > 1 ? ((k + splits - 1) / splits + kGemmK - 1) / kGemmK * kGemmK : std::max(k, 1);
-    const int used = splits > 1 ? (k + kc - 1) / kc : 1;
-    int tm, tn;
-    gemm_tile(m, n, tm, tn);
-    const dim3 grid(static_cast<unsigned>((n + tn - 1) / tn), static_cast<unsigned>((m + tm - 1) / tm),
+    const GemmPlan plan = gemm_plan(m, n, k, work && epi.kind != kEpiRowReduce, work_floats);
+    const int kc = plan.kc, used = plan.used;
+    const dim3 grid(static_cast<unsigned>((n + plan.tn - 1) / plan.tn), static_cast<unsigned>((m + plan.tm - 1) / plan.tm),
                     static_cast<unsigned>(used));
     const EpiParams ep{epi.bias, epi.out2, epi.pre, epi.sq, epi.ldv, epi.groups};
     hipError_t e = hipSuccess;

@@ -1,6 +1,7 @@
 // Internal declarations of the training step (matrix-core products and element-wise kernels).
 #pragma once
 
+#include "gemm_plan.h"
 #include "internal.h"
 
 namespace enova {
@@ -15,7 +16,7 @@ struct TrainHyper {
     float margin;   // cap of an anomalous window's reconstruction error (+inf: none)
 };
 // A long reduction over few output tiles is split into slices whose partial tiles go to `work`
-// (gemm_workspace_floats(m, n, k) floats; NULL: no split) and are then summed in slice order.
+// (gemm_workspace_floats(m, n, k) floats, gemm_plan.h; NULL: no split) and are then summed in slice order.
 // rowsum (or NULL) receives sum_k A(i, k) for every i < m. The epilogue fuses the element-wise
 // step that follows a product: store; C = product + bias[j] with out2 = act(C); or
 // C = product * act'(pre) (pre in C's layout).
@@ -36,9 +37,6 @@ struct GemmEpilogue {
     int ldv = 0;            // kEpiRowReduce: leading dimension of pre
     int groups = 0;         // kEpiRowReduce
 };
-int64_t gemm_workspace_floats(int m, int n, int k);
-// Column slots of an m x n kEpiRowReduce product (at most (n + 31) / 32).
-int gemm_reduce_slots(int m, int n);
 // ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
 // `work` holds work_floats floats; a product splits only as far as they allow (none when work is
 // NULL).

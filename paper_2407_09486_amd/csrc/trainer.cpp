@@ -90,14 +90,7 @@ enova_status alloc_floats(float **dst, size_t n)
 
 int64_t workspace_floats(const enova_trainer t, int B)
 {
-    // every product of a step, as (m, n, k)
-    const int D = t->D, H = t->H, L = t->L;
-    const int shapes[][3] = {{B, H, D},     {B, 2 * L, H}, {B, H, L}, {B, D, H}, {D, H, B}, {B, H, D},
-                             {H, L, B},     {B, L, H},     {2 * L, H, B}, {B, H, 2 * L}, {H, D, B}};
-    int64_t ws = 0;
-    for (const auto &sh : shapes)
-        ws = std::max(ws, gemm_workspace_floats(sh[0], sh[1], sh[2]));
-    return ws;
+    return train_gemm_workspace(B, t->D, t->H, t->L);
 }
 
 // Grows the batch buffers to B rows (freeing the old ones synchronises the device).

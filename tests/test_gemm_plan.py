@@ -1,0 +1,156 @@
+"""Host check of the matrix-core product's launch planner (csrc/gemm_plan.h), CPU only.
+
+A product whose reduction is split writes one partial tile (and row sums) per slice into a
+caller-given workspace; the planner must never launch more slices than that workspace holds.
+The variant pass once sized its workspace for a full chunk only and faulted the GPU on a short
+last chunk whose products split further; the planner now clamps the split to the workspace and
+the pass sizes it for both chunk lengths. The header is compiled for the host with g++ and its
+plans are checked here over the training, variant and benchmark shapes; nothing touches a GPU.
+"""
+import os
+import shutil
+import subprocess
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2407_09486_amd", "csrc")
+
+PROGRAM = r"""
+#include "gemm_plan.h"
+#include <cstdio>
+#include <cstring>
+using namespace enova;
+int main() {
+    char op[8];
+    while (std::scanf("%7s", op) == 1) {
+        if (!std::strcmp(op, "P")) {           // m n k may_split work_floats -> tm tn kc used
+            int m, n, k, may; long long ws;
+            std::scanf("%d %d %d %d %lld", &m, &n, &k, &may, &ws);
+            GemmPlan p = gemm_plan(m, n, k, may != 0, ws);
+            std::printf("%d %d %d %d\n", p.tm, p.tn, p.kc, p.used);
+        } else if (!std::strcmp(op, "S")) {    // m n k -> splits, workspace, slice floats
+            int m, n, k;
+            std::scanf("%d %d %d", &m, &n, &k);
+            std::printf("%d %lld %lld\n", gemm_splits(m, n, k), (long long)gemm_workspace_floats(m, n, k),
+                        (long long)gemm_slice_floats(m, n));
+        } else if (!std::strcmp(op, "V")) {    // D H L n_windows -> chunk, last rows, workspace
+            int D, H, L; long long N;
+            std::scanf("%d %d %d %lld", &D, &H, &L, &N);
+            int B = variants_chunk(D, N), last = variants_last_rows(N, B);
+            std::printf("%d %d %lld\n", B, last, (long long)variants_gemm_workspace(B, last, D, H, L));
+        } else if (!std::strcmp(op, "T")) {    // B D H L -> training workspace
+            int B, D, H, L;
+            std::scanf("%d %d %d %d", &B, &D, &H, &L);
+            std::printf("%lld\n", (long long)train_gemm_workspace(B, D, H, L));
+        }
+        std::fflush(stdout);
+    }
+    return 0;
+}
+"""
+
+
+class Planner:
+    def __init__(self, exe):
+        self.exe = exe
+
+    def run(self, lines):
+        r = subprocess.run([self.exe], input="\n".join(lines) + "\n", capture_output=True, text=True,
+                           check=True, timeout=60)
+        return [list(map(int, ln.split())) for ln in r.stdout.strip().splitlines()]
+
+
+@pytest.fixture(scope="module")
+def planner():
+    gxx = shutil.which("g++")
+    if not gxx:
+        pytest.skip("g++ not available")
+    d = tempfile.mkdtemp()
+    try:
+        src = os.path.join(d, "plan.cpp")
+        exe = os.path.join(d, "plan")
+        with open(src, "w") as f:
+            f.write(PROGRAM)
+        subprocess.run([gxx, "-std=c++17", "-O1", "-Wall", "-I", CSRC, src, "-o", exe], check=True)
+        yield Planner(exe)
+    finally:
+        shutil.rmtree(d, ignore_errors=True)
+
+
+def _check_plans(planner, shapes, ws, may=1):
+    """Every plan covers k exactly with whole slices and its partials fit the workspace."""
+    out = planner.run([f"P {m} {n} {k} {may} {ws}" for m, n, k in shapes])
+    slice_f = planner.run([f"S {m} {n} {k}" for m, n, k in shapes])
+    for (m, n, k), (tm, tn, kc, used), (_, _, per) in zip(shapes, out, slice_f):
+        assert used >= 1 and kc >= 1
+        assert (used - 1) * kc < max(k, 1) <= used * kc, (m, n, k, kc, used)
+        if used > 1:
+            assert kc % 32 == 0, (m, n, k, kc)
+            assert used * per <= ws, f"{(m, n, k)}: {used} slices x {per} floats > workspace {ws}"
+        assert tm in (32, 128) and tn in (32, 128)
+    return out
+
+
+# (D, H, L) of the five detector shapes and of the variant tests
+DET = [(256, 32, 16), (512, 64, 16), (2048, 128, 16), (8192, 256, 16), (1024, 128, 16),
+       (64 * 5, 128, 16), (32 * 3, 64, 8), (16 * 12, 32, 4)]
+
+
+def _variant_shapes(rows, D, H, L):
+    return [(rows, H, D), (rows, 2 * L, H), (rows, H, L), (rows, D, H)]
+
+
+@pytest.mark.parametrize("D,H,L", DET)
+def test_variant_pass_products_fit_their_workspace(planner, D, H, L):
+    # n_windows around the chunk length, the c5 benchmark's window count and its old fault case
+    chunk = planner.run([f"V {D} {H} {L} 1000000000"])[0][0]
+    counts = {1, 7, 255, 256, 257, 12842, chunk - 1, chunk, chunk + 1, 2 * chunk + 12842, 3 * chunk + 100,
+              134951466}
+    for N in sorted(c for c in counts if c >= 1):
+        B, last, ws = planner.run([f"V {D} {H} {L} {N}"])[0]
+        assert 1 <= last <= B and (N - last) % B == 0
+        assert B == min(N, max(256, min((1 << 28) // D, 262144)))
+        for rows in {B, last}:
+            _check_plans(planner, _variant_shapes(rows, D, H, L), ws)
+
+
+def test_short_last_chunk_is_clamped_to_a_full_chunk_workspace(planner):
+    """The fault's mechanism: c5's variant pass (D = 1024, H = 128, L = 16) in full chunks needs
+    no split workspace, but a short last chunk (2000 windows here) has so few output tiles that its
+    encoder product wants several slices; with a workspace sized for the full chunk only, the
+    planner must split less instead of writing past the workspace."""
+    D, H, L = 1024, 128, 16
+    B = planner.run([f"V {D} {H} {L} 1000000000"])[0][0]
+    _, _, ws_full_only = planner.run([f"V {D} {H} {L} {B}"])[0]
+    wanted = planner.run([f"S 2000 {H} {D}"])[0]
+    assert wanted[0] > 1 and wanted[0] * wanted[2] > ws_full_only      # it wants more than there is
+    out = _check_plans(planner, _variant_shapes(2000, D, H, L), ws_full_only)
+    assert out[0][3] * wanted[2] <= ws_full_only or out[0][3] == 1
+    # the pass itself sizes the workspace for the last chunk too, so there it splits as it wants
+    _, last, ws = planner.run([f"V {D} {H} {L} {B + 2000}"])[0]
+    assert last == 2000
+    out = _check_plans(planner, _variant_shapes(2000, D, H, L), ws)
+    assert out[0][3] == wanted[0]
+    # no workspace at all: nothing splits
+    out = _check_plans(planner, _variant_shapes(2000, D, H, L), 0)
+    assert all(p[3] == 1 for p in out)
+    # a product that may not split (a reduction epilogue) never does, whatever the workspace
+    out = _check_plans(planner, _variant_shapes(300, D, H, L), 1 << 40, may=0)
+    assert all(p[3] == 1 for p in out)
+
+
+@pytest.mark.parametrize("B", [1, 31, 32, 33, 127, 128, 500, 4096, 8192, 8193, 65536])
+@pytest.mark.parametrize("D,H,L", [(1024, 128, 16), (256, 32, 16), (8192, 256, 16), (12, 5, 3)])
+def test_training_products_fit_their_workspace(planner, B, D, H, L):
+    ws = planner.run([f"T {B} {D} {H} {L}"])[0][0]
+    shapes = [(B, H, D), (B, 2 * L, H), (B, H, L), (B, D, H), (D, H, B), (B, H, D), (H, L, B), (B, L, H),
+              (2 * L, H, B), (B, H, 2 * L), (H, D, B)]
+    out = _check_plans(planner, shapes, ws)
+    # with the step's own workspace every product splits as far as it wants
+    want = planner.run([f"S {m} {n} {k}" for m, n, k in shapes])
+    for (m, n, k), p, w in zip(shapes, out, want):
+        assert p[3] <= w[0]
+        if w[0] > 1:
+            assert p[3] > 1, (m, n, k)
