@@ -143,6 +143,27 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
                                 hipStream_t stream);
 
 /*
+ * enova_detect_score without any allocation, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, hosts that forbid hipMalloc). Arguments,
+ * results and errors are those of enova_detect_score, with the same kernels; it calls no
+ * hipMalloc, hipFree or allocating routine, and records no timing events (kernel timing reports
+ * nothing for it). Its workspace -- the reference statistics when ref_mean/ref_std are NULL
+ * (2 * n_streams * M floats), and for the matrix-core kernel the tile offsets
+ * ((n_streams + 1) int64) and block-to-stream map ((n_windows + Nb - 1) / Nb + n_streams ints,
+ * Nb = windows per tile: 128-512 by shape), each rounded up to 256 bytes -- lives in a fixed
+ * 16 MiB device array that the library holds on every GPU it runs on until the process ends,
+ * shared by all detectors on that GPU. A call that needs more returns ENOVA_ESHAPE before any
+ * launch. Every part of that workspace is fully rewritten by each call before it is read, so no
+ * clearing is needed between calls; calls that overlap on one GPU (on different streams, or from
+ * several threads) race on the array and must be serialised by the caller.
+ */
+enova_status enova_detect_score_noalloc(enova_detector det, const void *x, const int64_t *stream_offsets,
+                                        const int64_t *window_offsets, int32_t n_streams, int64_t n_windows,
+                                        const float *ref_mean, const float *ref_std, float threshold,
+                                        float *out_scores, float *out_md, uint8_t *out_flags,
+                                        hipStream_t stream);
+
+/*
  * Peaks-over-threshold threshold (Section IV-B, citing Siffer et al. 2017), static and global:
  * the calibration set is the scores of the windows lying wholly inside each stream's reference
  * prefix (k*S + W <= floor(ref_frac*T_s)); t is its order statistic at ceil(level*n) - 1

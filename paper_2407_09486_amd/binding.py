@@ -29,7 +29,8 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_train_init", "enova_train_step", "enova_train_params_get", "enova_train_grads_get",
            "enova_train_set_timing", "enova_train_set_graph", "enova_train_kernel_times", "enova_train_destroy",
            "enova_detect_score_ext", "enova_detect_ext_time", "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
-           "enova_config_scan", "enova_config_recommend", "enova_config_set_timing", "enova_config_kernel_time", "enova_status_str", "enova_last_error"]
+           "enova_config_scan", "enova_config_recommend", "enova_config_set_timing", "enova_config_kernel_time",
+           "enova_detect_score_noalloc", "enova_status_str", "enova_last_error"]
 
 
 class EnovaError(RuntimeError):
@@ -94,6 +95,7 @@ def lib():
     L.enova_detect_window_offsets.argtypes = [P, P, I32, P]
     L.enova_detect_ref_stats.argtypes = [P, P, P, I32, P, P, P]
     L.enova_detect_score.argtypes = [P, P, P, P, I32, I64, P, P, F, P, P, P, P]
+    L.enova_detect_score_noalloc.argtypes = [P, P, P, P, I32, I64, P, P, F, P, P, P, P]
     L.enova_detect_threshold.argtypes = [P, P, P, P, I32, I64, D, D, P, P, P, P]
     L.enova_detect_flag.argtypes = [P, P, I64, F, P, P]
     L.enova_detect_set_timing.argtypes = [P, I32]
@@ -199,6 +201,15 @@ def enova_detect_score(handle, x, stream_offsets, window_offsets, n_streams, n_w
                                     _dptr(ref_mean), _dptr(ref_std), float(threshold),
                                     _dptr(out_scores), _dptr(out_md), _dptr(out_flags), _stream(stream)),
            "enova_detect_score")
+
+
+def enova_detect_score_noalloc(handle, x, stream_offsets, window_offsets, n_streams, n_windows,
+                               ref_mean, ref_std, threshold, out_scores, out_md, out_flags, stream=None):
+    _check(lib().enova_detect_score_noalloc(ctypes.c_void_p(handle), _dptr(x), _dptr(stream_offsets),
+                                            _dptr(window_offsets), int(n_streams), int(n_windows),
+                                            _dptr(ref_mean), _dptr(ref_std), float(threshold),
+                                            _dptr(out_scores), _dptr(out_md), _dptr(out_flags), _stream(stream)),
+           "enova_detect_score_noalloc")
 
 
 def enova_detect_threshold(handle, scores, stream_offsets, window_offsets, n_streams, n_windows,

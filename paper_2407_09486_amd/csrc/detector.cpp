@@ -95,6 +95,9 @@ struct enova_detector_s {
     size_t gx_cap = 0;
     double *gpin = nullptr;       // pinned host staging of those points and sums
     size_t gpin_cap = 0;
+    // this device's fixed scratch (kScratchBytes, shared by every detector on the device), the
+    // only workspace of enova_detect_score_noalloc
+    void *scratch = nullptr;
     // dense fp32 weights of the output variants: W1 [H][D], [Wmu; Wlv] [2L][H], [bmu | blv] [2L],
     // Wd1 [H][L], Wd2 [D][H], bd2 [D] (one allocation)
     float *dense = nullptr;
@@ -355,6 +358,14 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
     if (hipGetDevice(&d->device) != hipSuccess) {
         free_detector(d);
         return fail(ENOVA_EHIP, "no current HIP device");
+    }
+    {
+        // the device address of this device's fixed scratch, looked up with the device current
+        const hipError_t e = scratch_setup(d->device, &d->scratch);
+        if (e != hipSuccess) {
+            free_detector(d);
+            return hip_fail(e, "device scratch lookup");
+        }
     }
 
     const int H = g.H, L = g.L, D = g.D, Hp = g.Hp;
@@ -644,11 +655,36 @@ enova_status enova_detect_ref_stats(enova_detector det, const void *x, const int
     return ENOVA_OK;
 }
 
-enova_status enova_detect_score(enova_detector det, const void *x, const int64_t *soff,
-                                const int64_t *woff, int32_t n, int64_t n_windows,
-                                const float *ref_mean, const float *ref_std, float threshold,
-                                float *out_scores, float *out_md, uint8_t *out_flags,
-                                hipStream_t stream)
+namespace {
+
+// The scoring path's workspace: reference statistics [2][n][M] floats (when the caller gives
+// none), the matrix-core kernel's first tile of each stream [n+1] and stream of each block [grid].
+struct ScoreWork {
+    float *stats = nullptr;
+    int64_t *tiles = nullptr;
+    int *tile_map = nullptr;
+};
+
+// Bytes of the fixed-scratch layout of that workspace, each part on a 256-byte boundary.
+size_t noalloc_bytes(const Geometry &g, int kind, int32_t n, int64_t grid, bool stats, size_t *o_tiles,
+                     size_t *o_map)
+{
+    auto up = [](size_t v) { return (v + 255) / 256 * 256; };
+    size_t o = stats ? up(2 * static_cast<size_t>(n) * g.M * sizeof(float)) : 0;
+    *o_tiles = o;
+    if (kind == 2)
+        o += up((static_cast<size_t>(n) + 1) * sizeof(int64_t));
+    *o_map = o;
+    if (kind == 2)
+        o += up(static_cast<size_t>(grid > 0 ? grid : 1) * sizeof(int));
+    return o;
+}
+
+// Both scoring entry points. noalloc: the workspace is carved from the device's fixed scratch
+// (no allocation, no timing events); otherwise it is the detector's grow-only workspace.
+enova_status score_common(enova_detector det, const void *x, const int64_t *soff, const int64_t *woff, int32_t n,
+                          int64_t n_windows, const float *ref_mean, const float *ref_std, float threshold,
+                          float *out_scores, float *out_md, uint8_t *out_flags, hipStream_t stream, bool noalloc)
 {
     if (!det)
         return fail(ENOVA_EINVAL, "detector is NULL");
@@ -662,30 +698,64 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
     if (!x || !soff || !woff || !out_scores)
         return fail(ENOVA_EINVAL, "NULL argument");
     const bool want_flags = out_flags != nullptr && !std::isnan(threshold);
+    const Geometry &g = det->g;
+    const int64_t grid = det->kind == 2 ? (n_windows + g.Nb - 1) / g.Nb + n : 0;
+    if (grid > 0x7fffffffLL)
+        return fail(ENOVA_EUNSUPPORTED, "too many tiles (%lld)", static_cast<long long>(grid));
+    if (det->kind != 2 && (n_windows + 15) / 16 > 0x7fffffffLL)
+        return fail(ENOVA_EUNSUPPORTED, "too many windows");
+    ScoreWork wk;
+    if (noalloc) {
+        size_t o_tiles = 0, o_map = 0;
+        const size_t need = noalloc_bytes(g, det->kind, n, grid, !ref_mean, &o_tiles, &o_map);
+        if (need > kScratchBytes)
+            return fail(ENOVA_ESHAPE,
+                        "the allocation-free call needs %zu bytes of device scratch for %d streams and %lld "
+                        "windows; it has %zu",
+                        need, n, static_cast<long long>(n_windows), kScratchBytes);
+        if (!det->scratch)
+            return fail(ENOVA_EHIP, "device scratch unavailable");
+        unsigned char *base = static_cast<unsigned char *>(det->scratch);
+        wk.stats = reinterpret_cast<float *>(base);
+        wk.tiles = reinterpret_cast<int64_t *>(base + o_tiles);
+        wk.tile_map = reinterpret_cast<int *>(base + o_map);
+    }
     DeviceGuard dg(det->device);
     if (!dg.ok)
         return fail(ENOVA_EHIP, "cannot select the detector's device");
-    const Geometry &g = det->g;
     hipError_t e;
-    if (det->timing && !det->ev[0]) {
+    const bool timing = det->timing && !noalloc;
+    if (timing && !det->ev[0]) {
         for (auto &ev : det->ev)
             if ((e = hipEventCreate(&ev)) != hipSuccess)
                 return hip_fail(e, "hipEventCreate");
     }
-    if (!ref_mean) {
-        enova_status st = ensure(&det->stats, &det->stats_cap, 2 * static_cast<size_t>(n) * g.M);
+    if (!noalloc) {
+        enova_status st = ENOVA_OK;
+        if (!ref_mean)
+            st = ensure(&det->stats, &det->stats_cap, 2 * static_cast<size_t>(n) * g.M);
+        if (st == ENOVA_OK && det->kind == 2) {
+            st = ensure(&det->tiles, &det->tiles_cap, static_cast<size_t>(n) + 1);
+            if (st == ENOVA_OK)
+                st = ensure(&det->tile_map, &det->tile_map_cap, static_cast<size_t>(grid > 0 ? grid : 1));
+        }
         if (st != ENOVA_OK)
             return st;
-        ref_mean = det->stats;
-        ref_std = det->stats + static_cast<size_t>(n) * g.M;
-        if (det->timing)
+        wk.stats = det->stats;
+        wk.tiles = det->tiles;
+        wk.tile_map = det->tile_map;
+    }
+    if (!ref_mean) {
+        ref_mean = wk.stats;
+        ref_std = wk.stats + static_cast<size_t>(n) * g.M;
+        if (timing)
             (void)hipEventRecord(det->ev[0], stream);
-        e = launch_ref_stats(g, x, soff, n, det->stats, det->stats + static_cast<size_t>(n) * g.M, stream);
+        e = launch_ref_stats(g, x, soff, n, wk.stats, wk.stats + static_cast<size_t>(n) * g.M, stream);
         if (e != hipSuccess)
             return hip_fail(e, "reference statistics kernel");
-        if (det->timing)
+        if (timing)
             (void)hipEventRecord(det->ev[1], stream);
-        det->ran_stats = true;
+        det->ran_stats = timing;
     }
     ScoreParams p{};
     p.x = x;
@@ -715,39 +785,50 @@ enova_status enova_detect_score(enova_detector det, const void *x, const int64_t
     p.md = out_md;
     p.flags = out_flags;
     if (det->kind == 2) {
-        enova_status st = ensure(&det->tiles, &det->tiles_cap, static_cast<size_t>(n) + 1);
-        if (st != ENOVA_OK)
-            return st;
-        e = launch_stream_scan(g, soff, woff, n, 0, g.Nb, det->tiles, stream);
+        e = launch_stream_scan(g, soff, woff, n, 0, g.Nb, wk.tiles, stream);
         if (e != hipSuccess)
             return hip_fail(e, "tile scan kernel");
-        p.tile_off = det->tiles;
-        const int64_t grid = (n_windows + g.Nb - 1) / g.Nb + n;
-        if (grid > 0x7fffffffLL)
-            return fail(ENOVA_EUNSUPPORTED, "too many tiles (%lld)", static_cast<long long>(grid));
-        st = ensure(&det->tile_map, &det->tile_map_cap, static_cast<size_t>(grid > 0 ? grid : 1));
-        if (st != ENOVA_OK)
-            return st;
-        e = launch_tile_map(det->tiles, n, grid, det->tile_map, stream);
+        p.tile_off = wk.tiles;
+        e = launch_tile_map(wk.tiles, n, grid, wk.tile_map, stream);
         if (e != hipSuccess)
             return hip_fail(e, "tile map kernel");
-        p.tile_stream = det->tile_map;
-        if (det->timing)
+        p.tile_stream = wk.tile_map;
+        if (timing)
             (void)hipEventRecord(det->ev[2], stream);
         e = launch_score_mfma(g, p, grid, stream);
     } else {
-        if ((n_windows + 15) / 16 > 0x7fffffffLL)
-            return fail(ENOVA_EUNSUPPORTED, "too many windows");
-        if (det->timing)
+        if (timing)
             (void)hipEventRecord(det->ev[2], stream);
         e = launch_score_valu(g, p, stream);
     }
     if (e != hipSuccess)
         return hip_fail(e, "scoring kernel");
-    if (det->timing)
+    if (timing)
         (void)hipEventRecord(det->ev[3], stream);
-    det->ran_score = true;
+    det->ran_score = timing;
     return ENOVA_OK;
+}
+
+}  // namespace
+
+enova_status enova_detect_score(enova_detector det, const void *x, const int64_t *soff,
+                                const int64_t *woff, int32_t n, int64_t n_windows,
+                                const float *ref_mean, const float *ref_std, float threshold,
+                                float *out_scores, float *out_md, uint8_t *out_flags,
+                                hipStream_t stream)
+{
+    return score_common(det, x, soff, woff, n, n_windows, ref_mean, ref_std, threshold, out_scores, out_md,
+                        out_flags, stream, false);
+}
+
+enova_status enova_detect_score_noalloc(enova_detector det, const void *x, const int64_t *soff,
+                                        const int64_t *woff, int32_t n, int64_t n_windows,
+                                        const float *ref_mean, const float *ref_std, float threshold,
+                                        float *out_scores, float *out_md, uint8_t *out_flags,
+                                        hipStream_t stream)
+{
+    return score_common(det, x, soff, woff, n, n_windows, ref_mean, ref_std, threshold, out_scores, out_md,
+                        out_flags, stream, true);
 }
 
 enova_status enova_detect_score_ext(enova_detector det, const void *x, const int64_t *soff, const int64_t *woff,

@@ -54,6 +54,12 @@ constexpr size_t kLdsLimit = 160 * 1024;
 constexpr int kPrefetchSteps = 8;
 constexpr int kPrefetchRows = 2;
 
+// Fixed device scratch of the allocation-free scoring entry point: kScratchBytes per device.
+// scratch_setup returns this device's copy (device must be current); the lookup happens once per
+// device and is then cached.
+constexpr size_t kScratchBytes = size_t{16} << 20;
+hipError_t scratch_setup(int device, void **out);
+
 // Error reporting of the C entry points: records the message returned by enova_last_error().
 enova_status fail(enova_status st, const char *fmt, ...);
 enova_status hip_fail(hipError_t e, const char *what);
