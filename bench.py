@@ -80,6 +80,19 @@ def load_traffic(config_name: str):
         return None
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (first processor of /proc/cpuinfo), or the platform's guess."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(cfg, weights, budget_s=10.0):
     """The oracle (all host cores) on groups of leading streams, each capped at a number of windows
     per stream, until about budget_s seconds of work have been timed."""
@@ -118,7 +131,54 @@ def cpu_baseline(cfg, weights, budget_s=10.0):
               + (f"first {max_w} windows each" if max_w else "all windows")
               + f" ({n_done} windows, {dt:.1f} s of fp64 oracle incl. reference statistics); "
               + f"on 1 thread {n1 / dt1:.4g} windows/s (stream 0, {n1} windows, {dt1:.1f} s)")
-    return {"value": n_done / dt, "unit": "windows/s", "cores": threads, "kind": "oracle", "sample": sample}
+    return {"value": n_done / dt, "unit": "windows/s", "cores": threads, "cpu_model": cpu_model(),
+            "kind": "oracle", "sample": sample}
+
+
+def secondary_leg(name, launches=5, warmup=2):
+    """Kernel-only timing of the scorer on a second workload (after the headline's timed region,
+    not part of ms_per_step): the bf16 matrix-core path of the 16384-stream workload by default."""
+    import numpy as np
+    import torch
+
+    from paper_2407_09486_amd import binding
+    from paper_2407_09486_amd import workloads as wl
+    cfg = wl.CONFIGS[name]
+    t0 = time.perf_counter()
+    w = wl.generate(cfg)
+    weights = wl.make_weights(cfg)
+    print(f"[bench] secondary {cfg.name}: generated in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+          flush=True)
+    dev = torch.device("cuda", 0)
+    x = torch.from_numpy(w.x_bits.view(np.int16) if cfg.dtype == "bf16" else w.x).to(dev)
+    so = torch.from_numpy(w.stream_offsets).to(dev)
+    so_h = w.stream_offsets
+    del w
+    det = binding.Detector(cfg.metrics, cfg.window, cfg.stride, cfg.hidden,
+                           binding.weights_for_library(weights, cfg.dtype), latent=cfg.latent,
+                           dtype=cfg.dtype, act=cfg.act, ref_frac=cfg.ref_frac)
+    binding.enova_detect_set_timing(det.handle, True)
+    woff_h = det.window_offsets(so_h)
+    N = int(woff_h[-1])
+    wo = torch.from_numpy(woff_h).to(dev)
+    scores = torch.empty(N, dtype=torch.float32, device=dev)
+    md = torch.empty(N, dtype=torch.float32, device=dev)
+    ks = []
+    for i in range(warmup + launches):
+        binding.enova_detect_score(det.handle, x, so, wo, len(so_h) - 1, N, None, None, math.nan, scores, md, None)
+        torch.cuda.synchronize()
+        if i >= warmup:
+            ks.append(binding.enova_detect_kernel_times(det.handle)[0])
+    det.close()
+    k_ms = float(np.median(ks))
+    fpw = flops_per_window(cfg)
+    achieved = fpw * N / (k_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    return {"workload": f"{cfg.name}: {cfg.description}", "dtype": cfg.dtype, "windows": N,
+            "kernel": "k_score_mfma", "kernel_ms": round(k_ms, 4), "launches": launches,
+            "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+            "traffic": load_traffic(cfg.name),
+            "note": "kernel-only (library HIP events, median of the launches); not part of ms_per_step"}
 
 
 def main():
@@ -134,6 +194,9 @@ def main():
     ap.add_argument("--norm", choices=["window", "reference"], default="window",
                     help="normalisation of --mode variants")
     ap.add_argument("--batch", type=int, default=8192, help="windows per training step (--mode train)")
+    ap.add_argument("--secondary", default="auto",
+                    help="second workload timed kernel-only after the headline (auto: c4 when the headline "
+                         "is c5; none: skip)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the detector shards by stream with no collectives, "
@@ -251,9 +314,16 @@ def main():
                    "wall_windows_per_s": round(value, 1), "threshold": thr_hist[-1]},
         "roofline": roof,
     }
+    det.close()
+    sec = args.secondary
+    if sec == "auto":
+        sec = "c4" if cfg.name == "c5" else "none"
+    if sec != "none":
+        del x, so, scores, md, flags
+        torch.cuda.empty_cache()
+        out["secondary"] = secondary_leg(sec)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, weights)
-    det.close()
     print(json.dumps(out), flush=True)
 
 
@@ -289,7 +359,7 @@ def stream_cpu_baseline(cfg, weights, x_ref, x_live, n_streams, pushes):
             sp.step(float(v))
     dt = time.perf_counter() - t0
     n = sc.size
-    return {"value": n / dt, "unit": "windows/s", "cores": int(info["threads"]), "kind": "oracle",
+    return {"value": n / dt, "unit": "windows/s", "cores": int(info["threads"]), "cpu_model": cpu_model(), "kind": "oracle",
             "sample": f"streams 0..{k - 1}, {sc.shape[1]} pushes each ({n} windows + SPOT steps, {dt:.1f} s)"}
 
 
@@ -427,7 +497,7 @@ def train_cpu_baseline(cfg, p0, batch, margin, budget_s=10.0):
             break
     threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     B = V.shape[0]
-    return {"value": round(k * B / dt, 1), "unit": "windows/s", "cores": int(threads), "kind": "oracle",
+    return {"value": round(k * B / dt, 1), "unit": "windows/s", "cores": int(threads), "cpu_model": cpu_model(), "kind": "oracle",
             "sample": f"{k} fp64 oracle steps on the same {B}-window batch ({dt:.1f} s, numpy BLAS threads)"}
 
 
@@ -530,7 +600,7 @@ def variants_cpu_baseline(cfg, w, work, norm, budget_s=10.0):
         n += len(r["score"])
         k += 1
     dt = time.perf_counter() - t0
-    return {"value": round(n / dt, 1), "unit": "windows/s", "cores": 1, "kind": "oracle",
+    return {"value": round(n / dt, 1), "unit": "windows/s", "cores": 1, "cpu_model": cpu_model(), "kind": "oracle",
             "sample": f"windows 0..{k - 1} of streams 0..63 ({n} windows, {dt:.1f} s, fp64, one core)"}
 
 
@@ -629,7 +699,7 @@ def config_cpu_baseline(x, offs, W, budget_s=10.0):
         n += len(r["b"])
         s += 1
     dt = time.perf_counter() - t0
-    return {"value": round(n / dt, 1), "unit": "windows/s", "cores": 1, "kind": "oracle",
+    return {"value": round(n / dt, 1), "unit": "windows/s", "cores": 1, "cpu_model": cpu_model(), "kind": "oracle",
             "sample": f"first 2048 steps of streams 0..{s - 1} ({n} windows, {dt:.1f} s, fp64 Python loops)"}
 
 
