@@ -71,6 +71,9 @@ struct enova_detector_s {
     int kind = 1;                 // 1 vector-ALU, 2 matrix-core
     // weights
     void *w1p = nullptr;          // matrix-core A fragments
+    void *ring_w = nullptr;       // ring kernel: W1, heads and decoder fragments (one allocation)
+    const uint4 *w1r = nullptr, *whr = nullptr;
+    const uint2 *wdr = nullptr;
     void *w1t = nullptr;          // [D][H] transposed W1
     float *small = nullptr;       // every small weight array, one allocation
     float *b1 = nullptr, *bh = nullptr, *bmu = nullptr, *blv = nullptr, *wmu = nullptr,
@@ -164,6 +167,28 @@ bool plan_geometry(const enova_detect_config &cfg, Geometry *g)
                    rows * 2 * sizeof(float) + 3 * sizeof(float) * static_cast<size_t>(g->S) * g->Mp;
     g->mfma_ok = g->H <= 256 && g->L <= 16 && cpr < (1 << 20) && kc < (1 << 24) &&
                  g->lds_bytes <= kLdsLimit;
+    // bf16 with 193..256 hidden units: the ring kernel when a block fits half a compute unit's LDS
+    // (a ring slot is one super-row of at most 64 chunks, i.e. one chunk per lane of a wave)
+    g->ring = false;
+    g->RP = g->RR = g->ring_floats = 0;
+    g->ring_lds = 0;
+    if (g->mfma_ok && g->dtype == ENOVA_BF16 && g->H > 192 && g->H <= kRingHidden && g->L <= 16) {
+        const int P = (g->CPR + 15) / 16 * 16;   // whole groups of four 4-chunk reduction steps
+        const int R = (kRingNb + 2 + 7) / 8 * 8;
+        const int64_t ring_f = std::max<int64_t>(static_cast<int64_t>(R) * P * 4,
+                                                 static_cast<int64_t>(kRingWaves) * 2 * (kRingNb / 16) * 4 * 64);
+        if (P <= 64) {
+            const size_t lds = ring_lds_bytes(P, g->Q, static_cast<int>(ring_f));
+            if (lds <= kLdsLimit / 2) {
+                g->ring = true;
+                g->RP = P;
+                g->RR = R;
+                g->ring_floats = static_cast<int>(ring_f);
+                g->ring_lds = lds;
+                g->Nb = kRingNb;
+            }
+        }
+    }
     if (!g->mfma_ok) {
         g->Hp = ((g->H + 31) / 32) * 32;
     }
@@ -208,12 +233,98 @@ enova_status ensure(T **buf, size_t *cap, size_t need)
     return ENOVA_OK;
 }
 
+// Fragments of the ring kernel (bf16 detectors with 193..256 hidden units), one allocation:
+//  W1      step i = q * KS + sp (KS = P / 4), hidden block hb (16 rows), lane l: the 8 bf16 of
+//          W1[16 hb + l % 16] at the elements of chunk 4 sp + l / 16 of super-row q (zero past the
+//          window, the hidden width or the super-row's chunks); kPrefetchSteps zero steps follow.
+//  heads   [wave w][m][zb][hi, lo][lane l] 8 bf16: row l % 16 of Wmu (zb = 0) or Wlv (zb = 1), zero
+//          past L, at hidden rows 16 (4w + 2m) + 4 (l / 16) + t (t < 4) and
+//          16 (4w + 2m + 1) + 4 (l / 16) + t - 4 (t >= 4) -- the accumulator rows the lane holds.
+//  decoder [hidden block hb][hi, lo][lane l] 4 bf16: Wd1[16 hb + l % 16][4 (l / 16) + t].
+// Weights of the heads and the decoder are split into bf16 hi + lo (the remainder rounded).
+enova_status pack_ring(enova_detector d, const enova_detect_weights *w)
+{
+    const Geometry &g = d->g;
+    const int H = g.H, L = g.L, D = g.D;
+    const int KS = g.RP / 4, NS = g.Q * KS;
+    constexpr int HBT = kRingHidden / 16;
+    const size_t n_w1 = static_cast<size_t>(NS + kPrefetchSteps) * HBT * 64;   // 16-byte fragments
+    const size_t n_wh = static_cast<size_t>(kRingWaves) * 2 * 2 * 2 * 64;       // 16-byte fragments
+    const size_t n_wd = static_cast<size_t>(HBT) * 2 * 64;                      // 8-byte fragments
+    std::vector<uint16_t> buf((n_w1 + n_wh) * 8 + n_wd * 4, 0);
+    uint16_t *w1r = buf.data(), *whr = w1r + n_w1 * 8, *wdr = whr + n_wh * 8;
+    const uint16_t *w1 = static_cast<const uint16_t *>(w->w1);
+    for (int i = 0; i < NS; ++i) {
+        const int q = i / KS, sp = i - q * KS;
+        for (int hb = 0; hb < HBT; ++hb)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int h = 16 * hb + (lane & 15);
+                const int c = 4 * sp + (lane >> 4);
+                if (h >= H || c >= g.CPR)
+                    continue;
+                uint16_t *dst = w1r + ((static_cast<size_t>(i) * HBT + hb) * 64 + lane) * 8;
+                for (int e = 0; e < 8; ++e) {
+                    const int jj = c * 8 + e;
+                    const int tt = jj / g.Mp, m = jj - (jj / g.Mp) * g.Mp;
+                    const int t = q * g.S + tt;
+                    if (t < g.W && m < g.M)
+                        dst[e] = w1[static_cast<int64_t>(h) * D + static_cast<int64_t>(t) * g.M + m];
+                }
+            }
+    }
+    auto split = [](float v, uint16_t &hi, uint16_t &lo) {
+        hi = float_to_bf16_bits(v);
+        lo = float_to_bf16_bits(v - bf16_bits_to_float(hi));
+    };
+    for (int wv = 0; wv < kRingWaves; ++wv)
+        for (int m = 0; m < 2; ++m)
+            for (int zb = 0; zb < 2; ++zb) {
+                const size_t base = (((static_cast<size_t>(wv) * 2 + m) * 2 + zb) * 2) * 64;
+                for (int lane = 0; lane < 64; ++lane) {
+                    const int row = lane & 15, grp = lane >> 4;
+                    for (int t = 0; t < 8; ++t) {
+                        const int h = t < 4 ? 16 * (4 * wv + 2 * m) + 4 * grp + t
+                                            : 16 * (4 * wv + 2 * m + 1) + 4 * grp + (t - 4);
+                        float v = 0.0f;
+                        if (h < H && row < L)
+                            v = zb == 0 ? w->wmu[row * H + h] : w->wlv[row * H + h];
+                        uint16_t hi, lo;
+                        split(v, hi, lo);
+                        whr[(base + lane) * 8 + t] = hi;
+                        whr[(base + 64 + lane) * 8 + t] = lo;
+                    }
+                }
+            }
+    for (int hb = 0; hb < HBT; ++hb)
+        for (int lane = 0; lane < 64; ++lane)
+            for (int t = 0; t < 4; ++t) {
+                const int h = 16 * hb + (lane & 15);
+                const int l = 4 * (lane >> 4) + t;
+                float v = 0.0f;
+                if (h < H && l < L)
+                    v = w->wd1[h * L + l];
+                uint16_t hi, lo;
+                split(v, hi, lo);
+                wdr[((static_cast<size_t>(hb) * 2 + 0) * 64 + lane) * 4 + t] = hi;
+                wdr[((static_cast<size_t>(hb) * 2 + 1) * 64 + lane) * 4 + t] = lo;
+            }
+    enova_status st = dev_upload(&d->ring_w, buf.data(), buf.size() * sizeof(uint16_t));
+    if (st != ENOVA_OK)
+        return st;
+    const uint4 *base = static_cast<const uint4 *>(d->ring_w);
+    d->w1r = base;
+    d->whr = base + n_w1;
+    d->wdr = reinterpret_cast<const uint2 *>(base + n_w1 + n_wh);
+    const hipError_t e = prepare_score_ring(g);
+    return e == hipSuccess ? ENOVA_OK : hip_fail(e, "configure the ring scoring kernel");
+}
+
 void free_detector(enova_detector d)
 {
     if (!d)
         return;
     void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->tile_map, d->cal, d->hist,
-                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws};
+                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws, d->ring_w};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
@@ -593,6 +704,8 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
             if (e != hipSuccess)
                 st = hip_fail(e, "configure matrix-core kernel");
         }
+        if (st == ENOVA_OK && g.ring)
+            st = pack_ring(d, w);
     }
     if (st == ENOVA_OK) {
         hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 256 * sizeof(unsigned int));
@@ -778,6 +891,9 @@ enova_status score_common(enova_detector det, const void *x, const int64_t *soff
     p.blv = det->blv;
     p.bd1 = det->bd1;
     p.u = det->u;
+    p.w1r = det->w1r;
+    p.whr = det->whr;
+    p.wdr = det->wdr;
     p.sum_bd2 = det->sum_bd2;
     p.threshold = threshold;
     p.write_flags = want_flags ? 1 : 0;
@@ -795,7 +911,7 @@ enova_status score_common(enova_detector det, const void *x, const int64_t *soff
         p.tile_stream = wk.tile_map;
         if (timing)
             (void)hipEventRecord(det->ev[2], stream);
-        e = launch_score_mfma(g, p, grid, stream);
+        e = g.ring ? launch_score_ring(g, p, grid, stream) : launch_score_mfma(g, p, grid, stream);
     } else {
         if (timing)
             (void)hipEventRecord(det->ev[2], stream);

@@ -41,7 +41,19 @@ struct Geometry {
     int Nb;                 // windows per tile
     size_t lds_bytes;       // dynamic LDS of the matrix-core kernel
     bool mfma_ok;
+    // bf16 detectors with 193..256 hidden units take the ring kernel (k_score_ring.hip) instead:
+    // 128-window tiles, a ring of RR super-rows of RP chunks in LDS, two blocks per compute unit
+    bool ring;
+    int RP, RR;
+    int ring_floats;        // floats of the ring region (at least the epilogue's 64 KiB exchange)
+    size_t ring_lds;        // dynamic LDS of the ring kernel
 };
+
+constexpr int kRingNb = 128;        // windows per tile of the ring kernel
+constexpr int kRingWaves = 4;       // waves per block: 64 hidden rows each
+constexpr int kRingHidden = 256;    // hidden units the ring kernel is laid out for (padded)
+// dynamic LDS of the ring kernel for ring slots of P chunks, Q super-rows per window
+size_t ring_lds_bytes(int P, int Q, int ring_floats);
 
 constexpr int kWaves = 4;                 // waves per block of the other kernels
 constexpr int kThreads = 64 * kWaves;
@@ -112,6 +124,11 @@ struct ScoreParams {
     const float *bmu, *blv;      // [L]
     const float *bd1;            // [Hp]
     const float *u;              // [Hp] column sums of Wd2
+    // ring kernel: W1 as 16x16x32 A fragments [steps + kPrefetchSteps][16][64 lanes], the heads as
+    // bf16 hi/lo fragments [wave][2][2][hi, lo][64], the decoder hidden layer [16][hi, lo][64]
+    const uint4 *w1r;
+    const uint4 *whr;
+    const uint2 *wdr;
     float sum_bd2;
     float threshold;
     int write_flags;
@@ -132,6 +149,8 @@ hipError_t launch_stream_scan(const Geometry &g, const int64_t *soff, const int6
 hipError_t launch_tile_map(const int64_t *tile_off, int n, int64_t grid, int *map, hipStream_t st);
 hipError_t launch_score_valu(const Geometry &g, const ScoreParams &p, hipStream_t st);
 hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st);
+hipError_t prepare_score_ring(const Geometry &g);
+hipError_t launch_score_ring(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st);
 hipError_t launch_flag(const float *scores, int64_t n, float thr, uint8_t *flags, hipStream_t st);
 // Radix-select pass over the calibration scores: histogram of the 8-bit digit at `shift`
 // among keys whose bits above shift+8 equal `prefix`.
