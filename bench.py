@@ -52,18 +52,25 @@ def flops_per_window(cfg) -> int:
     return 2 * H * D + 4 * L * H + 2 * L * H + 2 * H
 
 
+def score_kernel_name(cfg) -> str:
+    """The library's scoring kernel for a workload: bf16 detectors with 193..256 hidden units take
+    the ring kernel, every other matrix-core shape the general one."""
+    return "k_score_ring" if cfg.dtype == "bf16" and 192 < cfg.hidden <= 256 else "k_score_mfma"
+
+
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for name in ("k_score_mfma.hip", "mfma_common.h", "internal.h"):
+    for name in ("k_score_mfma.hip", "k_score_ring.hip", "mfma_common.h", "internal.h"):
         with open(os.path.join(ROOT, "paper_2407_09486_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(config_name: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it still
-    describes the current kernel source (else None)."""
-    path = os.path.join(ROOT, "profiles", f"score_mfma_{config_name}_counters.txt")
+def load_traffic(cfg):
+    """HBM bytes per launch of the workload's scoring kernel from the committed rocprofv3 counter
+    summary (profiles/<kernel>_<workload>_counters.txt, read from a file, not measured in this run),
+    if it still describes the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{score_kernel_name(cfg)[2:]}_{cfg.name}_counters.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -175,9 +182,11 @@ def secondary_leg(name, launches=5, warmup=2):
     achieved = fpw * N / (k_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[cfg.dtype]
     return {"workload": f"{cfg.name}: {cfg.description}", "dtype": cfg.dtype, "windows": N,
-            "kernel": "k_score_mfma", "kernel_ms": round(k_ms, 4), "launches": launches,
+            "kernel": score_kernel_name(cfg), "kernel_ms": round(k_ms, 4), "launches": launches,
             "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-            "traffic": load_traffic(cfg.name),
+            "traffic": load_traffic(cfg),
+            "traffic_source": f"profiles/{score_kernel_name(cfg)[2:]}_{cfg.name}_counters.txt (rocprofv3 FETCH_SIZE + "
+                              "WRITE_SIZE, read from the file when its kernel source hash matches; null otherwise)",
             "note": "kernel-only (library HIP events, median of the launches); not part of ms_per_step"}
 
 
@@ -296,10 +305,12 @@ def main():
     fpw = flops_per_window(cfg)
     achieved = fpw * N / (k_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[cfg.dtype]
-    traffic = load_traffic(cfg.name)
+    traffic = load_traffic(cfg)
     roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4), "traffic": traffic,
-            "kernel": "k_score_mfma", "kernel_ms": round(k_ms, 4),
+            "traffic_source": f"profiles/{score_kernel_name(cfg)[2:]}_{cfg.name}_counters.txt (rocprofv3 FETCH_SIZE "
+                              "+ WRITE_SIZE, read from the file when its kernel source hash matches; null otherwise)",
+            "kernel": score_kernel_name(cfg), "kernel_ms": round(k_ms, 4),
             "flops_per_window": fpw, "windows_per_launch": N,
             "stats_kernel_ms": round(float(np.mean(stats_ms)), 4)}
     out = {
