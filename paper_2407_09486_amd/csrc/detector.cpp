@@ -74,6 +74,9 @@ struct enova_detector_s {
     void *ring_w = nullptr;       // ring kernel: W1, heads and decoder fragments (one allocation)
     const uint4 *w1r = nullptr, *whr = nullptr;
     const uint2 *wdr = nullptr;
+    void *stream_w = nullptr;     // streaming kernel: W1, heads and decoder fragments (one allocation)
+    const uint4 *w1s = nullptr;
+    const float *whs = nullptr, *wds = nullptr;
     void *w1t = nullptr;          // [D][H] transposed W1
     float *small = nullptr;       // every small weight array, one allocation
     float *b1 = nullptr, *bh = nullptr, *bmu = nullptr, *blv = nullptr, *wmu = nullptr,
@@ -319,12 +322,86 @@ enova_status pack_ring(enova_detector d, const enova_detect_weights *w)
     return e == hipSuccess ? ENOVA_OK : hip_fail(e, "configure the ring scoring kernel");
 }
 
+// Fragments of the streaming kernel's 16x16 matrix ops: W1 as A fragments
+// [stream_w1_steps][Hp/16][64 lanes] x 16 bytes (lane l: hidden row 16 hb + l%16, chunk
+// 4 step + l/16 in the detector's chunk order, zeros past the window), the heads as
+// [Hp/16][4][2][64] floats (op (hb, r) of head 0 = mean, 1 = log-variance: lane l holds the head
+// row l%16 at hidden unit 16 hb + 4 (l/16) + r) and the decoder's hidden layer as [Hp/16][4][64]
+// floats (op (hb, r): lane l holds Wd1[16 hb + l%16][4 (l/16) + r]).
+enova_status pack_stream(enova_detector d, const enova_detect_weights *w)
+{
+    const Geometry &g = d->g;
+    const int H = g.H, L = g.L, D = g.D, NHB = g.Hp / 16;
+    const bool bf = g.dtype == ENOVA_BF16;
+    const int steps = stream_w1_steps(g);
+    const size_t n_w1 = static_cast<size_t>(steps) * NHB * 64;   // 16-byte fragments
+    const size_t n_wh = static_cast<size_t>(NHB) * 4 * 2 * 64;   // floats
+    const size_t n_wd = static_cast<size_t>(NHB) * 4 * 64;       // floats
+    std::vector<uint32_t> buf(n_w1 * 4 + n_wh + n_wd, 0u);
+    for (int j = 0; j < steps; ++j)
+        for (int hb = 0; hb < NHB; ++hb)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int h = 16 * hb + (lane & 15);
+                const int kappa = 4 * j + (lane >> 4);
+                if (h >= H || kappa >= g.KC)
+                    continue;
+                const int q = kappa / g.CPR;
+                const int c = kappa - q * g.CPR;
+                uint16_t bits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                float vals[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                for (int e = 0; e < g.epc; ++e) {
+                    const int jj = c * g.epc + e;
+                    const int tt = jj / g.Mp;
+                    const int m = jj - tt * g.Mp;
+                    const int t = q * g.S + tt;
+                    if (q < g.Q && t < g.W && m < g.M) {
+                        const int64_t at = static_cast<int64_t>(h) * D + static_cast<int64_t>(t) * g.M + m;
+                        if (bf)
+                            bits[e] = static_cast<const uint16_t *>(w->w1)[at];
+                        else
+                            vals[e] = static_cast<const float *>(w->w1)[at];
+                    }
+                }
+                uint32_t *dst = &buf[((static_cast<size_t>(j) * NHB + hb) * 64 + lane) * 4];
+                if (bf) {
+                    for (int e = 0; e < 4; ++e)
+                        dst[e] = static_cast<uint32_t>(bits[2 * e]) | (static_cast<uint32_t>(bits[2 * e + 1]) << 16);
+                } else {
+                    std::memcpy(dst, vals, 16);
+                }
+            }
+    float *wh = reinterpret_cast<float *>(buf.data() + n_w1 * 4);
+    float *wd = wh + n_wh;
+    for (int hb = 0; hb < NHB; ++hb)
+        for (int r = 0; r < 4; ++r)
+            for (int lane = 0; lane < 64; ++lane) {
+                const int row = lane & 15;
+                const int hh = 16 * hb + 4 * (lane >> 4) + r;
+                if (hh < H && row < L) {
+                    wh[((hb * 4 + r) * 2 + 0) * 64 + lane] = w->wmu[row * H + hh];
+                    wh[((hb * 4 + r) * 2 + 1) * 64 + lane] = w->wlv[row * H + hh];
+                }
+                const int hd = 16 * hb + row;
+                const int l = 4 * (lane >> 4) + r;
+                if (hd < H && l < L)
+                    wd[(hb * 4 + r) * 64 + lane] = w->wd1[hd * L + l];
+            }
+    enova_status st = dev_upload(&d->stream_w, buf.data(), buf.size() * sizeof(uint32_t));
+    if (st != ENOVA_OK)
+        return st;
+    d->w1s = static_cast<const uint4 *>(d->stream_w);
+    d->whs = reinterpret_cast<const float *>(d->w1s + n_w1);
+    d->wds = d->whs + n_wh;
+    const hipError_t e = prepare_stream_score(g);
+    return e == hipSuccess ? ENOVA_OK : hip_fail(e, "configure the streaming scoring kernel");
+}
+
 void free_detector(enova_detector d)
 {
     if (!d)
         return;
     void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->tile_map, d->cal, d->hist,
-                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws, d->ring_w};
+                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws, d->ring_w, d->stream_w};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
@@ -706,6 +783,8 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
         }
         if (st == ENOVA_OK && g.ring)
             st = pack_ring(d, w);
+        if (st == ENOVA_OK && stream_score_supported(g))
+            st = pack_stream(d, w);
     }
     if (st == ENOVA_OK) {
         hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 256 * sizeof(unsigned int));
@@ -1363,12 +1442,10 @@ enova_status enova_stream_create(enova_detector det, int32_t n, const float *ref
     if (n_cal > 0 && !calib_scores)
         return fail(ENOVA_EINVAL, "calib_scores is NULL");
     const Geometry &g = det->g;
-    if (det->kind != 2 || !stream_score_supported(g))
+    if (det->kind != 2 || !det->w1s)
         return fail(ENOVA_EUNSUPPORTED, "streaming needs the matrix-core kernel's shapes");
     DeviceGuard dg(det->device);
-    hipError_t e = prepare_stream_score(g);
-    if (e != hipSuccess)
-        return hip_fail(e, "streaming kernel attributes");
+    hipError_t e = hipSuccess;
 
     enova_stream s = new (std::nothrow) enova_stream_s;
     if (!s)
@@ -1448,9 +1525,9 @@ enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_sc
     p.first_slot = static_cast<int>(s->steps % g.W);
     p.mean = s->mean;
     p.std = s->std;
-    p.w1p = static_cast<const uint4 *>(det->w1p);
-    p.whp = det->whp;
-    p.wd1p = det->wd1p;
+    p.w1p = det->w1s;
+    p.whp = det->whs;
+    p.wd1p = det->wds;
     p.b1 = det->b1;
     p.bd1 = det->bd1;
     p.u = det->u;

@@ -24,12 +24,11 @@ namespace enova {
 
 namespace {
 
-constexpr int kStreamWaves = 4;
 constexpr int kStreamThreads = 64 * kStreamWaves;
-constexpr size_t kStreamSliceBytes = 48 * 1024;   // LDS for one staged slice of a tile
 
 struct StreamShape {
-    int M, S, W, Mp, Q, CPR, KC, KS, KCP, HBT;
+    int M, S, W, Mp, Q, CPR;
+    int iters;        // reduction iterations of each wave (a multiple of the window prefetch depth)
     float inv_d;
 };
 
@@ -49,320 +48,346 @@ __global__ __launch_bounds__(256) void k_stream_append(const T *__restrict__ x, 
 }
 
 // ---- scoring of the newest windows ----------------------------------------------------------
-// HBW hidden blocks per wave, WH waves along the hidden rows, 4/WH window groups of 32 windows.
-template <int DT, int HBW, int WH, int ACT>
+// A block scores kStreamNb = 16 windows (one per stream). No two of them share data, so nothing
+// is staged: each wave streams its own share of the reduction straight from HBM into
+// registers. Reduction step j covers chunks 4j .. 4j+3 of every window (chunk kappa = q*CPR + c:
+// chunk c of super-row q, the packed W1's order); wave w takes the steps j = w mod 4, lane l
+// loads chunk 4j + l/16 of window l%16 (the B operand of the 16x16 matrix ops) and the W1
+// fragments of the same step arrive from L2 (the A operand). The four waves' partial hidden
+// sums meet in LDS and are added in a fixed order; the epilogue then chains heads and decoder on
+// 16x16x4 fp32 matrix ops from the accumulator layout (lane l, register r: row 4*(l/16) + r,
+// column l%16), which is the B-operand layout of the next op with its reduction index permuted
+// to match (the packed head and decoder weights carry that permutation).
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <int DT>
+__device__ __forceinline__ v4f mfma_step(uint4 a, uint4 b, v4f c)
+{
+    if constexpr (DT == ENOVA_F32) {
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    } else {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b),
+                                                       c, 0, 0, 0);
+    }
+}
+
+// The normalised chunk: (x - mean) / std of its elements (rounded to bf16 for the bf16
+// detector), zeros where ok is false; sum gains the values as they enter the matrix ops.
+template <int DT, int EPC>
+__device__ __forceinline__ uint4 normalise_chunk(uint4 raw, const float (&mu)[EPC], const float (&is)[EPC],
+                                                 bool ok, float &sum)
+{
+    float xv[EPC];
+    if constexpr (DT == ENOVA_F32) {
+        xv[0] = __uint_as_float(raw.x);
+        xv[1] = __uint_as_float(raw.y);
+        xv[2] = __uint_as_float(raw.z);
+        xv[3] = __uint_as_float(raw.w);
+    } else {
+        xv[0] = bf16_lo(raw.x);
+        xv[1] = bf16_hi(raw.x);
+        xv[2] = bf16_lo(raw.y);
+        xv[3] = bf16_hi(raw.y);
+        xv[4] = bf16_lo(raw.z);
+        xv[5] = bf16_hi(raw.z);
+        xv[6] = bf16_lo(raw.w);
+        xv[7] = bf16_hi(raw.w);
+    }
+    float v[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e)
+        v[e] = ok ? (xv[e] - mu[e]) * is[e] : 0.0f;
+    uint4 out;
+    if constexpr (DT == ENOVA_F32) {
+        out.x = __float_as_uint(v[0]);
+        out.y = __float_as_uint(v[1]);
+        out.z = __float_as_uint(v[2]);
+        out.w = __float_as_uint(v[3]);
+        sum += (v[0] + v[1]) + (v[2] + v[3]);
+    } else {
+        out.x = pack_bf16x2(v[0], v[1]);
+        out.y = pack_bf16x2(v[2], v[3]);
+        out.z = pack_bf16x2(v[4], v[5]);
+        out.w = pack_bf16x2(v[6], v[7]);
+        sum += ((bf16_lo(out.x) + bf16_hi(out.x)) + (bf16_lo(out.y) + bf16_hi(out.y))) +
+               ((bf16_lo(out.z) + bf16_hi(out.z)) + (bf16_lo(out.w) + bf16_hi(out.w)));
+    }
+    return out;
+}
+
+// Chunk kappa of window s gathered element by element (any metric count and padding).
+template <int DT>
+__device__ __forceinline__ uint4 gather_chunk(const StreamScoreParams &p, const StreamShape &g, int s, bool live,
+                                              int kappa, float &sum)
+{
+    constexpr int EPC = DT == ENOVA_F32 ? 4 : 8;
+    const int q = kappa / g.CPR;
+    const int c = kappa - q * g.CPR;
+    float v[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+        const int jj = c * EPC + e;
+        const int tt = jj / g.Mp;
+        const int m = jj - tt * g.Mp;
+        const int step = q * g.S + tt;
+        float val = 0.0f;
+        if (live && q < g.Q && m < g.M && step < g.W) {
+            const int64_t at = (static_cast<int64_t>(s) * 2 * g.W + p.first_slot + step) * g.M + m;
+            const int64_t sm = static_cast<int64_t>(s) * g.M + m;
+            val = (load_x<DT>(p.ring, at) - p.mean[sm]) * (1.0f / p.std[sm]);
+        }
+        v[e] = val;
+    }
+    uint4 out;
+    if constexpr (DT == ENOVA_F32) {
+        out.x = __float_as_uint(v[0]);
+        out.y = __float_as_uint(v[1]);
+        out.z = __float_as_uint(v[2]);
+        out.w = __float_as_uint(v[3]);
+        sum += (v[0] + v[1]) + (v[2] + v[3]);
+    } else {
+        out.x = pack_bf16x2(v[0], v[1]);
+        out.y = pack_bf16x2(v[2], v[3]);
+        out.z = pack_bf16x2(v[4], v[5]);
+        out.w = pack_bf16x2(v[6], v[7]);
+        sum += ((bf16_lo(out.x) + bf16_hi(out.x)) + (bf16_lo(out.y) + bf16_hi(out.y))) +
+               ((bf16_lo(out.z) + bf16_hi(out.z)) + (bf16_lo(out.w) + bf16_hi(out.w)));
+    }
+    return out;
+}
+
+// NHB 16-row hidden blocks (Hp = 16 NHB). VEC: the window is a contiguous run of the ring whose
+// chunks hold whole groups of metrics, and each lane normalises the same EPC metrics at every
+// step (M divides 4 EPC), so the chunks are loaded raw PB steps ahead and normalised with
+// per-lane constants; otherwise every chunk is gathered element by element.
+template <int DT, int NHB, int ACT, bool VEC>
 __global__ __launch_bounds__(kStreamThreads) void k_stream_score(StreamScoreParams p, StreamShape g)
 {
-    constexpr int NW = kStreamWaves, NT = kStreamThreads;
-    constexpr int WN = NW / WH;
-    constexpr int NBS = 32 * WN;                   // windows (streams) per tile
     constexpr int EPC = DT == ENOVA_F32 ? 4 : 8;
-    extern __shared__ uint4 lds[];
+    constexpr int PA = stream_pa(NHB), PB = stream_pb(DT), U = PA > PB ? PA : PB;
+    constexpr int OWN = (NHB + kStreamWaves - 1) / kStreamWaves;   // hidden blocks of a wave's epilogue
+    extern __shared__ float lds[];
+    float *xp = lds;                                   // [wave][hb][r][lane] encoder partial sums
+    float *xz = xp + kStreamWaves * NHB * 4 * 64;      // [wave][head][r][lane] head partial sums
+    float *xs = xz + kStreamWaves * 2 * 4 * 64;        // [wave][window] partial window sums
+    float *xd = xs + kStreamWaves * kStreamNb;         // [wave][window] partial u . hd
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int half = lane >> 5;
-    const int wh = wave % WH;
-    const int wn = wave / WH;
-    const int s0 = blockIdx.x * NBS;
-    const int M = g.M, Mp = g.Mp, S = g.S, W = g.W, Q = g.Q, CPR = g.CPR, KS = g.KS, KCP = g.KCP;
-    const int HBT = g.HBT, HP = 32 * HBT;
+    const int n = lane & 15;
+    const int grp = lane >> 4;
+    const int s = blockIdx.x * kStreamNb + n;
+    const bool live = s < p.n_streams;
+    const int sc = live ? s : 0;                       // addresses of dead lanes stay in stream 0
+    const int WM = g.W * g.M;
 
-    // LDS: the staged slice (later the epilogue's exchange area), window sums, small vectors
-    const size_t buf_chunks = static_cast<size_t>(NBS) * KCP;
-    constexpr int XCHG = WH > 1 ? epi_xchg_floats(NW, 1) : 0;
-    const size_t span = buf_chunks > XCHG / 4 ? buf_chunks : XCHG / 4;
-    uint4 *buf = lds;
-    float *wsum = reinterpret_cast<float *>(lds + span);
-    float *s_b1 = wsum + NBS;
-    float *s_bd1 = s_b1 + HP;
-    float *s_u = s_bd1 + HP;
-    float *s_bh = s_u + HP;
-    for (int i = tid; i < HP; i += NT) {
-        s_b1[i] = p.b1[i];
-        s_bd1[i] = p.bd1[i];
-        s_u[i] = p.u[i];
-    }
-    if (tid < 32)
-        s_bh[tid] = p.bh[tid];
+    v4f acc[NHB];
+#pragma unroll
+    for (int hb = 0; hb < NHB; ++hb)
+        acc[hb] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    float wsum = 0.0f;
 
-    const int nl = wn * 32 + (lane & 31);          // this lane's window in the tile
-    const int brow = nl * KCP;
-    v16f acc[HBW][1];
+    // iteration i of this wave is reduction step 4i + wave: lane chunk 16 i + 4 wave + grp
+    const int kap0 = 4 * wave + grp;
+    const uint4 *ap = p.w1p + static_cast<size_t>(wave) * NHB * 64 + lane;
+    constexpr size_t kIterA = static_cast<size_t>(4) * NHB * 64;   // fragments per iteration
+    uint4 a[PA][NHB];
 #pragma unroll
-    for (int hb = 0; hb < HBW; ++hb)
+    for (int k = 0; k < PA; ++k)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            acc[hb][0][r] = 0.0f;
-    v16f acc2[HBW];                                // fp32: the odd reduction slots
-#pragma unroll
-    for (int hb = 0; hb < HBW; ++hb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            acc2[hb][r] = 0.0f;
-    float my_sum = 0.0f;                           // thread nl < NBS: window nl's sum of v
+        for (int hb = 0; hb < NHB; ++hb)
+            a[k][hb] = ap[k * kIterA + hb * 64];
 
-    // padding-free windows (M a multiple of the chunk's elements) stage with vector loads
-    const bool linear = Mp == M && M % EPC == 0;
-    const uint4 *ap = p.w1p + (wh * HBW) * 64 + lane;
-    for (int k0 = 0; k0 < g.KC; k0 += KS) {
-        const int ks = g.KC - k0 < KS ? g.KC - k0 : KS;   // a multiple of 16
-        __syncthreads();                                   // the previous slice is consumed
-        if (linear) {
-            // chunk kappa is elements [kappa*EPC, +EPC) of the window, contiguous in the ring,
-            // with consecutive metrics: one 16-byte load of x and EPC/4 of mean and std each;
-            // SU chunks per thread in flight
-            constexpr int SU = 4;
-            for (int base = tid; base < NBS * ks; base += NT * SU) {
-                uint4 raw[SU];
-                float4 mu[SU][EPC / 4], sd[SU][EPC / 4];
-                bool ok[SU];
+    if constexpr (VEC) {
+        float mu[EPC], is[EPC];
+        {
+            const float *mp = p.mean + static_cast<int64_t>(sc) * g.M + (grp * EPC) % g.M;
+            const float *sp = p.std + static_cast<int64_t>(sc) * g.M + (grp * EPC) % g.M;
 #pragma unroll
-                for (int u = 0; u < SU; ++u) {
-                    const int idx = base + u * NT;
-                    const int w = idx / ks;
-                    const int kc = idx - w * ks;
-                    const int s = s0 + w;
-                    const int e0 = (k0 + kc) * EPC;
-                    ok[u] = idx < NBS * ks && s < p.n_streams && e0 < W * M;
-                    if (ok[u]) {
-                        const int64_t at = (static_cast<int64_t>(s) * 2 * W + p.first_slot) * M + e0;
-                        if constexpr (DT == ENOVA_F32)
-                            raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const float *>(p.ring) + at);
-                        else
-                            raw[u] = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.ring) + at);
-                        const int64_t sm = static_cast<int64_t>(s) * M + e0 % M;
-#pragma unroll
-                        for (int h = 0; h < EPC / 4; ++h) {
-                            mu[u][h] = reinterpret_cast<const float4 *>(p.mean + sm)[h];
-                            sd[u][h] = reinterpret_cast<const float4 *>(p.std + sm)[h];
-                        }
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < SU; ++u) {
-                    const int idx = base + u * NT;
-                    if (idx >= NBS * ks)
-                        continue;
-                    const int w = idx / ks;
-                    const int kc = idx - w * ks;
-                    float v[EPC];
-                    if (ok[u]) {
-                        float xv[EPC], mv[EPC], sv[EPC];
-                        if constexpr (DT == ENOVA_F32) {
-                            xv[0] = __uint_as_float(raw[u].x);
-                            xv[1] = __uint_as_float(raw[u].y);
-                            xv[2] = __uint_as_float(raw[u].z);
-                            xv[3] = __uint_as_float(raw[u].w);
-                        } else {
-                            xv[0] = bf16_lo(raw[u].x);
-                            xv[1] = bf16_hi(raw[u].x);
-                            xv[2] = bf16_lo(raw[u].y);
-                            xv[3] = bf16_hi(raw[u].y);
-                            xv[4] = bf16_lo(raw[u].z);
-                            xv[5] = bf16_hi(raw[u].z);
-                            xv[6] = bf16_lo(raw[u].w);
-                            xv[7] = bf16_hi(raw[u].w);
-                        }
-#pragma unroll
-                        for (int h = 0; h < EPC / 4; ++h) {
-                            mv[4 * h + 0] = mu[u][h].x;
-                            mv[4 * h + 1] = mu[u][h].y;
-                            mv[4 * h + 2] = mu[u][h].z;
-                            mv[4 * h + 3] = mu[u][h].w;
-                            sv[4 * h + 0] = sd[u][h].x;
-                            sv[4 * h + 1] = sd[u][h].y;
-                            sv[4 * h + 2] = sd[u][h].z;
-                            sv[4 * h + 3] = sd[u][h].w;
-                        }
-#pragma unroll
-                        for (int e = 0; e < EPC; ++e)
-                            v[e] = (xv[e] - mv[e]) * (1.0f / sv[e]);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < EPC; ++e)
-                            v[e] = 0.0f;
-                    }
-                    uint4 out;
-                    if constexpr (DT == ENOVA_F32) {
-                        out.x = __float_as_uint(v[0]);
-                        out.y = __float_as_uint(v[1]);
-                        out.z = __float_as_uint(v[2]);
-                        out.w = __float_as_uint(v[3]);
-                    } else {
-                        out.x = pack_bf16x2(v[0], v[1]);
-                        out.y = pack_bf16x2(v[2], v[3]);
-                        out.z = pack_bf16x2(v[4], v[5]);
-                        out.w = pack_bf16x2(v[6], v[7]);
-                    }
-                    buf[w * KCP + kc] = out;
-                }
-            }
-        } else {
-            for (int idx = tid; idx < NBS * ks; idx += NT) {
-                const int w = idx / ks;
-                const int kc = idx - w * ks;
-                const int kappa = k0 + kc;
-                const int q = kappa / CPR;
-                const int c = kappa - q * CPR;
-                const int s = s0 + w;
-                float v[EPC];
-    #pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    const int jj = c * EPC + e;
-                    const int tt = jj / Mp;
-                    const int m = jj - tt * Mp;
-                    const int step = q * S + tt;
-                    float val = 0.0f;
-                    if (s < p.n_streams && q < Q && m < M && step < W) {
-                        const int64_t at = (static_cast<int64_t>(s) * 2 * W + p.first_slot + step) * M + m;
-                        const float x = load_x<DT>(p.ring, at);
-                        const int64_t sm = static_cast<int64_t>(s) * M + m;
-                        val = (x - p.mean[sm]) * (1.0f / p.std[sm]);
-                    }
-                    v[e] = val;
-                }
-                uint4 out;
-                if constexpr (DT == ENOVA_F32) {
-                    out.x = __float_as_uint(v[0]);
-                    out.y = __float_as_uint(v[1]);
-                    out.z = __float_as_uint(v[2]);
-                    out.w = __float_as_uint(v[3]);
-                } else {
-                    out.x = pack_bf16x2(v[0], v[1]);
-                    out.y = pack_bf16x2(v[2], v[3]);
-                    out.z = pack_bf16x2(v[4], v[5]);
-                    out.w = pack_bf16x2(v[6], v[7]);
-                }
-                buf[w * KCP + kc] = out;
+            for (int h = 0; h < EPC / 4; ++h) {
+                const float4 m4 = reinterpret_cast<const float4 *>(mp)[h];
+                const float4 s4 = reinterpret_cast<const float4 *>(sp)[h];
+                mu[4 * h + 0] = m4.x;
+                mu[4 * h + 1] = m4.y;
+                mu[4 * h + 2] = m4.z;
+                mu[4 * h + 3] = m4.w;
+                is[4 * h + 0] = 1.0f / s4.x;
+                is[4 * h + 1] = 1.0f / s4.y;
+                is[4 * h + 2] = 1.0f / s4.z;
+                is[4 * h + 3] = 1.0f / s4.w;
             }
         }
-        __syncthreads();
-        if (tid < NBS) {
-            // the window's sum of the staged (rounded) values, in a fixed order
-            for (int kc = 0; kc < ks; ++kc) {
-                const uint4 q4 = buf[tid * KCP + kc];
-                if constexpr (DT == ENOVA_F32) {
-                    my_sum += __uint_as_float(q4.x) + __uint_as_float(q4.y) + __uint_as_float(q4.z) +
-                              __uint_as_float(q4.w);
-                } else {
-                    my_sum += bf16_lo(q4.x) + bf16_hi(q4.x) + bf16_lo(q4.y) + bf16_hi(q4.y) +
-                              bf16_lo(q4.z) + bf16_hi(q4.z) + bf16_lo(q4.w) + bf16_hi(q4.w);
-                }
+        const int64_t wbase = (static_cast<int64_t>(sc) * 2 * g.W + p.first_slot) * g.M;
+        auto load_raw = [&](int it) __attribute__((always_inline)) -> uint4 {
+            const int e0 = (16 * it + kap0) * EPC;
+            const int64_t at = live && e0 < WM ? wbase + e0 : 0;
+            if constexpr (DT == ENOVA_F32)
+                return *reinterpret_cast<const uint4 *>(static_cast<const float *>(p.ring) + at);
+            else
+                return *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(p.ring) + at);
+        };
+        uint4 b[PB];
+#pragma unroll
+        for (int k = 0; k < PB; ++k)
+            b[k] = load_raw(k);
+        for (int i = 0; i < g.iters; i += U) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int it = i + u;
+                const bool ok = live && (16 * it + kap0) * EPC < WM;
+                const uint4 bv = normalise_chunk<DT, EPC>(b[u % PB], mu, is, ok, wsum);
+                b[u % PB] = load_raw(it + PB);
+#pragma unroll
+                for (int hb = 0; hb < NHB; ++hb)
+                    acc[hb] = mfma_step<DT>(a[u % PA][hb], bv, acc[hb]);
+                // iterations up to iters + PA - 1 are read: the packed W1 carries them as zeros
+#pragma unroll
+                for (int hb = 0; hb < NHB; ++hb)
+                    a[u % PA][hb] = ap[(it + PA) * kIterA + hb * 64];
             }
         }
-        // contraction over the slice: step i covers chunks 2i (lanes 0..31) and 2i+1 (32..63).
-        // W1 fragments run PD steps ahead in a register ring (a step is only a few matrix ops);
-        // fp32 alternates two accumulators so consecutive ops do not wait on each other.
-        constexpr int PD = 8;
-        static_assert(PD <= kPrefetchSteps, "the packed W1 carries kPrefetchSteps zero steps");
-        const int nsteps = ks / 2;                 // a multiple of PD
-        const int64_t st0 = k0 / 2;
-        uint4 a[PD][HBW];
+    } else {
+        for (int i = 0; i < g.iters; i += PA) {
 #pragma unroll
-        for (int j = 0; j < PD; ++j)
+            for (int u = 0; u < PA; ++u) {
+                const int it = i + u;
+                const uint4 bv = gather_chunk<DT>(p, g, sc, live, 16 * it + kap0, wsum);
 #pragma unroll
-            for (int hb = 0; hb < HBW; ++hb)
-                a[j][hb] = ap[((st0 + j) * HBT + hb) * 64];
-        for (int i = 0; i < nsteps; i += PD) {
+                for (int hb = 0; hb < NHB; ++hb)
+                    acc[hb] = mfma_step<DT>(a[u][hb], bv, acc[hb]);
 #pragma unroll
-            for (int j = 0; j < PD; ++j) {
-                const uint4 bq = buf[brow + 2 * (i + j) + half];
-                if constexpr (DT == ENOVA_F32) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float bv = __uint_as_float(e == 0 ? bq.x : e == 1 ? bq.y : e == 2 ? bq.z : bq.w);
-#pragma unroll
-                        for (int hb = 0; hb < HBW; ++hb) {
-                            const float av = __uint_as_float(e == 0 ? a[j][hb].x : e == 1 ? a[j][hb].y
-                                                            : e == 2 ? a[j][hb].z : a[j][hb].w);
-                            if (e & 1)
-                                acc2[hb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc2[hb], 0, 0, 0);
-                            else
-                                acc[hb][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[hb][0], 0, 0, 0);
-                        }
-                    }
-                } else {
-#pragma unroll
-                    for (int hb = 0; hb < HBW; ++hb)
-                        acc[hb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(v8bf, a[j][hb]), __builtin_bit_cast(v8bf, bq), acc[hb][0], 0, 0, 0);
-                }
-                // steps up to KC/2 + PD - 1 are read: the packed W1 carries zero steps past the end
-#pragma unroll
-                for (int hb = 0; hb < HBW; ++hb)
-                    a[j][hb] = ap[((st0 + i + j + PD) * HBT + hb) * 64];
+                for (int hb = 0; hb < NHB; ++hb)
+                    a[u][hb] = ap[(it + PA) * kIterA + hb * 64];
             }
         }
     }
-    if constexpr (DT == ENOVA_F32) {
+
+    // ---- the four waves' partial sums, added in a fixed order ----
 #pragma unroll
-        for (int hb = 0; hb < HBW; ++hb)
-            acc[hb][0] += acc2[hb];
-    }
-    __syncthreads();                               // the staging buffer becomes the exchange area
-    if (tid < NBS)
-        wsum[tid] = my_sum;
+    for (int hb = 0; hb < NHB; ++hb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            xp[((wave * NHB + hb) * 4 + r) * 64 + lane] = acc[hb][r];
+    wsum += __shfl_xor(wsum, 16);
+    wsum += __shfl_xor(wsum, 32);
+    if (grp == 0)
+        xs[wave * kStreamNb + n] = wsum;
     __syncthreads();
 
-    const EpiArgs ea{p.whp, p.wd1p, s_b1, s_bd1, s_u, s_bh, reinterpret_cast<float *>(buf),
-                     lane, half, wave, wh, wn};
-    score_epilogue<DT, HBW, 1, WH, NW, ACT>(acc, ea, [&](int, float sc, float dot) __attribute__((always_inline)) {
-        const int s = s0 + nl;
-        if (wh == 0 && half == 0 && s < p.n_streams) {
-            p.scores[s] = sc;
-            if (p.md)
-                p.md[s] = wsum[nl] * g.inv_d - (dot + p.sum_bd2) * g.inv_d;
+    // hidden activations of the blocks hb = wave + 4 t feed this wave's share of the heads
+    v4f zm = v4f{0.0f, 0.0f, 0.0f, 0.0f}, zl = zm;
+#pragma unroll
+    for (int t = 0; t < OWN; ++t) {
+        const int hb = wave + kStreamWaves * t;
+        if (hb < NHB) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float h = 0.0f;
+#pragma unroll
+                for (int w2 = 0; w2 < kStreamWaves; ++w2)
+                    h += xp[((w2 * NHB + hb) * 4 + r) * 64 + lane];
+                const float hv = act_fn<ACT>(h + p.b1[16 * hb + 4 * grp + r]);
+                zm = __builtin_amdgcn_mfma_f32_16x16x4f32(p.whp[((hb * 4 + r) * 2 + 0) * 64 + lane], hv, zm, 0, 0, 0);
+                zl = __builtin_amdgcn_mfma_f32_16x16x4f32(p.whp[((hb * 4 + r) * 2 + 1) * 64 + lane], hv, zl, 0, 0, 0);
+            }
         }
-    });
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        xz[((wave * 2 + 0) * 4 + r) * 64 + lane] = zm[r];
+        xz[((wave * 2 + 1) * 4 + r) * 64 + lane] = zl[r];
+    }
+    __syncthreads();
+    // mean and log-variance of latent 4 grp + r, window n (every wave the same sums)
+    float mu[4], kl = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float m = 0.0f, lv = 0.0f;
+#pragma unroll
+        for (int w2 = 0; w2 < kStreamWaves; ++w2) {
+            m += xz[((w2 * 2 + 0) * 4 + r) * 64 + lane];
+            lv += xz[((w2 * 2 + 1) * 4 + r) * 64 + lane];
+        }
+        mu[r] = m + p.bh[4 * grp + r];
+        lv += p.bh[16 + 4 * grp + r];
+        kl += mu[r] * mu[r] + kl_g(lv);
+    }
+    kl += __shfl_xor(kl, 16);
+    kl += __shfl_xor(kl, 32);
+
+    // decoder hidden layer at z = mu for the same hidden blocks, dotted with u
+    float dot = 0.0f;
+#pragma unroll
+    for (int t = 0; t < OWN; ++t) {
+        const int hb = wave + kStreamWaves * t;
+        if (hb < NHB) {
+            v4f d = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                d = __builtin_amdgcn_mfma_f32_16x16x4f32(p.wd1p[(hb * 4 + r) * 64 + lane], mu[r], d, 0, 0, 0);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int h = 16 * hb + 4 * grp + r;
+                dot += p.u[h] * act_fn<ACT>(d[r] + p.bd1[h]);
+            }
+        }
+    }
+    dot += __shfl_xor(dot, 16);
+    dot += __shfl_xor(dot, 32);
+    if (grp == 0)
+        xd[wave * kStreamNb + n] = dot;
+    __syncthreads();
+    if (wave == 0 && grp == 0 && live) {
+        float ws = 0.0f, dt = 0.0f;
+#pragma unroll
+        for (int w2 = 0; w2 < kStreamWaves; ++w2) {
+            ws += xs[w2 * kStreamNb + n];
+            dt += xd[w2 * kStreamNb + n];
+        }
+        p.scores[s] = 0.5f * kl;
+        if (p.md)
+            p.md[s] = ws * g.inv_d - (dt + p.sum_bd2) * g.inv_d;
+    }
 }
 
 using StreamKernel = void (*)(StreamScoreParams, StreamShape);
 
-template <int DT, int ACT>
-StreamKernel pick_stream(int hb)
+template <int DT, int ACT, bool VEC>
+StreamKernel pick_stream(int nhb)
 {
-    switch (hb) {
-    case 1: return k_stream_score<DT, 1, 1, ACT>;
-    case 2: return k_stream_score<DT, 1, 2, ACT>;
-    case 4: return k_stream_score<DT, 1, 4, ACT>;
-    case 8: return k_stream_score<DT, 2, 4, ACT>;
+    switch (nhb) {
+    case 2: return k_stream_score<DT, 2, ACT, VEC>;
+    case 4: return k_stream_score<DT, 4, ACT, VEC>;
+    case 8: return k_stream_score<DT, 8, ACT, VEC>;
+    case 16: return k_stream_score<DT, 16, ACT, VEC>;
     default: return nullptr;
     }
+}
+
+template <int DT, int ACT>
+StreamKernel pick_stream(int nhb, bool vec)
+{
+    return vec ? pick_stream<DT, ACT, true>(nhb) : pick_stream<DT, ACT, false>(nhb);
 }
 
 StreamKernel pick_stream(const Geometry &g)
 {
     const bool relu = g.act == ENOVA_RELU;
+    const int nhb = g.Hp / 16;
+    const bool vec = stream_vec(g);
     if (g.dtype == ENOVA_F32)
-        return relu ? pick_stream<ENOVA_F32, ENOVA_RELU>(g.HB) : pick_stream<ENOVA_F32, ENOVA_TANH>(g.HB);
-    return relu ? pick_stream<ENOVA_BF16, ENOVA_RELU>(g.HB) : pick_stream<ENOVA_BF16, ENOVA_TANH>(g.HB);
+        return relu ? pick_stream<ENOVA_F32, ENOVA_RELU>(nhb, vec) : pick_stream<ENOVA_F32, ENOVA_TANH>(nhb, vec);
+    return relu ? pick_stream<ENOVA_BF16, ENOVA_RELU>(nhb, vec) : pick_stream<ENOVA_BF16, ENOVA_TANH>(nhb, vec);
 }
 
-// Tile shape of the streaming kernel for g: windows per tile, chunks per slice and LDS bytes.
-struct StreamPlan {
-    int nbs, ks, kcp;
-    size_t lds;
-};
-
-StreamPlan stream_plan(const Geometry &g)
+size_t stream_lds(const Geometry &g)
 {
-    StreamPlan sp{};
-    const int wh = g.HB < 4 ? g.HB : 4;
-    sp.nbs = 32 * (kStreamWaves / wh);
-    int ks = static_cast<int>(kStreamSliceBytes / (static_cast<size_t>(sp.nbs) * 16)) - 1;
-    ks = ks / 16 * 16;
-    if (ks < 16)
-        ks = 16;
-    if (ks > g.KC)
-        ks = g.KC;
-    sp.ks = ks;
-    sp.kcp = ks + 1;                               // odd pitch: the 32 windows of a fragment read spread over the banks
-    const size_t buf = static_cast<size_t>(sp.nbs) * sp.kcp * 16;
-    const size_t xchg = wh > 1 ? static_cast<size_t>(epi_xchg_floats(kStreamWaves, 1)) * sizeof(float) : 0;
-    sp.lds = (buf > xchg ? buf : xchg) + (static_cast<size_t>(sp.nbs) + 3 * static_cast<size_t>(g.Hp) + 32) * sizeof(float);
-    return sp;
+    const size_t nhb = static_cast<size_t>(g.Hp / 16);
+    return (kStreamWaves * nhb * 4 * 64 + kStreamWaves * 2 * 4 * 64 + 2 * kStreamWaves * kStreamNb) * sizeof(float);
 }
 
 // ---- SPOT -------------------------------------------------------------------------------------
@@ -895,7 +920,7 @@ hipError_t launch_stream_append(const Geometry &g, const void *x_step, int n, in
 
 bool stream_score_supported(const Geometry &g)
 {
-    return g.mfma_ok && pick_stream(g) != nullptr && stream_plan(g).lds <= kLdsLimit;
+    return g.mfma_ok && pick_stream(g) != nullptr && stream_lds(g) <= kLdsLimit;
 }
 
 hipError_t prepare_stream_score(const Geometry &g)
@@ -904,7 +929,7 @@ hipError_t prepare_stream_score(const Geometry &g)
     if (!k)
         return hipErrorInvalidValue;
     return hipFuncSetAttribute(reinterpret_cast<const void *>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
-                               static_cast<int>(kLdsLimit));
+                               static_cast<int>(stream_lds(g)));
 }
 
 hipError_t launch_stream_score(const Geometry &g, const StreamScoreParams &p, hipStream_t st)
@@ -914,7 +939,6 @@ hipError_t launch_stream_score(const Geometry &g, const StreamScoreParams &p, hi
     StreamKernel k = pick_stream(g);
     if (!k)
         return hipErrorInvalidValue;
-    const StreamPlan sp = stream_plan(g);
     StreamShape sh;
     sh.M = g.M;
     sh.S = g.S;
@@ -922,13 +946,10 @@ hipError_t launch_stream_score(const Geometry &g, const StreamScoreParams &p, hi
     sh.Mp = g.Mp;
     sh.Q = g.Q;
     sh.CPR = g.CPR;
-    sh.KC = g.KC;
-    sh.KS = sp.ks;
-    sh.KCP = sp.kcp;
-    sh.HBT = g.HB;
+    sh.iters = stream_iters(g);
     sh.inv_d = 1.0f / static_cast<float>(g.D);
-    const unsigned grid = static_cast<unsigned>((p.n_streams + sp.nbs - 1) / sp.nbs);
-    hipLaunchKernelGGL(k, dim3(grid), dim3(kStreamThreads), sp.lds, st, p, sh);
+    const unsigned grid = static_cast<unsigned>((p.n_streams + kStreamNb - 1) / kStreamNb);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(kStreamThreads), stream_lds(g), st, p, sh);
     return hipGetLastError();
 }
 

@@ -15,13 +15,35 @@ struct StreamScoreParams {
     int n_streams;
     int first_slot;              // slot of the newest window's first step (the same in every stream)
     const float *mean, *std;     // [n][M]
-    const uint4 *w1p;            // the detector's packed W1 fragments
-    const float *whp, *wd1p;     // the detector's epilogue fragments
+    const uint4 *w1p;            // W1 as 16x16 fragments [stream_w1_steps][Hp/16][64 lanes]
+    const float *whp, *wd1p;     // heads [Hp/16][4][2][64] and decoder [Hp/16][4][64] fragments
     const float *b1, *bd1, *u, *bh;
     float sum_bd2;
     float *scores;               // [n]
     float *md;                   // [n] or null
 };
+// Scoring kernel of the newest windows: kStreamNb windows per block of kStreamWaves waves; wave w
+// takes the reduction steps j = w mod 4 (four 16-byte chunks of every window each), one
+// iteration per step, with W1 fragments fetched stream_pa iterations ahead and, when the window
+// is a contiguous run of whole metric groups (stream_vec), window chunks stream_pb ahead.
+constexpr int kStreamNb = 16;
+constexpr int kStreamWaves = 4;
+constexpr int stream_pa(int nhb) { return nhb >= 16 ? 2 : nhb >= 8 ? 4 : 8; }
+constexpr int stream_pb(int dtype) { return dtype == ENOVA_F32 ? 8 : 16; }
+inline bool stream_vec(const Geometry &g)
+{
+    return g.Mp == g.M && g.M % g.epc == 0 && (4 * g.epc) % g.M == 0;
+}
+// Iterations of every wave: KC / 16 rounded up to a multiple of the window prefetch depth.
+inline int stream_iters(const Geometry &g)
+{
+    const int u = stream_pb(g.dtype);
+    return (g.KC / 16 + u - 1) / u * u;
+}
+// Reduction steps of the packed W1: every iteration's step plus the prefetch's overrun (zeros
+// past the window's KC chunks).
+inline int stream_w1_steps(const Geometry &g) { return 4 * (stream_iters(g) + stream_pa(g.Hp / 16)); }
+
 // x_step [n][M] becomes step number `step` (0-based) of every stream.
 hipError_t launch_stream_append(const Geometry &g, const void *x_step, int n, int64_t step, void *ring,
                                 hipStream_t st);
