@@ -576,7 +576,7 @@ def train_main(args, cfg):
                    "last_loss": float(inf[0]), "last_beta": float(inf[3])},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": None,
-                     "kernel": "k_gemm (the 11 matrix products of a step)",
+                     "kernel": "k_gemm_rs + k_gemm (the 11 matrix products of a step)",
                      "kernel_ms": round(g_ms, 4), "flops_per_window": fpw, "windows_per_launch": B},
     }
     if not args.no_cpu_baseline:

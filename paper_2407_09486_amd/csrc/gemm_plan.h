@@ -103,17 +103,90 @@ inline GemmPlan gemm_plan(int m, int n, int k, bool may_split, int64_t work_floa
     return p;
 }
 
+// ---------------------------------------------------------------------------------------------
+// Register-streamed products (k_gemm_rs): no LDS staging and no barrier inside the reduction.
+// The four waves of a block each cover every fourth 16-deep step of the block's reduction range
+// for the whole tile; the partial tiles are added in LDS in wave order. Every operand fragment is
+// one 16-byte load per lane straight from global memory: along the reduction index for a
+// k-contiguous operand, along its rows for a row-contiguous one. Only whole tiles and whole
+// prefetch groups are planned; anything else takes k_gemm.
+//   kRsK4: k-contiguous A, either B, a reduction of at least 512; 32 x 128 tiles
+//   kRsR4: both row-contiguous (weight gradients); 64 x 64 tiles, the reduction also split over
+//          blocks when the tiles are few (partials summed in slice order)
+// ---------------------------------------------------------------------------------------------
+enum { kRsNone = 0, kRsK4 = 1, kRsR4 = 3 };
+constexpr int kRsStep = 16;          // reduction indices per wave iteration
+constexpr int kRsWaves = 4;          // waves of a block, along the reduction
+struct RsShape {
+    int tm, tn;      // block tile
+    int pd;          // register slots of operand prefetch (loads run pd - 1 iterations ahead; the
+                     // unroll of the reduction loop)
+};
+constexpr RsShape rs_shape(int kind) { return kind == kRsK4 ? RsShape{32, 128, 2} : RsShape{64, 64, 2}; }
+// Reduction indices one block covers per unrolled loop trip.
+constexpr int rs_k_unit(int kind) { return kRsStep * kRsWaves * rs_shape(kind).pd; }
+
+struct RsPlan {
+    int kind;        // kRsNone: use k_gemm
+    int kc;          // reduction indices per slice (k when not split)
+    int used;        // slices
+};
+
+// Slices a kRsR4 product wants: about kGemmTargetBlocks blocks, each slice a whole number of
+// loop trips.
+inline int rs_r4_splits(int m, int n, int k, int64_t work_floats)
+{
+    const int64_t tiles = static_cast<int64_t>(m / rs_shape(kRsR4).tm) * (n / rs_shape(kRsR4).tn);
+    const int unit = rs_k_unit(kRsR4);
+    const int64_t want = (kGemmTargetBlocks + tiles - 1) / tiles;
+    int s = 1;
+    for (int c = 2; c <= kGemmMaxSplits && c <= want; ++c)
+        if (k % (c * unit) == 0 && static_cast<int64_t>(c) * gemm_slice_floats(m, n) <= work_floats)
+            s = c;
+    return s;
+}
+
+// The register-streamed launch of an m x n x k product, or kind kRsNone. `epi_ok`: the epilogue
+// is one the kernel applies (store, bias + activation, activation derivative); `vec`: both
+// operands are 16-byte aligned with leading dimensions that are multiples of 4. Splits (kRsR4
+// only) obey the same workspace bound as gemm_plan: used * gemm_slice_floats(m, n) <= work_floats.
+inline RsPlan gemm_rs_plan(int m, int n, int k, bool a_k, bool b_k, bool epi_ok, bool vec, bool may_split,
+                           int64_t work_floats)
+{
+    RsPlan p{kRsNone, 0, 0};
+    if (!epi_ok || !vec || m <= 0 || n <= 0 || k <= 0)
+        return p;
+    if (a_k && k >= 512 && m % 32 == 0 && n % 128 == 0 && k % rs_k_unit(kRsK4) == 0) {
+        p = RsPlan{kRsK4, k, 1};
+    } else if (!a_k && !b_k && m % 64 == 0 && n % 64 == 0 && k % rs_k_unit(kRsR4) == 0) {
+        const int s = may_split ? rs_r4_splits(m, n, k, work_floats) : 1;
+        p = RsPlan{kRsR4, k / s, s};
+    }
+    return p;
+}
+
+// Workspace a register-streamed product wants (0: none, or it does not take that kernel).
+inline int64_t gemm_rs_workspace_floats(int m, int n, int k, bool a_k, bool b_k)
+{
+    const RsPlan p = gemm_rs_plan(m, n, k, a_k, b_k, true, true, true, int64_t{1} << 60);
+    return p.used > 1 ? static_cast<int64_t>(p.used) * gemm_slice_floats(m, n) : 0;
+}
+
 // Split workspace (floats) of one training step over a batch of B windows: every product of the
 // step as (m, n, k) -- forward encoder, heads, decoder hidden and output; backward the decoder
 // output's weight and input gradients, the decoder hidden layer's, the heads', the encoder's
 // weight gradient.
 inline int64_t train_gemm_workspace(int B, int D, int H, int L)
 {
-    const int shapes[][3] = {{B, H, D}, {B, 2 * L, H}, {B, H, L},     {B, D, H},     {D, H, B}, {B, H, D},
-                             {H, L, B}, {B, L, H},     {2 * L, H, B}, {B, H, 2 * L}, {H, D, B}};
+    // (m, n, k, A k-contiguous, B k-contiguous)
+    const int shapes[][5] = {{B, H, D, 1, 1},     {B, 2 * L, H, 1, 1}, {B, H, L, 1, 1}, {B, D, H, 1, 1},
+                             {D, H, B, 0, 0},     {B, H, D, 1, 0},     {H, L, B, 0, 0}, {B, L, H, 1, 0},
+                             {2 * L, H, B, 0, 0}, {B, H, 2 * L, 1, 0}, {H, D, B, 0, 0}};
     int64_t ws = 0;
-    for (const auto &sh : shapes)
+    for (const auto &sh : shapes) {
         ws = std::max(ws, gemm_workspace_floats(sh[0], sh[1], sh[2]));
+        ws = std::max(ws, gemm_rs_workspace_floats(sh[0], sh[1], sh[2], sh[3] != 0, sh[4] != 0));
+    }
     return ws;
 }
 

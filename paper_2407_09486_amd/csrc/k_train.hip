@@ -439,6 +439,179 @@ __global__ __launch_bounds__(256, 2) void k_gemm(const float *__restrict__ A, in
         }
 }
 
+// ---- register-streamed products -------------------------------------------------------------
+// C(i, j) = sum_k A(i, k) B(k, j) on 16x16x4 fp32 matrix ops with no LDS staging and no barrier
+// inside the reduction (the launch shapes and their conditions are gemm_rs_plan's). The four
+// waves of a block each compute the whole block tile over every fourth 16-deep reduction step;
+// their partial tiles are added in LDS in wave order at the end. An operand fragment is one
+// 16-byte load per lane l (p = l % 16, g = l / 16) straight from global memory into the
+// matrix-op layout:
+//   k-contiguous, fragment f:     row 16 f + p, indices k0 + 4 g + c (c = 0..3, the components);
+//   row-contiguous, fragment f:   index k0 + 4 g + f % 4, rows 64 (f / 4) + 4 p + c.
+// Matrix op t of an iteration takes, in lane l, reduction index k0 + 4 g + t for both operands (a
+// relabelling of the sum), so a 16-row output block `a` of A reads component t of fragment a
+// (k-contiguous) or component a % 4 of fragment 4 (a / 4) + t (row-contiguous), and likewise for
+// B's 16-column blocks. Output row slot q = 4 g + r of block a (register r) is row 16 a + q, or
+// 64 (a / 4) + 4 q + a % 4 for a row-contiguous A; the same for columns with slot p.
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float comp4(const float4 &v, int c)
+{
+    return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
+}
+
+template <bool KMODE>
+__device__ __forceinline__ int rs_index(int blk, int slot)
+{
+    return KMODE ? 16 * blk + slot : 64 * (blk >> 2) + 4 * slot + (blk & 3);
+}
+
+// MR 16-row blocks x NC 16-column blocks per wave, PD register slots of operand prefetch. RS: the
+// blocks of the first column tile also write rowsum[z m + i] = sum_k A(i, k) over the slice.
+template <bool AK, bool BK, int EPI, int ACT, int MR, int NC, int PD>
+__global__ __launch_bounds__(64 * kRsWaves) void k_gemm_rs(const float *__restrict__ A, int64_t lda,
+                                                           const float *__restrict__ B, int64_t ldb,
+                                                           float *__restrict__ C, int64_t ldc,
+                                                           float *__restrict__ rowsum, EpiParams ep, int m, int kc)
+{
+    constexpr int WK = kRsWaves;
+    constexpr int TM = 16 * MR, TN = 16 * NC;
+    constexpr int NF = MR * NC;                         // output blocks of the tile
+    static_assert(AK || MR % 4 == 0, "row-contiguous A comes in 64-row groups");
+    static_assert(BK || NC % 4 == 0, "row-contiguous B comes in 64-column groups");
+    __shared__ __align__(16) float red[WK * NF * 4 * 64];
+    __shared__ float rred[WK * TM];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int p = lane & 15, g = lane >> 4;
+    const int i0 = blockIdx.y * TM;
+    const int j0 = blockIdx.x * TN;
+    const int kw = blockIdx.z * kc + kRsStep * wave;   // first reduction index of iteration 0
+    const int iters = kc / (kRsStep * WK);
+    C += static_cast<int64_t>(blockIdx.z) * m * ldc;
+
+    // per-lane bases of iteration 0 and the stride between iterations
+    const float *ab = AK ? A + static_cast<int64_t>(i0 + p) * lda + kw + 4 * g
+                         : A + static_cast<int64_t>(kw + 4 * g) * lda + i0 + 4 * p;
+    const float *bb = BK ? B + static_cast<int64_t>(j0 + p) * ldb + kw + 4 * g
+                         : B + static_cast<int64_t>(kw + 4 * g) * ldb + j0 + 4 * p;
+    const int64_t astep = AK ? kRsStep * WK : static_cast<int64_t>(kRsStep) * WK * lda;
+    const int64_t bstep = BK ? kRsStep * WK : static_cast<int64_t>(kRsStep) * WK * ldb;
+    auto aoff = [&](int f) -> int64_t { return AK ? 16 * f * lda : (f & 3) * lda + 64 * (f >> 2); };
+    auto boff = [&](int f) -> int64_t { return BK ? 16 * f * ldb : (f & 3) * ldb + 64 * (f >> 2); };
+
+    v4f acc[MR][NC];
+#pragma unroll
+    for (int a = 0; a < MR; ++a)
+#pragma unroll
+        for (int b = 0; b < NC; ++b)
+            acc[a][b] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    constexpr bool RS = !AK;
+    float rs[RS ? MR : 1];
+#pragma unroll
+    for (int a = 0; a < (RS ? MR : 1); ++a)
+        rs[a] = 0.0f;
+
+    // One iteration's fragments, always issued in the same order (the scheduling barriers): the
+    // prologue and the loop then agree on which loads are in flight at the loop head.
+    float4 ar[PD][MR], br[PD][NC];
+    auto fetch = [&](int it, float4 (&ra)[MR], float4 (&rb)[NC]) __attribute__((always_inline)) {
+        const float *pa = ab + it * astep;
+        const float *pb = bb + it * bstep;
+#pragma unroll
+        for (int f = 0; f < MR; ++f) {
+            ra[f] = *reinterpret_cast<const float4 *>(pa + aoff(f));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int f = 0; f < NC; ++f) {
+            rb[f] = *reinterpret_cast<const float4 *>(pb + boff(f));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    // PD register slots: iteration `it` first issues the loads of iteration it + PD - 1 into the
+    // slot the previous iteration freed, then runs the matrix ops of slot it % PD.
+#pragma unroll
+    for (int u = 0; u < PD - 1; ++u) {
+        fetch(u < iters ? u : iters - 1, ar[u], br[u]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // let the prologue's loads land (vmcnt(0), once per block): the loop head then merges only
+    // the loop's own in-flight loads, whose wait counts stay exact
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    for (int i = 0; i < iters; i += PD) {
+#pragma unroll
+        for (int u = 0; u < PD; ++u) {
+            // past the last iteration the last one is fetched again (never read): loads stay in
+            // range. The barriers keep the loads here (the scheduler would sink them to their use).
+            const int nx = i + u + PD - 1;
+            fetch(nx < iters ? nx : iters - 1, ar[(u + PD - 1) % PD], br[(u + PD - 1) % PD]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int a = 0; a < MR; ++a) {
+                    const float av = AK ? comp4(ar[u][a], t) : comp4(ar[u][4 * (a >> 2) + t], a & 3);
+                    if constexpr (RS)
+                        rs[a] += av;
+#pragma unroll
+                    for (int b = 0; b < NC; ++b) {
+                        const float bv = BK ? comp4(br[u][b], t) : comp4(br[u][4 * (b >> 2) + t], b & 3);
+                        acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[a][b], 0, 0, 0);
+                    }
+                }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    // partial tiles and row sums (the latter over the four lane groups first) into LDS
+#pragma unroll
+    for (int a = 0; a < MR; ++a)
+#pragma unroll
+        for (int b = 0; b < NC; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                red[((wave * NF + a * NC + b) * 4 + r) * 64 + lane] = acc[a][b][r];
+    if constexpr (RS) {
+#pragma unroll
+        for (int a = 0; a < MR; ++a) {
+            rs[a] += __shfl_xor(rs[a], 16);
+            rs[a] += __shfl_xor(rs[a], 32);
+            if (g == 0)
+                rred[wave * TM + a * 16 + p] = rs[a];
+        }
+    }
+    __syncthreads();
+    // wave w finishes the output blocks f = w, w + 4, ... (partials added in wave order)
+    for (int f = wave; f < NF; f += WK) {
+        const int a = f / NC, b = f - (f / NC) * NC;
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float s = 0.0f;
+#pragma unroll
+            for (int w2 = 0; w2 < WK; ++w2)
+                s += red[((w2 * NF + f) * 4 + r) * 64 + lane];
+            v[r] = s;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            epi_store<EPI, ACT>(C, ldc, i0 + rs_index<AK>(a, 4 * g + r), j0 + rs_index<BK>(b, p), v[r], ep);
+    }
+    if constexpr (RS) {
+        if (rowsum != nullptr && blockIdx.x == 0 && wave == 0 && g == 0) {
+#pragma unroll
+            for (int a = 0; a < MR; ++a) {
+                float s = 0.0f;
+#pragma unroll
+                for (int w2 = 0; w2 < WK; ++w2)
+                    s += rred[w2 * TM + a * 16 + p];
+                rowsum[static_cast<int64_t>(blockIdx.z) * m + i0 + rs_index<AK>(a, p)] = s;
+            }
+        }
+    }
+}
+
 // C(i, j) = epilogue(sum over the slices s = 0, 1, ... (in order) of P[s][i][j]) for i < m, j < n,
 // and, with rowsum != NULL, rowsum[i] = sum over the slices of R[s][i].
 template <int EPI, int ACT>
@@ -797,6 +970,25 @@ void sum_run(unsigned blocks, hipStream_t st, const float *P, const float *R, in
                        ep);
 }
 
+// The register-streamed kernel of plan kind `kind` for the operand layouts.
+template <int EPI, int ACT>
+void rs_layouts(int kind, bool a_k, bool b_k, dim3 grid, hipStream_t st, const float *A, int64_t lda,
+                const float *B, int64_t ldb, float *C, int64_t ldc, float *rowsum, const EpiParams &ep, int m, int kc)
+{
+    // each kernel's tile is rs_shape(kind): tm = 16 MR, tn = 16 NC, pd register slots
+    const dim3 block(64 * kRsWaves);
+    if (kind == kRsK4 && b_k)
+        hipLaunchKernelGGL((k_gemm_rs<true, true, EPI, ACT, 2, 8, 2>), grid, block, 0, st, A, lda, B, ldb, C, ldc,
+                           rowsum, ep, m, kc);
+    else if (kind == kRsK4)
+        hipLaunchKernelGGL((k_gemm_rs<true, false, EPI, ACT, 2, 8, 2>), grid, block, 0, st, A, lda, B, ldb, C, ldc,
+                           rowsum, ep, m, kc);
+    else
+        hipLaunchKernelGGL((k_gemm_rs<false, false, EPI, ACT, 4, 4, 2>), grid, block, 0, st, A, lda, B, ldb, C, ldc,
+                           rowsum, ep, m, kc);
+    (void)a_k;
+}
+
 // The epilogue kind and activation as template arguments.
 template <template <int, int> class F, typename... Args>
 void with_epilogue(int kind, int act, Args &&...args)
@@ -815,6 +1007,26 @@ void with_epilogue(int kind, int act, Args &&...args)
         F<kEpiRowReduce, ENOVA_RELU>::run(args...);
     } else {
         F<kEpiStore, ENOVA_RELU>::run(args...);
+    }
+}
+
+// rs_layouts with the epilogue kind and activation as template arguments (store, bias +
+// activation, activation derivative: the kinds gemm_rs_plan accepts).
+template <typename... Args>
+void rs_epilogue(int kind, int act, Args &&...args)
+{
+    if (kind == kEpiBiasAct) {
+        if (act == ENOVA_TANH)
+            rs_layouts<kEpiBiasAct, ENOVA_TANH>(args...);
+        else
+            rs_layouts<kEpiBiasAct, ENOVA_RELU>(args...);
+    } else if (kind == kEpiDact) {
+        if (act == ENOVA_TANH)
+            rs_layouts<kEpiDact, ENOVA_TANH>(args...);
+        else
+            rs_layouts<kEpiDact, ENOVA_RELU>(args...);
+    } else {
+        rs_layouts<kEpiStore, ENOVA_RELU>(args...);
     }
 }
 
@@ -854,17 +1066,48 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
     if (epi.kind == kEpiRowReduce &&
         (epi.groups < 1 || epi.groups > 32 || (epi.groups & (epi.groups - 1)) != 0 || !epi.sq || !epi.out2))
         return hipErrorInvalidValue;
+    const EpiParams epp{epi.bias, epi.out2, epi.pre, epi.sq, epi.ldv, epi.groups};
+    {
+        // whole tiles with aligned operands: the register-streamed kernel
+        const bool epi_rs = epi.kind == kEpiStore || epi.kind == kEpiBiasAct || epi.kind == kEpiDact;
+        const RsPlan rp = gemm_rs_plan(m, n, k, a_k, b_k, epi_rs, va && vb, work != nullptr, work_floats);
+        if (rp.kind != kRsNone) {
+            const RsShape sh = rs_shape(rp.kind);
+            const dim3 rgrid(static_cast<unsigned>(n / sh.tn), static_cast<unsigned>(m / sh.tm),
+                             static_cast<unsigned>(rp.used));
+            hipError_t e = hipSuccess;
+            if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess)
+                return e;
+            if (rp.used == 1) {
+                rs_epilogue(epi.kind, epi.act, rp.kind, a_k, b_k, rgrid, st, A, lda, B, ldb, C, ldc, rowsum, epp, m,
+                            rp.kc);
+                if ((e = hipGetLastError()) != hipSuccess)
+                    return e;
+                return ev1 ? hipEventRecord(ev1, st) : hipSuccess;
+            }
+            float *part_rows = rowsum ? work + static_cast<int64_t>(rp.used) * m * n : nullptr;
+            rs_layouts<kEpiStore, ENOVA_RELU>(rp.kind, a_k, b_k, rgrid, st, A, lda, B, ldb, work,
+                                              static_cast<int64_t>(n), part_rows, EpiParams{}, m, rp.kc);
+            if ((e = hipGetLastError()) != hipSuccess)
+                return e;
+            if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess)
+                return e;
+            const unsigned blocks = blocks_for(static_cast<int64_t>(m) * n + (rowsum ? m : 0));
+            with_epilogue<SumF>(epi.kind, epi.act, blocks, st, static_cast<const float *>(work),
+                                static_cast<const float *>(part_rows), rp.used, m, n, C, ldc, rowsum, epp);
+            return hipGetLastError();
+        }
+    }
     // never more slices than the caller's workspace holds (a row reduction is never split)
     const GemmPlan plan = gemm_plan(m, n, k, work && epi.kind != kEpiRowReduce, work_floats);
     const int kc = plan.kc, used = plan.used;
     const dim3 grid(static_cast<unsigned>((n + plan.tn - 1) / plan.tn), static_cast<unsigned>((m + plan.tm - 1) / plan.tm),
                     static_cast<unsigned>(used));
-    const EpiParams ep{epi.bias, epi.out2, epi.pre, epi.sq, epi.ldv, epi.groups};
     hipError_t e = hipSuccess;
     if (ev0 && (e = hipEventRecord(ev0, st)) != hipSuccess)
         return e;
     if (used == 1) {
-        with_epilogue<GemmF>(epi.kind, epi.act, a_k, b_k, grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, ep, m, n,
+        with_epilogue<GemmF>(epi.kind, epi.act, a_k, b_k, grid, st, A, lda, va, B, ldb, vb, C, ldc, rowsum, epp, m, n,
                              k, kc);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
@@ -880,7 +1123,7 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
         return e;
     const unsigned blocks = blocks_for(static_cast<int64_t>(m) * n + (rowsum ? m : 0));
     with_epilogue<SumF>(epi.kind, epi.act, blocks, st, static_cast<const float *>(work),
-                        static_cast<const float *>(part_rows), used, m, n, C, ldc, rowsum, ep);
+                        static_cast<const float *>(part_rows), used, m, n, C, ldc, rowsum, epp);
     return hipGetLastError();
 }
 

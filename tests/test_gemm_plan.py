@@ -40,6 +40,12 @@ int main() {
             std::scanf("%d %d %d %lld", &D, &H, &L, &N);
             int B = variants_chunk(D, N), last = variants_last_rows(N, B);
             std::printf("%d %d %lld\n", B, last, (long long)variants_gemm_workspace(B, last, D, H, L));
+        } else if (!std::strcmp(op, "R")) {    // m n k a_k b_k may_split work -> kind tm tn unit kc used
+            int m, n, k, ak, bk, may; long long ws;
+            std::scanf("%d %d %d %d %d %d %lld", &m, &n, &k, &ak, &bk, &may, &ws);
+            RsPlan p = gemm_rs_plan(m, n, k, ak != 0, bk != 0, true, true, may != 0, ws);
+            RsShape sh = rs_shape(p.kind);
+            std::printf("%d %d %d %d %d %d\n", p.kind, sh.tm, sh.tn, p.kind ? rs_k_unit(p.kind) : 0, p.kc, p.used);
         } else if (!std::strcmp(op, "T")) {    // B D H L -> training workspace
             int B, D, H, L;
             std::scanf("%d %d %d %d", &B, &D, &H, &L);
@@ -154,3 +160,50 @@ def test_training_products_fit_their_workspace(planner, B, D, H, L):
         assert p[3] <= w[0]
         if w[0] > 1:
             assert p[3] > 1, (m, n, k)
+
+
+# the step's products as (m, n, k, A k-contiguous, B k-contiguous), in launch order
+def _train_layouts(B, D, H, L):
+    return [(B, H, D, 1, 1), (B, 2 * L, H, 1, 1), (B, H, L, 1, 1), (B, D, H, 1, 1), (D, H, B, 0, 0),
+            (B, H, D, 1, 0), (H, L, B, 0, 0), (B, L, H, 1, 0), (2 * L, H, B, 0, 0), (B, H, 2 * L, 1, 0),
+            (H, D, B, 0, 0)]
+
+
+def _check_rs(planner, layouts, ws, may=1):
+    out = planner.run([f"R {m} {n} {k} {a} {b} {may} {ws}" for m, n, k, a, b in layouts])
+    for (m, n, k, a, b), (kind, tm, tn, unit, kc, used) in zip(layouts, out):
+        if kind == 0:
+            continue
+        assert kind in (1, 3)
+        assert m % tm == 0 and n % tn == 0, (m, n, k, kind)
+        assert kc * used == k and kc % unit == 0, (m, n, k, kc, used, unit)
+        if kind == 1:
+            assert a == 1 and used == 1 and k >= 512
+        if kind == 3:
+            assert a == 0 and b == 0
+        if used > 1:
+            assert may and used * (m * n + m) <= ws, (m, n, k, used, ws)
+    return out
+
+
+@pytest.mark.parametrize("B", [1, 32, 64, 500, 512, 3000, 4096, 8192, 65536])
+@pytest.mark.parametrize("D,H,L", [(1024, 128, 16), (512, 128, 16), (256, 32, 16), (8192, 256, 16), (102, 70, 16)])
+def test_register_streamed_plans_cover_whole_tiles(planner, B, D, H, L):
+    ws = planner.run([f"T {B} {D} {H} {L}"])[0][0]
+    _check_rs(planner, _train_layouts(B, D, H, L), ws)
+    _check_rs(planner, _train_layouts(B, D, H, L), 0, may=0)
+
+
+def test_register_streamed_plans_of_the_training_workload(planner):
+    """c5's training shape (D = 1024, H = 128, L = 16, B = 8192): the encoder, dJ/da2 and the two
+    large weight gradients take the register-streamed kernel (the weight gradients split their
+    8192-long reduction over blocks); the decoder output (a reduction of 128) and the thin
+    products stay on the LDS-tiled kernel."""
+    B, D, H, L = 8192, 1024, 128, 16
+    ws = planner.run([f"T {B} {D} {H} {L}"])[0][0]
+    out = _check_rs(planner, _train_layouts(B, D, H, L), ws)
+    kinds = [o[0] for o in out]
+    assert kinds[0] == 1 and kinds[5] == 1 and kinds[3] == 0      # encoder, dJ/da2; decoder output
+    assert kinds[4] == 3 and kinds[10] == 3                       # dWd2, dW1
+    assert out[4][5] == 8 and out[10][5] == 8
+    assert kinds[1] == kinds[2] == kinds[6] == kinds[7] == kinds[8] == kinds[9] == 0

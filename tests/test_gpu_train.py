@@ -123,6 +123,18 @@ def test_step_matches_oracle_ragged_tiles(act, seed):
     _check_adam_first_step(r, HYPER["lr"], act)
 
 
+def test_step_matches_oracle_whole_tiles():
+    """D = 32 x 16 = 512, H = 128, L = 16, B = 512: every large product is a whole number of the
+    register-streamed kernel's tiles (the encoder and dJ/da1-type products with the reduction
+    split over the waves, the decoder output with the columns split, the weight gradients with
+    both operands row-contiguous and the reduction split over blocks as well)."""
+    cfg = _cfg(16, 32, 128, 16, "tanh")
+    r = _one_step(cfg, 512, 6)
+    _check_info(r["info"], r["ref_info"], 1e-5, "whole tiles")
+    _check_grads(r["g_gpu"], r["g_ref"], GRAD_RTOL, "whole tiles")
+    _check_adam_first_step(r, HYPER["lr"], "whole tiles")
+
+
 @pytest.mark.parametrize("what,B,frac,labels", [("one window", 1, 0.0, None),
                                                 ("all anomalous", 40, 0.0, -1.0),
                                                 ("all normal", 40, 0.0, 1.0)])
