@@ -44,4 +44,57 @@ __host__ __device__ inline void gpd_terms(double t, double &a, double &b)
     b = kd * kLn2Hi + (kd * kLn2Lo + (lm + c));
 }
 
+// Device form of gpd_terms: both quotients from the hardware reciprocal refined by two Newton
+// steps (r <- r + r (1 - u r)), the second quotient corrected once more, and the exponent split of
+// 1 + t read from its bits (frexp only for a subnormal or non-finite 1 + t); r = 1/(1 + t) is
+// returned for the derivatives. The results stay within a few ulps of gpd_terms.
+__device__ inline void gpd_terms_fast(double t, double &a, double &b, double &r)
+{
+    const double u = 1.0 + t;
+    r = __builtin_amdgcn_rcp(u);
+    r = fma(r, fma(-u, r, 1.0), r);
+    r = fma(r, fma(-u, r, 1.0), r);
+    a = t * r;
+    const double c = (t - (u - 1.0)) * r;
+    const long long bits = __double_as_longlong(u);
+    const int ebits = static_cast<int>((bits >> 52) & 0x7ff);
+    int k;
+    double m;
+    if (ebits == 0 || ebits == 0x7ff) {
+        m = frexp(u, &k);
+    } else {
+        k = ebits - 1022;
+        m = __longlong_as_double((bits & static_cast<long long>(0x800fffffffffffffULL)) | 0x3fe0000000000000LL);
+    }
+    if (m < 0.70710678118654752440) {
+        m *= 2.0;
+        --k;
+    }
+    const double d = m + 1.0, nm = m - 1.0;
+    double rd = __builtin_amdgcn_rcp(d);
+    rd = fma(rd, fma(-d, rd, 1.0), rd);
+    rd = fma(rd, fma(-d, rd, 1.0), rd);
+    double s = nm * rd;
+    s = fma(rd, fma(-d, s, nm), s);
+    const double z = s * s;
+    double p = 1.0 / 19.0;
+    p = p * z + 1.0 / 17.0;
+    p = p * z + 1.0 / 15.0;
+    p = p * z + 1.0 / 13.0;
+    p = p * z + 1.0 / 11.0;
+    p = p * z + 1.0 / 9.0;
+    p = p * z + 1.0 / 7.0;
+    p = p * z + 1.0 / 5.0;
+    p = p * z + 1.0 / 3.0;
+    const double lm = 2.0 * s + (2.0 * s * z) * p;
+    const double kd = static_cast<double>(k);
+    b = kd * kLn2Hi + (kd * kLn2Lo + (lm + c));
+}
+
+__device__ inline void gpd_terms_fast(double t, double &a, double &b)
+{
+    double r;
+    gpd_terms_fast(t, a, b, r);
+}
+
 }  // namespace enova

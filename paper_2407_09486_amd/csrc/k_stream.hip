@@ -11,7 +11,8 @@
 //
 // SPOT refits run on the device, one block per stream with a new peak, with the batch fit's
 // method: Grimshaw's reduction bracketed on geometric 512-point grids of both admissible
-// intervals and refined by k-section, the exponential tail always a candidate.
+// intervals, each bracket refined to fp64 resolution (here by Newton's method kept inside the
+// bracket), the exponential tail always a candidate.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -532,24 +533,26 @@ __global__ __launch_bounds__(256) void k_spot_update(const float *__restrict__ s
 }
 
 constexpr int kFitGrid = 512;       // grid points per admissible interval
-constexpr int kFitInterior = 63;    // k-section points per bracket and round
-constexpr int kFitRounds = 40;
+constexpr int kFitRounds = 64;      // evaluations per bracket at most
 constexpr int kFitMaxBrackets = 64; // sign changes kept per fit
-constexpr int kFitBatch = 16;       // brackets refined per evaluation batch
+constexpr int kFitThreads = 1024;   // threads of a refit block (16 waves: four per SIMD)
+constexpr int kFitWaves = kFitThreads / 64;
+constexpr int kFitMaxPoints = 2 * kFitGrid;
+constexpr int kFitLdsPeaks = 4096;  // a stream with at most this many peaks refits from an LDS copy
+static_assert(kFitMaxPoints <= kFitThreads, "one point per thread");
 
 struct FitShared {
-    double xs[2 * kFitGrid];
-    double sa[2 * kFitGrid];
-    double sb[2 * kFitGrid];
-    double red[256], red2[256];
-    double blo[kFitMaxBrackets], bhi[kFitMaxBrackets], broot[kFitMaxBrackets];
+    double yl[kFitLdsPeaks];     // the stream's peaks
+    double xs[kFitMaxPoints];
+    double sa[kFitMaxPoints];
+    double sb[kFitMaxPoints];
+    double red[3][kFitWaves + 1];
+    double blo[kFitMaxBrackets], bhi[kFitMaxBrackets], broot[kFitMaxBrackets], bx[kFitMaxBrackets];
     int bneg[kFitMaxBrackets], bdone[kFitMaxBrackets], bround[kFitMaxBrackets];
     double roots[2 * kFitMaxBrackets];
-    int batch[kFitBatch];
-    int coll[kFitBatch];         // 1: the batch bracket's points are not strictly inside it
-    int scan[256];
+    int batch[kFitWaves];        // the brackets the waves refine in this evaluation
+    int wcount[2][kFitWaves];    // per-wave counts of roots and of sign changes
     int nbr, nroots, npts, ngrid, nbatch;
-    double ysum, ymin, ymax;
 };
 
 __device__ __forceinline__ double fit_w(double sa, double sb, double n)
@@ -565,110 +568,101 @@ __device__ __forceinline__ double fit_quantile(double t, double gamma, double si
     return t + sigma / gamma * (pow(ratio, -gamma) - 1.0);
 }
 
-// sa/sb at the first npts (<= 1024) points of sh.xs over all N excesses. Many points: each
-// thread takes up to four; few points: T threads share a point (power of two, T * npts <= 256),
-// each summing every T-th excess, and the T partial sums are added in order. A fixed order
-// either way.
-__device__ void fit_eval(FitShared &sh, const double *y, int N)
+// sa/sb at the first npts (<= kFitMaxPoints) points of sh.xs over all N excesses (with
+// nw > 0: sa = w(sa, sb, nw) = b - a - a b instead). The points go
+// in groups of four; the T threads of a group (T a power of two, at most 64, consecutive lanes
+// of one wave) each sum every T-th excess for the group's four points side by side (independent
+// dependency chains), and the T partial sums are added by a fixed butterfly. A fixed order.
+__device__ void fit_eval(FitShared &sh, const double *y, int N, double nw = 0.0)
 {
     const int np = sh.npts;
-    if (np > 128) {
-        // up to four points per thread, evaluated side by side (independent dependency chains)
-        double x[4], a[4], b[4];
+    const int groups = (np + 3) / 4;
+    int T = 1;
+    while (T < 64 && 2 * T * groups <= kFitThreads)
+        T *= 2;
+    const int gi = static_cast<int>(threadIdx.x) / T;
+    const int part = static_cast<int>(threadIdx.x) % T;
+    double x[4], a[4], b[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int p = threadIdx.x + 256 * k;
-            x[k] = p < np ? sh.xs[p] : 0.0;
-            a[k] = 0.0;
-            b[k] = 0.0;
-        }
-        for (int i = 0; i < N; ++i) {
+    for (int k = 0; k < 4; ++k) {
+        const int p = 4 * gi + k;
+        x[k] = gi < groups && p < np ? sh.xs[p] : 0.0;
+        a[k] = 0.0;
+        b[k] = 0.0;
+    }
+    if (gi < groups) {
+        for (int i = part; i < N; i += T) {
             const double yi = y[i];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 double ta, tb;
-                gpd_terms(x[k] * yi, ta, tb);
+                gpd_terms_fast(x[k] * yi, ta, tb);
                 a[k] += ta;
                 b[k] += tb;
             }
         }
+    }
+    // every lane of the wave takes part in the butterfly (T divides 64)
+    for (int off = T / 2; off >= 1; off >>= 1) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const int p = threadIdx.x + 256 * k;
+            a[k] += __shfl_xor(a[k], off);
+            b[k] += __shfl_xor(b[k], off);
+        }
+    }
+    if (gi < groups && part == 0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int p = 4 * gi + k;
             if (p < np) {
-                sh.sa[p] = a[k];
+                sh.sa[p] = nw > 0.0 ? fit_w(a[k], b[k], nw) : a[k];
                 sh.sb[p] = b[k];
             }
         }
-        __syncthreads();
-        return;
-    }
-    int T = 1;
-    while (T < 64 && 2 * T * np <= 256)
-        T *= 2;
-    const int per = 256 / T;
-    const int part = threadIdx.x % T;
-    for (int p0 = 0; p0 < np; p0 += per) {
-        const int p = p0 + static_cast<int>(threadIdx.x) / T;
-        double a = 0.0, b = 0.0;
-        if (p < np) {
-            const double x = sh.xs[p];
-            for (int i = part; i < N; i += T) {
-                double ta, tb;
-                gpd_terms(x * y[i], ta, tb);
-                a += ta;
-                b += tb;
-            }
-        }
-        if (T == 1) {
-            if (p < np) {
-                sh.sa[p] = a;
-                sh.sb[p] = b;
-            }
-        } else {
-            sh.red[threadIdx.x] = a;
-            sh.red2[threadIdx.x] = b;
-            __syncthreads();
-            if (part == 0 && p < np) {
-                double sa = 0.0, sb = 0.0;
-                for (int k = 0; k < T; ++k) {
-                    sa += sh.red[threadIdx.x + k];
-                    sb += sh.red2[threadIdx.x + k];
-                }
-                sh.sa[p] = sa;
-                sh.sb[p] = sb;
-            }
-            __syncthreads();
-        }
     }
     __syncthreads();
 }
 
-// w = b - a - a b at the first npts points, into sh.sa (every thread a share).
-__device__ void fit_w_all(FitShared &sh, double n)
+// Fixed-order block reductions of one value per thread: a butterfly in each wave, then the wave
+// results in wave order. block_reduce3 forms the sum of v0, the minimum of v1 and the maximum of
+// v2 together; block_sum the sum of v.
+__device__ void block_reduce3(FitShared &sh, double &v0, double &v1, double &v2)
 {
-    for (int p = threadIdx.x; p < sh.npts; p += 256)
-        sh.sa[p] = fit_w(sh.sa[p], sh.sb[p], n);
+    for (int off = 32; off >= 1; off >>= 1) {
+        v0 += __shfl_xor(v0, off);
+        v1 = fmin(v1, __shfl_xor(v1, off));
+        v2 = fmax(v2, __shfl_xor(v2, off));
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        sh.red[0][wave] = v0;
+        sh.red[1][wave] = v1;
+        sh.red[2][wave] = v2;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double r0 = sh.red[0][0], r1 = sh.red[1][0], r2 = sh.red[2][0];
+        for (int w = 1; w < kFitWaves; ++w) {
+            r0 += sh.red[0][w];
+            r1 = fmin(r1, sh.red[1][w]);
+            r2 = fmax(r2, sh.red[2][w]);
+        }
+        sh.red[0][kFitWaves] = r0;
+        sh.red[1][kFitWaves] = r1;
+        sh.red[2][kFitWaves] = r2;
+    }
+    __syncthreads();
+    v0 = sh.red[0][kFitWaves];
+    v1 = sh.red[1][kFitWaves];
+    v2 = sh.red[2][kFitWaves];
     __syncthreads();
 }
 
-// Fixed-order block reduction (sum, min or max) of one value per thread.
-template <int OP>
-__device__ double block_reduce(FitShared &sh, double v)
+__device__ double block_sum(FitShared &sh, double v)
 {
-    sh.red[threadIdx.x] = v;
-    __syncthreads();
-    for (int w = 128; w >= 1; w >>= 1) {
-        if (threadIdx.x < w) {
-            const double o = sh.red[threadIdx.x + w];
-            double &m = sh.red[threadIdx.x];
-            m = OP == 0 ? m + o : (OP == 1 ? fmin(m, o) : fmax(m, o));
-        }
-        __syncthreads();
-    }
-    const double r = sh.red[0];
-    __syncthreads();
-    return r;
+    double lo = INFINITY, hi = -INFINITY;
+    block_reduce3(sh, v, lo, hi);
+    return v;
 }
 
 // Refit of z for one marked stream by one block: N_t <= 1 gives t; 2 <= N_t < 10 the method of
@@ -676,28 +670,33 @@ __device__ double block_reduce(FitShared &sh, double v)
 __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState &st)
 {
     const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
     const int N = st.npk[s];
     const double t = st.t[s];
     const double n = static_cast<double>(st.cnt[s]);
-    const double *y = st.peaks + static_cast<int64_t>(s) * st.cap;
+    const double *yg = st.peaks + static_cast<int64_t>(s) * st.cap;
     double z = t;
     if (N >= 2) {
+        // the peaks are read once per pass below: from an LDS copy when they fit
+        const double *y = N <= kFitLdsPeaks ? sh.yl : yg;
         double ps = 0.0, pmin = INFINITY, pmax = -INFINITY;
-        for (int i = tid; i < N; i += 256) {
-            ps += y[i];
-            pmin = fmin(pmin, y[i]);
-            pmax = fmax(pmax, y[i]);
+        for (int i = tid; i < N; i += kFitThreads) {
+            const double v = yg[i];
+            if (N <= kFitLdsPeaks)
+                sh.yl[i] = v;
+            ps += v;
+            pmin = fmin(pmin, v);
+            pmax = fmax(pmax, v);
         }
-        const double ysum = block_reduce<0>(sh, ps);
-        const double ymin = block_reduce<1>(sh, pmin);
-        const double ymax = block_reduce<2>(sh, pmax);
+        block_reduce3(sh, ps, pmin, pmax);     // its barriers also publish the LDS copy
+        const double ysum = ps, ymin = pmin, ymax = pmax;
         const double Nd = static_cast<double>(N);
         const double ymean = ysum / Nd;
         if (N < 10) {
             double pv = 0.0;
-            for (int i = tid; i < N; i += 256)
+            for (int i = tid; i < N; i += kFitThreads)
                 pv += (y[i] - ymean) * (y[i] - ymean);
-            const double s2 = block_reduce<0>(sh, pv) / (Nd - 1.0);
+            const double s2 = block_sum(sh, pv) / (Nd - 1.0);
             if (s2 > 0.0) {
                 const double gamma = 0.5 * (1.0 - ymean * ymean / s2);
                 const double sigma = 0.5 * ymean * (1.0 + ymean * ymean / s2);
@@ -709,29 +708,29 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
             const double f0 = eps * ymax;
             const double right = 2.0 * (ymean - ymin) / (ymin * ymin);
             const bool has_left = f0 < 0.5, has_right = right > 2.0 * eps;
-            const int left_at = 0, right_at = has_left ? kFitGrid : 0;
-            for (int i = tid; i < kFitGrid; i += 256) {
-                if (has_left) {
+            const int right_at = has_left ? kFitGrid : 0;
+            // threads 0 .. kFitGrid-1 the left grid, the others the right one
+            static_assert(2 * kFitGrid <= kFitThreads, "a grid point per thread");
+            {
+                const int i = tid % kFitGrid;
+                if (tid < kFitGrid && has_left) {
                     const double zlo = log(f0 / (1.0 - f0)), zhi = 30.0;
                     const double zz = zlo + (zhi - zlo) * static_cast<double>(i) / static_cast<double>(kFitGrid - 1);
-                    sh.xs[left_at + i] = -(1.0 / (1.0 + exp(-zz))) / ymax;
+                    sh.xs[i] = -(1.0 / (1.0 + exp(-zz))) / ymax;
                 }
-                if (has_right)
+                if (tid >= kFitGrid && tid < 2 * kFitGrid && has_right)
                     sh.xs[right_at + i] = eps * pow(right / eps, static_cast<double>(i) / static_cast<double>(kFitGrid - 1));
             }
             if (tid == 0) {
                 sh.ngrid = (has_left ? 1 : 0) + (has_right ? 1 : 0);
                 sh.npts = sh.ngrid * kFitGrid;
-                sh.nbr = 0;
-                sh.nroots = 0;
             }
             __syncthreads();
-            fit_eval(sh, y, N);
-            fit_w_all(sh, Nd);
+            fit_eval(sh, y, N, Nd);
             // every grid point: an exact root, and/or a sign change to the next point of its grid;
-            // both kept in grid order (ordered compaction over the block)
-            for (int p0 = 0; p0 < sh.npts; p0 += 256) {
-                const int i = p0 + tid;
+            // both kept in grid order (wave ballots, then the waves in order)
+            {
+                const int i = tid;
                 int root = 0, br = 0;
                 if (i < sh.npts) {
                     const int gi = i % kFitGrid;
@@ -741,17 +740,23 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                     else if (gi + 1 < kFitGrid && wi * sh.sa[i + 1] < 0.0)
                         br = 1;
                 }
-                sh.scan[tid] = root | (br << 16);
-                __syncthreads();
-                for (int off = 1; off < 256; off <<= 1) {
-                    const int v = tid >= off ? sh.scan[tid - off] : 0;
-                    __syncthreads();
-                    sh.scan[tid] += v;
-                    __syncthreads();
+                const uint64_t mr = __ballot(root), mb = __ballot(br);
+                const uint64_t below = lane ? (~uint64_t{0} >> (64 - lane)) : 0;
+                if (lane == 0) {
+                    sh.wcount[0][wave] = __popcll(mr);
+                    sh.wcount[1][wave] = __popcll(mb);
                 }
-                const int incl = sh.scan[tid];
-                const int r_at = sh.nroots + (incl & 0xffff) - root;
-                const int b_at = sh.nbr + (incl >> 16) - br;
+                __syncthreads();
+                int r_at = __popcll(mr & below), b_at = __popcll(mb & below);
+                int nr = 0, nb = 0;
+                for (int w = 0; w < kFitWaves; ++w) {
+                    if (w < wave) {
+                        r_at += sh.wcount[0][w];
+                        b_at += sh.wcount[1][w];
+                    }
+                    nr += sh.wcount[0][w];
+                    nb += sh.wcount[1][w];
+                }
                 if (root && r_at < 2 * kFitMaxBrackets)
                     sh.roots[r_at] = sh.xs[i];
                 if (br && b_at < kFitMaxBrackets) {
@@ -764,80 +769,83 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                     sh.bround[b_at] = 0;
                     sh.broot[b_at] = 0.0;
                 }
-                __syncthreads();
-                if (tid == 255) {
-                    const int nr = sh.nroots + (incl & 0xffff), nb = sh.nbr + (incl >> 16);
+                if (tid == 0) {
                     sh.nroots = nr < 2 * kFitMaxBrackets ? nr : 2 * kFitMaxBrackets;
                     sh.nbr = nb < kFitMaxBrackets ? nb : kFitMaxBrackets;
                 }
                 __syncthreads();
             }
-            // k-section, up to kFitBatch open brackets per evaluation: the points and w are
-            // computed by all threads, one thread keeps the brackets
+            // Newton's method on w inside each bracket: one wave per open bracket evaluates w and
+            // w' at the bracket's current point over all peaks (lane l sums the peaks l, l + 64,
+            // ..., a butterfly adds the lanes), and its lane 0 keeps the bracket on the sign of w,
+            // taking the Newton step when it lands strictly inside and the midpoint otherwise. A
+            // bracket ends at an exact zero of w, when the step falls to 4 ulp of the point, when
+            // the bracket can no longer be split, or after kFitRounds evaluations.
+            if (tid < sh.nbr)
+                sh.bx[tid] = 0.5 * (sh.blo[tid] + sh.bhi[tid]);
             for (;;) {
                 if (tid == 0) {
                     sh.nbatch = 0;
-                    for (int b = 0; b < sh.nbr && sh.nbatch < kFitBatch; ++b) {
-                        if (sh.bdone[b])
-                            continue;
-                        if (sh.bround[b] >= kFitRounds) {
-                            sh.bdone[b] = 1;
-                            sh.broot[b] = 0.5 * (sh.blo[b] + sh.bhi[b]);
-                            continue;
-                        }
-                        sh.coll[sh.nbatch] = 0;
-                        sh.batch[sh.nbatch++] = b;
-                    }
-                    sh.npts = sh.nbatch * kFitInterior;
+                    for (int b = 0; b < sh.nbr && sh.nbatch < kFitWaves; ++b)
+                        if (!sh.bdone[b])
+                            sh.batch[sh.nbatch++] = b;
                 }
                 __syncthreads();
                 if (sh.nbatch == 0)
                     break;
-                for (int i = tid; i < sh.npts; i += 256) {
-                    const int k = i / kFitInterior, j = i - k * kFitInterior + 1;
-                    const int b = sh.batch[k];
-                    const double lo = sh.blo[b], hi = sh.bhi[b];
-                    sh.xs[i] = lo + (hi - lo) * static_cast<double>(j) / (kFitInterior + 1);
-                }
-                __syncthreads();
-                for (int i = tid; i < sh.npts; i += 256) {
-                    // a bracket that can no longer shrink: its points are not strictly inside
-                    const int k = i / kFitInterior, j = i - k * kFitInterior + 1;
-                    const int b = sh.batch[k];
-                    const double prev = j == 1 ? sh.blo[b] : sh.xs[i - 1];
-                    if (!(sh.xs[i] > prev) || !(sh.xs[i] < sh.bhi[b]))
-                        sh.coll[k] = 1;
-                }
-                fit_eval(sh, y, N);
-                fit_w_all(sh, Nd);
-                if (tid == 0) {
-                    for (int k = 0; k < sh.nbatch; ++k) {
-                        const int b = sh.batch[k];
-                        if (sh.coll[k]) {
+                if (wave < sh.nbatch) {
+                    const int b = sh.batch[wave];
+                    const double x = sh.bx[b];
+                    double sa = 0.0, sb = 0.0, sda = 0.0, sdb = 0.0;
+                    for (int i = lane; i < N; i += 64) {
+                        const double yi = y[i];
+                        double ta, tb, r;
+                        gpd_terms_fast(x * yi, ta, tb, r);
+                        sa += ta;
+                        sb += tb;
+                        sdb += yi * r;
+                        sda += (yi * r) * r;
+                    }
+                    for (int off = 32; off >= 1; off >>= 1) {
+                        sa += __shfl_xor(sa, off);
+                        sb += __shfl_xor(sb, off);
+                        sda += __shfl_xor(sda, off);
+                        sdb += __shfl_xor(sdb, off);
+                    }
+                    if (lane == 0) {
+                        const double a = sa / Nd, bm = sb / Nd, da = sda / Nd, db = sdb / Nd;
+                        const double wv = bm - a - a * bm;
+                        const double wd = db - da - da * bm - a * db;
+                        const int it = sh.bround[b] + 1;
+                        sh.bround[b] = it;
+                        if (wv == 0.0) {
                             sh.bdone[b] = 1;
-                            sh.broot[b] = 0.5 * (sh.blo[b] + sh.bhi[b]);
-                            continue;
-                        }
-                        double new_lo = sh.blo[b], new_hi = sh.bhi[b];
-                        for (int j = 0; j < kFitInterior; ++j) {
-                            const int pi = k * kFitInterior + j;
-                            const double wj = sh.sa[pi];
-                            if (wj == 0.0) {
+                            sh.broot[b] = x;
+                        } else {
+                            double lo = sh.blo[b], hi = sh.bhi[b];
+                            if ((wv < 0.0) == (sh.bneg[b] != 0))
+                                lo = x;
+                            else
+                                hi = x;
+                            const double xn = x - wv / wd;
+                            const bool inside = xn > lo && xn < hi;     // false for NaN
+                            const double mid = 0.5 * (lo + hi);
+                            const double tol = 0x1p-50 * fmax(fabs(lo), fabs(hi));
+                            sh.blo[b] = lo;
+                            sh.bhi[b] = hi;
+                            if (inside && fabs(xn - x) <= tol) {
                                 sh.bdone[b] = 1;
-                                sh.broot[b] = sh.xs[pi];
-                                break;
+                                sh.broot[b] = xn;
+                            } else if (!inside && !(mid > lo && mid < hi)) {
+                                sh.bdone[b] = 1;
+                                sh.broot[b] = mid;
+                            } else if (it >= kFitRounds) {
+                                sh.bdone[b] = 1;
+                                sh.broot[b] = inside ? xn : mid;
+                            } else {
+                                sh.bx[b] = inside ? xn : mid;
                             }
-                            if ((wj < 0.0) != (sh.bneg[b] != 0)) {
-                                new_hi = sh.xs[pi];
-                                break;
-                            }
-                            new_lo = sh.xs[pi];
                         }
-                        if (!sh.bdone[b]) {
-                            sh.blo[b] = new_lo;
-                            sh.bhi[b] = new_hi;
-                        }
-                        sh.bround[b] += 1;
                     }
                 }
                 __syncthreads();
@@ -879,21 +887,20 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
 }
 
 // One block per stream, the unmarked ones leaving at once (the start of a streaming set).
-__global__ __launch_bounds__(256) void k_spot_fit_all(double q, SpotState st)
+__global__ __launch_bounds__(kFitThreads) void k_spot_fit_all(double q, SpotState st)
 {
     __shared__ FitShared sh;
     if (st.mark[blockIdx.x])
         spot_fit_stream(sh, blockIdx.x, q, st);
 }
 
-// The streams the last update listed, spread over a fixed grid of blocks (a push refits a few
-// percent of the streams; launching a block per stream would mostly launch empty blocks).
-__global__ __launch_bounds__(256) void k_spot_fit_list(double q, SpotState st)
+// The streams the last update listed, one block each (a grid of one block per stream, the blocks
+// past the list's length leaving at once).
+__global__ __launch_bounds__(kFitThreads) void k_spot_fit_list(double q, SpotState st)
 {
     __shared__ FitShared sh;
-    const int cnt = *st.count;
-    for (int i = blockIdx.x; i < cnt; i += gridDim.x)
-        spot_fit_stream(sh, st.list[i], q, st);
+    if (static_cast<int>(blockIdx.x) < *st.count)
+        spot_fit_stream(sh, st.list[blockIdx.x], q, st);
 }
 
 }  // namespace
@@ -980,14 +987,9 @@ hipError_t launch_spot_fit(int n, double q, const SpotState &s, bool all, hipStr
     if (n <= 0)
         return hipSuccess;
     if (all) {
-        hipLaunchKernelGGL(k_spot_fit_all, dim3(static_cast<unsigned>(n)), dim3(256), 0, st, q, s);
+        hipLaunchKernelGGL(k_spot_fit_all, dim3(static_cast<unsigned>(n)), dim3(kFitThreads), 0, st, q, s);
     } else {
-        int dev = 0, cus = 256;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            cus = 256;
-        const int blocks = n < 2 * cus ? n : 2 * cus;
-        hipLaunchKernelGGL(k_spot_fit_list, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, q, s);
+        hipLaunchKernelGGL(k_spot_fit_list, dim3(static_cast<unsigned>(n)), dim3(kFitThreads), 0, st, q, s);
     }
     return hipGetLastError();
 }
