@@ -110,7 +110,8 @@ inline GemmPlan gemm_plan(int m, int n, int k, bool may_split, int64_t work_floa
 // one 16-byte load per lane straight from global memory: along the reduction index for a
 // k-contiguous operand, along its rows for a row-contiguous one. Only whole tiles and whole
 // prefetch groups are planned; anything else takes k_gemm.
-//   kRsK4: k-contiguous A, either B, a reduction of at least 512; 32 x 128 tiles
+//   kRsK4: k-contiguous A, either B, a reduction of at least 512, fewer than 128 tiles of
+//          128 x 128; 32 x 128 tiles
 //   kRsR4: both row-contiguous (weight gradients); 64 x 64 tiles, the reduction also split over
 //          blocks when the tiles are few (partials summed in slice order)
 // ---------------------------------------------------------------------------------------------
@@ -156,7 +157,11 @@ inline RsPlan gemm_rs_plan(int m, int n, int k, bool a_k, bool b_k, bool epi_ok,
     RsPlan p{kRsNone, 0, 0};
     if (!epi_ok || !vec || m <= 0 || n <= 0 || k <= 0)
         return p;
-    if (a_k && k >= 512 && m % 32 == 0 && n % 128 == 0 && k % rs_k_unit(kRsK4) == 0) {
+    // kRsK4 only where k_gemm's 128 x 128 tiles would leave most of the chip idle (it then cuts
+    // 32-wide tiles, the shape this kernel beats); with many tiles k_gemm's LDS reuse wins
+    const int64_t tiles128 = static_cast<int64_t>((m + kGemmTile - 1) / kGemmTile) * ((n + kGemmTile - 1) / kGemmTile);
+    if (a_k && k >= 512 && m % 32 == 0 && n % 128 == 0 && k % rs_k_unit(kRsK4) == 0 &&
+        tiles128 < kGemmTargetBlocks / 2) {
         p = RsPlan{kRsK4, k, 1};
     } else if (!a_k && !b_k && m % 64 == 0 && n % 64 == 0 && k % rs_k_unit(kRsR4) == 0) {
         const int s = may_split ? rs_r4_splits(m, n, k, work_floats) : 1;

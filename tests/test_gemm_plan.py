@@ -179,6 +179,7 @@ def _check_rs(planner, layouts, ws, may=1):
         assert kc * used == k and kc % unit == 0, (m, n, k, kc, used, unit)
         if kind == 1:
             assert a == 1 and used == 1 and k >= 512
+            assert ((m + 127) // 128) * ((n + 127) // 128) < 128, (m, n, k)
         if kind == 3:
             assert a == 0 and b == 0
         if used > 1:
@@ -203,6 +204,8 @@ def test_register_streamed_plans_of_the_training_workload(planner):
     ws = planner.run([f"T {B} {D} {H} {L}"])[0][0]
     out = _check_rs(planner, _train_layouts(B, D, H, L), ws)
     kinds = [o[0] for o in out]
+    # the variant pass's encoder over a full chunk of 262144 windows keeps the LDS-tiled kernel
+    assert _check_rs(planner, [(262144, H, D, 1, 1)], 0, may=0)[0][0] == 0
     assert kinds[0] == 1 and kinds[5] == 1 and kinds[3] == 0      # encoder, dJ/da2; decoder output
     assert kinds[4] == 3 and kinds[10] == 3                       # dWd2, dW1
     assert out[4][5] == 8 and out[10][5] == 8
