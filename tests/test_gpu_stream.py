@@ -159,3 +159,38 @@ def test_stream_window_steps_and_stride():
     assert r["sc"].shape[0] == (41 - 5) // 3 + 1
     _check_scores(cfg, r)
     _check_spot(r)
+
+
+def test_stream_full_size_sampled():
+    """The streaming benchmark's shape and launch: 4096 streams of c5's detector (16 metrics,
+    W = 64, S = 1, H = 128, fp32), so the scoring kernel runs its full grid of 256 blocks; five
+    scoring pushes. Scores and md of 128 sampled streams against the oracle, and their SPOT
+    steps against the oracle's SPOT fed with the same scores."""
+    cfg = wl.CONFIGS["c5"].replace(n_streams=4096, kind="ragged_mix")
+    n = 4096
+    log(f"[stream] full size: {n} streams, M={cfg.metrics} W={cfg.window} H={cfg.hidden}")
+    r = _run(cfg, n=n, t_ref=300, t_live=cfg.window + 4)
+    assert r["sc"].shape == (5, n)
+    rng = np.random.default_rng(7)
+    pick = np.unique(np.concatenate([[0, 1, 15, 16, 255, 256, n - 1], rng.choice(n, 121, replace=False)]))
+    live = r["live"]
+    x = live.values_f64()
+    offs = live.stream_offsets
+    xs = np.concatenate([x[offs[s]:offs[s + 1]] for s in pick])
+    so = np.concatenate([[0], np.cumsum([offs[s + 1] - offs[s] for s in pick])]).astype(np.int64)
+    o_sc, o_md, info = oracle.score(xs, so, window=cfg.window, stride=cfg.stride, weights=r["weights"].as_f64(),
+                                    act=cfg.act, bf16=False, ref_mean=r["mean"][pick], ref_std=r["std"][pick],
+                                    return_stats=True)
+    k = r["sc"].shape[0]
+    o_sc = o_sc.reshape(len(pick), k).T
+    o_md = o_md.reshape(len(pick), k).T
+    scale = info["md_scale"].reshape(len(pick), k).T
+    check_scores(r["sc"][:, pick].ravel(), o_sc.ravel(), cfg.dtype, "full-size stream scores")
+    check_md(r["md"][:, pick].ravel(), o_md.ravel(), scale.ravel(), cfg.dtype, "full-size stream md")
+    sub = dict(r)
+    sub["cal"] = [r["cal"][s] for s in pick]
+    sub["sc"] = r["sc"][:, pick]
+    sub["fl"] = r["fl"][:, pick]
+    sub["state"] = tuple(np.asarray(a)[pick] for a in r["state"])
+    sub["start"] = tuple(np.asarray(a)[pick] for a in r["start"])
+    _check_spot(sub)
