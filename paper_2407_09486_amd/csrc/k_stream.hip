@@ -3,11 +3,11 @@
 // al. -- the POT method Section IV-B cites; Section V runs the detector in a stream-computing
 // job).
 //
-// Scoring: the newest windows of NBS streams form one tile. Unlike the sliding-window batch
-// kernel, no two windows of a tile share data, so each window's D inputs are staged in LDS in
-// the padded chunk order of the packed W1 (chunk kappa = q*CPR + c: chunk c of super-row q),
-// KS chunks at a time, and the encoder contraction C[h][n] = sum_k W1[h][k] V[n][k] runs on the
-// matrix cores slice by slice; the epilogue is the batch kernel's.
+// Scoring: a block scores the newest windows of 16 streams (Section IV-B: normalise, encoder,
+// heads, KL score, decoder hidden layer for the md). Unlike the sliding-window batch kernel, no
+// two windows share data, so nothing is staged: each wave streams its share of the reduction
+// from the rings straight into registers and the four waves' partial sums meet in LDS once
+// (the scoring section below).
 //
 // SPOT refits run on the device, one block per stream with a new peak, with the batch fit's
 // method: Grimshaw's reduction bracketed on geometric 512-point grids of both admissible
