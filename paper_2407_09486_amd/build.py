@@ -21,7 +21,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
 
 SOURCES = ["detector.cpp", "pot.cpp", "k_aux.hip", "k_score_valu.hip", "k_score_mfma.hip", "k_stream.hip",
            "k_train.hip", "trainer.cpp", "k_config.hip", "config.cpp", "k_variants.hip", "scratch.hip",
-           "k_score_ring.hip"]
+           "k_score_ring.hip", "k_ext_fused.hip"]
 
 
 def _compile(src: str) -> str:

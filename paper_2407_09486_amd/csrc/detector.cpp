@@ -77,6 +77,8 @@ struct enova_detector_s {
     void *stream_w = nullptr;     // streaming kernel: W1, heads and decoder fragments (one allocation)
     const uint4 *w1s = nullptr;
     const float *whs = nullptr, *wds = nullptr;
+    void *ext_w = nullptr;        // fused variant pass: decoder-output fragments (Wd2, bd2)
+    const float4 *wd2p = nullptr, *bd2p = nullptr;
     void *w1t = nullptr;          // [D][H] transposed W1
     float *small = nullptr;       // every small weight array, one allocation
     float *b1 = nullptr, *bh = nullptr, *bmu = nullptr, *blv = nullptr, *wmu = nullptr,
@@ -396,12 +398,52 @@ enova_status pack_stream(enova_detector d, const enova_detect_weights *w)
     return e == hipSuccess ? ENOVA_OK : hip_fail(e, "configure the streaming scoring kernel");
 }
 
+// Row of register r for lane half g inside a 32x32 matrix-op accumulator block.
+int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+// Decoder-output fragments of the fused variant pass (32x32x2 fp32 ops whose B operand is the
+// decoder hidden layer's accumulator): Wd2 as [D/32][HB][4][64 lanes] x 4 floats, where lane l,
+// component e of (ob, hb, r4) holds Wd2[32 ob + l%32][32 hb + crow(4 r4 + e, l/32)] (zero past
+// H), and bd2 as [D/32][4][64 lanes] x 4 floats, lane l component e of (ob, g) holding
+// bd2[32 ob + crow(4 g + e, l/32)] (the accumulator's initial value).
+enova_status pack_ext_fused(enova_detector d, const enova_detect_weights *w)
+{
+    const Geometry &g = d->g;
+    const int H = g.H, D = g.D, HB = g.HB, nob = D / 32;
+    const size_t n_w = static_cast<size_t>(nob) * HB * 4 * 64 * 4, n_b = static_cast<size_t>(nob) * 4 * 64 * 4;
+    std::vector<float> buf(n_w + n_b, 0.0f);
+    for (int ob = 0; ob < nob; ++ob) {
+        for (int hb = 0; hb < HB; ++hb)
+            for (int r4 = 0; r4 < 4; ++r4)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int e = 0; e < 4; ++e) {
+                        const int j = 32 * ob + (lane & 31);
+                        const int h = 32 * hb + crow(4 * r4 + e, lane >> 5);
+                        if (h < H)
+                            buf[((((static_cast<size_t>(ob) * HB + hb) * 4 + r4) * 64 + lane) * 4) + e] =
+                                w->wd2[static_cast<int64_t>(j) * H + h];
+                    }
+        for (int gq = 0; gq < 4; ++gq)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int e = 0; e < 4; ++e)
+                    buf[n_w + ((static_cast<size_t>(ob) * 4 + gq) * 64 + lane) * 4 + e] =
+                        w->bd2[32 * ob + crow(4 * gq + e, lane >> 5)];
+    }
+    enova_status st = dev_upload(&d->ext_w, buf.data(), buf.size() * sizeof(float));
+    if (st != ENOVA_OK)
+        return st;
+    d->wd2p = static_cast<const float4 *>(d->ext_w);
+    d->bd2p = d->wd2p + n_w / 4;
+    const hipError_t e = prepare_ext_fused(g);
+    return e == hipSuccess ? ENOVA_OK : hip_fail(e, "configure the fused variant kernel");
+}
+
 void free_detector(enova_detector d)
 {
     if (!d)
         return;
     void *ptrs[] = {d->w1p, d->w1t, d->small, d->stats, d->tiles, d->tile_map, d->cal, d->hist,
-                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws, d->ring_w, d->stream_w};
+                    d->peaks, d->blk, d->gx, d->dense, d->ext_ws, d->ring_w, d->stream_w, d->ext_w};
     for (void *p : ptrs)
         if (p)
             (void)hipFree(p);
@@ -415,8 +457,6 @@ void free_detector(enova_detector d)
             (void)hipEventDestroy(e);
     delete d;
 }
-
-int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 
 enova_status check_config(const enova_detect_config *c)
 {
@@ -785,6 +825,8 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
             st = pack_ring(d, w);
         if (st == ENOVA_OK && stream_score_supported(g))
             st = pack_stream(d, w);
+        if (st == ENOVA_OK && ext_fused_supported(g))
+            st = pack_ext_fused(d, w);
     }
     if (st == ENOVA_OK) {
         hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 256 * sizeof(unsigned int));
@@ -1057,6 +1099,59 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
                 return hip_fail(e, "hipEventCreate");
     }
     const int D = g.D, H = g.H, L = g.L, M = g.M;
+    if (det->wd2p) {
+        // fused pass: one block per 256-window tile, every output written directly
+        const int64_t grid = (n_windows + kExtFusedNb - 1) / kExtFusedNb + n;
+        if (grid > 0x7fffffffLL)
+            return fail(ENOVA_EUNSUPPORTED, "too many tiles (%lld)", static_cast<long long>(grid));
+        const bool stats = norm == ENOVA_NORM_REFERENCE && !ref_mean;
+        // workspace: reference statistics [2][n][M] floats, first tile of each stream [n+1]
+        // int64, stream of each block [grid] ints
+        const size_t n_st = stats ? (2 * static_cast<size_t>(n) * M + 3) / 4 * 4 : 0;
+        const size_t n_tiles = 2 * (static_cast<size_t>(n) + 1);
+        enova_status st = ensure(&det->ext_ws, &det->ext_ws_cap, n_st + n_tiles + static_cast<size_t>(grid) + 4);
+        if (st != ENOVA_OK)
+            return st;
+        int64_t *tiles = reinterpret_cast<int64_t *>(det->ext_ws + n_st);
+        int *tmap = reinterpret_cast<int *>(tiles + n + 1);
+        if (det->timing)
+            (void)hipEventRecord(det->ext_ev[0], stream);
+        if (stats) {
+            ref_mean = det->ext_ws;
+            ref_std = det->ext_ws + static_cast<size_t>(n) * M;
+            if ((e = launch_ref_stats(g, x, soff, n, det->ext_ws, det->ext_ws + static_cast<size_t>(n) * M,
+                                      stream)) != hipSuccess)
+                return hip_fail(e, "reference statistics kernel");
+        }
+        if ((e = launch_stream_scan(g, soff, woff, n, 0, kExtFusedNb, tiles, stream)) != hipSuccess)
+            return hip_fail(e, "tile scan kernel");
+        if ((e = launch_tile_map(tiles, n, grid, tmap, stream)) != hipSuccess)
+            return hip_fail(e, "tile map kernel");
+        ExtFusedParams fp{};
+        fp.x = static_cast<const float *>(x);
+        fp.soff = soff;
+        fp.woff = woff;
+        fp.tile_off = tiles;
+        fp.tile_stream = tmap;
+        fp.mean = ref_mean;
+        fp.std = ref_std;
+        fp.w1p = static_cast<const uint4 *>(det->w1p);
+        fp.cst = det->whp;
+        fp.wd2p = det->wd2p;
+        fp.bd2p = det->bd2p;
+        fp.scores = out_scores;
+        fp.md = out_md;
+        fp.mdm = out_md_metric;
+        fp.rec = out_recon;
+        fp.norm = norm;
+        fp.decode = (out_md || out_md_metric || out_recon) ? 1 : 0;
+        if ((e = launch_ext_fused(g, fp, grid, stream)) != hipSuccess)
+            return hip_fail(e, "fused variant kernel");
+        if (det->timing)
+            (void)hipEventRecord(det->ext_ev[1], stream);
+        det->ran_ext = true;
+        return ENOVA_OK;
+    }
     const int B = variants_chunk(D, n_windows);
     // workspace: V, out [B][D]; a1, h, a2, hd [B][H]; ml [B][2L]; the products' split partials,
     // for a full chunk and for the last, shorter one

@@ -25,4 +25,33 @@ hipError_t launch_ext_finish(const float *P, const float *Q, int rows, int slots
 hipError_t launch_ext_reduce(const float *V, const float *out, const float *bd2, int rows, int M, int W, float *md,
                              float *md_metric, float *recon, hipStream_t st);
 
+// ---------------------------------------------------------------------------------------------
+// Fused variant pass (k_ext_fused.hip): fp32 detectors with 4, 8 or 16 metrics, at most 64
+// hidden units (128 with ReLU), at most 16 latent units and W*M a multiple of 32. One block per
+// tile of kExtFusedNb consecutive windows of a stream (tile_off / tile_stream as the scoring
+// kernel's), every output written directly.
+// ---------------------------------------------------------------------------------------------
+constexpr int kExtFusedNb = 256;
+struct ExtFusedParams {
+    const float *x;
+    const int64_t *soff, *woff, *tile_off;
+    const int *tile_stream;
+    const float *mean, *std;     // reference statistics [n][M] (reference normalisation only)
+    const uint4 *w1p;            // the scoring kernel's encoder A fragments
+    const float *cst;            // the scoring kernel's block: heads, decoder hidden layer, b1, bd1, u, bh
+    const float4 *wd2p;          // [D/32][HB][4][64 lanes]: Wd2[32 ob + l%32][32 hb + crow(4 r4 + e, l/32)], e = 0..3
+    const float4 *bd2p;          // [D/32][4][64 lanes]: bd2[32 ob + crow(4 g + e, l/32)], e = 0..3
+    float *scores, *md, *mdm, *rec;   // any may be NULL
+    int norm;                    // ENOVA_NORM_REFERENCE or ENOVA_NORM_WINDOW
+    int decode;                  // 0: scores only (the decoder is skipped)
+};
+struct ExtFusedShape {
+    int S, W, Q, CPR, CPRP, KC, spare, D;
+    float inv_w, inv_d;
+};
+bool ext_fused_supported(const Geometry &g);
+size_t ext_fused_lds_bytes(const Geometry &g);
+hipError_t prepare_ext_fused(const Geometry &g);
+hipError_t launch_ext_fused(const Geometry &g, const ExtFusedParams &p, int64_t grid, hipStream_t st);
+
 }  // namespace enova
