@@ -78,7 +78,7 @@ struct enova_detector_s {
     const uint4 *w1s = nullptr;
     const float *whs = nullptr, *wds = nullptr;
     void *ext_w = nullptr;        // fused variant pass: decoder-output fragments (Wd2, bd2)
-    const float4 *wd2p = nullptr, *bd2p = nullptr;
+    const float4 *wd2p = nullptr;
     void *w1t = nullptr;          // [D][H] transposed W1
     float *small = nullptr;       // every small weight array, one allocation
     float *b1 = nullptr, *bh = nullptr, *bmu = nullptr, *blv = nullptr, *wmu = nullptr,
@@ -404,15 +404,14 @@ int crow(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
 // Decoder-output fragments of the fused variant pass (32x32x2 fp32 ops whose B operand is the
 // decoder hidden layer's accumulator): Wd2 as [D/32][HB][4][64 lanes] x 4 floats, where lane l,
 // component e of (ob, hb, r4) holds Wd2[32 ob + l%32][32 hb + crow(4 r4 + e, l/32)] (zero past
-// H), and bd2 as [D/32][4][64 lanes] x 4 floats, lane l component e of (ob, g) holding
-// bd2[32 ob + crow(4 g + e, l/32)] (the accumulator's initial value).
+// H).
 enova_status pack_ext_fused(enova_detector d, const enova_detect_weights *w)
 {
     const Geometry &g = d->g;
     const int H = g.H, D = g.D, HB = g.HB, nob = D / 32;
-    const size_t n_w = static_cast<size_t>(nob) * HB * 4 * 64 * 4, n_b = static_cast<size_t>(nob) * 4 * 64 * 4;
-    std::vector<float> buf(n_w + n_b, 0.0f);
-    for (int ob = 0; ob < nob; ++ob) {
+    const size_t n_w = static_cast<size_t>(nob) * HB * 4 * 64 * 4;
+    std::vector<float> buf(n_w, 0.0f);
+    for (int ob = 0; ob < nob; ++ob)
         for (int hb = 0; hb < HB; ++hb)
             for (int r4 = 0; r4 < 4; ++r4)
                 for (int lane = 0; lane < 64; ++lane)
@@ -423,17 +422,10 @@ enova_status pack_ext_fused(enova_detector d, const enova_detect_weights *w)
                             buf[((((static_cast<size_t>(ob) * HB + hb) * 4 + r4) * 64 + lane) * 4) + e] =
                                 w->wd2[static_cast<int64_t>(j) * H + h];
                     }
-        for (int gq = 0; gq < 4; ++gq)
-            for (int lane = 0; lane < 64; ++lane)
-                for (int e = 0; e < 4; ++e)
-                    buf[n_w + ((static_cast<size_t>(ob) * 4 + gq) * 64 + lane) * 4 + e] =
-                        w->bd2[32 * ob + crow(4 * gq + e, lane >> 5)];
-    }
     enova_status st = dev_upload(&d->ext_w, buf.data(), buf.size() * sizeof(float));
     if (st != ENOVA_OK)
         return st;
     d->wd2p = static_cast<const float4 *>(d->ext_w);
-    d->bd2p = d->wd2p + n_w / 4;
     const hipError_t e = prepare_ext_fused(g);
     return e == hipSuccess ? ENOVA_OK : hip_fail(e, "configure the fused variant kernel");
 }
@@ -569,15 +561,18 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
     Geometry &g = d->g;
     plan_geometry(*config, &g);
     if (config->kernel == ENOVA_KERNEL_MFMA && !g.mfma_ok) {
+        // the message reads the geometry, which the detector owns: format it before the free
+        st = fail(ENOVA_EUNSUPPORTED,
+                  "matrix-core kernel needs hidden <= 256, latent <= 16 and a tile that fits LDS "
+                  "(H=%d L=%d LDS=%zu)", g.H, g.L, g.lds_bytes);
         free_detector(d);
-        return fail(ENOVA_EUNSUPPORTED,
-                    "matrix-core kernel needs hidden <= 256, latent <= 16 and a tile that fits LDS "
-                    "(H=%d L=%d LDS=%zu)", g.H, g.L, g.lds_bytes);
+        return st;
     }
     if (config->kernel == ENOVA_KERNEL_VALU || !g.mfma_ok) {
         if (g.H > 1024) {
+            st = fail(ENOVA_EUNSUPPORTED, "hidden width %d > 1024 is not supported", g.H);
             free_detector(d);
-            return fail(ENOVA_EUNSUPPORTED, "hidden width %d > 1024 is not supported", g.H);
+            return st;
         }
         d->kind = 1;
     } else {
@@ -1138,7 +1133,7 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
         fp.w1p = static_cast<const uint4 *>(det->w1p);
         fp.cst = det->whp;
         fp.wd2p = det->wd2p;
-        fp.bd2p = det->bd2p;
+        fp.bd2 = det->d_bd2;
         fp.scores = out_scores;
         fp.md = out_md;
         fp.mdm = out_md_metric;

@@ -82,18 +82,23 @@ __global__ __launch_bounds__(kFusedWaves * 64, 2) void k_ext_fused(ExtFusedParam
     const int nrows = nv + Q - 1 + g.spare;
 
     // LDS: heads fragments, decoder hidden-layer fragments, b1, bd1, u, head biases (the host's
-    // contiguous block), then the raw super-rows at a pitch of CPRP chunks
+    // contiguous block), bd2, then the raw super-rows at a pitch of CPRP chunks
     float *s_whp = reinterpret_cast<float *>(lds);
     float *s_wd1p = s_whp + N_WHP;
     float *s_b1 = s_wd1p + N_WD1P;
     float *s_bd1 = s_b1 + HP;
     float *s_bh = s_bd1 + 2 * HP;
-    uint4 *seg = lds + N_CONST / 4;
+    float *s_bd2 = s_whp + N_CONST;   // [D]
+    uint4 *seg = lds + N_CONST / 4 + g.D / 4;
     {
         const float4 *src = reinterpret_cast<const float4 *>(p.cst);
         float4 *dst = reinterpret_cast<float4 *>(s_whp);
         for (int i = tid; i < N_CONST / 4; i += NT)
             dst[i] = src[i];
+        const float4 *src2 = reinterpret_cast<const float4 *>(p.bd2);
+        float4 *dst2 = reinterpret_cast<float4 *>(s_bd2);
+        for (int i = tid; i < g.D / 4; i += NT)
+            dst2[i] = src2[i];
     }
 
     // ---- stage the tile's super-rows: one contiguous span of the stream (zero past its end)
@@ -298,35 +303,9 @@ __global__ __launch_bounds__(kFusedWaves * 64, 2) void k_ext_fused(ExtFusedParam
         kl[i] += __shfl_xor(kl[i], 32);
     }
 
-    // ---- decoder hidden layer at z = mu, kept as the decoder output's B operands
+    // ---- decoder, one window block at a time: the hidden layer hd = act(Wd1 mu + bd1) (the
+    // decoder output's B operands), then the output blocks, each reduced against v in registers
     const bool decode = p.decode != 0;
-    v16f hd[HB][NBW];
-    if (decode) {
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-#pragma unroll
-            for (int i = 0; i < NBW; ++i)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    hd[hb][i][r] = 0.0f;
-#pragma unroll
-            for (int r = 0; r < 8; ++r) {
-                const float wv = s_wd1p[(hb * 8 + r) * 64 + lane];
-#pragma unroll
-                for (int i = 0; i < NBW; ++i)
-                    hd[hb][i] = __builtin_amdgcn_mfma_f32_32x32x2f32(wv, z[i][r], hd[hb][i], 0, 0, 0);
-            }
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float bh = s_bd1[hb * 32 + crow(r, half)];
-#pragma unroll
-                for (int i = 0; i < NBW; ++i)
-                    hd[hb][i][r] = act_fn<ACT>(hd[hb][i][r] + bh);
-            }
-        }
-    }
-
-    // ---- decoder output, one 32-element block at a time, reduced against v in registers
     float4 sm[NBW][CH];
     float sq[NBW];
 #pragma unroll
@@ -337,46 +316,63 @@ __global__ __launch_bounds__(kFusedWaves * 64, 2) void k_ext_fused(ExtFusedParam
             sm[i][j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
     if (decode) {
-        const float4 *wa = p.wd2p + lane;
-        const float4 *ba = p.bd2p + lane;
+        // Wd2 fragments of one output block (HB * 4 16-byte loads) run one block ahead in a
+        // register ring: fragment (ob, hb, r4) is replaced right after its four matrix ops by the
+        // same fragment of block ob + 1 (of block 0 after the last block, for the next window block)
         const int nob = g.D / 32;
-        for (int ob = 0; ob < nob; ++ob) {
-            v16f o[NBW];
+        constexpr int PF = HB * 4;
+        const float4 *wa = p.wd2p + lane;
+        float4 ar[PF];
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                const float4 bv = ba[(ob * 4 + gq) * 64];
+        for (int f = 0; f < PF; ++f)
+            ar[f] = wa[f * 64];
 #pragma unroll
-                for (int i = 0; i < NBW; ++i)
+        for (int i = 0; i < NBW; ++i) {
+            v16f hd[HB];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        o[i][4 * gq + e] = comp(bv, e);
+            for (int hb = 0; hb < HB; ++hb) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    hd[hb][r] = 0.0f;
+#pragma unroll
+                for (int r = 0; r < 8; ++r)
+                    hd[hb] = __builtin_amdgcn_mfma_f32_32x32x2f32(s_wd1p[(hb * 8 + r) * 64 + lane], z[i][r], hd[hb], 0,
+                                                                  0, 0);
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    hd[hb][r] = act_fn<ACT>(hd[hb][r] + s_bd1[hb * 32 + crow(r, half)]);
             }
+            for (int ob = 0; ob < nob; ++ob) {
+                const float4 *wnext = wa + (ob + 1 == nob ? 0 : (ob + 1) * PF * 64);
+                v16f o;
 #pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
+                for (int r = 0; r < 16; ++r)
+                    o[r] = 0.0f;
 #pragma unroll
-                for (int r4 = 0; r4 < 4; ++r4) {
-                    const float4 w4 = wa[((ob * HB + hb) * 4 + r4) * 64];
+                for (int f = 0; f < PF; ++f) {
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-#pragma unroll
-                        for (int i = 0; i < NBW; ++i)
-                            o[i] = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(w4, e), hd[hb][i][4 * r4 + e], o[i], 0,
-                                                                        0, 0);
+                        o = __builtin_amdgcn_mfma_f32_32x32x2f32(comp(ar[f], e), hd[f / 4][4 * (f % 4) + e], o, 0, 0,
+                                                                 0);
+                    __builtin_amdgcn_sched_barrier(0);
+                    ar[f] = wnext[f * 64];
                 }
-            // registers 4 gq .. 4 gq + 3 hold the chunk (8 ob + 2 gq + half) of the window, i.e.
-            // step t = chunk / MC, metric chunk = chunk mod MC (constant set gq mod 2 when MC = 4)
+                // registers 4 gq .. 4 gq + 3 hold the chunk (8 ob + 2 gq + half) of the window,
+                // i.e. step t = chunk / MC, metric chunk = chunk mod MC (constant set gq mod 2
+                // when MC = 4)
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                const int t = (8 * ob + 2 * gq + half) / MC;
-                const int cj = CH == 2 ? (gq & 1) : 0;
-                const int off = S == 1 ? t * CPRP + mchunk(cj)
-                                       : (t / S) * CPRP + (t % S) * MC + mchunk(cj);
-#pragma unroll
-                for (int i = 0; i < NBW; ++i) {
+                for (int gq = 0; gq < 4; ++gq) {
+                    const int t = (8 * ob + 2 * gq + half) / MC;
+                    const int cj = CH == 2 ? (gq & 1) : 0;
+                    const int off = S == 1 ? t * CPRP + mchunk(cj) : (t / S) * CPRP + (t % S) * MC + mchunk(cj);
+                    const float4 bd = reinterpret_cast<const float4 *>(s_bd2)[ob * 8 + 2 * gq + half];
                     const float4 x4 = reinterpret_cast<const float4 &>(seg[rb[i] + off]);
                     const float4 v4 = fma4(x4, ca[i][cj], cb[i][cj]);
-                    const float d0 = v4.x - o[i][4 * gq + 0], d1 = v4.y - o[i][4 * gq + 1];
-                    const float d2 = v4.z - o[i][4 * gq + 2], d3 = v4.w - o[i][4 * gq + 3];
+                    const float d0 = (v4.x - bd.x) - o[4 * gq + 0];
+                    const float d1 = (v4.y - bd.y) - o[4 * gq + 1];
+                    const float d2 = (v4.z - bd.z) - o[4 * gq + 2];
+                    const float d3 = (v4.w - bd.w) - o[4 * gq + 3];
                     sm[i][cj].x += d0;
                     sm[i][cj].y += d1;
                     sm[i][cj].z += d2;
@@ -447,13 +443,14 @@ FusedKernel pick_mc(int hb, int mc)
     case 2 * 8 + 4: return k_ext_fused<2, 4, ACT>;
     default: break;
     }
-    if constexpr (ACT == ENOVA_RELU) {   // with tanh, 128 hidden units do not fit the registers
-        switch (hb * 8 + mc) {
-        case 4 * 8 + 1: return k_ext_fused<4, 1, ACT>;
-        case 4 * 8 + 2: return k_ext_fused<4, 2, ACT>;
-        case 4 * 8 + 4: return k_ext_fused<4, 4, ACT>;
-        default: break;
-        }
+    switch (hb * 8 + mc) {
+    case 4 * 8 + 1: return k_ext_fused<4, 1, ACT>;
+    case 4 * 8 + 2: return k_ext_fused<4, 2, ACT>;
+    default: break;
+    }
+    if constexpr (ACT == ENOVA_RELU) {   // with tanh, 128 hidden units and 16 metrics exceed the registers
+        if (hb == 4 && mc == 4)
+            return k_ext_fused<4, 4, ACT>;
     }
     return nullptr;
 }
@@ -471,14 +468,14 @@ size_t ext_fused_lds_bytes(const Geometry &g)
 {
     const size_t n_const = static_cast<size_t>(g.HB) * (16 * 64 + 8 * 64) + 3 * static_cast<size_t>(g.Hp) + 32;
     const size_t rows = static_cast<size_t>(kExtFusedNb + g.Q - 1 + g.spare);
-    return n_const * sizeof(float) + rows * g.CPRP * 16;
+    return (n_const + static_cast<size_t>(g.D)) * sizeof(float) + rows * g.CPRP * 16;
 }
 
 bool ext_fused_supported(const Geometry &g)
 {
     return g.mfma_ok && !g.ring && g.dtype == ENOVA_F32 && (g.M == 4 || g.M == 8 || g.M == 16) && g.Mp == g.M &&
-           (g.HB <= 2 || (g.HB == 4 && g.act == ENOVA_RELU)) && g.L <= 16 && g.D % 32 == 0 && g.KC % 4 == 0 &&
-           ext_fused_lds_bytes(g) <= kLdsLimit / 2;
+           (g.HB <= 2 || (g.HB == 4 && (g.act == ENOVA_RELU || g.M <= 8))) && g.L <= 16 && g.D % 32 == 0 &&
+           g.KC % 4 == 0 && ext_fused_lds_bytes(g) <= kLdsLimit / 2;
 }
 
 hipError_t prepare_ext_fused(const Geometry &g)

@@ -26,10 +26,10 @@ hipError_t launch_ext_reduce(const float *V, const float *out, const float *bd2,
                              float *md_metric, float *recon, hipStream_t st);
 
 // ---------------------------------------------------------------------------------------------
-// Fused variant pass (k_ext_fused.hip): fp32 detectors with 4, 8 or 16 metrics, at most 64
-// hidden units (128 with ReLU), at most 16 latent units and W*M a multiple of 32. One block per
-// tile of kExtFusedNb consecutive windows of a stream (tile_off / tile_stream as the scoring
-// kernel's), every output written directly.
+// Fused variant pass (k_ext_fused.hip): fp32 detectors with 4, 8 or 16 metrics, at most 128
+// hidden units (64 with tanh and 16 metrics), at most 16 latent units and W*M a multiple of 32.
+// One block per tile of kExtFusedNb consecutive windows of a stream (tile_off / tile_stream as
+// the scoring kernel's), every output written directly.
 // ---------------------------------------------------------------------------------------------
 constexpr int kExtFusedNb = 256;
 struct ExtFusedParams {
@@ -40,7 +40,7 @@ struct ExtFusedParams {
     const uint4 *w1p;            // the scoring kernel's encoder A fragments
     const float *cst;            // the scoring kernel's block: heads, decoder hidden layer, b1, bd1, u, bh
     const float4 *wd2p;          // [D/32][HB][4][64 lanes]: Wd2[32 ob + l%32][32 hb + crow(4 r4 + e, l/32)], e = 0..3
-    const float4 *bd2p;          // [D/32][4][64 lanes]: bd2[32 ob + crow(4 g + e, l/32)], e = 0..3
+    const float *bd2;            // [D]
     float *scores, *md, *mdm, *rec;   // any may be NULL
     int norm;                    // ENOVA_NORM_REFERENCE or ENOVA_NORM_WINDOW
     int decode;                  // 0: scores only (the decoder is skipped)

@@ -74,6 +74,17 @@ def test_init_rejects_bad_config(over):
     assert binding.lib().enova_last_error()
 
 
+@pytest.mark.parametrize("over,text", [(dict(hidden=300, kernel=binding.ENOVA_KERNEL_MFMA), "H=300 L=16"),
+                                       (dict(hidden=1100, kernel=binding.ENOVA_KERNEL_VALU), "hidden width 1100")])
+def test_unsupported_shapes_are_named_in_the_error(over, text):
+    """Shapes no kernel takes are refused on the host before any device call, and the message
+    names the shape (it is formatted before the half-built detector is released)."""
+    _ensure_built()
+    st, h = _init_status(**over)
+    assert st == binding.ENOVA_EUNSUPPORTED and not h
+    assert text in binding.lib().enova_last_error().decode()
+
+
 def test_null_arguments_are_rejected():
     _ensure_built()
     L = binding.lib()

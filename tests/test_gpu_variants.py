@@ -57,7 +57,13 @@ def _check(g, ref, dtype, what, idx=None):
                                         kind="ar1_spikes"),
                                    dict(metrics=32, window=5, stride=1, hidden=48, latent=16, act="relu"),
                                    # the detector's c5 window shape (M = 16, D = 1024)
-                                   dict(metrics=16, window=64, stride=1, hidden=32, latent=16, act="relu")])
+                                   dict(metrics=16, window=64, stride=1, hidden=32, latent=16, act="relu"),
+                                   # fused single-launch shapes with strides above one: 128 hidden
+                                   # units with tanh and 8 metrics; a partial last super-row
+                                   # (W = 14, S = 3); 4 metrics (both lane halves on one chunk)
+                                   dict(metrics=8, window=16, stride=2, hidden=100, latent=10, act="tanh"),
+                                   dict(metrics=16, window=14, stride=3, hidden=64, latent=16, act="relu"),
+                                   dict(metrics=4, window=24, stride=3, hidden=128, latent=8, act="relu")])
 def test_variants_match_oracle(norm, shape):
     cfg = wl.CONFIGS["c1"].replace(n_streams=5, t_len=0, t_min=20, t_max=900, **{"kind": "ragged_mix", **shape})
     w = wl.make_weights(cfg, bias_scale=0.1)
