@@ -68,11 +68,12 @@ def kernel_source_hash(kernel="k_score_mfma") -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(cfg):
-    """HBM bytes per launch of the workload's scoring kernel from the committed rocprofv3 counter
-    summary (profiles/<kernel>_<workload>_counters.txt, read from a file, not measured in this run),
-    if it still describes the current kernel source (else None)."""
-    path = os.path.join(ROOT, "profiles", f"{score_kernel_name(cfg)[2:]}_{cfg.name}_counters.txt")
+def load_traffic(cfg, kernel=None):
+    """HBM bytes per launch of a workload's kernel (default: its scoring kernel) from the committed
+    rocprofv3 counter summary (profiles/<kernel>_<workload>_counters.txt, read from a file, not
+    measured in this run), if it still describes the current kernel source (else None)."""
+    kernel = kernel or score_kernel_name(cfg)
+    path = os.path.join(ROOT, "profiles", f"{kernel[2:]}_{cfg.name}_counters.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -81,7 +82,7 @@ def load_traffic(cfg):
             if "=" in line and not line.startswith("#"):
                 k, v = line.strip().split("=", 1)
                 kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_sha") != kernel_source_hash(score_kernel_name(cfg)):
+    if kv.get("kernel_source_sha") != kernel_source_hash(kernel):
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -650,6 +651,7 @@ def variants_main(args, cfg):
 
     def step():
         binding.enova_detect_score_ext(det.handle, x, so, wo, work.n_streams, N, None, None, norm, sc, md, mdm, rec)
+    kernel = "k_ext_fused" if det.ext_fused() else "chunked"
     for _ in range(args.warmup):
         step()
     binding.enova_detect_set_timing(det.handle, True)
@@ -665,9 +667,17 @@ def variants_main(args, cfg):
     ev1.record(stream)
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / args.steps
+    if args.copy_probe_gib > 0:
+        # a device copy of known size, the scale of the HBM byte counters
+        a = torch.empty(int(args.copy_probe_gib * (1 << 30)) // 4, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
     km = float(np.mean(k_ms))
     fpw = variants_flops_per_window(cfg)
     achieved = fpw * N / (km / 1e3) / 1e12
+    fused = kernel == "k_ext_fused"
     out = {
         "metric": "windows evaluated/sec (KL score, md, per-metric md vector, reconstruction error)",
         "value": round(N / (ms / 1e3), 1), "unit": "windows/s", "n_gpus": 1, "steps": args.steps,
@@ -678,8 +688,14 @@ def variants_main(args, cfg):
                                f"S={cfg.stride}, H={cfg.hidden}, {cfg.dtype} ({N} windows), {args.norm} normalisation",
                    "windows": N},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_TFLOPS["f32"], "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_TFLOPS["f32"], 4), "traffic": None,
-                     "kernel": "the whole variant pass (staging, 4 products, latent, reductions)",
+                     "frac": round(achieved / PEAK_TFLOPS["f32"], 4),
+                     "traffic": load_traffic(cfg, kernel) if fused else None,
+                     "traffic_source": (f"profiles/{kernel[2:]}_{cfg.name}_counters.txt (rocprofv3 FETCH_SIZE + "
+                                        "WRITE_SIZE, read from the file when its kernel source hash matches; null "
+                                        "otherwise)") if fused else None,
+                     "kernel": (kernel + " (one launch: staging, per-window statistics, encoder, heads, decoder, "
+                                "reductions; timed with its tile scan and map)") if fused else
+                               "the chunked variant pass (staging, 4 products, latent, reductions)",
                      "kernel_ms": round(km, 4), "flops_per_window": fpw, "windows_per_launch": N},
     }
     if not args.no_cpu_baseline:

@@ -328,9 +328,9 @@ enova_status enova_train_kernel_times(enova_trainer t, double *gemm_ms, double *
 enova_status enova_train_destroy(enova_trainer t);
 
 /*
- * Detector-output variants (Section IV-B). The windows are evaluated densely, in chunks: each is
- * normalised against its stream's reference statistics (ENOVA_NORM_REFERENCE, as
- * enova_detect_score) or against itself (ENOVA_NORM_WINDOW: per metric the window's own mean and
+ * Detector-output variants (Section IV-B). Every window is normalised against its stream's
+ * reference statistics (ENOVA_NORM_REFERENCE, as enova_detect_score) or against itself
+ * (ENOVA_NORM_WINDOW: per metric the window's own mean and
  * population std, a std <= 1e-6 max(1, |mean|) counting as 1 -- the literal reading of
  * per-window normalisation); then the encoder, the KL score, and the decoder's full output
  * m' = Wd2 act(Wd1 mu + bd1) + bd2 at z = mu. Per window: out_scores (the KL score),
@@ -338,6 +338,8 @@ enova_status enova_train_destroy(enova_trainer t);
  * metric, out_recon_err = mean_j (v_j - m'_j)^2 (device outputs; any may be NULL; with the last
  * three NULL the decoder is not evaluated). ref_mean /
  * ref_std as in enova_detect_score (NULL: computed; ignored for ENOVA_NORM_WINDOW). M <= 4096.
+ * enova_detect_ext_mode tells whether a detector's windows take one fused launch or are
+ * evaluated in chunks.
  * The products run in fp32 on the matrix cores (x and W1 of a bf16 detector are bf16 values;
  * v is rounded to bf16 as in enova_detect_score). Asynchronous. Errors: EINVAL, EUNSUPPORTED,
  * ENOMEM, EHIP.
@@ -352,6 +354,14 @@ enova_status enova_detect_score_ext(enova_detector det, const void *x, const int
 /* With timing enabled (enova_detect_set_timing), the last enova_detect_score_ext call's duration
  * from its first to its last kernel, milliseconds. */
 enova_status enova_detect_ext_time(enova_detector det, double *ms);
+
+/* How enova_detect_score_ext evaluates this detector's windows (fixed at init): *fused = 1 for
+ * one launch per call that stages each tile's raw steps once and keeps every window's v, hidden
+ * layers and decoder output on chip (fp32 detectors of 4, 8 or 16 metrics, at most 128 hidden
+ * units -- 64 with tanh and 16 metrics --, at most 16 latent units, W*M a multiple of 32, and a
+ * tile that fits half a compute unit's LDS); 0 for the chunked evaluation of normalised windows
+ * in device memory. Errors: EINVAL. */
+enova_status enova_detect_ext_mode(enova_detector det, int32_t *fused);
 
 /*
  * Configuration scans (Section IV-A, Eqs. (4)-(6), Table II) over the same monitoring series.

@@ -28,7 +28,7 @@ EXPORTS = ["enova_detect_init", "enova_detect_destroy", "enova_detect_window_off
            "enova_stream_state", "enova_stream_kernel_times", "enova_stream_destroy",
            "enova_train_init", "enova_train_step", "enova_train_params_get", "enova_train_grads_get",
            "enova_train_set_timing", "enova_train_set_graph", "enova_train_kernel_times", "enova_train_destroy",
-           "enova_detect_score_ext", "enova_detect_ext_time", "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
+           "enova_detect_score_ext", "enova_detect_ext_time", "enova_detect_ext_mode", "enova_config_t_critical", "enova_config_init", "enova_config_destroy", "enova_config_window_offsets",
            "enova_config_scan", "enova_config_recommend", "enova_config_set_timing", "enova_config_kernel_time",
            "enova_detect_score_noalloc", "enova_status_str", "enova_last_error"]
 
@@ -117,6 +117,7 @@ def lib():
     L.enova_train_destroy.argtypes = [P]
     L.enova_detect_score_ext.argtypes = [P, P, P, P, I32, I64, P, P, I32, P, P, P, P, P]
     L.enova_detect_ext_time.argtypes = [P, P]
+    L.enova_detect_ext_mode.argtypes = [P, P]
     L.enova_config_t_critical.argtypes = [D, I32, P]
     L.enova_config_init.argtypes = [ctypes.POINTER(enova_config_params), ctypes.POINTER(P)]
     L.enova_config_destroy.argtypes = [P]
@@ -368,6 +369,12 @@ def enova_detect_ext_time(handle):
     return v.value
 
 
+def enova_detect_ext_mode(handle):
+    v = ctypes.c_int32()
+    _check(lib().enova_detect_ext_mode(ctypes.c_void_p(handle), ctypes.byref(v)), "enova_detect_ext_mode")
+    return v.value
+
+
 def enova_config_t_critical(alpha, dof):
     v = ctypes.c_double()
     _check(lib().enova_config_t_critical(float(alpha), int(dof), ctypes.byref(v)), "enova_config_t_critical")
@@ -476,6 +483,9 @@ class Detector:
     @property
     def kernel_kind(self):
         return {1: "valu", 2: "mfma"}[enova_detect_kernel_kind(self.handle)]
+
+    def ext_fused(self):
+        return enova_detect_ext_mode(self.handle) == 1
 
     def window_offsets(self, stream_offsets_host):
         return enova_detect_window_offsets(self.handle, stream_offsets_host)

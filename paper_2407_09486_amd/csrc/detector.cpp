@@ -1451,6 +1451,14 @@ enova_status enova_detect_kernel_times(enova_detector det, double *score_ms, dou
     return ENOVA_OK;
 }
 
+enova_status enova_detect_ext_mode(enova_detector det, int32_t *fused)
+{
+    if (!det || !fused)
+        return fail(ENOVA_EINVAL, "NULL argument");
+    *fused = det->wd2p ? 1 : 0;
+    return ENOVA_OK;
+}
+
 enova_status enova_detect_kernel_kind(enova_detector det, int32_t *kind)
 {
     if (!det || !kind)

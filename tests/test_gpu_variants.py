@@ -76,6 +76,26 @@ def test_variants_match_oracle(norm, shape):
     _check(g, ref, "f32", f"{norm} {shape}")
 
 
+@pytest.mark.parametrize("name,over,fused", [
+    ("c5", {}, True),                                            # M = 16, H = 128, ReLU
+    ("c2", {}, True),                                            # M = 8, H = 64
+    ("c1", dict(metrics=8, window=16, stride=2, hidden=100, latent=10, act="tanh"), True),
+    ("c1", dict(metrics=16, window=16, hidden=100, act="tanh"), False),   # tanh, 128 units, 16 metrics
+    ("c1", dict(metrics=5, window=32), False),                  # 5 metrics
+    ("c3", {}, False),                                           # a 256-window tile exceeds half the LDS
+    ("c4", {}, False),                                           # bf16 detector
+])
+def test_variant_evaluation_mode(name, over, fused):
+    """Which shapes take the fused single launch (the rest are evaluated in chunks); both kinds are
+    checked against the oracle above."""
+    cfg = wl.CONFIGS[name].replace(**over)
+    det = detector(cfg, wl.make_weights(cfg), "mfma")
+    try:
+        assert det.ext_fused() == fused
+    finally:
+        det.close()
+
+
 @pytest.mark.parametrize("window", [16, 32])
 @pytest.mark.parametrize("norm", ["reference", "window"])
 def test_variants_bf16_detector(norm, window):
@@ -107,16 +127,21 @@ def test_reference_variants_agree_with_the_batch_path():
     det.close()
 
 
-def test_windows_across_chunks_and_constant_metrics():
-    """More windows than one chunk (2^28 / D = 65536 windows for D = 512 x 8): windows on both
-    sides of every chunk boundary, and a metric that is constant inside some windows (the
-    per-window guard)."""
-    cfg = wl.CONFIGS["c1"].replace(n_streams=3, t_len=30000, window=512)
+@pytest.mark.parametrize("hidden,fused", [(32, True), (200, False)])
+def test_windows_across_chunks_and_constant_metrics(hidden, fused):
+    """More windows than one chunk of the chunked evaluation (2^28 / D = 65536 windows for
+    D = 512 x 8; 200 hidden units keep the detector off the fused kernel): windows on both sides
+    of every chunk boundary, and a metric that is constant inside some windows (the per-window
+    guard), on both evaluations."""
+    cfg = wl.CONFIGS["c1"].replace(n_streams=3, t_len=30000, window=512, hidden=hidden)
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg)
     xv = work.x.copy()
     xv[1000:1700, 3] = 2.5                           # constant inside windows 1000..1188 of stream 0
     work = wl.from_arrays(cfg, xv, work.stream_offsets)
+    det = detector(cfg, w, "mfma")
+    assert det.ext_fused() == fused
+    det.close()
     for norm in ("window", "reference"):
         g, woff = _run(cfg, w, work, norm)
         N = int(woff[-1])
@@ -132,11 +157,15 @@ def test_windows_across_chunks_and_constant_metrics():
 
 
 def test_short_last_chunk_splits_its_products():
-    """65536 + 300 windows of D = 512 x 8 (chunks of 65536): the last chunk's encoder product has
-    few output tiles and splits its reduction; its windows must match the oracle like the others."""
-    cfg = wl.CONFIGS["c1"].replace(n_streams=1, t_len=65536 + 300 + 511, window=512)
+    """65536 + 300 windows of D = 512 x 8 (chunks of 65536) on the chunked evaluation (200 hidden
+    units): the last chunk's encoder product has few output tiles and splits its reduction; its
+    windows must match the oracle like the others."""
+    cfg = wl.CONFIGS["c1"].replace(n_streams=1, t_len=65536 + 300 + 511, window=512, hidden=200)
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg)
+    det = detector(cfg, w, "mfma")
+    assert not det.ext_fused()
+    det.close()
     g, woff = _run(cfg, w, work, "window")
     N = int(woff[-1])
     assert N == 65536 + 300
@@ -147,11 +176,13 @@ def test_short_last_chunk_splits_its_products():
     _check(g, ref, "f32", "short last chunk", idx=np.asarray(glob))
 
 
-def test_scores_only_skip_the_decoder():
-    """With md, md_m and the error all NULL the decoder products are skipped; the scores are the
-    same kernels' output, so they match a full call bit for bit. No windows: nothing to do."""
+@pytest.mark.parametrize("hidden", [64, 200])
+def test_scores_only_skip_the_decoder(hidden):
+    """With md, md_m and the error all NULL the decoder is skipped (fused kernel with 64 hidden
+    units, chunked evaluation with 200); the scores are the same kernels' output, so they match a
+    full call bit for bit. No windows: nothing to do."""
     import torch
-    cfg = wl.CONFIGS["c2"].replace(n_streams=3, t_len=2000)
+    cfg = wl.CONFIGS["c2"].replace(n_streams=3, t_len=2000, hidden=hidden)
     w = wl.make_weights(cfg, bias_scale=0.1)
     work = wl.generate(cfg)
     det = detector(cfg, w, "mfma")
@@ -172,8 +203,8 @@ def test_scores_only_skip_the_decoder():
 
 def test_variants_full_size_sampled():
     """The benchmarked workload (c5, per-window normalisation, every output) at its real size,
-    launched as bench.py launches it; sampled windows (random ones, stream edges and both sides
-    of every chunk boundary) against the oracle."""
+    launched as bench.py launches it (one fused launch); sampled windows (random ones, stream
+    edges, tile edges of the chunked evaluation's chunks) against the oracle."""
     import torch
     from test_gpu_fullsize import _sample, _sub_workload
     cfg = wl.CONFIGS["c5"]
@@ -186,7 +217,7 @@ def test_variants_full_size_sampled():
     log(f"variants full size: {N} windows")
     sc, md, mdm, rec = det.score_ext(x, so, torch.from_numpy(woff).cuda(), N, norm="window")
     g, s, k = _sample(woff, 128, np.random.default_rng(7), n_random=500, n_streams=20)
-    chunk = (1 << 28) // cfg.d                       # windows per chunk of the variant pass
+    chunk = (1 << 28) // cfg.d                       # windows per chunk of the chunked evaluation
     edges = [e for c in range(chunk, N, chunk) for e in (c - 1, c)]
     g = np.array(sorted(set(g.tolist()) | set(edges)), np.int64)
     s = np.searchsorted(woff, g, side="right") - 1
