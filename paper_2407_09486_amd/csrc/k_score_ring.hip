@@ -9,10 +9,11 @@
 //    blocks): 32 matrix ops per 32-deep reduction step, A = W1 fragments streamed from L2,
 //    B = window fragments from LDS.
 //  * The window is cut into Q super-rows of S steps (as in k_score_mfma); window n at reduction
-//    super-row q reads tile super-row n + q. The LDS holds a ring of R >= 130 super-rows (R a
-//    multiple of 8) instead of all 127 + Q of them: before the loop the first 129 are staged;
-//    during super-row step q one wave loads, normalises and writes super-row q + 129 into the
-//    slot of a super-row no window reads any more, and one barrier per step publishes it.
+//    super-row q reads tile super-row n + q. The LDS holds a ring of R >= 136 super-rows (R a
+//    multiple of 8) instead of all 127 + Q of them: before the loop the first 130 are staged;
+//    during super-row step q one wave loads, normalises and writes super-row q + 130 (first read
+//    two steps later) into the slot of a super-row no window reads any more, and a barrier after
+//    every second step publishes it.
 //    That keeps a block's LDS under half a compute unit's, so two blocks run per compute unit
 //    and one block's staging and epilogue overlap the other's matrix work.
 //  * Chunk c (16 bytes, 8 bf16) of tile super-row r, held in ring slot r mod R, lives at
@@ -58,7 +59,7 @@ struct RingShape {
     int M, S, Mp, Q, CPR;
     int P;            // LDS chunks per ring slot (multiple of 16)
     int KS;           // reduction steps per super-row: P / 4 (a multiple of kPd)
-    int R;            // ring slots (multiple of 8, >= kRingNb + 2)
+    int R;            // ring slots (multiple of 8, >= kRingNb + 8)
     int SMp;          // elements of a super-row: S * Mp = 8 * CPR
     int tail_elems;   // elements of a window's last super-row that belong to the window
     int rs_rows;      // entries of the row-sum arrays: kRingNb + Q + 1
@@ -260,17 +261,17 @@ __global__ __launch_bounds__(kNT, 2) void k_score_ring(ScoreParams p, RingShape 
     };
 
     const int rows_need = nv + Q - 1;            // tile super-rows any valid window reads
-    // ---- stage super-rows 0 .. kRingNb into slots 0 .. kRingNb, every load of a thread in flight
+    // ---- stage super-rows 0 .. kRingNb + 1 into slots 0 .. kRingNb + 1, every load of a thread in flight
     // at once (one HBM round trip for the usual shapes); the super-rows the loop streams in later
     // are touched once per 128-byte line meanwhile, so their loads hit L2
     {
         constexpr int SU = 20;
-        const int n_chunks = (kRingNb + 1) * P;
+        const int n_chunks = (kRingNb + 2) * P;
         const int lines_per_row = P / 8;
-        const int n_pre = rows_need > kRingNb + 1 ? (rows_need - kRingNb - 1) * lines_per_row : 0;
+        const int n_pre = rows_need > kRingNb + 2 ? (rows_need - kRingNb - 2) * lines_per_row : 0;
         float sink = 0.0f;
         for (int i = tid; i < n_pre; i += kNT) {
-            const int r = kRingNb + 1 + i / lines_per_row;
+            const int r = kRingNb + 2 + i / lines_per_row;
             const int64_t e0 = (static_cast<int64_t>(r) * CPR + (i % lines_per_row) * 8) * 8;
             if (e0 < eavail)
                 sink += load_x<ENOVA_BF16>(p.x, ebase + e0);
@@ -298,7 +299,7 @@ __global__ __launch_bounds__(kNT, 2) void k_score_ring(ScoreParams p, RingShape 
         asm volatile("" ::"v"(sink));          // keeps the line touches (their values are not used)
     }
     __syncthreads();
-    for (int r = wave; r <= kRingNb; r += kRingWaves) {
+    for (int r = wave; r <= kRingNb + 1; r += kRingWaves) {
         uint4 q = make_uint4(0, 0, 0, 0);
         if (lane < P)
             q = ring[r * P + (lane ^ ring_key(r))];
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(kNT, 2) void k_score_ring(ScoreParams p, RingShape 
             }
         };
         int sl0 = col;                            // ring slot of tile super-row col + q
-        int sn = kRingNb + 1;                     // ring slot of this step's new super-row q + kRingNb + 1
+        int sn = kRingNb + 2;                     // ring slot of this step's new super-row q + kRingNb + 2
         int xo = ring_key(col);                   // XOR key of every block's super-row 16 nb + col + q
         offsets(sl0, bofs);
 #pragma unroll
@@ -383,7 +384,7 @@ __global__ __launch_bounds__(kNT, 2) void k_score_ring(ScoreParams p, RingShape 
             bq[nb] = ring[bofs[nb] + (grp ^ xo)];
         for (int q = 0; q < Q; ++q) {
             // this step's new super-row: wave q % 4 loads it now and writes it after the matrix work
-            const int rn = q + kRingNb + 1;
+            const int rn = q + kRingNb + 2;
             const bool stager = (q & (kRingWaves - 1)) == wave && rn < rows_need;
             // the stager's per-lane values are recomputed from an opaque copy of the lane index,
             // so they are not kept live (or spilled) across the matrix work
@@ -438,7 +439,12 @@ __global__ __launch_bounds__(kNT, 2) void k_score_ring(ScoreParams p, RingShape 
             xo = xo1;
             offsets(sl0, bofs);
             sn = sn + 1 == R ? 0 : sn + 1;
-            lds_barrier();
+            // a barrier after every odd step (and the last): the super-row staged at step q is first
+            // read in step q + 2 (by the next-fragment read of its last reduction step), and one of
+            // q, q + 1 is odd; the slot it overwrites was last read in step q - 6, and no wave runs
+            // more than three steps ahead of another
+            if ((q & 1) || q == Q - 1)
+                lds_barrier();
         }
     };
     auto go = [&](auto nba_tag) {
