@@ -77,7 +77,7 @@ struct enova_detector_s {
     void *stream_w = nullptr;     // streaming kernel: W1, heads and decoder fragments (one allocation)
     const uint4 *w1s = nullptr;
     const float *whs = nullptr, *wds = nullptr;
-    void *ext_w = nullptr;        // fused variant pass: decoder-output fragments (Wd2, bd2)
+    void *ext_w = nullptr;        // fused variant pass: decoder-output fragments of Wd2
     const float4 *wd2p = nullptr;
     void *w1t = nullptr;          // [D][H] transposed W1
     float *small = nullptr;       // every small weight array, one allocation
@@ -111,7 +111,7 @@ struct enova_detector_s {
     float *dense = nullptr;
     float *d_w1 = nullptr, *d_wml = nullptr, *d_bml = nullptr, *d_wd1 = nullptr, *d_wd2 = nullptr,
           *d_bd2 = nullptr;
-    // workspace of the output variants (one chunk of windows)
+    // workspace of the output variants (one chunk of windows; the fused pass's tile scan and map)
     float *ext_ws = nullptr;
     size_t ext_ws_cap = 0;        // floats
     // timing

@@ -98,6 +98,8 @@ def test_null_arguments_are_rejected():
     assert L.enova_detect_score(None, None, None, None, 0, 0, None, None, 0.0, None, None, None,
                                 None) == binding.ENOVA_EINVAL
     assert L.enova_detect_destroy(None) == binding.ENOVA_OK
+    mode = ctypes.c_int32()
+    assert L.enova_detect_ext_mode(None, ctypes.byref(mode)) == binding.ENOVA_EINVAL
     thr = ctypes.c_float()
     assert L.enova_detect_threshold(None, None, None, None, 1, 1, 0.98, 1e-3, ctypes.byref(thr), None,
                                     None, None) == binding.ENOVA_EINVAL
