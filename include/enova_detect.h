@@ -235,13 +235,19 @@ enova_status enova_stream_create(enova_detector det, int32_t n_streams, const fl
  *                (as it stood before this score)
  *   out_due      HOST int32 or NULL: 1 if this push scored windows, else 0 (then nothing is
  *                written to the device outputs)
- * Asynchronous on `stream`. Errors: EINVAL, EHIP.
+ * Asynchronous on `stream`. The threshold update and the refit of the streams that took a new
+ * peak run on a stream of the set's own (default priority), ordered by events: the update after
+ * this push's scores, later work on `stream` after the update (its flags are then written), the
+ * next push's update and any enova_stream_state after the refit. The refit thus overlaps the
+ * next push's append and scoring, and every push and state read sees the thresholds in push
+ * order.
+ * Errors: EINVAL, EHIP.
  */
 enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_scores, float *out_md,
                                uint8_t *out_flags, int32_t *out_due, hipStream_t stream);
 
-/* Per-stream SPOT state into HOST arrays [n] (each may be NULL): t, z, n, stored peaks.
- * Synchronises `stream`. */
+/* Per-stream SPOT state into HOST arrays [n] (each may be NULL): t, z, n, stored peaks, after
+ * the last push's refit. Synchronises `stream`. */
 enova_status enova_stream_state(enova_stream s, double *t, double *z, int64_t *n, int32_t *n_peaks,
                                 hipStream_t stream);
 

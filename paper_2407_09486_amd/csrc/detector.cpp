@@ -1483,6 +1483,13 @@ struct enova_stream_s {
     SpotState spot{};
     hipEvent_t ev[3] = {nullptr, nullptr, nullptr};   // score start, score end / spot start, spot end
     bool timed = false;           // the last scoring push recorded ev
+    // the threshold update and the refit run on the set's own stream (default priority), so a
+    // push's refit overlaps the next push's append and scoring: the update waits for the push's
+    // scores (score_ev), `stream` waits for the update (upd_ev: flags written, scores read), and
+    // a state read waits for the refit (fit_ev)
+    hipStream_t fit_stream = nullptr;
+    hipEvent_t score_ev = nullptr, upd_ev = nullptr, fit_ev = nullptr;
+    bool fit_pending = false;
 };
 
 namespace {
@@ -1500,6 +1507,14 @@ void free_stream(enova_stream s)
     for (hipEvent_t e : s->ev)
         if (e)
             (void)hipEventDestroy(e);
+    if (s->score_ev)
+        (void)hipEventDestroy(s->score_ev);
+    if (s->upd_ev)
+        (void)hipEventDestroy(s->upd_ev);
+    if (s->fit_ev)
+        (void)hipEventDestroy(s->fit_ev);
+    if (s->fit_stream)
+        (void)hipStreamDestroy(s->fit_stream);
     delete s;
 }
 
@@ -1562,7 +1577,7 @@ enova_status enova_stream_create(enova_detector det, int32_t n, const float *ref
         (st = dev_alloc(&s->spot.npk, n)) != ENOVA_OK ||
         (st = dev_alloc(&s->spot.peaks, static_cast<size_t>(n) * peak_cap)) != ENOVA_OK ||
         (st = dev_alloc(&s->spot.mark, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.err, 1)) != ENOVA_OK ||
-        (st = dev_alloc(&s->spot.list, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.count, 1)) != ENOVA_OK ||
+        (st = dev_alloc(&s->spot.list, n)) != ENOVA_OK || (st = dev_alloc(&s->spot.count, 2)) != ENOVA_OK ||
         (st = dev_alloc(&d_off, static_cast<size_t>(n) + 1)) != ENOVA_OK) {
         (void)hipFree(d_off);
         free_stream(s);
@@ -1574,6 +1589,7 @@ enova_status enova_stream_create(enova_detector det, int32_t n, const float *ref
         (e = hipMemcpyAsync(s->mean, ref_mean, nm * sizeof(float), hipMemcpyDeviceToDevice, stream)) != hipSuccess ||
         (e = hipMemcpyAsync(s->std, ref_std, nm * sizeof(float), hipMemcpyDeviceToDevice, stream)) != hipSuccess ||
         (e = hipMemsetAsync(s->spot.err, 0, sizeof(int), stream)) != hipSuccess ||
+        (e = hipMemsetAsync(s->spot.count, 0, 2 * sizeof(int), stream)) != hipSuccess ||
         (e = hipMemcpyAsync(d_off, calib_offsets, (static_cast<size_t>(n) + 1) * sizeof(int64_t),
                             hipMemcpyHostToDevice, stream)) != hipSuccess ||
         (e = launch_spot_init(n_cal > 0 ? calib_scores : s->scores, d_off, n, level, s->spot, stream)) != hipSuccess ||
@@ -1645,11 +1661,32 @@ enova_status enova_stream_push(enova_stream s, const void *x_step, float *out_sc
         return hip_fail(e, "streaming scoring kernel");
     if (timed)
         (void)hipEventRecord(s->ev[1], stream);
-    if ((e = launch_spot_update(p.scores, s->n, s->spot, out_flags, stream)) != hipSuccess ||
-        (e = launch_spot_fit(s->n, s->q, s->spot, false, stream)) != hipSuccess)
-        return hip_fail(e, "streaming threshold kernels");
+    if (!s->fit_stream) {
+        if ((e = hipStreamCreateWithFlags(&s->fit_stream, hipStreamNonBlocking)) != hipSuccess ||
+            (e = hipEventCreateWithFlags(&s->score_ev, hipEventDisableTiming)) != hipSuccess ||
+            (e = hipEventCreateWithFlags(&s->upd_ev, hipEventDisableTiming)) != hipSuccess ||
+            (e = hipEventCreateWithFlags(&s->fit_ev, hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "streaming refit stream");
+    }
+    // on the set's stream, behind the previous push's refit (whose thresholds it compares with,
+    // and whose peaks, counts and list it rewrites): this push's update, then its refit, which
+    // overlaps the next push's append and scoring on `stream`
+    if ((e = hipEventRecord(s->score_ev, stream)) != hipSuccess ||
+        (e = hipStreamWaitEvent(s->fit_stream, s->score_ev, 0)) != hipSuccess)
+        return hip_fail(e, "streaming threshold order");
+    s->spot.cur ^= 1;   // this push's list counter (cleared by the previous push's refit)
+    if ((e = launch_spot_update(p.scores, s->n, s->spot, out_flags, s->fit_stream)) != hipSuccess)
+        return hip_fail(e, "streaming threshold update");
+    if ((e = hipEventRecord(s->upd_ev, s->fit_stream)) != hipSuccess ||
+        (e = launch_spot_fit(s->n, s->q, s->spot, false, s->fit_stream)) != hipSuccess ||
+        (e = hipEventRecord(s->fit_ev, s->fit_stream)) != hipSuccess)
+        return hip_fail(e, "streaming refit");
     if (timed)
-        (void)hipEventRecord(s->ev[2], stream);
+        (void)hipEventRecord(s->ev[2], s->fit_stream);
+    // later work on `stream` sees this push's flags, and may overwrite the scores the update read
+    if ((e = hipStreamWaitEvent(stream, s->upd_ev, 0)) != hipSuccess)
+        return hip_fail(e, "streaming threshold order");
+    s->fit_pending = true;
     s->timed = timed;
     return ENOVA_OK;
 }
@@ -1662,6 +1699,8 @@ enova_status enova_stream_state(enova_stream s, double *t, double *z, int64_t *n
     DeviceGuard dg(s->det->device);
     const size_t k = static_cast<size_t>(s->n);
     hipError_t e = hipSuccess;
+    if (s->fit_pending && (e = hipStreamWaitEvent(stream, s->fit_ev, 0)) != hipSuccess)
+        return hip_fail(e, "streaming refit wait");
     if ((t && (e = hipMemcpyAsync(t, s->spot.t, k * sizeof(double), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
         (z && (e = hipMemcpyAsync(z, s->spot.z, k * sizeof(double), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
         (n && (e = hipMemcpyAsync(n, s->spot.cnt, k * sizeof(int64_t), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||

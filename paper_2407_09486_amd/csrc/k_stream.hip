@@ -524,7 +524,7 @@ __global__ __launch_bounds__(256) void k_spot_update(const float *__restrict__ s
                 st.peaks[static_cast<int64_t>(s) * st.cap + np] = xd - t;
                 st.npk[s] = np + 1;
                 st.mark[s] = 1;
-                st.list[atomicAdd(st.count, 1)] = s;
+                st.list[atomicAdd(st.count + st.cur, 1)] = s;
             }
         }
     }
@@ -895,11 +895,14 @@ __global__ __launch_bounds__(kFitThreads) void k_spot_fit_all(double q, SpotStat
 }
 
 // The streams the last update listed, one block each (a grid of one block per stream, the blocks
-// past the list's length leaving at once).
+// past the list's length leaving at once). The next push's update counts in the other counter,
+// which block 0 clears (no block of this launch reads it).
 __global__ __launch_bounds__(kFitThreads) void k_spot_fit_list(double q, SpotState st)
 {
     __shared__ FitShared sh;
-    if (static_cast<int>(blockIdx.x) < *st.count)
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        st.count[st.cur ^ 1] = 0;
+    if (static_cast<int>(blockIdx.x) < st.count[st.cur])
         spot_fit_stream(sh, st.list[blockIdx.x], q, st);
 }
 
@@ -974,9 +977,6 @@ hipError_t launch_spot_update(const float *scores, int n, const SpotState &s, ui
 {
     if (n <= 0)
         return hipSuccess;
-    hipError_t e = hipMemsetAsync(s.count, 0, sizeof(int), st);
-    if (e != hipSuccess)
-        return e;
     hipLaunchKernelGGL(k_spot_update, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, st,
                        scores, n, s, flags);
     return hipGetLastError();

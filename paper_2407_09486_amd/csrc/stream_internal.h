@@ -62,7 +62,9 @@ struct SpotState {
     uint8_t *mark;               // 1: z must be refitted
     int *err;                    // set to 1 if a stream's calibration peaks exceed cap
     int *list;                   // [n]: streams that took a new peak in this push (any order)
-    int *count;                  // entries of list (cleared before each update)
+    int *count;                  // [2]: entries of list, alternating between pushes: a push's update
+                                 // counts in count[cur], its refit reads that and clears the other
+    int cur;                     // this push's counter (0 or 1)
 };
 hipError_t launch_spot_init(const float *cal, const int64_t *cal_off, int n, double level,
                             const SpotState &s, hipStream_t st);
