@@ -762,12 +762,17 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                 if (br && b_at < kFitMaxBrackets) {
                     const double x0 = sh.xs[i], x1 = sh.xs[i + 1];
                     const double wi = sh.sa[i], wn = sh.sa[i + 1];
-                    sh.blo[b_at] = x0 < x1 ? x0 : x1;
-                    sh.bhi[b_at] = x0 < x1 ? x1 : x0;
+                    const double lo = x0 < x1 ? x0 : x1, hi = x0 < x1 ? x1 : x0;
+                    sh.blo[b_at] = lo;
+                    sh.bhi[b_at] = hi;
                     sh.bneg[b_at] = x0 < x1 ? (wi < 0.0) : (wn < 0.0);
                     sh.bdone[b_at] = 0;
                     sh.bround[b_at] = 0;
                     sh.broot[b_at] = 0.0;
+                    // the first point: the secant of w through the bracket's ends (the grid has w
+                    // there), else the midpoint
+                    const double xsec = x0 - wi * (x1 - x0) / (wn - wi);
+                    sh.bx[b_at] = xsec > lo && xsec < hi ? xsec : 0.5 * (lo + hi);
                 }
                 if (tid == 0) {
                     sh.nroots = nr < 2 * kFitMaxBrackets ? nr : 2 * kFitMaxBrackets;
@@ -776,13 +781,12 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                 __syncthreads();
             }
             // Newton's method on w inside each bracket: one wave per open bracket evaluates w and
-            // w' at the bracket's current point over all peaks (lane l sums the peaks l, l + 64,
-            // ..., a butterfly adds the lanes), and its lane 0 keeps the bracket on the sign of w,
-            // taking the Newton step when it lands strictly inside and the midpoint otherwise. A
-            // bracket ends at an exact zero of w, when the step falls to 4 ulp of the point, when
-            // the bracket can no longer be split, or after kFitRounds evaluations.
-            if (tid < sh.nbr)
-                sh.bx[tid] = 0.5 * (sh.blo[tid] + sh.bhi[tid]);
+            // w' at the bracket's current point (first the secant point of the grid values) over
+            // all peaks (lane l sums the peaks l, l + 64, ..., a butterfly adds the lanes), and
+            // its lane 0 keeps the bracket on the sign of w, taking the Newton step when it lands
+            // strictly inside and the midpoint otherwise. A bracket ends at an exact zero of w,
+            // when the step falls to 4 ulp of the point, when the bracket can no longer be split,
+            // or after kFitRounds evaluations.
             for (;;) {
                 if (tid == 0) {
                     sh.nbatch = 0;
