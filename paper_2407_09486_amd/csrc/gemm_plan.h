@@ -195,6 +195,24 @@ inline int64_t train_gemm_workspace(int B, int D, int H, int L)
     return ws;
 }
 
+// The step's four weight-gradient products (both operands row-contiguous, k = B) leave their
+// slice partials for the Adam step to sum, so each has a workspace region of its own:
+// which = 0 dWd2 (D x H), 1 dWd1 (H x L), 2 the heads' [dWmu; dWlv] (2L x H), 3 dW1 (H x D).
+constexpr int kTrainGradProducts = 4;
+inline void train_grad_shape(int B, int D, int H, int L, int which, int &m, int &n, int &k)
+{
+    const int shapes[kTrainGradProducts][2] = {{D, H}, {H, L}, {2 * L, H}, {H, D}};
+    m = shapes[which][0];
+    n = shapes[which][1];
+    k = B;
+}
+inline int64_t train_grad_workspace(int B, int D, int H, int L, int which)
+{
+    int m, n, k;
+    train_grad_shape(B, D, H, L, which, m, n, k);
+    return std::max(gemm_workspace_floats(m, n, k), gemm_rs_workspace_floats(m, n, k, false, false));
+}
+
 // ---------------------------------------------------------------------------------------------
 // Variant pass: windows are evaluated densely in chunks of `variants_chunk` rows, the last chunk
 // shorter. Its four products per chunk (rows x H x D encoder, rows x 2L x H heads, rows x H x L

@@ -870,16 +870,21 @@ __global__ __launch_bounds__(1024) void k_beta(const float *__restrict__ kl, con
         b = b < beta_min ? beta_min : (b > beta_max ? beta_max : b);
         st[0] = static_cast<float>(integ);
         beta_out[0] = static_cast<float>(b);
-        const long long k_adam = step[0] + 1;
-        step[0] = k_adam;
-        corr[0] = static_cast<float>(1.0 / (1.0 - pow(static_cast<double>(b1), static_cast<double>(k_adam))));
-        corr[1] = static_cast<float>(1.0 / (1.0 - pow(static_cast<double>(b2), static_cast<double>(k_adam))));
         if (info) {
             info[0] = static_cast<float>(-(s_la - b * s_kn) / rows);
             info[1] = static_cast<float>(s_lp / rows);
             info[2] = static_cast<float>(mkl);
             info[3] = static_cast<float>(b);
         }
+    } else if (threadIdx.x == 64 || threadIdx.x == 65) {
+        // the Adam step count and its two bias corrections, in a second wave beside the
+        // controller (both lanes take one pow together; the count is read before lane 64 stores it)
+        const int c = static_cast<int>(threadIdx.x) - 64;
+        const long long k_adam = step[0] + 1;
+        const double bc = static_cast<double>(c == 0 ? b1 : b2);
+        corr[c] = static_cast<float>(1.0 / (1.0 - pow(bc, static_cast<double>(k_adam))));
+        if (c == 0)
+            step[0] = k_adam;
     }
 }
 
@@ -904,14 +909,56 @@ __global__ __launch_bounds__(256) void k_latent_grad(const float *__restrict__ g
     }
 }
 
-__global__ __launch_bounds__(256) void k_adam(float *__restrict__ p, const float *__restrict__ g,
+// Adam on every flat parameter. An entry inside one of the `sums` ranges first adds its
+// gradient's slices in slice order and stores the result in g; every other entry reads g. The
+// slices are loaded 16 at a time while 16 remain, then 8 at a time, so a thin product's 64
+// slices take four round trips to memory.
+__global__ __launch_bounds__(256) void k_adam(float *__restrict__ p, float *__restrict__ g,
                                               float *__restrict__ m, float *__restrict__ v, int64_t total,
                                               float lr, float b1, float b2, float eps,
-                                              const float *__restrict__ corr)
+                                              const float *__restrict__ corr, GradSums sums)
 {
     const float c1 = corr[0], c2 = corr[1];
     for (int64_t e = blockIdx.x * 256LL + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
-        const float ge = g[e];
+        bool summed = false;
+        float ge = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kMaxGradSums; ++q) {
+            if (q >= sums.n)
+                break;
+            const int64_t i = e - sums.s[q].begin;
+            if (i < 0 || i >= sums.s[q].count)
+                continue;
+            const float *src = sums.s[q].src + i;
+            const int64_t stride = sums.s[q].stride;
+            const int splits = sums.s[q].splits;
+            int sp = 0;
+            for (; sp + 16 <= splits; sp += 16) {
+                float t[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u)
+                    t[u] = src[(sp + u) * stride];
+#pragma unroll
+                for (int u = 0; u < 16; ++u)
+                    ge += t[u];
+            }
+            for (; sp + 8 <= splits; sp += 8) {
+                float t[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    t[u] = src[(sp + u) * stride];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    ge += t[u];
+            }
+            for (; sp < splits; ++sp)
+                ge += src[sp * stride];
+            summed = true;
+        }
+        if (summed)
+            g[e] = ge;
+        else
+            ge = g[e];
         const float me = b1 * m[e] + (1.0f - b1) * ge;
         const float ve = b2 * v[e] + (1.0f - b2) * ge * ge;
         m[e] = me;
@@ -1052,8 +1099,13 @@ struct SumF {
 
 hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
                        int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
-                       int64_t work_floats, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1)
+                       int64_t work_floats, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, GemmSplit *defer)
 {
+    if (defer) {
+        *defer = GemmSplit{};
+        if (epi.kind != kEpiStore || ldc != n)
+            return hipErrorInvalidValue;
+    }
     if (m <= 0 || n <= 0)
         return hipSuccess;
     // each operand needs a unit stride along the reduction index or along its row index
@@ -1092,6 +1144,10 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
                 return e;
             if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess)
                 return e;
+            if (defer) {
+                *defer = GemmSplit{work, part_rows, rp.used};
+                return hipSuccess;
+            }
             const unsigned blocks = blocks_for(static_cast<int64_t>(m) * n + (rowsum ? m : 0));
             with_epilogue<SumF>(epi.kind, epi.act, blocks, st, static_cast<const float *>(work),
                                 static_cast<const float *>(part_rows), rp.used, m, n, C, ldc, rowsum, epp);
@@ -1121,6 +1177,10 @@ hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int6
         return e;
     if (ev1 && (e = hipEventRecord(ev1, st)) != hipSuccess)
         return e;
+    if (defer) {
+        *defer = GemmSplit{work, part_rows, used};
+        return hipSuccess;
+    }
     const unsigned blocks = blocks_for(static_cast<int64_t>(m) * n + (rowsum ? m : 0));
     with_epilogue<SumF>(epi.kind, epi.act, blocks, st, static_cast<const float *>(work),
                         static_cast<const float *>(part_rows), used, m, n, C, ldc, rowsum, epp);
@@ -1194,11 +1254,18 @@ hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, cons
     return hipGetLastError();
 }
 
-hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
-                       const float *corr, hipStream_t st)
+hipError_t launch_adam(float *p, float *g, float *m, float *v, int64_t total, const TrainHyper &h,
+                       const float *corr, const GradSums &sums, hipStream_t st)
 {
+    if (sums.n < 0 || sums.n > kMaxGradSums)
+        return hipErrorInvalidValue;
+    for (int q = 0; q < sums.n; ++q) {
+        const GradSum &r = sums.s[q];
+        if (r.begin < 0 || r.count < 0 || r.begin + r.count > total || r.splits < 1 || !r.src || r.stride < r.count)
+            return hipErrorInvalidValue;
+    }
     hipLaunchKernelGGL(k_adam, dim3(blocks_for(total)), dim3(256), 0, st, p, g, m, v, total, h.lr, h.b1, h.b2,
-                       h.eps, corr);
+                       h.eps, corr, sums);
     return hipGetLastError();
 }
 

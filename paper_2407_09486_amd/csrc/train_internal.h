@@ -37,12 +37,21 @@ struct GemmEpilogue {
     int ldv = 0;            // kEpiRowReduce: leading dimension of pre
     int groups = 0;         // kEpiRowReduce
 };
+// A split product's slice partials left for a later pass: part [splits][m][n] and rows
+// [splits][m] (NULL without row sums), in `work`; splits == 0 when the product did not split and
+// C (and rowsum) already hold the result.
+struct GemmSplit {
+    const float *part = nullptr, *rows = nullptr;
+    int splits = 0;
+};
 // ev0 / ev1 (or NULL) are recorded around the product kernel itself (not the slice sum).
 // `work` holds work_floats floats; a product splits only as far as they allow (none when work is
-// NULL).
+// NULL). With `defer` (a plain store into C with ldc == n only) a split product's slices are not
+// summed: *defer describes them, and C and rowsum are left untouched.
 hipError_t launch_gemm(const GemmEpilogue &epi, const float *A, int64_t ai, int64_t ak, const float *B, int64_t bk,
                        int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, float *work,
-                       int64_t work_floats, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                       int64_t work_floats, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
+                       GemmSplit *defer = nullptr);
 // ml: [rows][2L] = [mu | lv] per window (biases bml = [bmu | blv] added in place).
 hipError_t launch_latent(float *ml, const float *bml, const float *eps, float *sd, float *z, float *kl, int rows,
                          int L, hipStream_t st);
@@ -56,7 +65,22 @@ hipError_t launch_beta(const float *kl, const float *logp, const float *labels, 
 // gz: [rows][L] = dJ/dz; gml: [rows][2L] = [dJ/dmu | dJ/dlv].
 hipError_t launch_latent_grad(const float *gz, float *gml, const float *ml, const float *sd, const float *eps,
                               const float *labels, const float *beta, int rows, int L, hipStream_t st);
-hipError_t launch_adam(float *p, const float *g, float *m, float *v, int64_t total, const TrainHyper &h,
-                       const float *corr, hipStream_t st);
+// The gradient of the flat range [begin, begin + count) as the sum of a deferred product's slices:
+// g[begin + i] = sum over s = 0, 1, ..., splits - 1 (in order) of src[s * stride + i].
+struct GradSum {
+    int64_t begin, count;
+    const float *src;
+    int64_t stride;
+    int splits;
+};
+constexpr int kMaxGradSums = 2 * kTrainGradProducts;   // a weight and a bias range per product
+struct GradSums {
+    int n = 0;
+    GradSum s[kMaxGradSums] = {};
+};
+// One Adam step over the flat parameters; the ranges in `sums` first form their gradient from the
+// slices (and store it in g), every other entry of g is read as it is.
+hipError_t launch_adam(float *p, float *g, float *m, float *v, int64_t total, const TrainHyper &h,
+                       const float *corr, const GradSums &sums, hipStream_t st);
 
 }  // namespace enova

@@ -88,9 +88,28 @@ enova_status alloc_floats(float **dst, size_t n)
     return ENOVA_OK;
 }
 
+// Workspace of a step over B windows: the products whose slices are summed right away share the
+// first train_gemm_workspace floats; each weight-gradient product, whose slices the Adam step sums,
+// has a region of its own after them (off[1 + which], cap[1 + which]).
+struct StepWork {
+    int64_t off[1 + kTrainGradProducts], cap[1 + kTrainGradProducts], total;
+};
+StepWork step_work(const enova_trainer t, int B)
+{
+    StepWork w{};
+    w.cap[0] = train_gemm_workspace(B, t->D, t->H, t->L);
+    for (int q = 0; q < kTrainGradProducts; ++q)
+        w.cap[1 + q] = train_grad_workspace(B, t->D, t->H, t->L, q);
+    for (int q = 0; q <= kTrainGradProducts; ++q) {
+        w.off[q] = w.total;
+        w.total += w.cap[q];
+    }
+    return w;
+}
+
 int64_t workspace_floats(const enova_trainer t, int B)
 {
-    return train_gemm_workspace(B, t->D, t->H, t->L);
+    return step_work(t, B).total;
 }
 
 // Grows the batch buffers to B rows (freeing the old ones synchronises the device).
@@ -252,15 +271,32 @@ hipError_t enqueue_step(enova_trainer t, const float *V, const float *labels, co
         if (t->timed && ne < enova_trainer_s::kMaxEvents)
             run(hipEventRecord(t->ev[ne++], s));
     };
-    // every product of the step; with timing on, its product kernel is bracketed by two events
+    // every product of the step; with timing on, its product kernel is bracketed by two events.
+    // A weight-gradient product (grad = which, train_grad_shape) splits into its own workspace
+    // region and leaves the slices to the Adam step.
+    const StepWork wk = step_work(t, B);
+    GradSums sums;
     auto gemm = [&](const GemmEpilogue &ep, const float *A, int64_t ai, int64_t ak, const float *Bm, int64_t bk,
-                    int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum) {
+                    int64_t bj, float *C, int64_t ldc, int m, int n, int k, float *rowsum, int grad = -1) {
         hipEvent_t e0 = nullptr, e1 = nullptr;
         if (t->timed && ne + 2 < enova_trainer_s::kMaxEvents) {
             e0 = t->ev[ne++];
             e1 = t->ev[ne++];
         }
-        run(launch_gemm(ep, A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, rowsum, t->work, t->work_cap, s, e0, e1));
+        const int r = grad < 0 ? 0 : 1 + grad;
+        GemmSplit sp;
+        run(launch_gemm(ep, A, ai, ak, Bm, bk, bj, C, ldc, m, n, k, rowsum, t->work + wk.off[r], wk.cap[r], s, e0,
+                        e1, grad < 0 ? nullptr : &sp));
+        if (sp.splits > 0) {
+            if (sums.n + 2 > kMaxGradSums) {
+                run(hipErrorInvalidValue);
+                return;
+            }
+            const int64_t mn = static_cast<int64_t>(m) * n;
+            sums.s[sums.n++] = GradSum{C - G, mn, sp.part, mn, sp.splits};
+            if (rowsum)
+                sums.s[sums.n++] = GradSum{rowsum - G, m, sp.rows, m, sp.splits};
+        }
     };
     const GemmEpilogue plain{};
     auto bias_act = [&](const float *bias, float *out) {
@@ -292,17 +328,17 @@ hipError_t enqueue_step(enova_trainer t, const float *V, const float *labels, co
     run(launch_beta(t->kl, t->logp, labels, B, D, t->hyper, t->state, t->state + 1, info, t->step, t->state + 2,
                     s));
     // backward through the decoder (G = dJ/dm' in out); bias gradients are the row sums of G^T
-    gemm(plain, t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, G + o[P_BD2]);    // dWd2 = G^T hd
-    gemm(dact(t->a2), t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, nullptr);   // dJ/da2
-    gemm(plain, t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, G + o[P_BD1]);      // dWd1 = G^T z
-    gemm(plain, t->gh, H, 1, P + o[P_WD1], L, 1, t->gz, L, B, L, H, nullptr);          // dJ/dz = G Wd1
+    gemm(plain, t->out, 1, D, t->hd, H, 1, G + o[P_WD2], H, D, H, B, G + o[P_BD2], 0);    // dWd2 = G^T hd
+    gemm(dact(t->a2), t->out, D, 1, P + o[P_WD2], H, 1, t->gh, H, B, H, D, nullptr);      // dJ/da2
+    gemm(plain, t->gh, 1, H, t->z, L, 1, G + o[P_WD1], L, H, L, B, G + o[P_BD1], 1);      // dWd1 = G^T z
+    gemm(plain, t->gh, H, 1, P + o[P_WD1], L, 1, t->gz, L, B, L, H, nullptr);             // dJ/dz = G Wd1
     // latent: [dJ/dmu | dJ/dlv], then the fused heads' gradients and dJ/da1 = (G_ml [Wmu; Wlv]) act'(a1)
     run(launch_latent_grad(t->gz, t->gml, t->ml, t->sd, eps, labels, t->state + 1, B, L, s));
-    gemm(plain, t->gml, 1, 2 * L, t->h, H, 1, G + o[P_WMU], H, 2 * L, H, B, G + o[P_BMU]);
+    gemm(plain, t->gml, 1, 2 * L, t->h, H, 1, G + o[P_WMU], H, 2 * L, H, B, G + o[P_BMU], 2);
     gemm(dact(t->a1), t->gml, 2 * L, 1, P + o[P_WMU], H, 1, t->gh, H, B, H, 2 * L, nullptr);
-    gemm(plain, t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, G + o[P_B1]);            // dW1 = G^T V
-    // Adam
-    run(launch_adam(P, G, t->m, t->v, t->total, t->hyper, t->state + 2, s));
+    gemm(plain, t->gh, 1, H, V, D, 1, G + o[P_W1], D, H, D, B, G + o[P_B1], 3);            // dW1 = G^T V
+    // Adam, forming the split weight gradients from their slices first
+    run(launch_adam(P, G, t->m, t->v, t->total, t->hyper, t->state + 2, sums, s));
     mark();
     t->n_events = ne;
     return e;

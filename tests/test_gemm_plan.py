@@ -50,6 +50,11 @@ int main() {
             int B, D, H, L;
             std::scanf("%d %d %d %d", &B, &D, &H, &L);
             std::printf("%lld\n", (long long)train_gemm_workspace(B, D, H, L));
+        } else if (!std::strcmp(op, "G")) {    // B D H L which -> m n k, its own workspace
+            int B, D, H, L, w, m, n, k;
+            std::scanf("%d %d %d %d %d", &B, &D, &H, &L, &w);
+            train_grad_shape(B, D, H, L, w, m, n, k);
+            std::printf("%d %d %d %lld\n", m, n, k, (long long)train_grad_workspace(B, D, H, L, w));
         }
         std::fflush(stdout);
     }
@@ -160,6 +165,24 @@ def test_training_products_fit_their_workspace(planner, B, D, H, L):
         assert p[3] <= w[0]
         if w[0] > 1:
             assert p[3] > 1, (m, n, k)
+
+
+@pytest.mark.parametrize("B", [1, 31, 32, 33, 127, 128, 500, 4096, 8192, 8193, 65536])
+@pytest.mark.parametrize("D,H,L", [(1024, 128, 16), (256, 32, 16), (8192, 256, 16), (12, 5, 3)])
+def test_weight_gradient_products_fit_their_own_regions(planner, B, D, H, L):
+    """The four weight-gradient products keep their slices until the Adam step sums them, each in
+    a workspace region of its own: the region must hold every slice the product is planned to
+    write (on either kernel), and must not make it split less than with the shared workspace."""
+    shared = planner.run([f"T {B} {D} {H} {L}"])[0][0]
+    expect = [(D, H, B), (H, L, B), (2 * L, H, B), (H, D, B)]
+    for w in range(4):
+        m, n, k, ws = planner.run([f"G {B} {D} {H} {L} {w}"])[0]
+        assert (m, n, k) == expect[w]
+        assert ws <= shared
+        mine = _check_plans(planner, [(m, n, k)], ws)[0]
+        assert mine == _check_plans(planner, [(m, n, k)], shared)[0]
+        rs = _check_rs(planner, [(m, n, k, 0, 0)], ws)[0]
+        assert rs == _check_rs(planner, [(m, n, k, 0, 0)], shared)[0]
 
 
 # the step's products as (m, n, k, A k-contiguous, B k-contiguous), in launch order
