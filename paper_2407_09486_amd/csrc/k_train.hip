@@ -196,7 +196,8 @@ __device__ __forceinline__ void epi_tile(float *__restrict__ C, int64_t ldc, int
 // C(i, j) [+]= sum_k A(i, k) B(k, j) for i < m, j < n over the block's reduction slice
 // [z kc, min(kk, (z + 1) kc)), z = blockIdx.z; C(i, j) = C[z m ldc + i ldc + j] (with several
 // slices each writes its own partial tile, summed afterwards in slice order by k_sum_splits,
-// which then applies the epilogue EPI; a single slice applies it here).
+// which then applies the epilogue EPI, or by the Adam step for a weight gradient; a single slice
+// applies it here).
 // A is k-contiguous when AK (A(i, k) = A[i lda + k]), else row-contiguous (A[k lda + i]); B is
 // k-contiguous when BK (B(k, j) = B[j ldb + k]), else row-contiguous (B[k ldb + j]).
 // With rowsum != NULL the blocks of the first column tile also write sum_k A(i, k) over the slice
