@@ -169,12 +169,12 @@ hipError_t launch_calib_compact(const float *scores, const int64_t *woff, const 
 hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream_t st);
 // Partial likelihood sums at the points xs: pa[i*nsplit + j] = sum xs[i] y/(1 + xs[i] y) and
 // pb[i*nsplit + j] = sum log1p(xs[i] y) over the j-th of nsplit contiguous chunks of y (fixed-order
-// fp64 sums; the caller adds the chunks in order). gpd_split gives nsplit for n excesses and nx
-// points.
+// fp64 sums, device terms within a few ulps of gpd_terms). gpd_split gives nsplit for n excesses
+// and nx points.
 int gpd_split(int64_t n, int nx);
 hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
                            double *pa, double *pb, hipStream_t st);
-// sa[i], sb[i] = the chunk partials of point i added in chunk order.
+// sa[i], sb[i] = the chunk partials of point i added in a fixed order (one wave per point).
 hipError_t launch_gpd_reduce(const double *pa, const double *pb, int nx, int nsplit, double *sa, double *sb,
                              hipStream_t st);
 // out = {sum y, min y, max y}; work holds 3 * kPeakBlocks doubles of block partials

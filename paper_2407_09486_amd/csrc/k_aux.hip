@@ -349,7 +349,8 @@ __device__ __forceinline__ double wave_sum(double v)
 
 // Likelihood sums of the excesses: block (g, j) covers chunk j of nsplit contiguous chunks of y
 // at the kGpdX points xs[g*kGpdX ...] (each excess is loaded once for all of them) and writes
-// pa = sum xy/(1+xy), pb = sum log1p(xy) per point in a fixed order.
+// pa = sum xy/(1+xy), pb = sum log1p(xy) per point in a fixed order. The terms take the device
+// form (hardware reciprocal refined by Newton steps, within a few ulps of the divided form).
 constexpr int kGpdX = 8;
 __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, int64_t n,
                                                   const double *__restrict__ xs, int nx, int nsplit,
@@ -378,7 +379,7 @@ __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, 
 #pragma unroll
         for (int k = 0; k < kGpdX; ++k) {
             double ta, tb;
-            gpd_terms(x[k] * yi, ta, tb);
+            gpd_terms_fast(x[k] * yi, ta, tb);
             a[k] += ta;
             b[k] += tb;
         }
@@ -555,23 +556,29 @@ hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream
     return hipGetLastError();
 }
 
-// sa[i] = sum over j = 0, 1, ... (in order) of pa[i*nsplit + j], likewise sb from pb: the same
-// fp64 additions in the same order as the host adding the chunks.
+// sa[i] = the chunk partials pa[i*nsplit + j] of point i added by one wave in a fixed order:
+// lane l adds the chunks j = l, l + 64, ... in order, then a butterfly adds the lanes; likewise sb
+// from pb. Four points per block.
 __global__ __launch_bounds__(256) void k_gpd_reduce(const double *__restrict__ pa, const double *__restrict__ pb,
                                                     int nx, int nsplit, double *__restrict__ sa,
                                                     double *__restrict__ sb)
 {
-    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int i = blockIdx.x * 4 + static_cast<int>(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
     if (i >= nx)
         return;
     const double *a = pa + static_cast<int64_t>(i) * nsplit, *b = pb + static_cast<int64_t>(i) * nsplit;
     double ta = 0.0, tb = 0.0;
-    for (int j = 0; j < nsplit; ++j) {
+    for (int j = lane; j < nsplit; j += 64) {
         ta += a[j];
         tb += b[j];
     }
-    sa[i] = ta;
-    sb[i] = tb;
+    ta = wave_sum(ta);
+    tb = wave_sum(tb);
+    if (lane == 0) {
+        sa[i] = ta;
+        sb[i] = tb;
+    }
 }
 
 hipError_t launch_gpd_reduce(const double *pa, const double *pb, int nx, int nsplit, double *sa, double *sb,
@@ -579,7 +586,7 @@ hipError_t launch_gpd_reduce(const double *pa, const double *pb, int nx, int nsp
 {
     if (nx <= 0)
         return hipSuccess;
-    hipLaunchKernelGGL(k_gpd_reduce, dim3(static_cast<unsigned>((nx + 255) / 256)), dim3(256), 0, st, pa, pb, nx,
+    hipLaunchKernelGGL(k_gpd_reduce, dim3(static_cast<unsigned>((nx + 3) / 4)), dim3(256), 0, st, pa, pb, nx,
                        nsplit, sa, sb);
     return hipGetLastError();
 }
