@@ -785,8 +785,8 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
             // all peaks (lane l sums the peaks l, l + 64, ..., a butterfly adds the lanes), and
             // its lane 0 keeps the bracket on the sign of w, taking the Newton step when it lands
             // strictly inside and the midpoint otherwise. A bracket ends at an exact zero of w,
-            // when the step falls to 4 ulp of the point, when the bracket can no longer be split,
-            // or after kFitRounds evaluations.
+            // with the step taken once it falls below 2^-26 of the point, when the bracket can no
+            // longer be split, or after kFitRounds evaluations.
             for (;;) {
                 if (tid == 0) {
                     sh.nbatch = 0;
@@ -834,7 +834,11 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                             const double xn = x - wv / wd;
                             const bool inside = xn > lo && xn < hi;     // false for NaN
                             const double mid = 0.5 * (lo + hi);
-                            const double tol = 0x1p-50 * fmax(fabs(lo), fabs(hi));
+                            // converged once the step is below 2^-26 of the point: from there the
+                            // step's quadratic convergence lands within rounding of the root (a
+                            // tighter test only meets the rounding noise of the sums, and the
+                            // iterates then wander inside the bracket)
+                            const double tol = 0x1p-26 * fmax(fabs(lo), fabs(hi));
                             sh.blo[b] = lo;
                             sh.bhi[b] = hi;
                             if (inside && fabs(xn - x) <= tol) {
