@@ -170,8 +170,9 @@ enova_status enova_detect_score_noalloc(enova_detector det, const void *x, const
  * (ascending, 0-based); the excesses Y = {c - t : c > t} are fitted by a generalised Pareto
  * distribution (N_t >= 10: maximum likelihood by Grimshaw's reduction in fp64 -- the roots of
  * its one-variable equation are bracketed on a 512-point grid of each admissible interval and
- * refined by k-section, with the likelihood sums over the excesses reduced on the device in a
- * fixed order; 2 <= N_t < 10: method of moments with the unbiased sample variance;
+ * refined by Newton steps kept inside each bracket, with the likelihood sums over the excesses
+ * reduced on the device in a fixed order; 2 <= N_t < 10: method of moments with the unbiased
+ * sample variance;
  * N_t <= 1: the threshold is t) and
  *   z_q = t + sigma/gamma * ((q n / N_t)^(-gamma) - 1)   (z_q = t - sigma ln(q n / N_t) if gamma = 0).
  *   scores         device [n_windows] float (as written by enova_detect_score)

@@ -483,20 +483,30 @@ struct DeviceGpdSums : GpdSums {
         : d(d_), y(y_), n(n_), st(s_) {}
     bool eval(const double *xs, int nx, double *sa, double *sb) override
     {
+        return run(xs, nx, sa, sb, nullptr, nullptr);
+    }
+    bool eval_d(const double *xs, int nx, double *sa, double *sb, double *sda, double *sdb) override
+    {
+        return run(xs, nx, sa, sb, sda, sdb);
+    }
+    // the sums at nx points (with sda and sdb, else NULL, also their derivatives)
+    bool run(const double *xs, int nx, double *sa, double *sb, double *sda, double *sdb)
+    {
         if (nx <= 0)
             return true;
+        const int nv = sda ? 4 : 2;      // sums per point
         const int ns = gpd_split(n, nx);
         const size_t np = static_cast<size_t>(nx) * ns;
-        status = ensure(&d->gx, &d->gx_cap, 3 * static_cast<size_t>(nx) + 2 * np);
+        status = ensure(&d->gx, &d->gx_cap, 5 * static_cast<size_t>(nx) + 4 * np);
         if (status != ENOVA_OK)
             return false;
-        // pinned host staging: the points, then the two sums per point (3 nx doubles)
-        if (d->gpin_cap < 3 * static_cast<size_t>(nx)) {
+        // pinned host staging: the points, then the sums per point (5 nx doubles at most)
+        if (d->gpin_cap < 5 * static_cast<size_t>(nx)) {
             if (d->gpin)
                 (void)hipHostFree(d->gpin);
             d->gpin = nullptr;
             d->gpin_cap = 0;
-            const size_t cap = std::max<size_t>(3 * static_cast<size_t>(nx), 3 * 1024);
+            const size_t cap = std::max<size_t>(5 * static_cast<size_t>(nx), 5 * 1024);
             if (hipHostMalloc(reinterpret_cast<void **>(&d->gpin), cap * sizeof(double)) != hipSuccess) {
                 d->gpin = nullptr;
                 status = fail(ENOVA_ENOMEM, "pinned host buffer of %zu doubles", cap);
@@ -504,20 +514,28 @@ struct DeviceGpdSums : GpdSums {
             }
             d->gpin_cap = cap;
         }
-        double *dx = d->gx, *dsa = dx + nx, *dsb = dsa + nx, *dpa = dsb + nx, *dpb = dpa + np;
-        double *hx = d->gpin, *hsa = hx + nx, *hsb = hsa + nx;
+        // device: x, the sums [nv][nx], then the chunk partials [nv][nx][ns]
+        double *dx = d->gx, *ds = dx + nx, *dp = ds + 4 * static_cast<size_t>(nx);
+        double *dpart[4] = {dp, dp + np, dp + 2 * np, dp + 3 * np};
+        double *hx = d->gpin, *hs = hx + nx;
         std::copy(xs, xs + nx, hx);
         hipError_t e;
         if ((e = hipMemcpyAsync(dx, hx, sizeof(double) * nx, hipMemcpyHostToDevice, st)) != hipSuccess ||
-            (e = launch_gpd_sums(y, n, dx, nx, ns, dpa, dpb, st)) != hipSuccess ||
-            (e = launch_gpd_reduce(dpa, dpb, nx, ns, dsa, dsb, st)) != hipSuccess ||
-            (e = hipMemcpyAsync(hsa, dsa, sizeof(double) * 2 * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = launch_gpd_sums(y, n, dx, nx, ns, dpart[0], dpart[1], sda ? dpart[2] : nullptr,
+                                 sda ? dpart[3] : nullptr, st)) != hipSuccess ||
+            (e = launch_gpd_reduce(dpart[0], dpart[1], nx, ns, ds, ds + nx, st)) != hipSuccess ||
+            (sda && (e = launch_gpd_reduce(dpart[2], dpart[3], nx, ns, ds + 2 * nx, ds + 3 * nx, st)) != hipSuccess) ||
+            (e = hipMemcpyAsync(hs, ds, sizeof(double) * nv * nx, hipMemcpyDeviceToHost, st)) != hipSuccess ||
             (e = hipStreamSynchronize(st)) != hipSuccess) {
             status = hip_fail(e, "GPD likelihood sums");
             return false;
         }
-        std::copy(hsa, hsa + nx, sa);
-        std::copy(hsb, hsb + nx, sb);
+        std::copy(hs, hs + nx, sa);
+        std::copy(hs + nx, hs + 2 * nx, sb);
+        if (sda) {
+            std::copy(hs + 2 * nx, hs + 3 * nx, sda);
+            std::copy(hs + 3 * nx, hs + 4 * nx, sdb);
+        }
         return true;
     }
 };

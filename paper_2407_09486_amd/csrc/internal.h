@@ -169,11 +169,12 @@ hipError_t launch_calib_compact(const float *scores, const int64_t *woff, const 
 hipError_t launch_scan_i64(const int64_t *in, int64_t n, int64_t *out, hipStream_t st);
 // Partial likelihood sums at the points xs: pa[i*nsplit + j] = sum xs[i] y/(1 + xs[i] y) and
 // pb[i*nsplit + j] = sum log1p(xs[i] y) over the j-th of nsplit contiguous chunks of y (fixed-order
-// fp64 sums, device terms within a few ulps of gpd_terms). gpd_split gives nsplit for n excesses
-// and nx points.
+// fp64 sums, device terms within a few ulps of gpd_terms); with pda and pdb (else NULL) also
+// their derivatives in x, sum y/(1 + xs[i] y)^2 and sum y/(1 + xs[i] y). gpd_split gives nsplit
+// for n excesses and nx points.
 int gpd_split(int64_t n, int nx);
 hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
-                           double *pa, double *pb, hipStream_t st);
+                           double *pa, double *pb, double *pda, double *pdb, hipStream_t st);
 // sa[i], sb[i] = the chunk partials of point i added in a fixed order (one wave per point).
 hipError_t launch_gpd_reduce(const double *pa, const double *pb, int nx, int nsplit, double *sa, double *sb,
                              hipStream_t st);
@@ -192,6 +193,9 @@ struct GpdSums {
     virtual ~GpdSums() = default;
     // sa[i] = sum xs[i] y / (1 + xs[i] y), sb[i] = sum log1p(xs[i] y); false on failure
     virtual bool eval(const double *xs, int nx, double *su, double *sv) = 0;
+    // the same sums and their derivatives in x: sda[i] = sum y / (1 + xs[i] y)^2,
+    // sdb[i] = sum y / (1 + xs[i] y)
+    virtual bool eval_d(const double *xs, int nx, double *su, double *sv, double *sda, double *sdb) = 0;
 };
 // Maximum likelihood (n_peaks >= 10) given the excesses' sum, minimum and maximum.
 PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin, double ymax,

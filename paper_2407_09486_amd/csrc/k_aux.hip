@@ -349,14 +349,18 @@ __device__ __forceinline__ double wave_sum(double v)
 
 // Likelihood sums of the excesses: block (g, j) covers chunk j of nsplit contiguous chunks of y
 // at the kGpdX points xs[g*kGpdX ...] (each excess is loaded once for all of them) and writes
-// pa = sum xy/(1+xy), pb = sum log1p(xy) per point in a fixed order. The terms take the device
-// form (hardware reciprocal refined by Newton steps, within a few ulps of the divided form).
+// pa = sum xy/(1+xy), pb = sum log1p(xy) per point in a fixed order (DER: also pda = sum
+// y/(1+xy)^2 and pdb = sum y/(1+xy), their derivatives in x). The terms take the device form
+// (hardware reciprocal refined by Newton steps, within a few ulps of the divided form).
 constexpr int kGpdX = 8;
+template <bool DER>
 __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, int64_t n,
                                                   const double *__restrict__ xs, int nx, int nsplit,
-                                                  double *__restrict__ pa, double *__restrict__ pb)
+                                                  double *__restrict__ pa, double *__restrict__ pb,
+                                                  double *__restrict__ pda, double *__restrict__ pdb)
 {
-    __shared__ double red[4][2 * kGpdX];
+    constexpr int NV = DER ? 4 : 2;   // sums per point
+    __shared__ double red[4][NV * kGpdX];
     const int grp = blockIdx.x / nsplit;
     const int j = blockIdx.x - grp * nsplit;
     double x[kGpdX];
@@ -368,43 +372,48 @@ __global__ __launch_bounds__(256) void k_gpd_sums(const double *__restrict__ y, 
     const int64_t chunk = (n + nsplit - 1) / nsplit;
     const int64_t lo = j * chunk;
     const int64_t hi = lo + chunk < n ? lo + chunk : n;
-    double a[kGpdX], b[kGpdX];
+    double acc[NV][kGpdX];
 #pragma unroll
-    for (int k = 0; k < kGpdX; ++k) {
-        a[k] = 0.0;
-        b[k] = 0.0;
-    }
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int k = 0; k < kGpdX; ++k)
+            acc[v][k] = 0.0;
     for (int64_t i = lo + threadIdx.x; i < hi; i += 256) {
         const double yi = y[i];
 #pragma unroll
         for (int k = 0; k < kGpdX; ++k) {
-            double ta, tb;
-            gpd_terms_fast(x[k] * yi, ta, tb);
-            a[k] += ta;
-            b[k] += tb;
+            double ta, tb, r;
+            gpd_terms_fast(x[k] * yi, ta, tb, r);
+            acc[0][k] += ta;
+            acc[1][k] += tb;
+            if constexpr (DER) {
+                const double yr = yi * r;
+                acc[2][k] += yr * r;
+                acc[3][k] += yr;
+            }
         }
     }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int k = 0; k < kGpdX; ++k) {
-        a[k] = wave_sum(a[k]);
-        b[k] = wave_sum(b[k]);
-    }
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int k = 0; k < kGpdX; ++k)
+            acc[v][k] = wave_sum(acc[v][k]);
     if (lane == 0) {
 #pragma unroll
-        for (int k = 0; k < kGpdX; ++k) {
-            red[wave][k] = a[k];
-            red[wave][kGpdX + k] = b[k];
-        }
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int k = 0; k < kGpdX; ++k)
+                red[wave][v * kGpdX + k] = acc[v][k];
     }
     __syncthreads();
-    if (threadIdx.x < kGpdX) {
-        const int k = threadIdx.x;
+    if (threadIdx.x < NV * kGpdX) {
+        const int v = threadIdx.x / kGpdX, k = threadIdx.x - v * kGpdX;
         const int i = grp * kGpdX + k;
         if (i < nx) {
-            pa[static_cast<int64_t>(i) * nsplit + j] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
-            pb[static_cast<int64_t>(i) * nsplit + j] =
-                ((red[0][kGpdX + k] + red[1][kGpdX + k]) + red[2][kGpdX + k]) + red[3][kGpdX + k];
+            double *out = v == 0 ? pa : v == 1 ? pb : v == 2 ? pda : pdb;
+            const int c = threadIdx.x;
+            out[static_cast<int64_t>(i) * nsplit + j] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
         }
     }
 }
@@ -604,12 +613,19 @@ int gpd_split(int64_t n, int nx)
 }
 
 hipError_t launch_gpd_sums(const double *y, int64_t n, const double *xs, int nx, int nsplit,
-                           double *pa, double *pb, hipStream_t st)
+                           double *pa, double *pb, double *pda, double *pdb, hipStream_t st)
 {
     if (nx <= 0)
         return hipSuccess;
+    if ((pda == nullptr) != (pdb == nullptr))
+        return hipErrorInvalidValue;
     const unsigned groups = static_cast<unsigned>((nx + kGpdX - 1) / kGpdX);
-    hipLaunchKernelGGL(k_gpd_sums, dim3(groups * nsplit), dim3(256), 0, st, y, n, xs, nx, nsplit, pa, pb);
+    if (pda)
+        hipLaunchKernelGGL(k_gpd_sums<true>, dim3(groups * nsplit), dim3(256), 0, st, y, n, xs, nx, nsplit, pa, pb,
+                           pda, pdb);
+    else
+        hipLaunchKernelGGL(k_gpd_sums<false>, dim3(groups * nsplit), dim3(256), 0, st, y, n, xs, nx, nsplit, pa,
+                           pb, pda, pdb);
     return hipGetLastError();
 }
 

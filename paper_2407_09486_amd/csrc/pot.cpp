@@ -8,13 +8,19 @@
 //     w(x) = b - a - a b = 0,   a = mean xY/(1+xY) = 1 - u,   b = mean log1p(xY) = v - 1.
 // Roots are bracketed on geometric grids of both admissible intervals: (0, B], B =
 // 2 (mean - min) / min^2, which spans many decades once there are many peaks, and
-// (-1/Y_max, 0), resolved geometrically towards both ends; brackets are refined by k-section
-// (63 interior points per round, all brackets evaluated in one batch) until they cannot shrink.
+// (-1/Y_max, 0), resolved geometrically towards both ends; each bracket is refined by Newton's
+// method kept inside it (all open brackets evaluated in one batch per round, w' from two more
+// sums): the first point is the secant of the grid's w at the bracket's ends, a step that lands
+// strictly inside is taken, else the midpoint, and a bracket ends once the step falls below
+// 2^-26 of the point (quadratic convergence then puts the new point within rounding of the
+// root; a tighter test only meets the rounding noise of the sums), at an exact zero, or when it
+// can no longer be split.
 // The exponential tail (gamma = 0, sigma = mean Y) is always a candidate, and the candidate of
 // largest log-likelihood wins (ties: smaller |gamma|).
 //
 // The sums over the (possibly millions of) excesses come from a GpdSums evaluator; the
 // library's evaluator runs them on the device where the excesses were compacted.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <limits>
@@ -27,14 +33,14 @@ namespace enova {
 namespace {
 
 constexpr int kGrid = 512;       // grid points per admissible interval
-constexpr int kInterior = 63;    // k-section points per bracket and round
-constexpr int kRounds = 40;
+constexpr int kRounds = 64;      // evaluations per bracket at most
 
 struct Bracket {
     double lo, hi;
     bool lo_neg;     // sign of w(lo)
     bool done;
     double root;
+    double x;        // the point the next round evaluates
 };
 
 double w_of(double sa, double sb, double n)
@@ -134,78 +140,66 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
                 const double wn = w_of(su[base + i + 1], sv[base + i + 1], N);
                 if (wi * wn < 0.0) {
                     const double x0 = xs[base + i], x1 = xs[base + i + 1];
-                    // keep lo < hi; lo_neg is the sign of w at lo
-                    if (x0 < x1)
-                        br.push_back({x0, x1, wi < 0.0, false, 0.0});
-                    else
-                        br.push_back({x1, x0, wn < 0.0, false, 0.0});
+                    // keep lo < hi; lo_neg is the sign of w at lo; start at the secant point
+                    const double lo = x0 < x1 ? x0 : x1, hi = x0 < x1 ? x1 : x0;
+                    const double xsec = x0 - wi * (x1 - x0) / (wn - wi);
+                    const double x = xsec > lo && xsec < hi ? xsec : 0.5 * (lo + hi);
+                    br.push_back({lo, hi, x0 < x1 ? wi < 0.0 : wn < 0.0, false, 0.0, x});
                 }
             }
         }
         base += kGrid;
     }
-    // k-section of every open bracket, batched
+    // Newton's method inside every open bracket, batched
+    std::vector<double> sda, sdb;
+    std::vector<int> evals(br.size(), 0);
     for (int round = 0; round < kRounds; ++round) {
         xs.clear();
         std::vector<int> owner;
-        for (size_t b = 0; b < br.size(); ++b) {
-            Bracket &k = br[b];
-            if (k.done)
-                continue;
-            double prev = k.lo;
-            bool collapsed = false;
-            std::vector<double> pts;
-            for (int j = 1; j <= kInterior; ++j) {
-                const double p = k.lo + (k.hi - k.lo) * static_cast<double>(j) / (kInterior + 1);
-                if (!(p > prev) || !(p < k.hi)) {
-                    collapsed = true;
-                    break;
-                }
-                pts.push_back(p);
-                prev = p;
-            }
-            if (collapsed) {
-                k.done = true;
-                k.root = 0.5 * (k.lo + k.hi);
-                continue;
-            }
-            for (double p : pts) {
-                xs.push_back(p);
+        for (size_t b = 0; b < br.size(); ++b)
+            if (!br[b].done) {
+                xs.push_back(br[b].x);
                 owner.push_back(static_cast<int>(b));
             }
-        }
         if (xs.empty())
             break;
         su.assign(xs.size(), 0.0);
         sv.assign(xs.size(), 0.0);
-        if (!sums.eval(xs.data(), static_cast<int>(xs.size()), su.data(), sv.data()))
+        sda.assign(xs.size(), 0.0);
+        sdb.assign(xs.size(), 0.0);
+        if (!sums.eval_d(xs.data(), static_cast<int>(xs.size()), su.data(), sv.data(), sda.data(), sdb.data()))
             return r;
-        for (size_t i = 0; i < xs.size();) {
-            const int b = owner[i];
-            Bracket &k = br[b];
-            size_t j = i;
-            double new_lo = k.lo, new_hi = k.hi;
-            bool found = false;
-            for (; j < xs.size() && owner[j] == b; ++j) {
-                if (found)
-                    continue;
-                const double wj = w_of(su[j], sv[j], N);
-                if (wj == 0.0) {
-                    k.done = true;
-                    k.root = xs[j];
-                    found = true;
-                } else if ((wj < 0.0) != k.lo_neg) {
-                    new_hi = xs[j];
-                    found = true;
-                } else {
-                    new_lo = xs[j];
-                }
+        for (size_t i = 0; i < xs.size(); ++i) {
+            Bracket &k = br[owner[i]];
+            const double x = xs[i];
+            const double a = su[i] / N, b = sv[i] / N, da = sda[i] / N, db = sdb[i] / N;
+            const double wv = b - a - a * b;
+            const double wd = db - da - da * b - a * db;
+            if (wv == 0.0) {
+                k.done = true;
+                k.root = x;
+                continue;
             }
-            if (!k.done) {
-                k.lo = new_lo;
-                k.hi = new_hi;
+            if ((wv < 0.0) == k.lo_neg)
+                k.lo = x;
+            else
+                k.hi = x;
+            const double xn = x - wv / wd;
+            const bool inside = xn > k.lo && xn < k.hi;     // false for NaN
+            const double mid = 0.5 * (k.lo + k.hi);
+            const double tol = 0x1p-26 * std::max(std::fabs(k.lo), std::fabs(k.hi));
+            if (inside && std::fabs(xn - x) <= tol) {
+                k.done = true;
+                k.root = xn;
+            } else if (!inside && !(mid > k.lo && mid < k.hi)) {
+                k.done = true;
+                k.root = mid;
+            } else if (++evals[owner[i]] >= kRounds) {
+                k.done = true;
+                k.root = inside ? xn : mid;
+            } else {
+                k.x = inside ? xn : mid;
             }
-            i = j;
         }
     }
     for (auto &k : br)
