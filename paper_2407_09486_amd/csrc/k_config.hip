@@ -184,7 +184,9 @@ __device__ double kde_quantile(const float *v, int n, int np2, double q, float *
         return v[0];
     // Safeguarded Newton on F(x) - q (F' is the KDE density): every evaluation also tightens the
     // bracket [lo, hi], and a step that would leave it becomes a bisection step; stops when the
-    // bracket can no longer shrink or the step vanishes.
+    // bracket can no longer shrink, the step vanishes, or a Newton step falls below 2^-26 of the
+    // bracket's magnitude (taken: quadratic convergence then puts it within rounding of the root,
+    // where the sums' rounding noise would otherwise keep the iterates moving).
     double lo = sorted[0] - 10.0 * h, hi = sorted[n - 1] + 10.0 * h;
     const double scale = 1.0 / (h * 1.4142135623730951);
     const double dens = 1.0 / (h * 2.5066282746310002 * n);   // 1 / (h sqrt(2 pi) n)
@@ -205,10 +207,15 @@ __device__ double kde_quantile(const float *v, int n, int np2, double q, float *
         else
             hi = x;
         double nx = f1 > 0.0 ? x - (F - q) / f1 : 0.5 * (lo + hi);
-        if (!(nx > lo && nx < hi))
+        const bool newton = nx > lo && nx < hi;
+        if (!newton)
             nx = 0.5 * (lo + hi);
         if (nx == x || !(0.5 * (lo + hi) > lo && 0.5 * (lo + hi) < hi))
             break;
+        if (newton && fabs(nx - x) <= 0x1p-26 * fmax(fabs(lo), fabs(hi))) {
+            x = nx;
+            break;
+        }
         x = nx;
     }
     return x;
