@@ -94,7 +94,7 @@ struct enova_detector_s {
     size_t tile_map_cap = 0;      // entries
     int64_t *cal = nullptr;
     size_t cal_cap = 0;
-    unsigned int *hist = nullptr; // 256 radix bins
+    unsigned int *hist = nullptr; // 256 radix bins, then the radix state (RadixState at bin 256)
     double *peaks = nullptr;      // excesses over the level quantile, calibration order
     size_t peaks_cap = 0;
     int64_t *blk = nullptr;       // per-block peak counts, then their exclusive scan
@@ -842,7 +842,8 @@ enova_status enova_detect_init(const enova_detect_config *config, const enova_de
             st = pack_ext_fused(d, w);
     }
     if (st == ENOVA_OK) {
-        hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), 256 * sizeof(unsigned int));
+        static_assert(sizeof(RadixState) <= 8 * sizeof(unsigned int), "radix state after the bins");
+        hipError_t e = hipMalloc(reinterpret_cast<void **>(&d->hist), (256 + 8) * sizeof(unsigned int));
         if (e != hipSuccess)
             st = fail(ENOVA_ENOMEM, "hipMalloc(hist)");
     }
@@ -1325,53 +1326,42 @@ enova_status enova_detect_threshold(enova_detector det, const float *scores, con
     if (n_cal <= 0)
         return fail(ENOVA_ESHAPE, "no window lies inside a reference prefix");
 
-    // exact order statistic at ceil(level*n) - 1 by a 4-pass radix select over float keys
+    // exact order statistic at ceil(level*n) - 1 by a 4-pass radix select over float keys, each
+    // pass's digit picked on the device (no host round trip until the key is known)
     int64_t rank = static_cast<int64_t>(std::ceil(level * static_cast<double>(n_cal))) - 1;
     if (rank < 0)
         rank = 0;
     if (rank > n_cal - 1)
         rank = n_cal - 1;
-    uint32_t prefix = 0;
-    int64_t n_greater = 0;
-    unsigned int hist[256];
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        if ((e = hipMemsetAsync(det->hist, 0, 256 * sizeof(unsigned int), stream)) != hipSuccess)
-            return hip_fail(e, "hipMemsetAsync");
-        e = launch_calib_hist(scores, woff, det->cal, n, n_cal, shift, prefix, det->hist, stream);
-        if (e != hipSuccess)
+    RadixState *rs = reinterpret_cast<RadixState *>(det->hist + 256);
+    if ((e = launch_radix_init(rs, rank, det->hist, stream)) != hipSuccess)
+        return hip_fail(e, "radix select start");
+    for (int shift = 24; shift >= 0; shift -= 8)
+        if ((e = launch_calib_hist(scores, woff, det->cal, n, n_cal, shift, rs, det->hist, stream)) != hipSuccess)
             return hip_fail(e, "calibration histogram kernel");
-        if ((e = hipMemcpyAsync(hist, det->hist, sizeof(hist), hipMemcpyDeviceToHost, stream)) !=
-                hipSuccess ||
-            (e = hipStreamSynchronize(stream)) != hipSuccess)
-            return hip_fail(e, "calibration histogram copy");
-        int64_t cum = 0;
-        int digit = -1;
-        for (int dgt = 0; dgt < 256; ++dgt) {
-            if (digit < 0 && rank < cum + hist[dgt]) {
-                digit = dgt;
-                rank -= cum;
-            } else if (digit >= 0) {
-                n_greater += hist[dgt];
-            }
-            cum += hist[dgt];
-        }
-        if (digit < 0)
-            return fail(ENOVA_EHIP, "radix select lost the order statistic");
-        prefix = (prefix << 8) | static_cast<uint32_t>(digit);
-    }
-    const uint32_t key_t = prefix;
+    RadixState rh{};
+    if ((e = hipMemcpyAsync(&rh, rs, sizeof(rh), hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(stream)) != hipSuccess)
+        return hip_fail(e, "radix select state");
+    if (!rh.ok)
+        return fail(ENOVA_EHIP, "radix select lost the order statistic");
+    const int64_t n_greater = rh.n_greater;
+    const uint32_t key_t = rh.prefix;
     const uint32_t bits = (key_t & 0x80000000u) ? (key_t & 0x7fffffffu) : ~key_t;
     float t_f;
     std::memcpy(&t_f, &bits, 4);
     if (!std::isfinite(t_f))
         return fail(ENOVA_ENUMERIC, "non-finite calibration score at the level quantile");
-    // stable compaction of the excesses y = score - t of every calibration score above t
+    // stable compaction of the excesses y = score - t of every calibration score above t; with
+    // ten or more, their sum, minimum and maximum right behind it (one round trip for both)
     PotResult r{};
     const double t_d = static_cast<double>(t_f);
+    double ps[3] = {0.0, 0.0, 0.0};
     if (n_greater > 0) {
         const int64_t nblk = calib_blocks(n_cal);
         if ((st = ensure(&det->peaks, &det->peaks_cap, static_cast<size_t>(n_greater))) != ENOVA_OK ||
-            (st = ensure(&det->blk, &det->blk_cap, 2 * static_cast<size_t>(nblk) + 2)) != ENOVA_OK)
+            (st = ensure(&det->blk, &det->blk_cap, 2 * static_cast<size_t>(nblk) + 2)) != ENOVA_OK ||
+            (st = ensure(&det->gx, &det->gx_cap, 4 + 3 * kPeakBlocks)) != ENOVA_OK)
             return st;
         int64_t *cnt = det->blk, *off = det->blk + nblk + 1;
         if ((e = launch_calib_count(scores, woff, det->cal, n, n_cal, key_t, cnt, stream)) != hipSuccess ||
@@ -1379,9 +1369,14 @@ enova_status enova_detect_threshold(enova_detector det, const float *scores, con
             (e = launch_calib_compact(scores, woff, det->cal, n, n_cal, key_t, t_d, off, det->peaks,
                                       n_greater, stream)) != hipSuccess)
             return hip_fail(e, "peak compaction");
+        if (n_greater >= 10 && (e = launch_peak_stats(det->peaks, n_greater, det->gx, det->gx + 4, stream)) !=
+                                   hipSuccess)
+            return hip_fail(e, "peak statistics");
         int64_t total = 0;
         if ((e = hipMemcpyAsync(&total, off + nblk, sizeof(int64_t), hipMemcpyDeviceToHost, stream)) !=
                 hipSuccess ||
+            (n_greater >= 10 &&
+             (e = hipMemcpyAsync(ps, det->gx, sizeof(ps), hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
             (e = hipStreamSynchronize(stream)) != hipSuccess)
             return hip_fail(e, "peak count");
         if (total != n_greater)
@@ -1389,13 +1384,6 @@ enova_status enova_detect_threshold(enova_detector det, const float *scores, con
                         static_cast<long long>(n_greater));
     }
     if (n_greater >= 10) {
-        double ps[3];
-        if ((st = ensure(&det->gx, &det->gx_cap, 4 + 3 * kPeakBlocks)) != ENOVA_OK)
-            return st;
-        if ((e = launch_peak_stats(det->peaks, n_greater, det->gx, det->gx + 4, stream)) != hipSuccess ||
-            (e = hipMemcpyAsync(ps, det->gx, sizeof(ps), hipMemcpyDeviceToHost, stream)) != hipSuccess ||
-            (e = hipStreamSynchronize(stream)) != hipSuccess)
-            return hip_fail(e, "peak statistics");
         if (!std::isfinite(ps[0]) || !std::isfinite(ps[2]))
             return fail(ENOVA_ENUMERIC, "non-finite calibration score");
         DeviceGpdSums ev(det, det->peaks, n_greater, stream);

@@ -152,10 +152,21 @@ hipError_t launch_score_mfma(const Geometry &g, const ScoreParams &p, int64_t gr
 hipError_t prepare_score_ring(const Geometry &g);
 hipError_t launch_score_ring(const Geometry &g, const ScoreParams &p, int64_t grid, hipStream_t st);
 hipError_t launch_flag(const float *scores, int64_t n, float thr, uint8_t *flags, hipStream_t st);
-// Radix-select pass over the calibration scores: histogram of the 8-bit digit at `shift`
-// among keys whose bits above shift+8 equal `prefix`.
+// Radix select over the calibration scores' float keys, every pass's digit picked on the device.
+// The state lives in device memory: the key prefix chosen so far, the rank still sought among
+// the keys that share it, the count of keys above it, and ok = 0 if a pass lost the rank.
+struct RadixState {
+    uint32_t prefix;
+    int32_t ok;
+    int64_t rank;
+    int64_t n_greater;
+};
+// rs = {0, 1, rank, 0}; hist (256 bins) cleared.
+hipError_t launch_radix_init(RadixState *rs, int64_t rank, unsigned int *hist, hipStream_t st);
+// One pass: the histogram of the 8-bit digit at `shift` among keys whose bits above shift+8 equal
+// rs->prefix, then (one block) the digit holding rs->rank: rs updated, hist cleared again.
 hipError_t launch_calib_hist(const float *scores, const int64_t *woff, const int64_t *cal_off,
-                             int n, int64_t n_cal, int shift, uint32_t prefix,
+                             int n, int64_t n_cal, int shift, RadixState *rs,
                              unsigned int *hist, hipStream_t st);
 // Stable compaction of the calibration scores whose key exceeds `key`:
 // calib_blocks() blocks; pass 1 counts per block, an exclusive scan gives each block's output

@@ -208,11 +208,13 @@ __device__ __forceinline__ int find_stream(const int64_t *off, int n, int64_t ci
 __global__ __launch_bounds__(256) void k_calib_hist(const float *__restrict__ scores,
                                                     const int64_t *__restrict__ woff,
                                                     const int64_t *__restrict__ cal_off, int n,
-                                                    int64_t n_cal, int shift, uint32_t prefix,
+                                                    int64_t n_cal, int shift,
+                                                    const RadixState *__restrict__ rs,
                                                     unsigned int *__restrict__ hist)
 {
     __shared__ unsigned int h[256];
     const int tid = threadIdx.x;
+    const uint32_t prefix = rs->prefix;
     h[tid] = 0;
     __syncthreads();
     const int64_t start = static_cast<int64_t>(blockIdx.x) * 256 * kCalItems;
@@ -233,6 +235,59 @@ __global__ __launch_bounds__(256) void k_calib_hist(const float *__restrict__ sc
     __syncthreads();
     if (h[tid])
         atomicAdd(&hist[tid], h[tid]);
+}
+
+// The radix state's start: no prefix, the sought rank, nothing above; the bins cleared.
+__global__ __launch_bounds__(256) void k_radix_init(RadixState *__restrict__ rs, int64_t rank,
+                                                    unsigned int *__restrict__ hist)
+{
+    hist[threadIdx.x] = 0u;
+    if (threadIdx.x == 0) {
+        rs->prefix = 0u;
+        rs->ok = 1;
+        rs->rank = rank;
+        rs->n_greater = 0;
+    }
+}
+
+// One block of 256 threads, thread d holding bin d: an inclusive scan of the bins (in 64-bit)
+// finds the digit whose range [before, before + count) holds the rank; that thread appends the
+// digit to the prefix, keeps rank - before and adds the keys of the higher digits. The bins are
+// cleared for the next pass.
+__global__ __launch_bounds__(256) void k_radix_pick(RadixState *__restrict__ rs, unsigned int *__restrict__ hist)
+{
+    __shared__ int64_t wsum[4];
+    const int d = threadIdx.x, lane = d & 63, wave = d >> 6;
+    const int64_t c = hist[d];
+    hist[d] = 0u;
+    int64_t inc = c;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int64_t o = __shfl_up(inc, off);
+        if (lane >= off)
+            inc += o;
+    }
+    if (lane == 63)
+        wsum[wave] = inc;
+    __syncthreads();
+    int64_t base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        if (w < wave)
+            base += wsum[w];
+        total += wsum[w];
+    }
+    inc += base;
+    const int64_t before = inc - c;
+    const int64_t rank = rs->rank;
+    __syncthreads();
+    if (c > 0 && rank >= before && rank < inc) {
+        rs->prefix = (rs->prefix << 8) | static_cast<uint32_t>(d);
+        rs->rank = rank - before;
+        rs->n_greater += total - inc;
+    }
+    if (d == 0 && !(rank >= 0 && rank < total))
+        rs->ok = 0;
 }
 
 // Peaks of the calibration set, pass 1: how many keys above key_t each block holds.
@@ -525,14 +580,24 @@ static unsigned cal_blocks(int64_t n_cal)
     return static_cast<unsigned>((n_cal + 256 * kCalItems - 1) / (256 * kCalItems));
 }
 
+hipError_t launch_radix_init(RadixState *rs, int64_t rank, unsigned int *hist, hipStream_t st)
+{
+    hipLaunchKernelGGL(k_radix_init, dim3(1), dim3(256), 0, st, rs, rank, hist);
+    return hipGetLastError();
+}
+
 hipError_t launch_calib_hist(const float *scores, const int64_t *woff, const int64_t *cal_off,
-                             int n, int64_t n_cal, int shift, uint32_t prefix, unsigned int *hist,
+                             int n, int64_t n_cal, int shift, RadixState *rs, unsigned int *hist,
                              hipStream_t st)
 {
     if (n_cal <= 0)
         return hipSuccess;
     hipLaunchKernelGGL(k_calib_hist, dim3(cal_blocks(n_cal)), dim3(256), 0, st, scores, woff,
-                       cal_off, n, n_cal, shift, prefix, hist);
+                       cal_off, n, n_cal, shift, rs, hist);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(k_radix_pick, dim3(1), dim3(256), 0, st, rs, hist);
     return hipGetLastError();
 }
 
