@@ -697,7 +697,7 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
             for (int i = tid; i < N; i += kFitThreads)
                 pv += (y[i] - ymean) * (y[i] - ymean);
             const double s2 = block_sum(sh, pv) / (Nd - 1.0);
-            if (s2 > 0.0) {
+            if (s2 > 0.0 && wave == 0) {
                 const double gamma = 0.5 * (1.0 - ymean * ymean / s2);
                 const double sigma = 0.5 * ymean * (1.0 + ymean * ymean / s2);
                 z = fit_quantile(t, gamma, sigma, q * n / Nd);
@@ -868,23 +868,27 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
             }
             __syncthreads();
             fit_eval(sh, y, N);
-            double bg = 0.0, bs = ymean;
-            double bl = -Nd * log(ymean) - ysum / ymean;
-            for (int r = 0; r < sh.nroots; ++r) {
-                const double gm = sh.sb[r] / Nd;
-                if (gm == 0.0 || !isfinite(gm))
-                    continue;
-                const double sg = gm / sh.roots[r];
-                if (!(sg > 0.0))
-                    continue;
-                const double ll = -Nd * log(sg) - (1.0 + 1.0 / gm) * sh.sb[r];
-                if (ll > bl || (ll == bl && fabs(gm) < fabs(bg))) {
-                    bg = gm;
-                    bs = sg;
-                    bl = ll;
+            // the choice and the quantile in one wave (only thread 0 stores z; the other waves'
+            // copies of these fp64 chains would share its SIMDs' issue slots)
+            if (wave == 0) {
+                double bg = 0.0, bs = ymean;
+                double bl = -Nd * log(ymean) - ysum / ymean;
+                for (int r = 0; r < sh.nroots; ++r) {
+                    const double gm = sh.sb[r] / Nd;
+                    if (gm == 0.0 || !isfinite(gm))
+                        continue;
+                    const double sg = gm / sh.roots[r];
+                    if (!(sg > 0.0))
+                        continue;
+                    const double ll = -Nd * log(sg) - (1.0 + 1.0 / gm) * sh.sb[r];
+                    if (ll > bl || (ll == bl && fabs(gm) < fabs(bg))) {
+                        bg = gm;
+                        bs = sg;
+                        bl = ll;
+                    }
                 }
+                z = fit_quantile(t, bg, bs, q * n / Nd);
             }
-            z = fit_quantile(t, bg, bs, q * n / Nd);
         }
     }
     if (tid == 0) {
