@@ -100,36 +100,41 @@ __global__ __launch_bounds__(kCfgThreads) void k_cfg_scan(CfgParams c, int nb, c
         o.g1[out] = static_cast<float>(g1);
 }
 
-// Fixed-order block sum (tree over the threads' partials); every thread gets the total.
+// Fixed-order block sum: a butterfly in each wave, then the four wave sums as (w0 + w1) +
+// (w2 + w3); every thread gets the total. Two barriers (a tree over the threads took one per
+// level).
+static_assert(kCfgThreads == 256, "four waves");
+__device__ __forceinline__ double wave_sum_cfg(double v)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+        v += __shfl_xor(v, m);
+    return v;
+}
+
 __device__ double block_sum(double v, double *red)
 {
-    red[threadIdx.x] = v;
+    v = wave_sum_cfg(v);
+    if ((threadIdx.x & 63) == 0)
+        red[threadIdx.x >> 6] = v;
     __syncthreads();
-    for (int w = kCfgThreads / 2; w >= 1; w >>= 1) {
-        if (threadIdx.x < w)
-            red[threadIdx.x] += red[threadIdx.x + w];
-        __syncthreads();
-    }
-    const double r = red[0];
+    const double r = (red[0] + red[1]) + (red[2] + red[3]);
     __syncthreads();
     return r;
 }
 
-// Two fixed-order block sums at once (red holds 2 * kCfgThreads doubles).
+// Two fixed-order block sums at once.
 __device__ void block_sum2(double a, double b, double *red, double &ra, double &rb)
 {
-    red[threadIdx.x] = a;
-    red[kCfgThreads + threadIdx.x] = b;
-    __syncthreads();
-    for (int w = kCfgThreads / 2; w >= 1; w >>= 1) {
-        if (threadIdx.x < w) {
-            red[threadIdx.x] += red[threadIdx.x + w];
-            red[kCfgThreads + threadIdx.x] += red[kCfgThreads + threadIdx.x + w];
-        }
-        __syncthreads();
+    a = wave_sum_cfg(a);
+    b = wave_sum_cfg(b);
+    if ((threadIdx.x & 63) == 0) {
+        red[threadIdx.x >> 6] = a;
+        red[4 + (threadIdx.x >> 6)] = b;
     }
-    ra = red[0];
-    rb = red[kCfgThreads];
+    __syncthreads();
+    ra = (red[0] + red[1]) + (red[2] + red[3]);
+    rb = (red[4] + red[5]) + (red[6] + red[7]);
     __syncthreads();
 }
 
