@@ -87,6 +87,40 @@ def test_threshold_and_flags(name, n):
     det.close()
 
 
+# Scores that no detector produces but the threshold call accepts: negative values (whose float
+# keys order in reverse), heavy ties at the level quantile, all-negative sets and calibration
+# sets small enough for the method of moments or the bare quantile. The radix select's digits and
+# counts must give the oracle's order statistic and peak count exactly.
+@pytest.mark.parametrize("case", ["normal", "ties", "negative", "small_moments", "single_peak"])
+def test_threshold_on_arbitrary_scores(case):
+    import torch
+    cfg = wl.CONFIGS["c2"].replace(window=16, stride=2)
+    det = detector(cfg, wl.make_weights(cfg))
+    lengths = {"small_moments": [500, 300], "single_peak": [260]}.get(case, [3000, 1234, 4100])
+    so = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    woff = det.window_offsets(so)
+    nw = int(woff[-1])
+    rng = np.random.default_rng(20240712)
+    if case == "ties":
+        sc = np.round(rng.normal(0.0, 1.0, nw), 1)
+    elif case == "negative":
+        sc = -rng.exponential(2.0, nw)
+    else:
+        sc = rng.normal(0.0, 1.0, nw)
+    sc = sc.astype(np.float32)
+    thr_g, info_g, fl = det.threshold(torch.from_numpy(sc).cuda(), torch.from_numpy(so).cuda(),
+                                      torch.from_numpy(woff).cuda(), flags=True)
+    cal = oracle.calibration_scores(sc.astype(np.float64), so, window=cfg.window, stride=cfg.stride)
+    thr_o, info_o = oracle.pot_threshold(cal)
+    assert info_g["n"] == info_o["n"] and info_g["n_peaks"] == info_o["n_peaks"], (info_g, info_o)
+    assert info_g["t"] == info_o["t"] and info_g["method"] == info_o["method"], (info_g, info_o)
+    assert abs(thr_g - np.float32(thr_o)) <= 1e-6 * abs(thr_o) + 1e-30, (thr_g, thr_o)
+    assert np.array_equal(fl.cpu().numpy(), (sc > np.float32(thr_g)).astype(np.uint8))
+    log(f"[threshold] {case}: n={info_g['n']} N_t={info_g['n_peaks']} method={info_g['method']} "
+        f"t={info_g['t']:.6g} z={thr_g:.6g}")
+    det.close()
+
+
 def test_valu_and_mfma_agree_and_are_deterministic():
     cfg, w = _subset("c3", 2)
     weights = wl.make_weights(cfg, bias_scale=0.05)
