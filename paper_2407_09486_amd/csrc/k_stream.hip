@@ -548,7 +548,8 @@ struct FitShared {
     double sb[kFitMaxPoints];
     double red[3][kFitWaves + 1];
     double blo[kFitMaxBrackets], bhi[kFitMaxBrackets], broot[kFitMaxBrackets], bx[kFitMaxBrackets];
-    int bneg[kFitMaxBrackets], bdone[kFitMaxBrackets], bround[kFitMaxBrackets];
+    double bwlo[kFitMaxBrackets], bwhi[kFitMaxBrackets];   // w at the bracket's ends (Illinois-scaled)
+    int bneg[kFitMaxBrackets], bdone[kFitMaxBrackets], bround[kFitMaxBrackets], bside[kFitMaxBrackets];
     double roots[2 * kFitMaxBrackets];
     int batch[kFitWaves];        // the brackets the waves refine in this evaluation
     int wcount[2][kFitWaves];    // per-wave counts of roots and of sign changes
@@ -765,9 +766,12 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                     const double lo = x0 < x1 ? x0 : x1, hi = x0 < x1 ? x1 : x0;
                     sh.blo[b_at] = lo;
                     sh.bhi[b_at] = hi;
+                    sh.bwlo[b_at] = x0 < x1 ? wi : wn;
+                    sh.bwhi[b_at] = x0 < x1 ? wn : wi;
                     sh.bneg[b_at] = x0 < x1 ? (wi < 0.0) : (wn < 0.0);
                     sh.bdone[b_at] = 0;
                     sh.bround[b_at] = 0;
+                    sh.bside[b_at] = 0;
                     sh.broot[b_at] = 0.0;
                     // the first point: the secant of w through the bracket's ends (the grid has w
                     // there), else the midpoint
@@ -784,9 +788,10 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
             // w' at the bracket's current point (first the secant point of the grid values) over
             // all peaks (lane l sums the peaks l, l + 64, ..., a butterfly adds the lanes), and
             // its lane 0 keeps the bracket on the sign of w, taking the Newton step when it lands
-            // strictly inside and the midpoint otherwise. A bracket ends at an exact zero of w,
-            // with the step taken once it falls below 2^-26 of the point, when the bracket can no
-            // longer be split, or after kFitRounds evaluations.
+            // strictly inside and otherwise false position through the ends (Illinois), else the
+            // midpoint. A bracket ends at a zero of w to the rounding of its sums, with the step
+            // taken once it falls below 2^-26 of the point, when the bracket can no longer be
+            // split, or after kFitRounds evaluations.
             for (;;) {
                 if (tid == 0) {
                     sh.nbatch = 0;
@@ -827,13 +832,34 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                             sh.broot[b] = x;
                         } else {
                             double lo = sh.blo[b], hi = sh.bhi[b];
-                            if ((wv < 0.0) == (sh.bneg[b] != 0))
+                            double wlo = sh.bwlo[b], whi = sh.bwhi[b];
+                            // the end that x replaces takes w(x); an end kept twice in a row has
+                            // its w halved (Illinois), so the false-position fallback keeps
+                            // shrinking the bracket from both sides
+                            const int side = (wv < 0.0) == (sh.bneg[b] != 0) ? -1 : 1;
+                            if (side < 0) {
                                 lo = x;
-                            else
+                                wlo = wv;
+                                if (sh.bside[b] < 0)
+                                    whi *= 0.5;
+                            } else {
                                 hi = x;
+                                whi = wv;
+                                if (sh.bside[b] > 0)
+                                    wlo *= 0.5;
+                            }
+                            sh.bside[b] = side;
+                            sh.bwlo[b] = wlo;
+                            sh.bwhi[b] = whi;
                             const double xn = x - wv / wd;
                             const bool inside = xn > lo && xn < hi;     // false for NaN
-                            const double mid = 0.5 * (lo + hi);
+                            // when the Newton step leaves the bracket: false position through the
+                            // ends, else the midpoint
+                            const double xf = lo - wlo * (hi - lo) / (whi - wlo);
+                            const double mid = xf > lo && xf < hi ? xf : 0.5 * (lo + hi);
+                            // |w| within the rounding of the sums it is formed from: x is a root
+                            // to fp64 resolution (where w is flat, no step test would tell more)
+                            const bool flat = fabs(wv) <= 0x1p-46 * (fabs(bm) + fabs(a) + fabs(a * bm));
                             // converged once the step is below 2^-26 of the point: from there the
                             // step's quadratic convergence lands within rounding of the root (a
                             // tighter test only meets the rounding noise of the sums, and the
@@ -841,7 +867,10 @@ __device__ void spot_fit_stream(FitShared &sh, int s, double q, const SpotState 
                             const double tol = 0x1p-26 * fmax(fabs(lo), fabs(hi));
                             sh.blo[b] = lo;
                             sh.bhi[b] = hi;
-                            if (inside && fabs(xn - x) <= tol) {
+                            if (flat) {
+                                sh.bdone[b] = 1;
+                                sh.broot[b] = x;
+                            } else if (inside && fabs(xn - x) <= tol) {
                                 sh.bdone[b] = 1;
                                 sh.broot[b] = xn;
                             } else if (!inside && !(mid > lo && mid < hi)) {
