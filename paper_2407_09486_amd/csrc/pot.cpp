@@ -11,9 +11,10 @@
 // (-1/Y_max, 0), resolved geometrically towards both ends; each bracket is refined by Newton's
 // method kept inside it (all open brackets evaluated in one batch per round, w' from two more
 // sums): the first point is the secant of the grid's w at the bracket's ends, a step that lands
-// strictly inside is taken, else the midpoint, and a bracket ends once the step falls below
-// 2^-26 of the point (quadratic convergence then puts the new point within rounding of the
-// root; a tighter test only meets the rounding noise of the sums), at an exact zero, or when it
+// strictly inside is taken, else false position through the ends (Illinois), else the midpoint,
+// and a bracket ends once |w| is within the rounding of the sums it is formed from, once the
+// step falls below 2^-26 of the point (quadratic convergence then puts the new point within
+// rounding of the root; a tighter test only meets the rounding noise of the sums), or when it
 // can no longer be split.
 // The exponential tail (gamma = 0, sigma = mean Y) is always a candidate, and the candidate of
 // largest log-likelihood wins (ties: smaller |gamma|).
@@ -41,6 +42,8 @@ struct Bracket {
     bool done;
     double root;
     double x;        // the point the next round evaluates
+    double wlo, whi; // w at the ends (an end kept twice in a row has its w halved: Illinois)
+    int side;        // the end the last evaluation replaced (-1 lo, 1 hi, 0 none yet)
 };
 
 double w_of(double sa, double sb, double n)
@@ -144,7 +147,8 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
                     const double lo = x0 < x1 ? x0 : x1, hi = x0 < x1 ? x1 : x0;
                     const double xsec = x0 - wi * (x1 - x0) / (wn - wi);
                     const double x = xsec > lo && xsec < hi ? xsec : 0.5 * (lo + hi);
-                    br.push_back({lo, hi, x0 < x1 ? wi < 0.0 : wn < 0.0, false, 0.0, x});
+                    br.push_back({lo, hi, x0 < x1 ? wi < 0.0 : wn < 0.0, false, 0.0, x, x0 < x1 ? wi : wn,
+                                  x0 < x1 ? wn : wi, 0});
                 }
             }
         }
@@ -180,15 +184,31 @@ PotResult pot_mle(double t, int64_t n, int64_t n_peaks, double ysum, double ymin
                 k.root = x;
                 continue;
             }
-            if ((wv < 0.0) == k.lo_neg)
+            const int side = (wv < 0.0) == k.lo_neg ? -1 : 1;
+            if (side < 0) {
                 k.lo = x;
-            else
+                k.wlo = wv;
+                if (k.side < 0)
+                    k.whi *= 0.5;
+            } else {
                 k.hi = x;
+                k.whi = wv;
+                if (k.side > 0)
+                    k.wlo *= 0.5;
+            }
+            k.side = side;
             const double xn = x - wv / wd;
             const bool inside = xn > k.lo && xn < k.hi;     // false for NaN
-            const double mid = 0.5 * (k.lo + k.hi);
+            // when the Newton step leaves the bracket: false position through the ends, else the
+            // midpoint
+            const double xf = k.lo - k.wlo * (k.hi - k.lo) / (k.whi - k.wlo);
+            const double mid = xf > k.lo && xf < k.hi ? xf : 0.5 * (k.lo + k.hi);
             const double tol = 0x1p-26 * std::max(std::fabs(k.lo), std::fabs(k.hi));
-            if (inside && std::fabs(xn - x) <= tol) {
+            // |w| within the rounding of the sums it is formed from: x is a root to fp64 resolution
+            if (std::fabs(wv) <= 0x1p-46 * (std::fabs(b) + std::fabs(a) + std::fabs(a * b))) {
+                k.done = true;
+                k.root = x;
+            } else if (inside && std::fabs(xn - x) <= tol) {
                 k.done = true;
                 k.root = xn;
             } else if (!inside && !(mid > k.lo && mid < k.hi)) {
